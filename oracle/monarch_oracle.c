@@ -1,0 +1,259 @@
+/*
+ * fp64 CPU oracle of the MonarchAttention forward pass.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, plain reference that the
+ * HIP library is checked against.  Only the test suite, the smoke check and
+ * the benchmark's CPU-baseline leg may build, load or call it; the product
+ * path never does, and it shares no code, header or table with the HIP path.
+ *
+ * What it computes (paper, Sec. 3 "MonarchAttention" and its "Implementation"
+ * paragraph; the algorithm of Fig. "Python-like code for MonarchAttention"):
+ * for every (batch, head) slice with Q, K, V in R^{N x d}, N = m*b,
+ *
+ *   Qbar[j][l] = Q[l*b + j],  Kbar[k][i] = K[k*b + i],  Vbar[k][i] = V[k*b + i]
+ *                        (row (l,j) of the "transpose" permutation P, Sec. 2)
+ *   L^(0)[j][k][l] = delta_kl                            (init, Sec. 3)
+ *   for t = 1..T:
+ *     alpha_R[k][j] = sum_l L[j][k][l] Qbar[j][l]        (eq. beta_r)
+ *     c_R[k][j]     = sum_l L[j][k][l]                   (eq. beta_r)
+ *     beta_R[k][j][i] = <alpha_R[k][j], Kbar[k][i]>      (eq. beta_r)
+ *     R[k][j][:]    = softmax_i(beta_R[k][j][:] / c_R[k][j])       (eq. R_update)
+ *     alpha_L[j][k] = sum_i R[k][j][i] Kbar[k][i]        (eq. beta_l)
+ *     c_L[j][k]     = sum_i R[k][j][i] log R[k][j][i]    (eq. beta_l)
+ *     beta_L[j][k][l] = <alpha_L[j][k], Qbar[j][l]>      (eq. beta_l)
+ *     L[j][:][l]    = softmax_k(beta_L[j][:][l] - c_L[j][:])       (eq. L_update)
+ *   Y[j][k]     = sum_i R[k][j][i] Vbar[k][i]            (eq. monarch_multiply)
+ *   O[l*b + j]  = sum_k L[j][k][l] Y[j][k]               (eq. monarch_multiply)
+ *
+ * The scores use Q K^T / sqrt(d): the factor s = 1/sqrt(d) is absorbed into Q
+ * (Sec. 2, footnote on attention), i.e. Qbar above holds s * Q.
+ *
+ * Organisation: the state form of the Implementation paragraph, in which L and
+ * R are never stored; only alpha_R, c_R, alpha_L, c_L (and Y) are kept.  At
+ * t = 1 the identity L^(0) gives alpha_R[k][j] = Qbar[j][k] = s*Q[k*b + j] and
+ * c_R = 1.  The R half-step runs over all (k, j) and the L half-step over all
+ * (j, l); in the last iteration the L half-step is fused with the second
+ * Monarch product, exactly as the paper's last two kernels do.  OpenMP
+ * distributes the independent (head, k) and (head, j) units; it does not
+ * change any element's arithmetic.
+ *
+ * c_L follows its definition: sum_i R log R, with the limit 0 * log 0 = 0 for
+ * entries that underflow to zero.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define MO_OK 0
+#define MO_EINVAL 1
+#define MO_ENOMEM 4
+
+/* One R half-step for unit (head, k), eq. R_update, beta_r, beta_l.
+ * aR[k][j][:] and cR[k][j] are the inputs; writes aL[j][k][:], cL[j][k] and,
+ * when y != NULL, Y[j][k][:]. */
+static void r_half_step(const double *Kh, const double *Vh, const double *aR, const double *cR,
+                        double *aL, double *cL, double *Y, int64_t m, int64_t b, int64_t d,
+                        int64_t k, double *z)
+{
+    const double *Kk = Kh + k * b * d; /* Kbar[k][i] = K[k*b + i] */
+    const double *Vk = Vh ? Vh + k * b * d : NULL;
+    for (int64_t j = 0; j < b; ++j) {
+        const double *a = aR + (k * b + j) * d;
+        const double c = cR[k * b + j];
+        double zmax = -INFINITY;
+        for (int64_t i = 0; i < b; ++i) {
+            double beta = 0.0;
+            for (int64_t v = 0; v < d; ++v) beta += a[v] * Kk[i * d + v];
+            z[i] = beta / c;
+            if (z[i] > zmax) zmax = z[i];
+        }
+        double sum = 0.0;
+        for (int64_t i = 0; i < b; ++i) {
+            z[i] = exp(z[i] - zmax);
+            sum += z[i];
+        }
+        double neg_entropy = 0.0;
+        for (int64_t i = 0; i < b; ++i) {
+            z[i] /= sum; /* z now holds R[k][j][:] */
+            if (z[i] > 0.0) neg_entropy += z[i] * log(z[i]);
+        }
+        cL[j * m + k] = neg_entropy;
+        double *al = aL + (j * m + k) * d;
+        for (int64_t v = 0; v < d; ++v) {
+            double acc = 0.0;
+            for (int64_t i = 0; i < b; ++i) acc += z[i] * Kk[i * d + v];
+            al[v] = acc;
+        }
+        if (Y) {
+            double *y = Y + (j * m + k) * d;
+            for (int64_t v = 0; v < d; ++v) {
+                double acc = 0.0;
+                for (int64_t i = 0; i < b; ++i) acc += z[i] * Vk[i * d + v];
+                y[v] = acc;
+            }
+        }
+    }
+}
+
+/* One L half-step for unit (head, j), eq. L_update and beta_l.  Qs is s*Q of
+ * this head.  When O == NULL it accumulates aR[k][j][:] and cR[k][j] for the
+ * next R half-step (eq. beta_r); otherwise it forms O[l*b + j] from Y (eq.
+ * monarch_multiply). */
+static void l_half_step(const double *Qs, const double *aL, const double *cL, const double *Y,
+                        double *aR, double *cR, double *O, int64_t m, int64_t b, int64_t d,
+                        int64_t j, double *z)
+{
+    if (!O) {
+        for (int64_t k = 0; k < m; ++k) {
+            cR[k * b + j] = 0.0;
+            memset(aR + (k * b + j) * d, 0, (size_t)d * sizeof(double));
+        }
+    }
+    for (int64_t l = 0; l < m; ++l) {
+        const double *qb = Qs + (l * b + j) * d; /* Qbar[j][l] = Q[l*b + j] */
+        double zmax = -INFINITY;
+        for (int64_t k = 0; k < m; ++k) {
+            const double *al = aL + (j * m + k) * d;
+            double beta = 0.0;
+            for (int64_t v = 0; v < d; ++v) beta += al[v] * qb[v];
+            z[k] = beta - cL[j * m + k];
+            if (z[k] > zmax) zmax = z[k];
+        }
+        double sum = 0.0;
+        for (int64_t k = 0; k < m; ++k) {
+            z[k] = exp(z[k] - zmax);
+            sum += z[k];
+        }
+        for (int64_t k = 0; k < m; ++k) z[k] /= sum; /* z now holds L[j][:][l] */
+        if (!O) {
+            for (int64_t k = 0; k < m; ++k) {
+                cR[k * b + j] += z[k];
+                double *ar = aR + (k * b + j) * d;
+                for (int64_t v = 0; v < d; ++v) ar[v] += z[k] * qb[v];
+            }
+        } else {
+            double *o = O + (l * b + j) * d;
+            for (int64_t v = 0; v < d; ++v) {
+                double acc = 0.0;
+                for (int64_t k = 0; k < m; ++k) acc += z[k] * Y[(j * m + k) * d + v];
+                o[v] = acc;
+            }
+        }
+    }
+}
+
+int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double *out, int64_t B,
+                      int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
+                      int32_t threads)
+{
+    if (!q || !k || !v || !out) return MO_EINVAL;
+    if (B < 1 || H < 1 || d < 1 || m < 1 || b < 1 || T < 1 || m * b != N) return MO_EINVAL;
+    const int64_t BH = B * H, nd = N * d;
+    const double s = 1.0 / sqrt((double)d);
+    double *Qs = malloc(sizeof(double) * (size_t)(BH * nd));
+    double *aR = malloc(sizeof(double) * (size_t)(BH * nd));
+    double *aL = malloc(sizeof(double) * (size_t)(BH * nd));
+    double *Y = malloc(sizeof(double) * (size_t)(BH * nd));
+    double *cR = malloc(sizeof(double) * (size_t)(BH * N));
+    double *cL = malloc(sizeof(double) * (size_t)(BH * N));
+    if (!Qs || !aR || !aL || !Y || !cR || !cL) {
+        free(Qs); free(aR); free(aL); free(Y); free(cR); free(cL);
+        return MO_ENOMEM;
+    }
+#ifdef _OPENMP
+    if (threads > 0) omp_set_num_threads(threads);
+#else
+    (void)threads;
+#endif
+    const int64_t zlen = (m > b ? m : b);
+
+    /* Scale absorbed into Q; t = 1 state from L^(0) = I: alpha_R[k][j] = s*Q[k*b+j], c_R = 1. */
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < BH * nd; ++e) {
+        Qs[e] = s * q[e];
+        aR[e] = Qs[e];
+    }
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < BH * N; ++e) cR[e] = 1.0;
+
+    for (int32_t t = 1; t <= T; ++t) {
+        const int last = (t == T);
+#pragma omp parallel
+        {
+            double *z = malloc(sizeof(double) * (size_t)zlen);
+#pragma omp for collapse(2) schedule(static)
+            for (int64_t h = 0; h < BH; ++h)
+                for (int64_t kk = 0; kk < m; ++kk)
+                    r_half_step(k + h * nd, last ? v + h * nd : NULL, aR + h * nd, cR + h * N,
+                                aL + h * nd, cL + h * N, last ? Y + h * nd : NULL, m, b, d, kk, z);
+#pragma omp for collapse(2) schedule(static)
+            for (int64_t h = 0; h < BH; ++h)
+                for (int64_t j = 0; j < b; ++j)
+                    l_half_step(Qs + h * nd, aL + h * nd, cL + h * N, Y + h * nd, aR + h * nd,
+                                cR + h * N, last ? out + h * nd : NULL, m, b, d, j, z);
+            free(z);
+        }
+    }
+    free(Qs); free(aR); free(aL); free(Y); free(cR); free(cL);
+    return MO_OK;
+}
+
+/* Exact softmax attention O = softmax(Q K^T / sqrt(d)) V (eq. softmax_attention),
+ * used only for the approximation-quality number.  rows: number of query rows
+ * of each head to evaluate (row indices given in `row_idx`, or the first
+ * `rows` rows when row_idx == NULL); out is [B*H, rows, d]. */
+int ma_oracle_dense_attn_f64(const double *q, const double *k, const double *v, double *out,
+                             int64_t BH, int64_t N, int64_t d, const int64_t *row_idx,
+                             int64_t rows, int32_t threads)
+{
+    if (!q || !k || !v || !out || BH < 1 || N < 1 || d < 1 || rows < 1) return MO_EINVAL;
+#ifdef _OPENMP
+    if (threads > 0) omp_set_num_threads(threads);
+#else
+    (void)threads;
+#endif
+    const double s = 1.0 / sqrt((double)d);
+#pragma omp parallel
+    {
+        double *z = malloc(sizeof(double) * (size_t)N);
+#pragma omp for collapse(2) schedule(static)
+        for (int64_t h = 0; h < BH; ++h)
+            for (int64_t r = 0; r < rows; ++r) {
+                const int64_t row = row_idx ? row_idx[r] : r;
+                const double *qr = q + (h * N + row) * d;
+                const double *kh = k + h * N * d, *vh = v + h * N * d;
+                double zmax = -INFINITY, sum = 0.0;
+                for (int64_t c = 0; c < N; ++c) {
+                    double acc = 0.0;
+                    for (int64_t e = 0; e < d; ++e) acc += qr[e] * kh[c * d + e];
+                    z[c] = s * acc;
+                    if (z[c] > zmax) zmax = z[c];
+                }
+                for (int64_t c = 0; c < N; ++c) {
+                    z[c] = exp(z[c] - zmax);
+                    sum += z[c];
+                }
+                double *o = out + (h * rows + r) * d;
+                for (int64_t e = 0; e < d; ++e) o[e] = 0.0;
+                for (int64_t c = 0; c < N; ++c) {
+                    const double w = z[c] / sum;
+                    for (int64_t e = 0; e < d; ++e) o[e] += w * vh[c * d + e];
+                }
+            }
+        free(z);
+    }
+    return MO_OK;
+}
+
+int ma_oracle_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

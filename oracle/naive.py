@@ -1,0 +1,202 @@
+"""Materialised-factor fp64 oracle of MonarchAttention (numpy).
+
+TEST INFRASTRUCTURE ONLY: used by the test suite to pin the C oracle; the
+product path never imports it.
+
+This is the direct form of the alternating maximisation (Sec. 3, "Alternating
+Maximization with Constraints", eqs. R_update, L_update, beta_r, beta_l), with
+the factors L[j, k, l] and R[k, j, i] held explicitly, followed by the Monarch
+product of eq. monarch_multiply.  It is written with small per-(k, j) and
+per-(j, l) vector operations so that each line can be checked against one
+equation; it is meant for small N only.
+
+Indices are 0-based: query row (l, j) is row l*b + j of Q and key row (k, i)
+is row k*b + i of K (the rows of Qbar and Kbar in eq. beta_r).  Q is scaled by
+s = 1/sqrt(d) before use (Sec. 2, attention footnote).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def sigma(i: int, m: int, b: int) -> int:
+    """Index map of the "transpose" permutation P (Sec. 2): (P x)_i = x_sigma(i)."""
+    return b * (i % m) + i // m
+
+
+def perm_matrix(m: int, b: int) -> np.ndarray:
+    """P as an N x N 0/1 matrix whose row i is e_sigma(i)."""
+    n = m * b
+    p = np.zeros((n, n))
+    for i in range(n):
+        p[i, sigma(i, m, b)] = 1.0
+    return p
+
+
+def qbar(q: np.ndarray, m: int, b: int) -> np.ndarray:
+    """Qbar[j, l] = Q[l*b + j] (rows of P Q grouped in b blocks of m)."""
+    n, d = q.shape
+    out = np.empty((b, m, d))
+    for j in range(b):
+        for l in range(m):
+            out[j, l] = q[l * b + j]
+    return out
+
+
+def kbar(k: np.ndarray, m: int, b: int) -> np.ndarray:
+    """Kbar[k, i] = K[k*b + i] (consecutive blocks of b rows)."""
+    n, d = k.shape
+    out = np.empty((m, b, d))
+    for kk in range(m):
+        for i in range(b):
+            out[kk, i] = k[kk * b + i]
+    return out
+
+
+def _softmax(z: np.ndarray) -> np.ndarray:
+    e = np.exp(z - z.max())
+    return e / e.sum()
+
+
+def _xlogx_sum(p: np.ndarray) -> float:
+    nz = p > 0
+    return float(np.sum(p[nz] * np.log(p[nz])))
+
+
+def r_update(L: np.ndarray, Qb: np.ndarray, Kb: np.ndarray) -> np.ndarray:
+    """R = softmax_i(beta_R / c_R) with beta_R, c_R from L (eqs. R_update, beta_r)."""
+    b, m, _ = L.shape
+    R = np.empty((m, b, b))
+    for k in range(m):
+        for j in range(b):
+            alpha_r = L[j, k, :] @ Qb[j]          # sum_l L[j,k,l] Qbar[j,l,:]
+            c_r = L[j, k, :].sum()                # sum_l L[j,k,l]
+            beta_r = Kb[k] @ alpha_r              # beta_R[k,j,i] = <alpha_R[k,j], Kbar[k,i]>
+            R[k, j] = _softmax(beta_r / c_r)
+    return R
+
+
+def l_update(R: np.ndarray, Qb: np.ndarray, Kb: np.ndarray) -> np.ndarray:
+    """L = softmax_k(beta_L - c_L) with beta_L, c_L from R (eqs. L_update, beta_l)."""
+    m, b, _ = R.shape
+    L = np.empty((b, m, m))
+    for j in range(b):
+        alpha_l = np.stack([R[k, j] @ Kb[k] for k in range(m)])       # [k, v]
+        c_l = np.array([_xlogx_sum(R[k, j]) for k in range(m)])        # sum_i R log R
+        for l in range(m):
+            beta_l = alpha_l @ Qb[j, l]                                 # over k
+            L[j, :, l] = _softmax(beta_l - c_l)
+    return L
+
+
+def monarch_apply(L: np.ndarray, R: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """O = M V by the two-step product of eq. monarch_multiply."""
+    b, m, _ = L.shape
+    Vb = kbar(v, m, b)
+    Y = np.empty((b, m, v.shape[1]))
+    for j in range(b):
+        for k in range(m):
+            Y[j, k] = R[k, j] @ Vb[k]            # sum_i R[k,j,i] Vbar[k,i,:]
+    O = np.empty_like(v)
+    for l in range(m):
+        for j in range(b):
+            O[l * b + j] = L[j, :, l] @ Y[j]     # sum_k L[j,k,l] Y[j,k,:]
+    return O
+
+
+def factors(q, k, m, b, T, *, history=False):
+    """Run T (R, L) update pairs from L^(0) = I (Sec. 3).  q, k: one head [N, d].
+
+    Returns (L, R) after T steps; with history=True also the list of
+    (L, R) pairs after every half-step, starting with (L^(0), None).
+    """
+    n, d = q.shape
+    assert n == m * b and T >= 1
+    s = 1.0 / np.sqrt(d)
+    Qb = qbar(s * q, m, b)
+    Kb = kbar(k, m, b)
+    L = np.stack([np.eye(m) for _ in range(b)])    # L^(0)[j,k,l] = delta_kl
+    R = None
+    hist = [(L, None)]
+    for _ in range(T):
+        R = r_update(L, Qb, Kb)                     # R before L in every step
+        hist.append((L, R))
+        L = l_update(R, Qb, Kb)
+        hist.append((L, R))
+    return (L, R, hist) if history else (L, R)
+
+
+def monarch_attention_head(q, k, v, m, b, T):
+    """One head: O = M^(T) V.  q, k, v: [N, d] float64."""
+    L, R = factors(q, k, m, b, T)
+    return monarch_apply(L, R, v)
+
+
+def monarch_attention(q, k, v, m, b, T):
+    """All heads: q, k, v [B, H, N, d] float64."""
+    out = np.empty_like(v)
+    for bi in range(q.shape[0]):
+        for h in range(q.shape[1]):
+            out[bi, h] = monarch_attention_head(q[bi, h], k[bi, h], v[bi, h], m, b, T)
+    return out
+
+
+def dense_monarch(L: np.ndarray, R: np.ndarray) -> np.ndarray:
+    """M from the block/entrywise form (eq. monarch_entrywise): M[l*b+j, k*b+i] = L[j,k,l] R[k,j,i]."""
+    b, m, _ = L.shape
+    n = m * b
+    M = np.empty((n, n))
+    for l in range(m):
+        for j in range(b):
+            for k in range(m):
+                M[l * b + j, k * b: (k + 1) * b] = L[j, k, l] * R[k, j, :]
+    return M
+
+
+def dense_monarch_factored(L: np.ndarray, R: np.ndarray) -> np.ndarray:
+    """M = P^T B with B = blockdiag(L_j^T) P blockdiag(R_k) (Sec. 2, Monarch matrices)."""
+    b, m, _ = L.shape
+    n = m * b
+    left = np.zeros((n, n))
+    for j in range(b):
+        left[j * m:(j + 1) * m, j * m:(j + 1) * m] = L[j].T      # (L_j)[k, l] = L[j,k,l]
+    right = np.zeros((n, n))
+    for k in range(m):
+        right[k * b:(k + 1) * b, k * b:(k + 1) * b] = R[k]        # (R_k)[j, i] = R[k,j,i]
+    P = perm_matrix(m, b)
+    return P.T @ (left @ P @ right)
+
+
+def objective_dense(A: np.ndarray, q: np.ndarray, k: np.ndarray) -> float:
+    """f(A; Q, K) = <A, s Q K^T> + H(A) (eq. softmax_variational_attention), 0 log 0 = 0."""
+    s = 1.0 / np.sqrt(q.shape[1])
+    return float(np.sum(A * (s * q @ k.T))) - _xlogx_sum(A)
+
+
+def objective_monarch(L: np.ndarray, R: np.ndarray, q: np.ndarray, k: np.ndarray) -> float:
+    """f(M; Q, K) from the factors via the separable entropy (Sec. 3, Softmax Objective):
+    sum_{j,k} <Qtilde_j^T L_jk, K_k^T R_kj> + (1^T R_kj) H(L_jk) + (1^T L_jk) H(R_kj)."""
+    b, m, _ = L.shape
+    s = 1.0 / np.sqrt(q.shape[1])
+    Qb = qbar(s * q, m, b)
+    Kb = kbar(k, m, b)
+    f = 0.0
+    for j in range(b):
+        for kk in range(m):
+            lv, rv = L[j, kk], R[kk, j]
+            f += float((Qb[j].T @ lv) @ (Kb[kk].T @ rv))
+            f += rv.sum() * (-_xlogx_sum(lv)) + lv.sum() * (-_xlogx_sum(rv))
+    return f
+
+
+def dense_softmax_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """O = softmax(Q K^T / sqrt(d)) V, rows softmaxed (eq. softmax_attention). One head."""
+    z = (q @ k.T) / np.sqrt(q.shape[1])
+    z = z - z.max(axis=1, keepdims=True)
+    e = np.exp(z)
+    return (e / e.sum(axis=1, keepdims=True)) @ v
+
+
+def log_sum_exp(z: np.ndarray) -> float:
+    zm = z.max()
+    return float(zm + np.log(np.sum(np.exp(z - zm))))

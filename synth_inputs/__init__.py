@@ -1,0 +1,201 @@
+"""Seeded synthetic Q, K, V for the MonarchAttention forward pass.
+
+This module only draws numbers: it holds none of the method's arithmetic, and
+both the oracle and the HIP path take their inputs from it.  Every tensor is
+[B, H, N, d], drawn in float64 from numpy's PCG64 generator seeded by
+(seed, crc32(workload/tensor tag)), rounded once to the run dtype (bf16 and
+fp16 by round-to-nearest-even through float32), and handed out as float64
+arrays holding exactly the rounded values.
+
+Recipes (the paper's datasets and pretrained weights are not used; these are
+stand-ins with the shapes of its workloads):
+
+* ``iid``   -- Q, K, V iid N(0, 1).
+* ``vit``   -- Z, E, V iid N(0, 1); K = Z and Q = 0.7 Z + 0.7 E, which makes
+               attention peaky the way a trained ViT's is.
+* ``lm``    -- as ``vit`` plus a content vector u ~ N(0, I_d) shared by all
+               positions of a (batch, head), then a rotary phase: row p is
+               rotated pairwise, (x_2r, x_2r+1) by p * 10000^(-2r/d), so that
+               scores decay with |i - j|.
+               K_p = rot_p(Z_p + u), Q_p = rot_p(0.7 Z_p + 0.7 E_p + u).
+* ``speed`` -- Q, K, V iid N(0, 1), then Q and K both scaled by alpha, where
+               alpha is set by bisection so that the mean over 256 sampled
+               query rows of the largest softmax(Q K^T / sqrt(d)) weight is
+               0.10.
+"""
+from __future__ import annotations
+
+import dataclasses
+import zlib
+
+import numpy as np
+
+__all__ = [
+    "Workload",
+    "WORKLOADS",
+    "make_qkv",
+    "round_to_dtype",
+    "bf16_round",
+    "DTYPES",
+]
+
+DTYPES = ("f32", "bf16", "f16")
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    H: int
+    m: int
+    b: int
+    d: int
+    T: int
+    dtype: str
+    recipe: str
+
+    @property
+    def N(self) -> int:
+        return self.m * self.b
+
+    def with_(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+    def describe(self) -> dict:
+        return {
+            "workload": self.name,
+            "B": self.B,
+            "H": self.H,
+            "N": self.N,
+            "m": self.m,
+            "b": self.b,
+            "d": self.d,
+            "T": self.T,
+            "dtype": self.dtype,
+            "inputs": self.recipe,
+        }
+
+
+# The five workloads: a tiny fp32 parity case, ViT-B/16- and RoBERTa-base-
+# shaped attention, and the 4K / 16K speed points.
+WORKLOADS = {
+    "tiny_f32_n256": Workload("tiny_f32_n256", 1, 1, 16, 16, 64, 1, "f32", "iid"),
+    "vit_b16_n196": Workload("vit_b16_n196", 32, 12, 14, 14, 64, 2, "bf16", "vit"),
+    "roberta_n1024": Workload("roberta_n1024", 16, 12, 32, 32, 64, 2, "bf16", "lm"),
+    "speed_n4096": Workload("speed_n4096", 1, 16, 64, 64, 64, 1, "bf16", "speed"),
+    "speed_n16384": Workload("speed_n16384", 1, 16, 128, 128, 64, 2, "bf16", "speed"),
+}
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round to bfloat16 (nearest, ties to even) via float32; returns float64."""
+    f = np.ascontiguousarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+
+
+def round_to_dtype(x: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float32).astype(np.float64)
+    if dtype == "bf16":
+        return bf16_round(x)
+    if dtype == "f16":
+        return np.asarray(x, dtype=np.float32).astype(np.float16).astype(np.float64)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def _rng(seed: int, tag: str) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, zlib.crc32(tag.encode())])))
+
+
+def _normal(seed: int, tag: str, shape) -> np.ndarray:
+    return _rng(seed, tag).standard_normal(shape)
+
+
+def _rotary(x: np.ndarray) -> np.ndarray:
+    """Rotate pairs (x_2r, x_2r+1) of row p by the angle p * 10000^(-2r/d)."""
+    n, d = x.shape[-2], x.shape[-1]
+    p = np.arange(n, dtype=np.float64)[:, None]
+    r = np.arange(d // 2, dtype=np.float64)[None, :]
+    ang = p * np.power(10000.0, -2.0 * r / d)
+    c, s = np.cos(ang), np.sin(ang)
+    x0, x1 = x[..., 0::2], x[..., 1::2]
+    out = np.empty_like(x)
+    out[..., 0::2] = x0 * c - x1 * s
+    out[..., 1::2] = x0 * s + x1 * c
+    return out
+
+
+def _mean_rowmax(sraw: np.ndarray, alpha: float, d: int) -> float:
+    z = sraw * (alpha * alpha / np.sqrt(d))
+    z = z - z.max(axis=1, keepdims=True)
+    e = np.exp(z)
+    return float((e.max(axis=1) / e.sum(axis=1)).mean())
+
+
+def calibrate_alpha(q: np.ndarray, k: np.ndarray, seed: int, target: float = 0.10,
+                    rows: int = 256) -> float:
+    """Scale making the mean largest softmax weight of sampled rows equal `target`.
+
+    q, k: one head's unscaled [N, d] rows.
+    """
+    n, d = q.shape
+    idx = _rng(seed, "alpha-rows").choice(n, size=min(rows, n), replace=False)
+    sraw = q[idx] @ k.T
+    lo, hi = 0.0, 1.0
+    while _mean_rowmax(sraw, hi, d) < target:
+        hi *= 2.0
+        if hi > 1e3:
+            raise RuntimeError("cannot reach the target row-max weight")
+    for _ in range(60):
+        mid = 0.5 * (lo + hi)
+        if _mean_rowmax(sraw, mid, d) < target:
+            lo = mid
+        else:
+            hi = mid
+    return 0.5 * (lo + hi)
+
+
+def make_qkv(w: Workload, seed: int = 0):
+    """Return (q, k, v, meta): float64 [B, H, N, d] arrays of dtype-rounded values."""
+    shape = (w.B, w.H, w.N, w.d)
+    tag = f"{w.recipe}/B{w.B}H{w.H}N{w.N}d{w.d}"
+    meta = {"seed": seed, "recipe": w.recipe}
+    if w.recipe == "iid":
+        q = _normal(seed, tag + "/q", shape)
+        k = _normal(seed, tag + "/k", shape)
+        v = _normal(seed, tag + "/v", shape)
+    elif w.recipe in ("vit", "lm"):
+        z = _normal(seed, tag + "/z", shape)
+        e = _normal(seed, tag + "/e", shape)
+        v = _normal(seed, tag + "/v", shape)
+        k = z
+        q = 0.7 * z + 0.7 * e
+        if w.recipe == "lm":
+            u = _normal(seed, tag + "/u", (w.B, w.H, 1, w.d))
+            k = _rotary(k + u)
+            q = _rotary(q + u)
+    elif w.recipe == "speed":
+        q = _normal(seed, tag + "/q", shape)
+        k = _normal(seed, tag + "/k", shape)
+        v = _normal(seed, tag + "/v", shape)
+        alpha = calibrate_alpha(q[0, 0], k[0, 0], seed)
+        q *= alpha
+        k *= alpha
+        meta["alpha"] = alpha
+    else:
+        raise ValueError(f"unknown recipe {w.recipe!r}")
+    q = round_to_dtype(q, w.dtype)
+    k = round_to_dtype(k, w.dtype)
+    v = round_to_dtype(v, w.dtype)
+    return q, k, v, meta
+
+
+def random_qkv(B, H, N, d, dtype="f32", seed=0, scale=1.0):
+    """Plain iid N(0, scale^2) inputs of any shape, for small parity and property cases."""
+    tag = f"random/B{B}H{H}N{N}d{d}s{scale}"
+    q = round_to_dtype(scale * _normal(seed, tag + "/q", (B, H, N, d)), dtype)
+    k = round_to_dtype(scale * _normal(seed, tag + "/k", (B, H, N, d)), dtype)
+    v = round_to_dtype(_normal(seed, tag + "/v", (B, H, N, d)), dtype)
+    return q, k, v

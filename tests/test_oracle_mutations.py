@@ -1,0 +1,182 @@
+"""The pins are sharp: plant one plausible mistake in the (numpy) oracle at a
+time, on the CPU, and check that at least one pin then fails.
+
+Each mutant is a small edit of one update of the materialised-factor oracle
+(a dropped term, a wrong sign, a transposed index, a wrong initialisation).
+The pin battery below re-runs the paper-derived checks of
+test_oracle_pins.py against the mutated functions.
+"""
+import numpy as np
+import pytest
+
+import oracle.naive as nv
+import synth_inputs as si
+
+
+def _head(m, b, d, seed, scale=2.0):
+    q, k, v = si.random_qkv(1, 1, m * b, d, "f32", seed=seed, scale=scale)
+    return q[0, 0], k[0, 0], v[0, 0]
+
+
+def _battery():
+    """Return the names of the pins that fail with the current oracle functions."""
+    failed = []
+    # permutation worked example
+    x = np.arange(1.0, 7.0)
+    if not np.array_equal(nv.qbar(x[:, None], 2, 3).reshape(-1), np.array([1, 4, 2, 5, 3, 6.0])):
+        failed.append("perm")
+    # block maximisers and ascent, T = 2 and 3
+    for T in (2, 3):
+        m, b = 3, 4
+        q, k, v = _head(m, b, 5, seed=100 + T)
+        try:
+            L, R, hist = nv.factors(q, k, m, b, T, history=True)
+        except Exception:
+            failed.append("crash")
+            continue
+        M = nv.dense_monarch(L, R)
+        if not (np.all(M >= -1e-15) and np.allclose(M.sum(axis=1), 1.0, atol=1e-12)):
+            failed.append("stochastic")
+        vals = [nv.objective_dense(nv.dense_monarch(Lh, Rh), q, k) for Lh, Rh in hist[1:]]
+        if any(b2 < a2 - 1e-12 for a2, b2 in zip(vals, vals[1:])):
+            failed.append("ascent")
+        rng = np.random.default_rng(T)
+        Lp, Rl = hist[-2]
+        f_r = nv.objective_dense(nv.dense_monarch(Lp, Rl), q, k)
+        f_l = nv.objective_dense(nv.dense_monarch(L, R), q, k)
+        for _ in range(30):
+            kk, j = rng.integers(m), rng.integers(b)
+            R2 = Rl.copy()
+            R2[kk, j] = 0.99 * R2[kk, j] + 0.01 * rng.dirichlet(np.ones(b))
+            if nv.objective_dense(nv.dense_monarch(Lp, R2), q, k) > f_r + 1e-12:
+                failed.append("R-maximiser")
+                break
+        for _ in range(30):
+            j, l = rng.integers(b), rng.integers(m)
+            L2 = L.copy()
+            L2[j, :, l] = 0.99 * L2[j, :, l] + 0.01 * rng.dirichlet(np.ones(m))
+            if nv.objective_dense(nv.dense_monarch(L2, R), q, k) > f_l + 1e-12:
+                failed.append("L-maximiser")
+                break
+    # special cases
+    for (m, b, T) in ((1, 6, 2), (6, 1, 2)):
+        q, k, v = _head(m, b, 4, seed=200)
+        o = nv.monarch_attention_head(q, k, v, m, b, T)
+        if np.abs(o - nv.dense_softmax_attention(q, k, v)).max() > 1e-12:
+            failed.append(f"exact-m{m}-b{b}")
+    q, k, v = _head(4, 3, 4, seed=300)
+    q[:] = q[0]
+    if np.abs(nv.monarch_attention_head(q, k, v, 4, 3, 2) - nv.dense_softmax_attention(q, k, v)).max() > 1e-12:
+        failed.append("identical-queries")
+    q, k, v = _head(4, 3, 4, seed=301)
+    if np.abs(nv.monarch_attention_head(q, 0 * k, v, 4, 3, 2) - v.mean(axis=0)).max() > 1e-12:
+        failed.append("zero-keys")
+    # key-block permutation is not a symmetry (L^(0) = I pairs query block l with key block l)
+    q, k, v = _head(4, 3, 4, seed=302)
+    perm = np.concatenate([np.arange(3, 6), np.arange(0, 3), np.arange(6, 12)])
+    o1 = nv.monarch_attention_head(q, k, v, 4, 3, 1)
+    o2 = nv.monarch_attention_head(q, k[perm], v[perm], 4, 3, 1)
+    if np.abs(o1 - o2).max() < 1e-6:
+        failed.append("block-symmetry")
+    # apply against the dense matrix
+    m, b = 3, 4
+    q, k, v = _head(m, b, 5, seed=400)
+    L, R = nv.factors(q, k, m, b, 2)
+    if np.abs(nv.monarch_apply(L, R, v) - nv.dense_monarch(L, R) @ v).max() > 1e-12:
+        failed.append("apply")
+    return failed
+
+
+def test_unmutated_oracle_passes_battery():
+    assert _battery() == []
+
+
+def _softmax(z):
+    e = np.exp(z - z.max())
+    return e / e.sum()
+
+
+def _r_update_variant(kind):
+    def r_update(L, Qb, Kb):
+        b, m, _ = L.shape
+        R = np.empty((m, b, b))
+        for k in range(m):
+            for j in range(b):
+                a = L[j, k, :] @ Qb[j]
+                c = L[j, k, :].sum()
+                beta = Kb[k] @ a
+                if kind == "no-divide":
+                    R[k, j] = _softmax(beta)
+                elif kind == "times-c":
+                    R[k, j] = _softmax(beta * c)
+                elif kind == "transposed-L":
+                    R[k, j] = _softmax((Kb[k] @ (L[j, :, k] @ Qb[j])) / L[j, :, k].sum())
+        return R
+    return r_update
+
+
+def _l_update_variant(kind):
+    def l_update(R, Qb, Kb):
+        m, b, _ = R.shape
+        L = np.empty((b, m, m))
+        for j in range(b):
+            al = np.stack([R[k, j] @ Kb[k] for k in range(m)])
+            cl = np.array([np.sum(R[k, j] * np.log(R[k, j])) for k in range(m)])
+            if kind == "plus-c":
+                cl = -cl
+            elif kind == "no-c":
+                cl = 0 * cl
+            for l in range(m):
+                z = al @ Qb[j, l] - cl
+                L[j, :, l] = _softmax(z)
+            if kind == "softmax-over-l":
+                for k in range(m):
+                    L[j, k, :] = _softmax(np.array([al[k] @ Qb[j, l] - cl[k] for l in range(m)]))
+        return L
+    return l_update
+
+
+def _apply_transposed(L, R, v):
+    return nv.__dict__["_orig_apply"](np.transpose(L, (0, 2, 1)).copy(), R, v)
+
+
+def _qbar_wrong(q, m, b):
+    n, d = q.shape
+    return q.reshape(b, m, d).copy()      # rows j*m + l instead of l*b + j
+
+
+def _factors_uniform_init(q, k, m, b, T, *, history=False):
+    n, d = q.shape
+    s = 1.0 / np.sqrt(d)
+    Qb, Kb = nv.qbar(s * q, m, b), nv.kbar(k, m, b)
+    L = np.full((b, m, m), 1.0 / m)
+    hist = [(L, None)]
+    for _ in range(T):
+        R = nv.r_update(L, Qb, Kb)
+        hist.append((L, R))
+        L = nv.l_update(R, Qb, Kb)
+        hist.append((L, R))
+    return (L, R, hist) if history else (L, R)
+
+
+MUTANTS = {
+    "R: drop the 1/c_R": ("r_update", lambda: _r_update_variant("no-divide")),
+    "R: multiply by c_R": ("r_update", lambda: _r_update_variant("times-c")),
+    "R: transposed L index": ("r_update", lambda: _r_update_variant("transposed-L")),
+    "L: add c_L": ("l_update", lambda: _l_update_variant("plus-c")),
+    "L: drop c_L": ("l_update", lambda: _l_update_variant("no-c")),
+    "L: softmax over l": ("l_update", lambda: _l_update_variant("softmax-over-l")),
+    "apply: transposed L": ("monarch_apply", lambda: _apply_transposed),
+    "layout: wrong permutation": ("qbar", lambda: _qbar_wrong),
+    "init: uniform L0": ("factors", lambda: _factors_uniform_init),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_each_mutant_is_caught(monkeypatch, name):
+    attr, make = MUTANTS[name]
+    monkeypatch.setitem(nv.__dict__, "_orig_apply", nv.monarch_apply)
+    monkeypatch.setattr(nv, attr, make())
+    with np.errstate(all="ignore"):
+        failed = _battery()
+    assert failed, f"mutant {name!r} passed every pin"
