@@ -1,0 +1,114 @@
+/*
+ * monarch_attn.h -- C ABI of the MonarchAttention forward pass on MI355X (gfx950).
+ *
+ * MonarchAttention (Yaras et al., "MonarchAttention: Zero-Shot Conversion to
+ * Fast, Hardware-Aware Structured Attention") replaces softmax(Q K^T / sqrt(d))
+ * by a Monarch matrix M = P^T B (Sec. 2, "Monarch Matrices"), whose
+ * block-diagonal factors L and R are found by T alternating closed-form
+ * maximisations of the variational softmax objective (Sec. 3, eqs. R_update,
+ * L_update, beta_r, beta_l), and returns O = M V through the two-step Monarch
+ * product (eq. monarch_multiply).  L and R are never written to memory: only
+ * the states alpha_R, c_R, alpha_L, c_L of the Implementation paragraph of
+ * Sec. 3 (and Y) cross between kernels.
+ *
+ * Index convention (0-based): with N = m * b, query row l*b + j is Qbar[j][l]
+ * and key/value row k*b + i is Kbar[k][i] / Vbar[k][i]; R[k][j][:] is a
+ * softmax over i and L[j][:][l] a softmax over k.  The scores are scaled by
+ * 1/sqrt(d).  L starts at the identity and R is updated before L in each of
+ * the T steps (Sec. 3; Appendix "Naive Algorithm").
+ *
+ * All functions are plain C, thread-safe, and never throw.
+ */
+#ifndef MONARCH_ATTN_H
+#define MONARCH_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element types of q, k, v and out.  bf16/fp16 run the matrix products on
+ * MFMA with fp32 accumulation; all softmax statistics and the normalisers
+ * c_R, c_L are fp32.  fp32 runs fp32 MFMA throughout. */
+typedef enum { MA_F32 = 0, MA_BF16 = 1, MA_F16 = 2 } ma_dtype;
+
+typedef enum {
+    MA_OK = 0,
+    MA_EINVAL = 1,        /* malformed arguments: nothing was launched            */
+    MA_EUNSUPPORTED = 2,  /* well-formed but outside the supported shapes         */
+    MA_EHIP = 3,          /* a HIP runtime call or a launch failed                */
+    MA_ENOMEM = 4         /* the device workspace could not be allocated          */
+} ma_status;
+
+/*
+ * monarch_attn_fwd -- O = M^(T) V for every (batch, head) slice.
+ *
+ * Operation: Sec. 3 of the paper; the T-step alternating maximisation
+ * (eqs. R_update, L_update with beta_r, beta_l) from L^(0) = I, followed by
+ * eq. monarch_multiply.  Organised as in the paper's Implementation paragraph
+ * (state form, L and R kept on chip).
+ *
+ * q, k, v : DEVICE pointers to [B, H, N, d] row-major contiguous tensors of
+ *           element type `dtype`, 16-byte aligned.  Read only.
+ * out     : DEVICE pointer to a [B, H, N, d] tensor of the same type, 16-byte
+ *           aligned, not overlapping q, k or v.  Fully overwritten.
+ *           All four buffers are owned by the caller; the library neither
+ *           frees nor retains them.
+ * B, H    : batch and head counts (>= 1).
+ * N, m, b : sequence length, number of blocks and block size, N == m * b.
+ *           Supported: 1 <= m, b <= 128.
+ * d       : head dimension; supported: 64 or 128.  fp32 also needs
+ *           16*ceil(m/16)*d <= 8192 and 16*ceil(b/16)*d <= 8192.
+ * T       : number of (R, L) update pairs, 1 <= T <= 64.
+ * dtype   : an ma_dtype value.
+ * stream  : the hipStream_t to launch on (NULL = the null stream).
+ *
+ * Asynchronous on `stream`: returns after enqueueing, with no host
+ * synchronisation.  Arguments are checked before any HIP call; on MA_EINVAL or
+ * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  The library
+ * keeps one device workspace per device (3 N d elements plus 2 N floats per
+ * head), grown with hipMalloc on the first call that needs more; calls on
+ * different streams of one device must not overlap (they share it).  After
+ * the launches hipGetLastError is checked (MA_EHIP).  The message of the last
+ * failure on the calling thread is returned by monarch_attn_last_error().
+ */
+int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out,
+                     int64_t B, int64_t H, int64_t N, int64_t d,
+                     int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
+
+/* Text of the last failure on this thread ("" if none).  Valid until the next
+ * call into the library from this thread. */
+const char *monarch_attn_last_error(void);
+
+/* MA_OK if (N, d, m, b, T, dtype) is a supported shape, else MA_EINVAL or
+ * MA_EUNSUPPORTED (with last_error set).  Makes no HIP call. */
+int monarch_attn_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype);
+
+/* Bytes of device workspace monarch_attn_fwd needs for this shape (0 on bad
+ * arguments).  Makes no HIP call. */
+size_t monarch_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,
+                                    int64_t m, int64_t b, int32_t T, int32_t dtype);
+
+/* Free the workspace of the current device.  Must not race a running call. */
+int monarch_attn_release_workspace(void);
+
+/*
+ * Per-launch timing, for measurement only.  While enabled (flag != 0), every
+ * monarch_attn_fwd records a HIP event before and after each kernel it
+ * launches, on the caller's stream.  monarch_attn_timing_read() synchronises
+ * on the last call's final event and writes, for at most `cap` launches of
+ * that call, the duration in milliseconds to ms[i] and the kernel kind to
+ * kind[i] (0 R half-step, 1 L half-step, 2 last R half-step with Y,
+ * 3 last L half-step with the Monarch product and the store of O); it returns
+ * the number of launches of that call, or -1 on error.
+ */
+int monarch_attn_timing_enable(int32_t flag);
+int32_t monarch_attn_timing_read(float *ms, int32_t *kind, int32_t cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MONARCH_ATTN_H */

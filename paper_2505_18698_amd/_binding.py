@@ -1,0 +1,145 @@
+"""ctypes binding of libmonarch_attn.so: argument marshalling only.
+
+Every step of the forward pass runs in the library's HIP kernels.  There is
+no fallback: if the library is missing the import of this module fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmonarch_attn.so")
+
+MA_F32, MA_BF16, MA_F16 = 0, 1, 2
+MA_OK, MA_EINVAL, MA_EUNSUPPORTED, MA_EHIP, MA_ENOMEM = 0, 1, 2, 3, 4
+STATUS_NAMES = {0: "MA_OK", 1: "MA_EINVAL", 2: "MA_EUNSUPPORTED", 3: "MA_EHIP", 4: "MA_ENOMEM"}
+KIND_NAMES = {0: "r_half_step", 1: "l_half_step", 2: "r_half_step_final", 3: "monarch_apply"}
+
+# Every symbol declared in include/monarch_attn.h.
+EXPORTS = (
+    "monarch_attn_fwd",
+    "monarch_attn_last_error",
+    "monarch_attn_check",
+    "monarch_attn_workspace_bytes",
+    "monarch_attn_release_workspace",
+    "monarch_attn_timing_enable",
+    "monarch_attn_timing_read",
+)
+
+
+class MonarchAttnError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -m paper_2505_18698_amd.build` "
+            "(the HIP library is required, there is no fallback path)")
+    lib = ctypes.CDLL(LIB_PATH)
+    i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
+    lib.monarch_attn_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
+    lib.monarch_attn_fwd.restype = ctypes.c_int
+    lib.monarch_attn_last_error.argtypes = []
+    lib.monarch_attn_last_error.restype = ctypes.c_char_p
+    lib.monarch_attn_check.argtypes = [i64, i64, i64, i64, i32, i32]
+    lib.monarch_attn_check.restype = ctypes.c_int
+    lib.monarch_attn_workspace_bytes.argtypes = [i64, i64, i64, i64, i64, i64, i32, i32]
+    lib.monarch_attn_workspace_bytes.restype = ctypes.c_size_t
+    lib.monarch_attn_release_workspace.argtypes = []
+    lib.monarch_attn_release_workspace.restype = ctypes.c_int
+    lib.monarch_attn_timing_enable.argtypes = [i32]
+    lib.monarch_attn_timing_enable.restype = ctypes.c_int
+    lib.monarch_attn_timing_read.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32), i32]
+    lib.monarch_attn_timing_read.restype = ctypes.c_int32
+    return lib
+
+
+LIB = _load()
+
+
+def monarch_attn_last_error() -> str:
+    return LIB.monarch_attn_last_error().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != MA_OK:
+        raise MonarchAttnError(rc, monarch_attn_last_error())
+
+
+def monarch_attn_fwd_raw(q: int, k: int, v: int, out: int, B: int, H: int, N: int, d: int,
+                         m: int, b: int, T: int, dtype: int, stream: int | None) -> int:
+    """The C call with integer device addresses; returns the status code."""
+    return LIB.monarch_attn_fwd(q, k, v, out, B, H, N, d, m, b, T, dtype, stream or None)
+
+
+def dtype_code(torch_dtype) -> int:
+    import torch
+
+    codes = {torch.float32: MA_F32, torch.bfloat16: MA_BF16, torch.float16: MA_F16}
+    if torch_dtype not in codes:
+        raise TypeError(f"unsupported dtype {torch_dtype}")
+    return codes[torch_dtype]
+
+
+def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
+    """O = MonarchAttention(q, k, v) into `out`; torch device tensors [B, H, N, d].
+
+    `stream`: a torch.cuda.Stream, an integer hipStream_t, or None for torch's
+    current stream.  Asynchronous on that stream.  Returns `out`.
+    """
+    import torch
+
+    for name, t in (("q", q), ("k", k), ("v", v), ("out", out)):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            raise TypeError(f"{name} must be a device tensor")
+        if t.dim() != 4 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous [B, H, N, d] tensor")
+        if t.shape != q.shape or t.dtype != q.dtype:
+            raise ValueError(f"{name} must match q in shape and dtype")
+    B, H, N, d = q.shape
+    if stream is None:
+        stream = torch.cuda.current_stream(q.device).cuda_stream
+    elif not isinstance(stream, int):
+        stream = stream.cuda_stream
+    with torch.cuda.device(q.device):
+        _check(monarch_attn_fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                    B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
+    return out
+
+
+def monarch_attention(q, k, v, m: int, b: int, T: int, stream=None):
+    """Allocate `out` with torch and run monarch_attn_fwd."""
+    import torch
+
+    out = torch.empty_like(q)
+    return monarch_attn_fwd(q, k, v, out, m, b, T, stream)
+
+
+def monarch_attn_check(N: int, d: int, m: int, b: int, T: int, dtype: int) -> int:
+    return LIB.monarch_attn_check(N, d, m, b, T, dtype)
+
+
+def monarch_attn_workspace_bytes(B, H, N, d, m, b, T, dtype) -> int:
+    return int(LIB.monarch_attn_workspace_bytes(B, H, N, d, m, b, T, dtype))
+
+
+def monarch_attn_release_workspace() -> None:
+    _check(LIB.monarch_attn_release_workspace())
+
+
+def monarch_attn_timing_enable(flag: bool) -> None:
+    _check(LIB.monarch_attn_timing_enable(1 if flag else 0))
+
+
+def monarch_attn_timing_read(cap: int = 256):
+    """[(kind name, ms), ...] for the launches of the last timed call."""
+    ms = (ctypes.c_float * cap)()
+    kind = (ctypes.c_int32 * cap)()
+    n = LIB.monarch_attn_timing_read(ms, kind, cap)
+    if n < 0:
+        raise MonarchAttnError(MA_EHIP, monarch_attn_last_error())
+    return [(KIND_NAMES.get(kind[i], str(kind[i])), float(ms[i])) for i in range(min(n, cap))]

@@ -1,0 +1,101 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, it
+exports every function include/monarch_attn.h declares, and malformed or
+unsupported arguments are rejected before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "monarch_attn.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(monarch_attn_\w+)\s*\(", text)))
+
+
+def test_header_declarations_match_binding():
+    import paper_2505_18698_amd as ma
+
+    assert _declared_functions() == sorted(ma.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2505_18698_amd as ma
+
+    lib = ctypes.CDLL(ma.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+FAKE = 1 << 20  # an aligned non-null address that is never dereferenced: every case fails validation first
+
+
+@pytest.mark.parametrize(
+    "args,code",
+    [
+        # (q, k, v, out, B, H, N, d, m, b, T, dtype)
+        ((0, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),           # null q
+        ((FAKE, FAKE, FAKE, 0, 1, 1, 256, 64, 16, 16, 1, 1), 1),               # null out
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 0, 1, 256, 64, 16, 16, 1, 1), 1),        # B = 0
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 255, 64, 16, 16, 1, 1), 1),        # N != m b
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 0, 1), 1),        # T = 0
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 1, 7), 1),        # bad dtype
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 0, 16, 1, 1), 1),         # m = 0
+        ((FAKE + 2, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),    # misaligned q
+        ((FAKE, FAKE, FAKE, FAKE + 64, 1, 1, 256, 64, 16, 16, 1, 1), 1),       # out overlaps q
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 96, 16, 16, 1, 1), 2),        # d = 96
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 512, 64, 2, 256, 1, 1), 2),        # b > 128
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 65, 1), 2),       # T > 64
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 16384, 128, 128, 128, 1, 0), 2),   # fp32 tile too big
+    ],
+)
+def test_invalid_arguments_rejected_before_any_hip_call(args, code):
+    import paper_2505_18698_amd as ma
+
+    rc = ma.monarch_attn_fwd_raw(*args, None)
+    assert rc == code, ma.monarch_attn_last_error()
+    assert ma.monarch_attn_last_error() != ""
+
+
+@pytest.mark.parametrize(
+    "shape,ok",
+    [
+        ((256, 64, 16, 16, 1, 0), True),
+        ((196, 64, 14, 14, 2, 1), True),
+        ((1024, 64, 32, 32, 2, 1), True),
+        ((4096, 64, 64, 64, 3, 1), True),
+        ((16384, 64, 128, 128, 2, 1), True),
+        ((16384, 128, 128, 128, 2, 1), True),
+        ((16384, 128, 128, 128, 2, 2), True),
+        ((384, 64, 16, 24, 1, 1), True),
+        ((7, 64, 7, 1, 1, 1), True),
+        ((8192, 64, 64, 128, 2, 0), True),
+        ((16384, 128, 128, 128, 2, 0), False),
+    ],
+)
+def test_supported_shapes(shape, ok):
+    import paper_2505_18698_amd as ma
+
+    assert (ma.monarch_attn_check(*shape) == 0) == ok
+
+
+def test_workspace_bytes_formula():
+    import paper_2505_18698_amd as ma
+
+    B, H, N, d = 1, 16, 16384, 64
+    got = ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 2, 1)
+    state = B * H * N * d * 2
+    cvec = B * H * N * 4
+    assert got == 3 * state + 2 * cvec
+    assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 127, 2, 1) == 0
+
+
+def test_timing_read_without_a_timed_call_fails_cleanly():
+    import paper_2505_18698_amd as ma
+
+    with pytest.raises(ma.MonarchAttnError):
+        ma.monarch_attn_timing_read()
