@@ -1,0 +1,265 @@
+#!/usr/bin/env python
+"""Benchmark of the MonarchAttention forward pass on one MI355X.
+
+One step = one monarch_attn_fwd call: the whole forward pass (every R and L
+half-step, the Monarch product and the store of O) over one batch of
+synthetic Q, K, V already resident in HBM.  The headline workload is the
+long-sequence speed point (B=1, H=16, N=16384 = 128 x 128, d=64, bf16, T=2);
+the medium point (N=4096 = 64 x 64, T=1) is reported alongside in "also".
+
+Timed regions (HIP events on the stream the library launches on):
+  1. K steps back to back -> ms_per_step and value = B*H*N / time.
+  2. K more steps with the library's per-launch events enabled -> the average
+     duration of each kernel; the one with the largest share of the step is
+     the "dominant kernel" whose algorithmic bytes and flops give `roofline`.
+Inputs rotate over several copies (>= 512 MB in total) so that the 256 MB
+last-level cache cannot serve them from one step to the next.
+
+cpu_baseline: the fp64 C oracle, as it stands, on this host's cores, on the
+same workload (repeated whole forward passes, about 10-30 s in total).
+
+Only one GPU is supported: --gpus N with N > 1 exits with a message.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "MonarchAttention fwd heads*tokens/sec + % MFMA/HBM roofline at N=4K,16K"
+UNIT = "heads*tokens/s"
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, GB/s
+MFMA_PEAK_TFLOPS = {"bf16": 2516.6, "f16": 2516.6, "f32": 157.3}
+ROTATE_BYTES = 512 << 20
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def launch_plan(w):
+    """The kernels of one call in launch order, with the algorithmic bytes and
+    flops each moves and computes (all heads).
+
+    Bytes count each state or tensor element once per kernel that reads or
+    writes it: R half-step reads alpha_R (Q at t=1) and K, writes alpha_L and
+    c_L (reads c_R after t=1); the last one also reads V and writes Y.  The L
+    half-step reads Q, alpha_L, c_L and writes alpha_R, c_R.  The apply reads
+    Q, alpha_L, Y, c_L and writes O.  Flops are 2 per multiply-add of the
+    products (beta and alpha contractions, Y and O).
+    """
+    s = 2 if w.dtype in ("bf16", "f16") else 4
+    BH, N, d, m, b = w.B * w.H, w.N, w.d, w.m, w.b
+    nd = N * d * s
+    plan = []
+    for t in range(1, w.T + 1):
+        first, last = t == 1, t == w.T
+        rb = 3 * nd + 4 * N + (0 if first else 4 * N)
+        rf = 2 * 2 * N * b * d
+        if last:
+            rb += 2 * nd
+            rf += 2 * N * b * d
+        plan.append(("r_half_step_final" if last else "r_half_step", BH * rb, BH * rf))
+        if last:
+            plan.append(("monarch_apply", BH * (4 * nd + 4 * N), BH * 2 * 2 * N * m * d))
+        else:
+            plan.append(("l_half_step", BH * (3 * nd + 8 * N), BH * 2 * 2 * N * m * d))
+    return plan
+
+
+def call_work(w):
+    s = 2 if w.dtype in ("bf16", "f16") else 4
+    BH = w.B * w.H
+    compulsory = BH * 4 * w.N * w.d * s
+    macs = w.T * (2 * w.N * w.b * w.d + 2 * w.N * w.m * w.d) + w.N * w.b * w.d
+    return compulsory, 2 * BH * macs
+
+
+def measure(ma, torch, w, steps, warmup):
+    import synth_inputs as si
+
+    t0 = time.time()
+    q, k, v, meta = si.make_qkv(w)
+    log(f"[bench] {w.name}: inputs generated in {time.time() - t0:.1f}s")
+    td = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[w.dtype]
+    base = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
+    del q, k, v
+    set_bytes = 4 * base[0].numel() * base[0].element_size()
+    nsets = max(1, min(8, math.ceil(ROTATE_BYTES / set_bytes)))
+    sets = [(base[0].clone(), base[1].clone(), base[2].clone(), torch.empty_like(base[0])) for _ in range(nsets)]
+    del base
+
+    def step(i):
+        qq, kk, vv, oo = sets[i % nsets]
+        ma.monarch_attn_fwd(qq, kk, vv, oo, w.m, w.b, w.T)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        step(i)
+    end.record()
+    end.synchronize()
+    ms = start.elapsed_time(end) / steps
+    log(f"[bench] {w.name}: {ms * 1e3:.1f} us per step over {steps} steps ({nsets} rotating input sets)")
+
+    # per-launch kernel durations
+    plan = launch_plan(w)
+    sums = [0.0] * len(plan)
+    ma.monarch_attn_timing_enable(True)
+    try:
+        for i in range(steps):
+            step(i)
+            recs = ma.monarch_attn_timing_read()
+            assert len(recs) == len(plan), (recs, plan)
+            for j, (kind, t) in enumerate(recs):
+                assert kind == plan[j][0], (kind, plan[j][0])
+                sums[j] += t
+    finally:
+        ma.monarch_attn_timing_enable(False)
+    kernels = []
+    for (name, nbytes, nflops), tot in zip(plan, sums):
+        avg_ms = tot / steps
+        kernels.append({
+            "kernel": name,
+            "avg_us": round(avg_ms * 1e3, 3),
+            "alg_bytes": nbytes,
+            "alg_flops": nflops,
+            "GB_s": round(nbytes / (avg_ms * 1e-3) / 1e9, 1),
+            "TFLOP_s": round(nflops / (avg_ms * 1e-3) / 1e12, 2),
+        })
+    torch.cuda.synchronize()
+    del sets
+    torch.cuda.empty_cache()
+    return ms, kernels, meta, nsets
+
+
+def roofline_of(kernel, dtype):
+    t = kernel["avg_us"] * 1e-6
+    hbm_t = kernel["alg_bytes"] / (HBM_PEAK_GBS * 1e9)
+    mfma_t = kernel["alg_flops"] / (MFMA_PEAK_TFLOPS[dtype] * 1e12)
+    if hbm_t >= mfma_t:
+        achieved = kernel["alg_bytes"] / t / 1e9
+        return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": kernel["kernel"]}
+    achieved = kernel["alg_flops"] / t / 1e12
+    peak = MFMA_PEAK_TFLOPS[dtype]
+    return {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None, "kernel": kernel["kernel"]}
+
+
+def call_roofline(w, ms):
+    compulsory, flops = call_work(w)
+    t = ms * 1e-3
+    t_hbm = compulsory / (HBM_PEAK_GBS * 1e9)
+    t_mfma = flops / (MFMA_PEAK_TFLOPS[w.dtype] * 1e12)
+    return {"bound": "hbm" if t_hbm >= t_mfma else "mfma", "compulsory_bytes": compulsory, "flops": flops,
+            "t_roof_us": round(max(t_hbm, t_mfma) * 1e6, 3), "frac": round(max(t_hbm, t_mfma) / t, 4),
+            "GB_s": round(compulsory / t / 1e9, 1), "TFLOP_s": round(flops / t / 1e12, 2)}
+
+
+def cpu_baseline(w, budget_s=10.0, max_runs=20):
+    import oracle
+    import synth_inputs as si
+
+    oracle.build(force=False)
+    q, k, v, _ = si.make_qkv(w)
+    threads = oracle.max_threads()
+    runs, t0 = 0, time.time()
+    while True:
+        oracle.monarch_attention(q, k, v, w.m, w.b, w.T)
+        runs += 1
+        el = time.time() - t0
+        if el >= budget_s or runs >= max_runs:
+            break
+    rate = runs * w.B * w.H * w.N / el
+    return {"value": round(rate, 1), "unit": UNIT, "cores": threads, "kind": "oracle",
+            "sample": f"{runs} full forward passes of {w.name} (all {w.B * w.H} heads), fp64, {el:.1f}s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="speed_n16384")
+    ap.add_argument("--d", type=int, default=None, help="override the head dimension")
+    ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
+    ap.add_argument("--also", default="speed_n4096", help="comma-separated extra workloads ('' for none)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}); "
+              "the forward pass is not sharded across GPUs in this build.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    lib = os.path.join(ROOT, "paper_2505_18698_amd", "libmonarch_attn.so")
+    if not os.path.exists(lib):
+        import __graft_entry__
+
+        __graft_entry__.build()
+    import paper_2505_18698_amd as ma
+    import synth_inputs as si
+
+    w = si.WORKLOADS[args.workload]
+    if args.d:
+        w = w.with_(d=args.d)
+    if args.T:
+        w = w.with_(T=args.T)
+
+    ms, kernels, meta, nsets = measure(ma, torch, w, args.steps, args.warmup)
+    share = [k["avg_us"] for k in kernels]
+    dom = kernels[share.index(max(share))]
+    value = w.B * w.H * w.N / (ms * 1e-3)
+    cfg = w.describe()
+    cfg.update({"alpha": meta.get("alpha"), "rotating_input_sets": nsets})
+    result = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": cfg,
+        "roofline": roofline_of(dom, w.dtype),
+        "call_roofline": call_roofline(w, ms),
+        "kernels": kernels,
+    }
+    also = []
+    for name in [x for x in args.also.split(",") if x]:
+        w2 = si.WORKLOADS[name]
+        ms2, kern2, meta2, nsets2 = measure(ma, torch, w2, args.steps, args.warmup)
+        sh2 = [k["avg_us"] for k in kern2]
+        dom2 = kern2[sh2.index(max(sh2))]
+        cfg2 = w2.describe()
+        cfg2.update({"alpha": meta2.get("alpha"), "rotating_input_sets": nsets2})
+        also.append({"config": cfg2, "value": round(w2.B * w2.H * w2.N / (ms2 * 1e-3), 1), "unit": UNIT,
+                     "ms_per_step": round(ms2, 6), "roofline": roofline_of(dom2, w2.dtype),
+                     "call_roofline": call_roofline(w2, ms2), "kernels": kern2})
+    result["also"] = also
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

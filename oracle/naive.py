@@ -89,8 +89,13 @@ def l_update(R: np.ndarray, Qb: np.ndarray, Kb: np.ndarray) -> np.ndarray:
     return L
 
 
+def _f64(*xs):
+    return [np.asarray(x, dtype=np.float64) for x in xs]
+
+
 def monarch_apply(L: np.ndarray, R: np.ndarray, v: np.ndarray) -> np.ndarray:
     """O = M V by the two-step product of eq. monarch_multiply."""
+    (v,) = _f64(v)
     b, m, _ = L.shape
     Vb = kbar(v, m, b)
     Y = np.empty((b, m, v.shape[1]))
@@ -110,6 +115,7 @@ def factors(q, k, m, b, T, *, history=False):
     Returns (L, R) after T steps; with history=True also the list of
     (L, R) pairs after every half-step, starting with (L^(0), None).
     """
+    q, k = _f64(q, k)
     n, d = q.shape
     assert n == m * b and T >= 1
     s = 1.0 / np.sqrt(d)
@@ -127,13 +133,14 @@ def factors(q, k, m, b, T, *, history=False):
 
 
 def monarch_attention_head(q, k, v, m, b, T):
-    """One head: O = M^(T) V.  q, k, v: [N, d] float64."""
+    """One head: O = M^(T) V.  q, k, v: [N, d] (widened to float64)."""
     L, R = factors(q, k, m, b, T)
     return monarch_apply(L, R, v)
 
 
 def monarch_attention(q, k, v, m, b, T):
-    """All heads: q, k, v [B, H, N, d] float64."""
+    """All heads: q, k, v [B, H, N, d] (widened to float64)."""
+    q, k, v = _f64(q, k, v)
     out = np.empty_like(v)
     for bi in range(q.shape[0]):
         for h in range(q.shape[1]):
@@ -169,6 +176,7 @@ def dense_monarch_factored(L: np.ndarray, R: np.ndarray) -> np.ndarray:
 
 def objective_dense(A: np.ndarray, q: np.ndarray, k: np.ndarray) -> float:
     """f(A; Q, K) = <A, s Q K^T> + H(A) (eq. softmax_variational_attention), 0 log 0 = 0."""
+    q, k = _f64(q, k)
     s = 1.0 / np.sqrt(q.shape[1])
     return float(np.sum(A * (s * q @ k.T))) - _xlogx_sum(A)
 
@@ -176,6 +184,7 @@ def objective_dense(A: np.ndarray, q: np.ndarray, k: np.ndarray) -> float:
 def objective_monarch(L: np.ndarray, R: np.ndarray, q: np.ndarray, k: np.ndarray) -> float:
     """f(M; Q, K) from the factors via the separable entropy (Sec. 3, Softmax Objective):
     sum_{j,k} <Qtilde_j^T L_jk, K_k^T R_kj> + (1^T R_kj) H(L_jk) + (1^T L_jk) H(R_kj)."""
+    q, k = _f64(q, k)
     b, m, _ = L.shape
     s = 1.0 / np.sqrt(q.shape[1])
     Qb = qbar(s * q, m, b)
@@ -191,6 +200,7 @@ def objective_monarch(L: np.ndarray, R: np.ndarray, q: np.ndarray, k: np.ndarray
 
 def dense_softmax_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
     """O = softmax(Q K^T / sqrt(d)) V, rows softmaxed (eq. softmax_attention). One head."""
+    q, k, v = _f64(q, k, v)
     z = (q @ k.T) / np.sqrt(q.shape[1])
     z = z - z.max(axis=1, keepdims=True)
     e = np.exp(z)
@@ -198,5 +208,6 @@ def dense_softmax_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.n
 
 
 def log_sum_exp(z: np.ndarray) -> float:
+    (z,) = _f64(z)
     zm = z.max()
     return float(zm + np.log(np.sum(np.exp(z - zm))))

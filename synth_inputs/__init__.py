@@ -2,10 +2,10 @@
 
 This module only draws numbers: it holds none of the method's arithmetic, and
 both the oracle and the HIP path take their inputs from it.  Every tensor is
-[B, H, N, d], drawn in float64 from numpy's PCG64 generator seeded by
-(seed, crc32(workload/tensor tag)), rounded once to the run dtype (bf16 and
-fp16 by round-to-nearest-even through float32), and handed out as float64
-arrays holding exactly the rounded values.
+[B, H, N, d], drawn as float32 normals from numpy's PCG64 generator seeded by
+(seed, crc32(workload/tensor tag)), combined in float32, rounded once to the
+run dtype (bf16 and fp16 by round-to-nearest-even), and handed out as float32
+arrays holding exactly the rounded values (the oracle widens them to float64).
 
 Recipes (the paper's datasets and pretrained weights are not used; these are
 stand-ins with the shapes of its workloads):
@@ -88,20 +88,27 @@ WORKLOADS = {
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
-    """Round to bfloat16 (nearest, ties to even) via float32; returns float64."""
-    f = np.ascontiguousarray(x, dtype=np.float32)
-    u = f.view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
-    return u.astype(np.uint32).view(np.float32).astype(np.float64)
+    """Round to bfloat16 (nearest, ties to even) via float32; returns float32.
+
+    Finite inputs only (the carry of the rounding add cannot overflow 32 bits).
+    """
+    f = np.array(x, dtype=np.float32, copy=True, order="C")
+    u = f.view(np.uint32)
+    bias = (u >> 16) & np.uint32(1)
+    bias += np.uint32(0x7FFF)
+    u += bias
+    u &= np.uint32(0xFFFF0000)
+    return f
 
 
 def round_to_dtype(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round to the run dtype; returns float32 holding the rounded values."""
     if dtype == "f32":
-        return np.asarray(x, dtype=np.float32).astype(np.float64)
+        return np.array(x, dtype=np.float32, copy=True, order="C")
     if dtype == "bf16":
         return bf16_round(x)
     if dtype == "f16":
-        return np.asarray(x, dtype=np.float32).astype(np.float16).astype(np.float64)
+        return np.asarray(x, dtype=np.float32).astype(np.float16).astype(np.float32)
     raise ValueError(f"unknown dtype {dtype!r}")
 
 
@@ -110,7 +117,8 @@ def _rng(seed: int, tag: str) -> np.random.Generator:
 
 
 def _normal(seed: int, tag: str, shape) -> np.ndarray:
-    return _rng(seed, tag).standard_normal(shape)
+    """iid N(0, 1) drawn in float32 (ziggurat)."""
+    return _rng(seed, tag).standard_normal(shape, dtype=np.float32)
 
 
 def _rotary(x: np.ndarray) -> np.ndarray:
@@ -119,7 +127,7 @@ def _rotary(x: np.ndarray) -> np.ndarray:
     p = np.arange(n, dtype=np.float64)[:, None]
     r = np.arange(d // 2, dtype=np.float64)[None, :]
     ang = p * np.power(10000.0, -2.0 * r / d)
-    c, s = np.cos(ang), np.sin(ang)
+    c, s = np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32)
     x0, x1 = x[..., 0::2], x[..., 1::2]
     out = np.empty_like(x)
     out[..., 0::2] = x0 * c - x1 * s
@@ -142,7 +150,7 @@ def calibrate_alpha(q: np.ndarray, k: np.ndarray, seed: int, target: float = 0.1
     """
     n, d = q.shape
     idx = _rng(seed, "alpha-rows").choice(n, size=min(rows, n), replace=False)
-    sraw = q[idx] @ k.T
+    sraw = q[idx].astype(np.float64) @ k.T.astype(np.float64)
     lo, hi = 0.0, 1.0
     while _mean_rowmax(sraw, hi, d) < target:
         hi *= 2.0
@@ -158,7 +166,7 @@ def calibrate_alpha(q: np.ndarray, k: np.ndarray, seed: int, target: float = 0.1
 
 
 def make_qkv(w: Workload, seed: int = 0):
-    """Return (q, k, v, meta): float64 [B, H, N, d] arrays of dtype-rounded values."""
+    """Return (q, k, v, meta): float32 [B, H, N, d] arrays of dtype-rounded values."""
     shape = (w.B, w.H, w.N, w.d)
     tag = f"{w.recipe}/B{w.B}H{w.H}N{w.N}d{w.d}"
     meta = {"seed": seed, "recipe": w.recipe}
@@ -171,7 +179,7 @@ def make_qkv(w: Workload, seed: int = 0):
         e = _normal(seed, tag + "/e", shape)
         v = _normal(seed, tag + "/v", shape)
         k = z
-        q = 0.7 * z + 0.7 * e
+        q = np.float32(0.7) * z + np.float32(0.7) * e
         if w.recipe == "lm":
             u = _normal(seed, tag + "/u", (w.B, w.H, 1, w.d))
             k = _rotary(k + u)
@@ -181,8 +189,8 @@ def make_qkv(w: Workload, seed: int = 0):
         k = _normal(seed, tag + "/k", shape)
         v = _normal(seed, tag + "/v", shape)
         alpha = calibrate_alpha(q[0, 0], k[0, 0], seed)
-        q *= alpha
-        k *= alpha
+        q *= np.float32(alpha)
+        k *= np.float32(alpha)
         meta["alpha"] = alpha
     else:
         raise ValueError(f"unknown recipe {w.recipe!r}")
@@ -195,7 +203,7 @@ def make_qkv(w: Workload, seed: int = 0):
 def random_qkv(B, H, N, d, dtype="f32", seed=0, scale=1.0):
     """Plain iid N(0, scale^2) inputs of any shape, for small parity and property cases."""
     tag = f"random/B{B}H{H}N{N}d{d}s{scale}"
-    q = round_to_dtype(scale * _normal(seed, tag + "/q", (B, H, N, d)), dtype)
-    k = round_to_dtype(scale * _normal(seed, tag + "/k", (B, H, N, d)), dtype)
+    q = round_to_dtype(np.float32(scale) * _normal(seed, tag + "/q", (B, H, N, d)), dtype)
+    k = round_to_dtype(np.float32(scale) * _normal(seed, tag + "/k", (B, H, N, d)), dtype)
     v = round_to_dtype(_normal(seed, tag + "/v", (B, H, N, d)), dtype)
     return q, k, v

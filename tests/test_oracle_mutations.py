@@ -15,7 +15,7 @@ import synth_inputs as si
 
 def _head(m, b, d, seed, scale=2.0):
     q, k, v = si.random_qkv(1, 1, m * b, d, "f32", seed=seed, scale=scale)
-    return q[0, 0], k[0, 0], v[0, 0]
+    return q[0, 0].astype(np.float64), k[0, 0].astype(np.float64), v[0, 0].astype(np.float64)
 
 
 def _battery():

@@ -19,7 +19,7 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 def _head(m, b, d, seed=0, scale=1.5):
     q, k, v = si.random_qkv(1, 1, m * b, d, "f32", seed=seed, scale=scale)
-    return q[0, 0], k[0, 0], v[0, 0]
+    return q[0, 0].astype(np.float64), k[0, 0].astype(np.float64), v[0, 0].astype(np.float64)
 
 
 # -- the permutation P and the index layout -------------------------------------------
