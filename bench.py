@@ -183,6 +183,27 @@ def cpu_baseline(w, budget_s=10.0, max_runs=20):
             "sample": f"{runs} full forward passes of {w.name} (all {w.B * w.H} heads), fp64, {el:.1f}s"}
 
 
+def copy_sweep(torch, sizes_mb, steps, warmup):
+    """Device-to-device copies of known size (read + write = 2 x size bytes)."""
+    for mb in sizes_mb:
+        n = int(mb * (1 << 20)) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(warmup):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for _ in range(steps):
+            dst.copy_(src)
+        end.record()
+        end.synchronize()
+        ms = start.elapsed_time(end) / steps
+        print(json.dumps({"copy_mb": mb, "bytes_moved": 2 * n * 4, "us": round(ms * 1e3, 3),
+                          "GB_s": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}), flush=True)
+        del src, dst
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -193,6 +214,9 @@ def main():
     ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
     ap.add_argument("--also", default="speed_n4096", help="comma-separated extra workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-mb", type=str, default=None,
+                    help="instead of the benchmark: time torch's device copy at these sizes (MB, comma "
+                         "separated); the reference kernel for scaling HBM byte counters")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -211,6 +235,10 @@ def main():
         import __graft_entry__
 
         __graft_entry__.build()
+    if args.copy_mb:
+        copy_sweep(torch, [float(x) for x in args.copy_mb.split(",")], args.steps, args.warmup)
+        return
+
     import paper_2505_18698_amd as ma
     import synth_inputs as si
 

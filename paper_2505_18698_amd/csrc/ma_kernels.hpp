@@ -99,11 +99,6 @@ template <> struct Mma<_Float16> {
     }
 };
 
-// One wave per 16-row tile of the padded block (at most 8 waves).
-template <int NT> struct Waves {
-    static constexpr int value = NT < 8 ? NT : 8;
-};
-
 // Row stride (elements) of a row-major LDS tile with C columns: pad by 16 bytes.
 template <typename T, int C> struct Ld {
     static constexpr int row = C + 16 / (int)sizeof(T);
@@ -302,64 +297,174 @@ __device__ inline f32x4 gemm_colsum(const ProbFrags<T, NT> &pf)
     return acc;
 }
 
-// Row softmax of transposed score tiles: lane (c16, g) holds z for softmax
-// index 16t + 4g + q of row c16.  Replaces z by exp2(z - max) and returns the
-// row sum; also accumulates sum e*(z - max) into *t2 when t2 != nullptr.
-template <int NT>
-__device__ inline float softmax_cols(f32x4 *z, float *t2)
+// Row tiles per wave and waves per workgroup for a block of NT 16-row tiles:
+// two tiles per wave from 4 tiles up, so that every operand fragment read
+// from LDS feeds two MFMAs.
+#ifndef MA_ROW_TILES
+#define MA_ROW_TILES 1
+#endif
+template <int NT> struct Split {
+    static constexpr int RT = (NT >= 4 && MA_ROW_TILES >= 2) ? 2 : 1;
+    static constexpr int W = NT / RT;
+};
+
+// acc[r] = A[r0 + 0..15][0..D) * bf[r]^T for RT row blocks sharing the A
+// fragments (read once from LDS).  sA_row points to row (r0 + lane%16).
+template <typename T, int D, int RT>
+__device__ inline void gemm_scores_rt(const T *sA_row, const RowFrags<T, D> *bf, f32x4 *acc, int g)
+{
+    using M = Mma<T>;
+#pragma unroll
+    for (int r = 0; r < RT; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < D / M::KC; ++c) {
+        const typename M::frag a = *reinterpret_cast<const typename M::frag *>(sA_row + c * M::KC + g * M::KPL);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) acc[r] = M::mma(a, bf[r].f[c], acc[r]);
+    }
+}
+
+// acc[r][row][col] = sum_x X[x][c0 + row] * B_r[x][col] for RT operands B_r
+// given as fragments, sharing the A fragments read from LDS.
+template <typename T, int NT, int RT>
+__device__ inline void gemm_aggregate_rt(const T *X, int ld, int c0, const ProbFrags<T, NT> *pf, f32x4 *acc,
+                                         int lane)
+{
+    using M = Mma<T>;
+#pragma unroll
+    for (int r = 0; r < RT; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (std::is_same<T, float>::value) {
+        const int g = lane >> 4, c = lane & 15;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float a = X[(16 * t + 4 * g + q) * ld + c0 + c];
+#pragma unroll
+                for (int r = 0; r < RT; ++r) acc[r] = M::mma(a, pf[r].p[t][q], acc[r]);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < NT / 2; ++c) {
+            const typename M::frag4 lo = rows4<T>(X, ld, 32 * c, c0, lane);
+            const typename M::frag4 hi = rows4<T>(X, ld, 32 * c + 16, c0, lane);
+            const typename M::frag a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+            for (int r = 0; r < RT; ++r) acc[r] = M::mma(a, pf[r].f[c], acc[r]);
+        }
+        if constexpr (NT % 2 == 1) {
+            const typename M::frag4 a = rows4<T>(X, ld, 16 * (NT - 1), c0, lane);
+#pragma unroll
+            for (int r = 0; r < RT; ++r) acc[r] = M::mma4(a, pf[r].f4, acc[r]);
+        }
+    }
+}
+
+// Work unit of a block on an 8-XCD part: blocks are dispatched to XCDs
+// round-robin (block i runs on XCD i % 8), so unit = (i % 8) * (U / 8) + i / 8
+// gives every XCD a contiguous range of units (whole heads when U/8 is a
+// multiple of the units per head).  Falls back to i when U % 8 != 0.
+#ifndef MA_XCD_REMAP
+#define MA_XCD_REMAP 0
+#endif
+__device__ inline int64_t xcd_unit(int64_t i, int64_t U)
+{
+    return (MA_XCD_REMAP && U % 8 == 0) ? (i % 8) * (U / 8) + i / 8 : i;
+}
+
+// Maximum over the softmax index of transposed score tiles (lane holds index
+// 16t + 4g + q of row lane%16): in-lane, then across the four lane groups.
+// With RAGGED, entries at index >= n are left out.
+template <int NT, bool RAGGED>
+__device__ inline float tiles_max(const f32x4 *z, int n, int g)
 {
     float mx = kMasked;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) mx = fmaxf(fmaxf(fmaxf(mx, z[t][0]), fmaxf(z[t][1], z[t][2])), z[t][3]);
-    mx = wave_xor_max(mx, 16);
-    mx = wave_xor_max(mx, 32);
-    float sum = 0.f, acc2 = 0.f;
-#pragma unroll
     for (int t = 0; t < NT; ++t) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const float u = z[t][q] - mx;
-            const float e = __builtin_amdgcn_exp2f(u);
-            sum += e;
-            if (t2) acc2 += e * u;
-            z[t][q] = e;
+        for (int q = 0; q < 4; ++q)
+            if (!RAGGED || 16 * t + 4 * g + q < n) mx = fmaxf(mx, z[t][q]);
+    }
+    mx = wave_xor_max(mx, 16);
+    return wave_xor_max(mx, 32);
+}
+
+__device__ inline float lanegroup_sum(float x)
+{
+    x = wave_xor_sum(x, 16);
+    return wave_xor_sum(x, 32);
+}
+
+// Store the 16 x D output tile held as D/16 transposed MFMA tiles (lane holds
+// elements 16vt + 4g + q of row lane%16) to the row `row` (nullptr: skip).
+// Lanes 16g and 16(g^1) swap halves so that every lane writes 16-byte
+// chunks: each row receives 64 contiguous bytes per store instruction.
+template <typename T, int D>
+__device__ inline void store_row(T *row, const f32x4 *acc, float scale, int lane)
+{
+    const int g = lane >> 4;
+    if constexpr (std::is_same<T, float>::value) {
+        if (row) {
+#pragma unroll
+            for (int vt = 0; vt < D / 16; ++vt) *reinterpret_cast<f32x4 *>(row + 16 * vt + 4 * g) = acc[vt] * scale;
+        }
+    } else {
+        const bool odd = g & 1;
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i) {
+            u32x2 pk[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                T e[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) e[q] = to_elem<T>(acc[2 * i + h][q] * scale);
+                __builtin_memcpy(&pk[h], e, 8);
+            }
+            const u32x2 give = odd ? pk[0] : pk[1];
+            u32x2 got;
+            got[0] = __shfl_xor(give[0], 16);
+            got[1] = __shfl_xor(give[1], 16);
+            const u32x4 chunk = odd ? u32x4{got[0], got[1], pk[1][0], pk[1][1]}
+                                    : u32x4{pk[0][0], pk[0][1], got[0], got[1]};
+            if (row) *reinterpret_cast<u32x4 *>(row + 16 * (2 * i + (odd ? 1 : 0)) + 8 * (g >> 1)) = chunk;
         }
     }
-    sum = wave_xor_sum(sum, 16);
-    sum = wave_xor_sum(sum, 32);
-    if (t2) {
-        acc2 = wave_xor_sum(acc2, 16);
-        acc2 = wave_xor_sum(acc2, 32);
-        *t2 = acc2;
-    }
-    return sum;
 }
 
 struct HeadDims {
     int m, b;          // blocks and block size, N = m * b
     float s_log2e;     // log2(e) / sqrt(d)
+    int64_t units;     // work units of the launch (grid size)
 };
 
+// State layouts (per head, N = m * b):
+//   alpha_R [m][b][D] (row k*b + j), alpha_L and Y [b][m][D] (row j*m + k),
+//   c_L [m][b] (written by the R half-step of block k for all j),
+//   c_R [b][m] (written by the L half-step of class j for all k).
+// RAGGED: the softmax index range (b for R, m for L) is shorter than the padded tile.
+
 // ---------------------------------------------------------------------------------------
-// R half-step: one workgroup per (head, key block k), one wave per 16 rows j.
-// NB = b rounded up to 16.  FIRST: alpha_R = the rows of Q (L^(0) = I) and
-// c_R = 1.  FINAL: also Y.
+// R half-step: one workgroup per (head, key block k); each wave owns RT tiles
+// of 16 rows j.  NB = b rounded up to 16.  FIRST: alpha_R = the rows of Q
+// (L^(0) = I) and c_R = 1.  FINAL: also Y.
 // ---------------------------------------------------------------------------------------
-template <typename T, int NB, int D, bool FIRST, bool FINAL>
-__global__ __launch_bounds__(64 * Waves<NB / 16>::value) void r_half_step(
+template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED>
+__global__ __launch_bounds__(64 * Split<NB / 16>::W) void r_half_step(
     const T *__restrict__ q, const T *__restrict__ kmat, const T *__restrict__ vmat,
     const T *__restrict__ aR, const float *__restrict__ cR, T *__restrict__ aL,
     float *__restrict__ cL, T *__restrict__ Y, HeadDims hd)
 {
-    constexpr int NT = NB / 16, W = Waves<NT>::value;
+    constexpr int NT = NB / 16, RT = Split<NT>::RT, W = Split<NT>::W;
     constexpr int LDK = Ld<T, D>::row;
     __shared__ __attribute__((aligned(16))) T Ks[NB * LDK];
     __shared__ __attribute__((aligned(16))) T Vs[FINAL ? NB * LDK : 8];
 
     const int m = hd.m, b = hd.b;
     const int64_t N = (int64_t)m * b;
-    const int k = blockIdx.x % m;
-    const int64_t bh = blockIdx.x / m;
+    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
+    const int k = unit % m;
+    const int64_t bh = unit / m;
     const int64_t hoff = bh * N * D;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -371,65 +476,94 @@ __global__ __launch_bounds__(64 * Waves<NB / 16>::value) void r_half_step(
         load_tile<T, NB, D, LDK>([=](int r) { return vblk + (int64_t)r * D; }, b, Vs, tid, 64 * W);
     }
 
-    static_assert(W == NT, "one wave per 16-row tile");
-    {
-        const int j = wave * 16 + c16;
-        const bool jvalid = j < b;
-        const int64_t arow = hoff + ((int64_t)k * b + j) * D;  // alpha_R[k][j] (k-major)
-        RowFrags<T, D> bf;
-        bf.load(jvalid ? (FIRST ? q : aR) + arow : nullptr, g);
-        float rscale = hd.s_log2e;
+    int jr[RT];
+    RowFrags<T, D> bf[RT];
+    float rscale[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        jr[r] = (wave * RT + r) * 16 + c16;
+        const bool jvalid = jr[r] < b;
+        bf[r].load(jvalid ? (FIRST ? q : aR) + hoff + ((int64_t)k * b + jr[r]) * D : nullptr, g);
+        rscale[r] = hd.s_log2e;
         if constexpr (!FIRST) {
-            if (jvalid) rscale = hd.s_log2e / fmaxf(cR[bh * N + (int64_t)k * b + j], kTiny);
+            if (jvalid) rscale[r] = hd.s_log2e / fmaxf(cR[bh * N + (int64_t)jr[r] * m + k], kTiny);
         }
-        __syncthreads();
+    }
+    __syncthreads();
 
-        f32x4 sc[NT];  // lane holds S'[i = 16t + 4g + qq][j]
+    f32x4 sc[RT][NT];  // lane holds S'[i = 16t + 4g + qq][j] of row tile r
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+        f32x4 acc[RT];
+        gemm_scores_rt<T, D, RT>(Ks + (16 * t + c16) * LDK, bf, acc, g);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) sc[r][t] = acc[r];
+    }
+    ProbFrags<T, NT> pf[RT];
+    float inv[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        // Z = s S / c_R in log2 units: u = Z - max Z = S * rs - max S * rs  (rs > 0)
+        const float rs = rscale[r];
+        const float nb = -tiles_max<NT, RAGGED>(sc[r], b, g) * rs;
+        float sum = 0.f, t2 = 0.f;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
-            sc[t] = gemm_scores<T, D>(Ks + (16 * t + c16) * LDK, bf, g);
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq) sc[t][qq] = (16 * t + 4 * g + qq < b) ? sc[t][qq] * rscale : kMasked;
-        }
-        float t2;
-        const float sum = softmax_cols<NT>(sc, &t2);
-        const float inv = 1.0f / sum;
-        // c_L = sum_i R log R = sum_i R (Z - max) - log(sum)   (natural-log units)
-        if (g == 0 && jvalid) cL[bh * N + (int64_t)j * m + k] = kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum));
-#pragma unroll
-        for (int t = 0; t < NT; ++t) sc[t] *= inv;
-
-        ProbFrags<T, NT> pf;
-        pf.pack(sc);
-        T *aL_row = aL + hoff + ((int64_t)j * m + k) * D;  // alpha_L[j][k] (j-major)
-#pragma unroll
-        for (int vt = 0; vt < D / 16; ++vt) {
-            const f32x4 acc = gemm_aggregate<T, NT>(Ks, LDK, 16 * vt, pf, lane);
-            if (jvalid) store4<T>(aL_row + 16 * vt + 4 * g, acc);
-        }
-        if constexpr (FINAL) {
-            T *y_row = Y + hoff + ((int64_t)j * m + k) * D;
-#pragma unroll
-            for (int vt = 0; vt < D / 16; ++vt) {
-                const f32x4 acc = gemm_aggregate<T, NT>(Vs, LDK, 16 * vt, pf, lane);
-                if (jvalid) store4<T>(y_row + 16 * vt + 4 * g, acc);
+            for (int qq = 0; qq < 4; ++qq) {
+                const float u = __builtin_fmaf(sc[r][t][qq], rs, nb);
+                float e = __builtin_amdgcn_exp2f(u);
+                if (RAGGED && 16 * t + 4 * g + qq >= b) e = 0.f;
+                sum += e;
+                t2 = __builtin_fmaf(e, u, t2);
+                sc[r][t][qq] = e;
             }
         }
+        sum = lanegroup_sum(sum);
+        t2 = lanegroup_sum(t2);
+        inv[r] = 1.0f / sum;
+        // c_L = sum_i R log R = sum_i R (Z - max) - log(sum)   (natural-log units)
+        if (g == 0 && jr[r] < b)
+            cL[bh * N + (int64_t)k * b + jr[r]] = kLn2 * (t2 * inv[r] - __builtin_amdgcn_logf(sum));
+        pf[r].pack(sc[r]);  // unnormalised exp2 values; the row sum is divided out below
+    }
+    f32x4 out[RT][D / 16];
+#pragma unroll
+    for (int vt = 0; vt < D / 16; ++vt) {
+        f32x4 acc[RT];
+        gemm_aggregate_rt<T, NT, RT>(Ks, LDK, 16 * vt, pf, acc, lane);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
+    }
+#pragma unroll
+    for (int r = 0; r < RT; ++r)  // alpha_L[j][k] (j-major)
+        store_row<T, D>(jr[r] < b ? aL + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r], lane);
+    if constexpr (FINAL) {
+#pragma unroll
+        for (int vt = 0; vt < D / 16; ++vt) {
+            f32x4 acc[RT];
+            gemm_aggregate_rt<T, NT, RT>(Vs, LDK, 16 * vt, pf, acc, lane);
+#pragma unroll
+            for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
+        }
+#pragma unroll
+        for (int r = 0; r < RT; ++r)
+            store_row<T, D>(jr[r] < b ? Y + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r], lane);
     }
 }
 
 // ---------------------------------------------------------------------------------------
 // L half-step (not the last): one workgroup per (head, residue class j).
-// NM = m rounded up to 16.  Wave w first owns query rows l in [16w, 16w+16)
+// NM = m rounded up to 16.  Wave w first owns RT tiles of 16 query rows l
 // (scores and the softmax over k), then, after the probabilities have gone
-// through LDS, key-block columns k in [16w, 16w+16) (c_R and alpha_R).
+// through LDS, RT tiles of 16 key-block columns k (c_R and alpha_R).
 // ---------------------------------------------------------------------------------------
-template <typename T, int NM, int D>
-__global__ __launch_bounds__(64 * Waves<NM / 16>::value) void l_half_step(
+template <typename T, int NM, int D, bool RAGGED>
+__global__ __launch_bounds__(64 * Split<NM / 16>::W) void l_half_step(
     const T *__restrict__ q, const T *__restrict__ aL, const float *__restrict__ cL,
     T *__restrict__ aR, float *__restrict__ cR, HeadDims hd)
 {
-    constexpr int NT = NM / 16, W = Waves<NT>::value;
+    constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
     constexpr int LDQ = Ld<T, D>::row, LDP = Ld<T, NM>::row;
     constexpr int A_ELEMS = NM * LDQ, P_ELEMS = NM * LDP;
     __shared__ __attribute__((aligned(16))) T Qs[NM * LDQ];
@@ -438,8 +572,9 @@ __global__ __launch_bounds__(64 * Waves<NM / 16>::value) void l_half_step(
 
     const int m = hd.m, b = hd.b;
     const int64_t N = (int64_t)m * b;
-    const int j = blockIdx.x % b;
-    const int64_t bh = blockIdx.x / b;
+    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
+    const int j = unit % b;
+    const int64_t bh = unit / b;
     const int64_t hoff = bh * N * D;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -448,61 +583,95 @@ __global__ __launch_bounds__(64 * Waves<NM / 16>::value) void l_half_step(
     const T *al = aL + hoff + (int64_t)j * m * D;
     load_tile<T, NM, D, LDQ>([=](int l) { return qh + ((int64_t)l * b + j) * D; }, m, Qs, tid, 64 * W);
     load_tile<T, NM, D, LDQ>([=](int kk) { return al + (int64_t)kk * D; }, m, APs, tid, 64 * W);
-    for (int kk = tid; kk < NM; kk += 64 * W) cLs[kk] = kk < m ? cL[bh * N + (int64_t)j * m + kk] * kLog2e : 0.f;
+    for (int kk = tid; kk < NM; kk += 64 * W) cLs[kk] = kk < m ? cL[bh * N + (int64_t)kk * b + j] * kLog2e : 0.f;
     __syncthreads();
 
     // scores and softmax over k for the query rows of this wave
-    static_assert(W == NT, "one wave per 16-row tile");
-    const int l = wave * 16 + c16;
-    RowFrags<T, D> bf;
+    int lr[RT];
+    RowFrags<T, D> bf[RT];
 #pragma unroll
-    for (int c = 0; c < D / Mma<T>::KC; ++c)
-        bf.f[c] = *reinterpret_cast<const typename Mma<T>::frag *>(Qs + l * LDQ + c * Mma<T>::KC + g * Mma<T>::KPL);
-    f32x4 sc[NT];  // lane holds S'[k = 16t + 4g + qq][l]
+    for (int r = 0; r < RT; ++r) {
+        lr[r] = (wave * RT + r) * 16 + c16;
+#pragma unroll
+        for (int c = 0; c < D / Mma<T>::KC; ++c)
+            bf[r].f[c] = *reinterpret_cast<const typename Mma<T>::frag *>(Qs + lr[r] * LDQ + c * Mma<T>::KC +
+                                                                          g * Mma<T>::KPL);
+    }
+    f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-        sc[t] = gemm_scores<T, D>(APs + (16 * t + c16) * LDQ, bf, g);
+        f32x4 acc[RT];
+        gemm_scores_rt<T, D, RT>(APs + (16 * t + c16) * LDQ, bf, acc, g);
         const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
 #pragma unroll
-        for (int qq = 0; qq < 4; ++qq)
-            sc[t][qq] = (16 * t + 4 * g + qq < m) ? sc[t][qq] * hd.s_log2e - bias[qq] : kMasked;
+        for (int r = 0; r < RT; ++r) {
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
+        }
     }
-    const float sum = softmax_cols<NT>(sc, nullptr);
-    const float inv = (l < m) ? 1.0f / sum : 0.f;  // padded query rows carry no weight
+    float inv[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
+        float sum = 0.f;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
+                if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
+                sum += e;
+                sc[r][t][qq] = e;
+            }
+        }
+        sum = lanegroup_sum(sum);
+        inv[r] = (lr[r] < m) ? 1.0f / sum : 0.f;  // padded query rows carry no weight
+    }
     __syncthreads();  // every wave is done reading alpha_L
 
     // P[l][k] (row-major, k contiguous) into the alpha_L space
     using PT = typename std::conditional<std::is_same<T, float>::value, float, T>::type;
     PT *Ps = reinterpret_cast<PT *>(APs);
 #pragma unroll
-    for (int t = 0; t < NT; ++t) store4<PT>(Ps + l * LDP + 16 * t + 4 * g, sc[t] * inv);
+    for (int r = 0; r < RT; ++r) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) store4<PT>(Ps + lr[r] * LDP + 16 * t + 4 * g, sc[r][t] * inv[r]);
+    }
     __syncthreads();
 
-    // wave w: key-block columns k0 = 16w
-    const int k0 = wave * 16;
-    ProbFrags<T, NT> pf;  // B operand: P[l-slots][k0 + c16]
-    pf.gather(Ps, LDP, k0, lane);
-    const int kk = k0 + c16;
-    const f32x4 cs = gemm_colsum<T, NT>(pf);  // c_R[k][j] = sum_l L[j][k][l]
-    if (g == 0 && kk < m) cR[bh * N + (int64_t)kk * b + j] = cs[0];
-    T *ar_row = aR + hoff + ((int64_t)kk * b + j) * D;  // alpha_R[k][j] (k-major)
+    // wave w: key-block columns k in tiles wave*RT + r
+    int kr[RT];
+    ProbFrags<T, NT> pf[RT];  // B operand: P[l-slots][k]
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        kr[r] = (wave * RT + r) * 16 + c16;
+        pf[r].gather(Ps, LDP, (wave * RT + r) * 16, lane);
+        const f32x4 cs = gemm_colsum<T, NT>(pf[r]);  // c_R[k][j] = sum_l L[j][k][l]
+        if (g == 0 && kr[r] < m) cR[bh * N + (int64_t)j * m + kr[r]] = cs[0];
+    }
+    f32x4 out[RT][D / 16];
 #pragma unroll
     for (int vt = 0; vt < D / 16; ++vt) {
-        const f32x4 acc = gemm_aggregate<T, NT>(Qs, LDQ, 16 * vt, pf, lane);
-        if (kk < m) store4<T>(ar_row + 16 * vt + 4 * g, acc);
+        f32x4 acc[RT];
+        gemm_aggregate_rt<T, NT, RT>(Qs, LDQ, 16 * vt, pf, acc, lane);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
     }
+#pragma unroll
+    for (int r = 0; r < RT; ++r)  // alpha_R[k][j] (k-major)
+        store_row<T, D>(kr[r] < m ? aR + hoff + ((int64_t)kr[r] * b + j) * D : nullptr, out[r], 1.0f, lane);
 }
 
 // ---------------------------------------------------------------------------------------
 // Last L half-step fused with the second Monarch product and the store of O:
-// one workgroup per (head, j), one wave per 16 query rows l.
+// one workgroup per (head, j); each wave owns RT tiles of 16 query rows l.
 // ---------------------------------------------------------------------------------------
-template <typename T, int NM, int D>
-__global__ __launch_bounds__(64 * Waves<NM / 16>::value) void monarch_apply(
+template <typename T, int NM, int D, bool RAGGED>
+__global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(
     const T *__restrict__ q, const T *__restrict__ aL, const float *__restrict__ cL,
     const T *__restrict__ Y, T *__restrict__ out, HeadDims hd)
 {
-    constexpr int NT = NM / 16, W = Waves<NT>::value;
+    constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
     constexpr int LDK = Ld<T, D>::row;
     __shared__ __attribute__((aligned(16))) T As[NM * LDK];
     __shared__ __attribute__((aligned(16))) T Ys[NM * LDK];
@@ -510,8 +679,9 @@ __global__ __launch_bounds__(64 * Waves<NM / 16>::value) void monarch_apply(
 
     const int m = hd.m, b = hd.b;
     const int64_t N = (int64_t)m * b;
-    const int j = blockIdx.x % b;
-    const int64_t bh = blockIdx.x / b;
+    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
+    const int j = unit % b;
+    const int64_t bh = unit / b;
     const int64_t hoff = bh * N * D;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int g = lane >> 4, c16 = lane & 15;
@@ -520,39 +690,59 @@ __global__ __launch_bounds__(64 * Waves<NM / 16>::value) void monarch_apply(
     const T *yj = Y + hoff + (int64_t)j * m * D;
     load_tile<T, NM, D, LDK>([=](int kk) { return al + (int64_t)kk * D; }, m, As, tid, 64 * W);
     load_tile<T, NM, D, LDK>([=](int kk) { return yj + (int64_t)kk * D; }, m, Ys, tid, 64 * W);
-    for (int kk = tid; kk < NM; kk += 64 * W) cLs[kk] = kk < m ? cL[bh * N + (int64_t)j * m + kk] * kLog2e : 0.f;
+    for (int kk = tid; kk < NM; kk += 64 * W) cLs[kk] = kk < m ? cL[bh * N + (int64_t)kk * b + j] * kLog2e : 0.f;
 
-    static_assert(W == NT, "one wave per 16-row tile");
-    {
-        const int l = wave * 16 + c16;
-        const bool lvalid = l < m;
-        const int64_t qrow = hoff + ((int64_t)l * b + j) * D;  // Qbar[j][l]
-        RowFrags<T, D> bf;
-        bf.load(lvalid ? q + qrow : nullptr, g);
-        __syncthreads();
+    int lr[RT];
+    RowFrags<T, D> bf[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        lr[r] = (wave * RT + r) * 16 + c16;
+        bf[r].load(lr[r] < m ? q + hoff + ((int64_t)lr[r] * b + j) * D : nullptr, g);  // Qbar[j][l]
+    }
+    __syncthreads();
 
-        f32x4 sc[NT];  // lane holds S'[k = 16t + 4g + qq][l]
+    f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            sc[t] = gemm_scores<T, D>(As + (16 * t + c16) * LDK, bf, g);
-            const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
+    for (int t = 0; t < NT; ++t) {
+        f32x4 acc[RT];
+        gemm_scores_rt<T, D, RT>(As + (16 * t + c16) * LDK, bf, acc, g);
+        const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq)
-                sc[t][qq] = (16 * t + 4 * g + qq < m) ? sc[t][qq] * hd.s_log2e - bias[qq] : kMasked;
-        }
-        const float inv = 1.0f / softmax_cols<NT>(sc, nullptr);
+        for (int r = 0; r < RT; ++r) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) sc[t] *= inv;
-
-        ProbFrags<T, NT> pf;
-        pf.pack(sc);
-        T *o_row = out + qrow;
-#pragma unroll
-        for (int vt = 0; vt < D / 16; ++vt) {
-            const f32x4 acc = gemm_aggregate<T, NT>(Ys, LDK, 16 * vt, pf, lane);
-            if (lvalid) store4<T>(o_row + 16 * vt + 4 * g, acc);
+            for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
         }
     }
+    ProbFrags<T, NT> pf[RT];
+    float inv[RT];
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+        const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
+        float sum = 0.f;
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
+                if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
+                sum += e;
+                sc[r][t][qq] = e;
+            }
+        }
+        inv[r] = 1.0f / lanegroup_sum(sum);
+        pf[r].pack(sc[r]);  // unnormalised; the row sum is divided out of O below
+    }
+    f32x4 o[RT][D / 16];
+#pragma unroll
+    for (int vt = 0; vt < D / 16; ++vt) {
+        f32x4 acc[RT];
+        gemm_aggregate_rt<T, NT, RT>(Ys, LDK, 16 * vt, pf, acc, lane);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) o[r][vt] = acc[r];
+    }
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+        store_row<T, D>(lr[r] < m ? out + hoff + ((int64_t)lr[r] * b + j) * D : nullptr, o[r], inv[r], lane);
 }
 
 }  // namespace ma

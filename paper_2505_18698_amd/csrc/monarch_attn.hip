@@ -115,34 +115,36 @@ struct Bufs {
     float *cR, *cL;
 };
 
-template <typename T, int NB, int D>
+template <typename T, int NB, int D, bool RG>
 int launch_r(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool first, bool final_)
 {
-    constexpr int W = ma::Waves<NB / 16>::value;
-    const dim3 grid((unsigned)(BH * hd.m)), block(64 * W);
+    constexpr int W = ma::Split<NB / 16>::W;
+    hd.units = BH * hd.m;
+    const dim3 grid((unsigned)hd.units), block(64 * W);
     const T *q = (const T *)B.q, *k = (const T *)B.k, *v = (const T *)B.v;
     const T *aR = (const T *)B.aR;
     T *aL = (T *)B.aL, *Y = (T *)B.Y;
     const int kind = final_ ? 2 : 0;
     if (first && final_)
-        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, true, true>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
+        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, true, true, RG>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
     if (first)
-        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, true, false>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
+        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, true, false, RG>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
     if (final_)
-        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, false, true>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
-    return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, false, false>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
+        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, false, true, RG>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
+    return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, false, false, RG>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
 }
 
-template <typename T, int NM, int D>
+template <typename T, int NM, int D, bool RG>
 int launch_l(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool apply)
 {
-    constexpr int W = ma::Waves<NM / 16>::value;
-    const dim3 grid((unsigned)(BH * hd.b)), block(64 * W);
+    constexpr int W = ma::Split<NM / 16>::W;
+    hd.units = BH * hd.b;
+    const dim3 grid((unsigned)hd.units), block(64 * W);
     const T *q = (const T *)B.q;
     const T *aL = (const T *)B.aL, *Y = (const T *)B.Y;
     if (apply)
-        return L.run(3, [&] { hipLaunchKernelGGL((ma::monarch_apply<T, NM, D>), grid, block, 0, L.stream, q, aL, B.cL, Y, (T *)B.out, hd); });
-    return L.run(1, [&] { hipLaunchKernelGGL((ma::l_half_step<T, NM, D>), grid, block, 0, L.stream, q, aL, B.cL, (T *)B.aR, B.cR, hd); });
+        return L.run(3, [&] { hipLaunchKernelGGL((ma::monarch_apply<T, NM, D, RG>), grid, block, 0, L.stream, q, aL, B.cL, Y, (T *)B.out, hd); });
+    return L.run(1, [&] { hipLaunchKernelGGL((ma::l_half_step<T, NM, D, RG>), grid, block, 0, L.stream, q, aL, B.cL, (T *)B.aR, B.cR, hd); });
 }
 
 template <typename T, int D, int NB>
@@ -151,7 +153,8 @@ int dispatch_r(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool fir
     if constexpr (std::is_same<T, float>::value && NB * D > 8192) {
         return fail(MA_EUNSUPPORTED, "fp32 tile too large");
     } else {
-        return launch_r<T, NB, D>(L, B, hd, BH, first, final_);
+        return hd.b != NB ? launch_r<T, NB, D, true>(L, B, hd, BH, first, final_)
+                         : launch_r<T, NB, D, false>(L, B, hd, BH, first, final_);
     }
 }
 
@@ -161,7 +164,8 @@ int dispatch_l(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool app
     if constexpr (std::is_same<T, float>::value && NM * D > 8192) {
         return fail(MA_EUNSUPPORTED, "fp32 tile too large");
     } else {
-        return launch_l<T, NM, D>(L, B, hd, BH, apply);
+        return hd.m != NM ? launch_l<T, NM, D, true>(L, B, hd, BH, apply)
+                         : launch_l<T, NM, D, false>(L, B, hd, BH, apply);
     }
 }
 
@@ -325,7 +329,7 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
     const size_t cs = ((size_t)BH * N * sizeof(float) + 255) / 256 * 256;
     char *base = (char *)ws;
     Bufs bufs{q, k, v, out, base, base + st, base + 2 * st, (float *)(base + 3 * st), (float *)(base + 3 * st + cs)};
-    ma::HeadDims hd{(int)m, (int)b, (float)(1.4426950408889634 / std::sqrt((double)d))};
+    ma::HeadDims hd{(int)m, (int)b, (float)(1.4426950408889634 / std::sqrt((double)d)), 0};
 
     std::unique_lock<std::mutex> tlock(g_timing_mutex);
     Launcher L{(hipStream_t)stream, g_timing.enabled};
