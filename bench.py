@@ -140,18 +140,43 @@ def measure(ma, torch, w, steps, warmup):
     return ms, kernels, meta, nsets
 
 
-def roofline_of(kernel, dtype):
+def kernel_sources_sha():
+    import glob
+    import hashlib
+
+    src = b"".join(open(p, "rb").read()
+                   for p in sorted(glob.glob(os.path.join(ROOT, "paper_2505_18698_amd", "csrc", "*"))))
+    return hashlib.sha256(src).hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes (read + write) per launch from the committed rocprofv3 byte counters
+    (profiles/traffic.json), or None when the kernels changed since they were taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256_16") != kernel_sources_sha():
+        return None
+    k = rec.get("kernels", {}).get(f"{kernel}@{workload}")
+    return None if k is None else k["read_bytes"] + k["write_bytes"]
+
+
+def roofline_of(kernel, dtype, workload=None):
     t = kernel["avg_us"] * 1e-6
     hbm_t = kernel["alg_bytes"] / (HBM_PEAK_GBS * 1e9)
     mfma_t = kernel["alg_flops"] / (MFMA_PEAK_TFLOPS[dtype] * 1e12)
     if hbm_t >= mfma_t:
         achieved = kernel["alg_bytes"] / t / 1e9
         return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": kernel["kernel"]}
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(kernel["kernel"], workload),
+                "kernel": kernel["kernel"], "alg_bytes": kernel["alg_bytes"]}
     achieved = kernel["alg_flops"] / t / 1e12
     peak = MFMA_PEAK_TFLOPS[dtype]
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None, "kernel": kernel["kernel"]}
+            "frac": round(achieved / peak, 4), "traffic": measured_traffic(kernel["kernel"], workload),
+            "kernel": kernel["kernel"], "alg_flops": kernel["alg_flops"]}
 
 
 def call_roofline(w, ms):
@@ -268,7 +293,7 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": cfg,
-        "roofline": roofline_of(dom, w.dtype),
+        "roofline": roofline_of(dom, w.dtype, w.name),
         "call_roofline": call_roofline(w, ms),
         "kernels": kernels,
     }
@@ -281,7 +306,7 @@ def main():
         cfg2 = w2.describe()
         cfg2.update({"alpha": meta2.get("alpha"), "rotating_input_sets": nsets2})
         also.append({"config": cfg2, "value": round(w2.B * w2.H * w2.N / (ms2 * 1e-3), 1), "unit": UNIT,
-                     "ms_per_step": round(ms2, 6), "roofline": roofline_of(dom2, w2.dtype),
+                     "ms_per_step": round(ms2, 6), "roofline": roofline_of(dom2, w2.dtype, w2.name),
                      "call_roofline": call_roofline(w2, ms2), "kernels": kern2})
     result["also"] = also
     if not args.no_cpu_baseline:
