@@ -71,6 +71,18 @@ def launch_plan(w):
     return plan
 
 
+def plan_for(w, kinds):
+    """Launch plan matching the kernels one call actually ran."""
+    if kinds == ["monarch_persistent"]:
+        # one launch for the whole pass: its algorithmic traffic is the compulsory
+        # Q, K, V in and O out (the states stay on chip)
+        compulsory, flops = call_work(w)
+        return [("monarch_persistent", compulsory, flops)]
+    plan = launch_plan(w)
+    assert kinds == [p[0] for p in plan], (kinds, plan)
+    return plan
+
+
 def call_work(w):
     s = 2 if w.dtype in ("bf16", "f16") else 4
     BH = w.B * w.H
@@ -110,16 +122,17 @@ def measure(ma, torch, w, steps, warmup):
     log(f"[bench] {w.name}: {ms * 1e3:.1f} us per step over {steps} steps ({nsets} rotating input sets)")
 
     # per-launch kernel durations
-    plan = launch_plan(w)
-    sums = [0.0] * len(plan)
+    plan, sums = None, None
     ma.monarch_attn_timing_enable(True)
     try:
         for i in range(steps):
             step(i)
             recs = ma.monarch_attn_timing_read()
-            assert len(recs) == len(plan), (recs, plan)
+            if plan is None:
+                plan = plan_for(w, [kind for kind, _ in recs])
+                sums = [0.0] * len(plan)
+            assert [kind for kind, _ in recs] == [p[0] for p in plan], (recs, plan)
             for j, (kind, t) in enumerate(recs):
-                assert kind == plan[j][0], (kind, plan[j][0])
                 sums[j] += t
     finally:
         ma.monarch_attn_timing_enable(False)

@@ -68,9 +68,10 @@ typedef enum {
  * Asynchronous on `stream`: returns after enqueueing, with no host
  * synchronisation.  Arguments are checked before any HIP call; on MA_EINVAL or
  * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  The library
- * keeps one device workspace per device (3 N d elements plus 2 N floats per
- * head), grown with hipMalloc on the first call that needs more; calls on
- * different streams of one device must not overlap (they share it).  After
+ * keeps one device workspace per device ((2c + 1) N d elements plus 2c N
+ * floats per head, c = T for T <= 8 and c = 1 above, plus a few counters),
+ * grown with hipMalloc on the first call that needs more; calls on different
+ * streams of one device must not overlap (they share it).  After
  * the launches hipGetLastError is checked (MA_EHIP).  The message of the last
  * failure on the calling thread is returned by monarch_attn_last_error().
  */
@@ -95,14 +96,34 @@ size_t monarch_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,
 int monarch_attn_release_workspace(void);
 
 /*
+ * Execution path of monarch_attn_fwd (process-wide; returns the previous
+ * value, or -1 on an unknown value):
+ *   0  automatic (default): one launch per half-step;
+ *   1  one launch per half-step (the state form of the paper's
+ *      Implementation paragraph, states crossing kernels through memory);
+ *   2  single launch only: one cooperative kernel runs every half-step of a
+ *      head on the workgroups of one XCD, exchanging the states through that
+ *      XCD's L2 between in-kernel barriers; monarch_attn_fwd returns
+ *      MA_EUNSUPPORTED where it does not apply (m and b in different 16-row
+ *      tile classes, T > 8, or no cooperative launch).  Measured slower than
+ *      path 1 at every shape tried, so only taken on request.
+ * Both paths compute the same operation.  A barrier of the single-launch
+ * kernel that does not complete within its bounded wait makes the kernel
+ * return early; the next monarch_attn_fwd on that device then reports
+ * MA_EHIP.
+ */
+int monarch_attn_set_path(int32_t path);
+
+/*
  * Per-launch timing, for measurement only.  While enabled (flag != 0), every
  * monarch_attn_fwd records a HIP event before and after each kernel it
  * launches, on the caller's stream.  monarch_attn_timing_read() synchronises
  * on the last call's final event and writes, for at most `cap` launches of
  * that call, the duration in milliseconds to ms[i] and the kernel kind to
  * kind[i] (0 R half-step, 1 L half-step, 2 last R half-step with Y,
- * 3 last L half-step with the Monarch product and the store of O); it returns
- * the number of launches of that call, or -1 on error.
+ * 3 last L half-step with the Monarch product and the store of O,
+ * 4 the single-launch kernel); it returns the number of launches of that
+ * call, or -1 on error.
  */
 int monarch_attn_timing_enable(int32_t flag);
 int32_t monarch_attn_timing_read(float *ms, int32_t *kind, int32_t cap);

@@ -20,6 +20,9 @@ try:
         MA_F16,
         MA_F32,
         MA_OK,
+        PATH_AUTO,
+        PATH_HALF_STEPS,
+        PATH_SINGLE,
         MonarchAttnError,
         dtype_code,
         monarch_attention,
@@ -28,6 +31,7 @@ try:
         monarch_attn_fwd_raw,
         monarch_attn_last_error,
         monarch_attn_release_workspace,
+        monarch_attn_set_path,
         monarch_attn_timing_enable,
         monarch_attn_timing_read,
         monarch_attn_workspace_bytes,

@@ -14,7 +14,9 @@ LIB_PATH = os.path.join(_PKG, "libmonarch_attn.so")
 MA_F32, MA_BF16, MA_F16 = 0, 1, 2
 MA_OK, MA_EINVAL, MA_EUNSUPPORTED, MA_EHIP, MA_ENOMEM = 0, 1, 2, 3, 4
 STATUS_NAMES = {0: "MA_OK", 1: "MA_EINVAL", 2: "MA_EUNSUPPORTED", 3: "MA_EHIP", 4: "MA_ENOMEM"}
-KIND_NAMES = {0: "r_half_step", 1: "l_half_step", 2: "r_half_step_final", 3: "monarch_apply"}
+KIND_NAMES = {0: "r_half_step", 1: "l_half_step", 2: "r_half_step_final", 3: "monarch_apply",
+              4: "monarch_persistent"}
+PATH_AUTO, PATH_HALF_STEPS, PATH_SINGLE = 0, 1, 2
 
 # Every symbol declared in include/monarch_attn.h.
 EXPORTS = (
@@ -23,6 +25,7 @@ EXPORTS = (
     "monarch_attn_check",
     "monarch_attn_workspace_bytes",
     "monarch_attn_release_workspace",
+    "monarch_attn_set_path",
     "monarch_attn_timing_enable",
     "monarch_attn_timing_read",
 )
@@ -51,6 +54,8 @@ def _load() -> ctypes.CDLL:
     lib.monarch_attn_workspace_bytes.restype = ctypes.c_size_t
     lib.monarch_attn_release_workspace.argtypes = []
     lib.monarch_attn_release_workspace.restype = ctypes.c_int
+    lib.monarch_attn_set_path.argtypes = [i32]
+    lib.monarch_attn_set_path.restype = ctypes.c_int
     lib.monarch_attn_timing_enable.argtypes = [i32]
     lib.monarch_attn_timing_enable.restype = ctypes.c_int
     lib.monarch_attn_timing_read.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32), i32]
@@ -129,6 +134,14 @@ def monarch_attn_workspace_bytes(B, H, N, d, m, b, T, dtype) -> int:
 
 def monarch_attn_release_workspace() -> None:
     _check(LIB.monarch_attn_release_workspace())
+
+
+def monarch_attn_set_path(path: int) -> int:
+    """Select the execution path (PATH_AUTO, PATH_HALF_STEPS, PATH_SINGLE); returns the previous one."""
+    prev = LIB.monarch_attn_set_path(path)
+    if prev < 0:
+        raise MonarchAttnError(MA_EINVAL, monarch_attn_last_error())
+    return prev
 
 
 def monarch_attn_timing_enable(flag: bool) -> None:

@@ -1,16 +1,29 @@
-"""Build the HIP library libmonarch_attn.so in-tree for gfx950 with hipcc."""
+"""Build the HIP library libmonarch_attn.so in-tree for gfx950 with hipcc.
+
+Each translation unit of csrc/ (the C ABI and one dispatch unit per element
+type) is compiled separately and in parallel, then linked into one shared
+library.
+"""
 from __future__ import annotations
 
+import concurrent.futures
+import glob
 import os
 import shutil
 import subprocess
 import sys
+import tempfile
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SRC = os.path.join(PKG, "csrc", "monarch_attn.hip")
+CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmonarch_attn.so")
 ARCH = "gfx950"
+FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
+    # Packed-FP32 VALU forms are disabled; the compiler emits scalar fp32 ops instead.
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+]
 
 
 def hipcc() -> str:
@@ -20,28 +33,40 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build_command(out: str) -> list[str]:
-    return [
-        hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
-        # Packed-FP32 VALU forms are disabled; the compiler emits scalar fp32 ops instead.
-        "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-        "-I", os.path.join(ROOT, "include"),
-        SRC, "-o", out,
-    ]
+def sources() -> list[str]:
+    return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = build_command(tmp)
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed to build libmonarch_attn.so")
-    if verbose:
-        sys.stderr.write(res.stderr)
-    os.replace(tmp, LIB)
+    return res.returncode, res.stdout + res.stderr
+
+
+def build(verbose: bool = False, extra_flags=()) -> str:
+    cc = hipcc()
+    with tempfile.TemporaryDirectory(prefix="ma_build_") as tmp:
+        objs, jobs = [], []
+        for src in sources():
+            obj = os.path.join(tmp, os.path.basename(src) + ".o")
+            objs.append(obj)
+            jobs.append([cc, *FLAGS, *extra_flags, "-I", os.path.join(ROOT, "include"), "-c", src, "-o", obj])
+        workers = min(len(jobs), max(1, min(8, os.cpu_count() or 1)))
+        with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+            results = list(ex.map(_run, jobs))
+        for (rc, log), job in zip(results, jobs):
+            if rc != 0:
+                sys.stderr.write(log)
+                raise RuntimeError(f"hipcc failed on {job[-3]}")
+            if verbose:
+                sys.stderr.write(log)
+        tmp_lib = LIB + ".tmp"
+        rc, log = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp_lib])
+        if rc != 0:
+            sys.stderr.write(log)
+            raise RuntimeError("linking libmonarch_attn.so failed")
+        os.replace(tmp_lib, LIB)
     return LIB
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose="-v" in sys.argv))

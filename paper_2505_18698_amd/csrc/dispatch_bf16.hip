@@ -1,0 +1,9 @@
+// Kernels and dispatch for element type __bf16.
+#include "dispatch.hpp"
+
+namespace ma_host {
+template <> int run_call<__bf16>(Launcher &L, const CallBufs &B, const CallDims &c, int path)
+{
+    return run_call_impl<__bf16>(L, B, c, path);
+}
+}  // namespace ma_host

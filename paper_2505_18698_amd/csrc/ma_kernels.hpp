@@ -435,314 +435,526 @@ __device__ inline void store_row(T *row, const f32x4 *acc, float scale, int lane
 struct HeadDims {
     int m, b;          // blocks and block size, N = m * b
     float s_log2e;     // log2(e) / sqrt(d)
-    int64_t units;     // work units of the launch (grid size)
+    int64_t units;     // work units of a half-step launch (grid size)
 };
 
-// State layouts (per head, N = m * b):
+// Tensors and states of one call.  Layouts (per head, N = m * b):
+//   q, k, v, out [B*H][N][D];
 //   alpha_R [m][b][D] (row k*b + j), alpha_L and Y [b][m][D] (row j*m + k),
 //   c_L [m][b] (written by the R half-step of block k for all j),
 //   c_R [b][m] (written by the L half-step of class j for all k).
-// RAGGED: the softmax index range (b for R, m for L) is shorter than the padded tile.
+template <typename T> struct Bufs {
+    const T *q, *k, *v;
+    T *out;
+    T *aR, *aL, *Y;
+    float *cR, *cL;
+};
+
+// The work of one unit of each half-step, done by the first W waves of a
+// workgroup of `nthreads` threads (all threads take part in tile loads and
+// barriers).  RAGGED: the softmax index range (b for R, m for L) is shorter
+// than the padded tile.
 
 // ---------------------------------------------------------------------------------------
-// R half-step: one workgroup per (head, key block k); each wave owns RT tiles
-// of 16 rows j.  NB = b rounded up to 16.  FIRST: alpha_R = the rows of Q
-// (L^(0) = I) and c_R = 1.  FINAL: also Y.
+// R half-step for (head bh, key block k); each wave owns RT tiles of 16 rows j.
+// NB = b rounded up to 16.  FIRST: alpha_R = the rows of Q (L^(0) = I) and
+// c_R = 1.  FINAL: also Y.
 // ---------------------------------------------------------------------------------------
-template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED>
-__global__ __launch_bounds__(64 * Split<NB / 16>::W) void r_half_step(
-    const T *__restrict__ q, const T *__restrict__ kmat, const T *__restrict__ vmat,
-    const T *__restrict__ aR, const float *__restrict__ cR, T *__restrict__ aL,
-    float *__restrict__ cL, T *__restrict__ Y, HeadDims hd)
-{
-    constexpr int NT = NB / 16, RT = Split<NT>::RT, W = Split<NT>::W;
-    constexpr int LDK = Ld<T, D>::row;
-    __shared__ __attribute__((aligned(16))) T Ks[NB * LDK];
-    __shared__ __attribute__((aligned(16))) T Vs[FINAL ? NB * LDK : 8];
+template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct RHalf {
+    static constexpr int NT = NB / 16, RT = Split<NT>::RT, W = Split<NT>::W;
+    static constexpr int LDK = Ld<T, D>::row;
+    static constexpr int LDS_BYTES = (FINAL ? 2 : 1) * NB * LDK * (int)sizeof(T);
 
-    const int m = hd.m, b = hd.b;
-    const int64_t N = (int64_t)m * b;
-    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
-    const int k = unit % m;
-    const int64_t bh = unit / m;
-    const int64_t hoff = bh * N * D;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int g = lane >> 4, c16 = lane & 15;
+    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, char *lds, int tid,
+                               int nthreads)
+    {
+        T *Ks = reinterpret_cast<T *>(lds);
+        T *Vs = Ks + NB * LDK;
+        const int m = hd.m, b = hd.b;
+        const int64_t N = (int64_t)m * b;
+        const int64_t hoff = bh * N * D;
+        const int lane = tid & 63, wave = tid >> 6;
+        const int g = lane >> 4, c16 = lane & 15;
+        const bool active = wave < W;
 
-    const T *kblk = kmat + hoff + (int64_t)k * b * D;
-    load_tile<T, NB, D, LDK>([=](int r) { return kblk + (int64_t)r * D; }, b, Ks, tid, 64 * W);
-    if constexpr (FINAL) {
-        const T *vblk = vmat + hoff + (int64_t)k * b * D;
-        load_tile<T, NB, D, LDK>([=](int r) { return vblk + (int64_t)r * D; }, b, Vs, tid, 64 * W);
-    }
-
-    int jr[RT];
-    RowFrags<T, D> bf[RT];
-    float rscale[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-        jr[r] = (wave * RT + r) * 16 + c16;
-        const bool jvalid = jr[r] < b;
-        bf[r].load(jvalid ? (FIRST ? q : aR) + hoff + ((int64_t)k * b + jr[r]) * D : nullptr, g);
-        rscale[r] = hd.s_log2e;
-        if constexpr (!FIRST) {
-            if (jvalid) rscale[r] = hd.s_log2e / fmaxf(cR[bh * N + (int64_t)jr[r] * m + k], kTiny);
+        const T *kblk = p.k + hoff + (int64_t)k * b * D;
+        load_tile<T, NB, D, LDK>([=](int r) { return kblk + (int64_t)r * D; }, b, Ks, tid, nthreads);
+        if constexpr (FINAL) {
+            const T *vblk = p.v + hoff + (int64_t)k * b * D;
+            load_tile<T, NB, D, LDK>([=](int r) { return vblk + (int64_t)r * D; }, b, Vs, tid, nthreads);
         }
-    }
-    __syncthreads();
 
-    f32x4 sc[RT][NT];  // lane holds S'[i = 16t + 4g + qq][j] of row tile r
+        int jr[RT];
+        RowFrags<T, D> bf[RT];
+        float rscale[RT];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        f32x4 acc[RT];
-        gemm_scores_rt<T, D, RT>(Ks + (16 * t + c16) * LDK, bf, acc, g);
-#pragma unroll
-        for (int r = 0; r < RT; ++r) sc[r][t] = acc[r];
-    }
-    ProbFrags<T, NT> pf[RT];
-    float inv[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-        // Z = s S / c_R in log2 units: u = Z - max Z = S * rs - max S * rs  (rs > 0)
-        const float rs = rscale[r];
-        const float nb = -tiles_max<NT, RAGGED>(sc[r], b, g) * rs;
-        float sum = 0.f, t2 = 0.f;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-                const float u = __builtin_fmaf(sc[r][t][qq], rs, nb);
-                float e = __builtin_amdgcn_exp2f(u);
-                if (RAGGED && 16 * t + 4 * g + qq >= b) e = 0.f;
-                sum += e;
-                t2 = __builtin_fmaf(e, u, t2);
-                sc[r][t][qq] = e;
+        for (int r = 0; r < RT; ++r) {
+            jr[r] = (wave * RT + r) * 16 + c16;
+            const bool jvalid = active && jr[r] < b;
+            bf[r].load(jvalid ? (FIRST ? p.q : p.aR) + hoff + ((int64_t)k * b + jr[r]) * D : nullptr, g);
+            rscale[r] = hd.s_log2e;
+            if constexpr (!FIRST) {
+                if (jvalid) rscale[r] = hd.s_log2e / fmaxf(p.cR[bh * N + (int64_t)jr[r] * m + k], kTiny);
             }
         }
-        sum = lanegroup_sum(sum);
-        t2 = lanegroup_sum(t2);
-        inv[r] = 1.0f / sum;
-        // c_L = sum_i R log R = sum_i R (Z - max) - log(sum)   (natural-log units)
-        if (g == 0 && jr[r] < b)
-            cL[bh * N + (int64_t)k * b + jr[r]] = kLn2 * (t2 * inv[r] - __builtin_amdgcn_logf(sum));
-        pf[r].pack(sc[r]);  // unnormalised exp2 values; the row sum is divided out below
-    }
-    f32x4 out[RT][D / 16];
+        __syncthreads();
+        if (!active) return;
+
+        f32x4 sc[RT][NT];  // lane holds S'[i = 16t + 4g + qq][j] of row tile r
 #pragma unroll
-    for (int vt = 0; vt < D / 16; ++vt) {
-        f32x4 acc[RT];
-        gemm_aggregate_rt<T, NT, RT>(Ks, LDK, 16 * vt, pf, acc, lane);
+        for (int t = 0; t < NT; ++t) {
+            f32x4 acc[RT];
+            gemm_scores_rt<T, D, RT>(Ks + (16 * t + c16) * LDK, bf, acc, g);
 #pragma unroll
-        for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
-    }
+            for (int r = 0; r < RT; ++r) sc[r][t] = acc[r];
+        }
+        ProbFrags<T, NT> pf[RT];
+        float inv[RT];
 #pragma unroll
-    for (int r = 0; r < RT; ++r)  // alpha_L[j][k] (j-major)
-        store_row<T, D>(jr[r] < b ? aL + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r], lane);
-    if constexpr (FINAL) {
+        for (int r = 0; r < RT; ++r) {
+            // Z = s S / c_R in log2 units: u = Z - max Z = S * rs - max S * rs  (rs > 0)
+            const float rs = rscale[r];
+            const float nb = -tiles_max<NT, RAGGED>(sc[r], b, g) * rs;
+            float sum = 0.f, t2 = 0.f;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    const float u = __builtin_fmaf(sc[r][t][qq], rs, nb);
+                    float e = __builtin_amdgcn_exp2f(u);
+                    if (RAGGED && 16 * t + 4 * g + qq >= b) e = 0.f;
+                    sum += e;
+                    t2 = __builtin_fmaf(e, u, t2);
+                    sc[r][t][qq] = e;
+                }
+            }
+            sum = lanegroup_sum(sum);
+            t2 = lanegroup_sum(t2);
+            inv[r] = 1.0f / sum;
+            // c_L = sum_i R log R = sum_i R (Z - max) - log(sum)   (natural-log units)
+            if (g == 0 && jr[r] < b)
+                p.cL[bh * N + (int64_t)k * b + jr[r]] = kLn2 * (t2 * inv[r] - __builtin_amdgcn_logf(sum));
+            pf[r].pack(sc[r]);  // unnormalised exp2 values; the row sum is divided out below
+        }
+        f32x4 out[RT][D / 16];
 #pragma unroll
         for (int vt = 0; vt < D / 16; ++vt) {
             f32x4 acc[RT];
-            gemm_aggregate_rt<T, NT, RT>(Vs, LDK, 16 * vt, pf, acc, lane);
+            gemm_aggregate_rt<T, NT, RT>(Ks, LDK, 16 * vt, pf, acc, lane);
 #pragma unroll
             for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
         }
 #pragma unroll
+        for (int r = 0; r < RT; ++r)  // alpha_L[j][k] (j-major)
+            store_row<T, D>(jr[r] < b ? p.aL + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r], lane);
+        if constexpr (FINAL) {
+#pragma unroll
+            for (int vt = 0; vt < D / 16; ++vt) {
+                f32x4 acc[RT];
+                gemm_aggregate_rt<T, NT, RT>(Vs, LDK, 16 * vt, pf, acc, lane);
+#pragma unroll
+                for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
+            }
+#pragma unroll
+            for (int r = 0; r < RT; ++r)
+                store_row<T, D>(jr[r] < b ? p.Y + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r],
+                                lane);
+        }
+    }
+};
+
+// ---------------------------------------------------------------------------------------
+// L half-step (not the last) for (head bh, residue class j).  NM = m rounded
+// up to 16.  Wave w first owns RT tiles of 16 query rows l (scores and the
+// softmax over k), then, after the probabilities have gone through LDS, RT
+// tiles of 16 key-block columns k (c_R and alpha_R).
+// ---------------------------------------------------------------------------------------
+template <typename T, int NM, int D, bool RAGGED> struct LHalf {
+    static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
+    static constexpr int LDQ = Ld<T, D>::row, LDP = Ld<T, NM>::row;
+    static constexpr int A_ELEMS = NM * LDQ, P_ELEMS = NM * LDP;
+    static constexpr int AP_ELEMS = A_ELEMS > P_ELEMS ? A_ELEMS : P_ELEMS;
+    static constexpr int LDS_BYTES = (NM * LDQ + AP_ELEMS) * (int)sizeof(T) + NM * 4;
+
+    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, char *lds, int tid,
+                               int nthreads)
+    {
+        T *Qs = reinterpret_cast<T *>(lds);
+        T *APs = Qs + NM * LDQ;  // alpha_L, then P
+        float *cLs = reinterpret_cast<float *>(APs + AP_ELEMS);
+        const int m = hd.m, b = hd.b;
+        const int64_t N = (int64_t)m * b;
+        const int64_t hoff = bh * N * D;
+        const int lane = tid & 63, wave = tid >> 6;
+        const int g = lane >> 4, c16 = lane & 15;
+        const bool active = wave < W;
+
+        const T *qh = p.q + hoff;
+        const T *al = p.aL + hoff + (int64_t)j * m * D;
+        load_tile<T, NM, D, LDQ>([=](int l) { return qh + ((int64_t)l * b + j) * D; }, m, Qs, tid, nthreads);
+        load_tile<T, NM, D, LDQ>([=](int kk) { return al + (int64_t)kk * D; }, m, APs, tid, nthreads);
+        for (int kk = tid; kk < NM; kk += nthreads)
+            cLs[kk] = kk < m ? p.cL[bh * N + (int64_t)kk * b + j] * kLog2e : 0.f;
+        __syncthreads();
+
+        // scores and softmax over k for the query rows of this wave
+        int lr[RT];
+        float inv[RT];
+        f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
+        if (active) {
+            RowFrags<T, D> bf[RT];
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+                lr[r] = (wave * RT + r) * 16 + c16;
+#pragma unroll
+                for (int c = 0; c < D / Mma<T>::KC; ++c)
+                    bf[r].f[c] = *reinterpret_cast<const typename Mma<T>::frag *>(Qs + lr[r] * LDQ + c * Mma<T>::KC +
+                                                                                  g * Mma<T>::KPL);
+            }
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                f32x4 acc[RT];
+                gemm_scores_rt<T, D, RT>(APs + (16 * t + c16) * LDQ, bf, acc, g);
+                const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
+#pragma unroll
+                for (int r = 0; r < RT; ++r) {
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
+                }
+            }
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+                const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
+                float sum = 0.f;
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq) {
+                        float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
+                        if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
+                        sum += e;
+                        sc[r][t][qq] = e;
+                    }
+                }
+                sum = lanegroup_sum(sum);
+                inv[r] = (lr[r] < m) ? 1.0f / sum : 0.f;  // padded query rows carry no weight
+            }
+        }
+        __syncthreads();  // every wave is done reading alpha_L
+
+        // P[l][k] (row-major, k contiguous) into the alpha_L space
+        using PT = typename std::conditional<std::is_same<T, float>::value, float, T>::type;
+        PT *Ps = reinterpret_cast<PT *>(APs);
+        if (active) {
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) store4<PT>(Ps + lr[r] * LDP + 16 * t + 4 * g, sc[r][t] * inv[r]);
+            }
+        }
+        __syncthreads();
+        if (!active) return;
+
+        // wave w: key-block columns k in tiles wave*RT + r
+        int kr[RT];
+        ProbFrags<T, NT> pf[RT];  // B operand: P[l-slots][k]
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            kr[r] = (wave * RT + r) * 16 + c16;
+            pf[r].gather(Ps, LDP, (wave * RT + r) * 16, lane);
+            const f32x4 cs = gemm_colsum<T, NT>(pf[r]);  // c_R[k][j] = sum_l L[j][k][l]
+            if (g == 0 && kr[r] < m) p.cR[bh * N + (int64_t)j * m + kr[r]] = cs[0];
+        }
+        f32x4 out[RT][D / 16];
+#pragma unroll
+        for (int vt = 0; vt < D / 16; ++vt) {
+            f32x4 acc[RT];
+            gemm_aggregate_rt<T, NT, RT>(Qs, LDQ, 16 * vt, pf, acc, lane);
+#pragma unroll
+            for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
+        }
+#pragma unroll
+        for (int r = 0; r < RT; ++r)  // alpha_R[k][j] (k-major)
+            store_row<T, D>(kr[r] < m ? p.aR + hoff + ((int64_t)kr[r] * b + j) * D : nullptr, out[r], 1.0f, lane);
+    }
+};
+
+// ---------------------------------------------------------------------------------------
+// Last L half-step fused with the second Monarch product and the store of O
+// for (head bh, class j); each wave owns RT tiles of 16 query rows l.
+// ---------------------------------------------------------------------------------------
+template <typename T, int NM, int D, bool RAGGED> struct Apply {
+    static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
+    static constexpr int LDK = Ld<T, D>::row;
+    static constexpr int LDS_BYTES = 2 * NM * LDK * (int)sizeof(T) + NM * 4;
+
+    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, char *lds, int tid,
+                               int nthreads)
+    {
+        T *As = reinterpret_cast<T *>(lds);
+        T *Ys = As + NM * LDK;
+        float *cLs = reinterpret_cast<float *>(Ys + NM * LDK);
+        const int m = hd.m, b = hd.b;
+        const int64_t N = (int64_t)m * b;
+        const int64_t hoff = bh * N * D;
+        const int lane = tid & 63, wave = tid >> 6;
+        const int g = lane >> 4, c16 = lane & 15;
+        const bool active = wave < W;
+
+        const T *al = p.aL + hoff + (int64_t)j * m * D;
+        const T *yj = p.Y + hoff + (int64_t)j * m * D;
+        load_tile<T, NM, D, LDK>([=](int kk) { return al + (int64_t)kk * D; }, m, As, tid, nthreads);
+        load_tile<T, NM, D, LDK>([=](int kk) { return yj + (int64_t)kk * D; }, m, Ys, tid, nthreads);
+        for (int kk = tid; kk < NM; kk += nthreads)
+            cLs[kk] = kk < m ? p.cL[bh * N + (int64_t)kk * b + j] * kLog2e : 0.f;
+
+        int lr[RT];
+        RowFrags<T, D> bf[RT];
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            lr[r] = (wave * RT + r) * 16 + c16;
+            bf[r].load(active && lr[r] < m ? p.q + hoff + ((int64_t)lr[r] * b + j) * D : nullptr, g);  // Qbar[j][l]
+        }
+        __syncthreads();
+        if (!active) return;
+
+        f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            f32x4 acc[RT];
+            gemm_scores_rt<T, D, RT>(As + (16 * t + c16) * LDK, bf, acc, g);
+            const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
+            }
+        }
+        ProbFrags<T, NT> pf[RT];
+        float inv[RT];
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
+            float sum = 0.f;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
+                    if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
+                    sum += e;
+                    sc[r][t][qq] = e;
+                }
+            }
+            inv[r] = 1.0f / lanegroup_sum(sum);
+            pf[r].pack(sc[r]);  // unnormalised; the row sum is divided out of O below
+        }
+        f32x4 o[RT][D / 16];
+#pragma unroll
+        for (int vt = 0; vt < D / 16; ++vt) {
+            f32x4 acc[RT];
+            gemm_aggregate_rt<T, NT, RT>(Ys, LDK, 16 * vt, pf, acc, lane);
+#pragma unroll
+            for (int r = 0; r < RT; ++r) o[r][vt] = acc[r];
+        }
+#pragma unroll
         for (int r = 0; r < RT; ++r)
-            store_row<T, D>(jr[r] < b ? Y + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r], lane);
+            store_row<T, D>(lr[r] < m ? p.out + hoff + ((int64_t)lr[r] * b + j) * D : nullptr, o[r], inv[r], lane);
     }
+};
+
+// ---------------------------------------------------------------------------------------
+// One launch per half-step: one workgroup per unit.
+// ---------------------------------------------------------------------------------------
+template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED>
+__global__ __launch_bounds__(64 * Split<NB / 16>::W) void r_half_step(Bufs<T> p, HeadDims hd)
+{
+    using U = RHalf<T, NB, D, FIRST, FINAL, RAGGED>;
+    __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
+    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
+    U::run(p, hd, unit / hd.m, (int)(unit % hd.m), lds, threadIdx.x, 64 * U::W);
+}
+
+template <typename T, int NM, int D, bool RAGGED>
+__global__ __launch_bounds__(64 * Split<NM / 16>::W) void l_half_step(Bufs<T> p, HeadDims hd)
+{
+    using U = LHalf<T, NM, D, RAGGED>;
+    __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
+    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
+    U::run(p, hd, unit / hd.b, (int)(unit % hd.b), lds, threadIdx.x, 64 * U::W);
+}
+
+template <typename T, int NM, int D, bool RAGGED>
+__global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> p, HeadDims hd)
+{
+    using U = Apply<T, NM, D, RAGGED>;
+    __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
+    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
+    U::run(p, hd, unit / hd.b, (int)(unit % hd.b), lds, threadIdx.x, 64 * U::W);
 }
 
 // ---------------------------------------------------------------------------------------
-// L half-step (not the last): one workgroup per (head, residue class j).
-// NM = m rounded up to 16.  Wave w first owns RT tiles of 16 query rows l
-// (scores and the softmax over k), then, after the probabilities have gone
-// through LDS, RT tiles of 16 key-block columns k (c_R and alpha_R).
+// The whole forward pass in one cooperative launch.  Each head is processed by
+// the workgroups of a single XCD (read from the hardware XCC_ID register), so
+// every state a half-step writes is read back by the next half-step from that
+// XCD's L2.  The half-steps of a head are separated by a barrier among the
+// workgroups of its XCD: each thread waits until its stores have reached the
+// L2 (the vector L1 is write-through), then one thread per workgroup adds 1
+// to the XCD's counter and waits until it reaches the phase target.
+// Every state of iteration t has its own copy (`state_stride` elements,
+// `c_stride` floats apart), so within a launch no address is ever read before
+// its last write: a CU's L1 cannot hold a stale line of a state.
+// All waits are bounded: on a time-out the workgroup records the failure in
+// a host-visible flag and returns, so the grid always drains.
 // ---------------------------------------------------------------------------------------
-template <typename T, int NM, int D, bool RAGGED>
-__global__ __launch_bounds__(64 * Split<NM / 16>::W) void l_half_step(
-    const T *__restrict__ q, const T *__restrict__ aL, const float *__restrict__ cL,
-    T *__restrict__ aR, float *__restrict__ cR, HeadDims hd)
+struct SyncState {
+    unsigned *counters;    // [x]: workgroups on XCD x; [8]: arrivals; [16 + 16 x]: barrier of XCD x
+    int *error;            // host-visible flag, set to 1 on a barrier time-out
+    int64_t state_stride;  // elements between the per-iteration copies of alpha_R / alpha_L
+    int64_t c_stride;      // floats between the per-iteration copies of c_R / c_L
+    unsigned zero;         // 0 (see xcd_barrier)
+};
+
+constexpr unsigned kSpinLimit = 1u << 20;
+
+__device__ inline unsigned read_xcc_id()
 {
-    constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
-    constexpr int LDQ = Ld<T, D>::row, LDP = Ld<T, NM>::row;
-    constexpr int A_ELEMS = NM * LDQ, P_ELEMS = NM * LDP;
-    __shared__ __attribute__((aligned(16))) T Qs[NM * LDQ];
-    __shared__ __attribute__((aligned(16))) T APs[A_ELEMS > P_ELEMS ? A_ELEMS : P_ELEMS];  // alpha_L, then P
-    __shared__ __attribute__((aligned(16))) float cLs[NM];
-
-    const int m = hd.m, b = hd.b;
-    const int64_t N = (int64_t)m * b;
-    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
-    const int j = unit % b;
-    const int64_t bh = unit / b;
-    const int64_t hoff = bh * N * D;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int g = lane >> 4, c16 = lane & 15;
-
-    const T *qh = q + hoff;
-    const T *al = aL + hoff + (int64_t)j * m * D;
-    load_tile<T, NM, D, LDQ>([=](int l) { return qh + ((int64_t)l * b + j) * D; }, m, Qs, tid, 64 * W);
-    load_tile<T, NM, D, LDQ>([=](int kk) { return al + (int64_t)kk * D; }, m, APs, tid, 64 * W);
-    for (int kk = tid; kk < NM; kk += 64 * W) cLs[kk] = kk < m ? cL[bh * N + (int64_t)kk * b + j] * kLog2e : 0.f;
-    __syncthreads();
-
-    // scores and softmax over k for the query rows of this wave
-    int lr[RT];
-    RowFrags<T, D> bf[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-        lr[r] = (wave * RT + r) * 16 + c16;
-#pragma unroll
-        for (int c = 0; c < D / Mma<T>::KC; ++c)
-            bf[r].f[c] = *reinterpret_cast<const typename Mma<T>::frag *>(Qs + lr[r] * LDQ + c * Mma<T>::KC +
-                                                                          g * Mma<T>::KPL);
-    }
-    f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        f32x4 acc[RT];
-        gemm_scores_rt<T, D, RT>(APs + (16 * t + c16) * LDQ, bf, acc, g);
-        const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
-#pragma unroll
-        for (int r = 0; r < RT; ++r) {
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
-        }
-    }
-    float inv[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-        const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
-        float sum = 0.f;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-                float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
-                if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
-                sum += e;
-                sc[r][t][qq] = e;
-            }
-        }
-        sum = lanegroup_sum(sum);
-        inv[r] = (lr[r] < m) ? 1.0f / sum : 0.f;  // padded query rows carry no weight
-    }
-    __syncthreads();  // every wave is done reading alpha_L
-
-    // P[l][k] (row-major, k contiguous) into the alpha_L space
-    using PT = typename std::conditional<std::is_same<T, float>::value, float, T>::type;
-    PT *Ps = reinterpret_cast<PT *>(APs);
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-#pragma unroll
-        for (int t = 0; t < NT; ++t) store4<PT>(Ps + lr[r] * LDP + 16 * t + 4 * g, sc[r][t] * inv[r]);
-    }
-    __syncthreads();
-
-    // wave w: key-block columns k in tiles wave*RT + r
-    int kr[RT];
-    ProbFrags<T, NT> pf[RT];  // B operand: P[l-slots][k]
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-        kr[r] = (wave * RT + r) * 16 + c16;
-        pf[r].gather(Ps, LDP, (wave * RT + r) * 16, lane);
-        const f32x4 cs = gemm_colsum<T, NT>(pf[r]);  // c_R[k][j] = sum_l L[j][k][l]
-        if (g == 0 && kr[r] < m) cR[bh * N + (int64_t)j * m + kr[r]] = cs[0];
-    }
-    f32x4 out[RT][D / 16];
-#pragma unroll
-    for (int vt = 0; vt < D / 16; ++vt) {
-        f32x4 acc[RT];
-        gemm_aggregate_rt<T, NT, RT>(Qs, LDQ, 16 * vt, pf, acc, lane);
-#pragma unroll
-        for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
-    }
-#pragma unroll
-    for (int r = 0; r < RT; ++r)  // alpha_R[k][j] (k-major)
-        store_row<T, D>(kr[r] < m ? aR + hoff + ((int64_t)kr[r] * b + j) * D : nullptr, out[r], 1.0f, lane);
+    unsigned x;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+    return x & 7u;
 }
 
-// ---------------------------------------------------------------------------------------
-// Last L half-step fused with the second Monarch product and the store of O:
-// one workgroup per (head, j); each wave owns RT tiles of 16 query rows l.
-// ---------------------------------------------------------------------------------------
-template <typename T, int NM, int D, bool RAGGED>
-__global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(
-    const T *__restrict__ q, const T *__restrict__ aL, const float *__restrict__ cL,
-    const T *__restrict__ Y, T *__restrict__ out, HeadDims hd)
+// Thread 0 only: wait (bounded) until *ctr >= target.
+template <int ORDER = __ATOMIC_RELAXED>
+__device__ inline bool spin_until(unsigned *ctr, unsigned target)
 {
-    constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
-    constexpr int LDK = Ld<T, D>::row;
-    __shared__ __attribute__((aligned(16))) T As[NM * LDK];
-    __shared__ __attribute__((aligned(16))) T Ys[NM * LDK];
-    __shared__ __attribute__((aligned(16))) float cLs[NM];
+    unsigned it = 0;
+    while (__hip_atomic_load(ctr, ORDER, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        if (++it > kSpinLimit) return false;
+        __builtin_amdgcn_s_sleep(2);
+    }
+    return true;
+}
 
-    const int m = hd.m, b = hd.b;
-    const int64_t N = (int64_t)m * b;
-    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
-    const int j = unit % b;
-    const int64_t bh = unit / b;
-    const int64_t hoff = bh * N * D;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int g = lane >> 4, c16 = lane & 15;
-
-    const T *al = aL + hoff + (int64_t)j * m * D;
-    const T *yj = Y + hoff + (int64_t)j * m * D;
-    load_tile<T, NM, D, LDK>([=](int kk) { return al + (int64_t)kk * D; }, m, As, tid, 64 * W);
-    load_tile<T, NM, D, LDK>([=](int kk) { return yj + (int64_t)kk * D; }, m, Ys, tid, 64 * W);
-    for (int kk = tid; kk < NM; kk += 64 * W) cLs[kk] = kk < m ? cL[bh * N + (int64_t)kk * b + j] * kLog2e : 0.f;
-
-    int lr[RT];
-    RowFrags<T, D> bf[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-        lr[r] = (wave * RT + r) * 16 + c16;
-        bf[r].load(lr[r] < m ? q + hoff + ((int64_t)lr[r] * b + j) * D : nullptr, g);  // Qbar[j][l]
+// The poll is an atomic add of `zero` (0 at run time, opaque to the compiler,
+// which would otherwise turn an add of 0 into a load that the CU's L1 may
+// serve): it executes where the increments execute and returns the current
+// count.
+__device__ inline bool xcd_barrier(unsigned *ctr, unsigned target, unsigned zero, int *error, int *shared_ok)
+{
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        unsigned it = 0;
+        bool ok = true;
+        while (__hip_atomic_fetch_add(ctr, zero, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+            if (++it > kSpinLimit) {
+                ok = false;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        if (!ok) __hip_atomic_store(error, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        *shared_ok = ok;
     }
     __syncthreads();
+    return *shared_ok != 0;
+}
 
-    f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        f32x4 acc[RT];
-        gemm_scores_rt<T, D, RT>(As + (16 * t + c16) * LDK, bf, acc, g);
-        const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
-#pragma unroll
-        for (int r = 0; r < RT; ++r) {
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
+template <int A, int B> struct MaxOf {
+    static constexpr int value = A > B ? A : B;
+};
+
+template <typename T, int NB, int NM, int D, bool RGB, bool RGM> struct Persistent {
+    using R1 = RHalf<T, NB, D, true, false, RGB>;
+    using R1F = RHalf<T, NB, D, true, true, RGB>;
+    using RM = RHalf<T, NB, D, false, false, RGB>;
+    using RF = RHalf<T, NB, D, false, true, RGB>;
+    using LH = LHalf<T, NM, D, RGM>;
+    using AP = Apply<T, NM, D, RGM>;
+    static constexpr int W = MaxOf<R1::W, LH::W>::value;
+    static constexpr int LDS_BYTES = MaxOf<R1F::LDS_BYTES, MaxOf<LH::LDS_BYTES, AP::LDS_BYTES>::value>::value;
+};
+
+template <typename T, int NB, int NM, int D, bool RGB, bool RGM>
+__global__ __launch_bounds__((64 * Persistent<T, NB, NM, D, RGB, RGM>::W)) void monarch_persistent(
+    Bufs<T> p, HeadDims hd, int64_t BH, int T_, SyncState ss)
+{
+    using P = Persistent<T, NB, NM, D, RGB, RGM>;
+    __shared__ __attribute__((aligned(16))) char lds[P::LDS_BYTES];
+    __shared__ unsigned info[10];
+    __shared__ int ok;
+    const int tid = threadIdx.x, nthreads = 64 * P::W;
+    const unsigned xcc = read_xcc_id();
+
+    // registration: rank of this workgroup on its XCD, and workgroups per XCD
+    if (tid == 0) {
+        // the registration add completes (its value is returned) before the arrival add is issued
+        info[0] = __hip_atomic_fetch_add(&ss.counters[xcc], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __hip_atomic_fetch_add(&ss.counters[8], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const bool arrived = spin_until(&ss.counters[8], gridDim.x);
+        if (!arrived) __hip_atomic_store(ss.error, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        for (int x = 0; x < 8; ++x)
+            info[1 + x] = __hip_atomic_load(&ss.counters[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        info[9] = arrived;
+    }
+    __syncthreads();
+    if (!info[9]) return;
+    const unsigned rank = info[0], cnt = info[1 + xcc];
+    unsigned nx = 0, pos = 0;  // XCDs with workgroups, and this XCD's place among them
+    for (unsigned x = 0; x < 8; ++x) {
+        if (info[1 + x]) {
+            if (x < xcc) ++pos;
+            ++nx;
         }
     }
-    ProbFrags<T, NT> pf[RT];
-    float inv[RT];
-#pragma unroll
-    for (int r = 0; r < RT; ++r) {
-        const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
-        float sum = 0.f;
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-                float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
-                if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
-                sum += e;
-                sc[r][t][qq] = e;
-            }
+    unsigned *bar = &ss.counters[16 + 16 * xcc];
+    unsigned phase = 0;
+    const int m = hd.m, b = hd.b;
+    // heads of this XCD: bh = pos + nx * h for h < nheads; every phase covers all of them
+    const int64_t nheads = (int64_t)pos < BH ? (BH - pos + nx - 1) / nx : 0;
+
+    for (int t = 1; t <= T_; ++t) {
+        const bool first = (t == 1), last = (t == T_);
+        // iteration t: R reads alpha_R / c_R copy t-2 and writes alpha_L / c_L copy t-1;
+        // L reads alpha_L / c_L copy t-1 and writes alpha_R / c_R copy t-1.
+        Bufs<T> pt = p;
+        pt.aL += (t - 1) * ss.state_stride;
+        pt.cL += (t - 1) * ss.c_stride;
+        Bufs<T> pr = pt;
+        if (!first) {
+            pr.aR += (t - 2) * ss.state_stride;
+            pr.cR += (t - 2) * ss.c_stride;
         }
-        inv[r] = 1.0f / lanegroup_sum(sum);
-        pf[r].pack(sc[r]);  // unnormalised; the row sum is divided out of O below
+        for (int64_t u = rank; u < nheads * m; u += cnt) {
+            const int64_t bh = pos + nx * (u / m);
+            const int k = (int)(u % m);
+            if (first && last)
+                P::R1F::run(pr, hd, bh, k, lds, tid, nthreads);
+            else if (first)
+                P::R1::run(pr, hd, bh, k, lds, tid, nthreads);
+            else if (last)
+                P::RF::run(pr, hd, bh, k, lds, tid, nthreads);
+            else
+                P::RM::run(pr, hd, bh, k, lds, tid, nthreads);
+            __syncthreads();
+        }
+        if (!xcd_barrier(bar, ++phase * cnt, ss.zero, ss.error, &ok)) return;
+        pt.aR += (t - 1) * ss.state_stride;
+        pt.cR += (t - 1) * ss.c_stride;
+        for (int64_t u = rank; u < nheads * b; u += cnt) {
+            const int64_t bh = pos + nx * (u / b);
+            const int j = (int)(u % b);
+            if (last)
+                P::AP::run(pt, hd, bh, j, lds, tid, nthreads);
+            else
+                P::LH::run(pt, hd, bh, j, lds, tid, nthreads);
+            __syncthreads();
+        }
+        if (!last && !xcd_barrier(bar, ++phase * cnt, ss.zero, ss.error, &ok)) return;
     }
-    f32x4 o[RT][D / 16];
-#pragma unroll
-    for (int vt = 0; vt < D / 16; ++vt) {
-        f32x4 acc[RT];
-        gemm_aggregate_rt<T, NT, RT>(Ys, LDK, 16 * vt, pf, acc, lane);
-#pragma unroll
-        for (int r = 0; r < RT; ++r) o[r][vt] = acc[r];
-    }
-#pragma unroll
-    for (int r = 0; r < RT; ++r)
-        store_row<T, D>(lr[r] < m ? out + hoff + ((int64_t)lr[r] * b + j) * D : nullptr, o[r], inv[r], lane);
 }
 
 }  // namespace ma

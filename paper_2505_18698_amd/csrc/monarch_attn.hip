@@ -1,29 +1,21 @@
-// Host side of the MonarchAttention C ABI (include/monarch_attn.h): argument
-// checks, the per-device workspace, dispatch of the half-step kernels by
-// (dtype, d, padded m, padded b), and optional per-launch HIP-event timing.
-//
-// Launch order for T steps (paper, Implementation paragraph of Sec. 3; R is
-// updated before L in every step):
-//   T == 1 : R(first, final) -> apply
-//   T >= 2 : R(first) -> L -> [R -> L] x (T - 2) -> R(final) -> apply
-// "first" reads alpha_R straight from Q with c_R = 1 (L^(0) = I); "final" also
-// forms Y; apply is the last L half-step fused with O = sum_k L Y.
+// C ABI of the MonarchAttention forward pass (include/monarch_attn.h):
+// argument checks, the per-device workspace, path selection, the
+// host-visible error flag of the single-launch path, and per-launch timing.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <mutex>
 
-#include "ma_kernels.hpp"
-#include "../../include/monarch_attn.h"
+#include "host_common.hpp"
 
-namespace {
+namespace ma_host {
 
 thread_local char g_err[512] = "";
 
-int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 int fail(int code, const char *fmt, ...)
 {
     va_list ap;
@@ -33,7 +25,13 @@ int fail(int code, const char *fmt, ...)
     return code;
 }
 
-int pad16(int64_t x) { return (int)((x + 15) / 16 * 16); }
+Timing g_timing;
+
+}  // namespace ma_host
+
+namespace {
+
+using namespace ma_host;
 
 size_t elem_bytes(int32_t dtype) { return dtype == MA_F32 ? 4 : 2; }
 
@@ -51,164 +49,39 @@ int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t d
     return MA_OK;
 }
 
-size_t workspace_bytes(int64_t BH, int64_t N, int64_t d, int32_t dtype)
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int state_copies(int32_t T) { return T <= kMaxSingleT ? T : 1; }
+
+size_t workspace_bytes(int64_t BH, int64_t N, int64_t d, int32_t T, int32_t dtype)
 {
-    // alpha_R, alpha_L, Y in the element type; c_R, c_L in fp32; 256-byte aligned pieces.
-    const size_t st = ((size_t)BH * N * d * elem_bytes(dtype) + 255) / 256 * 256;
-    const size_t cs = ((size_t)BH * N * sizeof(float) + 255) / 256 * 256;
-    return 3 * st + 2 * cs;
+    // alpha_R, alpha_L (one copy per iteration up to kMaxSingleT) and Y in the
+    // element type; c_R, c_L (likewise) in fp32; the counters of the
+    // single-launch path.
+    const size_t st = align_up((size_t)BH * N * d * elem_bytes(dtype));
+    const size_t cs = align_up((size_t)BH * N * sizeof(float));
+    const size_t c = (size_t)state_copies(T);
+    return (2 * c + 1) * st + 2 * c * cs + align_up(kSyncWords * sizeof(unsigned));
 }
 
-struct Workspace {
-    void *ptr = nullptr;
-    size_t bytes = 0;
+struct Device {
+    void *ws = nullptr;
+    size_t ws_bytes = 0;
+    int *error = nullptr;  // pinned host memory, written by the single-launch kernel
+    int num_cus = 0;
 };
 
 constexpr int kMaxDevices = 64;
-std::mutex g_ws_mutex;
-Workspace g_ws[kMaxDevices];
-
-// ---- per-launch timing ----
-constexpr int kMaxLaunches = 2 * 64 + 2;
-struct Timing {
-    bool enabled = false;
-    bool ready = false;
-    int nlaunch = 0;
-    int kind[kMaxLaunches];
-    hipEvent_t ev[2 * kMaxLaunches];
-    bool created = false;
-};
+std::mutex g_dev_mutex;
+Device g_dev[kMaxDevices];
+std::atomic<int> g_path{kAuto};
 std::mutex g_timing_mutex;
-Timing g_timing;
 
 bool overlaps(const void *a, size_t na, const void *b, size_t nb)
 {
     const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
     return x < y + nb && y < x + na;
-}
-
-struct Launcher {
-    hipStream_t stream;
-    bool timed;
-    int n = 0;
-
-    template <typename F> int run(int kind, F &&launch)
-    {
-        if (timed) {
-            if (n >= kMaxLaunches) return fail(MA_EHIP, "too many launches to time");
-            if (hipEventRecord(g_timing.ev[2 * n], stream) != hipSuccess) return fail(MA_EHIP, "hipEventRecord failed");
-        }
-        launch();
-        if (timed) {
-            g_timing.kind[n] = kind;
-            if (hipEventRecord(g_timing.ev[2 * n + 1], stream) != hipSuccess) return fail(MA_EHIP, "hipEventRecord failed");
-        }
-        ++n;
-        return MA_OK;
-    }
-};
-
-struct Bufs {
-    const void *q, *k, *v;
-    void *out;
-    void *aR, *aL, *Y;
-    float *cR, *cL;
-};
-
-template <typename T, int NB, int D, bool RG>
-int launch_r(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool first, bool final_)
-{
-    constexpr int W = ma::Split<NB / 16>::W;
-    hd.units = BH * hd.m;
-    const dim3 grid((unsigned)hd.units), block(64 * W);
-    const T *q = (const T *)B.q, *k = (const T *)B.k, *v = (const T *)B.v;
-    const T *aR = (const T *)B.aR;
-    T *aL = (T *)B.aL, *Y = (T *)B.Y;
-    const int kind = final_ ? 2 : 0;
-    if (first && final_)
-        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, true, true, RG>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
-    if (first)
-        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, true, false, RG>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
-    if (final_)
-        return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, false, true, RG>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
-    return L.run(kind, [&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, false, false, RG>), grid, block, 0, L.stream, q, k, v, aR, B.cR, aL, B.cL, Y, hd); });
-}
-
-template <typename T, int NM, int D, bool RG>
-int launch_l(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool apply)
-{
-    constexpr int W = ma::Split<NM / 16>::W;
-    hd.units = BH * hd.b;
-    const dim3 grid((unsigned)hd.units), block(64 * W);
-    const T *q = (const T *)B.q;
-    const T *aL = (const T *)B.aL, *Y = (const T *)B.Y;
-    if (apply)
-        return L.run(3, [&] { hipLaunchKernelGGL((ma::monarch_apply<T, NM, D, RG>), grid, block, 0, L.stream, q, aL, B.cL, Y, (T *)B.out, hd); });
-    return L.run(1, [&] { hipLaunchKernelGGL((ma::l_half_step<T, NM, D, RG>), grid, block, 0, L.stream, q, aL, B.cL, (T *)B.aR, B.cR, hd); });
-}
-
-template <typename T, int D, int NB>
-int dispatch_r(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool first, bool final_)
-{
-    if constexpr (std::is_same<T, float>::value && NB * D > 8192) {
-        return fail(MA_EUNSUPPORTED, "fp32 tile too large");
-    } else {
-        return hd.b != NB ? launch_r<T, NB, D, true>(L, B, hd, BH, first, final_)
-                         : launch_r<T, NB, D, false>(L, B, hd, BH, first, final_);
-    }
-}
-
-template <typename T, int D, int NM>
-int dispatch_l(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool apply)
-{
-    if constexpr (std::is_same<T, float>::value && NM * D > 8192) {
-        return fail(MA_EUNSUPPORTED, "fp32 tile too large");
-    } else {
-        return hd.m != NM ? launch_l<T, NM, D, true>(L, B, hd, BH, apply)
-                         : launch_l<T, NM, D, false>(L, B, hd, BH, apply);
-    }
-}
-
-template <typename T, int D>
-int r_step(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool first, bool final_)
-{
-    switch (pad16(hd.b)) {
-    case 16: return dispatch_r<T, D, 16>(L, B, hd, BH, first, final_);
-    case 32: return dispatch_r<T, D, 32>(L, B, hd, BH, first, final_);
-    case 48: return dispatch_r<T, D, 64>(L, B, hd, BH, first, final_);
-    case 64: return dispatch_r<T, D, 64>(L, B, hd, BH, first, final_);
-    default: return dispatch_r<T, D, 128>(L, B, hd, BH, first, final_);
-    }
-}
-
-template <typename T, int D>
-int l_step(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, bool apply)
-{
-    switch (pad16(hd.m)) {
-    case 16: return dispatch_l<T, D, 16>(L, B, hd, BH, apply);
-    case 32: return dispatch_l<T, D, 32>(L, B, hd, BH, apply);
-    case 48: return dispatch_l<T, D, 64>(L, B, hd, BH, apply);
-    case 64: return dispatch_l<T, D, 64>(L, B, hd, BH, apply);
-    default: return dispatch_l<T, D, 128>(L, B, hd, BH, apply);
-    }
-}
-
-template <typename T, int D>
-int run_all(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, int T_)
-{
-    int rc;
-    for (int t = 1; t <= T_; ++t) {
-        const bool first = (t == 1), last = (t == T_);
-        if ((rc = r_step<T, D>(L, B, hd, BH, first, last)) != MA_OK) return rc;
-        if ((rc = l_step<T, D>(L, B, hd, BH, last)) != MA_OK) return rc;
-    }
-    return MA_OK;
-}
-
-template <typename T>
-int run_dtype(Launcher &L, const Bufs &B, ma::HeadDims hd, int64_t BH, int64_t d, int T_)
-{
-    return d == 64 ? run_all<T, 64>(L, B, hd, BH, T_) : run_all<T, 128>(L, B, hd, BH, T_);
 }
 
 }  // namespace
@@ -227,7 +100,7 @@ size_t monarch_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, 
                                     int32_t T, int32_t dtype)
 {
     if (B < 1 || H < 1 || check_shape(N, d, m, b, T, dtype) != MA_OK) return 0;
-    return workspace_bytes(B * H, N, d, dtype);
+    return workspace_bytes(B * H, N, d, T, dtype);
 }
 
 int monarch_attn_release_workspace(void)
@@ -235,13 +108,25 @@ int monarch_attn_release_workspace(void)
     g_err[0] = '\0';
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
-    std::lock_guard<std::mutex> lock(g_ws_mutex);
-    if (g_ws[dev].ptr) {
-        if (hipDeviceSynchronize() != hipSuccess || hipFree(g_ws[dev].ptr) != hipSuccess)
+    std::lock_guard<std::mutex> lock(g_dev_mutex);
+    Device &D = g_dev[dev];
+    if (D.ws) {
+        if (hipDeviceSynchronize() != hipSuccess || hipFree(D.ws) != hipSuccess)
             return fail(MA_EHIP, "freeing the workspace failed");
     }
-    g_ws[dev] = Workspace{};
+    D.ws = nullptr;
+    D.ws_bytes = 0;
     return MA_OK;
+}
+
+int monarch_attn_set_path(int32_t path)
+{
+    g_err[0] = '\0';
+    if (path != kAuto && path != kHalfSteps && path != kSingle) {
+        fail(MA_EINVAL, "unknown path %d", path);
+        return -1;
+    }
+    return g_path.exchange(path);
 }
 
 int monarch_attn_timing_enable(int32_t flag)
@@ -303,42 +188,80 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
 
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
-    const size_t need = workspace_bytes(BH, N, d, dtype);
+    const size_t need = workspace_bytes(BH, N, d, T, dtype);
     void *ws = nullptr;
+    int *error = nullptr;
+    int num_cus = 0;
     {
-        std::lock_guard<std::mutex> lock(g_ws_mutex);
-        Workspace &w = g_ws[dev];
-        if (w.bytes < need) {
-            if (w.ptr) {
+        std::lock_guard<std::mutex> lock(g_dev_mutex);
+        Device &D = g_dev[dev];
+        if (!D.error) {
+            hipDeviceProp_t prop;
+            if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return fail(MA_EHIP, "hipGetDeviceProperties failed");
+            D.num_cus = prop.multiProcessorCount;
+            void *h = nullptr;
+            if (hipHostMalloc(&h, sizeof(int), hipHostMallocDefault) != hipSuccess) {
+                (void)hipGetLastError();
+                return fail(MA_ENOMEM, "hipHostMalloc of the error flag failed");
+            }
+            D.error = (int *)h;
+            *D.error = 0;
+        }
+        if (__atomic_load_n(D.error, __ATOMIC_ACQUIRE) != 0) {
+            __atomic_store_n(D.error, 0, __ATOMIC_RELEASE);
+            return fail(MA_EHIP, "an earlier single-launch call on this device timed out at a barrier; "
+                                 "its output is invalid");
+        }
+        if (D.ws_bytes < need) {
+            if (D.ws) {
                 if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
-                (void)hipFree(w.ptr);
-                w = Workspace{};
+                (void)hipFree(D.ws);
+                D.ws = nullptr;
+                D.ws_bytes = 0;
             }
             void *p = nullptr;
             if (hipMalloc(&p, need) != hipSuccess) {
                 (void)hipGetLastError();
                 return fail(MA_ENOMEM, "hipMalloc of %zu workspace bytes failed", need);
             }
-            w.ptr = p;
-            w.bytes = need;
+            D.ws = p;
+            D.ws_bytes = need;
         }
-        ws = w.ptr;
+        ws = D.ws;
+        error = D.error;
+        num_cus = D.num_cus;
     }
 
-    const size_t st = ((size_t)BH * N * d * elem_bytes(dtype) + 255) / 256 * 256;
-    const size_t cs = ((size_t)BH * N * sizeof(float) + 255) / 256 * 256;
+    const size_t st = align_up((size_t)BH * N * d * elem_bytes(dtype));
+    const size_t cs = align_up((size_t)BH * N * sizeof(float));
+    const int copies = state_copies(T);
     char *base = (char *)ws;
-    Bufs bufs{q, k, v, out, base, base + st, base + 2 * st, (float *)(base + 3 * st), (float *)(base + 3 * st + cs)};
-    ma::HeadDims hd{(int)m, (int)b, (float)(1.4426950408889634 / std::sqrt((double)d)), 0};
+    char *cbase = base + (2 * copies + 1) * st;
+    CallBufs bufs{q,
+                  k,
+                  v,
+                  out,
+                  base,                                   // alpha_R copies
+                  base + copies * st,                     // alpha_L copies
+                  base + 2 * copies * st,                 // Y
+                  (float *)cbase,                         // c_R copies
+                  (float *)(cbase + copies * cs),         // c_L copies
+                  (unsigned *)(cbase + 2 * copies * cs),  // counters
+                  error,
+                  copies,
+                  (int64_t)(st / elem_bytes(dtype)),
+                  (int64_t)(cs / sizeof(float))};
+    CallDims dims{BH, (int)m, (int)b, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
 
     std::unique_lock<std::mutex> tlock(g_timing_mutex);
     Launcher L{(hipStream_t)stream, g_timing.enabled};
     if (!L.timed) tlock.unlock();
     (void)hipGetLastError();  // clear a stale error so the check below is ours
+    const int path = g_path.load();
     switch (dtype) {
-    case MA_F32: rc = run_dtype<float>(L, bufs, hd, BH, d, T); break;
-    case MA_BF16: rc = run_dtype<__bf16>(L, bufs, hd, BH, d, T); break;
-    default: rc = run_dtype<_Float16>(L, bufs, hd, BH, d, T); break;
+    case MA_F32: rc = run_call<float>(L, bufs, dims, path); break;
+    case MA_BF16: rc = run_call<__bf16>(L, bufs, dims, path); break;
+    default: rc = run_call<_Float16>(L, bufs, dims, path); break;
     }
     if (L.timed) {
         g_timing.nlaunch = L.n;

@@ -90,7 +90,11 @@ def test_workspace_bytes_formula():
     got = ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 2, 1)
     state = B * H * N * d * 2
     cvec = B * H * N * 4
-    assert got == 3 * state + 2 * cvec
+    counters = 768  # synchronisation words of the single-launch path, 256-byte aligned
+    T = 2           # one copy of alpha_R, alpha_L, c_R, c_L per iteration, one Y
+    assert got == (2 * T + 1) * state + 2 * T * cvec + counters
+    big_T = ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 20, 1)
+    assert big_T == 3 * state + 2 * cvec + counters
     assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 127, 2, 1) == 0
 
 
@@ -99,3 +103,12 @@ def test_timing_read_without_a_timed_call_fails_cleanly():
 
     with pytest.raises(ma.MonarchAttnError):
         ma.monarch_attn_timing_read()
+
+
+def test_set_path_rejects_unknown_values_and_returns_previous():
+    import paper_2505_18698_amd as ma
+
+    prev = ma.monarch_attn_set_path(ma.PATH_HALF_STEPS)
+    assert ma.monarch_attn_set_path(prev) == ma.PATH_HALF_STEPS
+    with pytest.raises(ma.MonarchAttnError):
+        ma.monarch_attn_set_path(7)

@@ -17,13 +17,33 @@ TOL = {"f32": 1e-5, "bf16": 2e-2, "f16": 2e-2}
 
 
 @pytest.fixture(scope="module")
-def ma():
+def lib():
     import torch
 
     assert torch.cuda.is_available(), "no GPU visible"
     import paper_2505_18698_amd as ma
 
     return ma
+
+
+def _tile(n):
+    p = -(-n // 16) * 16
+    return 16 if p <= 16 else 32 if p <= 32 else 64 if p <= 64 else 128
+
+
+# Every parity test runs on both execution paths: one launch per half-step,
+# and the single cooperative launch with XCD-local state exchange.
+@pytest.fixture(params=["half_steps", "single"])
+def ma(lib, request):
+    path = lib.PATH_HALF_STEPS if request.param == "half_steps" else lib.PATH_SINGLE
+    prev = lib.monarch_attn_set_path(path)
+    lib.path_name = request.param
+    yield lib
+    lib.monarch_attn_set_path(prev)
+
+
+def _single_applies(m, b):
+    return _tile(m) == _tile(b)
 
 
 def _torch_dtype(dtype):
@@ -35,6 +55,8 @@ def _torch_dtype(dtype):
 def gpu_run(ma, q, k, v, m, b, T, dtype):
     import torch
 
+    if ma.path_name == "single" and not _single_applies(m, b):
+        pytest.skip("the single-launch path needs m and b in one 16-row tile class")
     td = _torch_dtype(dtype)
     dq = torch.from_numpy(q).to(td).cuda()
     dk = torch.from_numpy(k).to(td).cuda()
@@ -173,3 +195,60 @@ def test_rejected_call_leaves_out_untouched(ma):
         ma.monarch_attn_fwd(q, q.clone(), q.clone(), out, 16, 15, 1)
     torch.cuda.synchronize()
     assert bool((out == 3.0).all())
+
+
+def test_single_path_unsupported_shape_is_rejected(lib):
+    """m and b in different tile classes: the forced single launch refuses
+    (nothing launched), the automatic path falls back to the half-steps."""
+    import torch
+
+    m, b = 8, 40
+    q, k, v = si.random_qkv(1, 1, m * b, 64, "bf16", seed=11)
+    dq, dk, dv = (torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (q, k, v))
+    out = torch.full_like(dq, 3.0)
+    prev = lib.monarch_attn_set_path(lib.PATH_SINGLE)
+    try:
+        with pytest.raises(lib.MonarchAttnError) as exc:
+            lib.monarch_attn_fwd(dq, dk, dv, out, m, b, 2)
+        assert exc.value.status == lib.MA_EUNSUPPORTED
+        torch.cuda.synchronize()
+        assert bool((out == 3.0).all())
+        lib.monarch_attn_set_path(lib.PATH_AUTO)
+        lib.monarch_attn_fwd(dq, dk, dv, out, m, b, 2)
+        torch.cuda.synchronize()
+    finally:
+        lib.monarch_attn_set_path(prev)
+    ref = oracle.monarch_attention(q, k, v, m, b, 2)
+    check(out.double().cpu().numpy(), ref, "bf16", "auto fallback m8 b40")
+
+
+@pytest.mark.parametrize("name", ["speed_n16384", "speed_n4096", "roberta_n1024"])
+def test_paths_agree_bitwise_without_stale_state(lib, name):
+    """Both paths run the same unit code.  The workspace is first filled from
+    other inputs (A); the single launch on inputs B must then reproduce the
+    half-step result on B bit for bit, twice: a read of a state before its
+    write (a stale value left by A) would show up as a difference."""
+    import torch
+
+    w = si.WORKLOADS[name].with_(T=2)
+    A = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in si.make_qkv(w, seed=1)[:3]]
+    B = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in si.make_qkv(w, seed=2)[:3]]
+
+    def run(t, path):
+        lib.monarch_attn_set_path(path)
+        out = torch.empty_like(t[0])
+        lib.monarch_attn_fwd(t[0], t[1], t[2], out, w.m, w.b, w.T)
+        torch.cuda.synchronize()
+        return out.cpu()
+
+    prev = lib.monarch_attn_set_path(lib.PATH_HALF_STEPS)
+    try:
+        ref = run(B, lib.PATH_HALF_STEPS)
+        run(A, lib.PATH_HALF_STEPS)
+        s1 = run(B, lib.PATH_SINGLE)
+        run(A, lib.PATH_SINGLE)
+        s2 = run(B, lib.PATH_SINGLE)
+    finally:
+        lib.monarch_attn_set_path(prev)
+    assert torch.equal(s1, ref)
+    assert torch.equal(s2, ref)
