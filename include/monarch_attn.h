@@ -67,11 +67,11 @@ typedef enum {
  *
  * Asynchronous on `stream`: returns after enqueueing, with no host
  * synchronisation.  Arguments are checked before any HIP call; on MA_EINVAL or
- * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  The library
- * keeps one device workspace per device ((2c + 1) N d elements plus 2c N
- * floats per head, c = T for T <= 8 and c = 1 above, plus a few counters),
- * grown with hipMalloc on the first call that needs more; calls on different
- * streams of one device must not overlap (they share it).  After
+ * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  Path 1 (see
+ * monarch_attn_set_path) uses one device workspace per device (3 N d
+ * elements plus 2 N floats per head), grown with hipMalloc on the first call
+ * that needs more; calls on different streams of one device must not overlap
+ * (they share it).  After
  * the launches hipGetLastError is checked (MA_EHIP).  The message of the last
  * failure on the calling thread is returned by monarch_attn_last_error().
  */
@@ -98,19 +98,16 @@ int monarch_attn_release_workspace(void);
 /*
  * Execution path of monarch_attn_fwd (process-wide; returns the previous
  * value, or -1 on an unknown value):
- *   0  automatic (default): one launch per half-step;
+ *   0  automatic (default): path 2 where it applies, else path 1;
  *   1  one launch per half-step (the state form of the paper's
- *      Implementation paragraph, states crossing kernels through memory);
- *   2  single launch only: one cooperative kernel runs every half-step of a
- *      head on the workgroups of one XCD, exchanging the states through that
- *      XCD's L2 between in-kernel barriers; monarch_attn_fwd returns
- *      MA_EUNSUPPORTED where it does not apply (m and b in different 16-row
- *      tile classes, T > 8, or no cooperative launch).  Measured slower than
- *      path 1 at every shape tried, so only taken on request.
- * Both paths compute the same operation.  A barrier of the single-launch
- * kernel that does not complete within its bounded wait makes the kernel
- * return early; the next monarch_attn_fwd on that device then reports
- * MA_EHIP.
+ *      Implementation paragraph, the states crossing launches through the
+ *      workspace);
+ *   2  one workgroup per (batch, head) running every half-step with Q, K and
+ *      all states in LDS (the fully fused one-head-per-block kernel for short
+ *      sequences, Sec. 4, paragraph "Benchmarking"): bf16 or fp16, d = 64,
+ *      m <= 16 and b <= 16; any other shape returns MA_EUNSUPPORTED.  Uses
+ *      no workspace.
+ * Both paths compute the same operation with the same per-unit arithmetic.
  */
 int monarch_attn_set_path(int32_t path);
 
@@ -122,7 +119,7 @@ int monarch_attn_set_path(int32_t path);
  * that call, the duration in milliseconds to ms[i] and the kernel kind to
  * kind[i] (0 R half-step, 1 L half-step, 2 last R half-step with Y,
  * 3 last L half-step with the Monarch product and the store of O,
- * 4 the single-launch kernel); it returns the number of launches of that
+ * 4 the one-workgroup-per-head kernel); it returns the number of launches of that
  * call, or -1 on error.
  */
 int monarch_attn_timing_enable(int32_t flag);

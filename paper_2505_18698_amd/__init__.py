@@ -22,9 +22,10 @@ try:
         MA_OK,
         PATH_AUTO,
         PATH_HALF_STEPS,
-        PATH_SINGLE,
+        PATH_FUSED,
         MonarchAttnError,
         dtype_code,
+        fused_applies,
         monarch_attention,
         monarch_attn_check,
         monarch_attn_fwd,

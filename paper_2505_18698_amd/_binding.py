@@ -15,8 +15,8 @@ MA_F32, MA_BF16, MA_F16 = 0, 1, 2
 MA_OK, MA_EINVAL, MA_EUNSUPPORTED, MA_EHIP, MA_ENOMEM = 0, 1, 2, 3, 4
 STATUS_NAMES = {0: "MA_OK", 1: "MA_EINVAL", 2: "MA_EUNSUPPORTED", 3: "MA_EHIP", 4: "MA_ENOMEM"}
 KIND_NAMES = {0: "r_half_step", 1: "l_half_step", 2: "r_half_step_final", 3: "monarch_apply",
-              4: "monarch_persistent"}
-PATH_AUTO, PATH_HALF_STEPS, PATH_SINGLE = 0, 1, 2
+              4: "monarch_fused_head"}
+PATH_AUTO, PATH_HALF_STEPS, PATH_FUSED = 0, 1, 2
 
 # Every symbol declared in include/monarch_attn.h.
 EXPORTS = (
@@ -128,6 +128,11 @@ def monarch_attn_check(N: int, d: int, m: int, b: int, T: int, dtype: int) -> in
     return LIB.monarch_attn_check(N, d, m, b, T, dtype)
 
 
+def fused_applies(d: int, m: int, b: int, dtype: int) -> bool:
+    """Whether the one-workgroup-per-head kernel covers this shape (PATH_AUTO takes it then)."""
+    return dtype in (MA_BF16, MA_F16) and d == 64 and m <= 16 and b <= 16
+
+
 def monarch_attn_workspace_bytes(B, H, N, d, m, b, T, dtype) -> int:
     return int(LIB.monarch_attn_workspace_bytes(B, H, N, d, m, b, T, dtype))
 
@@ -137,7 +142,7 @@ def monarch_attn_release_workspace() -> None:
 
 
 def monarch_attn_set_path(path: int) -> int:
-    """Select the execution path (PATH_AUTO, PATH_HALF_STEPS, PATH_SINGLE); returns the previous one."""
+    """Select the execution path (PATH_AUTO, PATH_HALF_STEPS, PATH_FUSED); returns the previous one."""
     prev = LIB.monarch_attn_set_path(path)
     if prev < 0:
         raise MonarchAttnError(MA_EINVAL, monarch_attn_last_error())

@@ -7,7 +7,8 @@
 //   T >= 2 : R(first) -> L -> [R -> L] x (T - 2) -> R(final) -> apply
 // "first" reads alpha_R straight from Q with c_R = 1 (L^(0) = I); "final" also
 // forms Y; apply is the last L half-step fused with O = sum_k L Y.
-// The single-launch path runs the same sequence inside monarch_persistent.
+// For small heads monarch_fused_head runs the same sequence in one workgroup
+// per head, with the states in LDS.
 #pragma once
 
 #include <type_traits>
@@ -121,86 +122,42 @@ int run_half_steps(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, 
     return MA_OK;
 }
 
-// ---- single launch ----
-// Returns MA_EUNSUPPORTED (nothing enqueued) when the cooperative launch is
-// not possible, so that the caller can fall back to the half-step launches.
-template <typename T, int NT, int D, bool RGB, bool RGM>
-int launch_persistent(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
+// ---- one workgroup per head ----
+template <typename T, bool RGB, bool RGM> int launch_fused(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
 {
-    using P = ma::Persistent<T, NT, NT, D, RGB, RGM>;
-    auto kern = ma::monarch_persistent<T, NT, NT, D, RGB, RGM>;
-    static int per_cu = -1;  // co-resident workgroups per CU, queried once
-    if (per_cu < 0) {
-        int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, 64 * P::W, 0) != hipSuccess) {
-            (void)hipGetLastError();
-            nb = 0;
-        }
-        per_cu = nb;
-    }
-    if (per_cu < 1 || c.num_cus < 1) return fail(MA_EUNSUPPORTED, "single launch: no co-resident workgroups");
-    // no more workgroups per XCD than the units of one phase on that XCD
-    const int64_t heads_per_xcd = (c.BH + 7) / 8;
-    const int64_t units = heads_per_xcd * (hd.m > hd.b ? hd.m : hd.b);
-    const int64_t cap = (int64_t)per_cu * c.num_cus;
-    const unsigned grid = (unsigned)(units * 8 < cap ? units * 8 : cap);
-    ma::Bufs<T> p = typed<T>(B);
-    int64_t BH = c.BH;
-    int T_ = c.T;
-    ma::SyncState ss{B.sync, B.error, B.state_stride, B.c_stride, 0u};
-    void *args[] = {&p, &hd, &BH, &T_, &ss};
-    return L.run(kPersistent, [&]() -> int {
-        if (hipMemsetAsync(B.sync, 0, kSyncWords * sizeof(unsigned), L.stream) != hipSuccess)
-            return fail(MA_EHIP, "hipMemsetAsync of the synchronisation counters failed");
-        const hipError_t e = hipLaunchCooperativeKernel((const void *)kern, dim3(grid), dim3(64 * P::W), args, 0, L.stream);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();
-            return fail(MA_EUNSUPPORTED, "cooperative launch failed: %s", hipGetErrorString(e));
-        }
-        return MA_OK;
+    using U = ma::FusedHead<T, RGB, RGM>;
+    hd.units = c.BH;
+    const ma::Bufs<T> p = typed<T>(B);
+    const int T_ = c.T;
+    return L.run(kFused, [&] {
+        return launched([&] {
+            hipLaunchKernelGGL((ma::monarch_fused_head<T, RGB, RGM>), dim3((unsigned)c.BH), dim3(64 * U::NW), 0,
+                               L.stream, p, hd, T_);
+        });
     });
 }
 
-template <typename T, int D, int NT>
-int dispatch_persistent(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
+template <typename T> int run_fused(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
 {
-    if constexpr (std::is_same<T, float>::value && NT * D > 8192) {
-        return fail(MA_EUNSUPPORTED, "fp32 tile too large");
+    if constexpr (sizeof(T) != 2) {
+        return fail(MA_EUNSUPPORTED, "the fused kernel needs 16-bit elements");
     } else {
-        const bool rgb = hd.b != NT, rgm = hd.m != NT;
-        if (rgb && rgm) return launch_persistent<T, NT, D, true, true>(L, B, hd, c);
-        if (rgb) return launch_persistent<T, NT, D, true, false>(L, B, hd, c);
-        if (rgm) return launch_persistent<T, NT, D, false, true>(L, B, hd, c);
-        return launch_persistent<T, NT, D, false, false>(L, B, hd, c);
+        const bool rgb = hd.b != 16, rgm = hd.m != 16;
+        if (rgb && rgm) return launch_fused<T, true, true>(L, B, hd, c);
+        if (rgb) return launch_fused<T, true, false>(L, B, hd, c);
+        if (rgm) return launch_fused<T, false, true>(L, B, hd, c);
+        return launch_fused<T, false, false>(L, B, hd, c);
     }
-}
-
-template <typename T, int D>
-int run_persistent(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
-{
-    if (tile_rows(hd.m) != tile_rows(hd.b)) return fail(MA_EUNSUPPORTED, "single launch needs m and b in one tile class");
-    switch (tile_rows(hd.b)) {
-    case 16: return dispatch_persistent<T, D, 16>(L, B, hd, c);
-    case 32: return dispatch_persistent<T, D, 32>(L, B, hd, c);
-    case 64: return dispatch_persistent<T, D, 64>(L, B, hd, c);
-    default: return dispatch_persistent<T, D, 128>(L, B, hd, c);
-    }
-}
-
-template <typename T, int D> int run_call_d(Launcher &L, const CallBufs &B, const CallDims &c, int path)
-{
-    ma::HeadDims hd{c.m, c.b, c.s_log2e, 0};
-    if (path == kSingle) {
-        // only on request: measured slower than the half-steps at every shape tried
-        if (B.copies < c.T) return fail(MA_EUNSUPPORTED, "single launch supports T <= %d", kMaxSingleT);
-        return run_persistent<T, D>(L, B, hd, c);
-    }
-    return run_half_steps<T, D>(L, B, hd, c.BH, c.T);
 }
 
 template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const CallDims &c, int path)
 {
-    return c.d == 64 ? run_call_d<T, 64>(L, B, c, path) : run_call_d<T, 128>(L, B, c, path);
+    const int32_t dtype = std::is_same<T, float>::value ? MA_F32 : std::is_same<T, __bf16>::value ? MA_BF16 : MA_F16;
+    ma::HeadDims hd{c.m, c.b, c.s_log2e, 0};
+    if (path == kFusedHead && !fused_applies(dtype, c.d, c.m, c.b))
+        return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d = 64 and m, b <= 16");
+    if (uses_fused(path, dtype, c.d, c.m, c.b)) return run_fused<T>(L, B, hd, c);
+    return c.d == 64 ? run_half_steps<T, 64>(L, B, hd, c.BH, c.T) : run_half_steps<T, 128>(L, B, hd, c.BH, c.T);
 }
 
 }  // namespace ma_host

@@ -16,7 +16,7 @@ int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 inline int pad16(int64_t x) { return (int)((x + 15) / 16 * 16); }
 
 // Kernel kinds reported by the timing interface.
-enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kPersistent = 4 };
+enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4 };
 
 // Per-launch HIP events around every kernel when timing is enabled.
 constexpr int kMaxLaunches = 2 * 64 + 2;
@@ -52,32 +52,37 @@ struct Launcher {
     }
 };
 
-// Untyped tensors, states and the single-launch synchronisation area of one call.
+// Untyped tensors and states of one call (the states are null on the fused path).
 struct CallBufs {
     const void *q, *k, *v;
     void *out;
     void *aR, *aL, *Y;
     float *cR, *cL;
-    unsigned *sync;     // zeroed counters for the single-launch path (kSyncWords words)
-    int *error;         // host-visible flag written by the single-launch path
-    int copies;         // per-iteration copies of alpha_R, alpha_L, c_R, c_L in the workspace
-    int64_t state_stride, c_stride;  // elements / floats between two copies
 };
-constexpr int kSyncWords = 16 + 16 * 8;
-// The single launch keeps one copy of every state per iteration; above this T
-// it is not used (and the workspace holds a single copy).
-constexpr int kMaxSingleT = 8;
 
 struct CallDims {
     int64_t BH;
     int m, b, d, T;
     float s_log2e;
-    int num_cus;
 };
 
-// Path selection: 0 = single launch when it applies, else one launch per
-// half-step; 1 = one launch per half-step; 2 = single launch or MA_EUNSUPPORTED.
-enum Path { kAuto = 0, kHalfSteps = 1, kSingle = 2 };
+// Path selection (monarch_attn_set_path): 0 = the fused kernel for small
+// heads when it applies, else one launch per half-step; 1 = one launch per
+// half-step; 2 = the fused kernel or MA_EUNSUPPORTED.
+enum Path { kAuto = 0, kHalfSteps = 1, kFusedHead = 2 };
+
+// The fused one-workgroup-per-head kernel holds Q, K and all states of a head
+// in LDS: 16-bit elements, d = 64, m and b at most 16.
+inline bool fused_applies(int32_t dtype, int64_t d, int64_t m, int64_t b)
+{
+    return (dtype == MA_BF16 || dtype == MA_F16) && d == 64 && m <= 16 && b <= 16;
+}
+
+// Whether a call with these arguments runs the fused kernel under `path`.
+inline bool uses_fused(int path, int32_t dtype, int64_t d, int64_t m, int64_t b)
+{
+    return path != kHalfSteps && fused_applies(dtype, d, m, b);
+}
 
 // Enqueue the whole forward pass for one element type (defined per dtype).
 template <typename T> int run_call(Launcher &L, const CallBufs &B, const CallDims &c, int path);

@@ -794,167 +794,224 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> 
 }
 
 // ---------------------------------------------------------------------------------------
-// The whole forward pass in one cooperative launch.  Each head is processed by
-// the workgroups of a single XCD (read from the hardware XCC_ID register), so
-// every state a half-step writes is read back by the next half-step from that
-// XCD's L2.  The half-steps of a head are separated by a barrier among the
-// workgroups of its XCD: each thread waits until its stores have reached the
-// L2 (the vector L1 is write-through), then one thread per workgroup adds 1
-// to the XCD's counter and waits until it reaches the phase target.
-// Every state of iteration t has its own copy (`state_stride` elements,
-// `c_stride` floats apart), so within a launch no address is ever read before
-// its last write: a CU's L1 cannot hold a stale line of a state.
-// All waits are bounded: on a time-out the workgroup records the failure in
-// a host-visible flag and returns, so the grid always drains.
+// Small heads (m, b <= 16, d = 64, 16-bit elements): the whole forward pass of
+// one head in one workgroup of 16 waves (the fully fused one-head-per-block
+// kernel for short sequences of Sec. 4, "Benchmarking"), with Q, K and every
+// state resident in LDS, so that only Q, K, V and O cross global memory.  LDS regions, each 16
+// blocks of 16 rows of LD elements, zero wherever there is no data:
+//   Qs[j][l] = Qbar[j][l] = Q[l*b + j]
+//   Ks[k][i] = Kbar[k][i] = K[k*b + i]; the last R half-step of block k
+//              overwrites its own block with Y[k][j]
+//   As[j][k] = alpha_L[j][k]; the L half-step of class j overwrites its own
+//              block with its probabilities P[l][k] (rows l >= m zero)
+//   Rs[k][j] = alpha_R[k][j]; the last R half-step of block k overwrites its
+//              own block with Vbar[k]
+// and c_R[k][j], c_L[j][k] in fp32.  In every half-step wave w does the unit
+// w (block k or class j; one wave per unit at 16 rows): it overwrites only its
+// own blocks, apart from the state it hands to the next half-step, and the
+// half-steps are separated by workgroup barriers.  A wave's LDS accesses take
+// effect in program order, so a unit may overwrite a block it has read.  The
+// arithmetic of a unit is that of RHalf / LHalf / Apply at 16 rows.
 // ---------------------------------------------------------------------------------------
-struct SyncState {
-    unsigned *counters;    // [x]: workgroups on XCD x; [8]: arrivals; [16 + 16 x]: barrier of XCD x
-    int *error;            // host-visible flag, set to 1 on a barrier time-out
-    int64_t state_stride;  // elements between the per-iteration copies of alpha_R / alpha_L
-    int64_t c_stride;      // floats between the per-iteration copies of c_R / c_L
-    unsigned zero;         // 0 (see xcd_barrier)
-};
+template <typename T, bool RGB, bool RGM> struct FusedHead {
+    static_assert(sizeof(T) == 2, "16-bit elements only");
+    static constexpr int D = 64, NW = 16, LD = Ld<T, D>::row;  // 64 * NW threads (the launch bound below)
+    static constexpr int REGION = 16 * 16 * LD;  // elements
+    static constexpr int LDS_BYTES = 4 * REGION * (int)sizeof(T) + 2 * 256 * 4;
 
-constexpr unsigned kSpinLimit = 1u << 20;
+    struct Ctx {
+        T *Qs, *Ks, *As, *Rs;
+        float *cRs, *cLs;  // c_R[k][j] at k*16 + j, c_L[j][k] at j*16 + k
+        int m, b, lane, g, c16;
+        float s_log2e;
+    };
 
-__device__ inline unsigned read_xcc_id()
-{
-    unsigned x;
-    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
-    return x & 7u;
-}
-
-// Thread 0 only: wait (bounded) until *ctr >= target.
-template <int ORDER = __ATOMIC_RELAXED>
-__device__ inline bool spin_until(unsigned *ctr, unsigned target)
-{
-    unsigned it = 0;
-    while (__hip_atomic_load(ctr, ORDER, __HIP_MEMORY_SCOPE_AGENT) < target) {
-        if (++it > kSpinLimit) return false;
-        __builtin_amdgcn_s_sleep(2);
+    template <bool FIRST, bool FINAL>
+    __device__ static void r_unit(const Ctx &c, int k, const u32x4 *vpre)
+    {
+        const int j = c.c16;
+        const bool jv = j < c.b;
+        RowFrags<T, D> bf;  // row j of alpha_R[k]; at t = 1 that is Q[k*b + j] = Qs[j][k]
+        bf.load(FIRST ? c.Qs + (j * 16 + k) * LD : c.Rs + (k * 16 + j) * LD, c.g);
+        float rs = c.s_log2e;
+        if constexpr (!FIRST) {
+            if (jv) rs = c.s_log2e / fmaxf(c.cRs[k * 16 + j], kTiny);
+        }
+        T *Kk = c.Ks + k * 16 * LD;
+        f32x4 sc;  // lane holds S'[i = 4g + qq][j]
+        gemm_scores_rt<T, D, 1>(Kk + c.c16 * LD, &bf, &sc, c.g);
+        const float nb = -tiles_max<1, RGB>(&sc, c.b, c.g) * rs;
+        float sum = 0.f, t2 = 0.f;
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+            const float u = __builtin_fmaf(sc[qq], rs, nb);
+            float e = __builtin_amdgcn_exp2f(u);
+            if (RGB && 4 * c.g + qq >= c.b) e = 0.f;
+            sum += e;
+            t2 = __builtin_fmaf(e, u, t2);
+            sc[qq] = e;
+        }
+        sum = lanegroup_sum(sum);
+        t2 = lanegroup_sum(t2);
+        const float inv = 1.0f / sum;
+        if (c.g == 0 && jv) c.cLs[j * 16 + k] = kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum));
+        ProbFrags<T, 1> pf;
+        pf.pack(&sc);
+        f32x4 out[D / 16];
+#pragma unroll
+        for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, 1>(Kk, LD, 16 * vt, pf, c.lane);
+        store_row<T, D>(jv ? c.As + (j * 16 + k) * LD : nullptr, out, inv, c.lane);  // alpha_L[j][k]
+        if constexpr (FINAL) {
+            T *Vk = c.Rs + k * 16 * LD;  // alpha_R[k] has been read: stage Vbar[k] in its place
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+                *reinterpret_cast<u32x4 *>(Vk + ((c.lane >> 3) + 8 * h) * LD + (c.lane & 7) * 8) = vpre[h];
+#pragma unroll
+            for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, 1>(Vk, LD, 16 * vt, pf, c.lane);
+            store_row<T, D>(jv ? Kk + j * LD : nullptr, out, inv, c.lane);  // Y[k][j] over Kbar[k]
+        }
     }
-    return true;
-}
 
-// The poll is an atomic add of `zero` (0 at run time, opaque to the compiler,
-// which would otherwise turn an add of 0 into a load that the CU's L1 may
-// serve): it executes where the increments execute and returns the current
-// count.
-__device__ inline bool xcd_barrier(unsigned *ctr, unsigned target, unsigned zero, int *error, int *shared_ok)
-{
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        unsigned it = 0;
-        bool ok = true;
-        while (__hip_atomic_fetch_add(ctr, zero, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            if (++it > kSpinLimit) {
-                ok = false;
-                break;
+    // Scores and softmax over k of class j, query row l = lane % 16 (lane
+    // holds k = 4g + qq); returns exp2 values and sets inv = 1 / row sum.
+    __device__ static f32x4 l_softmax(const Ctx &c, int j, float &inv)
+    {
+        RowFrags<T, D> bf;
+        bf.load(c.Qs + (j * 16 + c.c16) * LD, c.g);  // Qbar[j][l]
+        f32x4 acc;
+        gemm_scores_rt<T, D, 1>(c.As + (j * 16 + c.c16) * LD, &bf, &acc, c.g);
+        f32x4 sc;
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+            const int kk = 4 * c.g + qq;
+            const float bias = (!RGM || kk < c.m) ? c.cLs[j * 16 + kk] * kLog2e : 0.f;
+            sc[qq] = __builtin_fmaf(acc[qq], c.s_log2e, -bias);
+        }
+        const float mx = tiles_max<1, RGM>(&sc, c.m, c.g);
+        float sum = 0.f;
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) {
+            float e = __builtin_amdgcn_exp2f(sc[qq] - mx);
+            if (RGM && 4 * c.g + qq >= c.m) e = 0.f;
+            sum += e;
+            sc[qq] = e;
+        }
+        inv = 1.0f / lanegroup_sum(sum);
+        return sc;
+    }
+
+    __device__ static void l_unit(const Ctx &c, int j)
+    {
+        const int l = c.c16;
+        float inv;
+        const f32x4 e = l_softmax(c, j, inv);
+        T *Aj = c.As + j * 16 * LD;  // alpha_L[j] has been read: P[l][k] in its place
+        const f32x4 pr = l < c.m ? e * inv : f32x4{0.f, 0.f, 0.f, 0.f};  // padded query rows carry no weight
+        store4<T>(Aj + l * LD + 4 * c.g, pr);
+        ProbFrags<T, 1> pf;  // B operand: P[l-slots][k = lane % 16]
+        pf.gather(Aj, LD, 0, c.lane);
+        const int k = c.c16;
+        const f32x4 cs = gemm_colsum<T, 1>(pf);  // c_R[k][j] = sum_l L[j][k][l]
+        if (c.g == 0 && k < c.m) c.cRs[k * 16 + j] = cs[0];
+        f32x4 out[D / 16];
+#pragma unroll
+        for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, 1>(c.Qs + j * 16 * LD, LD, 16 * vt, pf, c.lane);
+        store_row<T, D>(k < c.m ? c.Rs + (k * 16 + j) * LD : nullptr, out, 1.0f, c.lane);  // alpha_R[k][j]
+    }
+
+    __device__ static void apply_unit(const Ctx &c, int j, T *out_h)
+    {
+        const int l = c.c16;
+        float inv;
+        const f32x4 e = l_softmax(c, j, inv);
+        ProbFrags<T, 1> pf;
+        pf.pack(&e);
+        f32x4 o[D / 16];  // O[l*b + j] = sum_k L[j][k][l] Y[k][j]; Y[k][j] is row k of Ks + j*LD at stride 16*LD
+#pragma unroll
+        for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, 1>(c.Ks + j * LD, 16 * LD, 16 * vt, pf, c.lane);
+        store_row<T, D>(l < c.m ? out_h + ((int64_t)l * c.b + j) * D : nullptr, o, inv, c.lane);
+    }
+
+    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int T_, char *lds)
+    {
+        Ctx c;
+        c.Qs = reinterpret_cast<T *>(lds);
+        c.Ks = c.Qs + REGION;
+        c.As = c.Ks + REGION;
+        c.Rs = c.As + REGION;
+        c.cRs = reinterpret_cast<float *>(c.Rs + REGION);
+        c.cLs = c.cRs + 256;
+        c.m = hd.m;
+        c.b = hd.b;
+        c.s_log2e = hd.s_log2e;
+        const int tid = threadIdx.x, w = tid >> 6;
+        c.lane = tid & 63;
+        c.g = c.lane >> 4;
+        c.c16 = c.lane & 15;
+        const int m = hd.m, b = hd.b;
+        const int64_t hoff = bh * (int64_t)m * b * D;
+        const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
+
+        // Qs and Ks: 2 regions x 256 rows x 8 chunks of 16 bytes, 4 per thread,
+        // all loads issued before the LDS stores; As and Rs zeroed.
+        constexpr int PER = 2 * 256 * 8 / (64 * NW);
+        u32x4 raw[PER];
+#pragma unroll
+        for (int h = 0; h < PER; ++h) {
+            const int idx = tid + h * 64 * NW;
+            const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
+            raw[h] = u32x4{0u, 0u, 0u, 0u};
+            if (reg == 0 && blk < b && r < m)
+                raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * D + col);  // Qbar[blk][r]
+            if (reg == 1 && blk < m && r < b)
+                raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * D + col);  // Kbar[blk][r]
+        }
+        // Vbar[w] for the last R half-step, held in registers until then
+        u32x4 vpre[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int r = (c.lane >> 3) + 8 * h, col = (c.lane & 7) * 8;
+            vpre[h] = u32x4{0u, 0u, 0u, 0u};
+            if (w < m && r < b) vpre[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * D + col);
+        }
+        for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) {
+            const int row = idx >> 3, col = (idx & 7) * 8;
+            *reinterpret_cast<u32x4 *>(c.As + row * LD + col) = u32x4{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int h = 0; h < PER; ++h) {
+            const int idx = tid + h * 64 * NW;
+            *reinterpret_cast<u32x4 *>(c.Qs + (idx >> 3) * LD + (idx & 7) * 8) = raw[h];
+        }
+        __syncthreads();
+
+        for (int t = 1; t <= T_; ++t) {
+            const bool first = t == 1, last = t == T_;
+            if (w < m) {
+                if (first && last)
+                    r_unit<true, true>(c, w, vpre);
+                else if (first)
+                    r_unit<true, false>(c, w, vpre);
+                else if (last)
+                    r_unit<false, true>(c, w, vpre);
+                else
+                    r_unit<false, false>(c, w, vpre);
             }
-            __builtin_amdgcn_s_sleep(1);
+            __syncthreads();
+            if (last) break;
+            if (w < b) l_unit(c, w);
+            __syncthreads();
         }
-        if (!ok) __hip_atomic_store(error, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-        *shared_ok = ok;
+        if (w < b) apply_unit(c, w, p.out + hoff);
     }
-    __syncthreads();
-    return *shared_ok != 0;
-}
-
-template <int A, int B> struct MaxOf {
-    static constexpr int value = A > B ? A : B;
 };
 
-template <typename T, int NB, int NM, int D, bool RGB, bool RGM> struct Persistent {
-    using R1 = RHalf<T, NB, D, true, false, RGB>;
-    using R1F = RHalf<T, NB, D, true, true, RGB>;
-    using RM = RHalf<T, NB, D, false, false, RGB>;
-    using RF = RHalf<T, NB, D, false, true, RGB>;
-    using LH = LHalf<T, NM, D, RGM>;
-    using AP = Apply<T, NM, D, RGM>;
-    static constexpr int W = MaxOf<R1::W, LH::W>::value;
-    static constexpr int LDS_BYTES = MaxOf<R1F::LDS_BYTES, MaxOf<LH::LDS_BYTES, AP::LDS_BYTES>::value>::value;
-};
-
-template <typename T, int NB, int NM, int D, bool RGB, bool RGM>
-__global__ __launch_bounds__((64 * Persistent<T, NB, NM, D, RGB, RGM>::W)) void monarch_persistent(
-    Bufs<T> p, HeadDims hd, int64_t BH, int T_, SyncState ss)
+template <typename T, bool RGB, bool RGM>
+__global__ __launch_bounds__(1024) void monarch_fused_head(Bufs<T> p, HeadDims hd, int T_)
 {
-    using P = Persistent<T, NB, NM, D, RGB, RGM>;
-    __shared__ __attribute__((aligned(16))) char lds[P::LDS_BYTES];
-    __shared__ unsigned info[10];
-    __shared__ int ok;
-    const int tid = threadIdx.x, nthreads = 64 * P::W;
-    const unsigned xcc = read_xcc_id();
-
-    // registration: rank of this workgroup on its XCD, and workgroups per XCD
-    if (tid == 0) {
-        // the registration add completes (its value is returned) before the arrival add is issued
-        info[0] = __hip_atomic_fetch_add(&ss.counters[xcc], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        __hip_atomic_fetch_add(&ss.counters[8], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const bool arrived = spin_until(&ss.counters[8], gridDim.x);
-        if (!arrived) __hip_atomic_store(ss.error, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-        for (int x = 0; x < 8; ++x)
-            info[1 + x] = __hip_atomic_load(&ss.counters[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        info[9] = arrived;
-    }
-    __syncthreads();
-    if (!info[9]) return;
-    const unsigned rank = info[0], cnt = info[1 + xcc];
-    unsigned nx = 0, pos = 0;  // XCDs with workgroups, and this XCD's place among them
-    for (unsigned x = 0; x < 8; ++x) {
-        if (info[1 + x]) {
-            if (x < xcc) ++pos;
-            ++nx;
-        }
-    }
-    unsigned *bar = &ss.counters[16 + 16 * xcc];
-    unsigned phase = 0;
-    const int m = hd.m, b = hd.b;
-    // heads of this XCD: bh = pos + nx * h for h < nheads; every phase covers all of them
-    const int64_t nheads = (int64_t)pos < BH ? (BH - pos + nx - 1) / nx : 0;
-
-    for (int t = 1; t <= T_; ++t) {
-        const bool first = (t == 1), last = (t == T_);
-        // iteration t: R reads alpha_R / c_R copy t-2 and writes alpha_L / c_L copy t-1;
-        // L reads alpha_L / c_L copy t-1 and writes alpha_R / c_R copy t-1.
-        Bufs<T> pt = p;
-        pt.aL += (t - 1) * ss.state_stride;
-        pt.cL += (t - 1) * ss.c_stride;
-        Bufs<T> pr = pt;
-        if (!first) {
-            pr.aR += (t - 2) * ss.state_stride;
-            pr.cR += (t - 2) * ss.c_stride;
-        }
-        for (int64_t u = rank; u < nheads * m; u += cnt) {
-            const int64_t bh = pos + nx * (u / m);
-            const int k = (int)(u % m);
-            if (first && last)
-                P::R1F::run(pr, hd, bh, k, lds, tid, nthreads);
-            else if (first)
-                P::R1::run(pr, hd, bh, k, lds, tid, nthreads);
-            else if (last)
-                P::RF::run(pr, hd, bh, k, lds, tid, nthreads);
-            else
-                P::RM::run(pr, hd, bh, k, lds, tid, nthreads);
-            __syncthreads();
-        }
-        if (!xcd_barrier(bar, ++phase * cnt, ss.zero, ss.error, &ok)) return;
-        pt.aR += (t - 1) * ss.state_stride;
-        pt.cR += (t - 1) * ss.c_stride;
-        for (int64_t u = rank; u < nheads * b; u += cnt) {
-            const int64_t bh = pos + nx * (u / b);
-            const int j = (int)(u % b);
-            if (last)
-                P::AP::run(pt, hd, bh, j, lds, tid, nthreads);
-            else
-                P::LH::run(pt, hd, bh, j, lds, tid, nthreads);
-            __syncthreads();
-        }
-        if (!last && !xcd_barrier(bar, ++phase * cnt, ss.zero, ss.error, &ok)) return;
-    }
+    using U = FusedHead<T, RGB, RGM>;
+    __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
+    U::run(p, hd, blockIdx.x, T_, lds);
 }
 
 }  // namespace ma

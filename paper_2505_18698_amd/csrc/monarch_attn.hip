@@ -1,6 +1,6 @@
 // C ABI of the MonarchAttention forward pass (include/monarch_attn.h):
-// argument checks, the per-device workspace, path selection, the
-// host-visible error flag of the single-launch path, and per-launch timing.
+// argument checks, the per-device workspace, path selection and per-launch
+// timing.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -52,24 +52,17 @@ int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t d
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-int state_copies(int32_t T) { return T <= kMaxSingleT ? T : 1; }
-
-size_t workspace_bytes(int64_t BH, int64_t N, int64_t d, int32_t T, int32_t dtype)
+size_t workspace_bytes(int64_t BH, int64_t N, int64_t d, int32_t dtype)
 {
-    // alpha_R, alpha_L (one copy per iteration up to kMaxSingleT) and Y in the
-    // element type; c_R, c_L (likewise) in fp32; the counters of the
-    // single-launch path.
+    // alpha_R, alpha_L and Y in the element type, c_R and c_L in fp32
     const size_t st = align_up((size_t)BH * N * d * elem_bytes(dtype));
     const size_t cs = align_up((size_t)BH * N * sizeof(float));
-    const size_t c = (size_t)state_copies(T);
-    return (2 * c + 1) * st + 2 * c * cs + align_up(kSyncWords * sizeof(unsigned));
+    return 3 * st + 2 * cs;
 }
 
 struct Device {
     void *ws = nullptr;
     size_t ws_bytes = 0;
-    int *error = nullptr;  // pinned host memory, written by the single-launch kernel
-    int num_cus = 0;
 };
 
 constexpr int kMaxDevices = 64;
@@ -100,7 +93,7 @@ size_t monarch_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, 
                                     int32_t T, int32_t dtype)
 {
     if (B < 1 || H < 1 || check_shape(N, d, m, b, T, dtype) != MA_OK) return 0;
-    return workspace_bytes(B * H, N, d, T, dtype);
+    return workspace_bytes(B * H, N, d, dtype);
 }
 
 int monarch_attn_release_workspace(void)
@@ -122,7 +115,7 @@ int monarch_attn_release_workspace(void)
 int monarch_attn_set_path(int32_t path)
 {
     g_err[0] = '\0';
-    if (path != kAuto && path != kHalfSteps && path != kSingle) {
+    if (path != kAuto && path != kHalfSteps && path != kFusedHead) {
         fail(MA_EINVAL, "unknown path %d", path);
         return -1;
     }
@@ -186,32 +179,16 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
         overlaps(out, tensor_bytes, v, tensor_bytes))
         return fail(MA_EINVAL, "out must not overlap q, k or v");
 
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
-    const size_t need = workspace_bytes(BH, N, d, T, dtype);
-    void *ws = nullptr;
-    int *error = nullptr;
-    int num_cus = 0;
-    {
+    const int path = g_path.load();
+    const size_t st = align_up((size_t)BH * N * d * elem_bytes(dtype));
+    const size_t cs = align_up((size_t)BH * N * sizeof(float));
+    CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr};
+    if (!uses_fused(path, dtype, d, m, b)) {  // the fused kernel keeps its states in LDS
+        int dev = 0;
+        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
+        const size_t need = workspace_bytes(BH, N, d, dtype);
         std::lock_guard<std::mutex> lock(g_dev_mutex);
         Device &D = g_dev[dev];
-        if (!D.error) {
-            hipDeviceProp_t prop;
-            if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return fail(MA_EHIP, "hipGetDeviceProperties failed");
-            D.num_cus = prop.multiProcessorCount;
-            void *h = nullptr;
-            if (hipHostMalloc(&h, sizeof(int), hipHostMallocDefault) != hipSuccess) {
-                (void)hipGetLastError();
-                return fail(MA_ENOMEM, "hipHostMalloc of the error flag failed");
-            }
-            D.error = (int *)h;
-            *D.error = 0;
-        }
-        if (__atomic_load_n(D.error, __ATOMIC_ACQUIRE) != 0) {
-            __atomic_store_n(D.error, 0, __ATOMIC_RELEASE);
-            return fail(MA_EHIP, "an earlier single-launch call on this device timed out at a barrier; "
-                                 "its output is invalid");
-        }
         if (D.ws_bytes < need) {
             if (D.ws) {
                 if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
@@ -227,37 +204,19 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
             D.ws = p;
             D.ws_bytes = need;
         }
-        ws = D.ws;
-        error = D.error;
-        num_cus = D.num_cus;
+        char *base = (char *)D.ws;
+        bufs.aR = base;
+        bufs.aL = base + st;
+        bufs.Y = base + 2 * st;
+        bufs.cR = (float *)(base + 3 * st);
+        bufs.cL = (float *)(base + 3 * st + cs);
     }
-
-    const size_t st = align_up((size_t)BH * N * d * elem_bytes(dtype));
-    const size_t cs = align_up((size_t)BH * N * sizeof(float));
-    const int copies = state_copies(T);
-    char *base = (char *)ws;
-    char *cbase = base + (2 * copies + 1) * st;
-    CallBufs bufs{q,
-                  k,
-                  v,
-                  out,
-                  base,                                   // alpha_R copies
-                  base + copies * st,                     // alpha_L copies
-                  base + 2 * copies * st,                 // Y
-                  (float *)cbase,                         // c_R copies
-                  (float *)(cbase + copies * cs),         // c_L copies
-                  (unsigned *)(cbase + 2 * copies * cs),  // counters
-                  error,
-                  copies,
-                  (int64_t)(st / elem_bytes(dtype)),
-                  (int64_t)(cs / sizeof(float))};
-    CallDims dims{BH, (int)m, (int)b, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
+    CallDims dims{BH, (int)m, (int)b, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d))};
 
     std::unique_lock<std::mutex> tlock(g_timing_mutex);
     Launcher L{(hipStream_t)stream, g_timing.enabled};
     if (!L.timed) tlock.unlock();
     (void)hipGetLastError();  // clear a stale error so the check below is ours
-    const int path = g_path.load();
     switch (dtype) {
     case MA_F32: rc = run_call<float>(L, bufs, dims, path); break;
     case MA_BF16: rc = run_call<__bf16>(L, bufs, dims, path); break;

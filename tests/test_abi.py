@@ -88,14 +88,22 @@ def test_workspace_bytes_formula():
 
     B, H, N, d = 1, 16, 16384, 64
     got = ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 2, 1)
-    state = B * H * N * d * 2
-    cvec = B * H * N * 4
-    counters = 768  # synchronisation words of the single-launch path, 256-byte aligned
-    T = 2           # one copy of alpha_R, alpha_L, c_R, c_L per iteration, one Y
-    assert got == (2 * T + 1) * state + 2 * T * cvec + counters
-    big_T = ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 20, 1)
-    assert big_T == 3 * state + 2 * cvec + counters
+    state = B * H * N * d * 2   # alpha_R, alpha_L, Y
+    cvec = B * H * N * 4        # c_R, c_L
+    assert got == 3 * state + 2 * cvec
+    assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 20, 1) == got  # independent of T
     assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 127, 2, 1) == 0
+
+
+def test_fused_path_applicability():
+    import paper_2505_18698_amd as ma
+
+    assert ma.fused_applies(64, 14, 14, ma.MA_BF16)
+    assert ma.fused_applies(64, 16, 16, ma.MA_F16)
+    assert ma.fused_applies(64, 1, 16, ma.MA_BF16)
+    assert not ma.fused_applies(64, 16, 17, ma.MA_BF16)
+    assert not ma.fused_applies(128, 16, 16, ma.MA_BF16)
+    assert not ma.fused_applies(64, 16, 16, ma.MA_F32)
 
 
 def test_timing_read_without_a_timed_call_fails_cleanly():

@@ -32,18 +32,14 @@ def _tile(n):
 
 
 # Every parity test runs on both execution paths: one launch per half-step,
-# and the single cooperative launch with XCD-local state exchange.
-@pytest.fixture(params=["half_steps", "single"])
+# and one workgroup per head with the states in LDS (small heads only).
+@pytest.fixture(params=["half_steps", "fused"])
 def ma(lib, request):
-    path = lib.PATH_HALF_STEPS if request.param == "half_steps" else lib.PATH_SINGLE
+    path = lib.PATH_HALF_STEPS if request.param == "half_steps" else lib.PATH_FUSED
     prev = lib.monarch_attn_set_path(path)
     lib.path_name = request.param
     yield lib
     lib.monarch_attn_set_path(prev)
-
-
-def _single_applies(m, b):
-    return _tile(m) == _tile(b)
 
 
 def _torch_dtype(dtype):
@@ -55,9 +51,9 @@ def _torch_dtype(dtype):
 def gpu_run(ma, q, k, v, m, b, T, dtype):
     import torch
 
-    if ma.path_name == "single" and not _single_applies(m, b):
-        pytest.skip("the single-launch path needs m and b in one 16-row tile class")
     td = _torch_dtype(dtype)
+    if ma.path_name == "fused" and not ma.fused_applies(q.shape[-1], m, b, ma.dtype_code(td)):
+        pytest.skip("the fused kernel covers 16-bit elements, d = 64, m and b <= 16")
     dq = torch.from_numpy(q).to(td).cuda()
     dk = torch.from_numpy(k).to(td).cuda()
     dv = torch.from_numpy(v).to(td).cuda()
@@ -197,16 +193,16 @@ def test_rejected_call_leaves_out_untouched(ma):
     assert bool((out == 3.0).all())
 
 
-def test_single_path_unsupported_shape_is_rejected(lib):
-    """m and b in different tile classes: the forced single launch refuses
-    (nothing launched), the automatic path falls back to the half-steps."""
+def test_fused_path_unsupported_shape_is_rejected(lib):
+    """b > 16: the forced fused path refuses (nothing launched), the automatic
+    path runs the half-steps."""
     import torch
 
     m, b = 8, 40
     q, k, v = si.random_qkv(1, 1, m * b, 64, "bf16", seed=11)
     dq, dk, dv = (torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (q, k, v))
     out = torch.full_like(dq, 3.0)
-    prev = lib.monarch_attn_set_path(lib.PATH_SINGLE)
+    prev = lib.monarch_attn_set_path(lib.PATH_FUSED)
     try:
         with pytest.raises(lib.MonarchAttnError) as exc:
             lib.monarch_attn_fwd(dq, dk, dv, out, m, b, 2)
@@ -222,33 +218,27 @@ def test_single_path_unsupported_shape_is_rejected(lib):
     check(out.double().cpu().numpy(), ref, "bf16", "auto fallback m8 b40")
 
 
-@pytest.mark.parametrize("name", ["speed_n16384", "speed_n4096", "roberta_n1024"])
-def test_paths_agree_bitwise_without_stale_state(lib, name):
-    """Both paths run the same unit code.  The workspace is first filled from
-    other inputs (A); the single launch on inputs B must then reproduce the
-    half-step result on B bit for bit, twice: a read of a state before its
-    write (a stale value left by A) would show up as a difference."""
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("m,b,T", [(14, 14, 2), (16, 16, 1), (16, 16, 3), (5, 16, 2), (16, 3, 2), (1, 1, 2)])
+def test_fused_and_half_steps_agree_bitwise(lib, dtype, m, b, T):
+    """The fused kernel runs the unit arithmetic of the half-step kernels at
+    16 rows on the same element-type states, so both paths give the same bits."""
     import torch
 
-    w = si.WORKLOADS[name].with_(T=2)
-    A = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in si.make_qkv(w, seed=1)[:3]]
-    B = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in si.make_qkv(w, seed=2)[:3]]
+    td = _torch_dtype(dtype)
+    q, k, v = si.random_qkv(3, 5, m * b, 64, dtype, seed=100 + m * 17 + b, scale=1.5)
+    t = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
 
-    def run(t, path):
+    def run(path):
         lib.monarch_attn_set_path(path)
-        out = torch.empty_like(t[0])
-        lib.monarch_attn_fwd(t[0], t[1], t[2], out, w.m, w.b, w.T)
+        out = torch.full_like(t[0], float("nan"))
+        lib.monarch_attn_fwd(t[0], t[1], t[2], out, m, b, T)
         torch.cuda.synchronize()
         return out.cpu()
 
     prev = lib.monarch_attn_set_path(lib.PATH_HALF_STEPS)
     try:
-        ref = run(B, lib.PATH_HALF_STEPS)
-        run(A, lib.PATH_HALF_STEPS)
-        s1 = run(B, lib.PATH_SINGLE)
-        run(A, lib.PATH_SINGLE)
-        s2 = run(B, lib.PATH_SINGLE)
+        ref, got = run(lib.PATH_HALF_STEPS), run(lib.PATH_FUSED)
     finally:
         lib.monarch_attn_set_path(prev)
-    assert torch.equal(s1, ref)
-    assert torch.equal(s2, ref)
+    assert torch.equal(got, ref), float((got.float() - ref.float()).abs().max())
