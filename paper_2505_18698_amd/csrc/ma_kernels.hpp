@@ -104,8 +104,47 @@ template <typename T, int C> struct Ld {
     static constexpr int row = C + 16 / (int)sizeof(T);
 };
 
-__device__ inline float wave_xor_max(float x, int mask) { return fmaxf(x, __shfl_xor(x, mask)); }
-__device__ inline float wave_xor_sum(float x, int mask) { return x + __shfl_xor(x, mask); }
+// gfx950's v_permlane16_swap / v_permlane32_swap applied to (x, x) return
+// x[lane] and x[lane ^ 16] (resp. x[lane ^ 32]), in an order that depends on
+// the lane: a VALU exchange with no LDS round trip.  The pair feeds
+// commutative operations only, except in xor16_value.
+template <int MASK> __device__ inline void xor_pair(uint32_t x, uint32_t &a, uint32_t &b)
+{
+    static_assert(MASK == 16 || MASK == 32, "lane distance 16 or 32");
+    if constexpr (MASK == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        a = r[0];
+        b = r[1];
+    } else {
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        a = r[0];
+        b = r[1];
+    }
+}
+
+template <int MASK> __device__ inline float wave_xor_max(float x)
+{
+    uint32_t a, b;
+    xor_pair<MASK>(__float_as_uint(x), a, b);
+    return fmaxf(__uint_as_float(a), __uint_as_float(b));
+}
+
+template <int MASK> __device__ inline float wave_xor_sum(float x)
+{
+    uint32_t a, b;
+    xor_pair<MASK>(__float_as_uint(x), a, b);
+    return __uint_as_float(a) + __uint_as_float(b);
+}
+
+// x[lane ^ 16]; odd_row = bit 4 of the lane.  The first result of
+// permlane16_swap holds the partner in odd rows of 16 lanes, the second in
+// even rows.
+__device__ inline uint32_t xor16_value(uint32_t x, bool odd_row)
+{
+    uint32_t a, b;
+    xor_pair<16>(x, a, b);
+    return odd_row ? a : b;
+}
 
 template <typename T> __device__ inline T to_elem(float x) { return static_cast<T>(x); }
 
@@ -386,14 +425,23 @@ __device__ inline float tiles_max(const f32x4 *z, int n, int g)
         for (int q = 0; q < 4; ++q)
             if (!RAGGED || 16 * t + 4 * g + q < n) mx = fmaxf(mx, z[t][q]);
     }
-    mx = wave_xor_max(mx, 16);
-    return wave_xor_max(mx, 32);
+    mx = wave_xor_max<16>(mx);
+    return wave_xor_max<32>(mx);
 }
+
+// 1 / x with the hardware reciprocal (at most 1 ulp from the rounded quotient).
+__device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// Whether a softmax is normalised before it feeds a product (4 NT multiplies
+// per lane) rather than after it (D / 16 * 4): whichever is fewer.
+template <int NT, int D> struct NormFirst {
+    static constexpr bool value = 16 * NT < D;
+};
 
 __device__ inline float lanegroup_sum(float x)
 {
-    x = wave_xor_sum(x, 16);
-    return wave_xor_sum(x, 32);
+    x = wave_xor_sum<16>(x);
+    return wave_xor_sum<32>(x);
 }
 
 // Store the 16 x D output tile held as D/16 transposed MFMA tiles (lane holds
@@ -423,13 +471,23 @@ __device__ inline void store_row(T *row, const f32x4 *acc, float scale, int lane
             }
             const u32x2 give = odd ? pk[0] : pk[1];
             u32x2 got;
-            got[0] = __shfl_xor(give[0], 16);
-            got[1] = __shfl_xor(give[1], 16);
+            got[0] = xor16_value(give[0], odd);
+            got[1] = xor16_value(give[1], odd);
             const u32x4 chunk = odd ? u32x4{got[0], got[1], pk[1][0], pk[1][1]}
                                     : u32x4{pk[0][0], pk[0][1], got[0], got[1]};
             if (row) *reinterpret_cast<u32x4 *>(row + 16 * (2 * i + (odd ? 1 : 0)) + 8 * (g >> 1)) = chunk;
         }
     }
+}
+
+// The same 16 x D tile to a row of an LDS matrix: 8 bytes per lane and MFMA
+// tile, no exchange between lanes (LDS has no coalescing to serve).
+template <typename T, int D> __device__ inline void store_row_lds(T *row, const f32x4 *acc, int lane)
+{
+    if (!row) return;
+    const int g = lane >> 4;
+#pragma unroll
+    for (int vt = 0; vt < D / 16; ++vt) store4<T>(row + 16 * vt + 4 * g, acc[vt]);
 }
 
 struct HeadDims {
@@ -462,6 +520,7 @@ template <typename T> struct Bufs {
 // ---------------------------------------------------------------------------------------
 template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct RHalf {
     static constexpr int NT = NB / 16, RT = Split<NT>::RT, W = Split<NT>::W;
+    static constexpr bool NF = NormFirst<NT, D>::value;
     static constexpr int LDK = Ld<T, D>::row;
     static constexpr int LDS_BYTES = (FINAL ? 2 : 1) * NB * LDK * (int)sizeof(T);
 
@@ -494,7 +553,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
             bf[r].load(jvalid ? (FIRST ? p.q : p.aR) + hoff + ((int64_t)k * b + jr[r]) * D : nullptr, g);
             rscale[r] = hd.s_log2e;
             if constexpr (!FIRST) {
-                if (jvalid) rscale[r] = hd.s_log2e / fmaxf(p.cR[bh * N + (int64_t)jr[r] * m + k], kTiny);
+                if (jvalid) rscale[r] = hd.s_log2e * fast_rcp(fmaxf(p.cR[bh * N + (int64_t)jr[r] * m + k], kTiny));
             }
         }
         __syncthreads();
@@ -530,11 +589,16 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
             }
             sum = lanegroup_sum(sum);
             t2 = lanegroup_sum(t2);
-            inv[r] = 1.0f / sum;
+            inv[r] = fast_rcp(sum);
             // c_L = sum_i R log R = sum_i R (Z - max) - log(sum)   (natural-log units)
             if (g == 0 && jr[r] < b)
                 p.cL[bh * N + (int64_t)k * b + jr[r]] = kLn2 * (t2 * inv[r] - __builtin_amdgcn_logf(sum));
-            pf[r].pack(sc[r]);  // unnormalised exp2 values; the row sum is divided out below
+            if constexpr (NF) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) sc[r][t] *= inv[r];
+                inv[r] = 1.0f;
+            }
+            pf[r].pack(sc[r]);  // !NF: unnormalised exp2 values, the row sum is divided out below
         }
         f32x4 out[RT][D / 16];
 #pragma unroll
@@ -637,7 +701,7 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
                     }
                 }
                 sum = lanegroup_sum(sum);
-                inv[r] = (lr[r] < m) ? 1.0f / sum : 0.f;  // padded query rows carry no weight
+                inv[r] = (lr[r] < m) ? fast_rcp(sum) : 0.f;  // padded query rows carry no weight
             }
         }
         __syncthreads();  // every wave is done reading alpha_L
@@ -685,6 +749,7 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
 // ---------------------------------------------------------------------------------------
 template <typename T, int NM, int D, bool RAGGED> struct Apply {
     static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
+    static constexpr bool NF = NormFirst<NT, D>::value;
     static constexpr int LDK = Ld<T, D>::row;
     static constexpr int LDS_BYTES = 2 * NM * LDK * (int)sizeof(T) + NM * 4;
 
@@ -746,8 +811,13 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
                     sc[r][t][qq] = e;
                 }
             }
-            inv[r] = 1.0f / lanegroup_sum(sum);
-            pf[r].pack(sc[r]);  // unnormalised; the row sum is divided out of O below
+            inv[r] = fast_rcp(lanegroup_sum(sum));
+            if constexpr (NF) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) sc[r][t] *= inv[r];
+                inv[r] = 1.0f;
+            }
+            pf[r].pack(sc[r]);  // !NF: unnormalised, the row sum is divided out of O below
         }
         f32x4 o[RT][D / 16];
 #pragma unroll
@@ -816,12 +886,16 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> 
 template <typename T, bool RGB, bool RGM> struct FusedHead {
     static_assert(sizeof(T) == 2, "16-bit elements only");
     static constexpr int D = 64, NW = 16, LD = Ld<T, D>::row;  // 64 * NW threads (the launch bound below)
-    static constexpr int REGION = 16 * 16 * LD;  // elements
-    static constexpr int LDS_BYTES = 4 * REGION * (int)sizeof(T) + 2 * 256 * 4;
+    // Blocks are BS elements apart: 16 rows plus 16 bytes, so that the 16
+    // lanes reading row r of 16 different blocks hit different LDS banks.
+    static constexpr int BS = 16 * LD + 8;
+    static constexpr int REGION = 16 * BS;  // elements
+    static constexpr int CS = 17;  // row stride (floats) of c_R and c_L: writes along a column avoid bank conflicts
+    static constexpr int LDS_BYTES = 4 * REGION * (int)sizeof(T) + 2 * 16 * CS * 4;
 
     struct Ctx {
         T *Qs, *Ks, *As, *Rs;
-        float *cRs, *cLs;  // c_R[k][j] at k*16 + j, c_L[j][k] at j*16 + k
+        float *cRs, *cLs;  // c_R[k][j] at k*CS + j, c_L[j][k] at j*CS + k
         int m, b, lane, g, c16;
         float s_log2e;
     };
@@ -832,12 +906,12 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         const int j = c.c16;
         const bool jv = j < c.b;
         RowFrags<T, D> bf;  // row j of alpha_R[k]; at t = 1 that is Q[k*b + j] = Qs[j][k]
-        bf.load(FIRST ? c.Qs + (j * 16 + k) * LD : c.Rs + (k * 16 + j) * LD, c.g);
+        bf.load(FIRST ? c.Qs + j * BS + k * LD : c.Rs + k * BS + j * LD, c.g);
         float rs = c.s_log2e;
         if constexpr (!FIRST) {
-            if (jv) rs = c.s_log2e / fmaxf(c.cRs[k * 16 + j], kTiny);
+            if (jv) rs = c.s_log2e * fast_rcp(fmaxf(c.cRs[k * CS + j], kTiny));
         }
-        T *Kk = c.Ks + k * 16 * LD;
+        T *Kk = c.Ks + k * BS;
         f32x4 sc;  // lane holds S'[i = 4g + qq][j]
         gemm_scores_rt<T, D, 1>(Kk + c.c16 * LD, &bf, &sc, c.g);
         const float nb = -tiles_max<1, RGB>(&sc, c.b, c.g) * rs;
@@ -853,22 +927,24 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         }
         sum = lanegroup_sum(sum);
         t2 = lanegroup_sum(t2);
-        const float inv = 1.0f / sum;
-        if (c.g == 0 && jv) c.cLs[j * 16 + k] = kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum));
+        const float inv = fast_rcp(sum);
+        if (c.g == 0 && jv) c.cLs[j * CS + k] = kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum));
+        static_assert(NormFirst<1, D>::value, "probabilities normalised before the products, as in RHalf");
+        sc *= inv;
         ProbFrags<T, 1> pf;
         pf.pack(&sc);
         f32x4 out[D / 16];
 #pragma unroll
         for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, 1>(Kk, LD, 16 * vt, pf, c.lane);
-        store_row<T, D>(jv ? c.As + (j * 16 + k) * LD : nullptr, out, inv, c.lane);  // alpha_L[j][k]
+        store_row_lds<T, D>(jv ? c.As + j * BS + k * LD : nullptr, out, c.lane);  // alpha_L[j][k]
         if constexpr (FINAL) {
-            T *Vk = c.Rs + k * 16 * LD;  // alpha_R[k] has been read: stage Vbar[k] in its place
+            T *Vk = c.Rs + k * BS;  // alpha_R[k] has been read: stage Vbar[k] in its place
 #pragma unroll
             for (int h = 0; h < 2; ++h)
                 *reinterpret_cast<u32x4 *>(Vk + ((c.lane >> 3) + 8 * h) * LD + (c.lane & 7) * 8) = vpre[h];
 #pragma unroll
             for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, 1>(Vk, LD, 16 * vt, pf, c.lane);
-            store_row<T, D>(jv ? Kk + j * LD : nullptr, out, inv, c.lane);  // Y[k][j] over Kbar[k]
+            store_row_lds<T, D>(jv ? Kk + j * LD : nullptr, out, c.lane);  // Y[k][j] over Kbar[k]
         }
     }
 
@@ -877,14 +953,14 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
     __device__ static f32x4 l_softmax(const Ctx &c, int j, float &inv)
     {
         RowFrags<T, D> bf;
-        bf.load(c.Qs + (j * 16 + c.c16) * LD, c.g);  // Qbar[j][l]
+        bf.load(c.Qs + j * BS + c.c16 * LD, c.g);  // Qbar[j][l]
         f32x4 acc;
-        gemm_scores_rt<T, D, 1>(c.As + (j * 16 + c.c16) * LD, &bf, &acc, c.g);
+        gemm_scores_rt<T, D, 1>(c.As + j * BS + c.c16 * LD, &bf, &acc, c.g);
         f32x4 sc;
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
             const int kk = 4 * c.g + qq;
-            const float bias = (!RGM || kk < c.m) ? c.cLs[j * 16 + kk] * kLog2e : 0.f;
+            const float bias = (!RGM || kk < c.m) ? c.cLs[j * CS + kk] * kLog2e : 0.f;
             sc[qq] = __builtin_fmaf(acc[qq], c.s_log2e, -bias);
         }
         const float mx = tiles_max<1, RGM>(&sc, c.m, c.g);
@@ -896,7 +972,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             sum += e;
             sc[qq] = e;
         }
-        inv = 1.0f / lanegroup_sum(sum);
+        inv = fast_rcp(lanegroup_sum(sum));
         return sc;
     }
 
@@ -905,31 +981,31 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         const int l = c.c16;
         float inv;
         const f32x4 e = l_softmax(c, j, inv);
-        T *Aj = c.As + j * 16 * LD;  // alpha_L[j] has been read: P[l][k] in its place
+        T *Aj = c.As + j * BS;  // alpha_L[j] has been read: P[l][k] in its place
         const f32x4 pr = l < c.m ? e * inv : f32x4{0.f, 0.f, 0.f, 0.f};  // padded query rows carry no weight
         store4<T>(Aj + l * LD + 4 * c.g, pr);
         ProbFrags<T, 1> pf;  // B operand: P[l-slots][k = lane % 16]
         pf.gather(Aj, LD, 0, c.lane);
         const int k = c.c16;
         const f32x4 cs = gemm_colsum<T, 1>(pf);  // c_R[k][j] = sum_l L[j][k][l]
-        if (c.g == 0 && k < c.m) c.cRs[k * 16 + j] = cs[0];
+        if (c.g == 0 && k < c.m) c.cRs[k * CS + j] = cs[0];
         f32x4 out[D / 16];
 #pragma unroll
-        for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, 1>(c.Qs + j * 16 * LD, LD, 16 * vt, pf, c.lane);
-        store_row<T, D>(k < c.m ? c.Rs + (k * 16 + j) * LD : nullptr, out, 1.0f, c.lane);  // alpha_R[k][j]
+        for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, 1>(c.Qs + j * BS, LD, 16 * vt, pf, c.lane);
+        store_row_lds<T, D>(k < c.m ? c.Rs + k * BS + j * LD : nullptr, out, c.lane);  // alpha_R[k][j]
     }
 
     __device__ static void apply_unit(const Ctx &c, int j, T *out_h)
     {
         const int l = c.c16;
         float inv;
-        const f32x4 e = l_softmax(c, j, inv);
+        const f32x4 e = l_softmax(c, j, inv) * inv;  // normalised first, as in Apply at 16 rows
         ProbFrags<T, 1> pf;
         pf.pack(&e);
-        f32x4 o[D / 16];  // O[l*b + j] = sum_k L[j][k][l] Y[k][j]; Y[k][j] is row k of Ks + j*LD at stride 16*LD
+        f32x4 o[D / 16];  // O[l*b + j] = sum_k L[j][k][l] Y[k][j]; Y[k][j] is row k of Ks + j*LD at stride BS
 #pragma unroll
-        for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, 1>(c.Ks + j * LD, 16 * LD, 16 * vt, pf, c.lane);
-        store_row<T, D>(l < c.m ? out_h + ((int64_t)l * c.b + j) * D : nullptr, o, inv, c.lane);
+        for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, 1>(c.Ks + j * LD, BS, 16 * vt, pf, c.lane);
+        store_row<T, D>(l < c.m ? out_h + ((int64_t)l * c.b + j) * D : nullptr, o, 1.0f, c.lane);
     }
 
     __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int T_, char *lds)
@@ -940,7 +1016,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         c.As = c.Ks + REGION;
         c.Rs = c.As + REGION;
         c.cRs = reinterpret_cast<float *>(c.Rs + REGION);
-        c.cLs = c.cRs + 256;
+        c.cLs = c.cRs + 16 * CS;
         c.m = hd.m;
         c.b = hd.b;
         c.s_log2e = hd.s_log2e;
@@ -974,15 +1050,14 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             vpre[h] = u32x4{0u, 0u, 0u, 0u};
             if (w < m && r < b) vpre[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * D + col);
         }
-        for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) {
-            const int row = idx >> 3, col = (idx & 7) * 8;
-            *reinterpret_cast<u32x4 *>(c.As + row * LD + col) = u32x4{0u, 0u, 0u, 0u};
-        }
+        // chunk idx of two regions: region idx >> 11, block (idx >> 7) & 15, row (idx >> 3) & 15
+        auto chunk = [](T *base, int idx) {
+            return reinterpret_cast<u32x4 *>(base + (idx >> 11) * REGION + ((idx >> 7) & 15) * BS +
+                                             ((idx >> 3) & 15) * LD + (idx & 7) * 8);
+        };
+        for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) *chunk(c.As, idx) = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
-        for (int h = 0; h < PER; ++h) {
-            const int idx = tid + h * 64 * NW;
-            *reinterpret_cast<u32x4 *>(c.Qs + (idx >> 3) * LD + (idx & 7) * 8) = raw[h];
-        }
+        for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
         __syncthreads();
 
         for (int t = 1; t <= T_; ++t) {
