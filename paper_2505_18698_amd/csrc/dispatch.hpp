@@ -126,13 +126,16 @@ int run_half_steps(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, 
 template <typename T, bool RGB, bool RGM> int launch_fused(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
 {
     using U = ma::FusedHead<T, RGB, RGM>;
+    // one workgroup per compute unit (its LDS holds one), each looping over heads
+    const int64_t grid = c.BH < c.num_cus ? c.BH : c.num_cus;
     hd.units = c.BH;
     const ma::Bufs<T> p = typed<T>(B);
+    const int64_t BH = c.BH;
     const int T_ = c.T;
     return L.run(kFused, [&] {
         return launched([&] {
-            hipLaunchKernelGGL((ma::monarch_fused_head<T, RGB, RGM>), dim3((unsigned)c.BH), dim3(64 * U::NW), 0,
-                               L.stream, p, hd, T_);
+            hipLaunchKernelGGL((ma::monarch_fused_head<T, RGB, RGM>), dim3((unsigned)grid), dim3(64 * U::NW), 0,
+                               L.stream, p, hd, BH, T_);
         });
     });
 }

@@ -64,6 +64,7 @@ struct CallDims {
     int64_t BH;
     int m, b, d, T;
     float s_log2e;
+    int num_cus;  // compute units of the device
 };
 
 // Path selection (monarch_attn_set_path): 0 = the fused kernel for small

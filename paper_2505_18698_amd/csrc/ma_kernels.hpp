@@ -1008,7 +1008,46 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         store_row<T, D>(l < c.m ? out_h + ((int64_t)l * c.b + j) * D : nullptr, o, 1.0f, c.lane);
     }
 
-    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int T_, char *lds)
+    static constexpr int PER = 2 * 256 * 8 / (64 * NW);  // 16-byte chunks of Qs and Ks per thread
+
+    // Issue the loads of head bh: Qbar and Kbar chunks (zero where there is no
+    // row) for the LDS regions, and Vbar[w] for wave w's last R half-step.
+    __device__ static void load_head(const Bufs<T> &p, int m, int b, int64_t bh, int tid, u32x4 *raw, u32x4 *vb)
+    {
+        const int64_t hoff = bh * (int64_t)m * b * D;
+        const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
+#pragma unroll
+        for (int h = 0; h < PER; ++h) {
+            const int idx = tid + h * 64 * NW;
+            const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
+            raw[h] = u32x4{0u, 0u, 0u, 0u};
+            if (reg == 0 && blk < b && r < m)
+                raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * D + col);  // Qbar[blk][r]
+            if (reg == 1 && blk < m && r < b)
+                raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * D + col);  // Kbar[blk][r]
+        }
+        const int w = tid >> 6, lane = tid & 63;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int r = (lane >> 3) + 8 * h, col = (lane & 7) * 8;
+            vb[h] = u32x4{0u, 0u, 0u, 0u};
+            if (w < m && r < b) vb[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * D + col);
+        }
+    }
+
+    // 16-byte chunk idx of two consecutive regions: region idx >> 11, block
+    // (idx >> 7) & 15, row (idx >> 3) & 15.
+    __device__ static u32x4 *chunk(T *base, int idx)
+    {
+        return reinterpret_cast<u32x4 *>(base + (idx >> 11) * REGION + ((idx >> 7) & 15) * BS + ((idx >> 3) & 15) * LD +
+                                         (idx & 7) * 8);
+    }
+
+    // Heads blockIdx.x, blockIdx.x + gridDim.x, ... < BH.  The loads of the
+    // next head are issued as soon as the current one is in LDS and land
+    // while it is computed.  As and Rs are zeroed once: every head of a launch
+    // leaves zero in their padding rows (see the units).
+    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t BH, int T_, char *lds)
     {
         Ctx c;
         c.Qs = reinterpret_cast<T *>(lds);
@@ -1025,68 +1064,48 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         c.g = c.lane >> 4;
         c.c16 = c.lane & 15;
         const int m = hd.m, b = hd.b;
-        const int64_t hoff = bh * (int64_t)m * b * D;
-        const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
 
-        // Qs and Ks: 2 regions x 256 rows x 8 chunks of 16 bytes, 4 per thread,
-        // all loads issued before the LDS stores; As and Rs zeroed.
-        constexpr int PER = 2 * 256 * 8 / (64 * NW);
-        u32x4 raw[PER];
-#pragma unroll
-        for (int h = 0; h < PER; ++h) {
-            const int idx = tid + h * 64 * NW;
-            const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
-            raw[h] = u32x4{0u, 0u, 0u, 0u};
-            if (reg == 0 && blk < b && r < m)
-                raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * D + col);  // Qbar[blk][r]
-            if (reg == 1 && blk < m && r < b)
-                raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * D + col);  // Kbar[blk][r]
-        }
-        // Vbar[w] for the last R half-step, held in registers until then
-        u32x4 vpre[2];
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int r = (c.lane >> 3) + 8 * h, col = (c.lane & 7) * 8;
-            vpre[h] = u32x4{0u, 0u, 0u, 0u};
-            if (w < m && r < b) vpre[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * D + col);
-        }
-        // chunk idx of two regions: region idx >> 11, block (idx >> 7) & 15, row (idx >> 3) & 15
-        auto chunk = [](T *base, int idx) {
-            return reinterpret_cast<u32x4 *>(base + (idx >> 11) * REGION + ((idx >> 7) & 15) * BS +
-                                             ((idx >> 3) & 15) * LD + (idx & 7) * 8);
-        };
+        u32x4 raw[PER], vcur[2], vnext[2];
+        int64_t bh = blockIdx.x;
+        load_head(p, m, b, bh, tid, raw, vcur);
         for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) *chunk(c.As, idx) = u32x4{0u, 0u, 0u, 0u};
+        for (; bh < BH; bh += gridDim.x) {
 #pragma unroll
-        for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
-        __syncthreads();
+            for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
+            __syncthreads();
+            if (bh + gridDim.x < BH) load_head(p, m, b, bh + gridDim.x, tid, raw, vnext);
 
-        for (int t = 1; t <= T_; ++t) {
-            const bool first = t == 1, last = t == T_;
-            if (w < m) {
-                if (first && last)
-                    r_unit<true, true>(c, w, vpre);
-                else if (first)
-                    r_unit<true, false>(c, w, vpre);
-                else if (last)
-                    r_unit<false, true>(c, w, vpre);
-                else
-                    r_unit<false, false>(c, w, vpre);
+            for (int t = 1; t <= T_; ++t) {
+                const bool first = t == 1, last = t == T_;
+                if (w < m) {
+                    if (first && last)
+                        r_unit<true, true>(c, w, vcur);
+                    else if (first)
+                        r_unit<true, false>(c, w, vcur);
+                    else if (last)
+                        r_unit<false, true>(c, w, vcur);
+                    else
+                        r_unit<false, false>(c, w, vcur);
+                }
+                __syncthreads();
+                if (last) break;
+                if (w < b) l_unit(c, w);
+                __syncthreads();
             }
-            __syncthreads();
-            if (last) break;
-            if (w < b) l_unit(c, w);
-            __syncthreads();
+            if (w < b) apply_unit(c, w, p.out + bh * (int64_t)m * b * D);
+            vcur[0] = vnext[0];
+            vcur[1] = vnext[1];
+            __syncthreads();  // the apply has read Qs, As and Ks
         }
-        if (w < b) apply_unit(c, w, p.out + hoff);
     }
 };
 
 template <typename T, bool RGB, bool RGM>
-__global__ __launch_bounds__(1024) void monarch_fused_head(Bufs<T> p, HeadDims hd, int T_)
+__global__ __launch_bounds__(1024) void monarch_fused_head(Bufs<T> p, HeadDims hd, int64_t BH, int T_)
 {
     using U = FusedHead<T, RGB, RGM>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
-    U::run(p, hd, blockIdx.x, T_, lds);
+    U::run(p, hd, BH, T_, lds);
 }
 
 }  // namespace ma

@@ -63,6 +63,7 @@ size_t workspace_bytes(int64_t BH, int64_t N, int64_t d, int32_t dtype)
 struct Device {
     void *ws = nullptr;
     size_t ws_bytes = 0;
+    int num_cus = 0;  // 0: not queried yet
 };
 
 constexpr int kMaxDevices = 64;
@@ -183,9 +184,21 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
     const size_t st = align_up((size_t)BH * N * d * elem_bytes(dtype));
     const size_t cs = align_up((size_t)BH * N * sizeof(float));
     CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
+    int num_cus = 0;
+    {
+        std::lock_guard<std::mutex> lock(g_dev_mutex);
+        Device &D = g_dev[dev];
+        if (D.num_cus == 0) {
+            int n = 0;
+            if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+                return fail(MA_EHIP, "querying the compute unit count failed");
+            D.num_cus = n;
+        }
+        num_cus = D.num_cus;
+    }
     if (!uses_fused(path, dtype, d, m, b)) {  // the fused kernel keeps its states in LDS
-        int dev = 0;
-        if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
         const size_t need = workspace_bytes(BH, N, d, dtype);
         std::lock_guard<std::mutex> lock(g_dev_mutex);
         Device &D = g_dev[dev];
@@ -211,7 +224,7 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
         bufs.cR = (float *)(base + 3 * st);
         bufs.cL = (float *)(base + 3 * st + cs);
     }
-    CallDims dims{BH, (int)m, (int)b, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d))};
+    CallDims dims{BH, (int)m, (int)b, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
 
     std::unique_lock<std::mutex> tlock(g_timing_mutex);
     Launcher L{(hipStream_t)stream, g_timing.enabled};

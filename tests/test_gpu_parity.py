@@ -219,14 +219,26 @@ def test_fused_path_unsupported_shape_is_rejected(lib):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
-@pytest.mark.parametrize("m,b,T", [(14, 14, 2), (16, 16, 1), (16, 16, 3), (5, 16, 2), (16, 3, 2), (1, 1, 2)])
-def test_fused_and_half_steps_agree_bitwise(lib, dtype, m, b, T):
+@pytest.mark.parametrize(
+    "B,H,m,b,T",
+    [
+        (3, 5, 14, 14, 2),
+        (3, 5, 16, 16, 1),
+        (3, 5, 16, 16, 3),
+        (3, 5, 5, 16, 2),
+        (3, 5, 16, 3, 2),
+        (3, 5, 1, 1, 2),
+        (40, 12, 14, 14, 3),   # more heads than compute units: workgroups loop over heads
+        (33, 17, 7, 13, 2),
+    ],
+)
+def test_fused_and_half_steps_agree_bitwise(lib, dtype, B, H, m, b, T):
     """The fused kernel runs the unit arithmetic of the half-step kernels at
     16 rows on the same element-type states, so both paths give the same bits."""
     import torch
 
     td = _torch_dtype(dtype)
-    q, k, v = si.random_qkv(3, 5, m * b, 64, dtype, seed=100 + m * 17 + b, scale=1.5)
+    q, k, v = si.random_qkv(B, H, m * b, 64, dtype, seed=100 + m * 17 + b, scale=1.5)
     t = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
 
     def run(path):
