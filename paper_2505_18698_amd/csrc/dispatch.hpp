@@ -11,7 +11,9 @@
 // per head, with the states in LDS.
 #pragma once
 
+#include <mutex>
 #include <type_traits>
+#include <unordered_map>
 
 #include "host_common.hpp"
 #include "ma_kernels.hpp"
@@ -30,54 +32,89 @@ template <typename F> int launched(F &&f)
     return MA_OK;
 }
 
-template <typename T, int NB, int D, bool RG>
-int launch_r(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, bool first, bool final_)
+// Workgroups of `kern` (at `threads` threads) resident on one compute unit,
+// queried once per kernel.
+inline int resident_per_cu(const void *kern, int threads)
+{
+    static std::mutex mu;
+    static std::unordered_map<const void *, int> cache;
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = cache.find(kern);
+    if (it != cache.end()) return it->second;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, threads, 0) != hipSuccess || n < 1) {
+        (void)hipGetLastError();
+        n = 1;
+    }
+    cache.emplace(kern, n);
+    return n;
+}
+
+// Grid of a half-step launch: every unit once, at most one workgroup per
+// resident slot (the workgroups loop over units).
+inline dim3 unit_grid(const void *kern, int threads, int64_t units, int num_cus)
+{
+    const int64_t cap = (int64_t)resident_per_cu(kern, threads) * num_cus;
+    return dim3((unsigned)(units < cap ? units : cap));
+}
+
+template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RG>
+int launch_r1(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int num_cus)
 {
     constexpr int W = ma::Split<NB / 16>::W;
+    auto kern = ma::r_half_step<T, NB, D, FIRST, FINAL, RG>;
     hd.units = BH * hd.m;
-    const dim3 grid((unsigned)hd.units), block(64 * W);
+    const dim3 grid = unit_grid((const void *)kern, 64 * W, hd.units, num_cus), block(64 * W);
     const ma::Bufs<T> p = typed<T>(B);
-    const int kind = final_ ? kRFinal : kR;
-    if (first && final_)
-        return L.run(kind, [&] { return launched([&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, true, true, RG>), grid, block, 0, L.stream, p, hd); }); });
-    if (first)
-        return L.run(kind, [&] { return launched([&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, true, false, RG>), grid, block, 0, L.stream, p, hd); }); });
-    if (final_)
-        return L.run(kind, [&] { return launched([&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, false, true, RG>), grid, block, 0, L.stream, p, hd); }); });
-    return L.run(kind, [&] { return launched([&] { hipLaunchKernelGGL((ma::r_half_step<T, NB, D, false, false, RG>), grid, block, 0, L.stream, p, hd); }); });
+    return L.run(FINAL ? kRFinal : kR,
+                 [&] { return launched([&] { hipLaunchKernelGGL(kern, grid, block, 0, L.stream, p, hd); }); });
+}
+
+template <typename T, int NB, int D, bool RG>
+int launch_r(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int num_cus, bool first, bool final_)
+{
+    if (first && final_) return launch_r1<T, NB, D, true, true, RG>(L, B, hd, BH, num_cus);
+    if (first) return launch_r1<T, NB, D, true, false, RG>(L, B, hd, BH, num_cus);
+    if (final_) return launch_r1<T, NB, D, false, true, RG>(L, B, hd, BH, num_cus);
+    return launch_r1<T, NB, D, false, false, RG>(L, B, hd, BH, num_cus);
 }
 
 template <typename T, int NM, int D, bool RG>
-int launch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, bool apply)
+int launch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int num_cus, bool apply)
 {
     constexpr int W = ma::Split<NM / 16>::W;
     hd.units = BH * hd.b;
-    const dim3 grid((unsigned)hd.units), block(64 * W);
     const ma::Bufs<T> p = typed<T>(B);
-    if (apply)
-        return L.run(kApply, [&] { return launched([&] { hipLaunchKernelGGL((ma::monarch_apply<T, NM, D, RG>), grid, block, 0, L.stream, p, hd); }); });
-    return L.run(kL, [&] { return launched([&] { hipLaunchKernelGGL((ma::l_half_step<T, NM, D, RG>), grid, block, 0, L.stream, p, hd); }); });
+    const dim3 block(64 * W);
+    if (apply) {
+        auto kern = ma::monarch_apply<T, NM, D, RG>;
+        const dim3 grid = unit_grid((const void *)kern, 64 * W, hd.units, num_cus);
+        return L.run(kApply, [&] { return launched([&] { hipLaunchKernelGGL(kern, grid, block, 0, L.stream, p, hd); }); });
+    }
+    auto kern = ma::l_half_step<T, NM, D, RG>;
+    const dim3 grid = unit_grid((const void *)kern, 64 * W, hd.units, num_cus);
+    return L.run(kL, [&] { return launched([&] { hipLaunchKernelGGL(kern, grid, block, 0, L.stream, p, hd); }); });
 }
 
 template <typename T, int D, int NB>
-int dispatch_r(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, bool first, bool final_)
+int dispatch_r(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int nc, bool first, bool final_)
 {
     if constexpr (std::is_same<T, float>::value && NB * D > 8192) {
         return fail(MA_EUNSUPPORTED, "fp32 tile too large");
     } else {
-        return hd.b != NB ? launch_r<T, NB, D, true>(L, B, hd, BH, first, final_)
-                          : launch_r<T, NB, D, false>(L, B, hd, BH, first, final_);
+        return hd.b != NB ? launch_r<T, NB, D, true>(L, B, hd, BH, nc, first, final_)
+                          : launch_r<T, NB, D, false>(L, B, hd, BH, nc, first, final_);
     }
 }
 
 template <typename T, int D, int NM>
-int dispatch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, bool apply)
+int dispatch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int nc, bool apply)
 {
     if constexpr (std::is_same<T, float>::value && NM * D > 8192) {
         return fail(MA_EUNSUPPORTED, "fp32 tile too large");
     } else {
-        return hd.m != NM ? launch_l<T, NM, D, true>(L, B, hd, BH, apply)
-                          : launch_l<T, NM, D, false>(L, B, hd, BH, apply);
+        return hd.m != NM ? launch_l<T, NM, D, true>(L, B, hd, BH, nc, apply)
+                          : launch_l<T, NM, D, false>(L, B, hd, BH, nc, apply);
     }
 }
 
@@ -89,35 +126,35 @@ inline int tile_rows(int n)
 }
 
 template <typename T, int D>
-int r_step(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, bool first, bool final_)
+int r_step(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int nc, bool first, bool final_)
 {
     switch (tile_rows(hd.b)) {
-    case 16: return dispatch_r<T, D, 16>(L, B, hd, BH, first, final_);
-    case 32: return dispatch_r<T, D, 32>(L, B, hd, BH, first, final_);
-    case 64: return dispatch_r<T, D, 64>(L, B, hd, BH, first, final_);
-    default: return dispatch_r<T, D, 128>(L, B, hd, BH, first, final_);
+    case 16: return dispatch_r<T, D, 16>(L, B, hd, BH, nc, first, final_);
+    case 32: return dispatch_r<T, D, 32>(L, B, hd, BH, nc, first, final_);
+    case 64: return dispatch_r<T, D, 64>(L, B, hd, BH, nc, first, final_);
+    default: return dispatch_r<T, D, 128>(L, B, hd, BH, nc, first, final_);
     }
 }
 
 template <typename T, int D>
-int l_step(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, bool apply)
+int l_step(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int nc, bool apply)
 {
     switch (tile_rows(hd.m)) {
-    case 16: return dispatch_l<T, D, 16>(L, B, hd, BH, apply);
-    case 32: return dispatch_l<T, D, 32>(L, B, hd, BH, apply);
-    case 64: return dispatch_l<T, D, 64>(L, B, hd, BH, apply);
-    default: return dispatch_l<T, D, 128>(L, B, hd, BH, apply);
+    case 16: return dispatch_l<T, D, 16>(L, B, hd, BH, nc, apply);
+    case 32: return dispatch_l<T, D, 32>(L, B, hd, BH, nc, apply);
+    case 64: return dispatch_l<T, D, 64>(L, B, hd, BH, nc, apply);
+    default: return dispatch_l<T, D, 128>(L, B, hd, BH, nc, apply);
     }
 }
 
 template <typename T, int D>
-int run_half_steps(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int T_)
+int run_half_steps(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
 {
     int rc;
-    for (int t = 1; t <= T_; ++t) {
-        const bool first = (t == 1), last = (t == T_);
-        if ((rc = r_step<T, D>(L, B, hd, BH, first, last)) != MA_OK) return rc;
-        if ((rc = l_step<T, D>(L, B, hd, BH, last)) != MA_OK) return rc;
+    for (int t = 1; t <= c.T; ++t) {
+        const bool first = (t == 1), last = (t == c.T);
+        if ((rc = r_step<T, D>(L, B, hd, c.BH, c.num_cus, first, last)) != MA_OK) return rc;
+        if ((rc = l_step<T, D>(L, B, hd, c.BH, c.num_cus, last)) != MA_OK) return rc;
     }
     return MA_OK;
 }
@@ -160,7 +197,7 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
     if (path == kFusedHead && !fused_applies(dtype, c.d, c.m, c.b))
         return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d = 64 and m, b <= 16");
     if (uses_fused(path, dtype, c.d, c.m, c.b)) return run_fused<T>(L, B, hd, c);
-    return c.d == 64 ? run_half_steps<T, 64>(L, B, hd, c.BH, c.T) : run_half_steps<T, 128>(L, B, hd, c.BH, c.T);
+    return c.d == 64 ? run_half_steps<T, 64>(L, B, hd, c) : run_half_steps<T, 128>(L, B, hd, c);
 }
 
 }  // namespace ma_host

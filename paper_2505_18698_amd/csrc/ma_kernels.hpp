@@ -161,20 +161,33 @@ template <typename T> __device__ inline void store4(T *dst, f32x4 v)
     }
 }
 
-// Cooperative load of a [NR][D] tile into row-major LDS (stride LDR); valid
-// rows r < `valid` start at rowptr(r), the others are zero.
-template <typename T, int NR, int D, int LDR, typename RowPtr>
-__device__ inline void load_tile(RowPtr rowptr, int valid, T *sRow, int tid, int nthreads)
-{
-    constexpr int V = 16 / (int)sizeof(T);
-    constexpr int CPR = D / V;
-    for (int idx = tid; idx < NR * CPR; idx += nthreads) {
-        const int r = idx / CPR, c = (idx % CPR) * V;
-        u32x4 raw = {0u, 0u, 0u, 0u};
-        if (r < valid) raw = *reinterpret_cast<const u32x4 *>(rowptr(r) + c);
-        *reinterpret_cast<u32x4 *>(sRow + r * LDR + c) = raw;
+// A [NR][D] tile split into 16-byte chunks over NTH threads (chunk idx =
+// tid + h * NTH is row idx / CPR), fetched from global memory into registers
+// and later staged into a row-major LDS tile.  Rows r >= `valid` are zero.
+template <typename T, int NR, int D, int NTH> struct TileChunks {
+    static constexpr int V = 16 / (int)sizeof(T), CPR = D / V, CH = NR * CPR / NTH;
+    static_assert(NR * CPR % NTH == 0, "whole chunks per thread");
+    u32x4 c[CH];
+
+    template <typename RowPtr> __device__ inline void fetch(RowPtr rowptr, int valid, int tid)
+    {
+#pragma unroll
+        for (int h = 0; h < CH; ++h) {
+            const int idx = tid + h * NTH, r = idx / CPR, col = (idx % CPR) * V;
+            c[h] = u32x4{0u, 0u, 0u, 0u};
+            if (r < valid) c[h] = *reinterpret_cast<const u32x4 *>(rowptr(r) + col);
+        }
     }
-}
+
+    template <int LDR> __device__ inline void stage(T *sRow, int tid) const
+    {
+#pragma unroll
+        for (int h = 0; h < CH; ++h) {
+            const int idx = tid + h * NTH, r = idx / CPR, col = (idx % CPR) * V;
+            *reinterpret_cast<u32x4 *>(sRow + r * LDR + col) = c[h];
+        }
+    }
+};
 
 // Lane 16g + c receives X[x0 + 4g + q][c0 + c], q = 0..3, from the row-major
 // LDS matrix X (row stride ld elements): the MFMA operand of a product that
@@ -400,18 +413,6 @@ __device__ inline void gemm_aggregate_rt(const T *X, int ld, int c0, const ProbF
     }
 }
 
-// Work unit of a block on an 8-XCD part: blocks are dispatched to XCDs
-// round-robin (block i runs on XCD i % 8), so unit = (i % 8) * (U / 8) + i / 8
-// gives every XCD a contiguous range of units (whole heads when U/8 is a
-// multiple of the units per head).  Falls back to i when U % 8 != 0.
-#ifndef MA_XCD_REMAP
-#define MA_XCD_REMAP 0
-#endif
-__device__ inline int64_t xcd_unit(int64_t i, int64_t U)
-{
-    return (MA_XCD_REMAP && U % 8 == 0) ? (i % 8) * (U / 8) + i / 8 : i;
-}
-
 // Maximum over the softmax index of transposed score tiles (lane holds index
 // 16t + 4g + q of row lane%16): in-lane, then across the four lane groups.
 // With RAGGED, entries at index >= n are left out.
@@ -508,10 +509,10 @@ template <typename T> struct Bufs {
     float *cR, *cL;
 };
 
-// The work of one unit of each half-step, done by the first W waves of a
-// workgroup of `nthreads` threads (all threads take part in tile loads and
-// barriers).  RAGGED: the softmax index range (b for R, m for L) is shorter
-// than the padded tile.
+// The work of one unit of each half-step, done by a workgroup of W waves in
+// three parts: fetch() issues its global loads into registers, stage() moves
+// the tiles into LDS, and compute() (after a barrier) does the rest.  RAGGED:
+// the softmax index range (b for R, m for L) is shorter than the padded tile.
 
 // ---------------------------------------------------------------------------------------
 // R half-step for (head bh, key block k); each wave owns RT tiles of 16 rows j.
@@ -519,13 +520,50 @@ template <typename T> struct Bufs {
 // c_R = 1.  FINAL: also Y.
 // ---------------------------------------------------------------------------------------
 template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct RHalf {
-    static constexpr int NT = NB / 16, RT = Split<NT>::RT, W = Split<NT>::W;
+    static constexpr int NT = NB / 16, RT = Split<NT>::RT, W = Split<NT>::W, NTH = 64 * W;
     static constexpr bool NF = NormFirst<NT, D>::value;
     static constexpr int LDK = Ld<T, D>::row;
     static constexpr int LDS_BYTES = (FINAL ? 2 : 1) * NB * LDK * (int)sizeof(T);
 
-    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, char *lds, int tid,
-                               int nthreads)
+    // What a unit reads from global memory, held in registers until staged.
+    struct Regs {
+        TileChunks<T, NB, D, NTH> kt, vt;  // Kbar[k]; Vbar[k] (FINAL)
+        RowFrags<T, D> bf[RT];             // rows j of alpha_R[k] (of Q when FIRST)
+        float cr[RT];                      // c_R[k][j] (not FIRST)
+    };
+
+    __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, int tid, Regs &gr)
+    {
+        const int m = hd.m, b = hd.b;
+        const int64_t N = (int64_t)m * b, hoff = bh * N * D;
+        const int lane = tid & 63, wave = tid >> 6;
+        const T *kblk = p.k + hoff + (int64_t)k * b * D;
+        gr.kt.fetch([=](int r) { return kblk + (int64_t)r * D; }, b, tid);
+        if constexpr (FINAL) {
+            const T *vblk = p.v + hoff + (int64_t)k * b * D;
+            gr.vt.fetch([=](int r) { return vblk + (int64_t)r * D; }, b, tid);
+        }
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            const int j = (wave * RT + r) * 16 + (lane & 15);
+            gr.bf[r].load(j < b ? (FIRST ? p.q : p.aR) + hoff + ((int64_t)k * b + j) * D : nullptr, lane >> 4);
+            gr.cr[r] = 1.0f;
+            if constexpr (!FIRST) {
+                if (j < b) gr.cr[r] = p.cR[bh * N + (int64_t)j * m + k];
+            }
+        }
+    }
+
+    __device__ static void stage(const Regs &gr, char *lds, int tid)
+    {
+        T *Ks = reinterpret_cast<T *>(lds);
+        gr.kt.template stage<LDK>(Ks, tid);
+        if constexpr (FINAL) gr.vt.template stage<LDK>(Ks + NB * LDK, tid);
+    }
+
+    // After stage() and a barrier.
+    __device__ static void compute(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, const Regs &gr,
+                                   char *lds, int tid)
     {
         T *Ks = reinterpret_cast<T *>(lds);
         T *Vs = Ks + NB * LDK;
@@ -534,36 +572,19 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
-        const bool active = wave < W;
-
-        const T *kblk = p.k + hoff + (int64_t)k * b * D;
-        load_tile<T, NB, D, LDK>([=](int r) { return kblk + (int64_t)r * D; }, b, Ks, tid, nthreads);
-        if constexpr (FINAL) {
-            const T *vblk = p.v + hoff + (int64_t)k * b * D;
-            load_tile<T, NB, D, LDK>([=](int r) { return vblk + (int64_t)r * D; }, b, Vs, tid, nthreads);
-        }
-
         int jr[RT];
-        RowFrags<T, D> bf[RT];
         float rscale[RT];
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             jr[r] = (wave * RT + r) * 16 + c16;
-            const bool jvalid = active && jr[r] < b;
-            bf[r].load(jvalid ? (FIRST ? p.q : p.aR) + hoff + ((int64_t)k * b + jr[r]) * D : nullptr, g);
-            rscale[r] = hd.s_log2e;
-            if constexpr (!FIRST) {
-                if (jvalid) rscale[r] = hd.s_log2e * fast_rcp(fmaxf(p.cR[bh * N + (int64_t)jr[r] * m + k], kTiny));
-            }
+            rscale[r] = (FIRST || jr[r] >= b) ? hd.s_log2e : hd.s_log2e * fast_rcp(fmaxf(gr.cr[r], kTiny));
         }
-        __syncthreads();
-        if (!active) return;
 
         f32x4 sc[RT][NT];  // lane holds S'[i = 16t + 4g + qq][j] of row tile r
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             f32x4 acc[RT];
-            gemm_scores_rt<T, D, RT>(Ks + (16 * t + c16) * LDK, bf, acc, g);
+            gemm_scores_rt<T, D, RT>(Ks + (16 * t + c16) * LDK, gr.bf, acc, g);
 #pragma unroll
             for (int r = 0; r < RT; ++r) sc[r][t] = acc[r];
         }
@@ -634,14 +655,40 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
 // tiles of 16 key-block columns k (c_R and alpha_R).
 // ---------------------------------------------------------------------------------------
 template <typename T, int NM, int D, bool RAGGED> struct LHalf {
-    static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
+    static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W, NTH = 64 * W;
     static constexpr int LDQ = Ld<T, D>::row, LDP = Ld<T, NM>::row;
     static constexpr int A_ELEMS = NM * LDQ, P_ELEMS = NM * LDP;
     static constexpr int AP_ELEMS = A_ELEMS > P_ELEMS ? A_ELEMS : P_ELEMS;
     static constexpr int LDS_BYTES = (NM * LDQ + AP_ELEMS) * (int)sizeof(T) + NM * 4;
 
-    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, char *lds, int tid,
-                               int nthreads)
+    struct Regs {
+        TileChunks<T, NM, D, NTH> qt, at;  // Qbar[j] (rows l), alpha_L[j] (rows k)
+        float cl;                          // c_L[k = tid][j]
+    };
+
+    __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, int tid, Regs &gr)
+    {
+        const int m = hd.m, b = hd.b;
+        const int64_t N = (int64_t)m * b, hoff = bh * N * D;
+        const T *qh = p.q + hoff;
+        const T *al = p.aL + hoff + (int64_t)j * m * D;
+        gr.qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * D; }, m, tid);
+        gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
+        gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
+    }
+
+    __device__ static void stage(const Regs &gr, char *lds, int tid)
+    {
+        T *Qs = reinterpret_cast<T *>(lds);
+        T *APs = Qs + NM * LDQ;
+        gr.qt.template stage<LDQ>(Qs, tid);
+        gr.at.template stage<LDQ>(APs, tid);
+        if (tid < NM) reinterpret_cast<float *>(APs + AP_ELEMS)[tid] = gr.cl * kLog2e;
+    }
+
+    // After stage() and a barrier.
+    __device__ static void compute(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, const Regs &, char *lds,
+                                   int tid)
     {
         T *Qs = reinterpret_cast<T *>(lds);
         T *APs = Qs + NM * LDQ;  // alpha_L, then P
@@ -651,73 +698,59 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
-        const bool active = wave < W;
-
-        const T *qh = p.q + hoff;
-        const T *al = p.aL + hoff + (int64_t)j * m * D;
-        load_tile<T, NM, D, LDQ>([=](int l) { return qh + ((int64_t)l * b + j) * D; }, m, Qs, tid, nthreads);
-        load_tile<T, NM, D, LDQ>([=](int kk) { return al + (int64_t)kk * D; }, m, APs, tid, nthreads);
-        for (int kk = tid; kk < NM; kk += nthreads)
-            cLs[kk] = kk < m ? p.cL[bh * N + (int64_t)kk * b + j] * kLog2e : 0.f;
-        __syncthreads();
 
         // scores and softmax over k for the query rows of this wave
         int lr[RT];
         float inv[RT];
         f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
-        if (active) {
-            RowFrags<T, D> bf[RT];
+        RowFrags<T, D> bf[RT];
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            lr[r] = (wave * RT + r) * 16 + c16;
+#pragma unroll
+            for (int c = 0; c < D / Mma<T>::KC; ++c)
+                bf[r].f[c] = *reinterpret_cast<const typename Mma<T>::frag *>(Qs + lr[r] * LDQ + c * Mma<T>::KC +
+                                                                              g * Mma<T>::KPL);
+        }
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            f32x4 acc[RT];
+            gemm_scores_rt<T, D, RT>(APs + (16 * t + c16) * LDQ, bf, acc, g);
+            const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
-                lr[r] = (wave * RT + r) * 16 + c16;
 #pragma unroll
-                for (int c = 0; c < D / Mma<T>::KC; ++c)
-                    bf[r].f[c] = *reinterpret_cast<const typename Mma<T>::frag *>(Qs + lr[r] * LDQ + c * Mma<T>::KC +
-                                                                                  g * Mma<T>::KPL);
+                for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
             }
+        }
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
+            float sum = 0.f;
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
-                f32x4 acc[RT];
-                gemm_scores_rt<T, D, RT>(APs + (16 * t + c16) * LDQ, bf, acc, g);
-                const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
 #pragma unroll
-                for (int r = 0; r < RT; ++r) {
-#pragma unroll
-                    for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
+                for (int qq = 0; qq < 4; ++qq) {
+                    float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
+                    if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
+                    sum += e;
+                    sc[r][t][qq] = e;
                 }
             }
-#pragma unroll
-            for (int r = 0; r < RT; ++r) {
-                const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
-                float sum = 0.f;
-#pragma unroll
-                for (int t = 0; t < NT; ++t) {
-#pragma unroll
-                    for (int qq = 0; qq < 4; ++qq) {
-                        float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
-                        if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
-                        sum += e;
-                        sc[r][t][qq] = e;
-                    }
-                }
-                sum = lanegroup_sum(sum);
-                inv[r] = (lr[r] < m) ? fast_rcp(sum) : 0.f;  // padded query rows carry no weight
-            }
+            sum = lanegroup_sum(sum);
+            inv[r] = (lr[r] < m) ? fast_rcp(sum) : 0.f;  // padded query rows carry no weight
         }
         __syncthreads();  // every wave is done reading alpha_L
 
         // P[l][k] (row-major, k contiguous) into the alpha_L space
         using PT = typename std::conditional<std::is_same<T, float>::value, float, T>::type;
         PT *Ps = reinterpret_cast<PT *>(APs);
-        if (active) {
 #pragma unroll
-            for (int r = 0; r < RT; ++r) {
+        for (int r = 0; r < RT; ++r) {
 #pragma unroll
-                for (int t = 0; t < NT; ++t) store4<PT>(Ps + lr[r] * LDP + 16 * t + 4 * g, sc[r][t] * inv[r]);
-            }
+            for (int t = 0; t < NT; ++t) store4<PT>(Ps + lr[r] * LDP + 16 * t + 4 * g, sc[r][t] * inv[r]);
         }
         __syncthreads();
-        if (!active) return;
 
         // wave w: key-block columns k in tiles wave*RT + r
         int kr[RT];
@@ -748,13 +781,46 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
 // for (head bh, class j); each wave owns RT tiles of 16 query rows l.
 // ---------------------------------------------------------------------------------------
 template <typename T, int NM, int D, bool RAGGED> struct Apply {
-    static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W;
+    static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W, NTH = 64 * W;
     static constexpr bool NF = NormFirst<NT, D>::value;
     static constexpr int LDK = Ld<T, D>::row;
     static constexpr int LDS_BYTES = 2 * NM * LDK * (int)sizeof(T) + NM * 4;
 
-    __device__ static void run(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, char *lds, int tid,
-                               int nthreads)
+    struct Regs {
+        TileChunks<T, NM, D, NTH> at, yt;  // alpha_L[j], Y[j] (rows k)
+        float cl;                          // c_L[k = tid][j]
+        RowFrags<T, D> bf[RT];             // Qbar[j] rows l
+    };
+
+    __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, int tid, Regs &gr)
+    {
+        const int m = hd.m, b = hd.b;
+        const int64_t N = (int64_t)m * b, hoff = bh * N * D;
+        const int lane = tid & 63, wave = tid >> 6;
+        const T *al = p.aL + hoff + (int64_t)j * m * D;
+        const T *yj = p.Y + hoff + (int64_t)j * m * D;
+        gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
+        gr.yt.fetch([=](int kk) { return yj + (int64_t)kk * D; }, m, tid);
+        gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
+#pragma unroll
+        for (int r = 0; r < RT; ++r) {
+            const int l = (wave * RT + r) * 16 + (lane & 15);
+            gr.bf[r].load(l < m ? p.q + hoff + ((int64_t)l * b + j) * D : nullptr, lane >> 4);  // Qbar[j][l]
+        }
+    }
+
+    __device__ static void stage(const Regs &gr, char *lds, int tid)
+    {
+        T *As = reinterpret_cast<T *>(lds);
+        T *Ys = As + NM * LDK;
+        gr.at.template stage<LDK>(As, tid);
+        gr.yt.template stage<LDK>(Ys, tid);
+        if (tid < NM) reinterpret_cast<float *>(Ys + NM * LDK)[tid] = gr.cl * kLog2e;
+    }
+
+    // After stage() and a barrier.
+    __device__ static void compute(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, const Regs &gr,
+                                   char *lds, int tid)
     {
         T *As = reinterpret_cast<T *>(lds);
         T *Ys = As + NM * LDK;
@@ -764,30 +830,15 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
-        const bool active = wave < W;
-
-        const T *al = p.aL + hoff + (int64_t)j * m * D;
-        const T *yj = p.Y + hoff + (int64_t)j * m * D;
-        load_tile<T, NM, D, LDK>([=](int kk) { return al + (int64_t)kk * D; }, m, As, tid, nthreads);
-        load_tile<T, NM, D, LDK>([=](int kk) { return yj + (int64_t)kk * D; }, m, Ys, tid, nthreads);
-        for (int kk = tid; kk < NM; kk += nthreads)
-            cLs[kk] = kk < m ? p.cL[bh * N + (int64_t)kk * b + j] * kLog2e : 0.f;
-
         int lr[RT];
-        RowFrags<T, D> bf[RT];
 #pragma unroll
-        for (int r = 0; r < RT; ++r) {
-            lr[r] = (wave * RT + r) * 16 + c16;
-            bf[r].load(active && lr[r] < m ? p.q + hoff + ((int64_t)lr[r] * b + j) * D : nullptr, g);  // Qbar[j][l]
-        }
-        __syncthreads();
-        if (!active) return;
+        for (int r = 0; r < RT; ++r) lr[r] = (wave * RT + r) * 16 + c16;
 
         f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             f32x4 acc[RT];
-            gemm_scores_rt<T, D, RT>(As + (16 * t + c16) * LDK, bf, acc, g);
+            gemm_scores_rt<T, D, RT>(As + (16 * t + c16) * LDK, gr.bf, acc, g);
             const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
@@ -834,15 +885,37 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
 };
 
 // ---------------------------------------------------------------------------------------
-// One launch per half-step: one workgroup per unit.
+// One launch per half-step.  The grid holds at most as many workgroups as
+// are resident at once; workgroup i takes units i, i + gridDim.x, ... and
+// issues the global loads of its next unit as soon as the current one is in
+// LDS, so that they land while it computes.  `per` is the number of units
+// per head (m for R, b for L).
 // ---------------------------------------------------------------------------------------
+template <typename U, typename T> __device__ inline void run_units(const Bufs<T> &p, const HeadDims &hd, int per, char *lds)
+{
+    const int tid = threadIdx.x;
+    int64_t u = blockIdx.x;
+    typename U::Regs cur, nxt;
+    U::fetch(p, hd, u / per, (int)(u % per), tid, cur);
+    while (true) {
+        U::stage(cur, lds, tid);
+        __syncthreads();
+        const int64_t un = u + gridDim.x;
+        if (un < hd.units) U::fetch(p, hd, un / per, (int)(un % per), tid, nxt);
+        U::compute(p, hd, u / per, (int)(u % per), cur, lds, tid);
+        if (un >= hd.units) break;
+        __syncthreads();  // LDS is restaged next
+        cur = nxt;
+        u = un;
+    }
+}
+
 template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED>
 __global__ __launch_bounds__(64 * Split<NB / 16>::W) void r_half_step(Bufs<T> p, HeadDims hd)
 {
     using U = RHalf<T, NB, D, FIRST, FINAL, RAGGED>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
-    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
-    U::run(p, hd, unit / hd.m, (int)(unit % hd.m), lds, threadIdx.x, 64 * U::W);
+    run_units<U>(p, hd, hd.m, lds);
 }
 
 template <typename T, int NM, int D, bool RAGGED>
@@ -850,8 +923,7 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) void l_half_step(Bufs<T> p,
 {
     using U = LHalf<T, NM, D, RAGGED>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
-    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
-    U::run(p, hd, unit / hd.b, (int)(unit % hd.b), lds, threadIdx.x, 64 * U::W);
+    run_units<U>(p, hd, hd.b, lds);
 }
 
 template <typename T, int NM, int D, bool RAGGED>
@@ -859,8 +931,7 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> 
 {
     using U = Apply<T, NM, D, RAGGED>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
-    const int64_t unit = xcd_unit(blockIdx.x, hd.units);
-    U::run(p, hd, unit / hd.b, (int)(unit % hd.b), lds, threadIdx.x, 64 * U::W);
+    run_units<U>(p, hd, hd.b, lds);
 }
 
 // ---------------------------------------------------------------------------------------
