@@ -5,7 +5,8 @@ One step = one monarch_attn_fwd call: the whole forward pass (every R and L
 half-step, the Monarch product and the store of O) over one batch of
 synthetic Q, K, V already resident in HBM.  The headline workload is the
 long-sequence speed point (B=1, H=16, N=16384 = 128 x 128, d=64, bf16, T=2);
-the medium point (N=4096 = 64 x 64, T=1) is reported alongside in "also".
+the medium point (N=4096 = 64 x 64, T=1) and ViT-B/16 (384 heads, N=196 = 14 x 14,
+T=2, the one-workgroup-per-head kernel) are reported alongside in "also".
 
 Timed regions (HIP events on the stream the library launches on):
   1. K steps back to back -> ms_per_step and value = B*H*N / time.
@@ -250,7 +251,8 @@ def main():
     ap.add_argument("--workload", default="speed_n16384")
     ap.add_argument("--d", type=int, default=None, help="override the head dimension")
     ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
-    ap.add_argument("--also", default="speed_n4096", help="comma-separated extra workloads ('' for none)")
+    ap.add_argument("--also", default="speed_n4096,vit_b16_n196",
+                    help="comma-separated extra workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mb", type=str, default=None,
                     help="instead of the benchmark: time torch's device copy at these sizes (MB, comma "

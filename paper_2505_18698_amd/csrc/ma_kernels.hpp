@@ -99,9 +99,13 @@ template <> struct Mma<_Float16> {
     }
 };
 
-// Row stride (elements) of a row-major LDS tile with C columns: pad by 16 bytes.
+// Row stride (elements) of a row-major LDS tile with C columns: pad by
+// MA_LDS_PAD bytes (32 measured fastest of 0, 16 and 32 on the half-steps).
+#ifndef MA_LDS_PAD
+#define MA_LDS_PAD 32
+#endif
 template <typename T, int C> struct Ld {
-    static constexpr int row = C + 16 / (int)sizeof(T);
+    static constexpr int row = C + MA_LDS_PAD / (int)sizeof(T);
 };
 
 // gfx950's v_permlane16_swap / v_permlane32_swap applied to (x, x) return
@@ -956,7 +960,7 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> 
 // ---------------------------------------------------------------------------------------
 template <typename T, bool RGB, bool RGM> struct FusedHead {
     static_assert(sizeof(T) == 2, "16-bit elements only");
-    static constexpr int D = 64, NW = 16, LD = Ld<T, D>::row;  // 64 * NW threads (the launch bound below)
+    static constexpr int D = 64, NW = 16, LD = D + 8;  // 64 * NW threads (the launch bound below); rows + 16 bytes
     // Blocks are BS elements apart: 16 rows plus 16 bytes, so that the 16
     // lanes reading row r of 16 different blocks hit different LDS banks.
     static constexpr int BS = 16 * LD + 8;
