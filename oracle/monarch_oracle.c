@@ -8,7 +8,8 @@
  *
  * What it computes (paper, Sec. 3 "MonarchAttention" and its "Implementation"
  * paragraph; the algorithm of Fig. "Python-like code for MonarchAttention"):
- * for every (batch, head) slice with Q, K, V in R^{N x d}, N = m*b,
+ * for every (batch, head) slice with Q, K, V in R^{N x d}, N = m*b (see below
+ * for N < m*b),
  *
  *   Qbar[j][l] = Q[l*b + j],  Kbar[k][i] = K[k*b + i],  Vbar[k][i] = V[k*b + i]
  *                        (row (l,j) of the "transpose" permutation P, Sec. 2)
@@ -39,6 +40,14 @@
  *
  * c_L follows its definition: sum_i R log R, with the limit 0 * log 0 = 0 for
  * entries that underflow to zero.
+ *
+ * Sequence lengths that are not a multiple of b (Appendix "Padding and
+ * Masking"): with m = ceil(N / b), Q, K and V are post-padded with zero rows
+ * to N' = m*b (the paper leaves the pad value open; zero is the reading taken
+ * here, and the padded query rows take part in the iteration like any other
+ * row), the mask omega adds -inf to Z_R for every key position k*b + i >= N
+ * before the softmax of eq. R_update, so that the last N' - N columns of M
+ * are zero, and only the first N rows of O are returned.
  */
 #include <math.h>
 #include <stdint.h>
@@ -54,10 +63,11 @@
 
 /* One R half-step for unit (head, k), eq. R_update, beta_r, beta_l.
  * aR[k][j][:] and cR[k][j] are the inputs; writes aL[j][k][:], cL[j][k] and,
- * when y != NULL, Y[j][k][:]. */
+ * when y != NULL, Y[j][k][:].  Keys i >= nkeys of block k are padding: the
+ * mask omega = -inf is added to their Z_R (Appendix "Padding and Masking"). */
 static void r_half_step(const double *Kh, const double *Vh, const double *aR, const double *cR,
                         double *aL, double *cL, double *Y, int64_t m, int64_t b, int64_t d,
-                        int64_t k, double *z)
+                        int64_t k, int64_t nkeys, double *z)
 {
     const double *Kk = Kh + k * b * d; /* Kbar[k][i] = K[k*b + i] */
     const double *Vk = Vh ? Vh + k * b * d : NULL;
@@ -68,7 +78,7 @@ static void r_half_step(const double *Kh, const double *Vh, const double *aR, co
         for (int64_t i = 0; i < b; ++i) {
             double beta = 0.0;
             for (int64_t v = 0; v < d; ++v) beta += a[v] * Kk[i * d + v];
-            z[i] = beta / c;
+            z[i] = i < nkeys ? beta / c : -INFINITY; /* + omega[k][j][i] */
             if (z[i] > zmax) zmax = z[i];
         }
         double sum = 0.0;
@@ -151,17 +161,22 @@ int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double 
                       int32_t threads)
 {
     if (!q || !k || !v || !out) return MO_EINVAL;
-    if (B < 1 || H < 1 || d < 1 || m < 1 || b < 1 || T < 1 || m * b != N) return MO_EINVAL;
-    const int64_t BH = B * H, nd = N * d;
+    if (B < 1 || H < 1 || d < 1 || m < 1 || b < 1 || T < 1 || N < 1) return MO_EINVAL;
+    if (N > m * b || N <= (m - 1) * b) return MO_EINVAL; /* m = ceil(N / b) */
+    const int64_t BH = B * H, Np = m * b, nd = Np * d;
     const double s = 1.0 / sqrt((double)d);
-    double *Qs = malloc(sizeof(double) * (size_t)(BH * nd));
+    /* Q (scaled), K, V post-padded with zero rows to Np = m*b; O on Np rows */
+    double *Qs = calloc((size_t)(BH * nd), sizeof(double));
+    double *Kp = calloc((size_t)(BH * nd), sizeof(double));
+    double *Vp = calloc((size_t)(BH * nd), sizeof(double));
+    double *Op = malloc(sizeof(double) * (size_t)(BH * nd));
     double *aR = malloc(sizeof(double) * (size_t)(BH * nd));
     double *aL = malloc(sizeof(double) * (size_t)(BH * nd));
     double *Y = malloc(sizeof(double) * (size_t)(BH * nd));
-    double *cR = malloc(sizeof(double) * (size_t)(BH * N));
-    double *cL = malloc(sizeof(double) * (size_t)(BH * N));
-    if (!Qs || !aR || !aL || !Y || !cR || !cL) {
-        free(Qs); free(aR); free(aL); free(Y); free(cR); free(cL);
+    double *cR = malloc(sizeof(double) * (size_t)(BH * Np));
+    double *cL = malloc(sizeof(double) * (size_t)(BH * Np));
+    if (!Qs || !Kp || !Vp || !Op || !aR || !aL || !Y || !cR || !cL) {
+        free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL);
         return MO_ENOMEM;
     }
 #ifdef _OPENMP
@@ -171,14 +186,18 @@ int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double 
 #endif
     const int64_t zlen = (m > b ? m : b);
 
-    /* Scale absorbed into Q; t = 1 state from L^(0) = I: alpha_R[k][j] = s*Q[k*b+j], c_R = 1. */
 #pragma omp parallel for schedule(static)
-    for (int64_t e = 0; e < BH * nd; ++e) {
-        Qs[e] = s * q[e];
-        aR[e] = Qs[e];
-    }
+    for (int64_t h = 0; h < BH; ++h)
+        for (int64_t e = 0; e < N * d; ++e) {
+            Qs[h * nd + e] = s * q[h * N * d + e]; /* scale absorbed into Q */
+            Kp[h * nd + e] = k[h * N * d + e];
+            Vp[h * nd + e] = v[h * N * d + e];
+        }
+    /* t = 1 state from L^(0) = I: alpha_R[k][j] = s*Q[k*b+j], c_R = 1. */
 #pragma omp parallel for schedule(static)
-    for (int64_t e = 0; e < BH * N; ++e) cR[e] = 1.0;
+    for (int64_t e = 0; e < BH * nd; ++e) aR[e] = Qs[e];
+#pragma omp parallel for schedule(static)
+    for (int64_t e = 0; e < BH * Np; ++e) cR[e] = 1.0;
 
     for (int32_t t = 1; t <= T; ++t) {
         const int last = (t == T);
@@ -187,18 +206,24 @@ int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double 
             double *z = malloc(sizeof(double) * (size_t)zlen);
 #pragma omp for collapse(2) schedule(static)
             for (int64_t h = 0; h < BH; ++h)
-                for (int64_t kk = 0; kk < m; ++kk)
-                    r_half_step(k + h * nd, last ? v + h * nd : NULL, aR + h * nd, cR + h * N,
-                                aL + h * nd, cL + h * N, last ? Y + h * nd : NULL, m, b, d, kk, z);
+                for (int64_t kk = 0; kk < m; ++kk) {
+                    const int64_t nkeys = N - kk * b < b ? N - kk * b : b;
+                    r_half_step(Kp + h * nd, last ? Vp + h * nd : NULL, aR + h * nd, cR + h * Np,
+                                aL + h * nd, cL + h * Np, last ? Y + h * nd : NULL, m, b, d, kk, nkeys, z);
+                }
 #pragma omp for collapse(2) schedule(static)
             for (int64_t h = 0; h < BH; ++h)
                 for (int64_t j = 0; j < b; ++j)
-                    l_half_step(Qs + h * nd, aL + h * nd, cL + h * N, Y + h * nd, aR + h * nd,
-                                cR + h * N, last ? out + h * nd : NULL, m, b, d, j, z);
+                    l_half_step(Qs + h * nd, aL + h * nd, cL + h * Np, Y + h * nd, aR + h * nd,
+                                cR + h * Np, last ? Op + h * nd : NULL, m, b, d, j, z);
             free(z);
         }
     }
-    free(Qs); free(aR); free(aL); free(Y); free(cR); free(cL);
+    /* the first N rows of every head */
+#pragma omp parallel for schedule(static)
+    for (int64_t h = 0; h < BH; ++h)
+        memcpy(out + h * N * d, Op + h * nd, sizeof(double) * (size_t)(N * d));
+    free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL);
     return MO_OK;
 }
 

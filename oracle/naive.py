@@ -13,6 +13,12 @@ equation; it is meant for small N only.
 Indices are 0-based: query row (l, j) is row l*b + j of Q and key row (k, i)
 is row k*b + i of K (the rows of Qbar and Kbar in eq. beta_r).  Q is scaled by
 s = 1/sqrt(d) before use (Sec. 2, attention footnote).
+
+A length N that is not a multiple of b follows Appendix "Padding and
+Masking": m = ceil(N / b), Q, K, V post-padded to m*b rows (zero rows unless
+the caller passes padded arrays), the mask omega (-inf at key positions
+k*b + i >= N) added to Z_R before the softmax of eq. R_update, and the first
+N rows of O kept.
 """
 from __future__ import annotations
 
@@ -53,6 +59,23 @@ def kbar(k: np.ndarray, m: int, b: int) -> np.ndarray:
     return out
 
 
+def pad_rows(x: np.ndarray, m: int, b: int) -> np.ndarray:
+    """Post-pad the rows of x with zero rows to m*b rows."""
+    out = np.zeros((m * b,) + x.shape[1:])
+    out[: x.shape[0]] = x
+    return out
+
+
+def key_mask(n: int, m: int, b: int) -> np.ndarray:
+    """omega[k, i] = 0 if key position k*b + i < n else -inf (Appendix "Padding and Masking")."""
+    omega = np.zeros((m, b))
+    for k in range(m):
+        for i in range(b):
+            if k * b + i >= n:
+                omega[k, i] = -np.inf
+    return omega
+
+
 def _softmax(z: np.ndarray) -> np.ndarray:
     e = np.exp(z - z.max())
     return e / e.sum()
@@ -63,8 +86,9 @@ def _xlogx_sum(p: np.ndarray) -> float:
     return float(np.sum(p[nz] * np.log(p[nz])))
 
 
-def r_update(L: np.ndarray, Qb: np.ndarray, Kb: np.ndarray) -> np.ndarray:
-    """R = softmax_i(beta_R / c_R) with beta_R, c_R from L (eqs. R_update, beta_r)."""
+def r_update(L: np.ndarray, Qb: np.ndarray, Kb: np.ndarray, omega=None) -> np.ndarray:
+    """R = softmax_i(beta_R / c_R + omega) with beta_R, c_R from L (eqs. R_update, beta_r);
+    omega is the padding mask, absent when N = m*b."""
     b, m, _ = L.shape
     R = np.empty((m, b, b))
     for k in range(m):
@@ -72,7 +96,10 @@ def r_update(L: np.ndarray, Qb: np.ndarray, Kb: np.ndarray) -> np.ndarray:
             alpha_r = L[j, k, :] @ Qb[j]          # sum_l L[j,k,l] Qbar[j,l,:]
             c_r = L[j, k, :].sum()                # sum_l L[j,k,l]
             beta_r = Kb[k] @ alpha_r              # beta_R[k,j,i] = <alpha_R[k,j], Kbar[k,i]>
-            R[k, j] = _softmax(beta_r / c_r)
+            z_r = beta_r / c_r
+            if omega is not None:
+                z_r = z_r + omega[k]
+            R[k, j] = _softmax(z_r)
     return R
 
 
@@ -94,9 +121,13 @@ def _f64(*xs):
 
 
 def monarch_apply(L: np.ndarray, R: np.ndarray, v: np.ndarray) -> np.ndarray:
-    """O = M V by the two-step product of eq. monarch_multiply."""
+    """O = M V by the two-step product of eq. monarch_multiply; v with N <= m*b rows
+    (zero-padded), O with the same N rows."""
     (v,) = _f64(v)
     b, m, _ = L.shape
+    n = v.shape[0]
+    if n < m * b:
+        v = pad_rows(v, m, b)
     Vb = kbar(v, m, b)
     Y = np.empty((b, m, v.shape[1]))
     for j in range(b):
@@ -106,18 +137,27 @@ def monarch_apply(L: np.ndarray, R: np.ndarray, v: np.ndarray) -> np.ndarray:
     for l in range(m):
         for j in range(b):
             O[l * b + j] = L[j, :, l] @ Y[j]     # sum_k L[j,k,l] Y[j,k,:]
-    return O
+    return O[:n]
 
 
-def factors(q, k, m, b, T, *, history=False):
+def factors(q, k, m, b, T, *, history=False, n=None):
     """Run T (R, L) update pairs from L^(0) = I (Sec. 3).  q, k: one head [N, d].
 
-    Returns (L, R) after T steps; with history=True also the list of
-    (L, R) pairs after every half-step, starting with (L^(0), None).
+    N < m*b rows are zero-padded to m*b.  Arrays that already have m*b rows
+    with n < m*b are taken as padded by the caller (rows >= n are padding,
+    whatever they hold).  Returns (L, R) after T steps; with history=True
+    also the list of (L, R) pairs after every half-step, starting with
+    (L^(0), None).
     """
     q, k = _f64(q, k)
-    n, d = q.shape
-    assert n == m * b and T >= 1
+    rows, d = q.shape
+    n = rows if n is None else n
+    assert (m - 1) * b < n <= m * b and T >= 1        # m = ceil(N / b)
+    if rows < m * b:
+        assert rows == n
+        q, k = pad_rows(q, m, b), pad_rows(k, m, b)
+    assert q.shape[0] == m * b
+    omega = key_mask(n, m, b) if n < m * b else None
     s = 1.0 / np.sqrt(d)
     Qb = qbar(s * q, m, b)
     Kb = kbar(k, m, b)
@@ -125,7 +165,7 @@ def factors(q, k, m, b, T, *, history=False):
     R = None
     hist = [(L, None)]
     for _ in range(T):
-        R = r_update(L, Qb, Kb)                     # R before L in every step
+        R = r_update(L, Qb, Kb, omega)              # R before L in every step
         hist.append((L, R))
         L = l_update(R, Qb, Kb)
         hist.append((L, R))

@@ -84,6 +84,40 @@ def _battery():
     L, R = nv.factors(q, k, m, b, 2)
     if np.abs(nv.monarch_apply(L, R, v) - nv.dense_monarch(L, R) @ v).max() > 1e-12:
         failed.append("apply")
+    failed += _padding_battery()
+    return failed
+
+
+def _padding_battery():
+    """Pins of Appendix "Padding and Masking" (N = 10 < m*b = 12)."""
+    failed = []
+    m, b, n = 3, 4, 10
+    q, k, v = _head(m, b, 5, seed=500)
+    q, k, v = q[:n], k[:n], v[:n]
+    try:
+        L, R = nv.factors(q, k, m, b, 2)
+    except Exception:
+        return ["pad-crash"]
+    M = nv.dense_monarch(L, R)
+    if np.abs(M[:, n:]).max() != 0.0 or not np.allclose(M.sum(axis=1), 1.0, atol=1e-12):
+        failed.append("pad-columns")
+    # explicit zero padding (rows >= n given by the caller) equals the automatic one
+    qz, kz = np.zeros((m * b, 5)), np.zeros((m * b, 5))
+    qz[:n], kz[:n] = q, k
+    L2, R2 = nv.factors(qz, kz, m, b, 2, n=n)
+    if np.abs(L2 - L).max() > 1e-15 or np.abs(R2 - R).max() > 1e-15:
+        failed.append("pad-value")
+    # any values in the padded key rows: same factors
+    kg = kz.copy()
+    kg[n:] = np.random.default_rng(1).normal(size=(m * b - n, 5)) * 3
+    L3, R3 = nv.factors(qz, kg, m, b, 2, n=n)
+    if np.abs(L3 - L).max() > 1e-12 or np.abs(R3 - R).max() > 1e-12:
+        failed.append("pad-keys")
+    # one block: exact softmax attention over the n real tokens
+    q1, k1, v1 = _head(1, 8, 4, seed=501)
+    o1 = nv.monarch_attention_head(q1[:5], k1[:5], v1[:5], 1, 8, 2)
+    if o1.shape != (5, 4) or np.abs(o1 - nv.dense_softmax_attention(q1[:5], k1[:5], v1[:5])).max() > 1e-12:
+        failed.append("pad-exact")
     return failed
 
 
@@ -97,20 +131,25 @@ def _softmax(z):
 
 
 def _r_update_variant(kind):
-    def r_update(L, Qb, Kb):
+    def r_update(L, Qb, Kb, omega=None):
         b, m, _ = L.shape
         R = np.empty((m, b, b))
+        if omega is not None and kind == "mask-front":       # the pre-padding side
+            omega = omega.reshape(-1)[::-1].reshape(m, b)
         for k in range(m):
+            om = 0.0 if omega is None or kind == "no-mask" else omega[k]
             for j in range(b):
                 a = L[j, k, :] @ Qb[j]
                 c = L[j, k, :].sum()
                 beta = Kb[k] @ a
                 if kind == "no-divide":
-                    R[k, j] = _softmax(beta)
+                    R[k, j] = _softmax(beta + om)
                 elif kind == "times-c":
-                    R[k, j] = _softmax(beta * c)
+                    R[k, j] = _softmax(beta * c + om)
                 elif kind == "transposed-L":
-                    R[k, j] = _softmax((Kb[k] @ (L[j, :, k] @ Qb[j])) / L[j, :, k].sum())
+                    R[k, j] = _softmax((Kb[k] @ (L[j, :, k] @ Qb[j])) / L[j, :, k].sum() + om)
+                else:
+                    R[k, j] = _softmax(beta / c + om)
         return R
     return r_update
 
@@ -145,14 +184,18 @@ def _qbar_wrong(q, m, b):
     return q.reshape(b, m, d).copy()      # rows j*m + l instead of l*b + j
 
 
-def _factors_uniform_init(q, k, m, b, T, *, history=False):
-    n, d = q.shape
+def _factors_uniform_init(q, k, m, b, T, *, history=False, n=None):
+    rows, d = q.shape
+    n = rows if n is None else n
+    if rows < m * b:
+        q, k = nv.pad_rows(q, m, b), nv.pad_rows(k, m, b)
+    omega = nv.key_mask(n, m, b) if n < m * b else None
     s = 1.0 / np.sqrt(d)
     Qb, Kb = nv.qbar(s * q, m, b), nv.kbar(k, m, b)
     L = np.full((b, m, m), 1.0 / m)
     hist = [(L, None)]
     for _ in range(T):
-        R = nv.r_update(L, Qb, Kb)
+        R = nv.r_update(L, Qb, Kb, omega)
         hist.append((L, R))
         L = nv.l_update(R, Qb, Kb)
         hist.append((L, R))
@@ -169,7 +212,16 @@ MUTANTS = {
     "apply: transposed L": ("monarch_apply", lambda: _apply_transposed),
     "layout: wrong permutation": ("qbar", lambda: _qbar_wrong),
     "init: uniform L0": ("factors", lambda: _factors_uniform_init),
+    "padding: mask omitted": ("r_update", lambda: _r_update_variant("no-mask")),
+    "padding: mask on the pre-padding side": ("r_update", lambda: _r_update_variant("mask-front")),
+    "padding: padded with ones": ("pad_rows", lambda: _pad_ones),
 }
+
+
+def _pad_ones(x, m, b):
+    out = np.ones((m * b,) + x.shape[1:])
+    out[: x.shape[0]] = x
+    return out
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))

@@ -257,3 +257,81 @@ def test_dense_attention_rows(oracle_lib):
     for h in range(2):
         ref = nv.dense_softmax_attention(q[0, h], k[0, h], v[0, h])[rows]
         assert np.abs(got[0, h] - ref).max() < 1e-13
+
+
+# -- sequence lengths that are not a multiple of b (Appendix "Padding and Masking") ------
+
+def _padded_head(n, m, b, d, seed):
+    q, k, v = _head(m, b, d, seed=seed)
+    return q[:n], k[:n], v[:n]
+
+
+@pytest.mark.parametrize("n,m,b", [(10, 3, 4), (197, 15, 14), (7, 2, 4)])
+def test_padding_zeroes_the_padded_columns_of_M(n, m, b):
+    """The mask omega (-inf on Z_R at key positions >= N) makes the last
+    m*b - N columns of the padded Monarch matrix exactly zero, which is what
+    the appendix asks of it; the rows still sum to one."""
+    q, k, v = _padded_head(n, m, b, 6, seed=90 + n)
+    L, R = nv.factors(q, k, m, b, 2)
+    M = nv.dense_monarch(L, R)
+    assert np.all(M[:, n:] == 0.0)
+    assert np.all(M >= 0) and np.allclose(M.sum(axis=1), 1.0, atol=1e-12)
+    # and O is M V on the real rows
+    assert np.abs(nv.monarch_apply(L, R, v) - M[:n, :n] @ v).max() < 1e-12
+
+
+def test_padding_ignores_padded_key_and_value_rows():
+    """Whatever the padded K and V rows hold, the real outputs are the same
+    (their R entries are exactly zero)."""
+    n, m, b, d = 10, 3, 4, 6
+    q, k, v = _padded_head(n, m, b, d, seed=95)
+    ref = nv.monarch_attention_head(q, k, v, m, b, 2)
+    rng = np.random.default_rng(5)
+    qp, kp, vp = (nv.pad_rows(x, m, b) for x in (q, k, v))
+    kp[n:] = 4 * rng.normal(size=(m * b - n, d))
+    vp[n:] = 4 * rng.normal(size=(m * b - n, d))
+    L, R = nv.factors(qp, kp, m, b, 2, n=n)
+    got = nv.monarch_apply(L, R, vp)[:n]
+    assert np.abs(got - ref).max() < 1e-13
+
+
+def test_padded_query_rows_take_part():
+    """Padded query rows are rows of the padded problem: they shape alpha_R and
+    c_R, so their values change the real outputs.  (This is why the pad value
+    is a convention; zero rows are the one used everywhere here.)"""
+    n, m, b, d = 10, 3, 4, 6
+    q, k, v = _padded_head(n, m, b, d, seed=96)
+    ref = nv.monarch_attention_head(q, k, v, m, b, 2)
+    qp, kp, vp = (nv.pad_rows(x, m, b) for x in (q, k, v))
+    qp[n:] = 3.0
+    L, R = nv.factors(qp, kp, m, b, 2, n=n)
+    assert np.abs(nv.monarch_apply(L, R, vp)[:n] - ref).max() > 1e-6
+
+
+@pytest.mark.parametrize("n,b,T", [(5, 8, 1), (11, 16, 3), (1, 4, 2)])
+def test_single_padded_block_is_exact_attention(oracle_lib, n, b, T):
+    """m = 1 with N < b: one block whose padded keys are masked, so M is the
+    exact softmax attention of the N real tokens."""
+    q, k, v = _padded_head(n, 1, b, 8, seed=97 + n)
+    ref = nv.dense_softmax_attention(q, k, v)
+    o = oracle.monarch_attention(q[None, None], k[None, None], v[None, None], 1, b, T)[0, 0]
+    assert o.shape == (n, 8)
+    assert oracle.rel_frobenius(o, ref) < 1e-13
+    assert oracle.rel_frobenius(nv.monarch_attention_head(q, k, v, 1, b, T), ref) < 1e-13
+
+
+@pytest.mark.parametrize("n,m,b,T", [(10, 3, 4, 1), (197, 15, 14, 2), (33, 3, 16, 3), (61, 4, 16, 2), (130, 2, 128, 2)])
+def test_state_form_matches_factor_form_padded(oracle_lib, n, m, b, T):
+    """The C state form with its internal padding equals the materialised-factor form."""
+    q, k, v = si.random_qkv(2, 1, n, 8, "bf16", seed=n * 7 + b, scale=2.0)
+    o1 = oracle.monarch_attention(q, k, v, m, b, T)
+    o2 = nv.monarch_attention(q, k, v, m, b, T)
+    assert o1.shape == q.shape
+    assert oracle.rel_frobenius(o1, o2) < 1e-12
+
+
+def test_padding_rejects_m_other_than_ceil_n_over_b(oracle_lib):
+    q, k, v = si.random_qkv(1, 1, 10, 4, "f32", seed=1)
+    for m in (2, 4):   # ceil(10 / 4) = 3
+        with pytest.raises(ValueError):
+            oracle.monarch_attention(q, k, v, m, 4, 1)
