@@ -57,8 +57,14 @@ typedef enum {
  *           All four buffers are owned by the caller; the library neither
  *           frees nor retains them.
  * B, H    : batch and head counts (>= 1).
- * N, m, b : sequence length, number of blocks and block size, N == m * b.
- *           Supported: 1 <= m, b <= 128.
+ * N, m, b : sequence length, number of blocks and block size:
+ *           m = ceil(N / b), i.e. (m - 1) * b < N <= m * b.  When N < m * b
+ *           the sequence is post-padded to m * b rows as in Appendix
+ *           "Padding and Masking": the padded rows of Q, K, V count as zero
+ *           rows (they are not read), keys at positions >= N are masked out
+ *           of every R softmax (omega = -inf on Z_R), and only the N real rows
+ *           of out are written.  The padded query rows take part in the
+ *           iteration like the others.  Supported: 1 <= m, b <= 128.
  * d       : head dimension; supported: 64 or 128.  fp32 also needs
  *           16*ceil(m/16)*d <= 8192 and 16*ceil(b/16)*d <= 8192.
  * T       : number of (R, L) update pairs, 1 <= T <= 64.
@@ -68,8 +74,8 @@ typedef enum {
  * Asynchronous on `stream`: returns after enqueueing, with no host
  * synchronisation.  Arguments are checked before any HIP call; on MA_EINVAL or
  * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  Path 1 (see
- * monarch_attn_set_path) uses one device workspace per device (3 N d
- * elements plus 2 N floats per head), grown with hipMalloc on the first call
+ * monarch_attn_set_path) uses one device workspace per device (3 m b d
+ * elements plus 2 m b floats per head), grown with hipMalloc on the first call
  * that needs more; calls on different streams of one device must not overlap
  * (they share it).  After
  * the launches hipGetLastError is checked (MA_EHIP).  The message of the last

@@ -62,7 +62,7 @@ struct CallBufs {
 
 struct CallDims {
     int64_t BH;
-    int m, b, d, T;
+    int m, b, n, d, T;  // n: rows per head, (m - 1) * b < n <= m * b
     float s_log2e;
     int num_cus;  // compute units of the device
 };

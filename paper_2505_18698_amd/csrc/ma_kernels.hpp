@@ -496,13 +496,21 @@ template <typename T, int D> __device__ inline void store_row_lds(T *row, const 
 }
 
 struct HeadDims {
-    int m, b;          // blocks and block size, N = m * b
+    int m, b;          // blocks and block size
+    int n;             // rows of q, k, v, out per head, (m - 1) * b < n <= m * b
     float s_log2e;     // log2(e) / sqrt(d)
     int64_t units;     // work units of a half-step launch (grid size)
 };
 
-// Tensors and states of one call.  Layouts (per head, N = m * b):
-//   q, k, v, out [B*H][N][D];
+// Real keys of block k (b except in a padded last block).
+__device__ inline int block_keys(const HeadDims &hd, int k) { return min(hd.b, hd.n - k * hd.b); }
+
+// Tensors and states of one call.  When n < m * b the sequence is taken as
+// post-padded with zero rows to N = m * b (Appendix "Padding and Masking"):
+// rows >= n of q, k, v are never read (zero is loaded instead), keys >= n are
+// masked out of every R softmax, rows >= n of out are never written, and the
+// states cover all N rows.  Layouts (per head):
+//   q, k, v, out [B*H][n][D];
 //   alpha_R [m][b][D] (row k*b + j), alpha_L and Y [b][m][D] (row j*m + k),
 //   c_L [m][b] (written by the R half-step of block k for all j),
 //   c_R [b][m] (written by the L half-step of class j for all k).
@@ -538,19 +546,25 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
 
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, int tid, Regs &gr)
     {
-        const int m = hd.m, b = hd.b;
-        const int64_t N = (int64_t)m * b, hoff = bh * N * D;
+        const int m = hd.m, b = hd.b, kv = block_keys(hd, k);
+        const int64_t N = (int64_t)m * b, hoff = bh * N * D, toff = bh * (int64_t)hd.n * D;
         const int lane = tid & 63, wave = tid >> 6;
-        const T *kblk = p.k + hoff + (int64_t)k * b * D;
-        gr.kt.fetch([=](int r) { return kblk + (int64_t)r * D; }, b, tid);
+        const T *kblk = p.k + toff + (int64_t)k * b * D;
+        gr.kt.fetch([=](int r) { return kblk + (int64_t)r * D; }, kv, tid);
         if constexpr (FINAL) {
-            const T *vblk = p.v + hoff + (int64_t)k * b * D;
-            gr.vt.fetch([=](int r) { return vblk + (int64_t)r * D; }, b, tid);
+            const T *vblk = p.v + toff + (int64_t)k * b * D;
+            gr.vt.fetch([=](int r) { return vblk + (int64_t)r * D; }, kv, tid);
         }
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int j = (wave * RT + r) * 16 + (lane & 15);
-            gr.bf[r].load(j < b ? (FIRST ? p.q : p.aR) + hoff + ((int64_t)k * b + j) * D : nullptr, lane >> 4);
+            const T *row = nullptr;  // alpha_R[k][j]; at t = 1 Q row k*b + j (zero if padding)
+            if constexpr (FIRST) {
+                if (j < kv) row = p.q + toff + ((int64_t)k * b + j) * D;
+            } else {
+                if (j < b) row = p.aR + hoff + ((int64_t)k * b + j) * D;
+            }
+            gr.bf[r].load(row, lane >> 4);
             gr.cr[r] = 1.0f;
             if constexpr (!FIRST) {
                 if (j < b) gr.cr[r] = p.cR[bh * N + (int64_t)j * m + k];
@@ -571,7 +585,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
     {
         T *Ks = reinterpret_cast<T *>(lds);
         T *Vs = Ks + NB * LDK;
-        const int m = hd.m, b = hd.b;
+        const int m = hd.m, b = hd.b, kv = block_keys(hd, k);  // keys >= kv: padding, masked (omega)
         const int64_t N = (int64_t)m * b;
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
@@ -598,7 +612,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
         for (int r = 0; r < RT; ++r) {
             // Z = s S / c_R in log2 units: u = Z - max Z = S * rs - max S * rs  (rs > 0)
             const float rs = rscale[r];
-            const float nb = -tiles_max<NT, RAGGED>(sc[r], b, g) * rs;
+            const float nb = -tiles_max<NT, RAGGED>(sc[r], kv, g) * rs;
             float sum = 0.f, t2 = 0.f;
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
@@ -606,7 +620,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
                 for (int qq = 0; qq < 4; ++qq) {
                     const float u = __builtin_fmaf(sc[r][t][qq], rs, nb);
                     float e = __builtin_amdgcn_exp2f(u);
-                    if (RAGGED && 16 * t + 4 * g + qq >= b) e = 0.f;
+                    if (RAGGED && 16 * t + 4 * g + qq >= kv) e = 0.f;
                     sum += e;
                     t2 = __builtin_fmaf(e, u, t2);
                     sc[r][t][qq] = e;
@@ -674,9 +688,10 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
     {
         const int m = hd.m, b = hd.b;
         const int64_t N = (int64_t)m * b, hoff = bh * N * D;
-        const T *qh = p.q + hoff;
+        const T *qh = p.q + bh * (int64_t)hd.n * D;
         const T *al = p.aL + hoff + (int64_t)j * m * D;
-        gr.qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * D; }, m, tid);
+        const int ml = (hd.n - j + b - 1) / b;  // real rows l of class j: l*b + j < n
+        gr.qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * D; }, ml, tid);
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
     }
@@ -809,7 +824,8 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int l = (wave * RT + r) * 16 + (lane & 15);
-            gr.bf[r].load(l < m ? p.q + hoff + ((int64_t)l * b + j) * D : nullptr, lane >> 4);  // Qbar[j][l]
+            gr.bf[r].load((int64_t)l * b + j < hd.n ? p.q + bh * (int64_t)hd.n * D + ((int64_t)l * b + j) * D : nullptr,
+                          lane >> 4);  // Qbar[j][l]; zero for padded rows
         }
     }
 
@@ -884,7 +900,9 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         }
 #pragma unroll
         for (int r = 0; r < RT; ++r)
-            store_row<T, D>(lr[r] < m ? p.out + hoff + ((int64_t)lr[r] * b + j) * D : nullptr, o[r], inv[r], lane);
+            store_row<T, D>((int64_t)lr[r] * b + j < hd.n ? p.out + bh * (int64_t)hd.n * D + ((int64_t)lr[r] * b + j) * D
+                                                         : nullptr,
+                            o[r], inv[r], lane);
     }
 };
 
@@ -977,7 +995,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
     struct Ctx {
         T *Qs, *Ks, *As, *Rs;
         float *cRs, *cLs;  // c_R[k][j] at k*CS + j, c_L[j][k] at j*CS + k
-        int m, b, lane, g, c16;
+        int m, b, n, lane, g, c16;  // n: real rows of the head (rows >= n are zero padding)
         float s_log2e;
     };
 
@@ -993,15 +1011,16 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             if (jv) rs = c.s_log2e * fast_rcp(fmaxf(c.cRs[k * CS + j], kTiny));
         }
         T *Kk = c.Ks + k * BS;
+        const int kv = min(c.b, c.n - k * c.b);  // keys >= kv: padding, masked (omega)
         f32x4 sc;  // lane holds S'[i = 4g + qq][j]
         gemm_scores_rt<T, D, 1>(Kk + c.c16 * LD, &bf, &sc, c.g);
-        const float nb = -tiles_max<1, RGB>(&sc, c.b, c.g) * rs;
+        const float nb = -tiles_max<1, RGB>(&sc, kv, c.g) * rs;
         float sum = 0.f, t2 = 0.f;
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
             const float u = __builtin_fmaf(sc[qq], rs, nb);
             float e = __builtin_amdgcn_exp2f(u);
-            if (RGB && 4 * c.g + qq >= c.b) e = 0.f;
+            if (RGB && 4 * c.g + qq >= kv) e = 0.f;
             sum += e;
             t2 = __builtin_fmaf(e, u, t2);
             sc[qq] = e;
@@ -1086,25 +1105,27 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         f32x4 o[D / 16];  // O[l*b + j] = sum_k L[j][k][l] Y[k][j]; Y[k][j] is row k of Ks + j*LD at stride BS
 #pragma unroll
         for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, 1>(c.Ks + j * LD, BS, 16 * vt, pf, c.lane);
-        store_row<T, D>(l < c.m ? out_h + ((int64_t)l * c.b + j) * D : nullptr, o, 1.0f, c.lane);
+        store_row<T, D>(l * c.b + j < c.n ? out_h + ((int64_t)l * c.b + j) * D : nullptr, o, 1.0f, c.lane);
     }
 
     static constexpr int PER = 2 * 256 * 8 / (64 * NW);  // 16-byte chunks of Qs and Ks per thread
 
     // Issue the loads of head bh: Qbar and Kbar chunks (zero where there is no
     // row) for the LDS regions, and Vbar[w] for wave w's last R half-step.
-    __device__ static void load_head(const Bufs<T> &p, int m, int b, int64_t bh, int tid, u32x4 *raw, u32x4 *vb)
+    // Rows >= n (padding) are zero and never read.
+    __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int64_t bh, int tid, u32x4 *raw,
+                                     u32x4 *vb)
     {
-        const int64_t hoff = bh * (int64_t)m * b * D;
+        const int64_t hoff = bh * (int64_t)n * D;
         const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
 #pragma unroll
         for (int h = 0; h < PER; ++h) {
             const int idx = tid + h * 64 * NW;
             const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
             raw[h] = u32x4{0u, 0u, 0u, 0u};
-            if (reg == 0 && blk < b && r < m)
+            if (reg == 0 && blk < b && r < m && r * b + blk < n)
                 raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * D + col);  // Qbar[blk][r]
-            if (reg == 1 && blk < m && r < b)
+            if (reg == 1 && blk < m && r < b && blk * b + r < n)
                 raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * D + col);  // Kbar[blk][r]
         }
         const int w = tid >> 6, lane = tid & 63;
@@ -1112,7 +1133,8 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         for (int h = 0; h < 2; ++h) {
             const int r = (lane >> 3) + 8 * h, col = (lane & 7) * 8;
             vb[h] = u32x4{0u, 0u, 0u, 0u};
-            if (w < m && r < b) vb[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * D + col);
+            if (w < m && r < b && w * b + r < n)
+                vb[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * D + col);
         }
     }
 
@@ -1139,6 +1161,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         c.cLs = c.cRs + 16 * CS;
         c.m = hd.m;
         c.b = hd.b;
+        c.n = hd.n;
         c.s_log2e = hd.s_log2e;
         const int tid = threadIdx.x, w = tid >> 6;
         c.lane = tid & 63;
@@ -1148,13 +1171,13 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
 
         u32x4 raw[PER], vcur[2], vnext[2];
         int64_t bh = blockIdx.x;
-        load_head(p, m, b, bh, tid, raw, vcur);
+        load_head(p, m, b, c.n, bh, tid, raw, vcur);
         for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) *chunk(c.As, idx) = u32x4{0u, 0u, 0u, 0u};
         for (; bh < BH; bh += gridDim.x) {
 #pragma unroll
             for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
             __syncthreads();
-            if (bh + gridDim.x < BH) load_head(p, m, b, bh + gridDim.x, tid, raw, vnext);
+            if (bh + gridDim.x < BH) load_head(p, m, b, c.n, bh + gridDim.x, tid, raw, vnext);
 
             for (int t = 1; t <= T_; ++t) {
                 const bool first = t == 1, last = t == T_;
@@ -1173,7 +1196,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
                 if (w < b) l_unit(c, w);
                 __syncthreads();
             }
-            if (w < b) apply_unit(c, w, p.out + bh * (int64_t)m * b * D);
+            if (w < b) apply_unit(c, w, p.out + bh * (int64_t)c.n * D);
             vcur[0] = vnext[0];
             vcur[1] = vnext[1];
             __syncthreads();  // the apply has read Qs, As and Ks

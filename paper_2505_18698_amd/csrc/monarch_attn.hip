@@ -39,7 +39,9 @@ int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t d
 {
     if (dtype != MA_F32 && dtype != MA_BF16 && dtype != MA_F16) return fail(MA_EINVAL, "unknown dtype %d", dtype);
     if (m < 1 || b < 1 || N < 1 || d < 1) return fail(MA_EINVAL, "N, d, m, b must be >= 1");
-    if (m * b != N) return fail(MA_EINVAL, "N (%lld) != m (%lld) * b (%lld)", (long long)N, (long long)m, (long long)b);
+    if (N > m * b || N <= (m - 1) * b)
+        return fail(MA_EINVAL, "m (%lld) must be ceil(N / b) (N = %lld, b = %lld)", (long long)m, (long long)N,
+                    (long long)b);
     if (T < 1) return fail(MA_EINVAL, "T must be >= 1 (got %d)", T);
     if (T > 64) return fail(MA_EUNSUPPORTED, "T > 64 is not supported (got %d)", T);
     if (m > 128 || b > 128) return fail(MA_EUNSUPPORTED, "m and b must be <= 128 (got m=%lld, b=%lld)", (long long)m, (long long)b);
@@ -52,11 +54,12 @@ int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t d
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-size_t workspace_bytes(int64_t BH, int64_t N, int64_t d, int32_t dtype)
+// Np = m * b: the states cover the padded sequence.
+size_t workspace_bytes(int64_t BH, int64_t Np, int64_t d, int32_t dtype)
 {
     // alpha_R, alpha_L and Y in the element type, c_R and c_L in fp32
-    const size_t st = align_up((size_t)BH * N * d * elem_bytes(dtype));
-    const size_t cs = align_up((size_t)BH * N * sizeof(float));
+    const size_t st = align_up((size_t)BH * Np * d * elem_bytes(dtype));
+    const size_t cs = align_up((size_t)BH * Np * sizeof(float));
     return 3 * st + 2 * cs;
 }
 
@@ -94,7 +97,7 @@ size_t monarch_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, 
                                     int32_t T, int32_t dtype)
 {
     if (B < 1 || H < 1 || check_shape(N, d, m, b, T, dtype) != MA_OK) return 0;
-    return workspace_bytes(B * H, N, d, dtype);
+    return workspace_bytes(B * H, m * b, d, dtype);
 }
 
 int monarch_attn_release_workspace(void)
@@ -181,8 +184,8 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
         return fail(MA_EINVAL, "out must not overlap q, k or v");
 
     const int path = g_path.load();
-    const size_t st = align_up((size_t)BH * N * d * elem_bytes(dtype));
-    const size_t cs = align_up((size_t)BH * N * sizeof(float));
+    const size_t st = align_up((size_t)BH * m * b * d * elem_bytes(dtype));
+    const size_t cs = align_up((size_t)BH * m * b * sizeof(float));
     CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
@@ -199,7 +202,7 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
         num_cus = D.num_cus;
     }
     if (!uses_fused(path, dtype, d, m, b)) {  // the fused kernel keeps its states in LDS
-        const size_t need = workspace_bytes(BH, N, d, dtype);
+        const size_t need = workspace_bytes(BH, m * b, d, dtype);
         std::lock_guard<std::mutex> lock(g_dev_mutex);
         Device &D = g_dev[dev];
         if (D.ws_bytes < need) {
@@ -224,7 +227,7 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
         bufs.cR = (float *)(base + 3 * st);
         bufs.cL = (float *)(base + 3 * st + cs);
     }
-    CallDims dims{BH, (int)m, (int)b, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
+    CallDims dims{BH, (int)m, (int)b, (int)N, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
 
     std::unique_lock<std::mutex> tlock(g_timing_mutex);
     Launcher L{(hipStream_t)stream, g_timing.enabled};

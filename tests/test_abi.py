@@ -41,7 +41,8 @@ FAKE = 1 << 20  # an aligned non-null address that is never dereferenced: every 
         ((0, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),           # null q
         ((FAKE, FAKE, FAKE, 0, 1, 1, 256, 64, 16, 16, 1, 1), 1),               # null out
         ((FAKE, FAKE, FAKE, 2 * FAKE, 0, 1, 256, 64, 16, 16, 1, 1), 1),        # B = 0
-        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 255, 64, 16, 16, 1, 1), 1),        # N != m b
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 257, 64, 16, 16, 1, 1), 1),        # N > m b
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 240, 64, 16, 16, 1, 1), 1),        # m > ceil(N / b)
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 0, 1), 1),        # T = 0
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 1, 7), 1),        # bad dtype
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 0, 16, 1, 1), 1),         # m = 0
@@ -75,6 +76,10 @@ def test_invalid_arguments_rejected_before_any_hip_call(args, code):
         ((7, 64, 7, 1, 1, 1), True),
         ((8192, 64, 64, 128, 2, 0), True),
         ((16384, 128, 128, 128, 2, 0), False),
+        ((197, 64, 15, 14, 2, 1), True),      # post-padded to 210 rows
+        ((7600, 64, 60, 128, 2, 1), True),
+        ((5, 64, 1, 16, 1, 1), True),
+        ((196, 64, 15, 14, 2, 1), False),     # m != ceil(N / b)
     ],
 )
 def test_supported_shapes(shape, ok):
@@ -93,6 +98,13 @@ def test_workspace_bytes_formula():
     assert got == 3 * state + 2 * cvec
     assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 20, 1) == got  # independent of T
     assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 127, 2, 1) == 0
+    # a padded sequence: the states cover m * b rows
+    padded = ma.monarch_attn_workspace_bytes(1, 1, 197, 64, 15, 14, 2, 1)
+    assert padded == 3 * _align(210 * 64 * 2) + 2 * _align(210 * 4)
+
+
+def _align(x):
+    return (x + 255) // 256 * 256
 
 
 def test_fused_path_applicability():

@@ -254,3 +254,81 @@ def test_fused_and_half_steps_agree_bitwise(lib, dtype, B, H, m, b, T):
     finally:
         lib.monarch_attn_set_path(prev)
     assert torch.equal(got, ref), float((got.float() - ref.float()).abs().max())
+
+
+# -- sequence lengths that are not a multiple of b (post-padding with the key mask) -------
+
+GUARD = 4096  # NaN elements after every tensor: a read past row N shows up as NaN in O
+
+
+def _guarded(torch, x, td):
+    """x [B, H, N, d] as a device view at the start of a NaN-filled buffer."""
+    flat = torch.full((x.size + GUARD,), float("nan"), dtype=td, device="cuda")
+    flat[: x.size].copy_(torch.from_numpy(x.reshape(-1)).to(td))
+    return flat, flat[: x.size].view(x.shape)
+
+
+def gpu_run_padded(ma, q, k, v, m, b, T, dtype):
+    import torch
+
+    td = _torch_dtype(dtype)
+    if ma.path_name == "fused" and not ma.fused_applies(q.shape[-1], m, b, ma.dtype_code(td)):
+        pytest.skip("the fused kernel covers 16-bit elements, d = 64, m and b <= 16")
+    bufs = [_guarded(torch, x, td) for x in (q, k, v)]
+    oflat, out = _guarded(torch, np.full(q.shape, np.nan, dtype=np.float32), td)
+    ma.monarch_attn_fwd(bufs[0][1], bufs[1][1], bufs[2][1], out, m, b, T)
+    torch.cuda.synchronize()
+    assert bool(torch.isnan(oflat[q.size:]).all()), "a store past row N"
+    return out.double().cpu().numpy()
+
+
+@pytest.mark.parametrize(
+    "B,H,n,m,b,T,dtype",
+    [
+        (2, 3, 197, 15, 14, 2, "bf16"),     # ViT-B/16 with its class token: 196 + 1
+        (1, 2, 10, 3, 4, 2, "f32"),
+        (1, 2, 33, 3, 16, 3, "bf16"),
+        (1, 2, 250, 16, 16, 2, "f16"),
+        (1, 1, 130, 2, 128, 2, "bf16"),     # last block holds 2 real keys
+        (2, 2, 1000, 8, 128, 1, "f16"),
+        (1, 1, 7600, 60, 128, 2, "bf16"),   # N = 7600 at b = 128
+        (1, 2, 250, 16, 16, 2, "f32"),
+    ],
+)
+def test_padded_lengths(ma, B, H, n, m, b, T, dtype):
+    q, k, v = si.random_qkv(B, H, n, 64, dtype, seed=n + 31 * b, scale=1.5)
+    ref = oracle.monarch_attention(q, k, v, m, b, T)
+    o = gpu_run_padded(ma, q, k, v, m, b, T, dtype)
+    check(o, ref, dtype, f"padded {dtype} B{B} H{H} N{n} m{m} b{b} T{T}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_padded_single_block_is_exact_attention(ma, dtype):
+    """m = 1 and N < b: exact softmax attention over the N real tokens."""
+    n, b = 5, 16
+    q, k, v = si.random_qkv(1, 2, n, 64, dtype, seed=12, scale=1.5)
+    o = gpu_run_padded(ma, q, k, v, 1, b, 2, dtype)
+    ref = np.stack([[nv.dense_softmax_attention(q[0, h], k[0, h], v[0, h]) for h in range(2)]])
+    check(o, ref, dtype, "padded exact m1 b16 N5")
+
+
+@pytest.mark.parametrize("n,m,b", [(197, 15, 14), (250, 16, 16), (37, 3, 13)])
+def test_fused_and_half_steps_agree_bitwise_padded(lib, n, m, b):
+    import torch
+
+    q, k, v = si.random_qkv(7, 5, n, 64, "bf16", seed=n, scale=1.5)
+    t = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (q, k, v)]
+
+    def run(path):
+        lib.monarch_attn_set_path(path)
+        out = torch.full_like(t[0], float("nan"))
+        lib.monarch_attn_fwd(t[0], t[1], t[2], out, m, b, 2)
+        torch.cuda.synchronize()
+        return out.cpu()
+
+    prev = lib.monarch_attn_set_path(lib.PATH_HALF_STEPS)
+    try:
+        ref, got = run(lib.PATH_HALF_STEPS), run(lib.PATH_FUSED)
+    finally:
+        lib.monarch_attn_set_path(prev)
+    assert torch.equal(got, ref)
