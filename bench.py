@@ -6,7 +6,8 @@ half-step, the Monarch product and the store of O) over one batch of
 synthetic Q, K, V already resident in HBM.  The headline workload is the
 long-sequence speed point (B=1, H=16, N=16384 = 128 x 128, d=64, bf16, T=2);
 the medium point (N=4096 = 64 x 64, T=1) and ViT-B/16 (384 heads, N=196 = 14 x 14,
-T=2, the one-workgroup-per-head kernel) are reported alongside in "also".
+T=2, the one-workgroup-per-head kernel; and N=197 with the class token,
+post-padded to 15 x 14) are reported alongside in "also".
 
 Timed regions (HIP events on the stream the library launches on):
   1. K steps back to back -> ms_per_step and value = B*H*N / time.
@@ -51,24 +52,28 @@ def launch_plan(w):
     c_L (reads c_R after t=1); the last one also reads V and writes Y.  The L
     half-step reads Q, alpha_L, c_L and writes alpha_R, c_R.  The apply reads
     Q, alpha_L, Y, c_L and writes O.  Flops are 2 per multiply-add of the
-    products (beta and alpha contractions, Y and O).
+    products (beta and alpha contractions, Y and O).  Tensors have N rows per
+    head; states and flops cover the Np = m * b rows of the padded sequence
+    (Np = N unless N is not a multiple of b).
     """
     s = 2 if w.dtype in ("bf16", "f16") else 4
     BH, N, d, m, b = w.B * w.H, w.N, w.d, w.m, w.b
-    nd = N * d * s
+    Np = m * b
+    nd, sd = N * d * s, Np * d * s   # one tensor, one state
     plan = []
     for t in range(1, w.T + 1):
         first, last = t == 1, t == w.T
-        rb = 3 * nd + 4 * N + (0 if first else 4 * N)
-        rf = 2 * 2 * N * b * d
+        # R: alpha_R (Q at t=1), K in; alpha_L, c_L out; c_R in after t=1; V in, Y out when last
+        rb = (nd if first else sd) + nd + sd + 4 * Np + (0 if first else 4 * Np)
+        rf = 2 * 2 * Np * b * d
         if last:
-            rb += 2 * nd
-            rf += 2 * N * b * d
+            rb += nd + sd
+            rf += 2 * Np * b * d
         plan.append(("r_half_step_final" if last else "r_half_step", BH * rb, BH * rf))
-        if last:
-            plan.append(("monarch_apply", BH * (4 * nd + 4 * N), BH * 2 * 2 * N * m * d))
-        else:
-            plan.append(("l_half_step", BH * (3 * nd + 8 * N), BH * 2 * 2 * N * m * d))
+        if last:  # Q, alpha_L, Y, c_L in; O out
+            plan.append(("monarch_apply", BH * (2 * nd + 2 * sd + 4 * Np), BH * 2 * 2 * Np * m * d))
+        else:     # Q, alpha_L, c_L in; alpha_R, c_R out
+            plan.append(("l_half_step", BH * (nd + 2 * sd + 8 * Np), BH * 2 * 2 * Np * m * d))
     return plan
 
 
@@ -85,10 +90,12 @@ def plan_for(w, kinds):
 
 
 def call_work(w):
+    """Compulsory bytes (Q, K, V in, O out: N rows) and flops of the method
+    (on the Np = m * b rows it runs over) of one call."""
     s = 2 if w.dtype in ("bf16", "f16") else 4
-    BH = w.B * w.H
+    BH, Np = w.B * w.H, w.m * w.b
     compulsory = BH * 4 * w.N * w.d * s
-    macs = w.T * (2 * w.N * w.b * w.d + 2 * w.N * w.m * w.d) + w.N * w.b * w.d
+    macs = w.T * (2 * Np * w.b * w.d + 2 * Np * w.m * w.d) + Np * w.b * w.d
     return compulsory, 2 * BH * macs
 
 
@@ -251,7 +258,7 @@ def main():
     ap.add_argument("--workload", default="speed_n16384")
     ap.add_argument("--d", type=int, default=None, help="override the head dimension")
     ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
-    ap.add_argument("--also", default="speed_n4096,vit_b16_n196",
+    ap.add_argument("--also", default="speed_n4096,vit_b16_n196,vit_b16_n197",
                     help="comma-separated extra workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-mb", type=str, default=None,

@@ -65,8 +65,11 @@ typedef enum {
  *           of every R softmax (omega = -inf on Z_R), and only the N real rows
  *           of out are written.  The padded query rows take part in the
  *           iteration like the others.  Supported: 1 <= m, b <= 128.
- * d       : head dimension; supported: 64 or 128.  fp32 also needs
- *           16*ceil(m/16)*d <= 8192 and 16*ceil(b/16)*d <= 8192.
+ * d       : head dimension; supported: d <= 128, a multiple of 8 (bf16,
+ *           fp16) or 4 (fp32), so that every row is a whole number of 16-byte
+ *           chunks.  The kernels work on tiles of width D = 64, 96 or 128
+ *           (the smallest that holds d) with the extra columns zero.  fp32
+ *           also needs 16*ceil(m/16)*D <= 8192 and 16*ceil(b/16)*D <= 8192.
  * T       : number of (R, L) update pairs, 1 <= T <= 64.
  * dtype   : an ma_dtype value.
  * stream  : the hipStream_t to launch on (NULL = the null stream).
@@ -74,7 +77,7 @@ typedef enum {
  * Asynchronous on `stream`: returns after enqueueing, with no host
  * synchronisation.  Arguments are checked before any HIP call; on MA_EINVAL or
  * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  Path 1 (see
- * monarch_attn_set_path) uses one device workspace per device (3 m b d
+ * monarch_attn_set_path) uses one device workspace per device (3 m b D
  * elements plus 2 m b floats per head), grown with hipMalloc on the first call
  * that needs more; calls on different streams of one device must not overlap
  * (they share it).  After
@@ -110,7 +113,7 @@ int monarch_attn_release_workspace(void);
  *      workspace);
  *   2  one workgroup per (batch, head) running every half-step with Q, K and
  *      all states in LDS (the fully fused one-head-per-block kernel for short
- *      sequences, Sec. 4, paragraph "Benchmarking"): bf16 or fp16, d = 64,
+ *      sequences, Sec. 4, paragraph "Benchmarking"): bf16 or fp16, d <= 64,
  *      m <= 16 and b <= 16; any other shape returns MA_EUNSUPPORTED.  Uses
  *      no workspace.
  * Both paths compute the same operation with the same per-unit arithmetic.

@@ -130,7 +130,7 @@ def monarch_attn_check(N: int, d: int, m: int, b: int, T: int, dtype: int) -> in
 
 def fused_applies(d: int, m: int, b: int, dtype: int) -> bool:
     """Whether the one-workgroup-per-head kernel covers this shape (PATH_AUTO takes it then)."""
-    return dtype in (MA_BF16, MA_F16) and d == 64 and m <= 16 and b <= 16
+    return dtype in (MA_BF16, MA_F16) and d <= 64 and m <= 16 and b <= 16
 
 
 def monarch_attn_workspace_bytes(B, H, N, d, m, b, T, dtype) -> int:

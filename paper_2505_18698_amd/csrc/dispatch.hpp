@@ -195,11 +195,15 @@ template <typename T> int run_fused(Launcher &L, const CallBufs &B, ma::HeadDims
 template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const CallDims &c, int path)
 {
     const int32_t dtype = std::is_same<T, float>::value ? MA_F32 : std::is_same<T, __bf16>::value ? MA_BF16 : MA_F16;
-    ma::HeadDims hd{c.m, c.b, c.n, c.s_log2e, 0};
+    ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};
     if (path == kFusedHead && !fused_applies(dtype, c.d, c.m, c.b))
-        return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d = 64 and m, b <= 16");
+        return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d <= 64 and m, b <= 16");
     if (uses_fused(path, dtype, c.d, c.m, c.b)) return run_fused<T>(L, B, hd, c);
-    return c.d == 64 ? run_half_steps<T, 64>(L, B, hd, c) : run_half_steps<T, 128>(L, B, hd, c);
+    switch (tile_d(c.d)) {
+    case 64: return run_half_steps<T, 64>(L, B, hd, c);
+    case 96: return run_half_steps<T, 96>(L, B, hd, c);
+    default: return run_half_steps<T, 128>(L, B, hd, c);
+    }
 }
 
 }  // namespace ma_host

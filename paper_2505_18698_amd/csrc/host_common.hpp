@@ -72,11 +72,14 @@ struct CallDims {
 // half-step; 2 = the fused kernel or MA_EUNSUPPORTED.
 enum Path { kAuto = 0, kHalfSteps = 1, kFusedHead = 2 };
 
+// Tile width of the kernels for head dimension d (columns d..D-1 are zero).
+inline int tile_d(int64_t d) { return d <= 64 ? 64 : d <= 96 ? 96 : 128; }
+
 // The fused one-workgroup-per-head kernel holds Q, K and all states of a head
-// in LDS: 16-bit elements, d = 64, m and b at most 16.
+// in LDS: 16-bit elements, d <= 64, m and b at most 16.
 inline bool fused_applies(int32_t dtype, int64_t d, int64_t m, int64_t b)
 {
-    return (dtype == MA_BF16 || dtype == MA_F16) && d == 64 && m <= 16 && b <= 16;
+    return (dtype == MA_BF16 || dtype == MA_F16) && d <= 64 && m <= 16 && b <= 16;
 }
 
 // Whether a call with these arguments runs the fused kernel under `path`.

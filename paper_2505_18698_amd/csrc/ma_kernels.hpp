@@ -173,13 +173,14 @@ template <typename T, int NR, int D, int NTH> struct TileChunks {
     static_assert(NR * CPR % NTH == 0, "whole chunks per thread");
     u32x4 c[CH];
 
-    template <typename RowPtr> __device__ inline void fetch(RowPtr rowptr, int valid, int tid)
+    // (columns >= dcols, a multiple of V, are zero as well)
+    template <typename RowPtr> __device__ inline void fetch(RowPtr rowptr, int valid, int tid, int dcols = D)
     {
 #pragma unroll
         for (int h = 0; h < CH; ++h) {
             const int idx = tid + h * NTH, r = idx / CPR, col = (idx % CPR) * V;
             c[h] = u32x4{0u, 0u, 0u, 0u};
-            if (r < valid) c[h] = *reinterpret_cast<const u32x4 *>(rowptr(r) + col);
+            if (r < valid && col < dcols) c[h] = *reinterpret_cast<const u32x4 *>(rowptr(r) + col);
         }
     }
 
@@ -213,11 +214,12 @@ template <typename T, int D> struct RowFrags {
     using M = Mma<T>;
     typename M::frag f[D / M::KC];
     // from global memory (row == nullptr: a zero row)
-    __device__ inline void load(const T *row, int g)
+    // (columns >= dcols: zero; dcols is a multiple of KPL)
+    __device__ inline void load(const T *row, int g, int dcols = D)
     {
 #pragma unroll
         for (int c = 0; c < D / M::KC; ++c) {
-            if (row) {
+            if (row && c * M::KC + g * M::KPL < dcols) {
                 f[c] = *reinterpret_cast<const typename M::frag *>(row + c * M::KC + g * M::KPL);
             } else {
                 f[c] = typename M::frag{};
@@ -453,14 +455,16 @@ __device__ inline float lanegroup_sum(float x)
 // elements 16vt + 4g + q of row lane%16) to the row `row` (nullptr: skip).
 // Lanes 16g and 16(g^1) swap halves so that every lane writes 16-byte
 // chunks: each row receives 64 contiguous bytes per store instruction.
+// Columns >= dcols (a multiple of 16 bytes' worth of elements) are not written.
 template <typename T, int D>
-__device__ inline void store_row(T *row, const f32x4 *acc, float scale, int lane)
+__device__ inline void store_row(T *row, const f32x4 *acc, float scale, int lane, int dcols = D)
 {
     const int g = lane >> 4;
     if constexpr (std::is_same<T, float>::value) {
         if (row) {
 #pragma unroll
-            for (int vt = 0; vt < D / 16; ++vt) *reinterpret_cast<f32x4 *>(row + 16 * vt + 4 * g) = acc[vt] * scale;
+            for (int vt = 0; vt < D / 16; ++vt)
+                if (16 * vt + 4 * g < dcols) *reinterpret_cast<f32x4 *>(row + 16 * vt + 4 * g) = acc[vt] * scale;
         }
     } else {
         const bool odd = g & 1;
@@ -480,7 +484,8 @@ __device__ inline void store_row(T *row, const f32x4 *acc, float scale, int lane
             got[1] = xor16_value(give[1], odd);
             const u32x4 chunk = odd ? u32x4{got[0], got[1], pk[1][0], pk[1][1]}
                                     : u32x4{pk[0][0], pk[0][1], got[0], got[1]};
-            if (row) *reinterpret_cast<u32x4 *>(row + 16 * (2 * i + (odd ? 1 : 0)) + 8 * (g >> 1)) = chunk;
+            const int col = 16 * (2 * i + (odd ? 1 : 0)) + 8 * (g >> 1);
+            if (row && col < dcols) *reinterpret_cast<u32x4 *>(row + col) = chunk;
         }
     }
 }
@@ -498,6 +503,7 @@ template <typename T, int D> __device__ inline void store_row_lds(T *row, const 
 struct HeadDims {
     int m, b;          // blocks and block size
     int n;             // rows of q, k, v, out per head, (m - 1) * b < n <= m * b
+    int d;             // head dimension of q, k, v, out (<= the tile width D; the states use D)
     float s_log2e;     // log2(e) / sqrt(d)
     int64_t units;     // work units of a half-step launch (grid size)
 };
@@ -510,7 +516,7 @@ __device__ inline int block_keys(const HeadDims &hd, int k) { return min(hd.b, h
 // rows >= n of q, k, v are never read (zero is loaded instead), keys >= n are
 // masked out of every R softmax, rows >= n of out are never written, and the
 // states cover all N rows.  Layouts (per head):
-//   q, k, v, out [B*H][n][D];
+//   q, k, v, out [B*H][n][d], d <= D (columns d..D-1 of every tile are zero);
 //   alpha_R [m][b][D] (row k*b + j), alpha_L and Y [b][m][D] (row j*m + k),
 //   c_L [m][b] (written by the R half-step of block k for all j),
 //   c_R [b][m] (written by the L half-step of class j for all k).
@@ -547,24 +553,25 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, int tid, Regs &gr)
     {
         const int m = hd.m, b = hd.b, kv = block_keys(hd, k);
-        const int64_t N = (int64_t)m * b, hoff = bh * N * D, toff = bh * (int64_t)hd.n * D;
+        const int dd = hd.d;
+        const int64_t N = (int64_t)m * b, hoff = bh * N * D, toff = bh * (int64_t)hd.n * dd;
         const int lane = tid & 63, wave = tid >> 6;
-        const T *kblk = p.k + toff + (int64_t)k * b * D;
-        gr.kt.fetch([=](int r) { return kblk + (int64_t)r * D; }, kv, tid);
+        const T *kblk = p.k + toff + (int64_t)k * b * dd;
+        gr.kt.fetch([=](int r) { return kblk + (int64_t)r * dd; }, kv, tid, dd);
         if constexpr (FINAL) {
-            const T *vblk = p.v + toff + (int64_t)k * b * D;
-            gr.vt.fetch([=](int r) { return vblk + (int64_t)r * D; }, kv, tid);
+            const T *vblk = p.v + toff + (int64_t)k * b * dd;
+            gr.vt.fetch([=](int r) { return vblk + (int64_t)r * dd; }, kv, tid, dd);
         }
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int j = (wave * RT + r) * 16 + (lane & 15);
             const T *row = nullptr;  // alpha_R[k][j]; at t = 1 Q row k*b + j (zero if padding)
             if constexpr (FIRST) {
-                if (j < kv) row = p.q + toff + ((int64_t)k * b + j) * D;
+                if (j < kv) row = p.q + toff + ((int64_t)k * b + j) * dd;
             } else {
                 if (j < b) row = p.aR + hoff + ((int64_t)k * b + j) * D;
             }
-            gr.bf[r].load(row, lane >> 4);
+            gr.bf[r].load(row, lane >> 4, FIRST ? dd : D);
             gr.cr[r] = 1.0f;
             if constexpr (!FIRST) {
                 if (j < b) gr.cr[r] = p.cR[bh * N + (int64_t)j * m + k];
@@ -688,10 +695,11 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
     {
         const int m = hd.m, b = hd.b;
         const int64_t N = (int64_t)m * b, hoff = bh * N * D;
-        const T *qh = p.q + bh * (int64_t)hd.n * D;
+        const int dd = hd.d;
+        const T *qh = p.q + bh * (int64_t)hd.n * dd;
         const T *al = p.aL + hoff + (int64_t)j * m * D;
         const int ml = (hd.n - j + b - 1) / b;  // real rows l of class j: l*b + j < n
-        gr.qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * D; }, ml, tid);
+        gr.qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * dd; }, ml, tid, dd);
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
     }
@@ -824,8 +832,9 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int l = (wave * RT + r) * 16 + (lane & 15);
-            gr.bf[r].load((int64_t)l * b + j < hd.n ? p.q + bh * (int64_t)hd.n * D + ((int64_t)l * b + j) * D : nullptr,
-                          lane >> 4);  // Qbar[j][l]; zero for padded rows
+            gr.bf[r].load((int64_t)l * b + j < hd.n ? p.q + bh * (int64_t)hd.n * hd.d + ((int64_t)l * b + j) * hd.d
+                                                    : nullptr,
+                          lane >> 4, hd.d);  // Qbar[j][l]; zero for padded rows
         }
     }
 
@@ -900,9 +909,10 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         }
 #pragma unroll
         for (int r = 0; r < RT; ++r)
-            store_row<T, D>((int64_t)lr[r] * b + j < hd.n ? p.out + bh * (int64_t)hd.n * D + ((int64_t)lr[r] * b + j) * D
-                                                         : nullptr,
-                            o[r], inv[r], lane);
+            store_row<T, D>((int64_t)lr[r] * b + j < hd.n
+                                ? p.out + bh * (int64_t)hd.n * hd.d + ((int64_t)lr[r] * b + j) * hd.d
+                                : nullptr,
+                            o[r], inv[r], lane, hd.d);
     }
 };
 
@@ -995,7 +1005,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
     struct Ctx {
         T *Qs, *Ks, *As, *Rs;
         float *cRs, *cLs;  // c_R[k][j] at k*CS + j, c_L[j][k] at j*CS + k
-        int m, b, n, lane, g, c16;  // n: real rows of the head (rows >= n are zero padding)
+        int m, b, n, d, lane, g, c16;  // n: real rows of the head (rows >= n are zero padding); d <= D
         float s_log2e;
     };
 
@@ -1105,7 +1115,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         f32x4 o[D / 16];  // O[l*b + j] = sum_k L[j][k][l] Y[k][j]; Y[k][j] is row k of Ks + j*LD at stride BS
 #pragma unroll
         for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, 1>(c.Ks + j * LD, BS, 16 * vt, pf, c.lane);
-        store_row<T, D>(l * c.b + j < c.n ? out_h + ((int64_t)l * c.b + j) * D : nullptr, o, 1.0f, c.lane);
+        store_row<T, D>(l * c.b + j < c.n ? out_h + ((int64_t)l * c.b + j) * c.d : nullptr, o, 1.0f, c.lane, c.d);
     }
 
     static constexpr int PER = 2 * 256 * 8 / (64 * NW);  // 16-byte chunks of Qs and Ks per thread
@@ -1113,28 +1123,29 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
     // Issue the loads of head bh: Qbar and Kbar chunks (zero where there is no
     // row) for the LDS regions, and Vbar[w] for wave w's last R half-step.
     // Rows >= n (padding) are zero and never read.
-    __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int64_t bh, int tid, u32x4 *raw,
+    // Rows >= n (padding) and columns >= d are zero and never read.
+    __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int d, int64_t bh, int tid, u32x4 *raw,
                                      u32x4 *vb)
     {
-        const int64_t hoff = bh * (int64_t)n * D;
+        const int64_t hoff = bh * (int64_t)n * d;
         const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
 #pragma unroll
         for (int h = 0; h < PER; ++h) {
             const int idx = tid + h * 64 * NW;
             const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
             raw[h] = u32x4{0u, 0u, 0u, 0u};
-            if (reg == 0 && blk < b && r < m && r * b + blk < n)
-                raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * D + col);  // Qbar[blk][r]
-            if (reg == 1 && blk < m && r < b && blk * b + r < n)
-                raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * D + col);  // Kbar[blk][r]
+            if (reg == 0 && blk < b && r < m && r * b + blk < n && col < d)
+                raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * d + col);  // Qbar[blk][r]
+            if (reg == 1 && blk < m && r < b && blk * b + r < n && col < d)
+                raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * d + col);  // Kbar[blk][r]
         }
         const int w = tid >> 6, lane = tid & 63;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int r = (lane >> 3) + 8 * h, col = (lane & 7) * 8;
             vb[h] = u32x4{0u, 0u, 0u, 0u};
-            if (w < m && r < b && w * b + r < n)
-                vb[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * D + col);
+            if (w < m && r < b && w * b + r < n && col < d)
+                vb[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * d + col);
         }
     }
 
@@ -1162,6 +1173,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         c.m = hd.m;
         c.b = hd.b;
         c.n = hd.n;
+        c.d = hd.d;
         c.s_log2e = hd.s_log2e;
         const int tid = threadIdx.x, w = tid >> 6;
         c.lane = tid & 63;
@@ -1171,13 +1183,13 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
 
         u32x4 raw[PER], vcur[2], vnext[2];
         int64_t bh = blockIdx.x;
-        load_head(p, m, b, c.n, bh, tid, raw, vcur);
+        load_head(p, m, b, c.n, c.d, bh, tid, raw, vcur);
         for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) *chunk(c.As, idx) = u32x4{0u, 0u, 0u, 0u};
         for (; bh < BH; bh += gridDim.x) {
 #pragma unroll
             for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
             __syncthreads();
-            if (bh + gridDim.x < BH) load_head(p, m, b, c.n, bh + gridDim.x, tid, raw, vnext);
+            if (bh + gridDim.x < BH) load_head(p, m, b, c.n, c.d, bh + gridDim.x, tid, raw, vnext);
 
             for (int t = 1; t <= T_; ++t) {
                 const bool first = t == 1, last = t == T_;
@@ -1196,7 +1208,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
                 if (w < b) l_unit(c, w);
                 __syncthreads();
             }
-            if (w < b) apply_unit(c, w, p.out + bh * (int64_t)c.n * D);
+            if (w < b) apply_unit(c, w, p.out + bh * (int64_t)c.n * c.d);
             vcur[0] = vnext[0];
             vcur[1] = vnext[1];
             __syncthreads();  // the apply has read Qs, As and Ks

@@ -45,20 +45,31 @@ int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t d
     if (T < 1) return fail(MA_EINVAL, "T must be >= 1 (got %d)", T);
     if (T > 64) return fail(MA_EUNSUPPORTED, "T > 64 is not supported (got %d)", T);
     if (m > 128 || b > 128) return fail(MA_EUNSUPPORTED, "m and b must be <= 128 (got m=%lld, b=%lld)", (long long)m, (long long)b);
-    if (d != 64 && d != 128) return fail(MA_EUNSUPPORTED, "d must be 64 or 128 (got %lld)", (long long)d);
-    if (dtype == MA_F32 && ((int64_t)pad16(m) * d > 8192 || (int64_t)pad16(b) * d > 8192))
-        return fail(MA_EUNSUPPORTED, "fp32 needs 16*ceil(m/16)*d <= 8192 and 16*ceil(b/16)*d <= 8192");
+    // rows of 16-byte multiples (so every row of q, k, v, out is 16-byte aligned), at most 128 wide
+    if (d > 128 || d % (16 / (int64_t)elem_bytes(dtype)) != 0)
+        return fail(MA_EUNSUPPORTED, "d must be a multiple of %d up to 128 (got %lld)", (int)(16 / elem_bytes(dtype)),
+                    (long long)d);
+    const int64_t D = tile_d(d);
+    if (dtype == MA_F32 && ((int64_t)pad16(m) * D > 8192 || (int64_t)pad16(b) * D > 8192))
+        return fail(MA_EUNSUPPORTED, "fp32 needs 16*ceil(m/16)*D <= 8192 and 16*ceil(b/16)*D <= 8192, D = %lld",
+                    (long long)D);
     return MA_OK;
 }
 
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Np = m * b: the states cover the padded sequence.
+// Np = m * b: the states cover the padded sequence, with rows of the tile
+// width D = tile_d(d).
+size_t state_bytes(int64_t BH, int64_t Np, int64_t d, int32_t dtype)
+{
+    return align_up((size_t)BH * Np * tile_d(d) * elem_bytes(dtype));
+}
+
 size_t workspace_bytes(int64_t BH, int64_t Np, int64_t d, int32_t dtype)
 {
     // alpha_R, alpha_L and Y in the element type, c_R and c_L in fp32
-    const size_t st = align_up((size_t)BH * Np * d * elem_bytes(dtype));
+    const size_t st = state_bytes(BH, Np, d, dtype);
     const size_t cs = align_up((size_t)BH * Np * sizeof(float));
     return 3 * st + 2 * cs;
 }
@@ -184,7 +195,7 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
         return fail(MA_EINVAL, "out must not overlap q, k or v");
 
     const int path = g_path.load();
-    const size_t st = align_up((size_t)BH * m * b * d * elem_bytes(dtype));
+    const size_t st = state_bytes(BH, m * b, d, dtype);
     const size_t cs = align_up((size_t)BH * m * b * sizeof(float));
     CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr};
     int dev = 0;

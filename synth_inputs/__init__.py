@@ -53,10 +53,11 @@ class Workload:
     T: int
     dtype: str
     recipe: str
+    n: int = 0  # sequence length when it is not m * b (post-padded to m * b rows); 0: m * b
 
     @property
     def N(self) -> int:
-        return self.m * self.b
+        return self.n or self.m * self.b
 
     def with_(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -81,6 +82,8 @@ class Workload:
 WORKLOADS = {
     "tiny_f32_n256": Workload("tiny_f32_n256", 1, 1, 16, 16, 64, 1, "f32", "iid"),
     "vit_b16_n196": Workload("vit_b16_n196", 32, 12, 14, 14, 64, 2, "bf16", "vit"),
+    # ViT-B/16 with its class token: N = 197, post-padded to 15 blocks of 14
+    "vit_b16_n197": Workload("vit_b16_n197", 32, 12, 15, 14, 64, 2, "bf16", "vit", n=197),
     "roberta_n1024": Workload("roberta_n1024", 16, 12, 32, 32, 64, 2, "bf16", "lm"),
     "speed_n4096": Workload("speed_n4096", 1, 16, 64, 64, 64, 1, "bf16", "speed"),
     "speed_n16384": Workload("speed_n16384", 1, 16, 128, 128, 64, 2, "bf16", "speed"),

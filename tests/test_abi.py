@@ -48,7 +48,9 @@ FAKE = 1 << 20  # an aligned non-null address that is never dereferenced: every 
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 0, 16, 1, 1), 1),         # m = 0
         ((FAKE + 2, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),    # misaligned q
         ((FAKE, FAKE, FAKE, FAKE + 64, 1, 1, 256, 64, 16, 16, 1, 1), 1),       # out overlaps q
-        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 96, 16, 16, 1, 1), 2),        # d = 96
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 100, 16, 16, 1, 1), 2),       # d not a multiple of 8
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 136, 16, 16, 1, 1), 2),       # d > 128
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 6, 16, 16, 1, 0), 2),         # fp32 d not a multiple of 4
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 512, 64, 2, 256, 1, 1), 2),        # b > 128
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 65, 1), 2),       # T > 64
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 16384, 128, 128, 128, 1, 0), 2),   # fp32 tile too big
@@ -80,6 +82,12 @@ def test_invalid_arguments_rejected_before_any_hip_call(args, code):
         ((7600, 64, 60, 128, 2, 1), True),
         ((5, 64, 1, 16, 1, 1), True),
         ((196, 64, 15, 14, 2, 1), False),     # m != ceil(N / b)
+        ((256, 72, 16, 16, 3, 1), True),      # DiT head dimension
+        ((7600, 48, 60, 128, 2, 1), True),    # GPS head dimension
+        ((256, 96, 16, 16, 2, 2), True),
+        ((256, 36, 16, 16, 2, 0), True),      # fp32: multiples of 4
+        ((256, 100, 16, 16, 2, 1), False),
+        ((16384, 96, 128, 128, 2, 0), False), # fp32 tile too big at D = 96
     ],
 )
 def test_supported_shapes(shape, ok):
@@ -101,6 +109,8 @@ def test_workspace_bytes_formula():
     # a padded sequence: the states cover m * b rows
     padded = ma.monarch_attn_workspace_bytes(1, 1, 197, 64, 15, 14, 2, 1)
     assert padded == 3 * _align(210 * 64 * 2) + 2 * _align(210 * 4)
+    # d = 72: states in tiles of width 96
+    assert ma.monarch_attn_workspace_bytes(1, 2, 256, 72, 16, 16, 2, 1) == 3 * _align(2 * 256 * 96 * 2) + 2 * _align(2 * 256 * 4)
 
 
 def _align(x):

@@ -332,3 +332,41 @@ def test_fused_and_half_steps_agree_bitwise_padded(lib, n, m, b):
     finally:
         lib.monarch_attn_set_path(prev)
     assert torch.equal(got, ref)
+
+
+# -- other head dimensions and rectangular blocks ----------------------------------------
+
+@pytest.mark.parametrize(
+    "B,H,n,m,b,d,T,dtype",
+    [
+        (2, 4, 256, 16, 16, 72, 3, "bf16"),    # DiT-XL: N = 256, d = 72, b = 16, T = 3
+        (1, 2, 7600, 60, 128, 48, 2, "bf16"),  # GPS: N = 7600, b = 128, d = 48
+        (1, 3, 256, 16, 16, 48, 2, "f16"),
+        (1, 2, 512, 16, 32, 96, 2, "bf16"),
+        (1, 2, 200, 10, 20, 120, 2, "f16"),
+        (1, 2, 100, 10, 10, 80, 2, "bf16"),
+        (1, 2, 256, 16, 16, 36, 2, "f32"),
+        (1, 2, 96, 8, 12, 68, 2, "f32"),
+        (2, 2, 197, 15, 14, 56, 2, "bf16"),
+    ],
+)
+def test_other_head_dims(ma, B, H, n, m, b, d, T, dtype):
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=d * 13 + n, scale=1.5)
+    ref = oracle.monarch_attention(q, k, v, m, b, T)
+    o = gpu_run_padded(ma, q, k, v, m, b, T, dtype)
+    check(o, ref, dtype, f"{dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T}")
+
+
+@pytest.mark.parametrize(
+    "n,m,b,T",
+    [
+        (384, 16, 24, 1), (384, 8, 48, 1), (384, 4, 96, 1), (384, 3, 128, 1),   # RoBERTa b sweep at N = 384
+        (2048, 64, 32, 2), (8192, 128, 64, 2),                                  # BART b = 32 and b = 64
+    ],
+)
+def test_rectangular_blocks(ma, n, m, b, T):
+    q, k, v = si.random_qkv(1, 3, n, 64, "bf16", seed=n + b, scale=1.5)
+    heads = [0, 2]
+    o = gpu_run_padded(ma, q, k, v, m, b, T, "bf16")
+    ref = oracle.monarch_attention(q[:, heads], k[:, heads], v[:, heads], m, b, T)
+    check(o[:, heads], ref, "bf16", f"rect N{n} m{m} b{b} T{T}")
