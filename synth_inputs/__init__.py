@@ -77,8 +77,9 @@ class Workload:
         }
 
 
-# The five workloads: a tiny fp32 parity case, ViT-B/16- and RoBERTa-base-
-# shaped attention, and the 4K / 16K speed points.
+# The workloads: a tiny fp32 parity case, ViT-B/16- and RoBERTa-base-shaped
+# attention, the 4K / 16K speed points, and further shapes of the paper's
+# conversions.
 WORKLOADS = {
     "tiny_f32_n256": Workload("tiny_f32_n256", 1, 1, 16, 16, 64, 1, "f32", "iid"),
     "vit_b16_n196": Workload("vit_b16_n196", 32, 12, 14, 14, 64, 2, "bf16", "vit"),
@@ -87,6 +88,20 @@ WORKLOADS = {
     "roberta_n1024": Workload("roberta_n1024", 16, 12, 32, 32, 64, 2, "bf16", "lm"),
     "speed_n4096": Workload("speed_n4096", 1, 16, 64, 64, 64, 1, "bf16", "speed"),
     "speed_n16384": Workload("speed_n16384", 1, 16, 128, 128, 64, 2, "bf16", "speed"),
+    # Shapes of the paper's other conversions, for measurement beside the
+    # workloads above (synthetic inputs with the same recipes):
+    # DiT-XL/2 at 256 x 256 (16 heads, N = 256, d = 72, b = 16, T = 3), 32 images
+    "dit_xl_n256": Workload("dit_xl_n256", 32, 16, 16, 16, 72, 3, "bf16", "vit"),
+    # RoBERTa-base on SQuAD at N = 384, T = 1, the b sweep (m = ceil(384 / b))
+    "roberta_n384_b24": Workload("roberta_n384_b24", 16, 12, 16, 24, 64, 1, "bf16", "lm"),
+    "roberta_n384_b48": Workload("roberta_n384_b48", 16, 12, 8, 48, 64, 1, "bf16", "lm"),
+    "roberta_n384_b96": Workload("roberta_n384_b96", 16, 12, 4, 96, 64, 1, "bf16", "lm"),
+    "roberta_n384_b128": Workload("roberta_n384_b128", 16, 12, 3, 128, 64, 1, "bf16", "lm"),
+    # BART-base encoder (12 heads, d = 64): b = 32 at N = 2048, b = 64 at N = 8192
+    "bart_n2048_b32": Workload("bart_n2048_b32", 1, 12, 64, 32, 64, 2, "bf16", "lm"),
+    "bart_n8192_b64": Workload("bart_n8192_b64", 1, 12, 128, 64, 64, 2, "bf16", "lm"),
+    # graph transformer node classification: N = 7600 nodes, b = 128, d = 48
+    "gps_n7600": Workload("gps_n7600", 1, 4, 60, 128, 48, 2, "bf16", "vit", n=7600),
 }
 
 
