@@ -942,14 +942,8 @@ template <typename U, typename T> __device__ inline void run_units(const Bufs<T>
     }
 }
 
-#ifdef MA_MAX_WAVES
-#define MA_HALF_STEP_ATTR __attribute__((amdgpu_waves_per_eu(MA_MAX_WAVES, MA_MAX_WAVES)))
-#else
-#define MA_HALF_STEP_ATTR
-#endif
-
 template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED>
-__global__ __launch_bounds__(64 * Split<NB / 16>::W) MA_HALF_STEP_ATTR void r_half_step(Bufs<T> p, HeadDims hd)
+__global__ __launch_bounds__(64 * Split<NB / 16>::W) void r_half_step(Bufs<T> p, HeadDims hd)
 {
     using U = RHalf<T, NB, D, FIRST, FINAL, RAGGED>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
@@ -957,7 +951,7 @@ __global__ __launch_bounds__(64 * Split<NB / 16>::W) MA_HALF_STEP_ATTR void r_ha
 }
 
 template <typename T, int NM, int D, bool RAGGED>
-__global__ __launch_bounds__(64 * Split<NM / 16>::W) MA_HALF_STEP_ATTR void l_half_step(Bufs<T> p, HeadDims hd)
+__global__ __launch_bounds__(64 * Split<NM / 16>::W) void l_half_step(Bufs<T> p, HeadDims hd)
 {
     using U = LHalf<T, NM, D, RAGGED>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
@@ -965,7 +959,7 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) MA_HALF_STEP_ATTR void l_ha
 }
 
 template <typename T, int NM, int D, bool RAGGED>
-__global__ __launch_bounds__(64 * Split<NM / 16>::W) MA_HALF_STEP_ATTR void monarch_apply(Bufs<T> p, HeadDims hd)
+__global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> p, HeadDims hd)
 {
     using U = Apply<T, NM, D, RAGGED>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
