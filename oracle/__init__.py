@@ -50,6 +50,8 @@ def _load():
                                                  ctypes.POINTER(ctypes.c_int64), i64, i32]
         lib.ma_oracle_dense_attn_f64.restype = ctypes.c_int
         lib.ma_oracle_max_threads.restype = ctypes.c_int
+        lib.ma_oracle_fwd_obj_f64.argtypes = [dp, dp, dp, dp, dp, i64, i64, i64, i64, i64, i64, i32, i32]
+        lib.ma_oracle_fwd_obj_f64.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -70,6 +72,23 @@ def monarch_attention(q, k, v, m: int, b: int, T: int, threads: int = 0) -> np.n
     if rc != 0:
         raise ValueError(f"oracle rejected the arguments (code {rc})")
     return out
+
+
+def monarch_attention_objective(q, k, v, m: int, b: int, T: int, threads: int = 0):
+    """(O, f): O as monarch_attention, and f[B, H, T], the objective f(M^(t); Q, K)
+    of Sec. 3 after every step t, in its separable form (on all m*b rows of the
+    padded problem when N < m*b)."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    B, H, N, d = q.shape
+    out = np.empty_like(q)
+    obj = np.empty((B, H, T))
+    rc = _load().ma_oracle_fwd_obj_f64(_dptr(q), _dptr(k), _dptr(v), _dptr(out), _dptr(obj),
+                                       B, H, N, d, m, b, T, threads)
+    if rc != 0:
+        raise ValueError(f"oracle rejected the arguments (code {rc})")
+    return out, obj
 
 
 def dense_attention_rows(q, k, v, rows=None, threads: int = 0) -> np.ndarray:

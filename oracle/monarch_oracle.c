@@ -112,12 +112,20 @@ static void r_half_step(const double *Kh, const double *Vh, const double *aR, co
 /* One L half-step for unit (head, j), eq. L_update and beta_l.  Qs is s*Q of
  * this head.  When O == NULL it accumulates aR[k][j][:] and cR[k][j] for the
  * next R half-step (eq. beta_r); otherwise it forms O[l*b + j] from Y (eq.
- * monarch_multiply). */
+ * monarch_multiply).  When fj != NULL it also accumulates aR, cR and writes
+ * to *fj the share of class j of the objective f(M) of the current factors,
+ * in the separable form of Sec. 3 ("Softmax Objective"):
+ *   sum_k <alpha_R[k][j], alpha_L[j][k]> + (1^T R_kj) H(L_jk) + (1^T L_jk) H(R_kj),
+ * with 1^T R_kj = 1, 1^T L_jk = c_R[k][j], H(R_kj) = -c_L[j][k] and
+ * H(L_jk) = -sum_l L log L (hl: m doubles of scratch). */
 static void l_half_step(const double *Qs, const double *aL, const double *cL, const double *Y,
                         double *aR, double *cR, double *O, int64_t m, int64_t b, int64_t d,
-                        int64_t j, double *z)
+                        int64_t j, double *z, double *fj, double *hl)
 {
-    if (!O) {
+    if (fj) {
+        for (int64_t k = 0; k < m; ++k) hl[k] = 0.0;
+    }
+    if (!O || fj) {
         for (int64_t k = 0; k < m; ++k) {
             cR[k * b + j] = 0.0;
             memset(aR + (k * b + j) * d, 0, (size_t)d * sizeof(double));
@@ -139,13 +147,18 @@ static void l_half_step(const double *Qs, const double *aL, const double *cL, co
             sum += z[k];
         }
         for (int64_t k = 0; k < m; ++k) z[k] /= sum; /* z now holds L[j][:][l] */
-        if (!O) {
+        if (fj) {
+            for (int64_t k = 0; k < m; ++k)
+                if (z[k] > 0.0) hl[k] -= z[k] * log(z[k]);
+        }
+        if (!O || fj) {
             for (int64_t k = 0; k < m; ++k) {
                 cR[k * b + j] += z[k];
                 double *ar = aR + (k * b + j) * d;
                 for (int64_t v = 0; v < d; ++v) ar[v] += z[k] * qb[v];
             }
-        } else {
+        }
+        if (O) {
             double *o = O + (l * b + j) * d;
             for (int64_t v = 0; v < d; ++v) {
                 double acc = 0.0;
@@ -154,11 +167,24 @@ static void l_half_step(const double *Qs, const double *aL, const double *cL, co
             }
         }
     }
+    if (fj) {
+        double f = 0.0;
+        for (int64_t k = 0; k < m; ++k) {
+            const double *ar = aR + (k * b + j) * d, *al = aL + (j * m + k) * d;
+            double dot = 0.0;
+            for (int64_t v = 0; v < d; ++v) dot += ar[v] * al[v];
+            f += dot + hl[k] - cR[k * b + j] * cL[j * m + k];
+        }
+        *fj = f;
+    }
 }
 
-int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double *out, int64_t B,
-                      int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
-                      int32_t threads)
+/* The forward pass; obj (NULL, or B*H*T doubles) receives f(M^(t); Q, K)
+ * after every step t (the objective of Sec. 3 with the factors of step t, on
+ * all m*b rows of the padded problem): obj[(h * T) + t - 1]. */
+int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, double *out, double *obj,
+                          int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
+                          int32_t threads)
 {
     if (!q || !k || !v || !out) return MO_EINVAL;
     if (B < 1 || H < 1 || d < 1 || m < 1 || b < 1 || T < 1 || N < 1) return MO_EINVAL;
@@ -175,8 +201,9 @@ int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double 
     double *Y = malloc(sizeof(double) * (size_t)(BH * nd));
     double *cR = malloc(sizeof(double) * (size_t)(BH * Np));
     double *cL = malloc(sizeof(double) * (size_t)(BH * Np));
-    if (!Qs || !Kp || !Vp || !Op || !aR || !aL || !Y || !cR || !cL) {
-        free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL);
+    double *fpart = malloc(sizeof(double) * (size_t)(BH * b)); /* objective share of (head, j) */
+    if (!Qs || !Kp || !Vp || !Op || !aR || !aL || !Y || !cR || !cL || !fpart) {
+        free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
         return MO_ENOMEM;
     }
 #ifdef _OPENMP
@@ -204,6 +231,7 @@ int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double 
 #pragma omp parallel
         {
             double *z = malloc(sizeof(double) * (size_t)zlen);
+            double *hl = malloc(sizeof(double) * (size_t)m);
 #pragma omp for collapse(2) schedule(static)
             for (int64_t h = 0; h < BH; ++h)
                 for (int64_t kk = 0; kk < m; ++kk) {
@@ -215,16 +243,32 @@ int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double 
             for (int64_t h = 0; h < BH; ++h)
                 for (int64_t j = 0; j < b; ++j)
                     l_half_step(Qs + h * nd, aL + h * nd, cL + h * Np, Y + h * nd, aR + h * nd,
-                                cR + h * Np, last ? Op + h * nd : NULL, m, b, d, j, z);
+                                cR + h * Np, last ? Op + h * nd : NULL, m, b, d, j, z,
+                                obj ? fpart + h * b + j : NULL, hl);
             free(z);
+            free(hl);
+        }
+        if (obj) {
+            for (int64_t h = 0; h < BH; ++h) {
+                double f = 0.0;
+                for (int64_t j = 0; j < b; ++j) f += fpart[h * b + j];
+                obj[h * T + (t - 1)] = f;
+            }
         }
     }
     /* the first N rows of every head */
 #pragma omp parallel for schedule(static)
     for (int64_t h = 0; h < BH; ++h)
         memcpy(out + h * N * d, Op + h * nd, sizeof(double) * (size_t)(N * d));
-    free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL);
+    free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
     return MO_OK;
+}
+
+int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double *out, int64_t B,
+                      int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
+                      int32_t threads)
+{
+    return ma_oracle_fwd_obj_f64(q, k, v, out, NULL, B, H, N, d, m, b, T, threads);
 }
 
 /* Exact softmax attention O = softmax(Q K^T / sqrt(d)) V (eq. softmax_attention),

@@ -238,6 +238,27 @@ def objective_monarch(L: np.ndarray, R: np.ndarray, q: np.ndarray, k: np.ndarray
     return f
 
 
+def objective_after_l_update(R: np.ndarray, q, k, m: int, b: int, n=None) -> float:
+    """f(M) right after the L update that follows R, as the sum over query rows
+    (j, l) of logsumexp_k of the L-update logits z[j,l,k] = <Qbar[j,l], alpha_L[j,k]>
+    - c_L[j,k] (eq. L_update): the L update maximises f over L with R fixed, and
+    row by row the maximum of <p, z> + H(p) over the simplex is logsumexp(z)
+    (eq. softmax_variational).  q, k: one head, zero-padded to m*b rows when n < m*b;
+    the sum runs over all m*b rows of the (padded) problem."""
+    q, k = _f64(q, k)
+    if q.shape[0] < m * b:
+        q, k = pad_rows(q, m, b), pad_rows(k, m, b)
+    s = 1.0 / np.sqrt(q.shape[1])
+    Qb, Kb = qbar(s * q, m, b), kbar(k, m, b)
+    f = 0.0
+    for j in range(b):
+        alpha_l = np.stack([R[kk, j] @ Kb[kk] for kk in range(m)])
+        c_l = np.array([_xlogx_sum(R[kk, j]) for kk in range(m)])
+        for l in range(m):
+            f += log_sum_exp(alpha_l @ Qb[j, l] - c_l)
+    return f
+
+
 def dense_softmax_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
     """O = softmax(Q K^T / sqrt(d)) V, rows softmaxed (eq. softmax_attention). One head."""
     q, k, v = _f64(q, k, v)

@@ -335,3 +335,42 @@ def test_padding_rejects_m_other_than_ceil_n_over_b(oracle_lib):
     for m in (2, 4):   # ceil(10 / 4) = 3
         with pytest.raises(ValueError):
             oracle.monarch_attention(q, k, v, m, 4, 1)
+
+
+# -- the objective as a convergence diagnostic ---------------------------------------------
+
+@pytest.mark.parametrize("m,b,T", [(3, 4, 1), (4, 4, 3), (2, 5, 2)])
+def test_objective_after_l_update_is_sum_of_row_logsumexps(m, b, T):
+    """After each L update, f(M) (separable form of Sec. 3, and the dense form
+    of eq. softmax_variational_attention) equals the sum over query rows of the
+    logsumexp of the L-update logits."""
+    q, k, v = _head(m, b, 6, seed=110 + T, scale=2.0)
+    _, _, hist = nv.factors(q, k, m, b, T, history=True)
+    for t in range(1, T + 1):
+        L, R = hist[2 * t]          # (L^(t), R^(t))
+        f_sep = nv.objective_monarch(L, R, q, k)
+        f_dense = nv.objective_dense(nv.dense_monarch(L, R), q, k)
+        f_lse = nv.objective_after_l_update(R, q, k, m, b)
+        assert abs(f_sep - f_dense) < 1e-10
+        assert abs(f_lse - f_sep) < 1e-10
+
+
+def test_objective_padded_sum_of_row_logsumexps():
+    """The same identity on a padded problem (all m*b rows, zero padding, masked keys)."""
+    n, m, b = 10, 3, 4
+    q, k, v = _padded_head(n, m, b, 6, seed=120)
+    L, R = nv.factors(q, k, m, b, 2)
+    qp, kp = nv.pad_rows(q, m, b), nv.pad_rows(k, m, b)
+    assert abs(nv.objective_after_l_update(R, q, k, m, b) - nv.objective_monarch(L, R, qp, kp)) < 1e-10
+
+
+@pytest.mark.parametrize("m,b,T", [(3, 4, 3), (5, 3, 2), (4, 9, 4)])
+def test_c_objective_matches_separable_form(oracle_lib, m, b, T):
+    """The C oracle's per-step objective (separable form from its states) equals
+    the numpy separable form on the materialised factors."""
+    q, k, v = _head(m, b, 7, seed=130 + m, scale=2.0)
+    _, f = oracle.monarch_attention_objective(q[None, None], k[None, None], v[None, None], m, b, T)
+    _, _, hist = nv.factors(q, k, m, b, T, history=True)
+    ref = [nv.objective_monarch(*hist[2 * t], q, k) for t in range(1, T + 1)]
+    assert np.abs(f[0, 0] - ref).max() < 1e-9 * max(1.0, np.abs(ref).max())
+    assert all(b2 >= a2 - 1e-12 for a2, b2 in zip(f[0, 0], f[0, 0][1:]))   # ascent over the steps
