@@ -88,6 +88,29 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out,
                      int64_t B, int64_t H, int64_t N, int64_t d,
                      int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
 
+/*
+ * monarch_attn_fwd_objective -- monarch_attn_fwd, plus the value of the
+ * variational objective f(M; Q, K) = <M, s Q K^T> + H(M) (Sec. 3, eq.
+ * softmax_variational_attention, in its separable form for Monarch M) after
+ * every step t = 1..T: a convergence diagnostic.  After the L update of step
+ * t, f equals the sum over the query rows of the logsumexp of that update's
+ * logits (the L update maximises f over L with R fixed, and row by row that
+ * maximum is the logsumexp, eq. softmax_variational); the kernels form it
+ * from the statistics of their softmax and reduce it in a fixed order, so
+ * the result is deterministic.  When N < m * b the sum runs over the m * b
+ * rows of the padded problem.  f never exceeds the exact-softmax value
+ * sum_rows logsumexp(s q K^T).
+ *
+ * obj : DEVICE pointer to B*H*T floats, 4-byte aligned, not overlapping the
+ *       tensors; obj[(b*H + h)*T + t - 1] receives f for (batch b, head h,
+ *       step t).  Owned by the caller.
+ * The other arguments, the errors and the asynchrony are those of
+ * monarch_attn_fwd; the workspace also holds B*H*T*b floats of partial sums.
+ */
+int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void *out, float *obj,
+                               int64_t B, int64_t H, int64_t N, int64_t d,
+                               int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
+
 /* Text of the last failure on this thread ("" if none).  Valid until the next
  * call into the library from this thread. */
 const char *monarch_attn_last_error(void);
@@ -128,7 +151,8 @@ int monarch_attn_set_path(int32_t path);
  * that call, the duration in milliseconds to ms[i] and the kernel kind to
  * kind[i] (0 R half-step, 1 L half-step, 2 last R half-step with Y,
  * 3 last L half-step with the Monarch product and the store of O,
- * 4 the one-workgroup-per-head kernel); it returns the number of launches of that
+ * 4 the one-workgroup-per-head kernel, 5 the sum of the objective shares);
+ * it returns the number of launches of that
  * call, or -1 on error.
  */
 int monarch_attn_timing_enable(int32_t flag);

@@ -15,12 +15,13 @@ MA_F32, MA_BF16, MA_F16 = 0, 1, 2
 MA_OK, MA_EINVAL, MA_EUNSUPPORTED, MA_EHIP, MA_ENOMEM = 0, 1, 2, 3, 4
 STATUS_NAMES = {0: "MA_OK", 1: "MA_EINVAL", 2: "MA_EUNSUPPORTED", 3: "MA_EHIP", 4: "MA_ENOMEM"}
 KIND_NAMES = {0: "r_half_step", 1: "l_half_step", 2: "r_half_step_final", 3: "monarch_apply",
-              4: "monarch_fused_head"}
+              4: "monarch_fused_head", 5: "objective_sum"}
 PATH_AUTO, PATH_HALF_STEPS, PATH_FUSED = 0, 1, 2
 
 # Every symbol declared in include/monarch_attn.h.
 EXPORTS = (
     "monarch_attn_fwd",
+    "monarch_attn_fwd_objective",
     "monarch_attn_last_error",
     "monarch_attn_check",
     "monarch_attn_workspace_bytes",
@@ -46,6 +47,8 @@ def _load() -> ctypes.CDLL:
     i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
     lib.monarch_attn_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
     lib.monarch_attn_fwd.restype = ctypes.c_int
+    lib.monarch_attn_fwd_objective.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
+    lib.monarch_attn_fwd_objective.restype = ctypes.c_int
     lib.monarch_attn_last_error.argtypes = []
     lib.monarch_attn_last_error.restype = ctypes.c_char_p
     lib.monarch_attn_check.argtypes = [i64, i64, i64, i64, i32, i32]
@@ -90,12 +93,7 @@ def dtype_code(torch_dtype) -> int:
     return codes[torch_dtype]
 
 
-def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
-    """O = MonarchAttention(q, k, v) into `out`; torch device tensors [B, H, N, d].
-
-    `stream`: a torch.cuda.Stream, an integer hipStream_t, or None for torch's
-    current stream.  Asynchronous on that stream.  Returns `out`.
-    """
+def _check_tensors(q, k, v, out):
     import torch
 
     for name, t in (("q", q), ("k", k), ("v", v), ("out", out)):
@@ -105,15 +103,48 @@ def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
             raise ValueError(f"{name} must be a contiguous [B, H, N, d] tensor")
         if t.shape != q.shape or t.dtype != q.dtype:
             raise ValueError(f"{name} must match q in shape and dtype")
-    B, H, N, d = q.shape
+
+
+def _stream(q, stream):
+    import torch
+
     if stream is None:
-        stream = torch.cuda.current_stream(q.device).cuda_stream
-    elif not isinstance(stream, int):
-        stream = stream.cuda_stream
+        return torch.cuda.current_stream(q.device).cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
+    """O = MonarchAttention(q, k, v) into `out`; torch device tensors [B, H, N, d].
+
+    `stream`: a torch.cuda.Stream, an integer hipStream_t, or None for torch's
+    current stream.  Asynchronous on that stream.  Returns `out`.
+    """
+    import torch
+
+    _check_tensors(q, k, v, out)
+    B, H, N, d = q.shape
+    stream = _stream(q, stream)
     with torch.cuda.device(q.device):
         _check(monarch_attn_fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                     B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
     return out
+
+
+def monarch_attn_fwd_objective(q, k, v, out, obj, m: int, b: int, T: int, stream=None):
+    """monarch_attn_fwd, plus obj[B, H, T] (float32 device tensor): the variational
+    objective f(M^(t); Q, K) after every step t.  Returns (out, obj)."""
+    import torch
+
+    _check_tensors(q, k, v, out)
+    if not isinstance(obj, torch.Tensor) or not obj.is_cuda or obj.dtype != torch.float32 \
+            or not obj.is_contiguous() or tuple(obj.shape) != (q.shape[0], q.shape[1], T):
+        raise ValueError("obj must be a contiguous float32 device tensor [B, H, T]")
+    B, H, N, d = q.shape
+    stream = _stream(q, stream)
+    with torch.cuda.device(q.device):
+        _check(LIB.monarch_attn_fwd_objective(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                              obj.data_ptr(), B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
+    return out, obj
 
 
 def monarch_attention(q, k, v, m: int, b: int, T: int, stream=None):

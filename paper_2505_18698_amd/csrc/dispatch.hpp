@@ -23,7 +23,7 @@ namespace ma_host {
 template <typename T> ma::Bufs<T> typed(const CallBufs &B)
 {
     return ma::Bufs<T>{(const T *)B.q, (const T *)B.k, (const T *)B.v, (T *)B.out, (T *)B.aR, (T *)B.aL, (T *)B.Y,
-                       B.cR, B.cL};
+                       B.cR, B.cL, B.obj_part};
 }
 
 template <typename F> int launched(F &&f)
@@ -153,8 +153,10 @@ template <typename T, int D>
 int run_half_steps(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
 {
     int rc;
+    hd.T = c.T;
     for (int t = 1; t <= c.T; ++t) {
         const bool first = (t == 1), last = (t == c.T);
+        hd.t = t;
         if ((rc = r_step<T, D>(L, B, hd, c.BH, c.num_cus, first, last)) != MA_OK) return rc;
         if ((rc = l_step<T, D>(L, B, hd, c.BH, c.num_cus, last)) != MA_OK) return rc;
     }
@@ -198,12 +200,27 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
     ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};
     if (path == kFusedHead && !fused_applies(dtype, c.d, c.m, c.b))
         return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d <= 64 and m, b <= 16");
-    if (uses_fused(path, dtype, c.d, c.m, c.b)) return run_fused<T>(L, B, hd, c);
-    switch (tile_d(c.d)) {
-    case 64: return run_half_steps<T, 64>(L, B, hd, c);
-    case 96: return run_half_steps<T, 96>(L, B, hd, c);
-    default: return run_half_steps<T, 128>(L, B, hd, c);
+    int rc;
+    if (uses_fused(path, dtype, c.d, c.m, c.b)) {
+        rc = run_fused<T>(L, B, hd, c);
+    } else {
+        switch (tile_d(c.d)) {
+        case 64: rc = run_half_steps<T, 64>(L, B, hd, c); break;
+        case 96: rc = run_half_steps<T, 96>(L, B, hd, c); break;
+        default: rc = run_half_steps<T, 128>(L, B, hd, c); break;
+        }
     }
+    if (rc != MA_OK || !B.obj) return rc;
+    const int64_t units = c.BH * c.T;  // one (head, step) per thread
+    const float *part = B.obj_part;
+    float *obj = B.obj;
+    const int b = c.b;
+    return L.run(kObjSum, [&] {
+        return launched([&] {
+            hipLaunchKernelGGL(ma::objective_sum, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, L.stream, part,
+                               obj, units, b);
+        });
+    });
 }
 
 }  // namespace ma_host

@@ -16,7 +16,7 @@ int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 inline int pad16(int64_t x) { return (int)((x + 15) / 16 * 16); }
 
 // Kernel kinds reported by the timing interface.
-enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4 };
+enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4, kObjSum = 5 };
 
 // Per-launch HIP events around every kernel when timing is enabled.
 constexpr int kMaxLaunches = 2 * 64 + 2;
@@ -52,12 +52,15 @@ struct Launcher {
     }
 };
 
-// Untyped tensors and states of one call (the states are null on the fused path).
+// Untyped tensors and states of one call (the states are null on the fused
+// path; obj_part and obj are null unless the objective is requested).
 struct CallBufs {
     const void *q, *k, *v;
     void *out;
     void *aR, *aL, *Y;
     float *cR, *cL;
+    float *obj_part;  // [B*H][T][b] shares (workspace)
+    float *obj;       // [B*H][T] result (caller's)
 };
 
 struct CallDims {

@@ -506,6 +506,7 @@ struct HeadDims {
     int d;             // head dimension of q, k, v, out (<= the tile width D; the states use D)
     float s_log2e;     // log2(e) / sqrt(d)
     int64_t units;     // work units of a half-step launch (grid size)
+    int t = 0, T = 0;  // step of this L half-step (1..T) and the step count, for the objective
 };
 
 // Real keys of block k (b except in a padded last block).
@@ -525,7 +526,26 @@ template <typename T> struct Bufs {
     T *out;
     T *aR, *aL, *Y;
     float *cR, *cL;
+    // Objective shares [B*H][T][b] (nullptr: not requested): after the L update
+    // of step t, the sum over the query rows of class j of the logsumexp of the
+    // L-update logits (natural units).  Their sum over j is f(M^(t); Q, K).
+    float *obj_part = nullptr;
 };
+
+// Sum over the 16 rows of a wave (lanes 16g + c, c = 0..15, the four lane
+// groups holding the same values): xor steps 8, 4, 2, 1; every lane ends with
+// the sum, always in this order.
+__device__ inline float rows16_sum(float x)
+{
+    x += __shfl_xor(x, 8);
+    x += __shfl_xor(x, 4);
+    x += __shfl_xor(x, 2);
+    return x + __shfl_xor(x, 1);
+}
+
+// logsumexp (natural units) of a row held as log2-domain logits with maximum
+// mx and sum of exp2(logit - mx) = sum.
+__device__ inline float row_lse(float mx, float sum) { return kLn2 * (mx + __builtin_amdgcn_logf(sum)); }
 
 // The work of one unit of each half-step, done by a workgroup of W waves in
 // three parts: fetch() issues its global loads into registers, stage() moves
@@ -684,7 +704,7 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
     static constexpr int LDQ = Ld<T, D>::row, LDP = Ld<T, NM>::row;
     static constexpr int A_ELEMS = NM * LDQ, P_ELEMS = NM * LDP;
     static constexpr int AP_ELEMS = A_ELEMS > P_ELEMS ? A_ELEMS : P_ELEMS;
-    static constexpr int LDS_BYTES = (NM * LDQ + AP_ELEMS) * (int)sizeof(T) + NM * 4;
+    static constexpr int LDS_BYTES = (NM * LDQ + AP_ELEMS) * (int)sizeof(T) + NM * 4 + W * 4;
 
     struct Regs {
         TileChunks<T, NM, D, NTH> qt, at;  // Qbar[j] (rows l), alpha_L[j] (rows k)
@@ -728,7 +748,7 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
 
         // scores and softmax over k for the query rows of this wave
         int lr[RT];
-        float inv[RT];
+        float inv[RT], lse[RT];
         f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
         RowFrags<T, D> bf[RT];
 #pragma unroll
@@ -766,8 +786,22 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
             }
             sum = lanegroup_sum(sum);
             inv[r] = (lr[r] < m) ? fast_rcp(sum) : 0.f;  // padded query rows carry no weight
+            lse[r] = (lr[r] < m) ? row_lse(mx, sum) : 0.f;
+        }
+        float *objs = cLs + NM;  // one objective share per wave
+        if (p.obj_part) {
+            float part = 0.f;
+#pragma unroll
+            for (int r = 0; r < RT; ++r) part += lse[r];
+            part = rows16_sum(part);
+            if (lane == 0) objs[wave] = part;
         }
         __syncthreads();  // every wave is done reading alpha_L
+        if (p.obj_part && tid == 0) {
+            float f = 0.f;
+            for (int w = 0; w < W; ++w) f += objs[w];
+            p.obj_part[(bh * hd.T + hd.t - 1) * b + j] = f;
+        }
 
         // P[l][k] (row-major, k contiguous) into the alpha_L space
         using PT = typename std::conditional<std::is_same<T, float>::value, float, T>::type;
@@ -811,7 +845,7 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
     static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W, NTH = 64 * W;
     static constexpr bool NF = NormFirst<NT, D>::value;
     static constexpr int LDK = Ld<T, D>::row;
-    static constexpr int LDS_BYTES = 2 * NM * LDK * (int)sizeof(T) + NM * 4;
+    static constexpr int LDS_BYTES = 2 * NM * LDK * (int)sizeof(T) + NM * 4 + W * 4;
 
     struct Regs {
         TileChunks<T, NM, D, NTH> at, yt;  // alpha_L[j], Y[j] (rows k)
@@ -876,7 +910,7 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
             }
         }
         ProbFrags<T, NT> pf[RT];
-        float inv[RT];
+        float inv[RT], lse[RT];
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
@@ -891,13 +925,29 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
                     sc[r][t][qq] = e;
                 }
             }
-            inv[r] = fast_rcp(lanegroup_sum(sum));
+            sum = lanegroup_sum(sum);
+            inv[r] = fast_rcp(sum);
+            lse[r] = (lr[r] < m) ? row_lse(mx, sum) : 0.f;
             if constexpr (NF) {
 #pragma unroll
                 for (int t = 0; t < NT; ++t) sc[r][t] *= inv[r];
                 inv[r] = 1.0f;
             }
             pf[r].pack(sc[r]);  // !NF: unnormalised, the row sum is divided out of O below
+        }
+        if (p.obj_part) {  // objective share of class j at the last step (uniform branch)
+            float *objs = cLs + NM;
+            float part = 0.f;
+#pragma unroll
+            for (int r = 0; r < RT; ++r) part += lse[r];
+            part = rows16_sum(part);
+            if (lane == 0) objs[wave] = part;
+            __syncthreads();
+            if (tid == 0) {
+                float f = 0.f;
+                for (int w = 0; w < W; ++w) f += objs[w];
+                p.obj_part[(bh * hd.T + hd.t - 1) * b + j] = f;
+            }
         }
         f32x4 o[RT][D / 16];
 #pragma unroll
@@ -1001,6 +1051,9 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         float *cRs, *cLs;  // c_R[k][j] at k*CS + j, c_L[j][k] at j*CS + k
         int m, b, n, d, lane, g, c16;  // n: real rows of the head (rows >= n are zero padding); d <= D
         float s_log2e;
+        int64_t bh;        // the head being computed
+        int steps;         // T, the step count
+        float *obj_part;   // objective shares [B*H][T][b], or nullptr
     };
 
     template <bool FIRST, bool FINAL>
@@ -1053,8 +1106,9 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
     }
 
     // Scores and softmax over k of class j, query row l = lane % 16 (lane
-    // holds k = 4g + qq); returns exp2 values and sets inv = 1 / row sum.
-    __device__ static f32x4 l_softmax(const Ctx &c, int j, float &inv)
+    // holds k = 4g + qq); returns exp2 values and sets inv = 1 / row sum and
+    // lse = the row's logsumexp (natural units; 0 for tile rows l >= m).
+    __device__ static f32x4 l_softmax(const Ctx &c, int j, float &inv, float &lse)
     {
         RowFrags<T, D> bf;
         bf.load(c.Qs + j * BS + c.c16 * LD, c.g);  // Qbar[j][l]
@@ -1076,15 +1130,26 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             sum += e;
             sc[qq] = e;
         }
-        inv = fast_rcp(lanegroup_sum(sum));
+        sum = lanegroup_sum(sum);
+        inv = fast_rcp(sum);
+        lse = c.c16 < c.m ? row_lse(mx, sum) : 0.f;
         return sc;
     }
 
-    __device__ static void l_unit(const Ctx &c, int j)
+    // Objective share of class j after the L update of step t (as LHalf / Apply).
+    __device__ static void objective_share(const Ctx &c, int j, int t, float lse)
+    {
+        if (!c.obj_part) return;
+        const float part = rows16_sum(lse);
+        if (c.lane == 0) c.obj_part[(c.bh * c.steps + t - 1) * c.b + j] = part;
+    }
+
+    __device__ static void l_unit(const Ctx &c, int j, int t)
     {
         const int l = c.c16;
-        float inv;
-        const f32x4 e = l_softmax(c, j, inv);
+        float inv, lse;
+        const f32x4 e = l_softmax(c, j, inv, lse);
+        objective_share(c, j, t, lse);
         T *Aj = c.As + j * BS;  // alpha_L[j] has been read: P[l][k] in its place
         const f32x4 pr = l < c.m ? e * inv : f32x4{0.f, 0.f, 0.f, 0.f};  // padded query rows carry no weight
         store4<T>(Aj + l * LD + 4 * c.g, pr);
@@ -1102,8 +1167,9 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
     __device__ static void apply_unit(const Ctx &c, int j, T *out_h)
     {
         const int l = c.c16;
-        float inv;
-        const f32x4 e = l_softmax(c, j, inv) * inv;  // normalised first, as in Apply at 16 rows
+        float inv, lse;
+        const f32x4 e = l_softmax(c, j, inv, lse) * inv;  // normalised first, as in Apply at 16 rows
+        objective_share(c, j, c.steps, lse);
         ProbFrags<T, 1> pf;
         pf.pack(&e);
         f32x4 o[D / 16];  // O[l*b + j] = sum_k L[j][k][l] Y[k][j]; Y[k][j] is row k of Ks + j*LD at stride BS
@@ -1116,7 +1182,6 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
 
     // Issue the loads of head bh: Qbar and Kbar chunks (zero where there is no
     // row) for the LDS regions, and Vbar[w] for wave w's last R half-step.
-    // Rows >= n (padding) are zero and never read.
     // Rows >= n (padding) and columns >= d are zero and never read.
     __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int d, int64_t bh, int tid, u32x4 *raw,
                                      u32x4 *vb)
@@ -1169,6 +1234,8 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         c.n = hd.n;
         c.d = hd.d;
         c.s_log2e = hd.s_log2e;
+        c.steps = T_;
+        c.obj_part = p.obj_part;
         const int tid = threadIdx.x, w = tid >> 6;
         c.lane = tid & 63;
         c.g = c.lane >> 4;
@@ -1180,6 +1247,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         load_head(p, m, b, c.n, c.d, bh, tid, raw, vcur);
         for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) *chunk(c.As, idx) = u32x4{0u, 0u, 0u, 0u};
         for (; bh < BH; bh += gridDim.x) {
+            c.bh = bh;
 #pragma unroll
             for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
             __syncthreads();
@@ -1199,7 +1267,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
                 }
                 __syncthreads();
                 if (last) break;
-                if (w < b) l_unit(c, w);
+                if (w < b) l_unit(c, w, t);
                 __syncthreads();
             }
             if (w < b) apply_unit(c, w, p.out + bh * (int64_t)c.n * c.d);
@@ -1216,6 +1284,17 @@ __global__ __launch_bounds__(1024) void monarch_fused_head(Bufs<T> p, HeadDims h
     using U = FusedHead<T, RGB, RGM>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
     U::run(p, hd, BH, T_, lds);
+}
+
+// f(M^(t); Q, K) of every (head, step): the objective shares summed over the
+// b classes, in class order.  One thread per (head, step).
+static __global__ __launch_bounds__(256) void objective_sum(const float *part, float *obj, int64_t units, int b)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= units) return;
+    float f = 0.f;
+    for (int j = 0; j < b; ++j) f += part[i * b + j];
+    obj[i] = f;
 }
 
 }  // namespace ma

@@ -92,6 +92,99 @@ bool overlaps(const void *a, size_t na, const void *b, size_t nb)
     return x < y + nb && y < x + na;
 }
 
+// The forward pass; with obj != nullptr also the objective per (head, step).
+int forward(const void *q, const void *k, const void *v, void *out, float *obj, int64_t B, int64_t H, int64_t N,
+            int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
+{
+    g_err[0] = '\0';
+    if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
+    if (B < 1 || H < 1) return fail(MA_EINVAL, "B and H must be >= 1");
+    int rc = check_shape(N, d, m, b, T, dtype);
+    if (rc != MA_OK) return rc;
+    if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)out) & 15u)
+        return fail(MA_EINVAL, "q, k, v and out must be 16-byte aligned");
+    const int64_t BH = B * H;
+    if (BH * (int64_t)(m > b ? m : b) > (int64_t)0x7fffffff) return fail(MA_EUNSUPPORTED, "too many heads for one grid");
+    const size_t tensor_bytes = (size_t)BH * N * d * elem_bytes(dtype);
+    if (overlaps(out, tensor_bytes, q, tensor_bytes) || overlaps(out, tensor_bytes, k, tensor_bytes) ||
+        overlaps(out, tensor_bytes, v, tensor_bytes))
+        return fail(MA_EINVAL, "out must not overlap q, k or v");
+    const size_t obj_bytes = (size_t)BH * T * sizeof(float);
+    if (obj && (overlaps(obj, obj_bytes, q, tensor_bytes) || overlaps(obj, obj_bytes, k, tensor_bytes) ||
+                overlaps(obj, obj_bytes, v, tensor_bytes) || overlaps(obj, obj_bytes, out, tensor_bytes)))
+        return fail(MA_EINVAL, "obj must not overlap q, k, v or out");
+
+    const int path = g_path.load();
+    const size_t st = state_bytes(BH, m * b, d, dtype);
+    const size_t cs = align_up((size_t)BH * m * b * sizeof(float));
+    CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, obj};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
+    int num_cus = 0;
+    {
+        std::lock_guard<std::mutex> lock(g_dev_mutex);
+        Device &D = g_dev[dev];
+        if (D.num_cus == 0) {
+            int n = 0;
+            if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+                return fail(MA_EHIP, "querying the compute unit count failed");
+            D.num_cus = n;
+        }
+        num_cus = D.num_cus;
+    }
+    const bool states = !uses_fused(path, dtype, d, m, b);  // the fused kernel keeps its states in LDS
+    const size_t obj_part_bytes = obj ? align_up((size_t)BH * T * b * sizeof(float)) : 0;
+    if (states || obj) {
+        const size_t state_ws = states ? workspace_bytes(BH, m * b, d, dtype) : 0;
+        const size_t need = state_ws + obj_part_bytes;
+        std::lock_guard<std::mutex> lock(g_dev_mutex);
+        Device &D = g_dev[dev];
+        if (D.ws_bytes < need) {
+            if (D.ws) {
+                if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
+                (void)hipFree(D.ws);
+                D.ws = nullptr;
+                D.ws_bytes = 0;
+            }
+            void *p = nullptr;
+            if (hipMalloc(&p, need) != hipSuccess) {
+                (void)hipGetLastError();
+                return fail(MA_ENOMEM, "hipMalloc of %zu workspace bytes failed", need);
+            }
+            D.ws = p;
+            D.ws_bytes = need;
+        }
+        char *base = (char *)D.ws;
+        if (states) {
+            bufs.aR = base;
+            bufs.aL = base + st;
+            bufs.Y = base + 2 * st;
+            bufs.cR = (float *)(base + 3 * st);
+            bufs.cL = (float *)(base + 3 * st + cs);
+        }
+        if (obj) bufs.obj_part = (float *)(base + state_ws);
+    }
+    CallDims dims{BH, (int)m, (int)b, (int)N, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
+
+    std::unique_lock<std::mutex> tlock(g_timing_mutex);
+    Launcher L{(hipStream_t)stream, g_timing.enabled};
+    if (!L.timed) tlock.unlock();
+    (void)hipGetLastError();  // clear a stale error so the check below is ours
+    switch (dtype) {
+    case MA_F32: rc = run_call<float>(L, bufs, dims, path); break;
+    case MA_BF16: rc = run_call<__bf16>(L, bufs, dims, path); break;
+    default: rc = run_call<_Float16>(L, bufs, dims, path); break;
+    }
+    if (L.timed) {
+        g_timing.nlaunch = L.n;
+        g_timing.ready = (rc == MA_OK && L.n > 0);
+    }
+    if (rc != MA_OK) return rc;
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(MA_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return MA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -180,83 +273,17 @@ int32_t monarch_attn_timing_read(float *ms, int32_t *kind, int32_t cap)
 int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int64_t B, int64_t H, int64_t N,
                      int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
 {
+    return forward(q, k, v, out, nullptr, B, H, N, d, m, b, T, dtype, stream);
+}
+
+int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void *out, float *obj, int64_t B,
+                               int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
+                               void *stream)
+{
     g_err[0] = '\0';
-    if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
-    if (B < 1 || H < 1) return fail(MA_EINVAL, "B and H must be >= 1");
-    int rc = check_shape(N, d, m, b, T, dtype);
-    if (rc != MA_OK) return rc;
-    if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)out) & 15u)
-        return fail(MA_EINVAL, "q, k, v and out must be 16-byte aligned");
-    const int64_t BH = B * H;
-    if (BH * (int64_t)(m > b ? m : b) > (int64_t)0x7fffffff) return fail(MA_EUNSUPPORTED, "too many heads for one grid");
-    const size_t tensor_bytes = (size_t)BH * N * d * elem_bytes(dtype);
-    if (overlaps(out, tensor_bytes, q, tensor_bytes) || overlaps(out, tensor_bytes, k, tensor_bytes) ||
-        overlaps(out, tensor_bytes, v, tensor_bytes))
-        return fail(MA_EINVAL, "out must not overlap q, k or v");
-
-    const int path = g_path.load();
-    const size_t st = state_bytes(BH, m * b, d, dtype);
-    const size_t cs = align_up((size_t)BH * m * b * sizeof(float));
-    CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
-    int num_cus = 0;
-    {
-        std::lock_guard<std::mutex> lock(g_dev_mutex);
-        Device &D = g_dev[dev];
-        if (D.num_cus == 0) {
-            int n = 0;
-            if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
-                return fail(MA_EHIP, "querying the compute unit count failed");
-            D.num_cus = n;
-        }
-        num_cus = D.num_cus;
-    }
-    if (!uses_fused(path, dtype, d, m, b)) {  // the fused kernel keeps its states in LDS
-        const size_t need = workspace_bytes(BH, m * b, d, dtype);
-        std::lock_guard<std::mutex> lock(g_dev_mutex);
-        Device &D = g_dev[dev];
-        if (D.ws_bytes < need) {
-            if (D.ws) {
-                if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
-                (void)hipFree(D.ws);
-                D.ws = nullptr;
-                D.ws_bytes = 0;
-            }
-            void *p = nullptr;
-            if (hipMalloc(&p, need) != hipSuccess) {
-                (void)hipGetLastError();
-                return fail(MA_ENOMEM, "hipMalloc of %zu workspace bytes failed", need);
-            }
-            D.ws = p;
-            D.ws_bytes = need;
-        }
-        char *base = (char *)D.ws;
-        bufs.aR = base;
-        bufs.aL = base + st;
-        bufs.Y = base + 2 * st;
-        bufs.cR = (float *)(base + 3 * st);
-        bufs.cL = (float *)(base + 3 * st + cs);
-    }
-    CallDims dims{BH, (int)m, (int)b, (int)N, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
-
-    std::unique_lock<std::mutex> tlock(g_timing_mutex);
-    Launcher L{(hipStream_t)stream, g_timing.enabled};
-    if (!L.timed) tlock.unlock();
-    (void)hipGetLastError();  // clear a stale error so the check below is ours
-    switch (dtype) {
-    case MA_F32: rc = run_call<float>(L, bufs, dims, path); break;
-    case MA_BF16: rc = run_call<__bf16>(L, bufs, dims, path); break;
-    default: rc = run_call<_Float16>(L, bufs, dims, path); break;
-    }
-    if (L.timed) {
-        g_timing.nlaunch = L.n;
-        g_timing.ready = (rc == MA_OK && L.n > 0);
-    }
-    if (rc != MA_OK) return rc;
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return fail(MA_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
-    return MA_OK;
+    if (!obj) return fail(MA_EINVAL, "null objective pointer");
+    if ((uintptr_t)obj & 3u) return fail(MA_EINVAL, "obj must be 4-byte aligned");
+    return forward(q, k, v, out, obj, B, H, N, d, m, b, T, dtype, stream);
 }
 
 }  // extern "C"

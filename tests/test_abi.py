@@ -142,3 +142,11 @@ def test_set_path_rejects_unknown_values_and_returns_previous():
     assert ma.monarch_attn_set_path(prev) == ma.PATH_HALF_STEPS
     with pytest.raises(ma.MonarchAttnError):
         ma.monarch_attn_set_path(7)
+
+
+def test_objective_rejects_null_obj():
+    import paper_2505_18698_amd as ma
+
+    rc = ma.LIB.monarch_attn_fwd_objective(FAKE, FAKE, FAKE, 2 * FAKE, None, 1, 1, 256, 64, 16, 16, 1, 1, None)
+    assert rc == ma.MA_EINVAL
+    assert "objective" in ma.monarch_attn_last_error()

@@ -370,3 +370,80 @@ def test_rectangular_blocks(ma, n, m, b, T):
     o = gpu_run_padded(ma, q, k, v, m, b, T, "bf16")
     ref = oracle.monarch_attention(q[:, heads], k[:, heads], v[:, heads], m, b, T)
     check(o[:, heads], ref, "bf16", f"rect N{n} m{m} b{b} T{T}")
+
+
+# -- the objective per step (convergence diagnostic) ---------------------------------------
+
+# Relative to max |f|.  f is a sum of row logsumexps, and a logsumexp moves
+# by at most the largest change of its logits.  Those carry the rounding of
+# the 16-bit states and probabilities (2^-9 relative per element): about 1e-3
+# of a logit at worst.  Measured: fp32 1.5e-7, bf16 <= 9.3e-5, fp16 1.8e-6.
+OBJ_TOL = {"f32": 1e-5, "bf16": 1e-3, "f16": 1e-3}
+
+
+def gpu_objective(ma, q, k, v, m, b, T, dtype):
+    import torch
+
+    td = _torch_dtype(dtype)
+    if ma.path_name == "fused" and not ma.fused_applies(q.shape[-1], m, b, ma.dtype_code(td)):
+        pytest.skip("the fused kernel covers 16-bit elements, d <= 64, m and b <= 16")
+    t = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
+    out = torch.empty_like(t[0])
+    obj = torch.full((q.shape[0], q.shape[1], T), float("nan"), dtype=torch.float32, device="cuda")
+    ma.monarch_attn_fwd_objective(t[0], t[1], t[2], out, obj, m, b, T)
+    torch.cuda.synchronize()
+    return out.double().cpu().numpy(), obj.double().cpu().numpy()
+
+
+@pytest.mark.parametrize(
+    "B,H,n,m,b,T,dtype",
+    [
+        (1, 2, 256, 16, 16, 3, "f32"),
+        (2, 3, 256, 16, 16, 3, "bf16"),
+        (2, 2, 197, 15, 14, 3, "bf16"),
+        (1, 2, 960, 24, 40, 2, "f16"),
+        (1, 4, 4096, 64, 64, 3, "bf16"),
+    ],
+)
+def test_objective_matches_oracle(ma, B, H, n, m, b, T, dtype):
+    q, k, v = si.random_qkv(B, H, n, 64, dtype, seed=n + T, scale=1.5)
+    o, f = gpu_objective(ma, q, k, v, m, b, T, dtype)
+    ref_o, ref_f = oracle.monarch_attention_objective(q, k, v, m, b, T)
+    check(o, ref_o, dtype, f"objective call O {dtype} N{n} m{m} b{b} T{T}")
+    rel = np.abs(f - ref_f).max() / np.abs(ref_f).max()
+    print(f"objective {dtype} N{n} m{m} b{b} T{T}: max rel err {rel:.3e}; f = {f[0, 0]}", flush=True)
+    assert np.isfinite(f).all()
+    assert rel <= OBJ_TOL[dtype]
+    # ascent over the steps (up to the tolerance) and the exact-softmax bound
+    assert (np.diff(f, axis=2) >= -OBJ_TOL[dtype] * np.abs(f[..., 1:])).all()
+    if n == m * b:
+        s = 1.0 / np.sqrt(64)
+        for bi, h in ((0, 0), (B - 1, H - 1)):
+            z = s * q[bi, h].astype(np.float64) @ k[bi, h].astype(np.float64).T
+            zm = z.max(axis=1, keepdims=True)
+            bound = float((zm[:, 0] + np.log(np.exp(z - zm).sum(axis=1))).sum())
+            assert f[bi, h, -1] <= bound * (1 + OBJ_TOL[dtype])
+
+
+@pytest.mark.parametrize("n,m,b", [(256, 16, 16), (197, 15, 14)])
+def test_objective_paths_agree_bitwise(lib, n, m, b):
+    import torch
+
+    q, k, v = si.random_qkv(6, 4, n, 64, "bf16", seed=n, scale=1.5)
+    t = [torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (q, k, v)]
+
+    def run(path):
+        lib.monarch_attn_set_path(path)
+        out = torch.empty_like(t[0])
+        obj = torch.empty((6, 4, 3), dtype=torch.float32, device="cuda")
+        lib.monarch_attn_fwd_objective(t[0], t[1], t[2], out, obj, m, b, 3)
+        torch.cuda.synchronize()
+        return out.cpu(), obj.cpu()
+
+    prev = lib.monarch_attn_set_path(lib.PATH_HALF_STEPS)
+    try:
+        (o1, f1), (o2, f2) = run(lib.PATH_HALF_STEPS), run(lib.PATH_FUSED)
+    finally:
+        lib.monarch_attn_set_path(prev)
+    assert torch.equal(o1, o2)
+    assert torch.equal(f1, f2)
