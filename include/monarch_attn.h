@@ -111,6 +111,24 @@ int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void
                                int64_t B, int64_t H, int64_t N, int64_t d,
                                int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
 
+/*
+ * monarch_attn_exact_fwd -- exact softmax attention O = softmax(s Q K^T) V,
+ * s = 1/sqrt(d) (eq. softmax_attention), the reference that the Monarch
+ * output's quality is measured against, and the logsumexp of every row of
+ * s Q K^T (natural log).  Their sum over the rows is the largest value the
+ * objective of monarch_attn_fwd_objective can take (the exact softmax
+ * maximises it, eq. softmax_variational_attention).
+ *
+ * q, k, v, out : DEVICE pointers to [B, H, N, d] tensors as in
+ *                monarch_attn_fwd (any N >= 1; d as there).
+ * lse          : NULL, or a DEVICE pointer to B*H*N floats (4-byte aligned,
+ *                not overlapping the tensors), lse[(b*H + h)*N + row].
+ * Asynchronous on `stream`; arguments are checked before any HIP call
+ * (MA_EINVAL / MA_EUNSUPPORTED, nothing launched); uses no workspace.
+ */
+int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *out, float *lse,
+                           int64_t B, int64_t H, int64_t N, int64_t d, int32_t dtype, void *stream);
+
 /* Text of the last failure on this thread ("" if none).  Valid until the next
  * call into the library from this thread. */
 const char *monarch_attn_last_error(void);
@@ -151,7 +169,8 @@ int monarch_attn_set_path(int32_t path);
  * that call, the duration in milliseconds to ms[i] and the kernel kind to
  * kind[i] (0 R half-step, 1 L half-step, 2 last R half-step with Y,
  * 3 last L half-step with the Monarch product and the store of O,
- * 4 the one-workgroup-per-head kernel, 5 the sum of the objective shares);
+ * 4 the one-workgroup-per-head kernel, 5 the sum of the objective shares,
+ * 6 exact attention);
  * it returns the number of launches of that
  * call, or -1 on error.
  */

@@ -15,13 +15,14 @@ MA_F32, MA_BF16, MA_F16 = 0, 1, 2
 MA_OK, MA_EINVAL, MA_EUNSUPPORTED, MA_EHIP, MA_ENOMEM = 0, 1, 2, 3, 4
 STATUS_NAMES = {0: "MA_OK", 1: "MA_EINVAL", 2: "MA_EUNSUPPORTED", 3: "MA_EHIP", 4: "MA_ENOMEM"}
 KIND_NAMES = {0: "r_half_step", 1: "l_half_step", 2: "r_half_step_final", 3: "monarch_apply",
-              4: "monarch_fused_head", 5: "objective_sum"}
+              4: "monarch_fused_head", 5: "objective_sum", 6: "exact_attention"}
 PATH_AUTO, PATH_HALF_STEPS, PATH_FUSED = 0, 1, 2
 
 # Every symbol declared in include/monarch_attn.h.
 EXPORTS = (
     "monarch_attn_fwd",
     "monarch_attn_fwd_objective",
+    "monarch_attn_exact_fwd",
     "monarch_attn_last_error",
     "monarch_attn_check",
     "monarch_attn_workspace_bytes",
@@ -49,6 +50,8 @@ def _load() -> ctypes.CDLL:
     lib.monarch_attn_fwd.restype = ctypes.c_int
     lib.monarch_attn_fwd_objective.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
     lib.monarch_attn_fwd_objective.restype = ctypes.c_int
+    lib.monarch_attn_exact_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i32, vp]
+    lib.monarch_attn_exact_fwd.restype = ctypes.c_int
     lib.monarch_attn_last_error.argtypes = []
     lib.monarch_attn_last_error.restype = ctypes.c_char_p
     lib.monarch_attn_check.argtypes = [i64, i64, i64, i64, i32, i32]
@@ -145,6 +148,24 @@ def monarch_attn_fwd_objective(q, k, v, out, obj, m: int, b: int, T: int, stream
         _check(LIB.monarch_attn_fwd_objective(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                               obj.data_ptr(), B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
     return out, obj
+
+
+def monarch_attn_exact_fwd(q, k, v, out, lse=None, stream=None):
+    """Exact softmax attention into `out`; with `lse` (float32 device tensor
+    [B, H, N]) also every row's logsumexp.  Returns (out, lse)."""
+    import torch
+
+    _check_tensors(q, k, v, out)
+    B, H, N, d = q.shape
+    if lse is not None and (not isinstance(lse, torch.Tensor) or not lse.is_cuda or lse.dtype != torch.float32
+                            or not lse.is_contiguous() or tuple(lse.shape) != (B, H, N)):
+        raise ValueError("lse must be a contiguous float32 device tensor [B, H, N]")
+    stream = _stream(q, stream)
+    with torch.cuda.device(q.device):
+        _check(LIB.monarch_attn_exact_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                          None if lse is None else lse.data_ptr(), B, H, N, d,
+                                          dtype_code(q.dtype), stream))
+    return out, lse
 
 
 def monarch_attention(q, k, v, m: int, b: int, T: int, stream=None):

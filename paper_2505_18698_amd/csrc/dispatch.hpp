@@ -11,6 +11,7 @@
 // per head, with the states in LDS.
 #pragma once
 
+#include <cmath>
 #include <mutex>
 #include <type_traits>
 #include <unordered_map>
@@ -191,6 +192,29 @@ template <typename T> int run_fused(Launcher &L, const CallBufs &B, ma::HeadDims
         if (rgb) return launch_fused<T, true, false>(L, B, hd, c);
         if (rgm) return launch_fused<T, false, true>(L, B, hd, c);
         return launch_fused<T, false, false>(L, B, hd, c);
+    }
+}
+
+template <typename T, int D> int launch_exact(Launcher &L, const CallBufs &B, float *lse, int64_t BH, int n, int d)
+{
+    const ma::Bufs<T> p = typed<T>(B);
+    const int64_t grid = BH * ((n + 63) / 64);
+    if (grid > 0x7fffffff) return fail(MA_EUNSUPPORTED, "too many query blocks for one grid");
+    const float s_log2e = (float)(1.4426950408889634 / std::sqrt((double)d));
+    return L.run(kExact, [&] {
+        return launched([&] {
+            hipLaunchKernelGGL((ma::exact_attention<T, D>), dim3((unsigned)grid), dim3(256), 0, L.stream, p, lse, n, d,
+                               s_log2e);
+        });
+    });
+}
+
+template <typename T> int run_exact_impl(Launcher &L, const CallBufs &B, float *lse, int64_t BH, int n, int d)
+{
+    switch (tile_d(d)) {
+    case 64: return launch_exact<T, 64>(L, B, lse, BH, n, d);
+    case 96: return launch_exact<T, 96>(L, B, lse, BH, n, d);
+    default: return launch_exact<T, 128>(L, B, lse, BH, n, d);
     }
 }
 

@@ -6,4 +6,8 @@ template <> int run_call<__bf16>(Launcher &L, const CallBufs &B, const CallDims 
 {
     return run_call_impl<__bf16>(L, B, c, path);
 }
+template <> int run_exact<__bf16>(Launcher &L, const CallBufs &B, float *lse, int64_t BH, int n, int d)
+{
+    return run_exact_impl<__bf16>(L, B, lse, BH, n, d);
+}
 }  // namespace ma_host

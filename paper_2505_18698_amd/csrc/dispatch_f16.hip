@@ -6,4 +6,8 @@ template <> int run_call<_Float16>(Launcher &L, const CallBufs &B, const CallDim
 {
     return run_call_impl<_Float16>(L, B, c, path);
 }
+template <> int run_exact<_Float16>(Launcher &L, const CallBufs &B, float *lse, int64_t BH, int n, int d)
+{
+    return run_exact_impl<_Float16>(L, B, lse, BH, n, d);
+}
 }  // namespace ma_host

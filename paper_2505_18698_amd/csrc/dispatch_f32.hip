@@ -6,4 +6,8 @@ template <> int run_call<float>(Launcher &L, const CallBufs &B, const CallDims &
 {
     return run_call_impl<float>(L, B, c, path);
 }
+template <> int run_exact<float>(Launcher &L, const CallBufs &B, float *lse, int64_t BH, int n, int d)
+{
+    return run_exact_impl<float>(L, B, lse, BH, n, d);
+}
 }  // namespace ma_host

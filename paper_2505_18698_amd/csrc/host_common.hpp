@@ -16,7 +16,7 @@ int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 inline int pad16(int64_t x) { return (int)((x + 15) / 16 * 16); }
 
 // Kernel kinds reported by the timing interface.
-enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4, kObjSum = 5 };
+enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4, kObjSum = 5, kExact = 6 };
 
 // Per-launch HIP events around every kernel when timing is enabled.
 constexpr int kMaxLaunches = 2 * 64 + 2;
@@ -93,5 +93,8 @@ inline bool uses_fused(int path, int32_t dtype, int64_t d, int64_t m, int64_t b)
 
 // Enqueue the whole forward pass for one element type (defined per dtype).
 template <typename T> int run_call(Launcher &L, const CallBufs &B, const CallDims &c, int path);
+
+// Enqueue exact softmax attention (with the row logsumexps when lse != null).
+template <typename T> int run_exact(Launcher &L, const CallBufs &B, float *lse, int64_t BH, int n, int d);
 
 }  // namespace ma_host

@@ -1297,4 +1297,102 @@ static __global__ __launch_bounds__(256) void objective_sum(const float *part, f
     obj[i] = f;
 }
 
+// ---------------------------------------------------------------------------------------
+// Exact softmax attention O = softmax(s Q K^T) V with the logsumexp of every
+// row (eq. softmax_attention): the quality reference the Monarch output is
+// measured against, and the upper bound of the objective (sum of the row
+// logsumexps).  One workgroup of 4 waves per 64 query rows; wave w owns 16
+// query rows (the B operand of the scores, in registers) and keeps an online
+// softmax (running max, sum and output) over tiles of 64 keys.  Scores are
+// transposed as in the half-steps (keys on the MFMA row axis), so the
+// probabilities feed the V product straight from registers; the key and value
+// tiles of the next step are fetched into registers while the current one is
+// computed.
+// ---------------------------------------------------------------------------------------
+template <typename T, int D> struct ExactAttn {
+    static constexpr int KT = 64, NT = KT / 16, W = 4, NTH = 64 * W;
+    static constexpr int LDK = Ld<T, D>::row;
+    static constexpr int LDS_BYTES = 2 * KT * LDK * (int)sizeof(T);
+
+    struct Tiles {
+        TileChunks<T, KT, D, NTH> kt, vt;
+    };
+
+    __device__ static void fetch(const T *kh, const T *vh, int n, int d, int key0, int tid, Tiles &g)
+    {
+        const int valid = n - key0 < KT ? n - key0 : KT;
+        g.kt.fetch([=](int r) { return kh + (int64_t)(key0 + r) * d; }, valid, tid, d);
+        g.vt.fetch([=](int r) { return vh + (int64_t)(key0 + r) * d; }, valid, tid, d);
+    }
+
+    __device__ static void run(const Bufs<T> &p, float *lse_out, int n, int d, float s_log2e, char *lds)
+    {
+        T *Ks = reinterpret_cast<T *>(lds);
+        T *Vs = Ks + KT * LDK;
+        const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4, c16 = lane & 15;
+        const int64_t qblocks = (n + 63) / 64;
+        const int64_t bh = blockIdx.x / qblocks;
+        const int row = (int)(blockIdx.x % qblocks) * 64 + wave * 16 + c16;  // this lane's query row
+        const int64_t hoff = bh * (int64_t)n * d;
+        const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
+
+        RowFrags<T, D> bf;
+        bf.load(row < n ? qh + (int64_t)row * d : nullptr, g, d);
+        float mx = kMasked, sum = 0.f;  // running max (log2 units) and sum of this query row
+        f32x4 o[D / 16];
+#pragma unroll
+        for (int vt = 0; vt < D / 16; ++vt) o[vt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        Tiles cur, nxt;
+        fetch(kh, vh, n, d, 0, tid, cur);
+        for (int key0 = 0; key0 < n; key0 += KT) {
+            cur.kt.template stage<LDK>(Ks, tid);
+            cur.vt.template stage<LDK>(Vs, tid);
+            __syncthreads();
+            if (key0 + KT < n) fetch(kh, vh, n, d, key0 + KT, tid, nxt);
+            const int kv = n - key0;  // keys >= kv of this tile are beyond N
+            f32x4 sc[NT];             // lane holds u = s log2(e) q.k for keys 16t + 4g + qq
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                f32x4 acc;
+                gemm_scores_rt<T, D, 1>(Ks + (16 * t + c16) * LDK, &bf, &acc, g);
+                sc[t] = acc * s_log2e;
+            }
+            const float tmax = tiles_max<NT, true>(sc, kv, g);
+            const float mnew = fmaxf(mx, tmax);
+            const float corr = __builtin_amdgcn_exp2f(mx - mnew);
+            float tsum = 0.f;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    float e = __builtin_amdgcn_exp2f(sc[t][qq] - mnew);
+                    if (16 * t + 4 * g + qq >= kv) e = 0.f;
+                    tsum += e;
+                    sc[t][qq] = e;
+                }
+            }
+            sum = sum * corr + lanegroup_sum(tsum);
+            mx = mnew;
+            ProbFrags<T, NT> pf;
+            pf.pack(sc);
+#pragma unroll
+            for (int vt = 0; vt < D / 16; ++vt) o[vt] = o[vt] * corr + gemm_aggregate<T, NT>(Vs, LDK, 16 * vt, pf, lane);
+            __syncthreads();  // the tiles are restaged next
+            cur = nxt;
+        }
+        const float inv = fast_rcp(sum);
+        store_row<T, D>(row < n ? p.out + hoff + (int64_t)row * d : nullptr, o, inv, lane, d);
+        if (lse_out && g == 0 && row < n) lse_out[bh * n + row] = row_lse(mx, sum);
+    }
+};
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void exact_attention(Bufs<T> p, float *lse, int n, int d, float s_log2e)
+{
+    using U = ExactAttn<T, D>;
+    __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
+    U::run(p, lse, n, d, s_log2e, lds);
+}
+
 }  // namespace ma

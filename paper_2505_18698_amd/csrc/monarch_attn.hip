@@ -276,6 +276,50 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
     return forward(q, k, v, out, nullptr, B, H, N, d, m, b, T, dtype, stream);
 }
 
+int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *out, float *lse, int64_t B,
+                           int64_t H, int64_t N, int64_t d, int32_t dtype, void *stream)
+{
+    g_err[0] = '\0';
+    if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
+    if (B < 1 || H < 1 || N < 1 || d < 1) return fail(MA_EINVAL, "B, H, N and d must be >= 1");
+    if (dtype != MA_F32 && dtype != MA_BF16 && dtype != MA_F16) return fail(MA_EINVAL, "unknown dtype %d", dtype);
+    if (d > 128 || d % (16 / (int64_t)elem_bytes(dtype)) != 0)
+        return fail(MA_EUNSUPPORTED, "d must be a multiple of %d up to 128 (got %lld)", (int)(16 / elem_bytes(dtype)),
+                    (long long)d);
+    if (N > 0x7fffffff) return fail(MA_EUNSUPPORTED, "N too large");
+    if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)out) & 15u)
+        return fail(MA_EINVAL, "q, k, v and out must be 16-byte aligned");
+    if ((uintptr_t)lse & 3u) return fail(MA_EINVAL, "lse must be 4-byte aligned");
+    const int64_t BH = B * H;
+    const size_t tensor_bytes = (size_t)BH * N * d * elem_bytes(dtype);
+    if (overlaps(out, tensor_bytes, q, tensor_bytes) || overlaps(out, tensor_bytes, k, tensor_bytes) ||
+        overlaps(out, tensor_bytes, v, tensor_bytes))
+        return fail(MA_EINVAL, "out must not overlap q, k or v");
+    const size_t lse_bytes = (size_t)BH * N * sizeof(float);
+    if (lse && (overlaps(lse, lse_bytes, q, tensor_bytes) || overlaps(lse, lse_bytes, k, tensor_bytes) ||
+                overlaps(lse, lse_bytes, v, tensor_bytes) || overlaps(lse, lse_bytes, out, tensor_bytes)))
+        return fail(MA_EINVAL, "lse must not overlap q, k, v or out");
+    CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+    std::unique_lock<std::mutex> tlock(g_timing_mutex);
+    Launcher L{(hipStream_t)stream, g_timing.enabled};
+    if (!L.timed) tlock.unlock();
+    (void)hipGetLastError();
+    int rc;
+    switch (dtype) {
+    case MA_F32: rc = run_exact<float>(L, bufs, lse, BH, (int)N, (int)d); break;
+    case MA_BF16: rc = run_exact<__bf16>(L, bufs, lse, BH, (int)N, (int)d); break;
+    default: rc = run_exact<_Float16>(L, bufs, lse, BH, (int)N, (int)d); break;
+    }
+    if (L.timed) {
+        g_timing.nlaunch = L.n;
+        g_timing.ready = (rc == MA_OK && L.n > 0);
+    }
+    if (rc != MA_OK) return rc;
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(MA_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return MA_OK;
+}
+
 int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void *out, float *obj, int64_t B,
                                int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
                                void *stream)

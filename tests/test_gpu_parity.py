@@ -447,3 +447,53 @@ def test_objective_paths_agree_bitwise(lib, n, m, b):
         lib.monarch_attn_set_path(prev)
     assert torch.equal(o1, o2)
     assert torch.equal(f1, f2)
+
+
+# -- exact softmax attention (the quality reference) ------------------------------------
+
+def _lse_rows(q, k, rows):
+    s = 1.0 / np.sqrt(q.shape[-1])
+    z = s * q[rows].astype(np.float64) @ k.astype(np.float64).T
+    zm = z.max(axis=1, keepdims=True)
+    return zm[:, 0] + np.log(np.exp(z - zm).sum(axis=1))
+
+
+def gpu_exact(lib, q, k, v, dtype):
+    import torch
+
+    td = _torch_dtype(dtype)
+    t = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
+    out = torch.full_like(t[0], float("nan"))
+    lse = torch.full(q.shape[:3], float("nan"), dtype=torch.float32, device="cuda")
+    lib.monarch_attn_exact_fwd(t[0], t[1], t[2], out, lse)
+    torch.cuda.synchronize()
+    return out.double().cpu().numpy(), lse.double().cpu().numpy()
+
+
+@pytest.mark.parametrize(
+    "B,H,n,d,dtype",
+    [(1, 2, 256, 64, "f32"), (2, 2, 200, 64, "bf16"), (1, 3, 1000, 128, "f16"), (1, 2, 333, 72, "bf16"),
+     (1, 1, 64, 48, "bf16"), (1, 2, 1, 64, "bf16"), (1, 1, 130, 96, "f32")],
+)
+def test_exact_attention(lib, B, H, n, d, dtype):
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=n + d, scale=1.5)
+    o, lse = gpu_exact(lib, q, k, v, dtype)
+    ref = oracle.dense_attention_rows(q, k, v)
+    check(o, ref, dtype, f"exact {dtype} B{B} H{H} N{n} d{d}")
+    for bi in range(B):
+        for h in range(H):
+            want = _lse_rows(q[bi, h], k[bi, h], np.arange(n))
+            assert np.abs(lse[bi, h] - want).max() <= 1e-4 * max(1.0, np.abs(want).max())
+
+
+def test_exact_attention_n16384_sampled_rows(lib):
+    w = si.WORKLOADS["speed_n16384"]
+    q, k, v, _ = si.make_qkv(w)
+    o, lse = gpu_exact(lib, q, k, v, w.dtype)
+    rows = np.random.default_rng(0).choice(w.N, size=48, replace=False)
+    heads = [0, 11]
+    ref = oracle.dense_attention_rows(q[:, heads], k[:, heads], v[:, heads], rows)
+    check(o[:, heads][:, :, rows], ref, w.dtype, "exact N16384 sampled rows")
+    for hi, h in enumerate(heads):
+        want = _lse_rows(q[0, h], k[0, h], rows)
+        assert np.abs(lse[0, h, rows] - want).max() <= 1e-4 * np.abs(want).max()
