@@ -20,6 +20,12 @@ last-level cache cannot serve them from one step to the next.
 cpu_baseline: the fp64 C oracle, as it stands, on this host's cores, on the
 same workload (repeated whole forward passes, about 10-30 s in total).
 
+quality: the error of O against exact softmax attention and the gap of the
+variational objective to its exact-softmax maximum, for T = 1, 2, 3, on the
+structured workloads (ViT- and RoBERTa-shaped, and 16K tokens with
+RoBERTa-like decaying scores; the speed points' iid Q, K have no structure
+to approximate).  GPU only, outside the timed regions.
+
 Only one GPU is supported: --gpus N with N > 1 exits with a message.
 """
 import argparse
@@ -161,6 +167,47 @@ def measure(ma, torch, w, steps, warmup):
     return ms, kernels, meta, nsets
 
 
+QUALITY_WORKLOADS = ("vit_b16_n196", "roberta_n1024", "lm_n16384")
+
+
+def quality(ma, torch, w, steps_list=(1, 2, 3)):
+    """Approximation quality on the workload's first input set, all on the GPU:
+    the relative Frobenius error of O against exact softmax attention
+    (monarch_attn_exact_fwd), and the objective gap per query row,
+    (sum of exact row logsumexps - f(M^(T))) / N in nats, for several T.
+    The exact kernel is this library's reference, not a tuned attention
+    kernel; its time is context only."""
+    import synth_inputs as si
+
+    q, k, v, _ = si.make_qkv(w)
+    td = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[w.dtype]
+    t = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
+    del q, k, v
+    exact = torch.empty_like(t[0])
+    lse = torch.empty(t[0].shape[:3], dtype=torch.float32, device="cuda")
+    ma.monarch_attn_exact_fwd(t[0], t[1], t[2], exact, lse)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    ma.monarch_attn_exact_fwd(t[0], t[1], t[2], exact, lse)
+    end.record()
+    end.synchronize()
+    ex = exact.double()
+    bound = lse.double().sum(dim=2)   # [B, H]
+    rows = []
+    for T in steps_list:
+        out = torch.empty_like(t[0])
+        obj = torch.empty((w.B, w.H, T), dtype=torch.float32, device="cuda")
+        ma.monarch_attn_fwd_objective(t[0], t[1], t[2], out, obj, w.m, w.b, T)
+        torch.cuda.synchronize()
+        err = float(torch.linalg.vector_norm(out.double() - ex) / torch.linalg.vector_norm(ex))
+        gap = ((bound - obj[..., -1].double()) / w.N).mean().item()
+        rows.append({"T": T, "rel_frob_vs_exact": round(err, 5), "objective_gap_per_row": round(gap, 5),
+                     "objective_per_step": [round(x, 2) for x in obj[0, 0].tolist()]})
+    torch.cuda.synchronize()
+    return {"workload": w.name, "exact_us": round(start.elapsed_time(end) * 1e3, 1),
+            "exact_objective_head0": round(float(bound[0, 0]), 2), "monarch": rows}
+
+
 def kernel_sources_sha():
     import glob
     import hashlib
@@ -261,6 +308,8 @@ def main():
     ap.add_argument("--also", default="speed_n4096,vit_b16_n196,vit_b16_n197",
                     help="comma-separated extra workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-quality", action="store_true",
+                    help="skip the approximation-quality figures (error against exact attention, objective gap)")
     ap.add_argument("--copy-mb", type=str, default=None,
                     help="instead of the benchmark: time torch's device copy at these sizes (MB, comma "
                          "separated); the reference kernel for scaling HBM byte counters")
@@ -331,6 +380,8 @@ def main():
                      "ms_per_step": round(ms2, 6), "roofline": roofline_of(dom2, w2.dtype, w2.name),
                      "call_roofline": call_roofline(w2, ms2), "kernels": kern2})
     result["also"] = also
+    if not args.no_quality:
+        result["quality"] = [quality(ma, torch, si.WORKLOADS[name]) for name in QUALITY_WORKLOADS]
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(result), flush=True)
