@@ -129,6 +129,50 @@ int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void
 int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *out, float *lse,
                            int64_t B, int64_t H, int64_t N, int64_t d, int32_t dtype, void *stream);
 
+/*
+ * monarch_attn_bwd -- the gradient of monarch_attn_fwd: given dout = dL/dO,
+ * dq, dk, dv = dL/dQ, dL/dK, dL/dV of the same T-step computation (reverse
+ * mode through the unrolled iteration of Sec. 3 from L^(0) = I and eq.
+ * monarch_multiply, the factors entering through eqs. R_update and L_update
+ * with beta_r, beta_l).  The paper states no gradient; this is the exact
+ * derivative of the forward pass as defined there, including the entropy
+ * terms c_L and the normalisers c_R, and the key mask of Appendix "Padding
+ * and Masking" when N < m * b.  Padded rows receive no gradient (dq, dk, dv
+ * have N rows).
+ *
+ * q, k, v, dout : DEVICE pointers to [B, H, N, d] tensors of element type
+ *                 `dtype`, 16-byte aligned, read only.
+ * dq, dk, dv    : DEVICE pointers to [B, H, N, d] tensors of that type,
+ *                 16-byte aligned, overlapping neither each other nor the
+ *                 inputs.  Fully overwritten.  All owned by the caller.
+ * B, H, N, d, m, b, T, dtype, stream : as monarch_attn_fwd, and in addition
+ *                 m, b <= 64, d <= 64 and T <= 32 (else MA_EUNSUPPORTED).
+ *
+ * Runs the forward half-steps again, keeping the states of every step, then
+ * one launch per half-step in reverse order; all of it on `stream`,
+ * asynchronously.  The arithmetic of the reverse sweep is fp32 (the states
+ * of the recomputed forward pass are in the element type, as in
+ * monarch_attn_fwd), and the result is deterministic (no atomics).
+ * Workspace: monarch_attn_bwd_workspace_bytes(), in the same per-device
+ * buffer as monarch_attn_fwd (same rules).  Errors as monarch_attn_fwd.
+ */
+int monarch_attn_bwd(const void *q, const void *k, const void *v, const void *dout,
+                     void *dq, void *dk, void *dv,
+                     int64_t B, int64_t H, int64_t N, int64_t d,
+                     int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
+
+/* MA_OK if monarch_attn_bwd supports (N, d, m, b, T, dtype), else MA_EINVAL or
+ * MA_EUNSUPPORTED (with last_error set).  Makes no HIP call. */
+int monarch_attn_bwd_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype);
+
+/* Bytes of device workspace monarch_attn_bwd needs (0 on bad arguments):
+ * 2T state tensors of m b 64 elements and 2T - 1 arrays of m b floats per head
+ * for the recomputed forward pass, 2 N d floats (dQ, dK accumulators), 3 m b 64
+ * floats and 2 m b floats (state gradients) per head, each array rounded up to
+ * 256 bytes.  Makes no HIP call. */
+size_t monarch_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,
+                                        int64_t m, int64_t b, int32_t T, int32_t dtype);
+
 /* Text of the last failure on this thread ("" if none).  Valid until the next
  * call into the library from this thread. */
 const char *monarch_attn_last_error(void);
@@ -163,16 +207,17 @@ int monarch_attn_set_path(int32_t path);
 
 /*
  * Per-launch timing, for measurement only.  While enabled (flag != 0), every
- * monarch_attn_fwd records a HIP event before and after each kernel it
- * launches, on the caller's stream.  monarch_attn_timing_read() synchronises
+ * call of the library (forward, objective, exact attention, gradient) records
+ * a HIP event before and after each kernel it launches, on the caller's
+ * stream.  monarch_attn_timing_read() synchronises
  * on the last call's final event and writes, for at most `cap` launches of
  * that call, the duration in milliseconds to ms[i] and the kernel kind to
  * kind[i] (0 R half-step, 1 L half-step, 2 last R half-step with Y,
  * 3 last L half-step with the Monarch product and the store of O,
  * 4 the one-workgroup-per-head kernel, 5 the sum of the objective shares,
- * 6 exact attention);
- * it returns the number of launches of that
- * call, or -1 on error.
+ * 6 exact attention, 7 an L half-step of the gradient, 8 an R half-step of
+ * the gradient); it returns the number of launches of that call, or -1 on
+ * error.
  */
 int monarch_attn_timing_enable(int32_t flag);
 int32_t monarch_attn_timing_read(float *ms, int32_t *kind, int32_t cap);

@@ -1,4 +1,4 @@
-"""MonarchAttention forward pass on MI355X (gfx950): HIP kernels behind a C ABI.
+"""MonarchAttention forward pass (and its gradient) on MI355X (gfx950): HIP kernels behind a C ABI.
 
 The C ABI is declared in include/monarch_attn.h; this package is its thin
 Python binding (ctypes, with torch used only for device memory and streams).
@@ -27,6 +27,9 @@ try:
         dtype_code,
         fused_applies,
         monarch_attention,
+        monarch_attn_bwd,
+        monarch_attn_bwd_check,
+        monarch_attn_bwd_workspace_bytes,
         monarch_attn_check,
         monarch_attn_fwd,
         monarch_attn_fwd_objective,

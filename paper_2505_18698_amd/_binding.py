@@ -15,7 +15,7 @@ MA_F32, MA_BF16, MA_F16 = 0, 1, 2
 MA_OK, MA_EINVAL, MA_EUNSUPPORTED, MA_EHIP, MA_ENOMEM = 0, 1, 2, 3, 4
 STATUS_NAMES = {0: "MA_OK", 1: "MA_EINVAL", 2: "MA_EUNSUPPORTED", 3: "MA_EHIP", 4: "MA_ENOMEM"}
 KIND_NAMES = {0: "r_half_step", 1: "l_half_step", 2: "r_half_step_final", 3: "monarch_apply",
-              4: "monarch_fused_head", 5: "objective_sum", 6: "exact_attention"}
+              4: "monarch_fused_head", 5: "objective_sum", 6: "exact_attention", 7: "l_bwd", 8: "r_bwd"}
 PATH_AUTO, PATH_HALF_STEPS, PATH_FUSED = 0, 1, 2
 
 # Every symbol declared in include/monarch_attn.h.
@@ -23,6 +23,9 @@ EXPORTS = (
     "monarch_attn_fwd",
     "monarch_attn_fwd_objective",
     "monarch_attn_exact_fwd",
+    "monarch_attn_bwd",
+    "monarch_attn_bwd_check",
+    "monarch_attn_bwd_workspace_bytes",
     "monarch_attn_last_error",
     "monarch_attn_check",
     "monarch_attn_workspace_bytes",
@@ -52,6 +55,12 @@ def _load() -> ctypes.CDLL:
     lib.monarch_attn_fwd_objective.restype = ctypes.c_int
     lib.monarch_attn_exact_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i32, vp]
     lib.monarch_attn_exact_fwd.restype = ctypes.c_int
+    lib.monarch_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
+    lib.monarch_attn_bwd.restype = ctypes.c_int
+    lib.monarch_attn_bwd_check.argtypes = [i64, i64, i64, i64, i32, i32]
+    lib.monarch_attn_bwd_check.restype = ctypes.c_int
+    lib.monarch_attn_bwd_workspace_bytes.argtypes = [i64, i64, i64, i64, i64, i64, i32, i32]
+    lib.monarch_attn_bwd_workspace_bytes.restype = ctypes.c_size_t
     lib.monarch_attn_last_error.argtypes = []
     lib.monarch_attn_last_error.restype = ctypes.c_char_p
     lib.monarch_attn_check.argtypes = [i64, i64, i64, i64, i32, i32]
@@ -166,6 +175,30 @@ def monarch_attn_exact_fwd(q, k, v, out, lse=None, stream=None):
                                           None if lse is None else lse.data_ptr(), B, H, N, d,
                                           dtype_code(q.dtype), stream))
     return out, lse
+
+
+def monarch_attn_bwd(q, k, v, dout, dq, dk, dv, m: int, b: int, T: int, stream=None):
+    """dq, dk, dv = the gradient of <MonarchAttention(q, k, v), dout> into the
+    given tensors (all [B, H, N, d], one dtype).  Asynchronous on `stream`
+    (torch's current stream when None).  Returns (dq, dk, dv)."""
+    import torch
+
+    _check_tensors(q, k, v, dout)
+    _check_tensors(q, dq, dk, dv)
+    B, H, N, d = q.shape
+    stream = _stream(q, stream)
+    with torch.cuda.device(q.device):
+        _check(LIB.monarch_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), dq.data_ptr(),
+                                    dk.data_ptr(), dv.data_ptr(), B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
+    return dq, dk, dv
+
+
+def monarch_attn_bwd_check(N: int, d: int, m: int, b: int, T: int, dtype: int) -> int:
+    return LIB.monarch_attn_bwd_check(N, d, m, b, T, dtype)
+
+
+def monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, dtype) -> int:
+    return int(LIB.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, dtype))
 
 
 def monarch_attention(q, k, v, m: int, b: int, T: int, stream=None):

@@ -1,0 +1,368 @@
+// Gradient of the MonarchAttention forward pass: reverse mode through the
+// unrolled T steps of Sec. 3 (the paper gives no gradient; the sweep below is
+// derived from the state form of its Implementation paragraph).
+//
+// Notation per head, with s = 1/sqrt(d), Qbar[j][l] = Q[l*b + j] (unscaled),
+// Kbar[k][i] = K[k*b + i], and the states of step t as the forward stores
+// them (alpha_R unscaled, the scale applied on the scores):
+//   R update of block k:  Z_R[j][i] = s <alpha_R[k][j], Kbar[k][i]> / c_R[k][j]
+//                         (keys i past the sequence masked), R = softmax_i Z_R,
+//                         alpha_L[j][k] = sum_i R Kbar[k][i], c_L[j][k] = sum_i R log R,
+//                         Y[j][k] = sum_i R Vbar[k][i] at the last step;
+//   L update of class j:  Z_L[l][k] = s <Qbar[j][l], alpha_L[j][k]> - c_L[j][k],
+//                         L = softmax_k Z_L, alpha_R'[k][j] = sum_l L Qbar[j][l],
+//                         c_R'[k][j] = sum_l L (inputs of step t+1), and at the
+//                         last step O[l*b + j] = sum_k L Y[j][k];
+//   step 1 starts from L = I: alpha_R[k][j] = Q[k*b + j], c_R = 1.
+// A softmax p = softmax(z) pulls dp back to dz = p (dp - <p, dp>).
+//
+// The sweep runs t = T .. 1, one launch per half-step:
+//   l_bwd (class j of step t):  dL = dO . Y (t = T; also dY = L^T dO) or
+//       dL = Qbar . d alpha_R' + d c_R' (t < T; also dQbar += L d alpha_R');
+//       dW = s L (dL - <L, dL>) (the scale folded in);  dQbar += dW alpha_L,
+//       d alpha_L = dW^T Qbar,  d c_L = -(1/s) sum_l dW.
+//   r_bwd (block k of step t):  dR = d alpha_L . Kbar + d c_L (log R + 1)
+//       (+ dY . Vbar at t = T, with dVbar = R^T dY);  dZ = R (dR - <R, dR>);
+//       dKbar += R^T d alpha_L + (s dZ / c_R)^T alpha_R;
+//       d alpha_R = (s dZ / c_R) Kbar;  d c_R = -sum_i dZ log R / c_R (the rows
+//       of dZ sum to zero, so log R stands in for the logits);  at t = 1
+//       d alpha_R is added to dQ (alpha_R = the rows of Q) and c_R is constant.
+//
+// Every unit keeps its matrices in fp32 LDS tiles and runs every product on
+// v_mfma_f32_16x16x4f32.  The gradients of the states and the dQ, dK
+// accumulators are fp32 in the workspace.  Within a launch the units write
+// disjoint rows, and launches that touch the same rows are ordered on the
+// stream, so read-modify-writes need no atomics and the result is
+// deterministic.  dq and dk are written in the element type by the step-1
+// R launch (the last one to touch them), dv by the step-T R launch.
+#pragma once
+
+#include "ma_kernels.hpp"
+
+namespace ma {
+
+template <typename T> struct BwdBufs {
+    const T *q, *k, *v, *dout;  // [B*H][n][d]
+    const T *aR, *aL, *Y;       // states of the step being undone ([m][b][D], [b][m][D], [b][m][D])
+    const float *cR, *cL;       // c_R [b][m] (j-major), c_L [m][b] (k-major), as the forward writes them
+    float *dQ, *dK;             // fp32 accumulators [B*H][n][d]
+    T *dq, *dk, *dv;            // results [B*H][n][d]
+    float *daL, *dcL, *dY;      // [b][m][D], [b][m], [b][m][D]: written by l_bwd, read by r_bwd of the step
+    float *daR, *dcR;           // [m][b][D], [m][b]: written by r_bwd of step t, read by l_bwd of step t-1
+};
+
+struct BwdDims {
+    int m, b, n, d;  // as in the forward; here m, b <= 64 and d <= 64 (states of width 64)
+    float s;         // 1/sqrt(d)
+};
+
+namespace bwd {
+
+constexpr int kD = 64;    // row width of the states (the forward's tile width for d <= 64)
+constexpr int kLd = 81;   // row stride (floats) of the LDS tiles: 17 mod 64 spreads both access orders
+constexpr int kWaves = 8;
+constexpr int kThreads = 64 * kWaves;
+
+__device__ inline int up16(int x) { return (x + 15) & ~15; }
+
+__device__ inline float wave_sum(float x)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    return x;
+}
+
+__device__ inline float wave_max(float x)
+{
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+    return x;
+}
+
+// A matrix view of an LDS tile: element (r, c) at p[r * rs + c * cs].
+struct View {
+    const float *p;
+    int rs, cs;
+};
+__device__ inline View as_is(const float *t) { return View{t, kLd, 1}; }
+__device__ inline View transposed(const float *t) { return View{t, 1, kLd}; }
+
+// out(r, c) = sum over the NOPS pairs of sum_k A(r, k) B(k, c), for r < M,
+// c < N (multiples of 16), k < K (a multiple of 4); the 16 x 16 output tiles
+// are shared out over the waves and each element is handed to st(r, c, value)
+// by exactly one lane.  A lane of v_mfma_f32_16x16x4f32 holds A(row lane%16,
+// k lane/16) and B(k lane/16, column lane%16) and receives the outputs
+// (4 (lane/16) + q, lane%16), q = 0..3.
+template <int NOPS, typename Store>
+__device__ inline void gemm(const View (&a)[NOPS], const View (&b)[NOPS], int M, int N, int K, int wave, int lane,
+                            Store &&st)
+{
+    const int g = lane >> 4, c = lane & 15, tn = N >> 4, tiles = (M >> 4) * tn;
+    for (int t = wave; t < tiles; t += kWaves) {
+        const int r0 = (t / tn) * 16, c0 = (t % tn) * 16;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int o = 0; o < NOPS; ++o) {
+            const float *pa = a[o].p + (r0 + c) * a[o].rs + g * a[o].cs;
+            const float *pb = b[o].p + g * b[o].rs + (c0 + c) * b[o].cs;
+            const int sa = 4 * a[o].cs, sb = 4 * b[o].rs;
+            for (int k0 = 0; k0 < K; k0 += 4) {
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(*pa, *pb, acc, 0, 0, 0);
+                pa += sa;
+                pb += sb;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) st(r0 + 4 * g + q, c0 + c, acc[q]);
+    }
+}
+
+__device__ inline auto to_lds(float *t)
+{
+    return [t](int r, int c, float v) { t[r * kLd + c] = v; };
+}
+
+// Rows r < R and columns c < C (R, C the padded extents, C <= 64) of an LDS
+// tile from a row-major global matrix whose row r starts at src(r): element
+// (r, c) is read while r < nr and c < nc, zero elsewhere.
+template <typename E, typename Src>
+__device__ inline void load_tile(float *dst, int R, int C, int nr, int nc, Src src, int tid)
+{
+    for (int idx = tid; idx < R * 64; idx += kThreads) {
+        const int r = idx >> 6, c = idx & 63;
+        if (c < C) dst[r * kLd + c] = (r < nr && c < nc) ? static_cast<float>(src(r)[c]) : 0.f;
+    }
+}
+
+// ---------------------------------------------------------------------------------------
+// The L update of class j of step t undone (LAST: t = T, the update that also
+// produced O).  S: rows of the tiles (16, 32 or 64, >= m).
+// ---------------------------------------------------------------------------------------
+template <typename T, int S, bool LAST> struct LBwd {
+    static constexpr int LDS_FLOATS = 6 * S * kLd + 2 * S;
+
+    __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
+    {
+        const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+        const int m = dm.m, b = dm.b, n = dm.n, d = dm.d;
+        const int64_t bh = blockIdx.x / b;
+        const int j = blockIdx.x % b;
+        const int MB = up16(m), DB = up16(d);
+        const int ml = (n - j + b - 1) / b;  // rows l with l*b + j < n
+        const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * kD, coff = bh * Np;
+        float *Qb = lds, *aL = Qb + S * kLd, *Lm = aL + S * kLd, *dL = Lm + S * kLd, *X = dL + S * kLd,
+              *G = X + S * kLd;
+        float *cL = G + S * kLd, *dcR = cL + S;
+
+        load_tile<T>(Qb, MB, DB, ml, d, [&](int l) { return p.q + toff + ((int64_t)l * b + j) * d; }, tid);
+        load_tile<T>(aL, MB, DB, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * kD; }, tid);
+        if constexpr (LAST) {
+            load_tile<T>(X, MB, DB, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * kD; }, tid);
+            load_tile<T>(G, MB, DB, ml, d, [&](int l) { return p.dout + toff + ((int64_t)l * b + j) * d; }, tid);
+        } else {
+            load_tile<float>(X, MB, DB, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * kD; }, tid);
+        }
+        for (int k = tid; k < S; k += kThreads) {
+            cL[k] = k < m ? p.cL[coff + (int64_t)k * b + j] : 0.f;
+            dcR[k] = (!LAST && k < m) ? p.dcR[coff + (int64_t)k * b + j] : 0.f;
+        }
+        __syncthreads();
+
+        // unnormalised scores <Qbar[l], alpha_L[k]>
+        gemm<1>({as_is(Qb)}, {transposed(aL)}, MB, MB, DB, wave, lane, to_lds(Lm));
+        __syncthreads();
+        // L[l][k] = softmax_k (s score - c_L[k]): one wave per row l, lane k
+        for (int l = wave; l < MB; l += kWaves) {
+            const int k = lane;
+            if (l >= m) {
+                if (k < MB) Lm[l * kLd + k] = 0.f;
+                continue;
+            }
+            const float z = k < m ? dm.s * Lm[l * kLd + k] - cL[k] : -INFINITY;
+            const float mx = wave_max(z);
+            const float e = k < m ? __expf(z - mx) : 0.f;
+            const float sum = wave_sum(e);
+            if (k < MB) Lm[l * kLd + k] = e / sum;
+        }
+        __syncthreads();
+
+        if constexpr (LAST) {
+            // dL = dO Y^T;  dY = L^T dO (to the workspace, read by r_bwd of this step)
+            gemm<1>({as_is(G)}, {transposed(X)}, MB, MB, DB, wave, lane, to_lds(dL));
+            float *dY = p.dY + soff + (int64_t)j * m * kD;
+            gemm<1>({transposed(Lm)}, {as_is(G)}, MB, DB, MB, wave, lane, [&](int k, int e, float v) {
+                if (k < m && e < d) dY[(int64_t)k * kD + e] = v;
+            });
+        } else {
+            // dL = Qbar d alpha_R'^T (+ d c_R' below);  G = L d alpha_R' (the alpha_R' term of dQbar)
+            gemm<1>({as_is(Qb)}, {transposed(X)}, MB, MB, DB, wave, lane, to_lds(dL));
+            gemm<1>({as_is(Lm)}, {as_is(X)}, MB, DB, MB, wave, lane, to_lds(G));
+        }
+        __syncthreads();
+        // dW = s L (dL - <L, dL>), in place of dL
+        for (int l = wave; l < MB; l += kWaves) {
+            const int k = lane;
+            const float pk = k < MB ? Lm[l * kLd + k] : 0.f;
+            const float w = k < MB ? dL[l * kLd + k] + dcR[k] : 0.f;
+            const float dot = wave_sum(pk * w);
+            if (k < MB) dL[l * kLd + k] = dm.s * pk * (w - dot);
+        }
+        __syncthreads();
+
+        // dQ rows l*b + j: dW alpha_L (+ L d alpha_R')
+        float *dQ = p.dQ + toff + (int64_t)j * d;
+        gemm<1>({as_is(dL)}, {as_is(aL)}, MB, DB, MB, wave, lane, [&](int l, int e, float v) {
+            if (l < ml && e < d) {
+                float *o = dQ + (int64_t)l * b * d + e;
+                if constexpr (LAST) {
+                    *o = v;
+                } else {
+                    *o += v + G[l * kLd + e];
+                }
+            }
+        });
+        // d alpha_L[k] = dW^T Qbar
+        float *daL = p.daL + soff + (int64_t)j * m * kD;
+        gemm<1>({transposed(dL)}, {as_is(Qb)}, MB, DB, MB, wave, lane, [&](int k, int e, float v) {
+            if (k < m && e < d) daL[(int64_t)k * kD + e] = v;
+        });
+        // d c_L[k] = -(1/s) sum_l dW[l][k]
+        for (int k = tid; k < m; k += kThreads) {
+            float cs = 0.f;
+            for (int l = 0; l < MB; ++l) cs += dL[l * kLd + k];
+            p.dcL[coff + (int64_t)j * m + k] = -cs / dm.s;
+        }
+    }
+};
+
+// ---------------------------------------------------------------------------------------
+// The R update of block k of step t undone (FIRST: t = 1, LAST: t = T).
+// S: rows of the tiles (16, 32 or 64, >= b).
+// ---------------------------------------------------------------------------------------
+template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
+    static constexpr int TILES = LAST ? 7 : 5;
+    static constexpr int LDS_FLOATS = TILES * S * kLd + 2 * S;
+
+    __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
+    {
+        const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+        const int m = dm.m, b = dm.b, n = dm.n, d = dm.d;
+        const int64_t bh = blockIdx.x / m;
+        const int k = blockIdx.x % m;
+        const int BB = up16(b), DB = up16(d);
+        const int kv = min(b, n - k * b);  // real keys (and query rows) of block k
+        const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * kD, coff = bh * Np;
+        const int64_t row0 = (int64_t)k * b;  // first row of block k
+        float *Kb = lds, *aR = Kb + S * kLd, *dA = aR + S * kLd, *Rm = dA + S * kLd, *dR = Rm + S * kLd;
+        float *Vb = dR + S * kLd, *dYt = Vb + S * kLd;  // LAST only
+        float *cR = lds + TILES * S * kLd, *dcL = cR + S;
+
+        load_tile<T>(Kb, BB, DB, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
+        if constexpr (FIRST) {
+            load_tile<T>(aR, BB, DB, kv, d, [&](int jj) { return p.q + toff + (row0 + jj) * d; }, tid);
+        } else {
+            load_tile<T>(aR, BB, DB, b, d, [&](int jj) { return p.aR + soff + (row0 + jj) * kD; }, tid);
+        }
+        load_tile<float>(dA, BB, DB, b, d, [&](int jj) { return p.daL + soff + ((int64_t)jj * m + k) * kD; }, tid);
+        if constexpr (LAST) {
+            load_tile<T>(Vb, BB, DB, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
+            load_tile<float>(dYt, BB, DB, b, d, [&](int jj) { return p.dY + soff + ((int64_t)jj * m + k) * kD; },
+                             tid);
+        }
+        for (int jj = tid; jj < S; jj += kThreads) {
+            cR[jj] = (FIRST || jj >= b) ? 1.f : p.cR[coff + (int64_t)jj * m + k];
+            dcL[jj] = jj < b ? p.dcL[coff + (int64_t)jj * m + k] : 0.f;
+        }
+        __syncthreads();
+
+        // unnormalised scores <alpha_R[j], Kbar[i]>;  dR = d alpha_L Kbar^T (+ dY Vbar^T)
+        gemm<1>({as_is(aR)}, {transposed(Kb)}, BB, BB, DB, wave, lane, to_lds(Rm));
+        if constexpr (LAST) {
+            gemm<2>({as_is(dA), as_is(dYt)}, {transposed(Kb), transposed(Vb)}, BB, BB, DB, wave, lane, to_lds(dR));
+        } else {
+            gemm<1>({as_is(dA)}, {transposed(Kb)}, BB, BB, DB, wave, lane, to_lds(dR));
+        }
+        __syncthreads();
+        // per row j (one wave, lane i): R, then dZ scaled by s / c_R[j] in place of dR
+        for (int jj = wave; jj < BB; jj += kWaves) {
+            const int i = lane;
+            if (jj >= b) {
+                if (i < BB) Rm[jj * kLd + i] = dR[jj * kLd + i] = 0.f;
+                continue;
+            }
+            const float sc = dm.s / cR[jj];
+            const bool live = i < kv;
+            const float z = live ? sc * Rm[jj * kLd + i] : -INFINITY;
+            const float mx = wave_max(z);
+            const float e = live ? __expf(z - mx) : 0.f;
+            const float sum = wave_sum(e);
+            const float r = e / sum;
+            const float logr = live ? z - mx - __logf(sum) : 0.f;
+            const float dr = live ? dR[jj * kLd + i] + dcL[jj] * (logr + 1.f) : 0.f;
+            const float dot = wave_sum(r * dr);
+            const float dz = r * (dr - dot);
+            const float dzlog = wave_sum(dz * logr);
+            if (i < BB) {
+                Rm[jj * kLd + i] = r;
+                dR[jj * kLd + i] = dz * sc;
+            }
+            if (!FIRST && i == 0) p.dcR[coff + row0 + jj] = -dzlog / cR[jj];
+        }
+        __syncthreads();
+
+        // d alpha_R[j] = sum_i dZs[j][i] Kbar[i]: to the workspace, or at step 1 into dq
+        if constexpr (FIRST) {
+            const float *dQ = p.dQ + toff + row0 * d;
+            T *dq = p.dq + toff + row0 * d;
+            gemm<1>({as_is(dR)}, {as_is(Kb)}, BB, DB, BB, wave, lane, [&](int jj, int e, float v) {
+                if (jj < kv && e < d) dq[(int64_t)jj * d + e] = static_cast<T>(dQ[(int64_t)jj * d + e] + v);
+            });
+        } else {
+            float *daR = p.daR + soff + row0 * kD;
+            gemm<1>({as_is(dR)}, {as_is(Kb)}, BB, DB, BB, wave, lane, [&](int jj, int e, float v) {
+                if (jj < b && e < d) daR[(int64_t)jj * kD + e] = v;
+            });
+        }
+        // dKbar[i] += sum_j R[j][i] d alpha_L[j] + sum_j dZs[j][i] alpha_R[j]
+        {
+            float *dK = p.dK + toff + row0 * d;
+            T *dk = p.dk + toff + row0 * d;
+            gemm<2>({transposed(Rm), transposed(dR)}, {as_is(dA), as_is(aR)}, BB, DB, BB, wave, lane,
+                    [&](int i, int e, float v) {
+                        if (i < kv && e < d) {
+                            const int64_t o = (int64_t)i * d + e;
+                            const float acc = LAST ? v : v + dK[o];
+                            if constexpr (FIRST) {
+                                dk[o] = static_cast<T>(acc);
+                            } else {
+                                dK[o] = acc;
+                            }
+                        }
+                    });
+        }
+        // dVbar[i] = sum_j R[j][i] dY[j]
+        if constexpr (LAST) {
+            T *dv = p.dv + toff + row0 * d;
+            gemm<1>({transposed(Rm)}, {as_is(dYt)}, BB, DB, BB, wave, lane, [&](int i, int e, float v) {
+                if (i < kv && e < d) dv[(int64_t)i * d + e] = static_cast<T>(v);
+            });
+        }
+    }
+};
+
+template <typename T, int S, bool LAST>
+__global__ __launch_bounds__(kThreads) void l_bwd(BwdBufs<T> p, BwdDims dm)
+{
+    __shared__ __attribute__((aligned(16))) float lds[LBwd<T, S, LAST>::LDS_FLOATS];
+    LBwd<T, S, LAST>::run(p, dm, lds);
+}
+
+template <typename T, int S, bool FIRST, bool LAST>
+__global__ __launch_bounds__(kThreads) void r_bwd(BwdBufs<T> p, BwdDims dm)
+{
+    __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, FIRST, LAST>::LDS_FLOATS];
+    RBwd<T, S, FIRST, LAST>::run(p, dm, lds);
+}
+
+}  // namespace bwd
+}  // namespace ma

@@ -10,4 +10,8 @@ template <> int run_exact<__bf16>(Launcher &L, const CallBufs &B, float *lse, in
 {
     return run_exact_impl<__bf16>(L, B, lse, BH, n, d);
 }
+template <> int run_bwd<__bf16>(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+{
+    return run_bwd_impl<__bf16>(L, B, c);
+}
 }  // namespace ma_host

@@ -10,4 +10,8 @@ template <> int run_exact<_Float16>(Launcher &L, const CallBufs &B, float *lse, 
 {
     return run_exact_impl<_Float16>(L, B, lse, BH, n, d);
 }
+template <> int run_bwd<_Float16>(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+{
+    return run_bwd_impl<_Float16>(L, B, c);
+}
 }  // namespace ma_host

@@ -10,4 +10,8 @@ template <> int run_exact<float>(Launcher &L, const CallBufs &B, float *lse, int
 {
     return run_exact_impl<float>(L, B, lse, BH, n, d);
 }
+template <> int run_bwd<float>(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+{
+    return run_bwd_impl<float>(L, B, c);
+}
 }  // namespace ma_host

@@ -16,7 +16,7 @@ int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 inline int pad16(int64_t x) { return (int)((x + 15) / 16 * 16); }
 
 // Kernel kinds reported by the timing interface.
-enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4, kObjSum = 5, kExact = 6 };
+enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4, kObjSum = 5, kExact = 6, kBwdL = 7, kBwdR = 8 };
 
 // Per-launch HIP events around every kernel when timing is enabled.
 constexpr int kMaxLaunches = 2 * 64 + 2;
@@ -93,6 +93,23 @@ inline bool uses_fused(int path, int32_t dtype, int64_t d, int64_t m, int64_t b)
 
 // Enqueue the whole forward pass for one element type (defined per dtype).
 template <typename T> int run_call(Launcher &L, const CallBufs &B, const CallDims &c, int path);
+
+// Buffers of one gradient call: the caller's tensors, the states of every
+// step of the recomputed forward pass (alpha_R and c_R of steps 2..T, alpha_L
+// and c_L of steps 1..T, `st` bytes resp. `cst` floats apart, and Y), and the
+// fp32 gradients of the states and accumulators of dQ, dK.
+struct BwdCallBufs {
+    const void *q, *k, *v, *dout;
+    void *dq, *dk, *dv;
+    char *aR, *aL;
+    void *Y;
+    float *cR, *cL;
+    size_t st, cst;
+    float *dQ, *dK, *daL, *dcL, *dY, *daR, *dcR;
+};
+
+// Enqueue the gradient (forward recompute, then the reverse sweep) for one element type.
+template <typename T> int run_bwd(Launcher &L, const BwdCallBufs &B, const CallDims &c);
 
 // Enqueue exact softmax attention (with the row logsumexps when lse != null).
 template <typename T> int run_exact(Launcher &L, const CallBufs &B, float *lse, int64_t BH, int n, int d);

@@ -92,6 +92,47 @@ bool overlaps(const void *a, size_t na, const void *b, size_t nb)
     return x < y + nb && y < x + na;
 }
 
+// The current device and its compute-unit count (queried once per device).
+int current_device(int &dev, int &num_cus)
+{
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
+    std::lock_guard<std::mutex> lock(g_dev_mutex);
+    Device &D = g_dev[dev];
+    if (D.num_cus == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+            return fail(MA_EHIP, "querying the compute unit count failed");
+        D.num_cus = n;
+    }
+    num_cus = D.num_cus;
+    return MA_OK;
+}
+
+// The workspace of device `dev`, grown with hipMalloc to at least `need` bytes
+// (after a device synchronisation, since earlier calls may still use it).
+int acquire_workspace(int dev, size_t need, char **base)
+{
+    std::lock_guard<std::mutex> lock(g_dev_mutex);
+    Device &D = g_dev[dev];
+    if (D.ws_bytes < need) {
+        if (D.ws) {
+            if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
+            (void)hipFree(D.ws);
+            D.ws = nullptr;
+            D.ws_bytes = 0;
+        }
+        void *p = nullptr;
+        if (hipMalloc(&p, need) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(MA_ENOMEM, "hipMalloc of %zu workspace bytes failed", need);
+        }
+        D.ws = p;
+        D.ws_bytes = need;
+    }
+    *base = (char *)D.ws;
+    return MA_OK;
+}
+
 // The forward pass; with obj != nullptr also the objective per (head, step).
 int forward(const void *q, const void *k, const void *v, void *out, float *obj, int64_t B, int64_t H, int64_t N,
             int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
@@ -118,43 +159,14 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     const size_t st = state_bytes(BH, m * b, d, dtype);
     const size_t cs = align_up((size_t)BH * m * b * sizeof(float));
     CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, obj};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
-    int num_cus = 0;
-    {
-        std::lock_guard<std::mutex> lock(g_dev_mutex);
-        Device &D = g_dev[dev];
-        if (D.num_cus == 0) {
-            int n = 0;
-            if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
-                return fail(MA_EHIP, "querying the compute unit count failed");
-            D.num_cus = n;
-        }
-        num_cus = D.num_cus;
-    }
+    int dev = 0, num_cus = 0;
+    if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
     const bool states = !uses_fused(path, dtype, d, m, b);  // the fused kernel keeps its states in LDS
     const size_t obj_part_bytes = obj ? align_up((size_t)BH * T * b * sizeof(float)) : 0;
     if (states || obj) {
         const size_t state_ws = states ? workspace_bytes(BH, m * b, d, dtype) : 0;
-        const size_t need = state_ws + obj_part_bytes;
-        std::lock_guard<std::mutex> lock(g_dev_mutex);
-        Device &D = g_dev[dev];
-        if (D.ws_bytes < need) {
-            if (D.ws) {
-                if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
-                (void)hipFree(D.ws);
-                D.ws = nullptr;
-                D.ws_bytes = 0;
-            }
-            void *p = nullptr;
-            if (hipMalloc(&p, need) != hipSuccess) {
-                (void)hipGetLastError();
-                return fail(MA_ENOMEM, "hipMalloc of %zu workspace bytes failed", need);
-            }
-            D.ws = p;
-            D.ws_bytes = need;
-        }
-        char *base = (char *)D.ws;
+        char *base = nullptr;
+        if ((rc = acquire_workspace(dev, state_ws + obj_part_bytes, &base)) != MA_OK) return rc;
         if (states) {
             bufs.aR = base;
             bufs.aL = base + st;
@@ -174,6 +186,104 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     case MA_F32: rc = run_call<float>(L, bufs, dims, path); break;
     case MA_BF16: rc = run_call<__bf16>(L, bufs, dims, path); break;
     default: rc = run_call<_Float16>(L, bufs, dims, path); break;
+    }
+    if (L.timed) {
+        g_timing.nlaunch = L.n;
+        g_timing.ready = (rc == MA_OK && L.n > 0);
+    }
+    if (rc != MA_OK) return rc;
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(MA_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
+    return MA_OK;
+}
+
+// ---- gradient ----
+
+// The gradient kernels hold one unit's matrices in 64-row fp32 LDS tiles.
+int check_bwd_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype)
+{
+    const int rc = check_shape(N, d, m, b, T, dtype);
+    if (rc != MA_OK) return rc;
+    if (m > 64 || b > 64 || d > 64)
+        return fail(MA_EUNSUPPORTED, "the gradient needs m, b and d <= 64 (got m=%lld, b=%lld, d=%lld)", (long long)m,
+                    (long long)b, (long long)d);
+    if (T > 32) return fail(MA_EUNSUPPORTED, "the gradient supports T <= 32 (got %d)", T);
+    return MA_OK;
+}
+
+// Workspace of one gradient call, in this order: alpha_R of steps 2..T, alpha_L
+// of steps 1..T and Y (element type, tile width 64); c_R of steps 2..T and c_L
+// of steps 1..T (fp32); the fp32 accumulators of dQ and dK ([B*H][N][d]); the
+// fp32 gradients d alpha_L, dY, d alpha_R (width 64) and d c_L, d c_R.
+struct BwdLayout {
+    size_t st, cs, acc, sg;
+    int32_t T;
+    size_t states() const { return (size_t)(2 * T) * st + (size_t)(2 * T - 1) * cs; }
+    size_t total() const { return states() + 2 * acc + 3 * sg + 2 * cs; }
+};
+
+BwdLayout bwd_layout(int64_t BH, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype)
+{
+    const int64_t Np = m * b;
+    return BwdLayout{state_bytes(BH, Np, d, dtype), align_up((size_t)BH * Np * sizeof(float)),
+                     align_up((size_t)BH * N * d * sizeof(float)), align_up((size_t)BH * Np * 64 * sizeof(float)),
+                     T};
+}
+
+int backward(const void *q, const void *k, const void *v, const void *dout, void *dq, void *dk, void *dv, int64_t B,
+             int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
+{
+    g_err[0] = '\0';
+    if (!q || !k || !v || !dout || !dq || !dk || !dv) return fail(MA_EINVAL, "null tensor pointer");
+    if (B < 1 || H < 1) return fail(MA_EINVAL, "B and H must be >= 1");
+    int rc = check_bwd_shape(N, d, m, b, T, dtype);
+    if (rc != MA_OK) return rc;
+    if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)dout | (uintptr_t)dq | (uintptr_t)dk |
+         (uintptr_t)dv) & 15u)
+        return fail(MA_EINVAL, "all tensors must be 16-byte aligned");
+    const int64_t BH = B * H;
+    if (BH * (int64_t)(m > b ? m : b) > (int64_t)0x7fffffff) return fail(MA_EUNSUPPORTED, "too many heads for one grid");
+    const size_t tb = (size_t)BH * N * d * elem_bytes(dtype);
+    const void *ins[4] = {q, k, v, dout};
+    void *outs[3] = {dq, dk, dv};
+    for (int o = 0; o < 3; ++o) {
+        for (int i = 0; i < 4; ++i)
+            if (overlaps(outs[o], tb, ins[i], tb)) return fail(MA_EINVAL, "dq, dk, dv must not overlap q, k, v or dout");
+        for (int o2 = o + 1; o2 < 3; ++o2)
+            if (overlaps(outs[o], tb, outs[o2], tb)) return fail(MA_EINVAL, "dq, dk and dv must not overlap");
+    }
+    int dev = 0, num_cus = 0;
+    if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
+    const BwdLayout lay = bwd_layout(BH, N, d, m, b, T, dtype);
+    char *base = nullptr;
+    if ((rc = acquire_workspace(dev, lay.total(), &base)) != MA_OK) return rc;
+    BwdCallBufs bufs{};
+    bufs.q = q, bufs.k = k, bufs.v = v, bufs.dout = dout, bufs.dq = dq, bufs.dk = dk, bufs.dv = dv;
+    char *p = base;
+    bufs.st = lay.st;
+    bufs.cst = lay.cs / sizeof(float);
+    bufs.aR = p, p += (size_t)(T - 1) * lay.st;
+    bufs.aL = p, p += (size_t)T * lay.st;
+    bufs.Y = p, p += lay.st;
+    bufs.cR = (float *)p, p += (size_t)(T - 1) * lay.cs;
+    bufs.cL = (float *)p, p += (size_t)T * lay.cs;
+    bufs.dQ = (float *)p, p += lay.acc;
+    bufs.dK = (float *)p, p += lay.acc;
+    bufs.daL = (float *)p, p += lay.sg;
+    bufs.dY = (float *)p, p += lay.sg;
+    bufs.daR = (float *)p, p += lay.sg;
+    bufs.dcL = (float *)p, p += lay.cs;
+    bufs.dcR = (float *)p;
+    CallDims dims{BH, (int)m, (int)b, (int)N, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
+
+    std::unique_lock<std::mutex> tlock(g_timing_mutex);
+    Launcher L{(hipStream_t)stream, g_timing.enabled};
+    if (!L.timed) tlock.unlock();
+    (void)hipGetLastError();
+    switch (dtype) {
+    case MA_F32: rc = run_bwd<float>(L, bufs, dims); break;
+    case MA_BF16: rc = run_bwd<__bf16>(L, bufs, dims); break;
+    default: rc = run_bwd<_Float16>(L, bufs, dims); break;
     }
     if (L.timed) {
         g_timing.nlaunch = L.n;
@@ -328,6 +438,26 @@ int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void
     if (!obj) return fail(MA_EINVAL, "null objective pointer");
     if ((uintptr_t)obj & 3u) return fail(MA_EINVAL, "obj must be 4-byte aligned");
     return forward(q, k, v, out, obj, B, H, N, d, m, b, T, dtype, stream);
+}
+
+int monarch_attn_bwd(const void *q, const void *k, const void *v, const void *dout, void *dq, void *dk, void *dv,
+                     int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
+                     void *stream)
+{
+    return backward(q, k, v, dout, dq, dk, dv, B, H, N, d, m, b, T, dtype, stream);
+}
+
+int monarch_attn_bwd_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype)
+{
+    g_err[0] = '\0';
+    return check_bwd_shape(N, d, m, b, T, dtype);
+}
+
+size_t monarch_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
+                                        int32_t dtype)
+{
+    if (B < 1 || H < 1 || check_bwd_shape(N, d, m, b, T, dtype) != MA_OK) return 0;
+    return bwd_layout(B * H, N, d, m, b, T, dtype).total();
 }
 
 }  // extern "C"

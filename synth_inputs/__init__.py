@@ -37,6 +37,7 @@ __all__ = [
     "round_to_dtype",
     "bf16_round",
     "DTYPES",
+    "random_cotangent",
 ]
 
 DTYPES = ("f32", "bf16", "f16")
@@ -229,3 +230,9 @@ def random_qkv(B, H, N, d, dtype="f32", seed=0, scale=1.0):
     k = round_to_dtype(np.float32(scale) * _normal(seed, tag + "/k", (B, H, N, d)), dtype)
     v = round_to_dtype(_normal(seed, tag + "/v", (B, H, N, d)), dtype)
     return q, k, v
+
+
+def random_cotangent(shape, dtype="f32", seed=0, tag="dout"):
+    """An iid N(0, 1) tensor of the given shape rounded to the run dtype: the
+    incoming gradient dO of a gradient test or benchmark."""
+    return round_to_dtype(_normal(seed, f"cotangent/{tag}/{'x'.join(map(str, shape))}", tuple(shape)), dtype)

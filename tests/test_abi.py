@@ -150,3 +150,67 @@ def test_objective_rejects_null_obj():
     rc = ma.LIB.monarch_attn_fwd_objective(FAKE, FAKE, FAKE, 2 * FAKE, None, 1, 1, 256, 64, 16, 16, 1, 1, None)
     assert rc == ma.MA_EINVAL
     assert "objective" in ma.monarch_attn_last_error()
+
+
+# ---- the gradient entry point ----
+
+@pytest.mark.parametrize(
+    "args,code",
+    [
+        # (q, k, v, dout, dq, dk, dv, B, H, N, d, m, b, T, dtype)
+        ((FAKE, FAKE, FAKE, FAKE, 0, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),           # null dq
+        ((FAKE, FAKE, FAKE, 0, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),       # null dout
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 0, 256, 64, 16, 16, 1, 1), 1),    # H = 0
+        ((FAKE, FAKE, FAKE, FAKE, FAKE + 64, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),   # dq overlaps q
+        ((FAKE, FAKE, FAKE, 5 * FAKE, 2 * FAKE, 3 * FAKE, 5 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),  # dv overlaps dout
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 2 * FAKE + 64, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),  # dk overlaps dq
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE + 8, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),  # misaligned dq
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 257, 64, 16, 16, 1, 1), 1),    # N > m b
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 8192, 64, 128, 64, 1, 1), 2),  # m > 64
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 8192, 64, 64, 128, 1, 1), 2),  # b > 64
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 72, 16, 16, 1, 1), 2),    # d > 64
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 33, 1), 2),   # T > 32
+    ],
+)
+def test_bwd_invalid_arguments_rejected_before_any_hip_call(args, code):
+    import paper_2505_18698_amd as ma
+
+    rc = ma.LIB.monarch_attn_bwd(*args, None)
+    assert rc == code, ma.monarch_attn_last_error()
+    assert ma.monarch_attn_last_error() != ""
+
+
+@pytest.mark.parametrize(
+    "shape,ok",
+    [
+        ((256, 64, 16, 16, 1, 1), True),
+        ((196, 64, 14, 14, 3, 1), True),
+        ((197, 64, 15, 14, 2, 2), True),
+        ((4096, 64, 64, 64, 2, 0), True),
+        ((7, 8, 7, 1, 1, 1), True),
+        ((1024, 64, 32, 32, 32, 1), True),
+        ((1024, 64, 32, 32, 33, 1), False),
+        ((16384, 64, 128, 128, 2, 1), False),
+        ((256, 96, 16, 16, 2, 1), False),
+        ((196, 64, 15, 14, 2, 1), False),
+    ],
+)
+def test_bwd_supported_shapes(shape, ok):
+    import paper_2505_18698_amd as ma
+
+    assert (ma.monarch_attn_bwd_check(*shape) == 0) == ok
+
+
+def test_bwd_workspace_bytes_formula():
+    import paper_2505_18698_amd as ma
+
+    B, H, N, d, m, b, T = 2, 3, 197, 64, 15, 14, 3
+    Np, BH = m * b, B * H
+    st, cs = _align(BH * Np * 64 * 2), _align(BH * Np * 4)
+    acc, sg = _align(BH * N * d * 4), _align(BH * Np * 64 * 4)
+    want = 2 * T * st + (2 * T - 1) * cs + 2 * acc + 3 * sg + 2 * cs
+    assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_BF16) == want
+    # fp32 states are twice as wide; unsupported shapes give 0
+    st32 = _align(BH * Np * 64 * 4)
+    assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_F32) == want + 2 * T * (st32 - st)
+    assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 16384, 64, 128, 128, 2, ma.MA_BF16) == 0

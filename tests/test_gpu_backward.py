@@ -1,0 +1,194 @@
+"""GPU parity of the gradient (monarch_attn_bwd, through the C ABI) against
+the fp64 oracle of oracle/backward.py (torch autograd through the unrolled
+T-step forward pass, itself pinned by finite differences and the textbook
+attention gradient) on the same seeded, dtype-rounded inputs.
+
+Bar: relative Frobenius error of each of dQ, dK, dV over the compared heads
+<= 2e-5 for fp32 and <= 3e-2 for bf16 / fp16.  The fp32 bound allows for the
+fp32 forward recompute and the fp32 reverse sweep (products of length <= 64,
+exp / log at a few ulp), amplified by the softmax pull-backs; the 16-bit
+bound for the states of the recomputed forward pass held in the element
+type (unit roundoff 2^-9 for bf16) and dq, dk, dv rounded to it.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import oracle.backward as ob
+import synth_inputs as si
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 2e-5, "bf16": 3e-2, "f16": 3e-2}
+
+
+@pytest.fixture(scope="module")
+def ma():
+    import torch
+
+    assert torch.cuda.is_available(), "no GPU visible"
+    import paper_2505_18698_amd as lib
+
+    return lib
+
+
+def _td(dtype):
+    import torch
+
+    return {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+
+
+def gpu_grads(ma, q, k, v, dout, m, b, T, dtype):
+    """(dq, dk, dv) from the HIP path, float64 numpy; outputs start as NaN so
+    that an unwritten element cannot pass."""
+    import torch
+
+    td = _td(dtype)
+    tq, tk, tv, tg = (torch.from_numpy(x).to(td).cuda() for x in (q, k, v, dout))
+    outs = [torch.full_like(tq, float("nan")) for _ in range(3)]
+    ma.monarch_attn_bwd(tq, tk, tv, tg, *outs, m, b, T)
+    torch.cuda.synchronize()
+    return [o.double().cpu().numpy() for o in outs]
+
+
+def oracle_grads(q, k, v, dout, m, b, T, heads):
+    res = [np.zeros(q.shape) for _ in range(3)]
+    for i, h in heads:
+        for r, g in zip(res, ob.autograd_grads(q[i, h], k[i, h], v[i, h], dout[i, h], m, b, T)):
+            r[i, h] = g
+    return res
+
+
+def check(got, ref, heads, dtype, label):
+    errs = []
+    for name, x, r in zip(("dq", "dk", "dv"), got, ref):
+        xs = np.stack([x[i, h] for i, h in heads])
+        rs = np.stack([r[i, h] for i, h in heads])
+        assert np.isfinite(x).all(), (label, name, "non-finite or unwritten elements")
+        errs.append(oracle.rel_frobenius(xs, rs))
+    print(f"{label} rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
+    for name, e in zip(("dq", "dk", "dv"), errs):
+        assert e <= TOL[dtype], (label, name, e)
+    return errs
+
+
+def run_case(ma, B, H, n, m, b, d, T, dtype, seed=0, heads=None, scale=1.5):
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=seed, scale=scale)
+    dout = si.random_cotangent((B, H, n, d), dtype, seed=seed)
+    heads = heads or [(i, h) for i in range(B) for h in range(H)]
+    got = gpu_grads(ma, q, k, v, dout, m, b, T, dtype)
+    ref = oracle_grads(q, k, v, dout, m, b, T, heads)
+    return check(got, ref, heads, dtype, f"{dtype} B{B} H{H} n{n} m{m} b{b} d{d} T{T}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize(
+    "B,H,m,b,d,T",
+    [
+        (1, 1, 16, 16, 64, 1),
+        (2, 2, 16, 16, 64, 2),
+        (1, 2, 5, 7, 64, 2),      # ragged tiles in both half-steps
+        (1, 1, 1, 16, 64, 2),     # m = 1
+        (1, 1, 16, 1, 64, 2),     # b = 1
+        (1, 2, 24, 40, 32, 3),    # m != b, d = 32
+        (1, 1, 14, 14, 64, 3),    # ViT-B/16 blocks
+        (1, 1, 33, 17, 64, 4),
+        (1, 1, 64, 64, 64, 2),    # the largest tiles
+        (1, 1, 48, 64, 16, 1),
+    ],
+)
+def test_random_shapes(ma, dtype, B, H, m, b, d, T):
+    run_case(ma, B, H, m * b, m, b, d, T, dtype, seed=m * 100 + b)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize(
+    "n,m,b,T",
+    [
+        (197, 15, 14, 2),   # ViT-B/16 with its class token
+        (100, 7, 16, 1),
+        (100, 7, 16, 3),
+        (5, 1, 16, 2),      # one short block
+        (33, 3, 16, 2),     # last block of one key
+        (1000, 63, 16, 2),
+    ],
+)
+def test_padded_lengths(ma, dtype, n, m, b, T):
+    run_case(ma, 1, 2, n, m, b, 64, T, dtype, seed=n)
+
+
+@pytest.mark.parametrize("T", [1, 3])
+@pytest.mark.parametrize("n", [16, 40, 64])
+def test_single_block_is_softmax_attention(ma, n, T):
+    """m = 1: M is the exact softmax matrix for every T, so the gradient is the
+    textbook attention gradient (no Monarch arithmetic on the reference side)."""
+    d = 32
+    q, k, v = si.random_qkv(1, 2, n, d, "f32", seed=n, scale=1.5)
+    dout = si.random_cotangent((1, 2, n, d), "f32", seed=n)
+    got = gpu_grads(ma, q, k, v, dout, 1, n, T, "f32")
+    ref = [np.zeros(q.shape) for _ in range(3)]
+    for h in range(2):
+        for r, g in zip(ref, ob.attention_grads(q[0, h], k[0, h], v[0, h], dout[0, h])):
+            r[0, h] = g
+    check(got, ref, [(0, 0), (0, 1)], "f32", f"softmax n{n} T{T}")
+
+
+def test_deterministic(ma):
+    import torch
+
+    q, k, v = si.random_qkv(2, 3, 197, 64, "bf16", seed=3)
+    dout = si.random_cotangent((2, 3, 197, 64), "bf16", seed=3)
+    a = gpu_grads(ma, q, k, v, dout, 15, 14, 3, "bf16")
+    b = gpu_grads(ma, q, k, v, dout, 15, 14, 3, "bf16")
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+    del torch
+
+
+def test_directional_derivative_matches_forward(ma):
+    """<grad, u> against a central difference of <O, dO> computed by the HIP
+    forward pass itself (fp32): ties the gradient to the forward kernels."""
+    import torch
+
+    B, H, m, b, d, T = 1, 2, 8, 8, 32, 2
+    n = m * b
+    q, k, v = si.random_qkv(B, H, n, d, "f32", seed=11, scale=1.0)
+    dout = si.random_cotangent((B, H, n, d), "f32", seed=11)
+    u = [si.random_cotangent((B, H, n, d), "f32", seed=12, tag=t) for t in ("uq", "uk", "uv")]
+    g = gpu_grads(ma, q, k, v, dout, m, b, T, "f32")
+    lin = sum(float(np.sum(gi * ui)) for gi, ui in zip(g, u))
+
+    def f(eps):
+        xs = [torch.from_numpy(x + eps * ui).cuda() for x, ui in zip((q, k, v), u)]
+        out = torch.empty_like(xs[0])
+        ma.monarch_attn_fwd(*xs, out, m, b, T)
+        torch.cuda.synchronize()
+        return float(np.sum(out.double().cpu().numpy() * dout))
+
+    eps = 1e-2
+    fd = (f(eps) - f(-eps)) / (2 * eps)
+    print(f"directional derivative: grad {lin:.6e} central difference {fd:.6e}", flush=True)
+    assert abs(fd - lin) <= 2e-3 * max(1.0, abs(lin))
+
+
+@pytest.mark.parametrize("T", [1, 2])
+def test_speed_n4096_sampled_heads(ma, T):
+    """The N = 4096 speed shape (16 heads, m = b = 64) at full size, oracle on 3 heads."""
+    w = si.WORKLOADS["speed_n4096"].with_(T=T)
+    q, k, v, _ = si.make_qkv(w)
+    dout = si.random_cotangent((w.B, w.H, w.N, w.d), w.dtype, seed=1)
+    heads = [(0, 0), (0, 7), (0, 15)]
+    got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
+    ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
+    check(got, ref, heads, w.dtype, f"{w.name} T{T}")
+
+
+def test_vit_workload_sampled_heads(ma):
+    """ViT-B/16 (32 images x 12 heads, N = 197 post-padded to 15 x 14), oracle on 4 heads."""
+    w = si.WORKLOADS["vit_b16_n197"]
+    q, k, v, _ = si.make_qkv(w)
+    dout = si.random_cotangent((w.B, w.H, w.N, w.d), w.dtype, seed=2)
+    heads = [(0, 0), (5, 3), (17, 11), (31, 6)]
+    got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
+    ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
+    check(got, ref, heads, w.dtype, w.name)
