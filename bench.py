@@ -20,6 +20,12 @@ last-level cache cannot serve them from one step to the next.
 cpu_baseline: the fp64 C oracle, as it stands, on this host's cores, on the
 same workload (repeated whole forward passes, about 10-30 s in total).
 
+backward: monarch_attn_bwd (the gradient: forward recompute keeping every
+step's states, then the reverse sweep) timed the same way on the 4K speed
+point and ViT-B/16 with its class token, with its per-kernel durations and
+the roofline of its dominant gradient kernel.  Reported beside the headline,
+not in it.
+
 quality: the error of O against exact softmax attention and the gap of the
 variational objective to its exact-softmax maximum, for T = 1, 2, 3, on the
 structured workloads (ViT- and RoBERTa-shaped, and 16K tokens with
@@ -167,6 +173,117 @@ def measure(ma, torch, w, steps, warmup):
     return ms, kernels, meta, nsets
 
 
+def bwd_kernel_work(w, kind, t):
+    """Algorithmic bytes and flops of one gradient launch (all heads) at step t.
+
+    l_bwd (per class j, m x m x d products: scores, dL, dY or L d alpha_R',
+    dQ, d alpha_L) reads Q, alpha_L and Y + dO (t = T) or d alpha_R' + d c_R'
+    (fp32), and c_L; writes dQ (fp32; read and written when t < T),
+    d alpha_L, d c_L and dY (t = T).  r_bwd (per block k, b x b x d products:
+    scores, dR (+ dY V^T at t = T), d alpha_R, two for dK, dV at t = T) reads
+    K, alpha_R (Q at t = 1), c_R, d alpha_L, d c_L, and V + dY at t = T;
+    writes d alpha_R + d c_R (t > 1), dK (fp32, read too unless t = T), and
+    at t = 1 reads dQ and writes dq, dk in the element type, at t = T dv.
+    Only the d real columns count; the states are stored 64 wide."""
+    s = 2 if w.dtype in ("bf16", "f16") else 4
+    BH, Np, d, m, b, T = w.B * w.H, w.m * w.b, w.d, w.m, w.b, w.T
+    rows = BH * Np
+    if kind == "l_bwd":
+        macs = 5 * rows * m * d
+        if t == T:
+            nbytes = rows * d * (4 * s + 12) + rows * 8
+        else:
+            nbytes = rows * d * (2 * s + 16) + rows * 12
+    else:
+        macs = (7 if t == T else 5) * rows * b * d
+        nbytes = rows * (2 * d * s + d * 4 + 4)        # K, alpha_R (Q at t = 1), d alpha_L, d c_L
+        if t > 1:
+            nbytes += rows * (4 + d * 4 + 4)           # c_R in; d alpha_R, d c_R out
+        if t == T:
+            nbytes += rows * d * (s + 4 + s)           # V, dY in; dv out
+        if t == 1:
+            nbytes += rows * d * (4 + s)               # dQ in, dq out
+            nbytes += rows * d * ((4 if T > 1 else 0) + s)   # dK in (when accumulated), dk out
+        else:
+            nbytes += rows * d * 4 * (1 if t == T else 2)    # dK accumulator written (and read when t < T)
+    return nbytes, 2 * macs
+
+
+def measure_backward(ma, torch, w, steps, warmup):
+    """Time monarch_attn_bwd: K calls back to back, then K with per-launch events."""
+    import synth_inputs as si
+
+    q, k, v, _ = si.make_qkv(w)
+    dout = si.random_cotangent((w.B, w.H, w.N, w.d), w.dtype, seed=1)
+    td = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[w.dtype]
+    base = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v, dout)]
+    del q, k, v, dout
+    set_bytes = 7 * base[0].numel() * base[0].element_size()
+    nsets = max(1, min(8, math.ceil(ROTATE_BYTES / set_bytes)))
+    sets = [[x.clone() for x in base] + [torch.empty_like(base[0]) for _ in range(3)] for _ in range(nsets)]
+    del base
+
+    def step(i):
+        ma.monarch_attn_bwd(*sets[i % nsets], w.m, w.b, w.T)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        step(i)
+    end.record()
+    end.synchronize()
+    ms = start.elapsed_time(end) / steps
+    log(f"[bench] backward {w.name} T{w.T}: {ms * 1e3:.1f} us per call over {steps} calls")
+
+    kinds, sums = None, None
+    ma.monarch_attn_timing_enable(True)
+    try:
+        for i in range(steps):
+            step(i)
+            recs = ma.monarch_attn_timing_read()
+            if kinds is None:
+                kinds = [kind for kind, _ in recs]
+                sums = [0.0] * len(kinds)
+            assert [kind for kind, _ in recs] == kinds, (recs, kinds)
+            for j, (_, t) in enumerate(recs):
+                sums[j] += t
+    finally:
+        ma.monarch_attn_timing_enable(False)
+    torch.cuda.synchronize()
+    del sets
+    torch.cuda.empty_cache()
+
+    # the recompute's launches follow the forward's plan (without the apply);
+    # the sweep runs t = T .. 1 as (l_bwd, r_bwd) pairs
+    fwd_plan = [p for p in launch_plan(w) if p[0] != "monarch_apply"]
+    nrec = len(fwd_plan)
+    assert kinds[:nrec] == [p[0] for p in fwd_plan], (kinds, fwd_plan)
+    kernels = []
+    for j, kind in enumerate(kinds):
+        avg_ms = sums[j] / steps
+        if j < nrec:
+            nbytes, nflops = fwd_plan[j][1], fwd_plan[j][2]
+            step_t = None
+        else:
+            step_t = w.T - (j - nrec) // 2
+            nbytes, nflops = bwd_kernel_work(w, kind, step_t)
+        kernels.append({"kernel": kind, "step": step_t, "avg_us": round(avg_ms * 1e3, 3), "alg_bytes": nbytes,
+                        "alg_flops": nflops, "GB_s": round(nbytes / (avg_ms * 1e-3) / 1e9, 1),
+                        "TFLOP_s": round(nflops / (avg_ms * 1e-3) / 1e12, 2)})
+    sweep = kernels[nrec:]
+    dom = max(sweep, key=lambda x: x["avg_us"])
+    # the sweep's products are fp32 MFMA whatever the element type
+    roof = roofline_of(dom, "f32")
+    roof["traffic"] = None
+    return {"config": w.describe(), "value": round(w.B * w.H * w.N / (ms * 1e-3), 1), "unit": UNIT,
+            "ms_per_call": round(ms, 6), "recompute_us": round(sum(x["avg_us"] for x in kernels[:nrec]), 3),
+            "sweep_us": round(sum(x["avg_us"] for x in sweep), 3), "roofline": roof, "kernels": kernels,
+            "rotating_input_sets": nsets}
+
+
 QUALITY_WORKLOADS = ("vit_b16_n196", "roberta_n1024", "lm_n16384")
 
 
@@ -307,6 +424,8 @@ def main():
     ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
     ap.add_argument("--also", default="speed_n4096,vit_b16_n196,vit_b16_n197",
                     help="comma-separated extra workloads ('' for none)")
+    ap.add_argument("--backward", default="speed_n4096,vit_b16_n197",
+                    help="comma-separated workloads for the gradient timing ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-quality", action="store_true",
                     help="skip the approximation-quality figures (error against exact attention, objective gap)")
@@ -380,6 +499,8 @@ def main():
                      "ms_per_step": round(ms2, 6), "roofline": roofline_of(dom2, w2.dtype, w2.name),
                      "call_roofline": call_roofline(w2, ms2), "kernels": kern2})
     result["also"] = also
+    result["backward"] = [measure_backward(ma, torch, si.WORKLOADS[name], args.steps, args.warmup)
+                          for name in [x for x in args.backward.split(",") if x]]
     if not args.no_quality:
         result["quality"] = [quality(ma, torch, si.WORKLOADS[name]) for name in QUALITY_WORKLOADS]
     if not args.no_cpu_baseline:
