@@ -58,63 +58,116 @@ struct BwdDims {
 
 namespace bwd {
 
-constexpr int kD = 64;    // row width of the states (the forward's tile width for d <= 64)
-constexpr int kLd = 81;   // row stride (floats) of the LDS tiles: 17 mod 64 spreads both access orders
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
+constexpr int kD = 64;   // row width of the states (the forward's tile width for d <= 64)
+constexpr int kLd = 84;  // row stride (floats) of the LDS tiles: 16-byte rows, both access orders conflict-free
+
+// Waves per workgroup for tiles of S rows: one 16 x 16 output tile of an
+// S x S product per wave at S = 64.
+template <int S> struct Waves {
+    static constexpr int value = S / 4;
+};
 
 __device__ inline int up16(int x) { return (x + 15) & ~15; }
 
+// Reductions over the 64 lanes with no LDS round trip: DPP within rows of 16
+// lanes (xor 1, xor 2, then mirrors of 8 and 16 lanes), then the permlane
+// swaps across rows.  Every lane ends with the same value.
+template <int CTRL> __device__ inline float dpp(float x)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
+}
+constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kRowHalfMirror = 0x141, kRowMirror = 0x140;
+
 __device__ inline float wave_sum(float x)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    return x;
+    x += dpp<kQuadXor1>(x);
+    x += dpp<kQuadXor2>(x);
+    x += dpp<kRowHalfMirror>(x);
+    x += dpp<kRowMirror>(x);
+    x = wave_xor_sum<16>(x);
+    return wave_xor_sum<32>(x);
 }
 
 __device__ inline float wave_max(float x)
 {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
-    return x;
+    x = fmaxf(x, dpp<kQuadXor1>(x));
+    x = fmaxf(x, dpp<kQuadXor2>(x));
+    x = fmaxf(x, dpp<kRowHalfMirror>(x));
+    x = fmaxf(x, dpp<kRowMirror>(x));
+    x = wave_xor_max<16>(x);
+    return wave_xor_max<32>(x);
 }
 
-// A matrix view of an LDS tile: element (r, c) at p[r * rs + c * cs].
-struct View {
-    const float *p;
-    int rs, cs;
-};
-__device__ inline View as_is(const float *t) { return View{t, kLd, 1}; }
-__device__ inline View transposed(const float *t) { return View{t, 1, kLd}; }
+// Operands of a product, as LDS tiles (row stride kLd):
+//   A(r, k) = TA ? A[k][r] : A[r][k],   B(k, n) = TB ? B[n][k] : B[k][n].
+// MFMA step s of a 16-long chunk k0 hands lane group g = lane/16 the index
+// k0 + 4g + s, so a lane reads four consecutive k at once: one 16-byte read
+// where k is contiguous (A as stored, B transposed), four conflict-free
+// scalar reads otherwise.
+template <bool TA, bool TB> struct Pair {
+    const float *A, *B;
 
-// out(r, c) = sum over the NOPS pairs of sum_k A(r, k) B(k, c), for r < M,
-// c < N (multiples of 16), k < K (a multiple of 4); the 16 x 16 output tiles
-// are shared out over the waves and each element is handed to st(r, c, value)
-// by exactly one lane.  A lane of v_mfma_f32_16x16x4f32 holds A(row lane%16,
-// k lane/16) and B(k lane/16, column lane%16) and receives the outputs
-// (4 (lane/16) + q, lane%16), q = 0..3.
-template <int NOPS, typename Store>
-__device__ inline void gemm(const View (&a)[NOPS], const View (&b)[NOPS], int M, int N, int K, int wave, int lane,
-                            Store &&st)
-{
-    const int g = lane >> 4, c = lane & 15, tn = N >> 4, tiles = (M >> 4) * tn;
-    for (int t = wave; t < tiles; t += kWaves) {
-        const int r0 = (t / tn) * 16, c0 = (t % tn) * 16;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    __device__ void load(float (&a)[4], float (&b)[4], int r, int n, int k) const
+    {
+        if constexpr (TA) {
 #pragma unroll
-        for (int o = 0; o < NOPS; ++o) {
-            const float *pa = a[o].p + (r0 + c) * a[o].rs + g * a[o].cs;
-            const float *pb = b[o].p + g * b[o].rs + (c0 + c) * b[o].cs;
-            const int sa = 4 * a[o].cs, sb = 4 * b[o].rs;
-            for (int k0 = 0; k0 < K; k0 += 4) {
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(*pa, *pb, acc, 0, 0, 0);
-                pa += sa;
-                pb += sb;
+            for (int s = 0; s < 4; ++s) a[s] = A[(k + s) * kLd + r];
+        } else {
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(A + r * kLd + k);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) a[s] = v[s];
+        }
+        if constexpr (TB) {
+            const f32x4 v = *reinterpret_cast<const f32x4 *>(B + n * kLd + k);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) b[s] = v[s];
+        } else {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) b[s] = B[(k + s) * kLd + n];
+        }
+    }
+
+    // acc += sum_k A(r0 + .., k) B(k, c0 + ..) over k < K (a multiple of 16),
+    // the next chunk's reads in flight during the current chunk's MFMAs.
+    __device__ void accumulate(f32x4 &acc, int r0, int c0, int K, int g, int c) const
+    {
+        float a[4], b[4], an[4], bn[4];
+        load(a, b, r0 + c, c0 + c, 4 * g);
+        for (int k0 = 0; k0 < K; k0 += 16) {
+            const int kn = min(k0 + 16, K - 16);  // a valid chunk; unused after the last
+            load(an, bn, r0 + c, c0 + c, kn + 4 * g);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                a[s] = an[s];
+                b[s] = bn[s];
             }
         }
+    }
+};
+
+// out(r, c) = sum over the pairs of A(r, :) B(:, c) for r < M, c < N
+// (multiples of 16), contraction K (a multiple of 16).  The 16 x 16 output
+// tiles are shared out over the W waves; lane (g, c) of v_mfma_f32_16x16x4f32
+// receives rows 4g + q, q = 0..3, of column c, and hands each element to
+// st(r, c, value): every element is stored by exactly one lane.
+template <int W, typename Store, typename... P>
+__device__ inline void gemm(int M, int N, int K, int wave, int lane, Store &&st, const P &...pairs)
+{
+    const int g = lane >> 4, c = lane & 15, tn = N >> 4, tiles = (M >> 4) * tn;
+    for (int t = wave; t < tiles; t += W) {
+        const int r0 = (t / tn) * 16, c0 = (t % tn) * 16;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        (pairs.accumulate(acc, r0, c0, K, g, c), ...);
 #pragma unroll
         for (int q = 0; q < 4; ++q) st(r0 + 4 * g + q, c0 + c, acc[q]);
     }
+}
+
+template <bool TA, bool TB> __device__ inline Pair<TA, TB> pair(const float *A, const float *B)
+{
+    return Pair<TA, TB>{A, B};
 }
 
 __device__ inline auto to_lds(float *t)
@@ -122,15 +175,31 @@ __device__ inline auto to_lds(float *t)
     return [t](int r, int c, float v) { t[r * kLd + c] = v; };
 }
 
-// Rows r < R and columns c < C (R, C the padded extents, C <= 64) of an LDS
-// tile from a row-major global matrix whose row r starts at src(r): element
-// (r, c) is read while r < nr and c < nc, zero elsewhere.
-template <typename E, typename Src>
+// Rows r < R and columns c < C (R, C the padded extents, C <= 64, a multiple
+// of 16) of an LDS tile from a row-major global matrix of element type E
+// whose row r starts at src(r) (16-byte aligned): element (r, c) is read while
+// r < nr and c < nc (nc a multiple of 16 bytes' worth of elements), zero
+// elsewhere.  One 16-byte global read per chunk.
+template <typename E, int NTH, typename Src>
 __device__ inline void load_tile(float *dst, int R, int C, int nr, int nc, Src src, int tid)
 {
-    for (int idx = tid; idx < R * 64; idx += kThreads) {
-        const int r = idx >> 6, c = idx & 63;
-        if (c < C) dst[r * kLd + c] = (r < nr && c < nc) ? static_cast<float>(src(r)[c]) : 0.f;
+    constexpr int V = 16 / (int)sizeof(E);
+    const int cpr = C / V;  // chunks per row
+    for (int idx = tid; idx < R * cpr; idx += NTH) {
+        const int r = idx / cpr, c = (idx - r * cpr) * V;
+        float v[V];
+        if (r < nr && c < nc) {
+            E e[V];
+            *reinterpret_cast<uint4 *>(e) = *reinterpret_cast<const uint4 *>(src(r) + c);
+#pragma unroll
+            for (int i = 0; i < V; ++i) v[i] = static_cast<float>(e[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < V; ++i) v[i] = 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < V; i += 4)
+            *reinterpret_cast<f32x4 *>(dst + r * kLd + c + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
     }
 }
 
@@ -139,6 +208,7 @@ __device__ inline void load_tile(float *dst, int R, int C, int nr, int nc, Src s
 // produced O).  S: rows of the tiles (16, 32 or 64, >= m).
 // ---------------------------------------------------------------------------------------
 template <typename T, int S, bool LAST> struct LBwd {
+    static constexpr int W = Waves<S>::value, NTH = 64 * W;
     static constexpr int LDS_FLOATS = 6 * S * kLd + 2 * S;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
@@ -154,25 +224,25 @@ template <typename T, int S, bool LAST> struct LBwd {
               *G = X + S * kLd;
         float *cL = G + S * kLd, *dcR = cL + S;
 
-        load_tile<T>(Qb, MB, DB, ml, d, [&](int l) { return p.q + toff + ((int64_t)l * b + j) * d; }, tid);
-        load_tile<T>(aL, MB, DB, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * kD; }, tid);
+        load_tile<T, NTH>(Qb, MB, DB, ml, d, [&](int l) { return p.q + toff + ((int64_t)l * b + j) * d; }, tid);
+        load_tile<T, NTH>(aL, MB, DB, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * kD; }, tid);
         if constexpr (LAST) {
-            load_tile<T>(X, MB, DB, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * kD; }, tid);
-            load_tile<T>(G, MB, DB, ml, d, [&](int l) { return p.dout + toff + ((int64_t)l * b + j) * d; }, tid);
+            load_tile<T, NTH>(X, MB, DB, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * kD; }, tid);
+            load_tile<T, NTH>(G, MB, DB, ml, d, [&](int l) { return p.dout + toff + ((int64_t)l * b + j) * d; }, tid);
         } else {
-            load_tile<float>(X, MB, DB, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * kD; }, tid);
+            load_tile<float, NTH>(X, MB, DB, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * kD; }, tid);
         }
-        for (int k = tid; k < S; k += kThreads) {
+        for (int k = tid; k < S; k += NTH) {
             cL[k] = k < m ? p.cL[coff + (int64_t)k * b + j] : 0.f;
             dcR[k] = (!LAST && k < m) ? p.dcR[coff + (int64_t)k * b + j] : 0.f;
         }
         __syncthreads();
 
         // unnormalised scores <Qbar[l], alpha_L[k]>
-        gemm<1>({as_is(Qb)}, {transposed(aL)}, MB, MB, DB, wave, lane, to_lds(Lm));
+        gemm<W>(MB, MB, DB, wave, lane, to_lds(Lm), pair<false, true>(Qb, aL));
         __syncthreads();
         // L[l][k] = softmax_k (s score - c_L[k]): one wave per row l, lane k
-        for (int l = wave; l < MB; l += kWaves) {
+        for (int l = wave; l < MB; l += W) {
             const int k = lane;
             if (l >= m) {
                 if (k < MB) Lm[l * kLd + k] = 0.f;
@@ -188,19 +258,22 @@ template <typename T, int S, bool LAST> struct LBwd {
 
         if constexpr (LAST) {
             // dL = dO Y^T;  dY = L^T dO (to the workspace, read by r_bwd of this step)
-            gemm<1>({as_is(G)}, {transposed(X)}, MB, MB, DB, wave, lane, to_lds(dL));
+            gemm<W>(MB, MB, DB, wave, lane, to_lds(dL), pair<false, true>(G, X));
             float *dY = p.dY + soff + (int64_t)j * m * kD;
-            gemm<1>({transposed(Lm)}, {as_is(G)}, MB, DB, MB, wave, lane, [&](int k, int e, float v) {
-                if (k < m && e < d) dY[(int64_t)k * kD + e] = v;
-            });
+            gemm<W>(
+                MB, DB, MB, wave, lane,
+                [&](int k, int e, float v) {
+                    if (k < m && e < d) dY[(int64_t)k * kD + e] = v;
+                },
+                pair<true, false>(Lm, G));
         } else {
             // dL = Qbar d alpha_R'^T (+ d c_R' below);  G = L d alpha_R' (the alpha_R' term of dQbar)
-            gemm<1>({as_is(Qb)}, {transposed(X)}, MB, MB, DB, wave, lane, to_lds(dL));
-            gemm<1>({as_is(Lm)}, {as_is(X)}, MB, DB, MB, wave, lane, to_lds(G));
+            gemm<W>(MB, MB, DB, wave, lane, to_lds(dL), pair<false, true>(Qb, X));
+            gemm<W>(MB, DB, MB, wave, lane, to_lds(G), pair<false, false>(Lm, X));
         }
         __syncthreads();
         // dW = s L (dL - <L, dL>), in place of dL
-        for (int l = wave; l < MB; l += kWaves) {
+        for (int l = wave; l < MB; l += W) {
             const int k = lane;
             const float pk = k < MB ? Lm[l * kLd + k] : 0.f;
             const float w = k < MB ? dL[l * kLd + k] + dcR[k] : 0.f;
@@ -211,23 +284,29 @@ template <typename T, int S, bool LAST> struct LBwd {
 
         // dQ rows l*b + j: dW alpha_L (+ L d alpha_R')
         float *dQ = p.dQ + toff + (int64_t)j * d;
-        gemm<1>({as_is(dL)}, {as_is(aL)}, MB, DB, MB, wave, lane, [&](int l, int e, float v) {
-            if (l < ml && e < d) {
-                float *o = dQ + (int64_t)l * b * d + e;
-                if constexpr (LAST) {
-                    *o = v;
-                } else {
-                    *o += v + G[l * kLd + e];
+        gemm<W>(
+            MB, DB, MB, wave, lane,
+            [&](int l, int e, float v) {
+                if (l < ml && e < d) {
+                    float *o = dQ + (int64_t)l * b * d + e;
+                    if constexpr (LAST) {
+                        *o = v;
+                    } else {
+                        *o += v + G[l * kLd + e];
+                    }
                 }
-            }
-        });
+            },
+            pair<false, false>(dL, aL));
         // d alpha_L[k] = dW^T Qbar
         float *daL = p.daL + soff + (int64_t)j * m * kD;
-        gemm<1>({transposed(dL)}, {as_is(Qb)}, MB, DB, MB, wave, lane, [&](int k, int e, float v) {
-            if (k < m && e < d) daL[(int64_t)k * kD + e] = v;
-        });
+        gemm<W>(
+            MB, DB, MB, wave, lane,
+            [&](int k, int e, float v) {
+                if (k < m && e < d) daL[(int64_t)k * kD + e] = v;
+            },
+            pair<true, false>(dL, Qb));
         // d c_L[k] = -(1/s) sum_l dW[l][k]
-        for (int k = tid; k < m; k += kThreads) {
+        for (int k = tid; k < m; k += NTH) {
             float cs = 0.f;
             for (int l = 0; l < MB; ++l) cs += dL[l * kLd + k];
             p.dcL[coff + (int64_t)j * m + k] = -cs / dm.s;
@@ -240,6 +319,7 @@ template <typename T, int S, bool LAST> struct LBwd {
 // S: rows of the tiles (16, 32 or 64, >= b).
 // ---------------------------------------------------------------------------------------
 template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
+    static constexpr int W = Waves<S>::value, NTH = 64 * W;
     static constexpr int TILES = LAST ? 7 : 5;
     static constexpr int LDS_FLOATS = TILES * S * kLd + 2 * S;
 
@@ -257,34 +337,34 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         float *Vb = dR + S * kLd, *dYt = Vb + S * kLd;  // LAST only
         float *cR = lds + TILES * S * kLd, *dcL = cR + S;
 
-        load_tile<T>(Kb, BB, DB, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
+        load_tile<T, NTH>(Kb, BB, DB, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
         if constexpr (FIRST) {
-            load_tile<T>(aR, BB, DB, kv, d, [&](int jj) { return p.q + toff + (row0 + jj) * d; }, tid);
+            load_tile<T, NTH>(aR, BB, DB, kv, d, [&](int jj) { return p.q + toff + (row0 + jj) * d; }, tid);
         } else {
-            load_tile<T>(aR, BB, DB, b, d, [&](int jj) { return p.aR + soff + (row0 + jj) * kD; }, tid);
+            load_tile<T, NTH>(aR, BB, DB, b, d, [&](int jj) { return p.aR + soff + (row0 + jj) * kD; }, tid);
         }
-        load_tile<float>(dA, BB, DB, b, d, [&](int jj) { return p.daL + soff + ((int64_t)jj * m + k) * kD; }, tid);
+        load_tile<float, NTH>(dA, BB, DB, b, d, [&](int jj) { return p.daL + soff + ((int64_t)jj * m + k) * kD; }, tid);
         if constexpr (LAST) {
-            load_tile<T>(Vb, BB, DB, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
-            load_tile<float>(dYt, BB, DB, b, d, [&](int jj) { return p.dY + soff + ((int64_t)jj * m + k) * kD; },
+            load_tile<T, NTH>(Vb, BB, DB, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
+            load_tile<float, NTH>(dYt, BB, DB, b, d, [&](int jj) { return p.dY + soff + ((int64_t)jj * m + k) * kD; },
                              tid);
         }
-        for (int jj = tid; jj < S; jj += kThreads) {
+        for (int jj = tid; jj < S; jj += NTH) {
             cR[jj] = (FIRST || jj >= b) ? 1.f : p.cR[coff + (int64_t)jj * m + k];
             dcL[jj] = jj < b ? p.dcL[coff + (int64_t)jj * m + k] : 0.f;
         }
         __syncthreads();
 
         // unnormalised scores <alpha_R[j], Kbar[i]>;  dR = d alpha_L Kbar^T (+ dY Vbar^T)
-        gemm<1>({as_is(aR)}, {transposed(Kb)}, BB, BB, DB, wave, lane, to_lds(Rm));
+        gemm<W>(BB, BB, DB, wave, lane, to_lds(Rm), pair<false, true>(aR, Kb));
         if constexpr (LAST) {
-            gemm<2>({as_is(dA), as_is(dYt)}, {transposed(Kb), transposed(Vb)}, BB, BB, DB, wave, lane, to_lds(dR));
+            gemm<W>(BB, BB, DB, wave, lane, to_lds(dR), pair<false, true>(dA, Kb), pair<false, true>(dYt, Vb));
         } else {
-            gemm<1>({as_is(dA)}, {transposed(Kb)}, BB, BB, DB, wave, lane, to_lds(dR));
+            gemm<W>(BB, BB, DB, wave, lane, to_lds(dR), pair<false, true>(dA, Kb));
         }
         __syncthreads();
         // per row j (one wave, lane i): R, then dZ scaled by s / c_R[j] in place of dR
-        for (int jj = wave; jj < BB; jj += kWaves) {
+        for (int jj = wave; jj < BB; jj += W) {
             const int i = lane;
             if (jj >= b) {
                 if (i < BB) Rm[jj * kLd + i] = dR[jj * kLd + i] = 0.f;
@@ -314,51 +394,62 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         if constexpr (FIRST) {
             const float *dQ = p.dQ + toff + row0 * d;
             T *dq = p.dq + toff + row0 * d;
-            gemm<1>({as_is(dR)}, {as_is(Kb)}, BB, DB, BB, wave, lane, [&](int jj, int e, float v) {
-                if (jj < kv && e < d) dq[(int64_t)jj * d + e] = static_cast<T>(dQ[(int64_t)jj * d + e] + v);
-            });
+            gemm<W>(
+                BB, DB, BB, wave, lane,
+                [&](int jj, int e, float v) {
+                    if (jj < kv && e < d) dq[(int64_t)jj * d + e] = static_cast<T>(dQ[(int64_t)jj * d + e] + v);
+                },
+                pair<false, false>(dR, Kb));
         } else {
             float *daR = p.daR + soff + row0 * kD;
-            gemm<1>({as_is(dR)}, {as_is(Kb)}, BB, DB, BB, wave, lane, [&](int jj, int e, float v) {
-                if (jj < b && e < d) daR[(int64_t)jj * kD + e] = v;
-            });
+            gemm<W>(
+                BB, DB, BB, wave, lane,
+                [&](int jj, int e, float v) {
+                    if (jj < b && e < d) daR[(int64_t)jj * kD + e] = v;
+                },
+                pair<false, false>(dR, Kb));
         }
         // dKbar[i] += sum_j R[j][i] d alpha_L[j] + sum_j dZs[j][i] alpha_R[j]
         {
             float *dK = p.dK + toff + row0 * d;
             T *dk = p.dk + toff + row0 * d;
-            gemm<2>({transposed(Rm), transposed(dR)}, {as_is(dA), as_is(aR)}, BB, DB, BB, wave, lane,
-                    [&](int i, int e, float v) {
-                        if (i < kv && e < d) {
-                            const int64_t o = (int64_t)i * d + e;
-                            const float acc = LAST ? v : v + dK[o];
-                            if constexpr (FIRST) {
-                                dk[o] = static_cast<T>(acc);
-                            } else {
-                                dK[o] = acc;
-                            }
+            gemm<W>(
+                BB, DB, BB, wave, lane,
+                [&](int i, int e, float v) {
+                    if (i < kv && e < d) {
+                        const int64_t o = (int64_t)i * d + e;
+                        const float acc = LAST ? v : v + dK[o];
+                        if constexpr (FIRST) {
+                            dk[o] = static_cast<T>(acc);
+                        } else {
+                            dK[o] = acc;
                         }
-                    });
+                    }
+                },
+                pair<true, false>(Rm, dA), pair<true, false>(dR, aR));
         }
         // dVbar[i] = sum_j R[j][i] dY[j]
         if constexpr (LAST) {
             T *dv = p.dv + toff + row0 * d;
-            gemm<1>({transposed(Rm)}, {as_is(dYt)}, BB, DB, BB, wave, lane, [&](int i, int e, float v) {
-                if (i < kv && e < d) dv[(int64_t)i * d + e] = static_cast<T>(v);
-            });
+            gemm<W>(
+                BB, DB, BB, wave, lane,
+                [&](int i, int e, float v) {
+                    if (i < kv && e < d) dv[(int64_t)i * d + e] = static_cast<T>(v);
+                },
+                pair<true, false>(Rm, dYt));
         }
     }
 };
 
 template <typename T, int S, bool LAST>
-__global__ __launch_bounds__(kThreads) void l_bwd(BwdBufs<T> p, BwdDims dm)
+__global__ __launch_bounds__(64 * Waves<S>::value) void l_bwd(BwdBufs<T> p, BwdDims dm)
 {
     __shared__ __attribute__((aligned(16))) float lds[LBwd<T, S, LAST>::LDS_FLOATS];
     LBwd<T, S, LAST>::run(p, dm, lds);
 }
 
 template <typename T, int S, bool FIRST, bool LAST>
-__global__ __launch_bounds__(kThreads) void r_bwd(BwdBufs<T> p, BwdDims dm)
+__global__ __launch_bounds__(64 * Waves<S>::value) void r_bwd(BwdBufs<T> p, BwdDims dm)
 {
     __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, FIRST, LAST>::LDS_FLOATS];
     RBwd<T, S, FIRST, LAST>::run(p, dm, lds);

@@ -252,7 +252,7 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
 template <typename T, int S, bool LAST>
 int launch_l_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
-    const dim3 grid((unsigned)(BH * dm.b)), block(ma::bwd::kThreads);
+    const dim3 grid((unsigned)(BH * dm.b)), block(64 * ma::bwd::Waves<S>::value);
     return L.run(kBwdL, [&] {
         return launched([&] { hipLaunchKernelGGL((ma::bwd::l_bwd<T, S, LAST>), grid, block, 0, L.stream, p, dm); });
     });
@@ -261,7 +261,7 @@ int launch_l_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, in
 template <typename T, int S, bool FIRST, bool LAST>
 int launch_r_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
-    const dim3 grid((unsigned)(BH * dm.m)), block(ma::bwd::kThreads);
+    const dim3 grid((unsigned)(BH * dm.m)), block(64 * ma::bwd::Waves<S>::value);
     return L.run(kBwdR, [&] {
         return launched(
             [&] { hipLaunchKernelGGL((ma::bwd::r_bwd<T, S, FIRST, LAST>), grid, block, 0, L.stream, p, dm); });
