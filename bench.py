@@ -17,6 +17,19 @@ Timed regions (HIP events on the stream the library launches on):
 Inputs rotate over several copies (>= 512 MB in total) so that the 256 MB
 last-level cache cannot serve them from one step to the next.
 
+Each workload also reports the p10 / median / p90 of single calls (each
+between its own events) and a "hot" time on one input set.  measured_peaks
+holds a 1 GiB device copy and 8192^3 GEMMs (bf16, fp32) timed on this GPU;
+every roofline record adds its fraction of that measured peak beside the
+fraction of the published one.
+
+sweep: the long-sequence points N = 256, 1024, 4096, 16384 (sqrt(N) x
+sqrt(N), d = 64 and 128, T = 2, 16 heads), with the call roofline and the
+dominant kernel of each; at d = 64 and the paper's quoted N it also times
+torch's fused scaled_dot_product_attention (flash or memory-efficient
+backend) on the same shape, as context beside the paper's own speed-ups over
+FlashAttention-2 on its hardware.
+
 cpu_baseline: the fp64 C oracle, as it stands, on this host's cores, on the
 same workload (repeated whole forward passes, about 10-30 s in total).
 
@@ -140,6 +153,7 @@ def measure(ma, torch, w, steps, warmup):
     end.synchronize()
     ms = start.elapsed_time(end) / steps
     log(f"[bench] {w.name}: {ms * 1e3:.1f} us per step over {steps} steps ({nsets} rotating input sets)")
+    extra = {"per_call_us": per_call_distribution(torch, step, steps), "hot_ms_per_step": hot_time(torch, step, steps)}
 
     # per-launch kernel durations
     plan, sums = None, None
@@ -170,7 +184,122 @@ def measure(ma, torch, w, steps, warmup):
     torch.cuda.synchronize()
     del sets
     torch.cuda.empty_cache()
-    return ms, kernels, meta, nsets
+    return ms, kernels, meta, nsets, extra
+
+
+def per_call_distribution(torch, step, steps):
+    """p10 / median / p90 of single calls, each between its own pair of events
+    (rotating inputs as in the main region)."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for i, (a, b) in enumerate(evs):
+        a.record()
+        step(i)
+        b.record()
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) * 1e3 for a, b in evs)
+
+    def q(f):
+        return round(t[min(len(t) - 1, int(f * (len(t) - 1) + 0.5))], 3)
+
+    return {"p10": q(0.1), "p50": q(0.5), "p90": q(0.9)}
+
+
+def hot_time(torch, step, steps):
+    """ms per call with the same input set every call (caches warm), labelled hot."""
+    step(0)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        step(0)
+    b.record()
+    b.synchronize()
+    return round(a.elapsed_time(b) / steps, 6)
+
+
+def measured_peaks(torch):
+    """Peaks measured on this GPU, beside the published ones: a 1 GiB device copy
+    (read + write bytes / time) and dense 8192^3 GEMMs through torch (hipBLASLt)
+    in bf16 and fp32.  Context for the roofline fractions, not a substitute."""
+    out = {}
+    n = (1 << 30) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(10):
+        dst.copy_(src)
+    b.record()
+    b.synchronize()
+    out["copy_GB_s"] = round(2 * n * 4 * 10 / (a.elapsed_time(b) * 1e-3) / 1e9, 1)
+    del src, dst
+    for name, dt in (("gemm_bf16_TFLOP_s", torch.bfloat16), ("gemm_f32_TFLOP_s", torch.float32)):
+        x = torch.randn(8192, 8192, device="cuda").to(dt)
+        y = torch.randn(8192, 8192, device="cuda").to(dt)
+        for _ in range(2):
+            torch.matmul(x, y)
+        a.record()
+        for _ in range(5):
+            torch.matmul(x, y)
+        b.record()
+        b.synchronize()
+        out[name] = round(2 * 8192 ** 3 * 5 / (a.elapsed_time(b) * 1e-3) / 1e12, 1)
+        del x, y
+    torch.cuda.empty_cache()
+    return out
+
+
+def with_measured(roof, peaks):
+    """Add the fraction of the measured peak to a roofline record."""
+    if peaks:
+        key = "copy_GB_s" if roof["unit"] == "GB/s" else (
+            "gemm_f32_TFLOP_s" if roof["peak"] == MFMA_PEAK_TFLOPS["f32"] else "gemm_bf16_TFLOP_s")
+        roof["measured_peak"] = peaks[key]
+        roof["frac_of_measured"] = round(roof["achieved"] / peaks[key], 4)
+    return roof
+
+
+# The paper's speed-ups of MonarchAttention over FlashAttention-2 (its own
+# hardware and Triton kernels), quoted as context beside the same ratio on this
+# GPU against torch's fused attention.
+PAPER_SPEEDUP_VS_FA2 = {256: 1.4, 4096: 4.5, 16384: 8.2}
+
+
+def sdpa_context(ma, torch, w, steps, warmup, monarch_ms):
+    """Time torch.nn.functional.scaled_dot_product_attention (flash or
+    memory-efficient backend only, never the math path) on the workload's
+    shape with rotating inputs, and the ratio to the Monarch call."""
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+
+    shape = (w.B, w.H, w.N, w.d)
+    per_set = 4 * w.B * w.H * w.N * w.d * 2
+    nsets = max(1, min(8, math.ceil(ROTATE_BYTES / per_set)))
+    sets = [[torch.randn(shape, device="cuda", dtype=torch.bfloat16) for _ in range(3)] for _ in range(nsets)]
+    res = {"N": w.N, "paper_speedup_vs_fa2": PAPER_SPEEDUP_VS_FA2.get(w.N)}
+    for backend in (SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION):
+        try:
+            with sdpa_kernel(backend):
+                for i in range(warmup):
+                    F.scaled_dot_product_attention(*sets[i % nsets])
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record()
+                for i in range(steps):
+                    F.scaled_dot_product_attention(*sets[i % nsets])
+                b.record()
+                b.synchronize()
+            ms = a.elapsed_time(b) / steps
+            res.update({"sdpa_backend": backend.name, "sdpa_ms": round(ms, 6), "monarch_ms": round(monarch_ms, 6),
+                        "speedup": round(ms / monarch_ms, 3)})
+            break
+        except RuntimeError as e:
+            res[f"{backend.name}_unavailable"] = str(e).splitlines()[0][:160]
+    del sets
+    torch.cuda.empty_cache()
+    return res
 
 
 def bwd_kernel_work(w, kind, t):
@@ -426,6 +555,11 @@ def main():
                     help="comma-separated extra workloads ('' for none)")
     ap.add_argument("--backward", default="speed_n4096,vit_b16_n197",
                     help="comma-separated workloads for the gradient timing ('' for none)")
+    ap.add_argument("--sweep", default=",".join(f"sweep_n{n}_d{d}" for n in (256, 1024, 4096, 16384)
+                                                   for d in (64, 128)),
+                    help="comma-separated workloads of the N / d sweep ('' for none)")
+    ap.add_argument("--no-sdpa", action="store_true", help="skip the torch fused-attention context timing")
+    ap.add_argument("--no-measured-peaks", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-quality", action="store_true",
                     help="skip the approximation-quality figures (error against exact attention, objective gap)")
@@ -463,7 +597,8 @@ def main():
     if args.T:
         w = w.with_(T=args.T)
 
-    ms, kernels, meta, nsets = measure(ma, torch, w, args.steps, args.warmup)
+    peaks = measured_peaks(torch) if not args.no_measured_peaks else None
+    ms, kernels, meta, nsets, extra = measure(ma, torch, w, args.steps, args.warmup)
     share = [k["avg_us"] for k in kernels]
     dom = kernels[share.index(max(share))]
     value = w.B * w.H * w.N / (ms * 1e-3)
@@ -483,22 +618,38 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": cfg,
-        "roofline": roofline_of(dom, w.dtype, w.name),
+        "roofline": with_measured(roofline_of(dom, w.dtype, w.name), peaks),
         "call_roofline": call_roofline(w, ms),
         "kernels": kernels,
+        **extra,
+        "measured_peaks": peaks,
     }
     also = []
     for name in [x for x in args.also.split(",") if x]:
         w2 = si.WORKLOADS[name]
-        ms2, kern2, meta2, nsets2 = measure(ma, torch, w2, args.steps, args.warmup)
+        ms2, kern2, meta2, nsets2, extra2 = measure(ma, torch, w2, args.steps, args.warmup)
         sh2 = [k["avg_us"] for k in kern2]
         dom2 = kern2[sh2.index(max(sh2))]
         cfg2 = w2.describe()
         cfg2.update({"alpha": meta2.get("alpha"), "rotating_input_sets": nsets2})
         also.append({"config": cfg2, "value": round(w2.B * w2.H * w2.N / (ms2 * 1e-3), 1), "unit": UNIT,
-                     "ms_per_step": round(ms2, 6), "roofline": roofline_of(dom2, w2.dtype, w2.name),
-                     "call_roofline": call_roofline(w2, ms2), "kernels": kern2})
+                     "ms_per_step": round(ms2, 6),
+                     "roofline": with_measured(roofline_of(dom2, w2.dtype, w2.name), peaks),
+                     "call_roofline": call_roofline(w2, ms2), "kernels": kern2, **extra2})
     result["also"] = also
+    sweep = []
+    for name in [x for x in args.sweep.split(",") if x]:
+        w3 = si.WORKLOADS[name]
+        ms3, kern3, meta3, _, extra3 = measure(ma, torch, w3, args.steps, args.warmup)
+        dom3 = max(kern3, key=lambda x: x["avg_us"])
+        rec = {"workload": name, "N": w3.N, "d": w3.d, "T": w3.T, "alpha": meta3.get("alpha"),
+               "value": round(w3.B * w3.H * w3.N / (ms3 * 1e-3), 1), "ms_per_step": round(ms3, 6),
+               "call_roofline": call_roofline(w3, ms3), "dominant": dom3["kernel"],
+               "roofline": with_measured(roofline_of(dom3, w3.dtype, name), peaks), **extra3}
+        if not args.no_sdpa and w3.d == 64 and w3.N in PAPER_SPEEDUP_VS_FA2:
+            rec["context_vs_torch_sdpa"] = sdpa_context(ma, torch, w3, args.steps, args.warmup, ms3)
+        sweep.append(rec)
+    result["sweep"] = sweep
     result["backward"] = [measure_backward(ma, torch, si.WORKLOADS[name], args.steps, args.warmup)
                           for name in [x for x in args.backward.split(",") if x]]
     if not args.no_quality:

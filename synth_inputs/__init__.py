@@ -108,6 +108,12 @@ WORKLOADS = {
     # graph transformer node classification: N = 7600 nodes, b = 128, d = 48
     "gps_n7600": Workload("gps_n7600", 1, 4, 60, 128, 48, 2, "bf16", "vit", n=7600),
 }
+# The long-sequence sweep: N = 256 .. 16384 in powers of 4 as sqrt(N) x sqrt(N),
+# d in {64, 128}, T = 2, the speed recipe (its scale recalibrated for every N).
+for _n, _r in ((256, 16), (1024, 32), (4096, 64), (16384, 128)):
+    for _d in (64, 128):
+        _name = f"sweep_n{_n}_d{_d}"
+        WORKLOADS[_name] = Workload(_name, 1, 16, _r, _r, _d, 2, "bf16", "speed")
 
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
