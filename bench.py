@@ -406,7 +406,7 @@ def measure_backward(ma, torch, w, steps, warmup):
     dom = max(sweep, key=lambda x: x["avg_us"])
     # the sweep's products are fp32 MFMA whatever the element type
     roof = roofline_of(dom, "f32")
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(f"{dom['kernel']}[t={dom['step']}]", w.name)
     return {"config": w.describe(), "value": round(w.B * w.H * w.N / (ms * 1e-3), 1), "unit": UNIT,
             "ms_per_call": round(ms, 6), "recompute_us": round(sum(x["avg_us"] for x in kernels[:nrec]), 3),
             "sweep_us": round(sum(x["avg_us"] for x in sweep), 3), "roofline": roof, "kernels": kernels,
@@ -454,27 +454,35 @@ def quality(ma, torch, w, steps_list=(1, 2, 3)):
             "exact_objective_head0": round(float(bound[0, 0]), 2), "monarch": rows}
 
 
-def kernel_sources_sha():
-    import glob
+# Sources whose text fixes each kernel's memory traffic: the kernels'
+# definitions and their launch configuration.
+CSRC = os.path.join(ROOT, "paper_2505_18698_amd", "csrc")
+FWD_SOURCES = ("ma_kernels.hpp", "dispatch.hpp")
+BWD_SOURCES = ("backward.hpp", "ma_kernels.hpp", "dispatch.hpp")
+
+
+def kernel_sources_sha(kernel):
     import hashlib
 
-    src = b"".join(open(p, "rb").read()
-                   for p in sorted(glob.glob(os.path.join(ROOT, "paper_2505_18698_amd", "csrc", "*"))))
+    files = BWD_SOURCES if kernel in ("l_bwd", "r_bwd") else FWD_SOURCES
+    src = b"".join(open(os.path.join(CSRC, f), "rb").read() for f in files)
     return hashlib.sha256(src).hexdigest()[:16]
 
 
 def measured_traffic(kernel, workload):
     """HBM bytes (read + write) per launch from the committed rocprofv3 byte counters
-    (profiles/traffic.json), or None when the kernels changed since they were taken."""
+    (profiles/traffic.json), or None when the kernel's sources changed since they
+    were taken (or it was not profiled on this workload)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         rec = json.load(open(path))
     except (OSError, ValueError):
         return None
-    if rec.get("source_sha256_16") != kernel_sources_sha():
-        return None
+    base = kernel.split("[")[0]
     k = rec.get("kernels", {}).get(f"{kernel}@{workload}")
-    return None if k is None else k["read_bytes"] + k["write_bytes"]
+    if k is None or k.get("source_sha256_16") != kernel_sources_sha(base):
+        return None
+    return k["read_bytes"] + k["write_bytes"]
 
 
 def roofline_of(kernel, dtype, workload=None):
