@@ -526,8 +526,21 @@ def cpu_baseline(w, budget_s=10.0, max_runs=20):
         if el >= budget_s or runs >= max_runs:
             break
     rate = runs * w.B * w.H * w.N / el
-    return {"value": round(rate, 1), "unit": UNIT, "cores": threads, "kind": "oracle",
-            "sample": f"{runs} full forward passes of {w.name} (all {w.B * w.H} heads), fp64, {el:.1f}s"}
+    res = {"value": round(rate, 1), "unit": UNIT, "cores": threads, "kind": "oracle",
+           "sample": f"{runs} full forward passes of {w.name} (all {w.B * w.H} heads), fp64, {el:.1f}s"}
+    # one thread on a bounded ViT-B/16 sample (48 of its 384 heads), for scaling context
+    v = si.WORKLOADS["vit_b16_n196"]
+    q1, k1, v1, _ = si.make_qkv(v.with_(B=4))
+    runs1, t1 = 0, time.time()
+    while True:
+        oracle.monarch_attention(q1, k1, v1, v.m, v.b, v.T, threads=1)
+        runs1 += 1
+        el1 = time.time() - t1
+        if el1 >= budget_s / 2 or runs1 >= max_runs:
+            break
+    res["single_thread"] = {"value": round(runs1 * 4 * v.H * v.N / el1, 1), "unit": UNIT, "cores": 1,
+                            "sample": f"{runs1} passes of {v.name} at B=4 (48 heads), fp64, 1 thread, {el1:.1f}s"}
+    return res
 
 
 def copy_sweep(torch, sizes_mb, steps, warmup):

@@ -207,13 +207,13 @@ int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, dou
         return MO_ENOMEM;
     }
 #ifdef _OPENMP
-    if (threads > 0) omp_set_num_threads(threads);
+    const int nt = threads > 0 ? threads : omp_get_max_threads(); /* this call only */
 #else
     (void)threads;
 #endif
     const int64_t zlen = (m > b ? m : b);
 
-#pragma omp parallel for schedule(static)
+#pragma omp parallel for schedule(static) num_threads(nt)
     for (int64_t h = 0; h < BH; ++h)
         for (int64_t e = 0; e < N * d; ++e) {
             Qs[h * nd + e] = s * q[h * N * d + e]; /* scale absorbed into Q */
@@ -221,14 +221,14 @@ int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, dou
             Vp[h * nd + e] = v[h * N * d + e];
         }
     /* t = 1 state from L^(0) = I: alpha_R[k][j] = s*Q[k*b+j], c_R = 1. */
-#pragma omp parallel for schedule(static)
+#pragma omp parallel for schedule(static) num_threads(nt)
     for (int64_t e = 0; e < BH * nd; ++e) aR[e] = Qs[e];
-#pragma omp parallel for schedule(static)
+#pragma omp parallel for schedule(static) num_threads(nt)
     for (int64_t e = 0; e < BH * Np; ++e) cR[e] = 1.0;
 
     for (int32_t t = 1; t <= T; ++t) {
         const int last = (t == T);
-#pragma omp parallel
+#pragma omp parallel num_threads(nt)
         {
             double *z = malloc(sizeof(double) * (size_t)zlen);
             double *hl = malloc(sizeof(double) * (size_t)m);
@@ -257,7 +257,7 @@ int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, dou
         }
     }
     /* the first N rows of every head */
-#pragma omp parallel for schedule(static)
+#pragma omp parallel for schedule(static) num_threads(nt)
     for (int64_t h = 0; h < BH; ++h)
         memcpy(out + h * N * d, Op + h * nd, sizeof(double) * (size_t)(N * d));
     free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
@@ -281,12 +281,12 @@ int ma_oracle_dense_attn_f64(const double *q, const double *k, const double *v, 
 {
     if (!q || !k || !v || !out || BH < 1 || N < 1 || d < 1 || rows < 1) return MO_EINVAL;
 #ifdef _OPENMP
-    if (threads > 0) omp_set_num_threads(threads);
+    const int nt = threads > 0 ? threads : omp_get_max_threads(); /* this call only */
 #else
     (void)threads;
 #endif
     const double s = 1.0 / sqrt((double)d);
-#pragma omp parallel
+#pragma omp parallel num_threads(nt)
     {
         double *z = malloc(sizeof(double) * (size_t)N);
 #pragma omp for collapse(2) schedule(static)

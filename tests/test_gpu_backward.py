@@ -192,3 +192,31 @@ def test_vit_workload_sampled_heads(ma):
     got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
     ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
     check(got, ref, heads, w.dtype, w.name)
+
+
+def test_forward_and_gradient_calls_share_the_workspace(ma):
+    """Forward (half-step path) and gradient calls of different sizes, in turn and
+    across a release of the workspace, each match their references: the shared
+    per-device workspace grows and is reused without stale state leaking."""
+    import torch
+
+    prev = ma.monarch_attn_set_path(ma.PATH_HALF_STEPS)
+    try:
+        cases = [(1, 2, 64, 8, 8, 64, 2), (2, 3, 1000, 63, 16, 64, 3), (1, 1, 256, 16, 16, 32, 1)]
+        for rnd in range(2):
+            for B, H, n, m, b, d, T in cases:
+                q, k, v = si.random_qkv(B, H, n, d, "bf16", seed=n + rnd, scale=1.5)
+                dout = si.random_cotangent((B, H, n, d), "bf16", seed=n + rnd)
+                tq, tk, tv = (torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (q, k, v))
+                out = torch.full_like(tq, float("nan"))
+                ma.monarch_attn_fwd(tq, tk, tv, out, m, b, T)
+                torch.cuda.synchronize()
+                err = oracle.rel_frobenius(out.double().cpu().numpy(), oracle.monarch_attention(q, k, v, m, b, T))
+                assert err <= 2e-2, ("forward", rnd, n, err)
+                got = gpu_grads(ma, q, k, v, dout, m, b, T, "bf16")
+                ref = oracle_grads(q, k, v, dout, m, b, T, [(0, 0)])
+                check(got, ref, [(0, 0)], "bf16", f"interleaved round {rnd} n{n} m{m} b{b} d{d} T{T}")
+            if rnd == 0:
+                ma.monarch_attn_release_workspace()
+    finally:
+        ma.monarch_attn_set_path(prev)
