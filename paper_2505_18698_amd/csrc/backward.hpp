@@ -67,8 +67,6 @@ template <int S> struct Waves {
     static constexpr int value = S / 4;
 };
 
-__device__ inline int up16(int x) { return (x + 15) & ~15; }
-
 // Reductions over the 64 lanes with no LDS round trip: DPP within rows of 16
 // lanes (xor 1, xor 2, then mirrors of 8 and 16 lanes), then the permlane
 // swaps across rows.  Every lane ends with the same value.
@@ -103,63 +101,57 @@ __device__ inline float wave_max(float x)
 // MFMA step s of a 16-long chunk k0 hands lane group g = lane/16 the index
 // k0 + 4g + s, so a lane reads four consecutive k at once: one 16-byte read
 // where k is contiguous (A as stored, B transposed), four conflict-free
-// scalar reads otherwise.
+// scalar reads otherwise.  The contraction length is a compile-time constant:
+// the loop unrolls, every read is the lane's base address plus an immediate
+// offset, and all reads can be issued ahead of the MFMAs.
 template <bool TA, bool TB> struct Pair {
     const float *A, *B;
 
-    __device__ void load(float (&a)[4], float (&b)[4], int r, int n, int k) const
+    // acc += sum_{k < K} A(r, k) B(k, n)
+    template <int K> __device__ void accumulate(f32x4 &acc, int r, int n, int g) const
     {
-        if constexpr (TA) {
+        const float *pa = TA ? A + 4 * g * kLd + r : A + r * kLd + 4 * g;
+        const float *pb = TB ? B + n * kLd + 4 * g : B + 4 * g * kLd + n;
 #pragma unroll
-            for (int s = 0; s < 4; ++s) a[s] = A[(k + s) * kLd + r];
-        } else {
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(A + r * kLd + k);
-#pragma unroll
-            for (int s = 0; s < 4; ++s) a[s] = v[s];
-        }
-        if constexpr (TB) {
-            const f32x4 v = *reinterpret_cast<const f32x4 *>(B + n * kLd + k);
-#pragma unroll
-            for (int s = 0; s < 4; ++s) b[s] = v[s];
-        } else {
-#pragma unroll
-            for (int s = 0; s < 4; ++s) b[s] = B[(k + s) * kLd + n];
-        }
-    }
-
-    // acc += sum_k A(r0 + .., k) B(k, c0 + ..) over k < K (a multiple of 16),
-    // the next chunk's reads in flight during the current chunk's MFMAs.
-    __device__ void accumulate(f32x4 &acc, int r0, int c0, int K, int g, int c) const
-    {
-        float a[4], b[4], an[4], bn[4];
-        load(a, b, r0 + c, c0 + c, 4 * g);
         for (int k0 = 0; k0 < K; k0 += 16) {
-            const int kn = min(k0 + 16, K - 16);  // a valid chunk; unused after the last
-            load(an, bn, r0 + c, c0 + c, kn + 4 * g);
+            float a[4], b[4];
+            if constexpr (TA) {
+#pragma unroll
+                for (int s = 0; s < 4; ++s) a[s] = pa[(k0 + s) * kLd];
+            } else {
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(pa + k0);
+#pragma unroll
+                for (int s = 0; s < 4; ++s) a[s] = v[s];
+            }
+            if constexpr (TB) {
+                const f32x4 v = *reinterpret_cast<const f32x4 *>(pb + k0);
+#pragma unroll
+                for (int s = 0; s < 4; ++s) b[s] = v[s];
+            } else {
+#pragma unroll
+                for (int s = 0; s < 4; ++s) b[s] = pb[(k0 + s) * kLd];
+            }
 #pragma unroll
             for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                a[s] = an[s];
-                b[s] = bn[s];
-            }
         }
     }
 };
 
-// out(r, c) = sum over the pairs of A(r, :) B(:, c) for r < M, c < N
-// (multiples of 16), contraction K (a multiple of 16).  The 16 x 16 output
-// tiles are shared out over the W waves; lane (g, c) of v_mfma_f32_16x16x4f32
-// receives rows 4g + q, q = 0..3, of column c, and hands each element to
+// out(r, c) = sum over the pairs of A(r, :) B(:, c) for r < M, c < N, with
+// contraction K (all multiples of 16, fixed at compile time: the tiles are
+// zero beyond the live rows and columns).  The 16 x 16 output tiles are
+// shared out over the W waves; lane (g, c) of v_mfma_f32_16x16x4f32 receives
+// rows 4g + q, q = 0..3, of column c, and hands each element to
 // st(r, c, value): every element is stored by exactly one lane.
-template <int W, typename Store, typename... P>
-__device__ inline void gemm(int M, int N, int K, int wave, int lane, Store &&st, const P &...pairs)
+template <int W, int M, int N, int K, typename Store, typename... P>
+__device__ inline void gemm(int wave, int lane, Store &&st, const P &...pairs)
 {
-    const int g = lane >> 4, c = lane & 15, tn = N >> 4, tiles = (M >> 4) * tn;
+    constexpr int tn = N / 16, tiles = (M / 16) * tn;
+    const int g = lane >> 4, c = lane & 15;
     for (int t = wave; t < tiles; t += W) {
         const int r0 = (t / tn) * 16, c0 = (t % tn) * 16;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        (pairs.accumulate(acc, r0, c0, K, g, c), ...);
+        (pairs.template accumulate<K>(acc, r0 + c, c0 + c, g), ...);
 #pragma unroll
         for (int q = 0; q < 4; ++q) st(r0 + 4 * g + q, c0 + c, acc[q]);
     }
@@ -175,18 +167,17 @@ __device__ inline auto to_lds(float *t)
     return [t](int r, int c, float v) { t[r * kLd + c] = v; };
 }
 
-// Rows r < R and columns c < C (R, C the padded extents, C <= 64, a multiple
-// of 16) of an LDS tile from a row-major global matrix of element type E
-// whose row r starts at src(r) (16-byte aligned): element (r, c) is read while
+// Rows r < R and columns c < C (compile-time extents, C <= 64 a multiple of
+// 16) of an LDS tile from a row-major global matrix of element type E whose
+// row r starts at src(r) (16-byte aligned): element (r, c) is read while
 // r < nr and c < nc (nc a multiple of 16 bytes' worth of elements), zero
 // elsewhere.  One 16-byte global read per chunk.
-template <typename E, int NTH, typename Src>
-__device__ inline void load_tile(float *dst, int R, int C, int nr, int nc, Src src, int tid)
+template <typename E, int NTH, int R, int C, typename Src>
+__device__ inline void load_tile(float *dst, int nr, int nc, Src src, int tid)
 {
-    constexpr int V = 16 / (int)sizeof(E);
-    const int cpr = C / V;  // chunks per row
-    for (int idx = tid; idx < R * cpr; idx += NTH) {
-        const int r = idx / cpr, c = (idx - r * cpr) * V;
+    constexpr int V = 16 / (int)sizeof(E), CPR = C / V;  // elements per chunk, chunks per row
+    for (int idx = tid; idx < R * CPR; idx += NTH) {
+        const int r = idx / CPR, c = (idx % CPR) * V;
         float v[V];
         if (r < nr && c < nc) {
             E e[V];
@@ -217,20 +208,19 @@ template <typename T, int S, bool LAST> struct LBwd {
         const int m = dm.m, b = dm.b, n = dm.n, d = dm.d;
         const int64_t bh = blockIdx.x / b;
         const int j = blockIdx.x % b;
-        const int MB = up16(m), DB = up16(d);
         const int ml = (n - j + b - 1) / b;  // rows l with l*b + j < n
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * kD, coff = bh * Np;
         float *Qb = lds, *aL = Qb + S * kLd, *Lm = aL + S * kLd, *dL = Lm + S * kLd, *X = dL + S * kLd,
               *G = X + S * kLd;
         float *cL = G + S * kLd, *dcR = cL + S;
 
-        load_tile<T, NTH>(Qb, MB, DB, ml, d, [&](int l) { return p.q + toff + ((int64_t)l * b + j) * d; }, tid);
-        load_tile<T, NTH>(aL, MB, DB, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * kD; }, tid);
+        load_tile<T, NTH, S, kD>(Qb, ml, d, [&](int l) { return p.q + toff + ((int64_t)l * b + j) * d; }, tid);
+        load_tile<T, NTH, S, kD>(aL, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * kD; }, tid);
         if constexpr (LAST) {
-            load_tile<T, NTH>(X, MB, DB, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * kD; }, tid);
-            load_tile<T, NTH>(G, MB, DB, ml, d, [&](int l) { return p.dout + toff + ((int64_t)l * b + j) * d; }, tid);
+            load_tile<T, NTH, S, kD>(X, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * kD; }, tid);
+            load_tile<T, NTH, S, kD>(G, ml, d, [&](int l) { return p.dout + toff + ((int64_t)l * b + j) * d; }, tid);
         } else {
-            load_tile<float, NTH>(X, MB, DB, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * kD; }, tid);
+            load_tile<float, NTH, S, kD>(X, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * kD; }, tid);
         }
         for (int k = tid; k < S; k += NTH) {
             cL[k] = k < m ? p.cL[coff + (int64_t)k * b + j] : 0.f;
@@ -239,53 +229,53 @@ template <typename T, int S, bool LAST> struct LBwd {
         __syncthreads();
 
         // unnormalised scores <Qbar[l], alpha_L[k]>
-        gemm<W>(MB, MB, DB, wave, lane, to_lds(Lm), pair<false, true>(Qb, aL));
+        gemm<W, S, S, kD>(wave, lane, to_lds(Lm), pair<false, true>(Qb, aL));
         __syncthreads();
         // L[l][k] = softmax_k (s score - c_L[k]): one wave per row l, lane k
-        for (int l = wave; l < MB; l += W) {
+        for (int l = wave; l < S; l += W) {
             const int k = lane;
             if (l >= m) {
-                if (k < MB) Lm[l * kLd + k] = 0.f;
+                if (k < S) Lm[l * kLd + k] = 0.f;
                 continue;
             }
             const float z = k < m ? dm.s * Lm[l * kLd + k] - cL[k] : -INFINITY;
             const float mx = wave_max(z);
             const float e = k < m ? __expf(z - mx) : 0.f;
             const float sum = wave_sum(e);
-            if (k < MB) Lm[l * kLd + k] = e / sum;
+            if (k < S) Lm[l * kLd + k] = e / sum;
         }
         __syncthreads();
 
         if constexpr (LAST) {
             // dL = dO Y^T;  dY = L^T dO (to the workspace, read by r_bwd of this step)
-            gemm<W>(MB, MB, DB, wave, lane, to_lds(dL), pair<false, true>(G, X));
+            gemm<W, S, S, kD>(wave, lane, to_lds(dL), pair<false, true>(G, X));
             float *dY = p.dY + soff + (int64_t)j * m * kD;
-            gemm<W>(
-                MB, DB, MB, wave, lane,
+            gemm<W, S, kD, S>(
+                wave, lane,
                 [&](int k, int e, float v) {
                     if (k < m && e < d) dY[(int64_t)k * kD + e] = v;
                 },
                 pair<true, false>(Lm, G));
         } else {
             // dL = Qbar d alpha_R'^T (+ d c_R' below);  G = L d alpha_R' (the alpha_R' term of dQbar)
-            gemm<W>(MB, MB, DB, wave, lane, to_lds(dL), pair<false, true>(Qb, X));
-            gemm<W>(MB, DB, MB, wave, lane, to_lds(G), pair<false, false>(Lm, X));
+            gemm<W, S, S, kD>(wave, lane, to_lds(dL), pair<false, true>(Qb, X));
+            gemm<W, S, kD, S>(wave, lane, to_lds(G), pair<false, false>(Lm, X));
         }
         __syncthreads();
         // dW = s L (dL - <L, dL>), in place of dL
-        for (int l = wave; l < MB; l += W) {
+        for (int l = wave; l < S; l += W) {
             const int k = lane;
-            const float pk = k < MB ? Lm[l * kLd + k] : 0.f;
-            const float w = k < MB ? dL[l * kLd + k] + dcR[k] : 0.f;
+            const float pk = k < S ? Lm[l * kLd + k] : 0.f;
+            const float w = k < S ? dL[l * kLd + k] + dcR[k] : 0.f;
             const float dot = wave_sum(pk * w);
-            if (k < MB) dL[l * kLd + k] = dm.s * pk * (w - dot);
+            if (k < S) dL[l * kLd + k] = dm.s * pk * (w - dot);
         }
         __syncthreads();
 
         // dQ rows l*b + j: dW alpha_L (+ L d alpha_R')
         float *dQ = p.dQ + toff + (int64_t)j * d;
-        gemm<W>(
-            MB, DB, MB, wave, lane,
+        gemm<W, S, kD, S>(
+            wave, lane,
             [&](int l, int e, float v) {
                 if (l < ml && e < d) {
                     float *o = dQ + (int64_t)l * b * d + e;
@@ -299,8 +289,8 @@ template <typename T, int S, bool LAST> struct LBwd {
             pair<false, false>(dL, aL));
         // d alpha_L[k] = dW^T Qbar
         float *daL = p.daL + soff + (int64_t)j * m * kD;
-        gemm<W>(
-            MB, DB, MB, wave, lane,
+        gemm<W, S, kD, S>(
+            wave, lane,
             [&](int k, int e, float v) {
                 if (k < m && e < d) daL[(int64_t)k * kD + e] = v;
             },
@@ -308,7 +298,7 @@ template <typename T, int S, bool LAST> struct LBwd {
         // d c_L[k] = -(1/s) sum_l dW[l][k]
         for (int k = tid; k < m; k += NTH) {
             float cs = 0.f;
-            for (int l = 0; l < MB; ++l) cs += dL[l * kLd + k];
+            for (int l = 0; l < S; ++l) cs += dL[l * kLd + k];
             p.dcL[coff + (int64_t)j * m + k] = -cs / dm.s;
         }
     }
@@ -329,7 +319,6 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         const int m = dm.m, b = dm.b, n = dm.n, d = dm.d;
         const int64_t bh = blockIdx.x / m;
         const int k = blockIdx.x % m;
-        const int BB = up16(b), DB = up16(d);
         const int kv = min(b, n - k * b);  // real keys (and query rows) of block k
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * kD, coff = bh * Np;
         const int64_t row0 = (int64_t)k * b;  // first row of block k
@@ -337,16 +326,16 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         float *Vb = dR + S * kLd, *dYt = Vb + S * kLd;  // LAST only
         float *cR = lds + TILES * S * kLd, *dcL = cR + S;
 
-        load_tile<T, NTH>(Kb, BB, DB, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
+        load_tile<T, NTH, S, kD>(Kb, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
         if constexpr (FIRST) {
-            load_tile<T, NTH>(aR, BB, DB, kv, d, [&](int jj) { return p.q + toff + (row0 + jj) * d; }, tid);
+            load_tile<T, NTH, S, kD>(aR, kv, d, [&](int jj) { return p.q + toff + (row0 + jj) * d; }, tid);
         } else {
-            load_tile<T, NTH>(aR, BB, DB, b, d, [&](int jj) { return p.aR + soff + (row0 + jj) * kD; }, tid);
+            load_tile<T, NTH, S, kD>(aR, b, d, [&](int jj) { return p.aR + soff + (row0 + jj) * kD; }, tid);
         }
-        load_tile<float, NTH>(dA, BB, DB, b, d, [&](int jj) { return p.daL + soff + ((int64_t)jj * m + k) * kD; }, tid);
+        load_tile<float, NTH, S, kD>(dA, b, d, [&](int jj) { return p.daL + soff + ((int64_t)jj * m + k) * kD; }, tid);
         if constexpr (LAST) {
-            load_tile<T, NTH>(Vb, BB, DB, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
-            load_tile<float, NTH>(dYt, BB, DB, b, d, [&](int jj) { return p.dY + soff + ((int64_t)jj * m + k) * kD; },
+            load_tile<T, NTH, S, kD>(Vb, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
+            load_tile<float, NTH, S, kD>(dYt, b, d, [&](int jj) { return p.dY + soff + ((int64_t)jj * m + k) * kD; },
                              tid);
         }
         for (int jj = tid; jj < S; jj += NTH) {
@@ -356,18 +345,18 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         __syncthreads();
 
         // unnormalised scores <alpha_R[j], Kbar[i]>;  dR = d alpha_L Kbar^T (+ dY Vbar^T)
-        gemm<W>(BB, BB, DB, wave, lane, to_lds(Rm), pair<false, true>(aR, Kb));
+        gemm<W, S, S, kD>(wave, lane, to_lds(Rm), pair<false, true>(aR, Kb));
         if constexpr (LAST) {
-            gemm<W>(BB, BB, DB, wave, lane, to_lds(dR), pair<false, true>(dA, Kb), pair<false, true>(dYt, Vb));
+            gemm<W, S, S, kD>(wave, lane, to_lds(dR), pair<false, true>(dA, Kb), pair<false, true>(dYt, Vb));
         } else {
-            gemm<W>(BB, BB, DB, wave, lane, to_lds(dR), pair<false, true>(dA, Kb));
+            gemm<W, S, S, kD>(wave, lane, to_lds(dR), pair<false, true>(dA, Kb));
         }
         __syncthreads();
         // per row j (one wave, lane i): R, then dZ scaled by s / c_R[j] in place of dR
-        for (int jj = wave; jj < BB; jj += W) {
+        for (int jj = wave; jj < S; jj += W) {
             const int i = lane;
             if (jj >= b) {
-                if (i < BB) Rm[jj * kLd + i] = dR[jj * kLd + i] = 0.f;
+                if (i < S) Rm[jj * kLd + i] = dR[jj * kLd + i] = 0.f;
                 continue;
             }
             const float sc = dm.s / cR[jj];
@@ -382,7 +371,7 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
             const float dot = wave_sum(r * dr);
             const float dz = r * (dr - dot);
             const float dzlog = wave_sum(dz * logr);
-            if (i < BB) {
+            if (i < S) {
                 Rm[jj * kLd + i] = r;
                 dR[jj * kLd + i] = dz * sc;
             }
@@ -394,16 +383,16 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         if constexpr (FIRST) {
             const float *dQ = p.dQ + toff + row0 * d;
             T *dq = p.dq + toff + row0 * d;
-            gemm<W>(
-                BB, DB, BB, wave, lane,
+            gemm<W, S, kD, S>(
+                wave, lane,
                 [&](int jj, int e, float v) {
                     if (jj < kv && e < d) dq[(int64_t)jj * d + e] = static_cast<T>(dQ[(int64_t)jj * d + e] + v);
                 },
                 pair<false, false>(dR, Kb));
         } else {
             float *daR = p.daR + soff + row0 * kD;
-            gemm<W>(
-                BB, DB, BB, wave, lane,
+            gemm<W, S, kD, S>(
+                wave, lane,
                 [&](int jj, int e, float v) {
                     if (jj < b && e < d) daR[(int64_t)jj * kD + e] = v;
                 },
@@ -413,8 +402,8 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         {
             float *dK = p.dK + toff + row0 * d;
             T *dk = p.dk + toff + row0 * d;
-            gemm<W>(
-                BB, DB, BB, wave, lane,
+            gemm<W, S, kD, S>(
+                wave, lane,
                 [&](int i, int e, float v) {
                     if (i < kv && e < d) {
                         const int64_t o = (int64_t)i * d + e;
@@ -431,8 +420,8 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         // dVbar[i] = sum_j R[j][i] dY[j]
         if constexpr (LAST) {
             T *dv = p.dv + toff + row0 * d;
-            gemm<W>(
-                BB, DB, BB, wave, lane,
+            gemm<W, S, kD, S>(
+                wave, lane,
                 [&](int i, int e, float v) {
                     if (i < kv && e < d) dv[(int64_t)i * d + e] = static_cast<T>(v);
                 },
