@@ -77,12 +77,14 @@ typedef enum {
  * Asynchronous on `stream`: returns after enqueueing, with no host
  * synchronisation.  Arguments are checked before any HIP call; on MA_EINVAL or
  * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  Path 1 (see
- * monarch_attn_set_path) uses one device workspace per device (3 m b D
- * elements plus 2 m b floats per head), grown with hipMalloc on the first call
- * that needs more; calls on different streams of one device must not overlap
- * (they share it).  After
- * the launches hipGetLastError is checked (MA_EHIP).  The message of the last
- * failure on the calling thread is returned by monarch_attn_last_error().
+ * monarch_attn_set_path) uses a device workspace (3 m b D elements plus 2 m b
+ * floats per head) owned by the library, one per (device, stream): calls on
+ * different streams may run concurrently, and calls on one stream (from any
+ * host thread) are enqueued one whole call at a time.  A stream's workspace
+ * is grown with hipMalloc by the first call that needs more, after waiting
+ * for that stream.  After the launches hipGetLastError is checked (MA_EHIP).
+ * The message of the last failure on the calling thread is returned by
+ * monarch_attn_last_error().
  */
 int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out,
                      int64_t B, int64_t H, int64_t N, int64_t d,
@@ -153,8 +155,9 @@ int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *ou
  * asynchronously.  The arithmetic of the reverse sweep is fp32 (the states
  * of the recomputed forward pass are in the element type, as in
  * monarch_attn_fwd), and the result is deterministic (no atomics).
- * Workspace: monarch_attn_bwd_workspace_bytes(), in the same per-device
- * buffer as monarch_attn_fwd (same rules).  Errors as monarch_attn_fwd.
+ * Workspace: monarch_attn_bwd_workspace_bytes(), in the same per-(device,
+ * stream) buffer as monarch_attn_fwd (same rules).  Errors as
+ * monarch_attn_fwd.
  */
 int monarch_attn_bwd(const void *q, const void *k, const void *v, const void *dout,
                      void *dq, void *dk, void *dv,
@@ -186,7 +189,9 @@ int monarch_attn_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, in
 size_t monarch_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,
                                     int64_t m, int64_t b, int32_t T, int32_t dtype);
 
-/* Free the workspace of the current device.  Must not race a running call. */
+/* Free the workspaces of the current device (all streams).  Waits for calls
+ * being enqueued and for the device to go idle first, so it may be called
+ * while other threads use the library; their next call allocates again. */
 int monarch_attn_release_workspace(void);
 
 /*

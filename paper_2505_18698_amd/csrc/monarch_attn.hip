@@ -8,7 +8,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <mutex>
+#include <unordered_map>
 
 #include "host_common.hpp"
 
@@ -74,10 +76,21 @@ size_t workspace_bytes(int64_t BH, int64_t Np, int64_t d, int32_t dtype)
     return 3 * st + 2 * cs;
 }
 
+// The workspace of one (device, stream): calls on one stream are ordered by
+// it, so they can share one; calls on different streams get their own.  `mu`
+// is held by a call from acquiring the workspace to its last launch, so that
+// the launches of two calls on one stream never interleave.
+struct Workspace {
+    std::mutex mu;
+    void *ptr = nullptr;
+    size_t bytes = 0;
+};
+
 struct Device {
-    void *ws = nullptr;
-    size_t ws_bytes = 0;
     int num_cus = 0;  // 0: not queried yet
+    // Entries are never erased (a caller may be waiting on an entry's mutex);
+    // release only frees their memory.
+    std::unordered_map<hipStream_t, std::unique_ptr<Workspace>> ws;
 };
 
 constexpr int kMaxDevices = 64;
@@ -108,28 +121,35 @@ int current_device(int &dev, int &num_cus)
     return MA_OK;
 }
 
-// The workspace of device `dev`, grown with hipMalloc to at least `need` bytes
-// (after a device synchronisation, since earlier calls may still use it).
-int acquire_workspace(int dev, size_t need, char **base)
+// The workspace of (dev, stream), locked into `hold` for the caller and grown
+// with hipMalloc to at least `need` bytes.  Growing first waits for the
+// stream, whose earlier calls may still use the old buffer.
+int acquire_workspace(int dev, hipStream_t stream, size_t need, char **base, std::unique_lock<std::mutex> &hold)
 {
-    std::lock_guard<std::mutex> lock(g_dev_mutex);
-    Device &D = g_dev[dev];
-    if (D.ws_bytes < need) {
-        if (D.ws) {
-            if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
-            (void)hipFree(D.ws);
-            D.ws = nullptr;
-            D.ws_bytes = 0;
+    Workspace *w;
+    {
+        std::lock_guard<std::mutex> lock(g_dev_mutex);
+        std::unique_ptr<Workspace> &slot = g_dev[dev].ws[stream];
+        if (!slot) slot.reset(new Workspace);
+        w = slot.get();
+    }
+    hold = std::unique_lock<std::mutex>(w->mu);
+    if (w->bytes < need) {
+        if (w->ptr) {
+            if (hipStreamSynchronize(stream) != hipSuccess) return fail(MA_EHIP, "hipStreamSynchronize failed");
+            (void)hipFree(w->ptr);
+            w->ptr = nullptr;
+            w->bytes = 0;
         }
         void *p = nullptr;
         if (hipMalloc(&p, need) != hipSuccess) {
             (void)hipGetLastError();
             return fail(MA_ENOMEM, "hipMalloc of %zu workspace bytes failed", need);
         }
-        D.ws = p;
-        D.ws_bytes = need;
+        w->ptr = p;
+        w->bytes = need;
     }
-    *base = (char *)D.ws;
+    *base = (char *)w->ptr;
     return MA_OK;
 }
 
@@ -161,12 +181,14 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, obj};
     int dev = 0, num_cus = 0;
     if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
+    std::unique_lock<std::mutex> ws_hold;  // the stream's workspace, held until the launches are enqueued
     const bool states = !uses_fused(path, dtype, d, m, b);  // the fused kernel keeps its states in LDS
     const size_t obj_part_bytes = obj ? align_up((size_t)BH * T * b * sizeof(float)) : 0;
     if (states || obj) {
         const size_t state_ws = states ? workspace_bytes(BH, m * b, d, dtype) : 0;
         char *base = nullptr;
-        if ((rc = acquire_workspace(dev, state_ws + obj_part_bytes, &base)) != MA_OK) return rc;
+        if ((rc = acquire_workspace(dev, (hipStream_t)stream, state_ws + obj_part_bytes, &base, ws_hold)) != MA_OK)
+            return rc;
         if (states) {
             bufs.aR = base;
             bufs.aL = base + st;
@@ -256,7 +278,8 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
     if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
     const BwdLayout lay = bwd_layout(BH, N, d, m, b, T, dtype);
     char *base = nullptr;
-    if ((rc = acquire_workspace(dev, lay.total(), &base)) != MA_OK) return rc;
+    std::unique_lock<std::mutex> ws_hold;  // the stream's workspace, held until the launches are enqueued
+    if ((rc = acquire_workspace(dev, (hipStream_t)stream, lay.total(), &base, ws_hold)) != MA_OK) return rc;
     BwdCallBufs bufs{};
     bufs.q = q, bufs.k = k, bufs.v = v, bufs.dout = dout, bufs.dq = dq, bufs.dk = dk, bufs.dv = dv;
     char *p = base;
@@ -321,12 +344,19 @@ int monarch_attn_release_workspace(void)
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return fail(MA_EHIP, "hipGetDevice failed");
     std::lock_guard<std::mutex> lock(g_dev_mutex);
     Device &D = g_dev[dev];
-    if (D.ws) {
-        if (hipDeviceSynchronize() != hipSuccess || hipFree(D.ws) != hipSuccess)
-            return fail(MA_EHIP, "freeing the workspace failed");
+    bool synced = false;
+    for (auto &entry : D.ws) {
+        Workspace &w = *entry.second;
+        std::lock_guard<std::mutex> wl(w.mu);
+        if (!w.ptr) continue;
+        if (!synced) {
+            if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
+            synced = true;
+        }
+        if (hipFree(w.ptr) != hipSuccess) return fail(MA_EHIP, "freeing the workspace failed");
+        w.ptr = nullptr;
+        w.bytes = 0;
     }
-    D.ws = nullptr;
-    D.ws_bytes = 0;
     return MA_OK;
 }
 

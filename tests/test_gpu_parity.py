@@ -497,3 +497,46 @@ def test_exact_attention_n16384_sampled_rows(lib):
     for hi, h in enumerate(heads):
         want = _lse_rows(q[0, h], k[0, h], rows)
         assert np.abs(lse[0, h, rows] - want).max() <= 1e-4 * np.abs(want).max()
+
+
+def test_concurrent_streams_get_separate_workspaces(lib):
+    """Two host threads, each on its own stream, run half-step forward calls of
+    different shapes at the same time: with one workspace per stream neither
+    corrupts the other's states."""
+    import threading
+
+    import torch
+
+    prev = lib.monarch_attn_set_path(lib.PATH_HALF_STEPS)
+    try:
+        shapes = [(2, 4, 32, 32, 64, 2), (1, 8, 64, 64, 64, 3)]
+        inputs, refs = [], []
+        for B, H, m, b, d, T in shapes:
+            q, k, v = si.random_qkv(B, H, m * b, d, "bf16", seed=m, scale=1.5)
+            inputs.append([torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (q, k, v)])
+            refs.append(oracle.monarch_attention(q, k, v, m, b, T))
+        outs = [torch.full_like(t[0], float("nan")) for t in inputs]
+        streams = [torch.cuda.Stream() for _ in shapes]
+        errors = []
+
+        def worker(i):
+            try:
+                B, H, m, b, d, T = shapes[i]
+                with torch.cuda.stream(streams[i]):
+                    for _ in range(20):
+                        lib.monarch_attn_fwd(*inputs[i], outs[i], m, b, T, stream=streams[i])
+                streams[i].synchronize()
+            except Exception as e:  # reported below
+                errors.append(e)
+
+        threads = [threading.Thread(target=worker, args=(i,)) for i in range(len(shapes))]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join()
+        assert not errors, errors
+        torch.cuda.synchronize()
+        for o, ref in zip(outs, refs):
+            check(o.double().cpu().numpy(), ref, "bf16", "concurrent streams")
+    finally:
+        lib.monarch_attn_set_path(prev)
