@@ -148,7 +148,7 @@ int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *ou
  *                 16-byte aligned, overlapping neither each other nor the
  *                 inputs.  Fully overwritten.  All owned by the caller.
  * B, H, N, d, m, b, T, dtype, stream : as monarch_attn_fwd, and in addition
- *                 m, b <= 64, d <= 64 and T <= 32 (else MA_EUNSUPPORTED).
+ *                 d <= 64 and T <= 32 (else MA_EUNSUPPORTED).
  *
  * Runs the forward half-steps again, keeping the states of every step, then
  * one launch per half-step in reverse order; all of it on `stream`,

@@ -29,7 +29,10 @@
 //       d alpha_R is added to dQ (alpha_R = the rows of Q) and c_R is constant.
 //
 // Every unit keeps its matrices in fp32 LDS tiles and runs every product on
-// v_mfma_f32_16x16x4f32.  The gradients of the states and the dQ, dK
+// v_mfma_f32_16x16x4f32.  Up to 64 rows per side a unit holds all of them at
+// once; at 128 (m or b up to 128) it walks its own rows (j in r_bwd, l in
+// l_bwd) in chunks of 32, the sums over those rows (dK, dV, dY, d alpha_L,
+// d c_L) accumulating in registers.  The gradients of the states and the dQ, dK
 // accumulators are fp32 in the workspace.  Within a launch the units write
 // disjoint rows, and launches that touch the same rows are ordered on the
 // stream, so read-modify-writes need no atomics and the result is
@@ -52,19 +55,26 @@ template <typename T> struct BwdBufs {
 };
 
 struct BwdDims {
-    int m, b, n, d;  // as in the forward; here m, b <= 64 and d <= 64 (states of width 64)
+    int m, b, n, d;  // as in the forward; here m, b <= 128 and d <= 64 (states of width 64)
     float s;         // 1/sqrt(d)
 };
 
 namespace bwd {
 
 constexpr int kD = 64;   // row width of the states (the forward's tile width for d <= 64)
-constexpr int kLd = 84;  // row stride (floats) of the LDS tiles: 16-byte rows, both access orders conflict-free
+constexpr int kLd = 84;  // row stride (floats) of 64-wide LDS tiles: 16-byte rows, 20 banks apart
 
-// Waves per workgroup for tiles of S rows: one 16 x 16 output tile of an
-// S x S product per wave at S = 64.
-template <int S> struct Waves {
-    static constexpr int value = S / 4;
+// Shape of the units for tiles of S rows (S = 16, 32, 64 or 128 >= m, b):
+// W waves (one 16 x 16 output tile of the widest product each), rows walked
+// in chunks of C, and the row stride LS of the C x S score tiles (16-byte
+// rows, 20 banks apart like kLd).
+template <int S> struct Geo {
+    static constexpr int W = S >= 64 ? 16 : S / 4;
+    static constexpr int NTH = 64 * W;
+    static constexpr int C = S > 64 ? 32 : S;
+    static constexpr int NCH = S / C;
+    static constexpr int LS = S > 64 ? 148 : kLd;
+    static constexpr int CPL = S > 64 ? S / 64 : 1;  // score columns per lane in the row passes
 };
 
 // Reductions over the 64 lanes with no LDS round trip: DPP within rows of 16
@@ -96,7 +106,7 @@ __device__ inline float wave_max(float x)
     return wave_xor_max<32>(x);
 }
 
-// Operands of a product, as LDS tiles (row stride kLd):
+// Operands of a product, as LDS tiles with row strides LA, LB:
 //   A(r, k) = TA ? A[k][r] : A[r][k],   B(k, n) = TB ? B[n][k] : B[k][n].
 // MFMA step s of a 16-long chunk k0 hands lane group g = lane/16 the index
 // k0 + 4g + s, so a lane reads four consecutive k at once: one 16-byte read
@@ -104,20 +114,20 @@ __device__ inline float wave_max(float x)
 // scalar reads otherwise.  The contraction length is a compile-time constant:
 // the loop unrolls, every read is the lane's base address plus an immediate
 // offset, and all reads can be issued ahead of the MFMAs.
-template <bool TA, bool TB> struct Pair {
+template <bool TA, bool TB, int LA, int LB> struct Pair {
     const float *A, *B;
 
     // acc += sum_{k < K} A(r, k) B(k, n)
     template <int K> __device__ void accumulate(f32x4 &acc, int r, int n, int g) const
     {
-        const float *pa = TA ? A + 4 * g * kLd + r : A + r * kLd + 4 * g;
-        const float *pb = TB ? B + n * kLd + 4 * g : B + 4 * g * kLd + n;
+        const float *pa = TA ? A + 4 * g * LA + r : A + r * LA + 4 * g;
+        const float *pb = TB ? B + n * LB + 4 * g : B + 4 * g * LB + n;
 #pragma unroll
         for (int k0 = 0; k0 < K; k0 += 16) {
             float a[4], b[4];
             if constexpr (TA) {
 #pragma unroll
-                for (int s = 0; s < 4; ++s) a[s] = pa[(k0 + s) * kLd];
+                for (int s = 0; s < 4; ++s) a[s] = pa[(k0 + s) * LA];
             } else {
                 const f32x4 v = *reinterpret_cast<const f32x4 *>(pa + k0);
 #pragma unroll
@@ -129,13 +139,19 @@ template <bool TA, bool TB> struct Pair {
                 for (int s = 0; s < 4; ++s) b[s] = v[s];
             } else {
 #pragma unroll
-                for (int s = 0; s < 4; ++s) b[s] = pb[(k0 + s) * kLd];
+                for (int s = 0; s < 4; ++s) b[s] = pb[(k0 + s) * LB];
             }
 #pragma unroll
             for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
         }
     }
 };
+
+template <bool TA, bool TB, int LA = kLd, int LB = kLd>
+__device__ inline Pair<TA, TB, LA, LB> pair(const float *A, const float *B)
+{
+    return Pair<TA, TB, LA, LB>{A, B};
+}
 
 // out(r, c) = sum over the pairs of A(r, :) B(:, c) for r < M, c < N, with
 // contraction K (all multiples of 16, fixed at compile time: the tiles are
@@ -157,14 +173,50 @@ __device__ inline void gemm(int wave, int lane, Store &&st, const P &...pairs)
     }
 }
 
-template <bool TA, bool TB> __device__ inline Pair<TA, TB> pair(const float *A, const float *B)
-{
-    return Pair<TA, TB>{A, B};
-}
+// An M x N product accumulated over several calls (one per row chunk) in the
+// registers of the waves that own its output tiles: the same tile-to-wave
+// assignment as gemm, each wave holding SLOTS tiles.
+template <int W, int M, int N> struct Acc {
+    static constexpr int TN = N / 16, TILES = (M / 16) * TN, SLOTS = (TILES + W - 1) / W;
+    f32x4 v[SLOTS];
 
-__device__ inline auto to_lds(float *t)
+    __device__ void zero()
+    {
+#pragma unroll
+        for (int s = 0; s < SLOTS; ++s) v[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    template <int K, typename... P> __device__ void add(int wave, int lane, const P &...pairs)
+    {
+        const int g = lane >> 4, c = lane & 15;
+#pragma unroll
+        for (int s = 0; s < SLOTS; ++s) {
+            const int t = wave + s * W;
+            if (t < TILES) {
+                const int r0 = (t / TN) * 16, c0 = (t % TN) * 16;
+                (pairs.template accumulate<K>(v[s], r0 + c, c0 + c, g), ...);
+            }
+        }
+    }
+
+    template <typename Store> __device__ void store(int wave, int lane, Store &&st) const
+    {
+        const int g = lane >> 4, c = lane & 15;
+#pragma unroll
+        for (int s = 0; s < SLOTS; ++s) {
+            const int t = wave + s * W;
+            if (t < TILES) {
+                const int r0 = (t / TN) * 16, c0 = (t % TN) * 16;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) st(r0 + 4 * g + q, c0 + c, v[s][q]);
+            }
+        }
+    }
+};
+
+template <int LD> __device__ inline auto to_lds(float *t)
 {
-    return [t](int r, int c, float v) { t[r * kLd + c] = v; };
+    return [t](int r, int c, float v) { t[r * LD + c] = v; };
 }
 
 // Rows r < R and columns c < C (compile-time extents, C <= 64 a multiple of
@@ -196,11 +248,12 @@ __device__ inline void load_tile(float *dst, int nr, int nc, Src src, int tid)
 
 // ---------------------------------------------------------------------------------------
 // The L update of class j of step t undone (LAST: t = T, the update that also
-// produced O).  S: rows of the tiles (16, 32 or 64, >= m).
+// produced O).  S >= m; query rows l in chunks of C.
 // ---------------------------------------------------------------------------------------
 template <typename T, int S, bool LAST> struct LBwd {
-    static constexpr int W = Waves<S>::value, NTH = 64 * W;
-    static constexpr int LDS_FLOATS = 6 * S * kLd + 2 * S;
+    using G_ = Geo<S>;
+    static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL;
+    static constexpr int LDS_FLOATS = 2 * S * kLd + 2 * C * kLd + 2 * C * LS + 2 * S;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
     {
@@ -210,108 +263,143 @@ template <typename T, int S, bool LAST> struct LBwd {
         const int j = blockIdx.x % b;
         const int ml = (n - j + b - 1) / b;  // rows l with l*b + j < n
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * kD, coff = bh * Np;
-        float *Qb = lds, *aL = Qb + S * kLd, *Lm = aL + S * kLd, *dL = Lm + S * kLd, *X = dL + S * kLd,
-              *G = X + S * kLd;
-        float *cL = G + S * kLd, *dcR = cL + S;
+        // whole-unit tiles (rows k): alpha_L[j][k]; Y[j][k] (LAST) or d alpha_R'[k][j]
+        float *aL = lds, *X = aL + S * kLd;
+        // chunk tiles (rows l of the chunk): Qbar, dO (LAST) or L d alpha_R', L, dL then dW
+        float *Qb = X + S * kLd, *G = Qb + C * kLd, *Lm = G + C * kLd, *dL = Lm + C * LS;
+        float *cL = dL + C * LS, *dcR = cL + S;
 
-        load_tile<T, NTH, S, kD>(Qb, ml, d, [&](int l) { return p.q + toff + ((int64_t)l * b + j) * d; }, tid);
         load_tile<T, NTH, S, kD>(aL, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * kD; }, tid);
         if constexpr (LAST) {
             load_tile<T, NTH, S, kD>(X, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * kD; }, tid);
-            load_tile<T, NTH, S, kD>(G, ml, d, [&](int l) { return p.dout + toff + ((int64_t)l * b + j) * d; }, tid);
         } else {
-            load_tile<float, NTH, S, kD>(X, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * kD; }, tid);
+            load_tile<float, NTH, S, kD>(X, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * kD; },
+                                         tid);
         }
         for (int k = tid; k < S; k += NTH) {
             cL[k] = k < m ? p.cL[coff + (int64_t)k * b + j] : 0.f;
             dcR[k] = (!LAST && k < m) ? p.dcR[coff + (int64_t)k * b + j] : 0.f;
         }
-        __syncthreads();
-
-        // unnormalised scores <Qbar[l], alpha_L[k]>
-        gemm<W, S, S, kD>(wave, lane, to_lds(Lm), pair<false, true>(Qb, aL));
-        __syncthreads();
-        // L[l][k] = softmax_k (s score - c_L[k]): one wave per row l, lane k
-        for (int l = wave; l < S; l += W) {
-            const int k = lane;
-            if (l >= m) {
-                if (k < S) Lm[l * kLd + k] = 0.f;
-                continue;
-            }
-            const float z = k < m ? dm.s * Lm[l * kLd + k] - cL[k] : -INFINITY;
-            const float mx = wave_max(z);
-            const float e = k < m ? __expf(z - mx) : 0.f;
-            const float sum = wave_sum(e);
-            if (k < S) Lm[l * kLd + k] = e / sum;
-        }
-        __syncthreads();
-
-        if constexpr (LAST) {
-            // dL = dO Y^T;  dY = L^T dO (to the workspace, read by r_bwd of this step)
-            gemm<W, S, S, kD>(wave, lane, to_lds(dL), pair<false, true>(G, X));
-            float *dY = p.dY + soff + (int64_t)j * m * kD;
-            gemm<W, S, kD, S>(
-                wave, lane,
-                [&](int k, int e, float v) {
-                    if (k < m && e < d) dY[(int64_t)k * kD + e] = v;
-                },
-                pair<true, false>(Lm, G));
-        } else {
-            // dL = Qbar d alpha_R'^T (+ d c_R' below);  G = L d alpha_R' (the alpha_R' term of dQbar)
-            gemm<W, S, S, kD>(wave, lane, to_lds(dL), pair<false, true>(Qb, X));
-            gemm<W, S, kD, S>(wave, lane, to_lds(G), pair<false, false>(Lm, X));
-        }
-        __syncthreads();
-        // dW = s L (dL - <L, dL>), in place of dL
-        for (int l = wave; l < S; l += W) {
-            const int k = lane;
-            const float pk = k < S ? Lm[l * kLd + k] : 0.f;
-            const float w = k < S ? dL[l * kLd + k] + dcR[k] : 0.f;
-            const float dot = wave_sum(pk * w);
-            if (k < S) dL[l * kLd + k] = dm.s * pk * (w - dot);
-        }
-        __syncthreads();
-
-        // dQ rows l*b + j: dW alpha_L (+ L d alpha_R')
+        Acc<W, S, kD> daL, dY;  // sums over all rows l
+        daL.zero();
+        if constexpr (LAST) dY.zero();
+        float dcl = 0.f;  // thread k < S: sum over l of dW[l][k]
         float *dQ = p.dQ + toff + (int64_t)j * d;
-        gemm<W, S, kD, S>(
-            wave, lane,
-            [&](int l, int e, float v) {
-                if (l < ml && e < d) {
-                    float *o = dQ + (int64_t)l * b * d + e;
-                    if constexpr (LAST) {
-                        *o = v;
-                    } else {
-                        *o += v + G[l * kLd + e];
-                    }
+
+        for (int ch = 0; ch < G_::NCH; ++ch) {
+            const int l0 = ch * C, lc = min(max(ml - l0, 0), C);  // live rows of the chunk
+            load_tile<T, NTH, C, kD>(Qb, lc, d, [&](int l) { return p.q + toff + ((int64_t)(l0 + l) * b + j) * d; },
+                                     tid);
+            if constexpr (LAST)
+                load_tile<T, NTH, C, kD>(
+                    G, lc, d, [&](int l) { return p.dout + toff + ((int64_t)(l0 + l) * b + j) * d; }, tid);
+            __syncthreads();
+
+            // unnormalised scores <Qbar[l], alpha_L[k]>
+            gemm<W, C, S, kD>(wave, lane, to_lds<LS>(Lm), pair<false, true>(Qb, aL));
+            __syncthreads();
+            // L[l][k] = softmax_k (s score - c_L[k]): one wave per row l, CPL columns k per lane
+            for (int l = wave; l < C; l += W) {
+                float* row = Lm + l * LS;
+                if (l0 + l >= m) {
+#pragma unroll
+                    for (int u = 0; u < CPL; ++u)
+                        if (lane + 64 * u < S) row[lane + 64 * u] = 0.f;
+                    continue;
                 }
-            },
-            pair<false, false>(dL, aL));
-        // d alpha_L[k] = dW^T Qbar
-        float *daL = p.daL + soff + (int64_t)j * m * kD;
-        gemm<W, S, kD, S>(
-            wave, lane,
-            [&](int k, int e, float v) {
-                if (k < m && e < d) daL[(int64_t)k * kD + e] = v;
-            },
-            pair<true, false>(dL, Qb));
-        // d c_L[k] = -(1/s) sum_l dW[l][k]
-        for (int k = tid; k < m; k += NTH) {
-            float cs = 0.f;
-            for (int l = 0; l < S; ++l) cs += dL[l * kLd + k];
-            p.dcL[coff + (int64_t)j * m + k] = -cs / dm.s;
+                float z[CPL], mx = -INFINITY;
+#pragma unroll
+                for (int u = 0; u < CPL; ++u) {
+                    const int k = lane + 64 * u;
+                    z[u] = k < m ? dm.s * row[k] - cL[k] : -INFINITY;
+                    mx = fmaxf(mx, z[u]);
+                }
+                mx = wave_max(mx);
+                float sum = 0.f;
+#pragma unroll
+                for (int u = 0; u < CPL; ++u) {
+                    z[u] = lane + 64 * u < m ? __expf(z[u] - mx) : 0.f;
+                    sum += z[u];
+                }
+                const float inv = 1.f / wave_sum(sum);
+#pragma unroll
+                for (int u = 0; u < CPL; ++u)
+                    if (lane + 64 * u < S) row[lane + 64 * u] = z[u] * inv;
+            }
+            __syncthreads();
+
+            if constexpr (LAST) {
+                // dL = dO Y^T;  dY += L^T dO
+                gemm<W, C, S, kD>(wave, lane, to_lds<LS>(dL), pair<false, true>(G, X));
+                dY.template add<C>(wave, lane, pair<true, false, LS, kLd>(Lm, G));
+            } else {
+                // dL = Qbar d alpha_R'^T (+ d c_R' below);  G = L d alpha_R' (the alpha_R' term of dQbar)
+                gemm<W, C, S, kD>(wave, lane, to_lds<LS>(dL), pair<false, true>(Qb, X));
+                gemm<W, C, kD, S>(wave, lane, to_lds<kLd>(G), pair<false, false, LS, kLd>(Lm, X));
+            }
+            __syncthreads();
+            // dW = s L (dL - <L, dL>), in place of dL
+            for (int l = wave; l < C; l += W) {
+                float *lr = Lm + l * LS, *wr = dL + l * LS;
+                float pk[CPL], w[CPL], dot = 0.f;
+#pragma unroll
+                for (int u = 0; u < CPL; ++u) {
+                    const int k = lane + 64 * u;
+                    pk[u] = k < S ? lr[k] : 0.f;
+                    w[u] = k < S ? wr[k] + dcR[k] : 0.f;
+                    dot += pk[u] * w[u];
+                }
+                dot = wave_sum(dot);
+#pragma unroll
+                for (int u = 0; u < CPL; ++u)
+                    if (lane + 64 * u < S) wr[lane + 64 * u] = dm.s * pk[u] * (w[u] - dot);
+            }
+            __syncthreads();
+
+            // dQ rows (l0 + l)*b + j: dW alpha_L (+ L d alpha_R')
+            gemm<W, C, kD, S>(
+                wave, lane,
+                [&](int l, int e, float v) {
+                    if (l < lc && e < d) {
+                        float *o = dQ + (int64_t)(l0 + l) * b * d + e;
+                        if constexpr (LAST) {
+                            *o = v;
+                        } else {
+                            *o += v + G[l * kLd + e];
+                        }
+                    }
+                },
+                pair<false, false, LS, kLd>(dL, aL));
+            // d alpha_L[k] += dW^T Qbar;  d c_L[k] += sum_l dW[l][k]
+            daL.template add<C>(wave, lane, pair<true, false, LS, kLd>(dL, Qb));
+            if (tid < S) {
+                for (int l = 0; l < C; ++l) dcl += dL[l * LS + tid];
+            }
+            __syncthreads();  // the next chunk overwrites the chunk tiles
         }
+
+        float *daLg = p.daL + soff + (int64_t)j * m * kD;
+        daL.store(wave, lane, [&](int k, int e, float v) {
+            if (k < m && e < d) daLg[(int64_t)k * kD + e] = v;
+        });
+        if constexpr (LAST) {
+            float *dYg = p.dY + soff + (int64_t)j * m * kD;
+            dY.store(wave, lane, [&](int k, int e, float v) {
+                if (k < m && e < d) dYg[(int64_t)k * kD + e] = v;
+            });
+        }
+        if (tid < m) p.dcL[coff + (int64_t)j * m + tid] = -dcl / dm.s;
     }
 };
 
 // ---------------------------------------------------------------------------------------
 // The R update of block k of step t undone (FIRST: t = 1, LAST: t = T).
-// S: rows of the tiles (16, 32 or 64, >= b).
+// S >= b; rows j in chunks of C.
 // ---------------------------------------------------------------------------------------
 template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
-    static constexpr int W = Waves<S>::value, NTH = 64 * W;
-    static constexpr int TILES = LAST ? 7 : 5;
-    static constexpr int LDS_FLOATS = TILES * S * kLd + 2 * S;
+    using G_ = Geo<S>;
+    static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL;
+    static constexpr int LDS_FLOATS = (LAST ? 2 : 1) * S * kLd + (LAST ? 3 : 2) * C * kLd + 2 * C * LS + 2 * C;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
     {
@@ -322,123 +410,158 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         const int kv = min(b, n - k * b);  // real keys (and query rows) of block k
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * kD, coff = bh * Np;
         const int64_t row0 = (int64_t)k * b;  // first row of block k
-        float *Kb = lds, *aR = Kb + S * kLd, *dA = aR + S * kLd, *Rm = dA + S * kLd, *dR = Rm + S * kLd;
-        float *Vb = dR + S * kLd, *dYt = Vb + S * kLd;  // LAST only
-        float *cR = lds + TILES * S * kLd, *dcL = cR + S;
+        // whole-unit tiles (rows i): Kbar, Vbar (LAST)
+        float *Kb = lds, *Vb = Kb + S * kLd;
+        // chunk tiles (rows j of the chunk): alpha_R, d alpha_L, dY (LAST), R, dR then dZ s / c_R
+        float *aR = Kb + (LAST ? 2 : 1) * S * kLd, *dA = aR + C * kLd, *dYt = dA + C * kLd;
+        float *Rm = dA + (LAST ? 2 : 1) * C * kLd, *dR = Rm + C * LS;
+        float *cR = dR + C * LS, *dcL = cR + C;
 
         load_tile<T, NTH, S, kD>(Kb, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
-        if constexpr (FIRST) {
-            load_tile<T, NTH, S, kD>(aR, kv, d, [&](int jj) { return p.q + toff + (row0 + jj) * d; }, tid);
-        } else {
-            load_tile<T, NTH, S, kD>(aR, b, d, [&](int jj) { return p.aR + soff + (row0 + jj) * kD; }, tid);
-        }
-        load_tile<float, NTH, S, kD>(dA, b, d, [&](int jj) { return p.daL + soff + ((int64_t)jj * m + k) * kD; }, tid);
-        if constexpr (LAST) {
-            load_tile<T, NTH, S, kD>(Vb, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
-            load_tile<float, NTH, S, kD>(dYt, b, d, [&](int jj) { return p.dY + soff + ((int64_t)jj * m + k) * kD; },
-                             tid);
-        }
-        for (int jj = tid; jj < S; jj += NTH) {
-            cR[jj] = (FIRST || jj >= b) ? 1.f : p.cR[coff + (int64_t)jj * m + k];
-            dcL[jj] = jj < b ? p.dcL[coff + (int64_t)jj * m + k] : 0.f;
-        }
-        __syncthreads();
+        if constexpr (LAST) load_tile<T, NTH, S, kD>(Vb, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
+        Acc<W, S, kD> dK, dV;  // sums over all rows j
+        dK.zero();
+        if constexpr (LAST) dV.zero();
 
-        // unnormalised scores <alpha_R[j], Kbar[i]>;  dR = d alpha_L Kbar^T (+ dY Vbar^T)
-        gemm<W, S, S, kD>(wave, lane, to_lds(Rm), pair<false, true>(aR, Kb));
-        if constexpr (LAST) {
-            gemm<W, S, S, kD>(wave, lane, to_lds(dR), pair<false, true>(dA, Kb), pair<false, true>(dYt, Vb));
-        } else {
-            gemm<W, S, S, kD>(wave, lane, to_lds(dR), pair<false, true>(dA, Kb));
-        }
-        __syncthreads();
-        // per row j (one wave, lane i): R, then dZ scaled by s / c_R[j] in place of dR
-        for (int jj = wave; jj < S; jj += W) {
-            const int i = lane;
-            if (jj >= b) {
-                if (i < S) Rm[jj * kLd + i] = dR[jj * kLd + i] = 0.f;
-                continue;
+        for (int ch = 0; ch < G_::NCH; ++ch) {
+            const int j0 = ch * C;
+            const int jb = min(max(b - j0, 0), C), jq = min(max(kv - j0, 0), C);  // live rows; rows of Q (t = 1)
+            if constexpr (FIRST) {
+                load_tile<T, NTH, C, kD>(aR, jq, d, [&](int jj) { return p.q + toff + (row0 + j0 + jj) * d; }, tid);
+            } else {
+                load_tile<T, NTH, C, kD>(aR, jb, d, [&](int jj) { return p.aR + soff + (row0 + j0 + jj) * kD; },
+                                         tid);
             }
-            const float sc = dm.s / cR[jj];
-            const bool live = i < kv;
-            const float z = live ? sc * Rm[jj * kLd + i] : -INFINITY;
-            const float mx = wave_max(z);
-            const float e = live ? __expf(z - mx) : 0.f;
-            const float sum = wave_sum(e);
-            const float r = e / sum;
-            const float logr = live ? z - mx - __logf(sum) : 0.f;
-            const float dr = live ? dR[jj * kLd + i] + dcL[jj] * (logr + 1.f) : 0.f;
-            const float dot = wave_sum(r * dr);
-            const float dz = r * (dr - dot);
-            const float dzlog = wave_sum(dz * logr);
-            if (i < S) {
-                Rm[jj * kLd + i] = r;
-                dR[jj * kLd + i] = dz * sc;
+            load_tile<float, NTH, C, kD>(
+                dA, jb, d, [&](int jj) { return p.daL + soff + ((int64_t)(j0 + jj) * m + k) * kD; }, tid);
+            if constexpr (LAST)
+                load_tile<float, NTH, C, kD>(
+                    dYt, jb, d, [&](int jj) { return p.dY + soff + ((int64_t)(j0 + jj) * m + k) * kD; }, tid);
+            for (int jj = tid; jj < C; jj += NTH) {
+                cR[jj] = (FIRST || jj >= jb) ? 1.f : p.cR[coff + (int64_t)(j0 + jj) * m + k];
+                dcL[jj] = jj < jb ? p.dcL[coff + (int64_t)(j0 + jj) * m + k] : 0.f;
             }
-            if (!FIRST && i == 0) p.dcR[coff + row0 + jj] = -dzlog / cR[jj];
-        }
-        __syncthreads();
+            __syncthreads();
 
-        // d alpha_R[j] = sum_i dZs[j][i] Kbar[i]: to the workspace, or at step 1 into dq
-        if constexpr (FIRST) {
-            const float *dQ = p.dQ + toff + row0 * d;
-            T *dq = p.dq + toff + row0 * d;
-            gemm<W, S, kD, S>(
-                wave, lane,
-                [&](int jj, int e, float v) {
-                    if (jj < kv && e < d) dq[(int64_t)jj * d + e] = static_cast<T>(dQ[(int64_t)jj * d + e] + v);
-                },
-                pair<false, false>(dR, Kb));
-        } else {
-            float *daR = p.daR + soff + row0 * kD;
-            gemm<W, S, kD, S>(
-                wave, lane,
-                [&](int jj, int e, float v) {
-                    if (jj < b && e < d) daR[(int64_t)jj * kD + e] = v;
-                },
-                pair<false, false>(dR, Kb));
-        }
-        // dKbar[i] += sum_j R[j][i] d alpha_L[j] + sum_j dZs[j][i] alpha_R[j]
-        {
-            float *dK = p.dK + toff + row0 * d;
-            T *dk = p.dk + toff + row0 * d;
-            gemm<W, S, kD, S>(
-                wave, lane,
-                [&](int i, int e, float v) {
-                    if (i < kv && e < d) {
-                        const int64_t o = (int64_t)i * d + e;
-                        const float acc = LAST ? v : v + dK[o];
-                        if constexpr (FIRST) {
-                            dk[o] = static_cast<T>(acc);
-                        } else {
-                            dK[o] = acc;
-                        }
+            // unnormalised scores <alpha_R[j], Kbar[i]>;  dR = d alpha_L Kbar^T (+ dY Vbar^T)
+            gemm<W, C, S, kD>(wave, lane, to_lds<LS>(Rm), pair<false, true>(aR, Kb));
+            if constexpr (LAST) {
+                gemm<W, C, S, kD>(wave, lane, to_lds<LS>(dR), pair<false, true>(dA, Kb), pair<false, true>(dYt, Vb));
+            } else {
+                gemm<W, C, S, kD>(wave, lane, to_lds<LS>(dR), pair<false, true>(dA, Kb));
+            }
+            __syncthreads();
+            // per row j (one wave, CPL keys i per lane): R, then dZ scaled by s / c_R[j] in place of dR
+            for (int jj = wave; jj < C; jj += W) {
+                float *rr = Rm + jj * LS, *dr = dR + jj * LS;
+                if (jj >= jb) {
+#pragma unroll
+                    for (int u = 0; u < CPL; ++u)
+                        if (lane + 64 * u < S) rr[lane + 64 * u] = dr[lane + 64 * u] = 0.f;
+                    continue;
+                }
+                const float sc = dm.s / cR[jj];
+                float z[CPL], mx = -INFINITY;
+#pragma unroll
+                for (int u = 0; u < CPL; ++u) {
+                    const int i = lane + 64 * u;
+                    z[u] = i < kv ? sc * rr[i] : -INFINITY;
+                    mx = fmaxf(mx, z[u]);
+                }
+                mx = wave_max(mx);
+                float e[CPL], sum = 0.f;
+#pragma unroll
+                for (int u = 0; u < CPL; ++u) {
+                    e[u] = lane + 64 * u < kv ? __expf(z[u] - mx) : 0.f;
+                    sum += e[u];
+                }
+                sum = wave_sum(sum);
+                const float lsum = __logf(sum), inv = 1.f / sum;
+                float r[CPL], logr[CPL], g[CPL], dot = 0.f;
+#pragma unroll
+                for (int u = 0; u < CPL; ++u) {
+                    const int i = lane + 64 * u;
+                    const bool live = i < kv;
+                    r[u] = e[u] * inv;
+                    logr[u] = live ? z[u] - mx - lsum : 0.f;
+                    g[u] = live ? dr[i] + dcL[jj] * (logr[u] + 1.f) : 0.f;
+                    dot += r[u] * g[u];
+                }
+                dot = wave_sum(dot);
+                float dzlog = 0.f;
+#pragma unroll
+                for (int u = 0; u < CPL; ++u) {
+                    const int i = lane + 64 * u;
+                    const float dz = r[u] * (g[u] - dot);
+                    dzlog += dz * logr[u];
+                    if (i < S) {
+                        rr[i] = r[u];
+                        dr[i] = dz * sc;
                     }
-                },
-                pair<true, false>(Rm, dA), pair<true, false>(dR, aR));
+                }
+                dzlog = wave_sum(dzlog);
+                if (!FIRST && lane == 0) p.dcR[coff + row0 + j0 + jj] = -dzlog / cR[jj];
+            }
+            __syncthreads();
+
+            // d alpha_R[j] = sum_i dZs[j][i] Kbar[i]: to the workspace, or at step 1 into dq
+            if constexpr (FIRST) {
+                const float *dQ = p.dQ + toff + (row0 + j0) * d;
+                T *dq = p.dq + toff + (row0 + j0) * d;
+                gemm<W, C, kD, S>(
+                    wave, lane,
+                    [&](int jj, int e, float v) {
+                        if (jj < jq && e < d) dq[(int64_t)jj * d + e] = static_cast<T>(dQ[(int64_t)jj * d + e] + v);
+                    },
+                    pair<false, false, LS, kLd>(dR, Kb));
+            } else {
+                float *daR = p.daR + soff + (row0 + j0) * kD;
+                gemm<W, C, kD, S>(
+                    wave, lane,
+                    [&](int jj, int e, float v) {
+                        if (jj < jb && e < d) daR[(int64_t)jj * kD + e] = v;
+                    },
+                    pair<false, false, LS, kLd>(dR, Kb));
+            }
+            // dKbar[i] += sum_j R[j][i] d alpha_L[j] + dZs[j][i] alpha_R[j];  dVbar[i] += sum_j R[j][i] dY[j]
+            dK.template add<C>(wave, lane, pair<true, false, LS, kLd>(Rm, dA), pair<true, false, LS, kLd>(dR, aR));
+            if constexpr (LAST) dV.template add<C>(wave, lane, pair<true, false, LS, kLd>(Rm, dYt));
+            __syncthreads();  // the next chunk overwrites the chunk tiles
         }
-        // dVbar[i] = sum_j R[j][i] dY[j]
+
+        {
+            float *dKg = p.dK + toff + row0 * d;
+            T *dk = p.dk + toff + row0 * d;
+            dK.store(wave, lane, [&](int i, int e, float v) {
+                if (i < kv && e < d) {
+                    const int64_t o = (int64_t)i * d + e;
+                    const float acc = LAST ? v : v + dKg[o];
+                    if constexpr (FIRST) {
+                        dk[o] = static_cast<T>(acc);
+                    } else {
+                        dKg[o] = acc;
+                    }
+                }
+            });
+        }
         if constexpr (LAST) {
             T *dv = p.dv + toff + row0 * d;
-            gemm<W, S, kD, S>(
-                wave, lane,
-                [&](int i, int e, float v) {
-                    if (i < kv && e < d) dv[(int64_t)i * d + e] = static_cast<T>(v);
-                },
-                pair<true, false>(Rm, dYt));
+            dV.store(wave, lane, [&](int i, int e, float v) {
+                if (i < kv && e < d) dv[(int64_t)i * d + e] = static_cast<T>(v);
+            });
         }
     }
 };
 
 template <typename T, int S, bool LAST>
-__global__ __launch_bounds__(64 * Waves<S>::value) void l_bwd(BwdBufs<T> p, BwdDims dm)
+__global__ __launch_bounds__(Geo<S>::NTH) void l_bwd(BwdBufs<T> p, BwdDims dm)
 {
     __shared__ __attribute__((aligned(16))) float lds[LBwd<T, S, LAST>::LDS_FLOATS];
     LBwd<T, S, LAST>::run(p, dm, lds);
 }
 
 template <typename T, int S, bool FIRST, bool LAST>
-__global__ __launch_bounds__(64 * Waves<S>::value) void r_bwd(BwdBufs<T> p, BwdDims dm)
+__global__ __launch_bounds__(Geo<S>::NTH) void r_bwd(BwdBufs<T> p, BwdDims dm)
 {
     __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, FIRST, LAST>::LDS_FLOATS];
     RBwd<T, S, FIRST, LAST>::run(p, dm, lds);

@@ -252,7 +252,7 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
 template <typename T, int S, bool LAST>
 int launch_l_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
-    const dim3 grid((unsigned)(BH * dm.b)), block(64 * ma::bwd::Waves<S>::value);
+    const dim3 grid((unsigned)(BH * dm.b)), block(ma::bwd::Geo<S>::NTH);
     return L.run(kBwdL, [&] {
         return launched([&] { hipLaunchKernelGGL((ma::bwd::l_bwd<T, S, LAST>), grid, block, 0, L.stream, p, dm); });
     });
@@ -261,7 +261,7 @@ int launch_l_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, in
 template <typename T, int S, bool FIRST, bool LAST>
 int launch_r_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
-    const dim3 grid((unsigned)(BH * dm.m)), block(64 * ma::bwd::Waves<S>::value);
+    const dim3 grid((unsigned)(BH * dm.m)), block(ma::bwd::Geo<S>::NTH);
     return L.run(kBwdR, [&] {
         return launched(
             [&] { hipLaunchKernelGGL((ma::bwd::r_bwd<T, S, FIRST, LAST>), grid, block, 0, L.stream, p, dm); });
@@ -296,7 +296,7 @@ template <typename T, int S> int bwd_sweep(Launcher &L, const BwdCallBufs &B, co
 }
 
 // The forward half-steps again, each step's states to buffers of their own,
-// then the reverse sweep.  m, b <= 64 and d <= 64 (checked by the caller).
+// then the reverse sweep.  m, b <= 128 and d <= 64 (checked by the caller).
 template <typename T> int run_bwd_impl(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {
     ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};
@@ -318,7 +318,8 @@ template <typename T> int run_bwd_impl(Launcher &L, const BwdCallBufs &B, const 
     switch (tile_rows(c.m > c.b ? c.m : c.b)) {
     case 16: return bwd_sweep<T, 16>(L, B, c);
     case 32: return bwd_sweep<T, 32>(L, B, c);
-    default: return bwd_sweep<T, 64>(L, B, c);
+    case 64: return bwd_sweep<T, 64>(L, B, c);
+    default: return bwd_sweep<T, 128>(L, B, c);
     }
 }
 

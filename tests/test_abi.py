@@ -166,8 +166,8 @@ def test_objective_rejects_null_obj():
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 2 * FAKE + 64, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),  # dk overlaps dq
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE + 8, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),  # misaligned dq
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 257, 64, 16, 16, 1, 1), 1),    # N > m b
-        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 8192, 64, 128, 64, 1, 1), 2),  # m > 64
-        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 8192, 64, 64, 128, 1, 1), 2),  # b > 64
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 16512, 64, 129, 128, 1, 1), 2),  # m > 128
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 16512, 64, 128, 129, 1, 1), 2),  # b > 128
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 72, 16, 16, 1, 1), 2),    # d > 64
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 33, 1), 2),   # T > 32
     ],
@@ -190,7 +190,13 @@ def test_bwd_invalid_arguments_rejected_before_any_hip_call(args, code):
         ((7, 8, 7, 1, 1, 1), True),
         ((1024, 64, 32, 32, 32, 1), True),
         ((1024, 64, 32, 32, 33, 1), False),
-        ((16384, 64, 128, 128, 2, 1), False),
+        ((16384, 64, 128, 128, 2, 1), True),
+        ((8192, 64, 128, 64, 2, 1), True),
+        ((384, 64, 3, 128, 1, 1), True),
+        ((7600, 48, 60, 128, 2, 1), True),
+        ((16384, 64, 128, 128, 2, 0), True),
+        ((16384, 128, 128, 128, 2, 1), False),
+        ((256, 72, 16, 16, 3, 1), False),
         ((256, 96, 16, 16, 2, 1), False),
         ((196, 64, 15, 14, 2, 1), False),
     ],
@@ -213,4 +219,4 @@ def test_bwd_workspace_bytes_formula():
     # fp32 states are twice as wide; unsupported shapes give 0
     st32 = _align(BH * Np * 64 * 4)
     assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_F32) == want + 2 * T * (st32 - st)
-    assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 16384, 64, 128, 128, 2, ma.MA_BF16) == 0
+    assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 16384, 128, 128, 128, 2, ma.MA_BF16) == 0

@@ -117,6 +117,23 @@ def test_padded_lengths(ma, dtype, n, m, b, T):
     run_case(ma, 1, 2, n, m, b, 64, T, dtype, seed=n)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize(
+    "H,n,m,b,d,T",
+    [
+        (2, 2048, 16, 128, 64, 2),   # b = 128: 128-row tiles, rows j in four chunks
+        (2, 2048, 128, 16, 64, 2),   # m = 128: query rows l in four chunks
+        (1, 9000, 100, 90, 64, 2),   # both sides padded to 128-row tiles
+        (1, 384, 3, 128, 64, 1),     # RoBERTa at N = 384 with b = 128
+        (1, 384, 4, 96, 64, 3),      # ... and b = 96
+        (1, 7600, 60, 128, 48, 2),   # graph transformer: N = 7600, b = 128, d = 48
+        (1, 8191, 128, 64, 32, 1),   # a last key block of 63 keys
+    ],
+)
+def test_large_blocks(ma, dtype, H, n, m, b, d, T):
+    run_case(ma, 1, H, n, m, b, d, T, dtype, seed=n + m)
+
+
 @pytest.mark.parametrize("T", [1, 3])
 @pytest.mark.parametrize("n", [16, 40, 64])
 def test_single_block_is_softmax_attention(ma, n, T):
@@ -220,3 +237,15 @@ def test_forward_and_gradient_calls_share_the_workspace(ma):
                 ma.monarch_attn_release_workspace()
     finally:
         ma.monarch_attn_set_path(prev)
+
+
+@pytest.mark.parametrize("name,heads", [("speed_n16384", [(0, 0), (0, 9)]), ("bart_n8192_b64", [(0, 0), (0, 11)])])
+def test_long_sequence_sampled_heads(ma, name, heads):
+    """The 16K speed point (m = b = 128, T = 2) and BART's N = 8192 with b = 64
+    (m = 128) at full size, oracle on two heads."""
+    w = si.WORKLOADS[name]
+    q, k, v, _ = si.make_qkv(w)
+    dout = si.random_cotangent((w.B, w.H, w.N, w.d), w.dtype, seed=3)
+    got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
+    ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
+    check(got, ref, heads, w.dtype, name)
