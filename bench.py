@@ -455,10 +455,11 @@ def quality(ma, torch, w, steps_list=(1, 2, 3)):
 
 
 # Sources whose text fixes each kernel's memory traffic: the kernels'
-# definitions and their launch configuration.
+# definitions and their launch configuration (the gradient's launches live
+# apart, so that changing them leaves the forward records valid).
 CSRC = os.path.join(ROOT, "paper_2505_18698_amd", "csrc")
 FWD_SOURCES = ("ma_kernels.hpp", "dispatch.hpp")
-BWD_SOURCES = ("backward.hpp", "ma_kernels.hpp", "dispatch.hpp")
+BWD_SOURCES = ("backward.hpp", "dispatch_bwd.hpp", "ma_kernels.hpp", "dispatch.hpp")
 
 
 def kernel_sources_sha(kernel):

@@ -1,5 +1,6 @@
 // Kernels and dispatch for element type __bf16.
 #include "dispatch.hpp"
+#include "dispatch_bwd.hpp"
 
 namespace ma_host {
 template <> int run_call<__bf16>(Launcher &L, const CallBufs &B, const CallDims &c, int path)

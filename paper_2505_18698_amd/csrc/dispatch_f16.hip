@@ -1,5 +1,6 @@
 // Kernels and dispatch for element type _Float16.
 #include "dispatch.hpp"
+#include "dispatch_bwd.hpp"
 
 namespace ma_host {
 template <> int run_call<_Float16>(Launcher &L, const CallBufs &B, const CallDims &c, int path)

@@ -1,5 +1,6 @@
 // Kernels and dispatch for element type float.
 #include "dispatch.hpp"
+#include "dispatch_bwd.hpp"
 
 namespace ma_host {
 template <> int run_call<float>(Launcher &L, const CallBufs &B, const CallDims &c, int path)
