@@ -148,7 +148,7 @@ int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *ou
  *                 16-byte aligned, overlapping neither each other nor the
  *                 inputs.  Fully overwritten.  All owned by the caller.
  * B, H, N, d, m, b, T, dtype, stream : as monarch_attn_fwd, and in addition
- *                 d <= 64 and T <= 32 (else MA_EUNSUPPORTED).
+ *                 T <= 32, and m, b <= 64 when d > 96 (else MA_EUNSUPPORTED).
  *
  * Runs the forward half-steps again, keeping the states of every step, then
  * one launch per half-step in reverse order; all of it on `stream`,
@@ -169,10 +169,11 @@ int monarch_attn_bwd(const void *q, const void *k, const void *v, const void *do
 int monarch_attn_bwd_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype);
 
 /* Bytes of device workspace monarch_attn_bwd needs (0 on bad arguments):
- * 2T state tensors of m b 64 elements and 2T - 1 arrays of m b floats per head
- * for the recomputed forward pass, 2 N d floats (dQ, dK accumulators), 3 m b 64
- * floats and 2 m b floats (state gradients) per head, each array rounded up to
- * 256 bytes.  Makes no HIP call. */
+ * 2T state tensors of m b D elements (D = 64, 96 or 128, the smallest that
+ * holds d) and 2T - 1 arrays of m b floats per head for the recomputed forward
+ * pass, 2 N d floats (dQ, dK accumulators), 3 m b D floats and 2 m b floats
+ * (state gradients) per head, each array rounded up to 256 bytes.  Makes no
+ * HIP call. */
 size_t monarch_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,
                                         int64_t m, int64_t b, int32_t T, int32_t dtype);
 

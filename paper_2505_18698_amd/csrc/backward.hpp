@@ -46,7 +46,7 @@ namespace ma {
 
 template <typename T> struct BwdBufs {
     const T *q, *k, *v, *dout;  // [B*H][n][d]
-    const T *aR, *aL, *Y;       // states of the step being undone ([m][b][D], [b][m][D], [b][m][D])
+    const T *aR, *aL, *Y;       // states of the step being undone ([m][b][D], [b][m][D], [b][m][D], D the tile width)
     const float *cR, *cL;       // c_R [b][m] (j-major), c_L [m][b] (k-major), as the forward writes them
     float *dQ, *dK;             // fp32 accumulators [B*H][n][d]
     T *dq, *dk, *dv;            // results [B*H][n][d]
@@ -55,26 +55,35 @@ template <typename T> struct BwdBufs {
 };
 
 struct BwdDims {
-    int m, b, n, d;  // as in the forward; here m, b <= 128 and d <= 64 (states of width 64)
+    int m, b, n, d;  // as in the forward (the states are D = 64, 96 or 128 wide, d <= D)
     float s;         // 1/sqrt(d)
 };
 
 namespace bwd {
 
-constexpr int kD = 64;   // row width of the states (the forward's tile width for d <= 64)
-constexpr int kLd = 84;  // row stride (floats) of 64-wide LDS tiles: 16-byte rows, 20 banks apart
+// Row strides (floats) of the LDS tiles of up to 128 columns: 16-byte rows
+// whose starting banks (mod 64) are 20 or 36 apart, so that 16 lanes reading
+// one row each (as the MFMA A operand) and 16 lanes reading one column of four
+// rows (transposed) both hit distinct banks.
+constexpr int row_stride(int cols) { return cols <= 64 ? 84 : cols <= 96 ? 100 : 148; }
 
-// Shape of the units for tiles of S rows (S = 16, 32, 64 or 128 >= m, b):
-// W waves (one 16 x 16 output tile of the widest product each), rows walked
-// in chunks of C, and the row stride LS of the C x S score tiles (16-byte
-// rows, 20 banks apart like kLd).
-template <int S> struct Geo {
-    static constexpr int W = S >= 64 ? 16 : S / 4;
+// Shape of the units for tiles of S rows (S = 16, 32, 64 or 128 >= m, b) and
+// D columns (the state width, 64, 96 or 128): W waves (one 16 x 16 output
+// tile of the widest product each), rows walked in chunks of C (as large as
+// the 160 KB of LDS allows), and the row strides LD of the D-wide tiles and
+// LS of the C x S score tiles.
+constexpr int unit_waves(int S) { return S >= 64 ? 16 : S / 4; }
+
+template <int S, int D> struct Geo {
+    static constexpr int W = unit_waves(S);
     static constexpr int NTH = 64 * W;
-    static constexpr int C = S > 64 ? 32 : S;
+    static constexpr int LD = row_stride(D);
+    static constexpr int LS = row_stride(S);
+    static constexpr int lds_floats(int c) { return 2 * S * LD + 3 * c * LD + 2 * c * LS + 2 * S; }
+    static constexpr int C = lds_floats(S) <= 40960 ? S : lds_floats(32) <= 40960 ? 32 : 16;
     static constexpr int NCH = S / C;
-    static constexpr int LS = S > 64 ? 148 : kLd;
     static constexpr int CPL = S > 64 ? S / 64 : 1;  // score columns per lane in the row passes
+    static_assert(lds_floats(C) <= 40960, "tile shape exceeds the LDS of one CU");
 };
 
 // Reductions over the 64 lanes with no LDS round trip: DPP within rows of 16
@@ -147,7 +156,7 @@ template <bool TA, bool TB, int LA, int LB> struct Pair {
     }
 };
 
-template <bool TA, bool TB, int LA = kLd, int LB = kLd>
+template <bool TA, bool TB, int LA, int LB>
 __device__ inline Pair<TA, TB, LA, LB> pair(const float *A, const float *B)
 {
     return Pair<TA, TB, LA, LB>{A, B};
@@ -219,12 +228,12 @@ template <int LD> __device__ inline auto to_lds(float *t)
     return [t](int r, int c, float v) { t[r * LD + c] = v; };
 }
 
-// Rows r < R and columns c < C (compile-time extents, C <= 64 a multiple of
-// 16) of an LDS tile from a row-major global matrix of element type E whose
+// Rows r < R and columns c < C (compile-time extents, C a multiple of 16;
+// row stride LDT) of an LDS tile from a row-major global matrix of element type E whose
 // row r starts at src(r) (16-byte aligned): element (r, c) is read while
 // r < nr and c < nc (nc a multiple of 16 bytes' worth of elements), zero
 // elsewhere.  One 16-byte global read per chunk.
-template <typename E, int NTH, int R, int C, typename Src>
+template <typename E, int NTH, int R, int C, int LDT, typename Src>
 __device__ inline void load_tile(float *dst, int nr, int nc, Src src, int tid)
 {
     constexpr int V = 16 / (int)sizeof(E), CPR = C / V;  // elements per chunk, chunks per row
@@ -242,7 +251,7 @@ __device__ inline void load_tile(float *dst, int nr, int nc, Src src, int tid)
         }
 #pragma unroll
         for (int i = 0; i < V; i += 4)
-            *reinterpret_cast<f32x4 *>(dst + r * kLd + c + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
+            *reinterpret_cast<f32x4 *>(dst + r * LDT + c + i) = f32x4{v[i], v[i + 1], v[i + 2], v[i + 3]};
     }
 }
 
@@ -250,10 +259,10 @@ __device__ inline void load_tile(float *dst, int nr, int nc, Src src, int tid)
 // The L update of class j of step t undone (LAST: t = T, the update that also
 // produced O).  S >= m; query rows l in chunks of C.
 // ---------------------------------------------------------------------------------------
-template <typename T, int S, bool LAST> struct LBwd {
-    using G_ = Geo<S>;
-    static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL;
-    static constexpr int LDS_FLOATS = 2 * S * kLd + 2 * C * kLd + 2 * C * LS + 2 * S;
+template <typename T, int S, int D, bool LAST> struct LBwd {
+    using G_ = Geo<S, D>;
+    static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
+    static constexpr int LDS_FLOATS = 2 * S * LD + 2 * C * LD + 2 * C * LS + 2 * S;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
     {
@@ -262,25 +271,25 @@ template <typename T, int S, bool LAST> struct LBwd {
         const int64_t bh = blockIdx.x / b;
         const int j = blockIdx.x % b;
         const int ml = (n - j + b - 1) / b;  // rows l with l*b + j < n
-        const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * kD, coff = bh * Np;
+        const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
         // whole-unit tiles (rows k): alpha_L[j][k]; Y[j][k] (LAST) or d alpha_R'[k][j]
-        float *aL = lds, *X = aL + S * kLd;
+        float *aL = lds, *X = aL + S * LD;
         // chunk tiles (rows l of the chunk): Qbar, dO (LAST) or L d alpha_R', L, dL then dW
-        float *Qb = X + S * kLd, *G = Qb + C * kLd, *Lm = G + C * kLd, *dL = Lm + C * LS;
+        float *Qb = X + S * LD, *G = Qb + C * LD, *Lm = G + C * LD, *dL = Lm + C * LS;
         float *cL = dL + C * LS, *dcR = cL + S;
 
-        load_tile<T, NTH, S, kD>(aL, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * kD; }, tid);
+        load_tile<T, NTH, S, D, LD>(aL, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * D; }, tid);
         if constexpr (LAST) {
-            load_tile<T, NTH, S, kD>(X, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * kD; }, tid);
+            load_tile<T, NTH, S, D, LD>(X, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * D; }, tid);
         } else {
-            load_tile<float, NTH, S, kD>(X, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * kD; },
+            load_tile<float, NTH, S, D, LD>(X, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * D; },
                                          tid);
         }
         for (int k = tid; k < S; k += NTH) {
             cL[k] = k < m ? p.cL[coff + (int64_t)k * b + j] : 0.f;
             dcR[k] = (!LAST && k < m) ? p.dcR[coff + (int64_t)k * b + j] : 0.f;
         }
-        Acc<W, S, kD> daL, dY;  // sums over all rows l
+        Acc<W, S, D> daL, dY;  // sums over all rows l
         daL.zero();
         if constexpr (LAST) dY.zero();
         float dcl = 0.f;  // thread k < S: sum over l of dW[l][k]
@@ -288,15 +297,15 @@ template <typename T, int S, bool LAST> struct LBwd {
 
         for (int ch = 0; ch < G_::NCH; ++ch) {
             const int l0 = ch * C, lc = min(max(ml - l0, 0), C);  // live rows of the chunk
-            load_tile<T, NTH, C, kD>(Qb, lc, d, [&](int l) { return p.q + toff + ((int64_t)(l0 + l) * b + j) * d; },
+            load_tile<T, NTH, C, D, LD>(Qb, lc, d, [&](int l) { return p.q + toff + ((int64_t)(l0 + l) * b + j) * d; },
                                      tid);
             if constexpr (LAST)
-                load_tile<T, NTH, C, kD>(
+                load_tile<T, NTH, C, D, LD>(
                     G, lc, d, [&](int l) { return p.dout + toff + ((int64_t)(l0 + l) * b + j) * d; }, tid);
             __syncthreads();
 
             // unnormalised scores <Qbar[l], alpha_L[k]>
-            gemm<W, C, S, kD>(wave, lane, to_lds<LS>(Lm), pair<false, true>(Qb, aL));
+            gemm<W, C, S, D>(wave, lane, to_lds<LS>(Lm), pair<false, true, LD, LD>(Qb, aL));
             __syncthreads();
             // L[l][k] = softmax_k (s score - c_L[k]): one wave per row l, CPL columns k per lane
             for (int l = wave; l < C; l += W) {
@@ -330,12 +339,12 @@ template <typename T, int S, bool LAST> struct LBwd {
 
             if constexpr (LAST) {
                 // dL = dO Y^T;  dY += L^T dO
-                gemm<W, C, S, kD>(wave, lane, to_lds<LS>(dL), pair<false, true>(G, X));
-                dY.template add<C>(wave, lane, pair<true, false, LS, kLd>(Lm, G));
+                gemm<W, C, S, D>(wave, lane, to_lds<LS>(dL), pair<false, true, LD, LD>(G, X));
+                dY.template add<C>(wave, lane, pair<true, false, LS, LD>(Lm, G));
             } else {
                 // dL = Qbar d alpha_R'^T (+ d c_R' below);  G = L d alpha_R' (the alpha_R' term of dQbar)
-                gemm<W, C, S, kD>(wave, lane, to_lds<LS>(dL), pair<false, true>(Qb, X));
-                gemm<W, C, kD, S>(wave, lane, to_lds<kLd>(G), pair<false, false, LS, kLd>(Lm, X));
+                gemm<W, C, S, D>(wave, lane, to_lds<LS>(dL), pair<false, true, LD, LD>(Qb, X));
+                gemm<W, C, D, S>(wave, lane, to_lds<LD>(G), pair<false, false, LS, LD>(Lm, X));
             }
             __syncthreads();
             // dW = s L (dL - <L, dL>), in place of dL
@@ -357,7 +366,7 @@ template <typename T, int S, bool LAST> struct LBwd {
             __syncthreads();
 
             // dQ rows (l0 + l)*b + j: dW alpha_L (+ L d alpha_R')
-            gemm<W, C, kD, S>(
+            gemm<W, C, D, S>(
                 wave, lane,
                 [&](int l, int e, float v) {
                     if (l < lc && e < d) {
@@ -365,27 +374,27 @@ template <typename T, int S, bool LAST> struct LBwd {
                         if constexpr (LAST) {
                             *o = v;
                         } else {
-                            *o += v + G[l * kLd + e];
+                            *o += v + G[l * LD + e];
                         }
                     }
                 },
-                pair<false, false, LS, kLd>(dL, aL));
+                pair<false, false, LS, LD>(dL, aL));
             // d alpha_L[k] += dW^T Qbar;  d c_L[k] += sum_l dW[l][k]
-            daL.template add<C>(wave, lane, pair<true, false, LS, kLd>(dL, Qb));
+            daL.template add<C>(wave, lane, pair<true, false, LS, LD>(dL, Qb));
             if (tid < S) {
                 for (int l = 0; l < C; ++l) dcl += dL[l * LS + tid];
             }
             __syncthreads();  // the next chunk overwrites the chunk tiles
         }
 
-        float *daLg = p.daL + soff + (int64_t)j * m * kD;
+        float *daLg = p.daL + soff + (int64_t)j * m * D;
         daL.store(wave, lane, [&](int k, int e, float v) {
-            if (k < m && e < d) daLg[(int64_t)k * kD + e] = v;
+            if (k < m && e < d) daLg[(int64_t)k * D + e] = v;
         });
         if constexpr (LAST) {
-            float *dYg = p.dY + soff + (int64_t)j * m * kD;
+            float *dYg = p.dY + soff + (int64_t)j * m * D;
             dY.store(wave, lane, [&](int k, int e, float v) {
-                if (k < m && e < d) dYg[(int64_t)k * kD + e] = v;
+                if (k < m && e < d) dYg[(int64_t)k * D + e] = v;
             });
         }
         if (tid < m) p.dcL[coff + (int64_t)j * m + tid] = -dcl / dm.s;
@@ -396,10 +405,10 @@ template <typename T, int S, bool LAST> struct LBwd {
 // The R update of block k of step t undone (FIRST: t = 1, LAST: t = T).
 // S >= b; rows j in chunks of C.
 // ---------------------------------------------------------------------------------------
-template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
-    using G_ = Geo<S>;
-    static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL;
-    static constexpr int LDS_FLOATS = (LAST ? 2 : 1) * S * kLd + (LAST ? 3 : 2) * C * kLd + 2 * C * LS + 2 * C;
+template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
+    using G_ = Geo<S, D>;
+    static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
+    static constexpr int LDS_FLOATS = (LAST ? 2 : 1) * S * LD + (LAST ? 3 : 2) * C * LD + 2 * C * LS + 2 * C;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
     {
@@ -408,18 +417,18 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
         const int64_t bh = blockIdx.x / m;
         const int k = blockIdx.x % m;
         const int kv = min(b, n - k * b);  // real keys (and query rows) of block k
-        const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * kD, coff = bh * Np;
+        const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
         const int64_t row0 = (int64_t)k * b;  // first row of block k
         // whole-unit tiles (rows i): Kbar, Vbar (LAST)
-        float *Kb = lds, *Vb = Kb + S * kLd;
+        float *Kb = lds, *Vb = Kb + S * LD;
         // chunk tiles (rows j of the chunk): alpha_R, d alpha_L, dY (LAST), R, dR then dZ s / c_R
-        float *aR = Kb + (LAST ? 2 : 1) * S * kLd, *dA = aR + C * kLd, *dYt = dA + C * kLd;
-        float *Rm = dA + (LAST ? 2 : 1) * C * kLd, *dR = Rm + C * LS;
+        float *aR = Kb + (LAST ? 2 : 1) * S * LD, *dA = aR + C * LD, *dYt = dA + C * LD;
+        float *Rm = dA + (LAST ? 2 : 1) * C * LD, *dR = Rm + C * LS;
         float *cR = dR + C * LS, *dcL = cR + C;
 
-        load_tile<T, NTH, S, kD>(Kb, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
-        if constexpr (LAST) load_tile<T, NTH, S, kD>(Vb, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
-        Acc<W, S, kD> dK, dV;  // sums over all rows j
+        load_tile<T, NTH, S, D, LD>(Kb, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
+        if constexpr (LAST) load_tile<T, NTH, S, D, LD>(Vb, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
+        Acc<W, S, D> dK, dV;  // sums over all rows j
         dK.zero();
         if constexpr (LAST) dV.zero();
 
@@ -427,16 +436,16 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
             const int j0 = ch * C;
             const int jb = min(max(b - j0, 0), C), jq = min(max(kv - j0, 0), C);  // live rows; rows of Q (t = 1)
             if constexpr (FIRST) {
-                load_tile<T, NTH, C, kD>(aR, jq, d, [&](int jj) { return p.q + toff + (row0 + j0 + jj) * d; }, tid);
+                load_tile<T, NTH, C, D, LD>(aR, jq, d, [&](int jj) { return p.q + toff + (row0 + j0 + jj) * d; }, tid);
             } else {
-                load_tile<T, NTH, C, kD>(aR, jb, d, [&](int jj) { return p.aR + soff + (row0 + j0 + jj) * kD; },
+                load_tile<T, NTH, C, D, LD>(aR, jb, d, [&](int jj) { return p.aR + soff + (row0 + j0 + jj) * D; },
                                          tid);
             }
-            load_tile<float, NTH, C, kD>(
-                dA, jb, d, [&](int jj) { return p.daL + soff + ((int64_t)(j0 + jj) * m + k) * kD; }, tid);
+            load_tile<float, NTH, C, D, LD>(
+                dA, jb, d, [&](int jj) { return p.daL + soff + ((int64_t)(j0 + jj) * m + k) * D; }, tid);
             if constexpr (LAST)
-                load_tile<float, NTH, C, kD>(
-                    dYt, jb, d, [&](int jj) { return p.dY + soff + ((int64_t)(j0 + jj) * m + k) * kD; }, tid);
+                load_tile<float, NTH, C, D, LD>(
+                    dYt, jb, d, [&](int jj) { return p.dY + soff + ((int64_t)(j0 + jj) * m + k) * D; }, tid);
             for (int jj = tid; jj < C; jj += NTH) {
                 cR[jj] = (FIRST || jj >= jb) ? 1.f : p.cR[coff + (int64_t)(j0 + jj) * m + k];
                 dcL[jj] = jj < jb ? p.dcL[coff + (int64_t)(j0 + jj) * m + k] : 0.f;
@@ -444,11 +453,11 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
             __syncthreads();
 
             // unnormalised scores <alpha_R[j], Kbar[i]>;  dR = d alpha_L Kbar^T (+ dY Vbar^T)
-            gemm<W, C, S, kD>(wave, lane, to_lds<LS>(Rm), pair<false, true>(aR, Kb));
+            gemm<W, C, S, D>(wave, lane, to_lds<LS>(Rm), pair<false, true, LD, LD>(aR, Kb));
             if constexpr (LAST) {
-                gemm<W, C, S, kD>(wave, lane, to_lds<LS>(dR), pair<false, true>(dA, Kb), pair<false, true>(dYt, Vb));
+                gemm<W, C, S, D>(wave, lane, to_lds<LS>(dR), pair<false, true, LD, LD>(dA, Kb), pair<false, true, LD, LD>(dYt, Vb));
             } else {
-                gemm<W, C, S, kD>(wave, lane, to_lds<LS>(dR), pair<false, true>(dA, Kb));
+                gemm<W, C, S, D>(wave, lane, to_lds<LS>(dR), pair<false, true, LD, LD>(dA, Kb));
             }
             __syncthreads();
             // per row j (one wave, CPL keys i per lane): R, then dZ scaled by s / c_R[j] in place of dR
@@ -508,24 +517,24 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
             if constexpr (FIRST) {
                 const float *dQ = p.dQ + toff + (row0 + j0) * d;
                 T *dq = p.dq + toff + (row0 + j0) * d;
-                gemm<W, C, kD, S>(
+                gemm<W, C, D, S>(
                     wave, lane,
                     [&](int jj, int e, float v) {
                         if (jj < jq && e < d) dq[(int64_t)jj * d + e] = static_cast<T>(dQ[(int64_t)jj * d + e] + v);
                     },
-                    pair<false, false, LS, kLd>(dR, Kb));
+                    pair<false, false, LS, LD>(dR, Kb));
             } else {
-                float *daR = p.daR + soff + (row0 + j0) * kD;
-                gemm<W, C, kD, S>(
+                float *daR = p.daR + soff + (row0 + j0) * D;
+                gemm<W, C, D, S>(
                     wave, lane,
                     [&](int jj, int e, float v) {
-                        if (jj < jb && e < d) daR[(int64_t)jj * kD + e] = v;
+                        if (jj < jb && e < d) daR[(int64_t)jj * D + e] = v;
                     },
-                    pair<false, false, LS, kLd>(dR, Kb));
+                    pair<false, false, LS, LD>(dR, Kb));
             }
             // dKbar[i] += sum_j R[j][i] d alpha_L[j] + dZs[j][i] alpha_R[j];  dVbar[i] += sum_j R[j][i] dY[j]
-            dK.template add<C>(wave, lane, pair<true, false, LS, kLd>(Rm, dA), pair<true, false, LS, kLd>(dR, aR));
-            if constexpr (LAST) dV.template add<C>(wave, lane, pair<true, false, LS, kLd>(Rm, dYt));
+            dK.template add<C>(wave, lane, pair<true, false, LS, LD>(Rm, dA), pair<true, false, LS, LD>(dR, aR));
+            if constexpr (LAST) dV.template add<C>(wave, lane, pair<true, false, LS, LD>(Rm, dYt));
             __syncthreads();  // the next chunk overwrites the chunk tiles
         }
 
@@ -553,18 +562,18 @@ template <typename T, int S, bool FIRST, bool LAST> struct RBwd {
     }
 };
 
-template <typename T, int S, bool LAST>
-__global__ __launch_bounds__(Geo<S>::NTH) void l_bwd(BwdBufs<T> p, BwdDims dm)
+template <typename T, int S, int D, bool LAST>
+__global__ __launch_bounds__(64 * unit_waves(S)) void l_bwd(BwdBufs<T> p, BwdDims dm)
 {
-    __shared__ __attribute__((aligned(16))) float lds[LBwd<T, S, LAST>::LDS_FLOATS];
-    LBwd<T, S, LAST>::run(p, dm, lds);
+    __shared__ __attribute__((aligned(16))) float lds[LBwd<T, S, D, LAST>::LDS_FLOATS];
+    LBwd<T, S, D, LAST>::run(p, dm, lds);
 }
 
-template <typename T, int S, bool FIRST, bool LAST>
-__global__ __launch_bounds__(Geo<S>::NTH) void r_bwd(BwdBufs<T> p, BwdDims dm)
+template <typename T, int S, int D, bool FIRST, bool LAST>
+__global__ __launch_bounds__(64 * unit_waves(S)) void r_bwd(BwdBufs<T> p, BwdDims dm)
 {
-    __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, FIRST, LAST>::LDS_FLOATS];
-    RBwd<T, S, FIRST, LAST>::run(p, dm, lds);
+    __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, D, FIRST, LAST>::LDS_FLOATS];
+    RBwd<T, S, D, FIRST, LAST>::run(p, dm, lds);
 }
 
 }  // namespace bwd

@@ -9,27 +9,27 @@
 namespace ma_host {
 
 // ---- gradient ----
-template <typename T, int S, bool LAST>
+template <typename T, int S, int D, bool LAST>
 int launch_l_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
-    const dim3 grid((unsigned)(BH * dm.b)), block(ma::bwd::Geo<S>::NTH);
+    const dim3 grid((unsigned)(BH * dm.b)), block(ma::bwd::Geo<S, D>::NTH);
     return L.run(kBwdL, [&] {
-        return launched([&] { hipLaunchKernelGGL((ma::bwd::l_bwd<T, S, LAST>), grid, block, 0, L.stream, p, dm); });
+        return launched([&] { hipLaunchKernelGGL((ma::bwd::l_bwd<T, S, D, LAST>), grid, block, 0, L.stream, p, dm); });
     });
 }
 
-template <typename T, int S, bool FIRST, bool LAST>
+template <typename T, int S, int D, bool FIRST, bool LAST>
 int launch_r_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
-    const dim3 grid((unsigned)(BH * dm.m)), block(ma::bwd::Geo<S>::NTH);
+    const dim3 grid((unsigned)(BH * dm.m)), block(ma::bwd::Geo<S, D>::NTH);
     return L.run(kBwdR, [&] {
         return launched(
-            [&] { hipLaunchKernelGGL((ma::bwd::r_bwd<T, S, FIRST, LAST>), grid, block, 0, L.stream, p, dm); });
+            [&] { hipLaunchKernelGGL((ma::bwd::r_bwd<T, S, D, FIRST, LAST>), grid, block, 0, L.stream, p, dm); });
     });
 }
 
 // The reverse sweep, t = T .. 1: the L update of step t, then its R update.
-template <typename T, int S> int bwd_sweep(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+template <typename T, int S, int D> int bwd_sweep(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {
     const ma::BwdDims dm{c.m, c.b, c.n, c.d, (float)(1.0 / std::sqrt((double)c.d))};
     ma::BwdBufs<T> p{(const T *)B.q, (const T *)B.k, (const T *)B.v, (const T *)B.dout, nullptr, nullptr,
@@ -42,13 +42,13 @@ template <typename T, int S> int bwd_sweep(Launcher &L, const BwdCallBufs &B, co
         p.cL = B.cL + (size_t)(t - 1) * B.cst;
         p.aR = first ? nullptr : (const T *)(B.aR + (size_t)(t - 2) * B.st);
         p.cR = first ? nullptr : B.cR + (size_t)(t - 2) * B.cst;
-        rc = last ? launch_l_bwd<T, S, true>(L, p, dm, c.BH) : launch_l_bwd<T, S, false>(L, p, dm, c.BH);
+        rc = last ? launch_l_bwd<T, S, D, true>(L, p, dm, c.BH) : launch_l_bwd<T, S, D, false>(L, p, dm, c.BH);
         if (rc != MA_OK) return rc;
         if (first) {
-            rc = last ? launch_r_bwd<T, S, true, true>(L, p, dm, c.BH) : launch_r_bwd<T, S, true, false>(L, p, dm, c.BH);
+            rc = last ? launch_r_bwd<T, S, D, true, true>(L, p, dm, c.BH) : launch_r_bwd<T, S, D, true, false>(L, p, dm, c.BH);
         } else {
-            rc = last ? launch_r_bwd<T, S, false, true>(L, p, dm, c.BH)
-                      : launch_r_bwd<T, S, false, false>(L, p, dm, c.BH);
+            rc = last ? launch_r_bwd<T, S, D, false, true>(L, p, dm, c.BH)
+                      : launch_r_bwd<T, S, D, false, false>(L, p, dm, c.BH);
         }
         if (rc != MA_OK) return rc;
     }
@@ -56,8 +56,9 @@ template <typename T, int S> int bwd_sweep(Launcher &L, const BwdCallBufs &B, co
 }
 
 // The forward half-steps again, each step's states to buffers of their own,
-// then the reverse sweep.  m, b <= 128 and d <= 64 (checked by the caller).
-template <typename T> int run_bwd_impl(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+// then the reverse sweep.  States of width D = tile_d(d); every (m, b, d) the
+// forward takes except 128-row tiles with D = 128 (checked by the caller).
+template <typename T, int D> int run_bwd_d(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {
     ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};
     hd.T = c.T;
@@ -69,17 +70,31 @@ template <typename T> int run_bwd_impl(Launcher &L, const BwdCallBufs &B, const 
                          first ? nullptr : B.aR + (size_t)(t - 2) * B.st, B.aL + (size_t)(t - 1) * B.st, B.Y,
                          first ? nullptr : B.cR + (size_t)(t - 2) * B.cst, B.cL + (size_t)(t - 1) * B.cst, nullptr,
                          nullptr};
-        if ((rc = r_step<T, 64>(L, r, hd, c.BH, c.num_cus, first, last)) != MA_OK) return rc;
+        if ((rc = r_step<T, D>(L, r, hd, c.BH, c.num_cus, first, last)) != MA_OK) return rc;
         if (last) break;
         const CallBufs l{B.q, B.k, B.v, nullptr, B.aR + (size_t)(t - 1) * B.st, B.aL + (size_t)(t - 1) * B.st, B.Y,
                          B.cR + (size_t)(t - 1) * B.cst, B.cL + (size_t)(t - 1) * B.cst, nullptr, nullptr};
-        if ((rc = l_step<T, 64>(L, l, hd, c.BH, c.num_cus, false)) != MA_OK) return rc;
+        if ((rc = l_step<T, D>(L, l, hd, c.BH, c.num_cus, false)) != MA_OK) return rc;
     }
     switch (tile_rows(c.m > c.b ? c.m : c.b)) {
-    case 16: return bwd_sweep<T, 16>(L, B, c);
-    case 32: return bwd_sweep<T, 32>(L, B, c);
-    case 64: return bwd_sweep<T, 64>(L, B, c);
-    default: return bwd_sweep<T, 128>(L, B, c);
+    case 16: return bwd_sweep<T, 16, D>(L, B, c);
+    case 32: return bwd_sweep<T, 32, D>(L, B, c);
+    case 64: return bwd_sweep<T, 64, D>(L, B, c);
+    default:
+        if constexpr (D == 128) {
+            return fail(MA_EUNSUPPORTED, "the gradient does not take 128-row blocks with d > 96");
+        } else {
+            return bwd_sweep<T, 128, D>(L, B, c);
+        }
+    }
+}
+
+template <typename T> int run_bwd_impl(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+{
+    switch (tile_d(c.d)) {
+    case 64: return run_bwd_d<T, 64>(L, B, c);
+    case 96: return run_bwd_d<T, 96>(L, B, c);
+    default: return run_bwd_d<T, 128>(L, B, c);
     }
 }
 

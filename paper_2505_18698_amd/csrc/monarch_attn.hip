@@ -221,21 +221,25 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
 
 // ---- gradient ----
 
-// The gradient kernels hold one unit's matrices in fp32 LDS tiles 64 columns
-// wide (d <= 64); m and b are bounded by the forward pass (<= 128).
+// The gradient kernels hold one unit's matrices in fp32 LDS tiles: blocks of
+// up to 128 rows (as the forward) at state widths D = 64 or 96, of up to 64
+// rows at D = 128.
 int check_bwd_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype)
 {
     const int rc = check_shape(N, d, m, b, T, dtype);
     if (rc != MA_OK) return rc;
-    if (d > 64) return fail(MA_EUNSUPPORTED, "the gradient needs d <= 64 (got d=%lld)", (long long)d);
+    if ((m > 64 || b > 64) && tile_d(d) == 128)
+        return fail(MA_EUNSUPPORTED, "the gradient needs m, b <= 64 when d > 96 (got m=%lld, b=%lld, d=%lld)",
+                    (long long)m, (long long)b, (long long)d);
     if (T > 32) return fail(MA_EUNSUPPORTED, "the gradient supports T <= 32 (got %d)", T);
     return MA_OK;
 }
 
 // Workspace of one gradient call, in this order: alpha_R of steps 2..T, alpha_L
-// of steps 1..T and Y (element type, tile width 64); c_R of steps 2..T and c_L
-// of steps 1..T (fp32); the fp32 accumulators of dQ and dK ([B*H][N][d]); the
-// fp32 gradients d alpha_L, dY, d alpha_R (width 64) and d c_L, d c_R.
+// of steps 1..T and Y (element type, tile width D = tile_d(d)); c_R of steps
+// 2..T and c_L of steps 1..T (fp32); the fp32 accumulators of dQ and dK
+// ([B*H][N][d]); the fp32 gradients d alpha_L, dY, d alpha_R (width D) and
+// d c_L, d c_R.
 struct BwdLayout {
     size_t st, cs, acc, sg;
     int32_t T;
@@ -247,7 +251,7 @@ BwdLayout bwd_layout(int64_t BH, int64_t N, int64_t d, int64_t m, int64_t b, int
 {
     const int64_t Np = m * b;
     return BwdLayout{state_bytes(BH, Np, d, dtype), align_up((size_t)BH * Np * sizeof(float)),
-                     align_up((size_t)BH * N * d * sizeof(float)), align_up((size_t)BH * Np * 64 * sizeof(float)),
+                     align_up((size_t)BH * N * d * sizeof(float)), align_up((size_t)BH * Np * tile_d(d) * sizeof(float)),
                      T};
 }
 

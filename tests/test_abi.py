@@ -168,7 +168,7 @@ def test_objective_rejects_null_obj():
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 257, 64, 16, 16, 1, 1), 1),    # N > m b
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 16512, 64, 129, 128, 1, 1), 2),  # m > 128
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 16512, 64, 128, 129, 1, 1), 2),  # b > 128
-        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 72, 16, 16, 1, 1), 2),    # d > 64
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 8192, 128, 128, 64, 1, 1), 2),  # m > 64 with d > 96
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 33, 1), 2),   # T > 32
     ],
 )
@@ -195,9 +195,13 @@ def test_bwd_invalid_arguments_rejected_before_any_hip_call(args, code):
         ((384, 64, 3, 128, 1, 1), True),
         ((7600, 48, 60, 128, 2, 1), True),
         ((16384, 64, 128, 128, 2, 0), True),
-        ((16384, 128, 128, 128, 2, 1), False),
-        ((256, 72, 16, 16, 3, 1), False),
-        ((256, 96, 16, 16, 2, 1), False),
+        ((16384, 128, 128, 128, 2, 1), False),   # 128-row tiles with d > 96
+        ((8192, 128, 64, 128, 2, 1), False),
+        ((256, 72, 16, 16, 3, 1), True),          # DiT
+        ((256, 96, 16, 16, 2, 1), True),
+        ((4096, 128, 64, 64, 2, 1), True),
+        ((8192, 96, 128, 64, 2, 1), True),
+        ((4096, 128, 64, 64, 2, 0), True),        # fp32 at the largest fp32 tile
         ((196, 64, 15, 14, 2, 1), False),
     ],
 )
@@ -220,3 +224,10 @@ def test_bwd_workspace_bytes_formula():
     st32 = _align(BH * Np * 64 * 4)
     assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_F32) == want + 2 * T * (st32 - st)
     assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 16384, 128, 128, 128, 2, ma.MA_BF16) == 0
+    # d = 72: states and state gradients 96 wide
+    B, H, N, d, m, b, T = 1, 2, 256, 72, 16, 16, 3
+    Np, BH = m * b, B * H
+    st, cs = _align(BH * Np * 96 * 2), _align(BH * Np * 4)
+    acc, sg = _align(BH * N * d * 4), _align(BH * Np * 96 * 4)
+    assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_BF16) == \
+        2 * T * st + (2 * T - 1) * cs + 2 * acc + 3 * sg + 2 * cs

@@ -134,6 +134,38 @@ def test_large_blocks(ma, dtype, H, n, m, b, d, T):
     run_case(ma, 1, H, n, m, b, d, T, dtype, seed=n + m)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize(
+    "H,n,m,b,d,T",
+    [
+        (2, 256, 16, 16, 72, 3),     # DiT-XL/2: d = 72 on 96-wide tiles
+        (1, 576, 24, 24, 96, 2),
+        (1, 1024, 32, 32, 128, 2),
+        (1, 4096, 64, 64, 128, 2),   # 128-wide tiles at 64 rows: rows in chunks of 16
+        (1, 4000, 63, 64, 96, 1),    # 96-wide at 64 rows, padded: chunks of 32
+        (1, 2048, 128, 16, 96, 2),   # 96-wide at 128 rows: chunks of 16
+        (1, 1000, 8, 125, 88, 2),    # padded in both, d = 88
+    ],
+)
+def test_wide_heads(ma, dtype, H, n, m, b, d, T):
+    if dtype == "f32" and (16 * -(-m // 16) * (96 if d <= 96 else 128) > 8192 or 16 * -(-b // 16) * (96 if d <= 96 else 128) > 8192):
+        pytest.skip("fp32 tile exceeds the supported LDS budget of the forward pass")
+    if dtype == "f32" and d % 4 or dtype != "f32" and d % 8:
+        pytest.skip("d not a whole number of 16-byte chunks")
+    run_case(ma, 1, H, n, m, b, d, T, dtype, seed=n + d)
+
+
+def test_dit_workload_sampled_heads(ma):
+    """DiT-XL/2 at 256 x 256 (32 images x 16 heads, N = 256, d = 72, T = 3), oracle on 3 heads."""
+    w = si.WORKLOADS["dit_xl_n256"]
+    q, k, v, _ = si.make_qkv(w)
+    dout = si.random_cotangent((w.B, w.H, w.N, w.d), w.dtype, seed=4)
+    heads = [(0, 0), (13, 7), (31, 15)]
+    got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
+    ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
+    check(got, ref, heads, w.dtype, w.name)
+
+
 @pytest.mark.parametrize("T", [1, 3])
 @pytest.mark.parametrize("n", [16, 40, 64])
 def test_single_block_is_softmax_attention(ma, n, T):
