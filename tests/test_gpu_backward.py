@@ -281,3 +281,26 @@ def test_long_sequence_sampled_heads(ma, name, heads):
     got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
     ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
     check(got, ref, heads, w.dtype, name)
+
+
+def test_timing_reports_every_gradient_launch(ma):
+    """With timing on, a gradient call reports its launches in order: the
+    forward half-steps of the recompute (without the apply), then l_bwd, r_bwd
+    for t = T .. 1, each with a positive duration."""
+    import torch
+
+    B, H, n, m, b, d, T = 1, 2, 1024, 32, 32, 64, 3
+    q, k, v = si.random_qkv(B, H, n, d, "bf16", seed=5)
+    dout = si.random_cotangent((B, H, n, d), "bf16", seed=5)
+    tq, tk, tv, tg = (torch.from_numpy(x).to(torch.bfloat16).cuda() for x in (q, k, v, dout))
+    grads = [torch.empty_like(tq) for _ in range(3)]
+    ma.monarch_attn_timing_enable(True)
+    try:
+        ma.monarch_attn_bwd(tq, tk, tv, tg, *grads, m, b, T)
+        recs = ma.monarch_attn_timing_read()
+    finally:
+        ma.monarch_attn_timing_enable(False)
+    kinds = [kd for kd, _ in recs]
+    recompute = ["r_half_step", "l_half_step"] * (T - 1) + ["r_half_step_final"]
+    assert kinds == recompute + ["l_bwd", "r_bwd"] * T, kinds
+    assert all(t > 0 for _, t in recs)
