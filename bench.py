@@ -5,7 +5,7 @@ One step = one monarch_attn_fwd call: the whole forward pass (every R and L
 half-step, the Monarch product and the store of O) over one batch of
 synthetic Q, K, V already resident in HBM.  The headline workload is the
 long-sequence speed point (B=1, H=16, N=16384 = 128 x 128, d=64, bf16, T=2);
-the medium point (N=4096 = 64 x 64, T=1) and ViT-B/16 (384 heads, N=196 = 14 x 14,
+the medium point (N=4096 = 64 x 64, T=1 and T=3) and ViT-B/16 (384 heads, N=196 = 14 x 14,
 T=2, the one-workgroup-per-head kernel; and N=197 with the class token,
 post-padded to 15 x 14) are reported alongside in "also".
 
@@ -573,7 +573,7 @@ def main():
     ap.add_argument("--workload", default="speed_n16384")
     ap.add_argument("--d", type=int, default=None, help="override the head dimension")
     ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
-    ap.add_argument("--also", default="speed_n4096,vit_b16_n196,vit_b16_n197",
+    ap.add_argument("--also", default="speed_n4096,speed_n4096_t3,vit_b16_n196,vit_b16_n197",
                     help="comma-separated extra workloads ('' for none)")
     ap.add_argument("--backward", default="speed_n16384,speed_n4096,vit_b16_n197",
                     help="comma-separated workloads for the gradient timing ('' for none)")

@@ -88,6 +88,8 @@ WORKLOADS = {
     "vit_b16_n197": Workload("vit_b16_n197", 32, 12, 15, 14, 64, 2, "bf16", "vit", n=197),
     "roberta_n1024": Workload("roberta_n1024", 16, 12, 32, 32, 64, 2, "bf16", "lm"),
     "speed_n4096": Workload("speed_n4096", 1, 16, 64, 64, 64, 1, "bf16", "speed"),
+    # the same point at T = 3 (T = 2 is the N = 4096, d = 64 point of the sweep below)
+    "speed_n4096_t3": Workload("speed_n4096_t3", 1, 16, 64, 64, 64, 3, "bf16", "speed"),
     "speed_n16384": Workload("speed_n16384", 1, 16, 128, 128, 64, 2, "bf16", "speed"),
     # Shapes of the paper's other conversions, for measurement beside the
     # workloads above (synthetic inputs with the same recipes):
