@@ -27,6 +27,7 @@ try:
         dtype_code,
         fused_applies,
         monarch_attention,
+        monarch_attention_autograd,
         monarch_attn_bwd,
         monarch_attn_bwd_check,
         monarch_attn_bwd_workspace_bytes,

@@ -209,6 +209,43 @@ def monarch_attention(q, k, v, m: int, b: int, T: int, stream=None):
     return monarch_attn_fwd(q, k, v, out, m, b, T, stream)
 
 
+_AUTOGRAD_FN = None
+
+
+def _autograd_function():
+    """torch.autograd.Function whose forward is monarch_attn_fwd and whose
+    backward is monarch_attn_bwd (both on torch's current stream)."""
+    global _AUTOGRAD_FN
+    if _AUTOGRAD_FN is None:
+        import torch
+
+        class MonarchAttentionFn(torch.autograd.Function):
+            @staticmethod
+            def forward(ctx, q, k, v, m, b, T):
+                q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
+                ctx.save_for_backward(q, k, v)
+                ctx.shape = (m, b, T)
+                out = torch.empty_like(q)
+                return monarch_attn_fwd(q, k, v, out, m, b, T)
+
+            @staticmethod
+            def backward(ctx, dout):
+                q, k, v = ctx.saved_tensors
+                m, b, T = ctx.shape
+                dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+                monarch_attn_bwd(q, k, v, dout.contiguous(), dq, dk, dv, m, b, T)
+                return dq, dk, dv, None, None, None
+
+        _AUTOGRAD_FN = MonarchAttentionFn
+    return _AUTOGRAD_FN
+
+
+def monarch_attention_autograd(q, k, v, m: int, b: int, T: int):
+    """MonarchAttention as a differentiable torch op: the forward pass and, on
+    backward, the gradient (monarch_attn_bwd) with respect to q, k and v."""
+    return _autograd_function().apply(q, k, v, m, b, T)
+
+
 def monarch_attn_check(N: int, d: int, m: int, b: int, T: int, dtype: int) -> int:
     return LIB.monarch_attn_check(N, d, m, b, T, dtype)
 

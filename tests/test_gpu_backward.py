@@ -304,3 +304,22 @@ def test_timing_reports_every_gradient_launch(ma):
     recompute = ["r_half_step", "l_half_step"] * (T - 1) + ["r_half_step_final"]
     assert kinds == recompute + ["l_bwd", "r_bwd"] * T, kinds
     assert all(t > 0 for _, t in recs)
+
+
+def test_autograd_function_matches_oracle(ma):
+    """loss.backward() through monarch_attention_autograd gives the oracle's
+    gradients (the binding's torch.autograd.Function around fwd and bwd)."""
+    import torch
+
+    B, H, n, m, b, d, T = 1, 2, 200, 15, 14, 64, 2
+    q, k, v = si.random_qkv(B, H, n, d, "bf16", seed=9)
+    g = si.random_cotangent((B, H, n, d), "bf16", seed=9)
+    tq, tk, tv = (torch.from_numpy(x).to(torch.bfloat16).cuda().requires_grad_() for x in (q, k, v))
+    out = ma.monarch_attention_autograd(tq, tk, tv, m, b, T)
+    (out * torch.from_numpy(g).to(torch.bfloat16).cuda()).float().sum().backward()
+    torch.cuda.synchronize()
+    got = [x.grad.double().cpu().numpy() for x in (tq, tk, tv)]
+    ref = oracle_grads(q, k, v, g, m, b, T, [(0, 0), (0, 1)])
+    check(got, ref, [(0, 0), (0, 1)], "bf16", "autograd function")
+    fwd = oracle.monarch_attention(q, k, v, m, b, T)
+    assert oracle.rel_frobenius(out.detach().double().cpu().numpy(), fwd) <= 2e-2
