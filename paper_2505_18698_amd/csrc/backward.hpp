@@ -82,37 +82,42 @@ template <int S, int D> struct Geo {
     static constexpr int lds_floats(int c) { return 2 * S * LD + 3 * c * LD + 2 * c * LS + 2 * S; }
     static constexpr int C = lds_floats(S) <= 40960 ? S : lds_floats(32) <= 40960 ? 32 : 16;
     static constexpr int NCH = S / C;
-    static constexpr int CPL = S > 64 ? S / 64 : 1;  // score columns per lane in the row passes
+    // row passes: a row of S scores spans SPAN lanes (CPL columns each), a wave
+    // instruction covers RPW rows
+    static constexpr int SPAN = S < 64 ? S : 64, RPW = 64 / SPAN, CPL = S > 64 ? S / 64 : 1;
     static_assert(lds_floats(C) <= 40960, "tile shape exceeds the LDS of one CU");
 };
 
-// Reductions over the 64 lanes with no LDS round trip: DPP within rows of 16
-// lanes (xor 1, xor 2, then mirrors of 8 and 16 lanes), then the permlane
-// swaps across rows.  Every lane ends with the same value.
+// Cross-lane reductions with no LDS round trip.
 template <int CTRL> __device__ inline float dpp(float x)
 {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xf, 0xf, false));
 }
 constexpr int kQuadXor1 = 0xB1, kQuadXor2 = 0x4E, kRowHalfMirror = 0x141, kRowMirror = 0x140;
 
-__device__ inline float wave_sum(float x)
+// Sum and max over groups of G consecutive lanes (G = 16, 32 or 64): DPP
+// within rows of 16 lanes, then the permlane swaps across rows as far as the
+// group reaches.  Every lane of a group ends with the group's value.
+template <int G> __device__ inline float group_sum(float x)
 {
     x += dpp<kQuadXor1>(x);
     x += dpp<kQuadXor2>(x);
     x += dpp<kRowHalfMirror>(x);
     x += dpp<kRowMirror>(x);
-    x = wave_xor_sum<16>(x);
-    return wave_xor_sum<32>(x);
+    if constexpr (G >= 32) x = wave_xor_sum<16>(x);
+    if constexpr (G >= 64) x = wave_xor_sum<32>(x);
+    return x;
 }
 
-__device__ inline float wave_max(float x)
+template <int G> __device__ inline float group_max(float x)
 {
     x = fmaxf(x, dpp<kQuadXor1>(x));
     x = fmaxf(x, dpp<kQuadXor2>(x));
     x = fmaxf(x, dpp<kRowHalfMirror>(x));
     x = fmaxf(x, dpp<kRowMirror>(x));
-    x = wave_xor_max<16>(x);
-    return wave_xor_max<32>(x);
+    if constexpr (G >= 32) x = wave_xor_max<16>(x);
+    if constexpr (G >= 64) x = wave_xor_max<32>(x);
+    return x;
 }
 
 // Operands of a product, as LDS tiles with row strides LA, LB:
@@ -262,6 +267,7 @@ __device__ inline void load_tile(float *dst, int nr, int nc, Src src, int tid)
 template <typename T, int S, int D, bool LAST> struct LBwd {
     using G_ = Geo<S, D>;
     static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
+    static constexpr int SPAN = G_::SPAN, RPW = G_::RPW;
     static constexpr int LDS_FLOATS = 2 * S * LD + 2 * C * LD + 2 * C * LS + 2 * S;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
@@ -307,33 +313,31 @@ template <typename T, int S, int D, bool LAST> struct LBwd {
             // unnormalised scores <Qbar[l], alpha_L[k]>
             gemm<W, C, S, D>(wave, lane, to_lds<LS>(Lm), pair<false, true, LD, LD>(Qb, aL));
             __syncthreads();
-            // L[l][k] = softmax_k (s score - c_L[k]): one wave per row l, CPL columns k per lane
-            for (int l = wave; l < C; l += W) {
-                float* row = Lm + l * LS;
-                if (l0 + l >= m) {
-#pragma unroll
-                    for (int u = 0; u < CPL; ++u)
-                        if (lane + 64 * u < S) row[lane + 64 * u] = 0.f;
-                    continue;
-                }
+            // L[l][k] = softmax_k (s score - c_L[k]): RPW rows l per wave instruction,
+            // SPAN lanes and CPL columns k per lane for each
+            for (int base = wave * RPW; base < C; base += W * RPW) {
+                const int l = base + lane / SPAN, col = lane % SPAN;
+                const bool live = l0 + l < m;
+                float *row = Lm + l * LS;
                 float z[CPL], mx = -INFINITY;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
-                    const int k = lane + 64 * u;
-                    z[u] = k < m ? dm.s * row[k] - cL[k] : -INFINITY;
+                    const int k = col + 64 * u;
+                    z[u] = live && k < m ? dm.s * row[k] - cL[k] : -INFINITY;
                     mx = fmaxf(mx, z[u]);
                 }
-                mx = wave_max(mx);
+                mx = group_max<SPAN>(mx);
                 float sum = 0.f;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
-                    z[u] = lane + 64 * u < m ? __expf(z[u] - mx) : 0.f;
+                    z[u] = live && col + 64 * u < m ? __expf(z[u] - mx) : 0.f;
                     sum += z[u];
                 }
-                const float inv = 1.f / wave_sum(sum);
+                sum = group_sum<SPAN>(sum);
+                const float inv = live ? 1.f / sum : 0.f;  // rows past m: all zero
 #pragma unroll
                 for (int u = 0; u < CPL; ++u)
-                    if (lane + 64 * u < S) row[lane + 64 * u] = z[u] * inv;
+                    if (col + 64 * u < S) row[col + 64 * u] = z[u] * inv;
             }
             __syncthreads();
 
@@ -348,20 +352,21 @@ template <typename T, int S, int D, bool LAST> struct LBwd {
             }
             __syncthreads();
             // dW = s L (dL - <L, dL>), in place of dL
-            for (int l = wave; l < C; l += W) {
+            for (int base = wave * RPW; base < C; base += W * RPW) {
+                const int l = base + lane / SPAN, col = lane % SPAN;
                 float *lr = Lm + l * LS, *wr = dL + l * LS;
                 float pk[CPL], w[CPL], dot = 0.f;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
-                    const int k = lane + 64 * u;
+                    const int k = col + 64 * u;
                     pk[u] = k < S ? lr[k] : 0.f;
                     w[u] = k < S ? wr[k] + dcR[k] : 0.f;
                     dot += pk[u] * w[u];
                 }
-                dot = wave_sum(dot);
+                dot = group_sum<SPAN>(dot);
 #pragma unroll
                 for (int u = 0; u < CPL; ++u)
-                    if (lane + 64 * u < S) wr[lane + 64 * u] = dm.s * pk[u] * (w[u] - dot);
+                    if (col + 64 * u < S) wr[col + 64 * u] = dm.s * pk[u] * (w[u] - dot);
             }
             __syncthreads();
 
@@ -408,6 +413,7 @@ template <typename T, int S, int D, bool LAST> struct LBwd {
 template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
     using G_ = Geo<S, D>;
     static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
+    static constexpr int SPAN = G_::SPAN, RPW = G_::RPW;
     static constexpr int LDS_FLOATS = (LAST ? 2 : 1) * S * LD + (LAST ? 3 : 2) * C * LD + 2 * C * LS + 2 * C;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
@@ -460,47 +466,45 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
                 gemm<W, C, S, D>(wave, lane, to_lds<LS>(dR), pair<false, true, LD, LD>(dA, Kb));
             }
             __syncthreads();
-            // per row j (one wave, CPL keys i per lane): R, then dZ scaled by s / c_R[j] in place of dR
-            for (int jj = wave; jj < C; jj += W) {
+            // per row j (RPW rows per wave instruction, SPAN lanes and CPL keys i per
+            // lane for each): R, then dZ scaled by s / c_R[j] in place of dR
+            for (int base = wave * RPW; base < C; base += W * RPW) {
+                const int jj = base + lane / SPAN, col = lane % SPAN;
+                const bool live = jj < jb;
                 float *rr = Rm + jj * LS, *dr = dR + jj * LS;
-                if (jj >= jb) {
-#pragma unroll
-                    for (int u = 0; u < CPL; ++u)
-                        if (lane + 64 * u < S) rr[lane + 64 * u] = dr[lane + 64 * u] = 0.f;
-                    continue;
-                }
-                const float sc = dm.s / cR[jj];
+                const float sc = dm.s / cR[jj];  // c_R = 1 past the live rows
                 float z[CPL], mx = -INFINITY;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
-                    const int i = lane + 64 * u;
-                    z[u] = i < kv ? sc * rr[i] : -INFINITY;
+                    const int i = col + 64 * u;
+                    z[u] = live && i < kv ? sc * rr[i] : -INFINITY;
                     mx = fmaxf(mx, z[u]);
                 }
-                mx = wave_max(mx);
+                mx = group_max<SPAN>(mx);
+                if (!live) mx = 0.f;  // rows past b: every term below is zero
                 float e[CPL], sum = 0.f;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
-                    e[u] = lane + 64 * u < kv ? __expf(z[u] - mx) : 0.f;
+                    e[u] = live && col + 64 * u < kv ? __expf(z[u] - mx) : 0.f;
                     sum += e[u];
                 }
-                sum = wave_sum(sum);
-                const float lsum = __logf(sum), inv = 1.f / sum;
+                sum = group_sum<SPAN>(sum);
+                const float lsum = live ? __logf(sum) : 0.f, inv = live ? 1.f / sum : 0.f;
                 float r[CPL], logr[CPL], g[CPL], dot = 0.f;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
-                    const int i = lane + 64 * u;
-                    const bool live = i < kv;
+                    const int i = col + 64 * u;
+                    const bool on = live && i < kv;
                     r[u] = e[u] * inv;
-                    logr[u] = live ? z[u] - mx - lsum : 0.f;
-                    g[u] = live ? dr[i] + dcL[jj] * (logr[u] + 1.f) : 0.f;
+                    logr[u] = on ? z[u] - mx - lsum : 0.f;
+                    g[u] = on ? dr[i] + dcL[jj] * (logr[u] + 1.f) : 0.f;
                     dot += r[u] * g[u];
                 }
-                dot = wave_sum(dot);
+                dot = group_sum<SPAN>(dot);
                 float dzlog = 0.f;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
-                    const int i = lane + 64 * u;
+                    const int i = col + 64 * u;
                     const float dz = r[u] * (g[u] - dot);
                     dzlog += dz * logr[u];
                     if (i < S) {
@@ -508,8 +512,8 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
                         dr[i] = dz * sc;
                     }
                 }
-                dzlog = wave_sum(dzlog);
-                if (!FIRST && lane == 0) p.dcR[coff + row0 + j0 + jj] = -dzlog / cR[jj];
+                dzlog = group_sum<SPAN>(dzlog);
+                if (!FIRST && live && col == 0) p.dcR[coff + row0 + j0 + jj] = -dzlog / cR[jj];
             }
             __syncthreads();
 
