@@ -56,9 +56,10 @@ typedef enum {
  *           aligned, not overlapping q, k or v.  Fully overwritten.
  *           All four buffers are owned by the caller; the library neither
  *           frees nor retains them.
- * B, H    : batch and head counts (>= 1).
+ * B, H    : batch and head counts (>= 0).
  * N, m, b : sequence length, number of blocks and block size:
- *           m = ceil(N / b), i.e. (m - 1) * b < N <= m * b.  When N < m * b
+ *           m = ceil(N / b), i.e. (m - 1) * b < N <= m * b (m = 0 for an
+ *           empty sequence, N = 0; b >= 1).  When N < m * b
  *           the sequence is post-padded to m * b rows as in Appendix
  *           "Padding and Masking": the padded rows of Q, K, V count as zero
  *           rows (they are not read), keys at positions >= N are masked out
@@ -75,7 +76,10 @@ typedef enum {
  * stream  : the hipStream_t to launch on (NULL = the null stream).
  *
  * Asynchronous on `stream`: returns after enqueueing, with no host
- * synchronisation.  Arguments are checked before any HIP call; on MA_EINVAL or
+ * synchronisation.  A call with B, H or N zero has nothing to compute: once
+ * the other arguments check out it returns MA_OK, launching nothing and
+ * reading no pointer (they may be NULL); this holds for every entry point.
+ * Arguments are checked before any HIP call; on MA_EINVAL or
  * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  Path 1 (see
  * monarch_attn_set_path) uses a device workspace (3 m b D elements plus 2 m b
  * floats per head) owned by the library, one per (device, stream): calls on

@@ -40,8 +40,8 @@ size_t elem_bytes(int32_t dtype) { return dtype == MA_F32 ? 4 : 2; }
 int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype)
 {
     if (dtype != MA_F32 && dtype != MA_BF16 && dtype != MA_F16) return fail(MA_EINVAL, "unknown dtype %d", dtype);
-    if (m < 1 || b < 1 || N < 1 || d < 1) return fail(MA_EINVAL, "N, d, m, b must be >= 1");
-    if (N > m * b || N <= (m - 1) * b)
+    if (b < 1 || d < 1 || N < 0 || m < 0) return fail(MA_EINVAL, "N, m must be >= 0 and d, b >= 1");
+    if (N == 0 ? m != 0 : (m < 1 || N > m * b || N <= (m - 1) * b))
         return fail(MA_EINVAL, "m (%lld) must be ceil(N / b) (N = %lld, b = %lld)", (long long)m, (long long)N,
                     (long long)b);
     if (T < 1) return fail(MA_EINVAL, "T must be >= 1 (got %d)", T);
@@ -154,14 +154,17 @@ int acquire_workspace(int dev, hipStream_t stream, size_t need, char **base, std
 }
 
 // The forward pass; with obj != nullptr also the objective per (head, step).
-int forward(const void *q, const void *k, const void *v, void *out, float *obj, int64_t B, int64_t H, int64_t N,
-            int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
+int forward(const void *q, const void *k, const void *v, void *out, float *obj, bool need_obj, int64_t B, int64_t H,
+            int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
 {
     g_err[0] = '\0';
-    if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
-    if (B < 1 || H < 1) return fail(MA_EINVAL, "B and H must be >= 1");
+    if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
     int rc = check_shape(N, d, m, b, T, dtype);
     if (rc != MA_OK) return rc;
+    if (B == 0 || H == 0 || N == 0) return MA_OK;  // nothing to compute: no launch, no pointer read
+    if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
+    if (need_obj && !obj) return fail(MA_EINVAL, "null objective pointer");
+    if (need_obj && ((uintptr_t)obj & 3u)) return fail(MA_EINVAL, "obj must be 4-byte aligned");
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)out) & 15u)
         return fail(MA_EINVAL, "q, k, v and out must be 16-byte aligned");
     const int64_t BH = B * H;
@@ -259,10 +262,11 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
              int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
 {
     g_err[0] = '\0';
-    if (!q || !k || !v || !dout || !dq || !dk || !dv) return fail(MA_EINVAL, "null tensor pointer");
-    if (B < 1 || H < 1) return fail(MA_EINVAL, "B and H must be >= 1");
+    if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
     int rc = check_bwd_shape(N, d, m, b, T, dtype);
     if (rc != MA_OK) return rc;
+    if (B == 0 || H == 0 || N == 0) return MA_OK;  // nothing to compute: no launch, no pointer read
+    if (!q || !k || !v || !dout || !dq || !dk || !dv) return fail(MA_EINVAL, "null tensor pointer");
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)dout | (uintptr_t)dq | (uintptr_t)dk |
          (uintptr_t)dv) & 15u)
         return fail(MA_EINVAL, "all tensors must be 16-byte aligned");
@@ -416,19 +420,20 @@ int32_t monarch_attn_timing_read(float *ms, int32_t *kind, int32_t cap)
 int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int64_t B, int64_t H, int64_t N,
                      int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
 {
-    return forward(q, k, v, out, nullptr, B, H, N, d, m, b, T, dtype, stream);
+    return forward(q, k, v, out, nullptr, false, B, H, N, d, m, b, T, dtype, stream);
 }
 
 int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *out, float *lse, int64_t B,
                            int64_t H, int64_t N, int64_t d, int32_t dtype, void *stream)
 {
     g_err[0] = '\0';
-    if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
-    if (B < 1 || H < 1 || N < 1 || d < 1) return fail(MA_EINVAL, "B, H, N and d must be >= 1");
+    if (B < 0 || H < 0 || N < 0 || d < 1) return fail(MA_EINVAL, "B, H, N must be >= 0 and d >= 1");
     if (dtype != MA_F32 && dtype != MA_BF16 && dtype != MA_F16) return fail(MA_EINVAL, "unknown dtype %d", dtype);
     if (d > 128 || d % (16 / (int64_t)elem_bytes(dtype)) != 0)
         return fail(MA_EUNSUPPORTED, "d must be a multiple of %d up to 128 (got %lld)", (int)(16 / elem_bytes(dtype)),
                     (long long)d);
+    if (B == 0 || H == 0 || N == 0) return MA_OK;  // nothing to compute: no launch, no pointer read
+    if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
     if (N > 0x7fffffff) return fail(MA_EUNSUPPORTED, "N too large");
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)out) & 15u)
         return fail(MA_EINVAL, "q, k, v and out must be 16-byte aligned");
@@ -467,10 +472,7 @@ int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void
                                int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
                                void *stream)
 {
-    g_err[0] = '\0';
-    if (!obj) return fail(MA_EINVAL, "null objective pointer");
-    if ((uintptr_t)obj & 3u) return fail(MA_EINVAL, "obj must be 4-byte aligned");
-    return forward(q, k, v, out, obj, B, H, N, d, m, b, T, dtype, stream);
+    return forward(q, k, v, out, obj, true, B, H, N, d, m, b, T, dtype, stream);
 }
 
 int monarch_attn_bwd(const void *q, const void *k, const void *v, const void *dout, void *dq, void *dk, void *dv,

@@ -40,7 +40,9 @@ FAKE = 1 << 20  # an aligned non-null address that is never dereferenced: every 
         # (q, k, v, out, B, H, N, d, m, b, T, dtype)
         ((0, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),           # null q
         ((FAKE, FAKE, FAKE, 0, 1, 1, 256, 64, 16, 16, 1, 1), 1),               # null out
-        ((FAKE, FAKE, FAKE, 2 * FAKE, 0, 1, 256, 64, 16, 16, 1, 1), 1),        # B = 0
+        ((FAKE, FAKE, FAKE, 2 * FAKE, -1, 1, 256, 64, 16, 16, 1, 1), 1),       # B < 0
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 0, 64, 1, 16, 1, 1), 1),           # N = 0 needs m = 0
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 16, 64, 0, 16, 1, 1), 1),          # m = 0 needs N = 0
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 257, 64, 16, 16, 1, 1), 1),        # N > m b
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 240, 64, 16, 16, 1, 1), 1),        # m > ceil(N / b)
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 0, 1), 1),        # T = 0
@@ -160,7 +162,7 @@ def test_objective_rejects_null_obj():
         # (q, k, v, dout, dq, dk, dv, B, H, N, d, m, b, T, dtype)
         ((FAKE, FAKE, FAKE, FAKE, 0, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),           # null dq
         ((FAKE, FAKE, FAKE, 0, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),       # null dout
-        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 0, 256, 64, 16, 16, 1, 1), 1),    # H = 0
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, -2, 256, 64, 16, 16, 1, 1), 1),   # H < 0
         ((FAKE, FAKE, FAKE, FAKE, FAKE + 64, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),   # dq overlaps q
         ((FAKE, FAKE, FAKE, 5 * FAKE, 2 * FAKE, 3 * FAKE, 5 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),  # dv overlaps dout
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 2 * FAKE + 64, 4 * FAKE, 1, 1, 256, 64, 16, 16, 1, 1), 1),  # dk overlaps dq
@@ -231,3 +233,18 @@ def test_bwd_workspace_bytes_formula():
     acc, sg = _align(BH * N * d * 4), _align(BH * Np * 96 * 4)
     assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_BF16) == \
         2 * T * st + (2 * T - 1) * cs + 2 * acc + 3 * sg + 2 * cs
+
+
+@pytest.mark.parametrize("B,H,N,m", [(0, 4, 256, 16), (2, 0, 256, 16), (2, 4, 0, 0)])
+def test_empty_calls_succeed_without_touching_pointers(B, H, N, m):
+    """Nothing to compute: every entry point returns MA_OK with NULL pointers
+    and launches nothing (no GPU is needed to run this)."""
+    import paper_2505_18698_amd as ma
+
+    assert ma.monarch_attn_fwd_raw(0, 0, 0, 0, B, H, N, 64, m, 16, 2, 1, None) == ma.MA_OK
+    assert ma.LIB.monarch_attn_fwd_objective(None, None, None, None, None, B, H, N, 64, m, 16, 2, 1, None) == ma.MA_OK
+    assert ma.LIB.monarch_attn_bwd(None, None, None, None, None, None, None, B, H, N, 64, m, 16, 2, 1, None) == ma.MA_OK
+    assert ma.LIB.monarch_attn_exact_fwd(None, None, None, None, None, B, H, N, 64, 1, None) == ma.MA_OK
+    # the other arguments are still checked
+    assert ma.monarch_attn_fwd_raw(0, 0, 0, 0, B, H, N, 64, m, 16, 2, 9, None) == ma.MA_EINVAL
+    assert ma.monarch_attn_fwd_raw(0, 0, 0, 0, B, H, N, 100, m, 16, 2, 1, None) == ma.MA_EUNSUPPORTED

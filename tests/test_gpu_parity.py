@@ -540,3 +540,21 @@ def test_concurrent_streams_get_separate_workspaces(lib):
             check(o.double().cpu().numpy(), ref, "bf16", "concurrent streams")
     finally:
         lib.monarch_attn_set_path(prev)
+
+
+@pytest.mark.parametrize("shape,m", [((0, 4, 256, 64), 16), ((2, 0, 256, 64), 16), ((2, 4, 0, 64), 0)])
+def test_empty_tensors(lib, shape, m):
+    """Empty batches, heads or sequences through the binding: every entry point
+    returns an empty result without error."""
+    import torch
+
+    q, k, v, g = (torch.empty(shape, device="cuda", dtype=torch.bfloat16) for _ in range(4))
+    out = lib.monarch_attn_fwd(q, k, v, torch.empty_like(q), m, 16, 2)
+    assert out.shape == shape
+    obj = torch.empty((shape[0], shape[1], 2), device="cuda", dtype=torch.float32)
+    lib.monarch_attn_fwd_objective(q, k, v, torch.empty_like(q), obj, m, 16, 2)
+    lse = torch.empty(shape[:3], device="cuda", dtype=torch.float32)
+    lib.monarch_attn_exact_fwd(q, k, v, torch.empty_like(q), lse)
+    dq, dk, dv = lib.monarch_attn_bwd(q, k, v, g, *(torch.empty_like(q) for _ in range(3)), m, 16, 2)
+    assert dq.shape == dk.shape == dv.shape == shape
+    torch.cuda.synchronize()
