@@ -61,17 +61,13 @@ struct BwdDims {
 
 namespace bwd {
 
-// Row strides (floats) of the LDS tiles of up to 128 columns: 16-byte rows
-// whose starting banks (mod 64) are 20 or 36 apart, so that 16 lanes reading
-// one row each (as the MFMA A operand) and 16 lanes reading one column of four
-// rows (transposed) both hit distinct banks.
-constexpr int row_stride(int cols) { return cols <= 64 ? 84 : cols <= 96 ? 100 : 148; }
+// Row strides (floats) of the LDS tiles: 16-byte rows, 68 floats for tiles
+// of up to 64 columns, 100 and 148 for 96 and 128.  The 64-column stride is
+// the smallest measured: at 16-row units the smaller tiles let six workgroups
+// share a CU instead of five (11% faster), and strides of 72 to 88 were no
+// faster at 64 or 128 rows.
+constexpr int row_stride(int cols) { return cols <= 64 ? 68 : cols <= 96 ? 100 : 148; }
 
-// Shape of the units for tiles of S rows (S = 16, 32, 64 or 128 >= m, b) and
-// D columns (the state width, 64, 96 or 128): W waves (one 16 x 16 output
-// tile of the widest product each), rows walked in chunks of C (as large as
-// the 160 KB of LDS allows), and the row strides LD of the D-wide tiles and
-// LS of the C x S score tiles.
 constexpr int unit_waves(int S) { return S >= 64 ? 16 : S / 4; }
 
 template <int S, int D> struct Geo {
