@@ -52,6 +52,9 @@ def _load():
         lib.ma_oracle_max_threads.restype = ctypes.c_int
         lib.ma_oracle_fwd_obj_f64.argtypes = [dp, dp, dp, dp, dp, i64, i64, i64, i64, i64, i64, i32, i32]
         lib.ma_oracle_fwd_obj_f64.restype = ctypes.c_int
+        lib.ma_oracle_fwd_varlen_f64.argtypes = [dp, dp, dp, dp, ctypes.POINTER(ctypes.c_int64),
+                                                 i64, i64, i64, i64, i64, i64, i32, i32]
+        lib.ma_oracle_fwd_varlen_f64.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -89,6 +92,26 @@ def monarch_attention_objective(q, k, v, m: int, b: int, T: int, threads: int = 
     if rc != 0:
         raise ValueError(f"oracle rejected the arguments (code {rc})")
     return out, obj
+
+
+def monarch_attention_varlen(q, k, v, lens, m: int, b: int, T: int, threads: int = 0) -> np.ndarray:
+    """O for a batch of post-padded sequences: q, k, v float64 [B, H, N, d],
+    lens[B] real rows per batch element (0..N); rows >= lens[beta] of O are
+    zero.  Whole key blocks of padding get R = 0 and no L weight."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    B, H, N, d = q.shape
+    lens = np.ascontiguousarray(lens, dtype=np.int64)
+    if lens.shape != (B,):
+        raise ValueError("lens must hold one length per batch element")
+    out = np.empty_like(q)
+    rc = _load().ma_oracle_fwd_varlen_f64(_dptr(q), _dptr(k), _dptr(v), _dptr(out),
+                                          lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                          B, H, N, d, m, b, T, threads)
+    if rc != 0:
+        raise ValueError(f"oracle rejected the arguments (code {rc})")
+    return out
 
 
 def dense_attention_rows(q, k, v, rows=None, threads: int = 0) -> np.ndarray:

@@ -48,6 +48,15 @@
  * row), the mask omega adds -inf to Z_R for every key position k*b + i >= N
  * before the softmax of eq. R_update, so that the last N' - N columns of M
  * are zero, and only the first N rows of O are returned.
+ *
+ * Batched sequences padded to a common length (the same appendix): with
+ * ma_oracle_fwd_varlen_f64, head h of batch element beta has lens[beta] <= N
+ * real rows and keeps the batch's m and b, so whole key blocks can be
+ * padding.  Such a block has no defined R softmax (every entry of its omega
+ * row is -inf); the reading taken here gives it R = 0 (so alpha_L, c_L and Y
+ * of that block are zero) and leaves it out of the L softmax (Z_L = -inf),
+ * so that M keeps unit row sums; with no real key at all L = 0.  Rows >=
+ * lens[beta] of O are zero.
  */
 #include <math.h>
 #include <stdint.h>
@@ -71,6 +80,14 @@ static void r_half_step(const double *Kh, const double *Vh, const double *aR, co
 {
     const double *Kk = Kh + k * b * d; /* Kbar[k][i] = K[k*b + i] */
     const double *Vk = Vh ? Vh + k * b * d : NULL;
+    if (nkeys <= 0) { /* a block of padding only: R[k] = 0 */
+        for (int64_t j = 0; j < b; ++j) {
+            cL[j * m + k] = 0.0;
+            memset(aL + (j * m + k) * d, 0, (size_t)d * sizeof(double));
+            if (Y) memset(Y + (j * m + k) * d, 0, (size_t)d * sizeof(double));
+        }
+        return;
+    }
     for (int64_t j = 0; j < b; ++j) {
         const double *a = aR + (k * b + j) * d;
         const double c = cR[k * b + j];
@@ -117,10 +134,12 @@ static void r_half_step(const double *Kh, const double *Vh, const double *aR, co
  * in the separable form of Sec. 3 ("Softmax Objective"):
  *   sum_k <alpha_R[k][j], alpha_L[j][k]> + (1^T R_kj) H(L_jk) + (1^T L_jk) H(R_kj),
  * with 1^T R_kj = 1, 1^T L_jk = c_R[k][j], H(R_kj) = -c_L[j][k] and
- * H(L_jk) = -sum_l L log L (hl: m doubles of scratch). */
+ * H(L_jk) = -sum_l L log L (hl: m doubles of scratch).  Key blocks k >= live
+ * hold no real key (batch padding): Z_L = -inf for them, and L = 0 when live
+ * is 0. */
 static void l_half_step(const double *Qs, const double *aL, const double *cL, const double *Y,
                         double *aR, double *cR, double *O, int64_t m, int64_t b, int64_t d,
-                        int64_t j, double *z, double *fj, double *hl)
+                        int64_t j, int64_t live, double *z, double *fj, double *hl)
 {
     if (fj) {
         for (int64_t k = 0; k < m; ++k) hl[k] = 0.0;
@@ -138,15 +157,19 @@ static void l_half_step(const double *Qs, const double *aL, const double *cL, co
             const double *al = aL + (j * m + k) * d;
             double beta = 0.0;
             for (int64_t v = 0; v < d; ++v) beta += al[v] * qb[v];
-            z[k] = beta - cL[j * m + k];
+            z[k] = k < live ? beta - cL[j * m + k] : -INFINITY;
             if (z[k] > zmax) zmax = z[k];
         }
-        double sum = 0.0;
-        for (int64_t k = 0; k < m; ++k) {
-            z[k] = exp(z[k] - zmax);
-            sum += z[k];
+        if (live > 0) {
+            double sum = 0.0;
+            for (int64_t k = 0; k < m; ++k) {
+                z[k] = exp(z[k] - zmax);
+                sum += z[k];
+            }
+            for (int64_t k = 0; k < m; ++k) z[k] /= sum; /* z now holds L[j][:][l] */
+        } else {
+            for (int64_t k = 0; k < m; ++k) z[k] = 0.0;
         }
-        for (int64_t k = 0; k < m; ++k) z[k] /= sum; /* z now holds L[j][:][l] */
         if (fj) {
             for (int64_t k = 0; k < m; ++k)
                 if (z[k] > 0.0) hl[k] -= z[k] * log(z[k]);
@@ -181,14 +204,20 @@ static void l_half_step(const double *Qs, const double *aL, const double *cL, co
 
 /* The forward pass; obj (NULL, or B*H*T doubles) receives f(M^(t); Q, K)
  * after every step t (the objective of Sec. 3 with the factors of step t, on
- * all m*b rows of the padded problem): obj[(h * T) + t - 1]. */
-int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, double *out, double *obj,
-                          int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
-                          int32_t threads)
+ * all m*b rows of the padded problem): obj[(h * T) + t - 1].  lens (NULL, or
+ * B lengths <= N) gives the real rows of each batch element. */
+static int forward(const double *q, const double *k, const double *v, double *out, double *obj,
+                   const int64_t *lens, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b,
+                   int32_t T, int32_t threads)
 {
     if (!q || !k || !v || !out) return MO_EINVAL;
     if (B < 1 || H < 1 || d < 1 || m < 1 || b < 1 || T < 1 || N < 1) return MO_EINVAL;
     if (N > m * b || N <= (m - 1) * b) return MO_EINVAL; /* m = ceil(N / b) */
+    if (lens) {
+        if (obj) return MO_EINVAL;
+        for (int64_t e = 0; e < B; ++e)
+            if (lens[e] < 0 || lens[e] > N) return MO_EINVAL;
+    }
     const int64_t BH = B * H, Np = m * b, nd = Np * d;
     const double s = 1.0 / sqrt((double)d);
     /* Q (scaled), K, V post-padded with zero rows to Np = m*b; O on Np rows */
@@ -215,7 +244,7 @@ int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, dou
 
 #pragma omp parallel for schedule(static) num_threads(nt)
     for (int64_t h = 0; h < BH; ++h)
-        for (int64_t e = 0; e < N * d; ++e) {
+        for (int64_t e = 0; e < (lens ? lens[h / H] : N) * d; ++e) { /* rows >= the length stay zero */
             Qs[h * nd + e] = s * q[h * N * d + e]; /* scale absorbed into Q */
             Kp[h * nd + e] = k[h * N * d + e];
             Vp[h * nd + e] = v[h * N * d + e];
@@ -235,7 +264,8 @@ int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, dou
 #pragma omp for collapse(2) schedule(static)
             for (int64_t h = 0; h < BH; ++h)
                 for (int64_t kk = 0; kk < m; ++kk) {
-                    const int64_t nkeys = N - kk * b < b ? N - kk * b : b;
+                    const int64_t n = lens ? lens[h / H] : N;
+                    const int64_t nkeys = n - kk * b < b ? n - kk * b : b; /* <= 0: padding only */
                     r_half_step(Kp + h * nd, last ? Vp + h * nd : NULL, aR + h * nd, cR + h * Np,
                                 aL + h * nd, cL + h * Np, last ? Y + h * nd : NULL, m, b, d, kk, nkeys, z);
                 }
@@ -243,8 +273,8 @@ int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, dou
             for (int64_t h = 0; h < BH; ++h)
                 for (int64_t j = 0; j < b; ++j)
                     l_half_step(Qs + h * nd, aL + h * nd, cL + h * Np, Y + h * nd, aR + h * nd,
-                                cR + h * Np, last ? Op + h * nd : NULL, m, b, d, j, z,
-                                obj ? fpart + h * b + j : NULL, hl);
+                                cR + h * Np, last ? Op + h * nd : NULL, m, b, d, j,
+                                lens ? (lens[h / H] + b - 1) / b : m, z, obj ? fpart + h * b + j : NULL, hl);
             free(z);
             free(hl);
         }
@@ -256,12 +286,31 @@ int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, dou
             }
         }
     }
-    /* the first N rows of every head */
+    /* the first N rows of every head; with lens, zero beyond the length */
 #pragma omp parallel for schedule(static) num_threads(nt)
-    for (int64_t h = 0; h < BH; ++h)
-        memcpy(out + h * N * d, Op + h * nd, sizeof(double) * (size_t)(N * d));
+    for (int64_t h = 0; h < BH; ++h) {
+        const int64_t n = lens ? lens[h / H] : N;
+        memcpy(out + h * N * d, Op + h * nd, sizeof(double) * (size_t)(n * d));
+        memset(out + h * N * d + n * d, 0, sizeof(double) * (size_t)((N - n) * d));
+    }
     free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
     return MO_OK;
+}
+
+int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, double *out, double *obj,
+                          int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
+                          int32_t threads)
+{
+    return forward(q, k, v, out, obj, NULL, B, H, N, d, m, b, T, threads);
+}
+
+/* Batch padding: lens[B] real rows per batch element (0 <= lens <= N). */
+int ma_oracle_fwd_varlen_f64(const double *q, const double *k, const double *v, double *out,
+                             const int64_t *lens, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m,
+                             int64_t b, int32_t T, int32_t threads)
+{
+    if (!lens) return MO_EINVAL;
+    return forward(q, k, v, out, NULL, lens, B, H, N, d, m, b, T, threads);
 }
 
 int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double *out, int64_t B,

@@ -19,6 +19,14 @@ Masking": m = ceil(N / b), Q, K, V post-padded to m*b rows (zero rows unless
 the caller passes padded arrays), the mask omega (-inf at key positions
 k*b + i >= N) added to Z_R before the softmax of eq. R_update, and the first
 N rows of O kept.
+
+The same appendix covers a batch of sequences padded to a common length.
+There m and b are fixed for the batch, so a shorter sequence can have whole
+key blocks of padding, whose row of omega is -inf throughout and whose
+softmax the paper leaves undefined.  The reading taken here
+(``batch_padding=True``): such a block gets R = 0, and the L update leaves
+it out (Z_L = -inf for it), so that M keeps unit row sums with zero columns
+at every padded key.  A sequence of length 0 has M = 0.
 """
 from __future__ import annotations
 
@@ -76,6 +84,11 @@ def key_mask(n: int, m: int, b: int) -> np.ndarray:
     return omega
 
 
+def live_blocks(n: int, b: int) -> int:
+    """Key blocks that hold at least one real key, ceil(n / b)."""
+    return -(-n // b)
+
+
 def _softmax(z: np.ndarray) -> np.ndarray:
     e = np.exp(z - z.max())
     return e / e.sum()
@@ -93,6 +106,9 @@ def r_update(L: np.ndarray, Qb: np.ndarray, Kb: np.ndarray, omega=None) -> np.nd
     R = np.empty((m, b, b))
     for k in range(m):
         for j in range(b):
+            if omega is not None and np.all(np.isneginf(omega[k])):
+                R[k, j] = 0.0                     # no real key in block k (batch padding)
+                continue
             alpha_r = L[j, k, :] @ Qb[j]          # sum_l L[j,k,l] Qbar[j,l,:]
             c_r = L[j, k, :].sum()                # sum_l L[j,k,l]
             beta_r = Kb[k] @ alpha_r              # beta_R[k,j,i] = <alpha_R[k,j], Kbar[k,i]>
@@ -103,16 +119,21 @@ def r_update(L: np.ndarray, Qb: np.ndarray, Kb: np.ndarray, omega=None) -> np.nd
     return R
 
 
-def l_update(R: np.ndarray, Qb: np.ndarray, Kb: np.ndarray) -> np.ndarray:
-    """L = softmax_k(beta_L - c_L) with beta_L, c_L from R (eqs. L_update, beta_l)."""
+def l_update(R: np.ndarray, Qb: np.ndarray, Kb: np.ndarray, live=None) -> np.ndarray:
+    """L = softmax_k(beta_L - c_L) with beta_L, c_L from R (eqs. L_update, beta_l).
+    live: key blocks k < live hold a real key; the others (batch padding) get
+    Z_L = -inf, and L = 0 when no block does."""
     m, b, _ = R.shape
-    L = np.empty((b, m, m))
+    live = m if live is None else live
+    L = np.zeros((b, m, m))
+    if live == 0:
+        return L
     for j in range(b):
         alpha_l = np.stack([R[k, j] @ Kb[k] for k in range(m)])       # [k, v]
         c_l = np.array([_xlogx_sum(R[k, j]) for k in range(m)])        # sum_i R log R
         for l in range(m):
             beta_l = alpha_l @ Qb[j, l]                                 # over k
-            L[j, :, l] = _softmax(beta_l - c_l)
+            L[j, :live, l] = _softmax((beta_l - c_l)[:live])
     return L
 
 
@@ -140,24 +161,30 @@ def monarch_apply(L: np.ndarray, R: np.ndarray, v: np.ndarray) -> np.ndarray:
     return O[:n]
 
 
-def factors(q, k, m, b, T, *, history=False, n=None):
+def factors(q, k, m, b, T, *, history=False, n=None, batch_padding=False):
     """Run T (R, L) update pairs from L^(0) = I (Sec. 3).  q, k: one head [N, d].
 
     N < m*b rows are zero-padded to m*b.  Arrays that already have m*b rows
     with n < m*b are taken as padded by the caller (rows >= n are padding,
-    whatever they hold).  Returns (L, R) after T steps; with history=True
-    also the list of (L, R) pairs after every half-step, starting with
+    whatever they hold).  With batch_padding, n may be any length 0..m*b
+    (whole blocks of padding allowed, see the module docstring); otherwise
+    m = ceil(n / b).  Returns (L, R) after T steps; with history=True also
+    the list of (L, R) pairs after every half-step, starting with
     (L^(0), None).
     """
     q, k = _f64(q, k)
     rows, d = q.shape
     n = rows if n is None else n
-    assert (m - 1) * b < n <= m * b and T >= 1        # m = ceil(N / b)
+    if batch_padding:
+        assert 0 <= n <= m * b and T >= 1
+    else:
+        assert (m - 1) * b < n <= m * b and T >= 1    # m = ceil(N / b)
     if rows < m * b:
         assert rows == n
         q, k = pad_rows(q, m, b), pad_rows(k, m, b)
     assert q.shape[0] == m * b
     omega = key_mask(n, m, b) if n < m * b else None
+    live = live_blocks(n, b)
     s = 1.0 / np.sqrt(d)
     Qb = qbar(s * q, m, b)
     Kb = kbar(k, m, b)
@@ -167,7 +194,7 @@ def factors(q, k, m, b, T, *, history=False, n=None):
     for _ in range(T):
         R = r_update(L, Qb, Kb, omega)              # R before L in every step
         hist.append((L, R))
-        L = l_update(R, Qb, Kb)
+        L = l_update(R, Qb, Kb, live)
         hist.append((L, R))
     return (L, R, hist) if history else (L, R)
 
@@ -185,6 +212,22 @@ def monarch_attention(q, k, v, m, b, T):
     for bi in range(q.shape[0]):
         for h in range(q.shape[1]):
             out[bi, h] = monarch_attention_head(q[bi, h], k[bi, h], v[bi, h], m, b, T)
+    return out
+
+
+def monarch_attention_varlen(q, k, v, lens, m, b, T):
+    """A batch of post-padded sequences: q, k, v [B, H, N, d], lens[B] <= N real
+    rows per batch element.  Each head is the single-sequence problem of its
+    first lens[beta] rows at the batch's m and b (with ``batch_padding``);
+    rows >= lens[beta] of O are zero."""
+    q, k, v = _f64(q, k, v)
+    out = np.zeros_like(v)
+    for bi in range(q.shape[0]):
+        n = int(lens[bi])
+        assert 0 <= n <= q.shape[2] <= m * b
+        for h in range(q.shape[1]):
+            L, R = factors(q[bi, h, :n], k[bi, h, :n], m, b, T, n=n, batch_padding=True)
+            out[bi, h, :n] = monarch_apply(L, R, v[bi, h, :n])
     return out
 
 

@@ -85,6 +85,39 @@ def _battery():
     if np.abs(nv.monarch_apply(L, R, v) - nv.dense_monarch(L, R) @ v).max() > 1e-12:
         failed.append("apply")
     failed += _padding_battery()
+    failed += _batch_padding_battery()
+    return failed
+
+
+def _batch_padding_battery():
+    """Pins of the batch-padding reading (whole key blocks of padding)."""
+    import oracle
+    failed = []
+    try:
+        # b = 1: exact attention over the real keys, T = 2
+        N = 8
+        q, k, v = _head(N, 1, 4, seed=600)
+        o = nv.monarch_attention_varlen(q[None, None], k[None, None], v[None, None], [5], N, 1, 2)[0, 0]
+        if np.abs(o[:5] - nv.dense_softmax_attention(q[:5], k[:5], v[:5])).max() > 1e-12 or np.any(o[5:] != 0):
+            failed.append("varlen-exact-b1")
+        # T = 1: the same real rows as the problem without the empty blocks
+        m, b, n = 4, 3, 5
+        q, k, v = _head(m, b, 5, seed=601)
+        o = nv.monarch_attention_varlen(q[None, None], k[None, None], v[None, None], [n], m, b, 1)[0, 0]
+        if np.abs(o[:n] - nv.monarch_attention_head(q[:n], k[:n], v[:n], 2, b, 1)).max() > 1e-12:
+            failed.append("varlen-fewer-blocks")
+        # M row-stochastic with zero padded columns
+        L, R = nv.factors(q[:n], k[:n], m, b, 2, n=n, batch_padding=True)
+        M = nv.dense_monarch(L, R)
+        if not (np.all(M >= 0) and np.all(M[:, n:] == 0) and np.allclose(M.sum(axis=1), 1.0, atol=1e-12)):
+            failed.append("varlen-stochastic")
+        # the state form in C agrees (T = 2)
+        ref = oracle.monarch_attention_varlen(q[None, None], k[None, None], v[None, None], np.array([n]), m, b, 2)
+        o2 = nv.monarch_attention_varlen(q[None, None], k[None, None], v[None, None], [n], m, b, 2)
+        if np.abs(o2 - ref).max() > 1e-12:
+            failed.append("varlen-two-forms")
+    except Exception:
+        failed.append("varlen-crash")
     return failed
 
 
@@ -139,6 +172,9 @@ def _r_update_variant(kind):
         for k in range(m):
             om = 0.0 if omega is None or kind == "no-mask" else omega[k]
             for j in range(b):
+                if np.all(np.isneginf(om)):
+                    R[k, j] = 0.0
+                    continue
                 a = L[j, k, :] @ Qb[j]
                 c = L[j, k, :].sum()
                 beta = Kb[k] @ a
@@ -155,21 +191,24 @@ def _r_update_variant(kind):
 
 
 def _l_update_variant(kind):
-    def l_update(R, Qb, Kb):
+    def l_update(R, Qb, Kb, live=None):
         m, b, _ = R.shape
-        L = np.empty((b, m, m))
+        live = m if live is None or kind == "empty-blocks-weighted" else live
+        L = np.zeros((b, m, m))
+        if live == 0:
+            return L
         for j in range(b):
             al = np.stack([R[k, j] @ Kb[k] for k in range(m)])
-            cl = np.array([np.sum(R[k, j] * np.log(R[k, j])) for k in range(m)])
+            cl = np.array([np.sum(R[k, j][R[k, j] > 0] * np.log(R[k, j][R[k, j] > 0])) for k in range(m)])
             if kind == "plus-c":
                 cl = -cl
             elif kind == "no-c":
                 cl = 0 * cl
             for l in range(m):
                 z = al @ Qb[j, l] - cl
-                L[j, :, l] = _softmax(z)
+                L[j, :live, l] = _softmax(z[:live])
             if kind == "softmax-over-l":
-                for k in range(m):
+                for k in range(live):
                     L[j, k, :] = _softmax(np.array([al[k] @ Qb[j, l] - cl[k] for l in range(m)]))
         return L
     return l_update
@@ -184,12 +223,13 @@ def _qbar_wrong(q, m, b):
     return q.reshape(b, m, d).copy()      # rows j*m + l instead of l*b + j
 
 
-def _factors_uniform_init(q, k, m, b, T, *, history=False, n=None):
+def _factors_uniform_init(q, k, m, b, T, *, history=False, n=None, batch_padding=False):
     rows, d = q.shape
     n = rows if n is None else n
     if rows < m * b:
         q, k = nv.pad_rows(q, m, b), nv.pad_rows(k, m, b)
     omega = nv.key_mask(n, m, b) if n < m * b else None
+    live = nv.live_blocks(n, b)
     s = 1.0 / np.sqrt(d)
     Qb, Kb = nv.qbar(s * q, m, b), nv.kbar(k, m, b)
     L = np.full((b, m, m), 1.0 / m)
@@ -197,7 +237,7 @@ def _factors_uniform_init(q, k, m, b, T, *, history=False, n=None):
     for _ in range(T):
         R = nv.r_update(L, Qb, Kb, omega)
         hist.append((L, R))
-        L = nv.l_update(R, Qb, Kb)
+        L = nv.l_update(R, Qb, Kb, live)
         hist.append((L, R))
     return (L, R, hist) if history else (L, R)
 
@@ -215,7 +255,20 @@ MUTANTS = {
     "padding: mask omitted": ("r_update", lambda: _r_update_variant("no-mask")),
     "padding: mask on the pre-padding side": ("r_update", lambda: _r_update_variant("mask-front")),
     "padding: padded with ones": ("pad_rows", lambda: _pad_ones),
+    "batch padding: empty blocks keep L weight": ("l_update", lambda: _l_update_variant("empty-blocks-weighted")),
+    "batch padding: partial block dropped": ("live_blocks", lambda: (lambda n, b: n // b)),
+    "batch padding: padded query rows dropped": ("monarch_attention_varlen", lambda: _varlen_fewer_blocks),
 }
+
+
+def _varlen_fewer_blocks(q, k, v, lens, m, b, T):
+    """Each sequence solved with m = ceil(n / b), leaving out the all-padding query rows."""
+    out = np.zeros_like(np.asarray(v, dtype=np.float64))
+    for bi, n in enumerate(lens):
+        for h in range(q.shape[1]):
+            if n > 0:
+                out[bi, h, :n] = nv.monarch_attention_head(q[bi, h, :n], k[bi, h, :n], v[bi, h, :n], -(-n // b), b, T)
+    return out
 
 
 def _pad_ones(x, m, b):
