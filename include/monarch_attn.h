@@ -95,6 +95,33 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out,
                      int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
 
 /*
+ * monarch_attn_fwd_varlen -- monarch_attn_fwd over a batch of sequences of
+ * different lengths, each post-padded to N rows (Appendix "Padding and
+ * Masking", which names batched sequences padded to a maximum length as the
+ * second use of its mask).
+ *
+ * lens : DEVICE pointer to B int32 values, 4-byte aligned, not overlapping
+ *        out; lens[beta] is the number of real rows of batch element beta
+ *        (for all its heads).  Read by the kernels, so its values are not
+ *        checked on the host: they are clamped to 0..N.  Owned by the caller.
+ * Batch element beta is computed as the single sequence of its first
+ * lens[beta] rows, post-padded with zero rows to m * b at the batch's m and
+ * b: rows >= lens[beta] of q, k, v are not read, keys at positions >=
+ * lens[beta] are masked out of every R softmax, and the padded query rows
+ * take part in the iteration as zero rows.  Here whole key blocks can be
+ * padding, which the paper leaves undefined: such a block gets R = 0 and no
+ * weight in the L softmax (Z_L = -inf), so that M keeps unit row sums and
+ * zero columns at every padded key; a sequence of length 0 has M = 0.
+ * Rows lens[beta]..N-1 of out are written as zero.  With lens[beta] = N for
+ * every beta the result is that of monarch_attn_fwd.
+ * The other arguments, the errors, the workspace and the asynchrony are
+ * those of monarch_attn_fwd.
+ */
+int monarch_attn_fwd_varlen(const void *q, const void *k, const void *v, void *out, const int32_t *lens,
+                            int64_t B, int64_t H, int64_t N, int64_t d,
+                            int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
+
+/*
  * monarch_attn_fwd_objective -- monarch_attn_fwd, plus the value of the
  * variational objective f(M; Q, K) = <M, s Q K^T> + H(M) (Sec. 3, eq.
  * softmax_variational_attention, in its separable form for Monarch M) after

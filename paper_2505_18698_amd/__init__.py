@@ -34,6 +34,7 @@ try:
         monarch_attn_check,
         monarch_attn_fwd,
         monarch_attn_fwd_objective,
+        monarch_attn_fwd_varlen,
         monarch_attn_exact_fwd,
         monarch_attn_fwd_raw,
         monarch_attn_last_error,

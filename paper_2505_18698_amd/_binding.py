@@ -21,6 +21,7 @@ PATH_AUTO, PATH_HALF_STEPS, PATH_FUSED = 0, 1, 2
 # Every symbol declared in include/monarch_attn.h.
 EXPORTS = (
     "monarch_attn_fwd",
+    "monarch_attn_fwd_varlen",
     "monarch_attn_fwd_objective",
     "monarch_attn_exact_fwd",
     "monarch_attn_bwd",
@@ -51,6 +52,8 @@ def _load() -> ctypes.CDLL:
     i64, i32, vp = ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p
     lib.monarch_attn_fwd.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
     lib.monarch_attn_fwd.restype = ctypes.c_int
+    lib.monarch_attn_fwd_varlen.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
+    lib.monarch_attn_fwd_varlen.restype = ctypes.c_int
     lib.monarch_attn_fwd_objective.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
     lib.monarch_attn_fwd_objective.restype = ctypes.c_int
     lib.monarch_attn_exact_fwd.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i32, vp]
@@ -139,6 +142,24 @@ def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
     with torch.cuda.device(q.device):
         _check(monarch_attn_fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                     B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
+    return out
+
+
+def monarch_attn_fwd_varlen(q, k, v, out, lens, m: int, b: int, T: int, stream=None):
+    """monarch_attn_fwd over a batch of post-padded sequences: lens (int32 device
+    tensor [B]) holds the real rows of each batch element; rows >= lens[beta]
+    of q, k, v are not read and those of out are written as zero.  Returns `out`."""
+    import torch
+
+    _check_tensors(q, k, v, out)
+    if not isinstance(lens, torch.Tensor) or lens.device != q.device or lens.dtype != torch.int32 \
+            or not lens.is_contiguous() or tuple(lens.shape) != (q.shape[0],):
+        raise ValueError("lens must be a contiguous int32 tensor [B] on the device of q")
+    B, H, N, d = q.shape
+    stream = _stream(q, stream)
+    with torch.cuda.device(q.device):
+        _check(LIB.monarch_attn_fwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                           lens.data_ptr(), B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
     return out
 
 

@@ -103,8 +103,9 @@ int dispatch_r(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int 
     if constexpr (std::is_same<T, float>::value && NB * D > 8192) {
         return fail(MA_EUNSUPPORTED, "fp32 tile too large");
     } else {
-        // masked softmax over i when the tile is padded or the last block is short
-        const bool ragged = hd.b != NB || hd.n != hd.m * hd.b;
+        // masked softmax over i when the tile is padded, the last block is short
+        // or the heads have their own lengths
+        const bool ragged = hd.lens || hd.b != NB || hd.n != hd.m * hd.b;
         return ragged ? launch_r<T, NB, D, true>(L, B, hd, BH, nc, first, final_)
                       : launch_r<T, NB, D, false>(L, B, hd, BH, nc, first, final_);
     }
@@ -116,8 +117,8 @@ int dispatch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int 
     if constexpr (std::is_same<T, float>::value && NM * D > 8192) {
         return fail(MA_EUNSUPPORTED, "fp32 tile too large");
     } else {
-        return hd.m != NM ? launch_l<T, NM, D, true>(L, B, hd, BH, nc, apply)
-                          : launch_l<T, NM, D, false>(L, B, hd, BH, nc, apply);
+        return (hd.lens || hd.m != NM) ? launch_l<T, NM, D, true>(L, B, hd, BH, nc, apply)
+                                       : launch_l<T, NM, D, false>(L, B, hd, BH, nc, apply);
     }
 }
 
@@ -187,7 +188,7 @@ template <typename T> int run_fused(Launcher &L, const CallBufs &B, ma::HeadDims
     if constexpr (sizeof(T) != 2) {
         return fail(MA_EUNSUPPORTED, "the fused kernel needs 16-bit elements");
     } else {
-        const bool rgb = hd.b != 16 || hd.n != hd.m * hd.b, rgm = hd.m != 16;
+        const bool rgb = hd.lens || hd.b != 16 || hd.n != hd.m * hd.b, rgm = hd.lens || hd.m != 16;
         if (rgb && rgm) return launch_fused<T, true, true>(L, B, hd, c);
         if (rgb) return launch_fused<T, true, false>(L, B, hd, c);
         if (rgm) return launch_fused<T, false, true>(L, B, hd, c);
@@ -222,6 +223,8 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
 {
     const int32_t dtype = std::is_same<T, float>::value ? MA_F32 : std::is_same<T, __bf16>::value ? MA_BF16 : MA_F16;
     ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};
+    hd.lens = B.lens;
+    hd.H = c.H;
     if (path == kFusedHead && !fused_applies(dtype, c.d, c.m, c.b))
         return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d <= 64 and m, b <= 16");
     int rc;

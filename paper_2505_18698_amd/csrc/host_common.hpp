@@ -61,10 +61,12 @@ struct CallBufs {
     float *cR, *cL;
     float *obj_part;  // [B*H][T][b] shares (workspace)
     float *obj;       // [B*H][T] result (caller's)
+    const int *lens = nullptr;  // [B] real rows per batch element (device), or null
 };
 
 struct CallDims {
     int64_t BH;
+    int64_t H;  // heads per batch element
     int m, b, n, d, T;  // n: rows per head, (m - 1) * b < n <= m * b
     float s_log2e;
     int num_cus;  // compute units of the device

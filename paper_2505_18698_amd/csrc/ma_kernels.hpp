@@ -507,16 +507,37 @@ struct HeadDims {
     float s_log2e;     // log2(e) / sqrt(d)
     int64_t units;     // work units of a half-step launch (grid size)
     int t = 0, T = 0;  // step of this L half-step (1..T) and the step count, for the objective
+    // Per-sequence lengths (batch padding): head bh has lens[bh / H] real
+    // rows (clamped to 0..n), or n when lens is null.
+    const int *lens = nullptr;
+    int64_t H = 1;
 };
 
-// Real keys of block k (b except in a padded last block).
-__device__ inline int block_keys(const HeadDims &hd, int k) { return min(hd.b, hd.n - k * hd.b); }
+// Real rows of head bh.
+__device__ inline int live_rows(const HeadDims &hd, int64_t bh)
+{
+    if (!hd.lens) return hd.n;
+    const int len = hd.lens[bh / hd.H];
+    return len < 0 ? 0 : len > hd.n ? hd.n : len;
+}
+
+// Real keys of block k of a head with nl real rows: b, fewer in a partly
+// padded block, none (<= 0) in a block of padding only.
+__device__ inline int block_keys(int b, int nl, int k) { return min(b, nl - k * b); }
+
+// Key blocks holding at least one real key, ceil(nl / b) (m unless the head
+// is batch-padded).
+__device__ inline int live_blocks(int m, int b, int nl) { return min(m, (nl + b - 1) / b); }
 
 // Tensors and states of one call.  When n < m * b the sequence is taken as
 // post-padded with zero rows to N = m * b (Appendix "Padding and Masking"):
 // rows >= n of q, k, v are never read (zero is loaded instead), keys >= n are
 // masked out of every R softmax, rows >= n of out are never written, and the
-// states cover all N rows.  Layouts (per head):
+// states cover all N rows.  With per-sequence lengths (HeadDims::lens) the
+// same holds for the real rows nl <= n of each head, and whole key blocks
+// can be padding: such a block gets R = 0 (zero alpha_L, c_L, Y) and no
+// weight in the L softmax (Z_L = -inf), rows nl..n-1 of out are written as
+// zero.  Layouts (per head):
 //   q, k, v, out [B*H][n][d], d <= D (columns d..D-1 of every tile are zero);
 //   alpha_R [m][b][D] (row k*b + j), alpha_L and Y [b][m][D] (row j*m + k),
 //   c_L [m][b] (written by the R half-step of block k for all j),
@@ -572,7 +593,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
 
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, int tid, Regs &gr)
     {
-        const int m = hd.m, b = hd.b, kv = block_keys(hd, k);
+        const int m = hd.m, b = hd.b, kv = block_keys(b, RAGGED ? live_rows(hd, bh) : hd.n, k);
         const int dd = hd.d;
         const int64_t N = (int64_t)m * b, hoff = bh * N * D, toff = bh * (int64_t)hd.n * dd;
         const int lane = tid & 63, wave = tid >> 6;
@@ -612,7 +633,8 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
     {
         T *Ks = reinterpret_cast<T *>(lds);
         T *Vs = Ks + NB * LDK;
-        const int m = hd.m, b = hd.b, kv = block_keys(hd, k);  // keys >= kv: padding, masked (omega)
+        // keys >= kv: padding, masked (omega); kv <= 0: padding only, R = 0
+        const int m = hd.m, b = hd.b, kv = block_keys(b, RAGGED ? live_rows(hd, bh) : hd.n, k);
         const int64_t N = (int64_t)m * b;
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
@@ -655,10 +677,12 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
             }
             sum = lanegroup_sum(sum);
             t2 = lanegroup_sum(t2);
-            inv[r] = fast_rcp(sum);
+            const bool live = !RAGGED || kv > 0;
+            inv[r] = live ? fast_rcp(sum) : 0.f;
             // c_L = sum_i R log R = sum_i R (Z - max) - log(sum)   (natural-log units)
             if (g == 0 && jr[r] < b)
-                p.cL[bh * N + (int64_t)k * b + jr[r]] = kLn2 * (t2 * inv[r] - __builtin_amdgcn_logf(sum));
+                p.cL[bh * N + (int64_t)k * b + jr[r]] =
+                    live ? kLn2 * (t2 * inv[r] - __builtin_amdgcn_logf(sum)) : 0.f;
             if constexpr (NF) {
 #pragma unroll
                 for (int t = 0; t < NT; ++t) sc[r][t] *= inv[r];
@@ -718,7 +742,8 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
         const int dd = hd.d;
         const T *qh = p.q + bh * (int64_t)hd.n * dd;
         const T *al = p.aL + hoff + (int64_t)j * m * D;
-        const int ml = (hd.n - j + b - 1) / b;  // real rows l of class j: l*b + j < n
+        const int nl = RAGGED ? live_rows(hd, bh) : hd.n;
+        const int ml = (nl - j + b - 1) / b;  // real rows l of class j: l*b + j < nl
         gr.qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * dd; }, ml, tid, dd);
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
@@ -745,6 +770,7 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
+        const int mk = RAGGED ? live_blocks(m, b, live_rows(hd, bh)) : m;  // blocks k >= mk: no real key
 
         // scores and softmax over k for the query rows of this wave
         int lr[RT];
@@ -772,21 +798,23 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
         }
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
-            const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
+            const float mx = tiles_max<NT, RAGGED>(sc[r], mk, g);
             float sum = 0.f;
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
 #pragma unroll
                 for (int qq = 0; qq < 4; ++qq) {
                     float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
-                    if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
+                    if (RAGGED && 16 * t + 4 * g + qq >= mk) e = 0.f;
                     sum += e;
                     sc[r][t][qq] = e;
                 }
             }
             sum = lanegroup_sum(sum);
-            inv[r] = (lr[r] < m) ? fast_rcp(sum) : 0.f;  // padded query rows carry no weight
-            lse[r] = (lr[r] < m) ? row_lse(mx, sum) : 0.f;
+            // tile rows l >= m carry no weight, nor does a head without a real key
+            const bool live = lr[r] < m && (!RAGGED || mk > 0);
+            inv[r] = live ? fast_rcp(sum) : 0.f;
+            lse[r] = live ? row_lse(mx, sum) : 0.f;
         }
         float *objs = cLs + NM;  // one objective share per wave
         if (p.obj_part) {
@@ -863,11 +891,12 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
         gr.yt.fetch([=](int kk) { return yj + (int64_t)kk * D; }, m, tid);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
+        const int nl = RAGGED ? live_rows(hd, bh) : hd.n;
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int l = (wave * RT + r) * 16 + (lane & 15);
-            gr.bf[r].load((int64_t)l * b + j < hd.n ? p.q + bh * (int64_t)hd.n * hd.d + ((int64_t)l * b + j) * hd.d
-                                                    : nullptr,
+            gr.bf[r].load((int64_t)l * b + j < nl ? p.q + bh * (int64_t)hd.n * hd.d + ((int64_t)l * b + j) * hd.d
+                                                  : nullptr,
                           lane >> 4, hd.d);  // Qbar[j][l]; zero for padded rows
         }
     }
@@ -893,6 +922,8 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
+        const int nl = RAGGED ? live_rows(hd, bh) : hd.n;
+        const int mk = RAGGED ? live_blocks(m, b, nl) : m;  // blocks k >= mk: no real key
         int lr[RT];
 #pragma unroll
         for (int r = 0; r < RT; ++r) lr[r] = (wave * RT + r) * 16 + c16;
@@ -913,21 +944,22 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         float inv[RT], lse[RT];
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
-            const float mx = tiles_max<NT, RAGGED>(sc[r], m, g);
+            const float mx = tiles_max<NT, RAGGED>(sc[r], mk, g);
             float sum = 0.f;
 #pragma unroll
             for (int t = 0; t < NT; ++t) {
 #pragma unroll
                 for (int qq = 0; qq < 4; ++qq) {
                     float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
-                    if (RAGGED && 16 * t + 4 * g + qq >= m) e = 0.f;
+                    if (RAGGED && 16 * t + 4 * g + qq >= mk) e = 0.f;
                     sum += e;
                     sc[r][t][qq] = e;
                 }
             }
             sum = lanegroup_sum(sum);
-            inv[r] = fast_rcp(sum);
-            lse[r] = (lr[r] < m) ? row_lse(mx, sum) : 0.f;
+            const bool any = !RAGGED || mk > 0;  // a head without a real key has L = 0
+            inv[r] = any ? fast_rcp(sum) : 0.f;
+            lse[r] = (lr[r] < m && any) ? row_lse(mx, sum) : 0.f;
             if constexpr (NF) {
 #pragma unroll
                 for (int t = 0; t < NT; ++t) sc[r][t] *= inv[r];
@@ -958,11 +990,11 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
             for (int r = 0; r < RT; ++r) o[r][vt] = acc[r];
         }
 #pragma unroll
-        for (int r = 0; r < RT; ++r)
-            store_row<T, D>((int64_t)lr[r] * b + j < hd.n
-                                ? p.out + bh * (int64_t)hd.n * hd.d + ((int64_t)lr[r] * b + j) * hd.d
-                                : nullptr,
-                            o[r], inv[r], lane, hd.d);
+        for (int r = 0; r < RT; ++r) {  // rows nl..n-1 (batch padding) are written as zero
+            const int64_t row = (int64_t)lr[r] * b + j;
+            store_row<T, D>(row < hd.n ? p.out + bh * (int64_t)hd.n * hd.d + row * hd.d : nullptr, o[r],
+                            row < nl ? inv[r] : 0.f, lane, hd.d);
+        }
     }
 };
 
@@ -1049,7 +1081,8 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
     struct Ctx {
         T *Qs, *Ks, *As, *Rs;
         float *cRs, *cLs;  // c_R[k][j] at k*CS + j, c_L[j][k] at j*CS + k
-        int m, b, n, d, lane, g, c16;  // n: real rows of the head (rows >= n are zero padding); d <= D
+        int m, b, n, d, lane, g, c16;  // n: rows of a head in q, k, v, out; d <= D
+        int nl, mk;        // real rows of the head being computed (rows >= nl are zero padding), live key blocks
         float s_log2e;
         int64_t bh;        // the head being computed
         int steps;         // T, the step count
@@ -1068,7 +1101,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             if (jv) rs = c.s_log2e * fast_rcp(fmaxf(c.cRs[k * CS + j], kTiny));
         }
         T *Kk = c.Ks + k * BS;
-        const int kv = min(c.b, c.n - k * c.b);  // keys >= kv: padding, masked (omega)
+        const int kv = block_keys(c.b, c.nl, k);  // keys >= kv: padding, masked (omega); none: R = 0
         f32x4 sc;  // lane holds S'[i = 4g + qq][j]
         gemm_scores_rt<T, D, 1>(Kk + c.c16 * LD, &bf, &sc, c.g);
         const float nb = -tiles_max<1, RGB>(&sc, kv, c.g) * rs;
@@ -1084,8 +1117,9 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         }
         sum = lanegroup_sum(sum);
         t2 = lanegroup_sum(t2);
-        const float inv = fast_rcp(sum);
-        if (c.g == 0 && jv) c.cLs[j * CS + k] = kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum));
+        const bool live = !RGB || kv > 0;
+        const float inv = live ? fast_rcp(sum) : 0.f;
+        if (c.g == 0 && jv) c.cLs[j * CS + k] = live ? kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum)) : 0.f;
         static_assert(NormFirst<1, D>::value, "probabilities normalised before the products, as in RHalf");
         sc *= inv;
         ProbFrags<T, 1> pf;
@@ -1121,18 +1155,19 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             const float bias = (!RGM || kk < c.m) ? c.cLs[j * CS + kk] * kLog2e : 0.f;
             sc[qq] = __builtin_fmaf(acc[qq], c.s_log2e, -bias);
         }
-        const float mx = tiles_max<1, RGM>(&sc, c.m, c.g);
+        const float mx = tiles_max<1, RGM>(&sc, c.mk, c.g);  // blocks k >= mk: no real key
         float sum = 0.f;
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
             float e = __builtin_amdgcn_exp2f(sc[qq] - mx);
-            if (RGM && 4 * c.g + qq >= c.m) e = 0.f;
+            if (RGM && 4 * c.g + qq >= c.mk) e = 0.f;
             sum += e;
             sc[qq] = e;
         }
         sum = lanegroup_sum(sum);
-        inv = fast_rcp(sum);
-        lse = c.c16 < c.m ? row_lse(mx, sum) : 0.f;
+        const bool any = !RGM || c.mk > 0;  // a head without a real key has L = 0
+        inv = any ? fast_rcp(sum) : 0.f;
+        lse = (c.c16 < c.m && any) ? row_lse(mx, sum) : 0.f;
         return sc;
     }
 
@@ -1175,16 +1210,18 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         f32x4 o[D / 16];  // O[l*b + j] = sum_k L[j][k][l] Y[k][j]; Y[k][j] is row k of Ks + j*LD at stride BS
 #pragma unroll
         for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, 1>(c.Ks + j * LD, BS, 16 * vt, pf, c.lane);
-        store_row<T, D>(l * c.b + j < c.n ? out_h + ((int64_t)l * c.b + j) * c.d : nullptr, o, 1.0f, c.lane, c.d);
+        const int row = l * c.b + j;  // rows nl..n-1 (batch padding) are written as zero
+        store_row<T, D>(row < c.n ? out_h + (int64_t)row * c.d : nullptr, o, row < c.nl ? 1.0f : 0.f, c.lane, c.d);
     }
 
     static constexpr int PER = 2 * 256 * 8 / (64 * NW);  // 16-byte chunks of Qs and Ks per thread
 
     // Issue the loads of head bh: Qbar and Kbar chunks (zero where there is no
     // row) for the LDS regions, and Vbar[w] for wave w's last R half-step.
-    // Rows >= n (padding) and columns >= d are zero and never read.
-    __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int d, int64_t bh, int tid, u32x4 *raw,
-                                     u32x4 *vb)
+    // Rows >= nl (padding) and columns >= d are zero and never read; a head
+    // has n rows in memory.
+    __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int nl, int d, int64_t bh, int tid,
+                                     u32x4 *raw, u32x4 *vb)
     {
         const int64_t hoff = bh * (int64_t)n * d;
         const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
@@ -1193,9 +1230,9 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             const int idx = tid + h * 64 * NW;
             const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
             raw[h] = u32x4{0u, 0u, 0u, 0u};
-            if (reg == 0 && blk < b && r < m && r * b + blk < n && col < d)
+            if (reg == 0 && blk < b && r < m && r * b + blk < nl && col < d)
                 raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * d + col);  // Qbar[blk][r]
-            if (reg == 1 && blk < m && r < b && blk * b + r < n && col < d)
+            if (reg == 1 && blk < m && r < b && blk * b + r < nl && col < d)
                 raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * d + col);  // Kbar[blk][r]
         }
         const int w = tid >> 6, lane = tid & 63;
@@ -1203,7 +1240,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         for (int h = 0; h < 2; ++h) {
             const int r = (lane >> 3) + 8 * h, col = (lane & 7) * 8;
             vb[h] = u32x4{0u, 0u, 0u, 0u};
-            if (w < m && r < b && w * b + r < n && col < d)
+            if (w < m && r < b && w * b + r < nl && col < d)
                 vb[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * d + col);
         }
     }
@@ -1244,14 +1281,17 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
 
         u32x4 raw[PER], vcur[2], vnext[2];
         int64_t bh = blockIdx.x;
-        load_head(p, m, b, c.n, c.d, bh, tid, raw, vcur);
+        load_head(p, m, b, c.n, live_rows(hd, bh), c.d, bh, tid, raw, vcur);
         for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) *chunk(c.As, idx) = u32x4{0u, 0u, 0u, 0u};
         for (; bh < BH; bh += gridDim.x) {
             c.bh = bh;
+            c.nl = live_rows(hd, bh);
+            c.mk = live_blocks(m, b, c.nl);
 #pragma unroll
             for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
             __syncthreads();
-            if (bh + gridDim.x < BH) load_head(p, m, b, c.n, c.d, bh + gridDim.x, tid, raw, vnext);
+            if (bh + gridDim.x < BH)
+                load_head(p, m, b, c.n, live_rows(hd, bh + gridDim.x), c.d, bh + gridDim.x, tid, raw, vnext);
 
             for (int t = 1; t <= T_; ++t) {
                 const bool first = t == 1, last = t == T_;

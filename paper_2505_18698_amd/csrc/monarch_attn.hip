@@ -153,9 +153,11 @@ int acquire_workspace(int dev, hipStream_t stream, size_t need, char **base, std
     return MA_OK;
 }
 
-// The forward pass; with obj != nullptr also the objective per (head, step).
-int forward(const void *q, const void *k, const void *v, void *out, float *obj, bool need_obj, int64_t B, int64_t H,
-            int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
+// The forward pass; with obj != nullptr also the objective per (head, step);
+// with need_lens, per-sequence lengths lens[B] (device).
+int forward(const void *q, const void *k, const void *v, void *out, float *obj, bool need_obj, const int32_t *lens,
+            bool need_lens, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
+            void *stream)
 {
     g_err[0] = '\0';
     if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
@@ -165,6 +167,8 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
     if (need_obj && !obj) return fail(MA_EINVAL, "null objective pointer");
     if (need_obj && ((uintptr_t)obj & 3u)) return fail(MA_EINVAL, "obj must be 4-byte aligned");
+    if (need_lens && !lens) return fail(MA_EINVAL, "null lens pointer");
+    if (need_lens && ((uintptr_t)lens & 3u)) return fail(MA_EINVAL, "lens must be 4-byte aligned");
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)out) & 15u)
         return fail(MA_EINVAL, "q, k, v and out must be 16-byte aligned");
     const int64_t BH = B * H;
@@ -177,11 +181,13 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     if (obj && (overlaps(obj, obj_bytes, q, tensor_bytes) || overlaps(obj, obj_bytes, k, tensor_bytes) ||
                 overlaps(obj, obj_bytes, v, tensor_bytes) || overlaps(obj, obj_bytes, out, tensor_bytes)))
         return fail(MA_EINVAL, "obj must not overlap q, k, v or out");
+    if (lens && overlaps(lens, (size_t)B * sizeof(int32_t), out, tensor_bytes))
+        return fail(MA_EINVAL, "lens must not overlap out");
 
     const int path = g_path.load();
     const size_t st = state_bytes(BH, m * b, d, dtype);
     const size_t cs = align_up((size_t)BH * m * b * sizeof(float));
-    CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, obj};
+    CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, obj, lens};
     int dev = 0, num_cus = 0;
     if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
     std::unique_lock<std::mutex> ws_hold;  // the stream's workspace, held until the launches are enqueued
@@ -201,7 +207,8 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
         }
         if (obj) bufs.obj_part = (float *)(base + state_ws);
     }
-    CallDims dims{BH, (int)m, (int)b, (int)N, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
+    CallDims dims{BH, H, (int)m, (int)b, (int)N, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)),
+                  num_cus};
 
     std::unique_lock<std::mutex> tlock(g_timing_mutex);
     Launcher L{(hipStream_t)stream, g_timing.enabled};
@@ -304,7 +311,8 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
     bufs.daR = (float *)p, p += lay.sg;
     bufs.dcL = (float *)p, p += lay.cs;
     bufs.dcR = (float *)p;
-    CallDims dims{BH, (int)m, (int)b, (int)N, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)), num_cus};
+    CallDims dims{BH, H, (int)m, (int)b, (int)N, (int)d, T, (float)(1.4426950408889634 / std::sqrt((double)d)),
+                  num_cus};
 
     std::unique_lock<std::mutex> tlock(g_timing_mutex);
     Launcher L{(hipStream_t)stream, g_timing.enabled};
@@ -420,7 +428,14 @@ int32_t monarch_attn_timing_read(float *ms, int32_t *kind, int32_t cap)
 int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int64_t B, int64_t H, int64_t N,
                      int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
 {
-    return forward(q, k, v, out, nullptr, false, B, H, N, d, m, b, T, dtype, stream);
+    return forward(q, k, v, out, nullptr, false, nullptr, false, B, H, N, d, m, b, T, dtype, stream);
+}
+
+int monarch_attn_fwd_varlen(const void *q, const void *k, const void *v, void *out, const int32_t *lens, int64_t B,
+                            int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
+                            void *stream)
+{
+    return forward(q, k, v, out, nullptr, false, lens, true, B, H, N, d, m, b, T, dtype, stream);
 }
 
 int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *out, float *lse, int64_t B,
@@ -472,7 +487,7 @@ int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void
                                int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
                                void *stream)
 {
-    return forward(q, k, v, out, obj, true, B, H, N, d, m, b, T, dtype, stream);
+    return forward(q, k, v, out, obj, true, nullptr, false, B, H, N, d, m, b, T, dtype, stream);
 }
 
 int monarch_attn_bwd(const void *q, const void *k, const void *v, const void *dout, void *dq, void *dk, void *dv,

@@ -240,6 +240,13 @@ def random_qkv(B, H, N, d, dtype="f32", seed=0, scale=1.0):
     return q, k, v
 
 
+def sequence_lengths(B: int, N: int, seed: int = 0, low: int = 1) -> np.ndarray:
+    """Lengths of a batch of sequences padded to N rows: int32 [B], iid uniform
+    on low..N (a stand-in for the length mix of a padded batch)."""
+    g = _rng(seed, f"lengths/B{B}N{N}lo{low}")
+    return g.integers(low, N + 1, size=B).astype(np.int32)
+
+
 def random_cotangent(shape, dtype="f32", seed=0, tag="dout"):
     """An iid N(0, 1) tensor of the given shape rounded to the run dtype: the
     incoming gradient dO of a gradient test or benchmark."""

@@ -154,6 +154,22 @@ def test_objective_rejects_null_obj():
     assert "objective" in ma.monarch_attn_last_error()
 
 
+def test_varlen_rejects_null_or_misaligned_lens():
+    import paper_2505_18698_amd as ma
+
+    f = ma.LIB.monarch_attn_fwd_varlen
+    assert f(FAKE, FAKE, FAKE, 2 * FAKE, None, 2, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_EINVAL
+    assert "lens" in ma.monarch_attn_last_error()
+    assert f(FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE + 2, 2, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_EINVAL
+    assert "aligned" in ma.monarch_attn_last_error()
+    # lens inside out (written by the kernels while lens is read)
+    assert f(FAKE, FAKE, FAKE, 2 * FAKE, 2 * FAKE + 64, 2, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_EINVAL
+    assert "overlap" in ma.monarch_attn_last_error()
+    # the shape checks of the plain call apply
+    assert f(FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 2, 1, 256, 64, 15, 16, 1, 1, None) == ma.MA_EINVAL
+    assert f(None, None, None, None, None, 0, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_OK
+
+
 # ---- the gradient entry point ----
 
 @pytest.mark.parametrize(

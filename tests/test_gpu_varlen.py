@@ -1,0 +1,166 @@
+"""GPU parity of monarch_attn_fwd_varlen (batch padding: every batch element
+has its own length, m and b are the batch's) against the fp64 oracle on the
+same seeded, dtype-rounded inputs.
+
+Bar: the forward's, rel-Frobenius <= 1e-5 (fp32) and <= 2e-2 (bf16 / fp16)
+over the real rows of the whole batch, each sequence also checked on its
+own; rows beyond a sequence's length must be exactly zero.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth_inputs as si
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2, "f16": 2e-2}
+
+
+@pytest.fixture(scope="module")
+def ma():
+    import torch
+
+    assert torch.cuda.is_available(), "no GPU visible"
+    import paper_2505_18698_amd as lib
+
+    return lib
+
+
+@pytest.fixture(params=["auto", "half_steps"])
+def path(ma, request):
+    prev = ma.monarch_attn_set_path(ma.PATH_AUTO if request.param == "auto" else ma.PATH_HALF_STEPS)
+    yield request.param
+    ma.monarch_attn_set_path(prev)
+
+
+def _td(dtype):
+    import torch
+
+    return {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+
+
+def run_varlen(ma, q, k, v, lens, m, b, T, dtype):
+    import torch
+
+    td = _td(dtype)
+    dq, dk, dv = (torch.from_numpy(x).to(td).cuda() for x in (q, k, v))
+    out = torch.full_like(dq, float("nan"))
+    ma.monarch_attn_fwd_varlen(dq, dk, dv, out, torch.tensor(lens, dtype=torch.int32, device="cuda"), m, b, T)
+    torch.cuda.synchronize()
+    return out.double().cpu().numpy()
+
+
+def check_varlen(o, ref, lens, dtype, label):
+    lens = [int(x) for x in lens]
+    assert np.isfinite(o).all(), label
+    for bi, n in enumerate(lens):
+        assert np.all(o[bi, :, n:] == 0.0), (label, "padding rows not zero", bi)
+    real = np.concatenate([o[bi, :, :n].ravel() for bi, n in enumerate(lens)])
+    want = np.concatenate([ref[bi, :, :n].ravel() for bi, n in enumerate(lens)])
+    err = float(np.linalg.norm(real - want) / np.linalg.norm(want)) if real.size else 0.0
+    per = [oracle.rel_frobenius(o[bi, :, :n], ref[bi, :, :n]) for bi, n in enumerate(lens) if n > 0]
+    print(f"{label} lens={lens} rel_frob={err:.3e} max_seq={max(per) if per else 0:.3e}", flush=True)
+    assert err <= TOL[dtype], (label, err)
+    assert max(per, default=0.0) <= 2 * TOL[dtype], (label, per)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize(
+    "m,b,d,lens",
+    [
+        (10, 10, 64, [100, 0, 37, 9, 10, 91]),       # square, ragged tiles
+        (16, 16, 64, [256, 1, 16, 17, 200, 255]),    # the fused kernel's shape
+        (14, 14, 64, [196, 150, 14, 13, 0, 28]),     # ViT-B/16 grid
+        (8, 48, 64, [384, 100, 48, 47, 0, 383]),     # m != b (b-sweep at N = 384)
+        (24, 16, 128, [384, 5, 200, 383]),           # d = 128
+        (13, 29, 72, [377, 29, 30, 150]),            # d = 72
+    ],
+)
+@pytest.mark.parametrize("T", [1, 2])
+def test_varlen_matches_oracle(ma, path, dtype, m, b, d, lens, T):
+    if dtype == "f32" and max(-(-m // 16) * 16, -(-b // 16) * 16) * (64 if d <= 64 else 96 if d <= 96 else 128) > 8192:
+        pytest.skip("fp32 tiles of this size are not supported")
+    N = m * b
+    B = len(lens)
+    q, k, v = si.random_qkv(B, 2, N, d, dtype, seed=7 * m + b + T, scale=1.5)
+    o = run_varlen(ma, q, k, v, lens, m, b, T, dtype)
+    ref = oracle.monarch_attention_varlen(q, k, v, np.array(lens), m, b, T)
+    check_varlen(o, ref, lens, dtype, f"varlen {path} {dtype} m={m} b={b} d={d} T={T}")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_varlen_ragged_total_length(ma, path, dtype):
+    """N not a multiple of b: the batch's N is itself post-padded, and each
+    sequence is shorter still."""
+    m, b, d, T, N = 9, 12, 64, 3, 103
+    lens = [103, 60, 12, 11, 1, 0, 97]
+    q, k, v = si.random_qkv(len(lens), 3, N, d, dtype, seed=31, scale=1.5)
+    o = run_varlen(ma, q, k, v, lens, m, b, T, dtype)
+    ref = oracle.monarch_attention_varlen(q, k, v, np.array(lens), m, b, T)
+    check_varlen(o, ref, lens, dtype, f"varlen {path} ragged-N {dtype}")
+
+
+def test_varlen_long_sequences(ma):
+    """The long-sequence shape, N = 16384 = 128 x 128 at d = 64, with lengths
+    that leave whole blocks and most of the sequence as padding."""
+    m = b = 128
+    lens = [16384, 5000, 129]
+    q, k, v = si.random_qkv(len(lens), 1, m * b, 64, "bf16", seed=41, scale=1.5)
+    o = run_varlen(ma, q, k, v, lens, m, b, 2, "bf16")
+    ref = oracle.monarch_attention_varlen(q, k, v, np.array(lens), m, b, 2)
+    check_varlen(o, ref, lens, "bf16", "varlen long")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_full_lengths_equal_the_plain_call(ma, path, dtype):
+    import torch
+
+    m, b, d, T = 12, 12, 64, 2
+    q, k, v = si.random_qkv(3, 2, m * b, d, dtype, seed=51)
+    o_var = run_varlen(ma, q, k, v, [m * b] * 3, m, b, T, dtype)
+    td = _td(dtype)
+    dq, dk, dv = (torch.from_numpy(x).to(td).cuda() for x in (q, k, v))
+    out = torch.empty_like(dq)
+    ma.monarch_attn_fwd(dq, dk, dv, out, m, b, T)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(o_var, out.double().cpu().numpy(), rtol=0, atol=1e-6 if dtype == "f32" else 1e-2)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_padding_rows_are_not_read(ma, path, dtype):
+    """NaN in every padded row of q, k and v changes nothing."""
+    m, b, d, T = 10, 16, 64, 2
+    lens = [160, 77, 16, 3]
+    q, k, v = si.random_qkv(len(lens), 2, m * b, d, dtype, seed=61)
+    o1 = run_varlen(ma, q, k, v, lens, m, b, T, dtype)
+    q2, k2, v2 = q.copy(), k.copy(), v.copy()
+    for bi, n in enumerate(lens):
+        for x in (q2, k2, v2):
+            x[bi, :, n:] = np.nan
+    o2 = run_varlen(ma, q2, k2, v2, lens, m, b, T, dtype)
+    np.testing.assert_array_equal(o1, o2)
+
+
+def test_lengths_are_clamped(ma, path):
+    m, b, d, T = 8, 8, 64, 2
+    q, k, v = si.random_qkv(3, 2, m * b, d, "bf16", seed=71)
+    o1 = run_varlen(ma, q, k, v, [-5, 1000, 30], m, b, T, "bf16")
+    o2 = run_varlen(ma, q, k, v, [0, 64, 30], m, b, T, "bf16")
+    np.testing.assert_array_equal(o1, o2)
+    assert np.all(o1[0] == 0.0)
+
+
+def test_single_key_blocks_are_exact_attention(ma):
+    """b = 1 on the GPU: exact softmax attention over the real keys, T = 3."""
+    import oracle.naive as nv
+
+    m, b, d = 40, 1, 64
+    lens = [40, 23, 1]
+    q, k, v = si.random_qkv(len(lens), 2, m, d, "f32", seed=81)
+    o = run_varlen(ma, q, k, v, lens, m, b, 3, "f32")
+    for bi, n in enumerate(lens):
+        for h in range(2):
+            ref = nv.dense_softmax_attention(q[bi, h, :n], k[bi, h, :n], v[bi, h, :n])
+            assert oracle.rel_frobenius(o[bi, h, :n], ref) <= 1e-5
+        assert np.all(o[bi, :, n:] == 0.0)
