@@ -39,6 +39,10 @@ point and ViT-B/16 with its class token, with its per-kernel durations and
 the roofline of its dominant gradient kernel.  Reported beside the headline,
 not in it.
 
+varlen: monarch_attn_fwd_varlen on a padded batch (RoBERTa-base shape at
+N = 384, b = 48, T = 1; lengths iid uniform on 64..384), beside the plain
+call on the same tensors.
+
 quality: the error of O against exact softmax attention and the gap of the
 variational objective to its exact-softmax maximum, for T = 1, 2, 3, on the
 structured workloads (ViT- and RoBERTa-shaped, and 16K tokens with
@@ -416,6 +420,79 @@ def measure_backward(ma, torch, w, steps, warmup):
 QUALITY_WORKLOADS = ("vit_b16_n196", "roberta_n1024", "lm_n16384")
 
 
+def time_calls(torch, step, steps, warmup):
+    """ms per call of `step(i)` over `steps` calls back to back, after `warmup`."""
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(steps):
+        step(i)
+    end.record()
+    end.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def kernel_times(ma, step, steps):
+    """Average duration (us) of each launch of `step`, from the library's
+    per-launch events, in launch order."""
+    sums, names = None, None
+    ma.monarch_attn_timing_enable(True)
+    try:
+        for i in range(steps):
+            step(i)
+            recs = ma.monarch_attn_timing_read()
+            if sums is None:
+                names, sums = [kind for kind, _ in recs], [0.0] * len(recs)
+            for j, (_, t) in enumerate(recs):
+                sums[j] += t
+    finally:
+        ma.monarch_attn_timing_enable(False)
+    return [[name, round(t / steps * 1e3, 3)] for name, t in zip(names, sums)]
+
+
+def measure_varlen(ma, torch, w, steps, warmup, low=64):
+    """monarch_attn_fwd_varlen over a padded batch of w's shape with lengths
+    iid uniform on low..N (seed 0), and the plain call on the same tensors."""
+    import synth_inputs as si
+
+    q, k, v, meta = si.make_qkv(w)
+    lens_np = si.sequence_lengths(w.B, w.N, seed=0, low=min(low, w.N))
+    td = {"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[w.dtype]
+    base = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
+    del q, k, v
+    lens = torch.from_numpy(lens_np).cuda()
+    set_bytes = 4 * base[0].numel() * base[0].element_size()
+    nsets = max(1, min(8, math.ceil(ROTATE_BYTES / set_bytes)))
+    sets = [(base[0].clone(), base[1].clone(), base[2].clone(), torch.empty_like(base[0])) for _ in range(nsets)]
+    del base
+
+    def step_varlen(i):
+        qq, kk, vv, oo = sets[i % nsets]
+        ma.monarch_attn_fwd_varlen(qq, kk, vv, oo, lens, w.m, w.b, w.T)
+
+    def step_plain(i):
+        qq, kk, vv, oo = sets[i % nsets]
+        ma.monarch_attn_fwd(qq, kk, vv, oo, w.m, w.b, w.T)
+
+    ms = time_calls(torch, step_varlen, steps, warmup)
+    ms_plain = time_calls(torch, step_plain, steps, warmup)
+    kern, kern_plain = kernel_times(ma, step_varlen, steps), kernel_times(ma, step_plain, steps)
+    del sets
+    torch.cuda.empty_cache()
+    real = int(lens_np.sum())
+    cfg = w.describe()
+    cfg.update({"lengths": f"iid uniform on {min(low, w.N)}..{w.N}, seed 0", "real_rows": real,
+                "padded_rows": w.B * w.N, "rotating_input_sets": nsets})
+    log(f"[bench] varlen {w.name}: {ms * 1e3:.1f} us per call (plain call {ms_plain * 1e3:.1f} us), "
+        f"{real} of {w.B * w.N} rows real")
+    return {"config": cfg, "value": round(w.B * w.H * w.N / (ms * 1e-3), 1), "unit": UNIT,
+            "ms_per_call": round(ms, 6), "plain_ms_per_call": round(ms_plain, 6),
+            "real_heads_tokens_per_s": round(w.H * real / (ms * 1e-3), 1),
+            "kernels_us": kern, "plain_kernels_us": kern_plain}
+
+
 def quality(ma, torch, w, steps_list=(1, 2, 3)):
     """Approximation quality on the workload's first input set, all on the GPU:
     the relative Frobenius error of O against exact softmax attention
@@ -580,6 +657,8 @@ def main():
     ap.add_argument("--sweep", default=",".join(f"sweep_n{n}_d{d}" for n in (256, 1024, 4096, 16384)
                                                    for d in (64, 128)),
                     help="comma-separated workloads of the N / d sweep ('' for none)")
+    ap.add_argument("--varlen", default="roberta_n384_b48",
+                    help="comma-separated workloads timed as padded batches with per-sequence lengths ('' for none)")
     ap.add_argument("--no-sdpa", action="store_true", help="skip the torch fused-attention context timing")
     ap.add_argument("--no-measured-peaks", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -674,6 +753,8 @@ def main():
     result["sweep"] = sweep
     result["backward"] = [measure_backward(ma, torch, si.WORKLOADS[name], args.steps, args.warmup)
                           for name in [x for x in args.backward.split(",") if x]]
+    result["varlen"] = [measure_varlen(ma, torch, si.WORKLOADS[name], args.steps, args.warmup)
+                        for name in [x for x in args.varlen.split(",") if x]]
     if not args.no_quality:
         result["quality"] = [quality(ma, torch, si.WORKLOADS[name]) for name in QUALITY_WORKLOADS]
     if not args.no_cpu_baseline:

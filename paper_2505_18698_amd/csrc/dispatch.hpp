@@ -59,11 +59,11 @@ inline dim3 unit_grid(const void *kern, int threads, int64_t units, int num_cus)
     return dim3((unsigned)(units < cap ? units : cap));
 }
 
-template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RG>
+template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RG, bool LENS>
 int launch_r1(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int num_cus)
 {
     constexpr int W = ma::Split<NB / 16>::W;
-    auto kern = ma::r_half_step<T, NB, D, FIRST, FINAL, RG>;
+    auto kern = ma::r_half_step<T, NB, D, FIRST, FINAL, RG, LENS>;
     hd.units = BH * hd.m;
     const dim3 grid = unit_grid((const void *)kern, 64 * W, hd.units, num_cus), block(64 * W);
     const ma::Bufs<T> p = typed<T>(B);
@@ -71,16 +71,16 @@ int launch_r1(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int n
                  [&] { return launched([&] { hipLaunchKernelGGL(kern, grid, block, 0, L.stream, p, hd); }); });
 }
 
-template <typename T, int NB, int D, bool RG>
+template <typename T, int NB, int D, bool RG, bool LENS = false>
 int launch_r(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int num_cus, bool first, bool final_)
 {
-    if (first && final_) return launch_r1<T, NB, D, true, true, RG>(L, B, hd, BH, num_cus);
-    if (first) return launch_r1<T, NB, D, true, false, RG>(L, B, hd, BH, num_cus);
-    if (final_) return launch_r1<T, NB, D, false, true, RG>(L, B, hd, BH, num_cus);
-    return launch_r1<T, NB, D, false, false, RG>(L, B, hd, BH, num_cus);
+    if (first && final_) return launch_r1<T, NB, D, true, true, RG, LENS>(L, B, hd, BH, num_cus);
+    if (first) return launch_r1<T, NB, D, true, false, RG, LENS>(L, B, hd, BH, num_cus);
+    if (final_) return launch_r1<T, NB, D, false, true, RG, LENS>(L, B, hd, BH, num_cus);
+    return launch_r1<T, NB, D, false, false, RG, LENS>(L, B, hd, BH, num_cus);
 }
 
-template <typename T, int NM, int D, bool RG>
+template <typename T, int NM, int D, bool RG, bool LENS = false>
 int launch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int num_cus, bool apply)
 {
     constexpr int W = ma::Split<NM / 16>::W;
@@ -88,11 +88,11 @@ int launch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int nu
     const ma::Bufs<T> p = typed<T>(B);
     const dim3 block(64 * W);
     if (apply) {
-        auto kern = ma::monarch_apply<T, NM, D, RG>;
+        auto kern = ma::monarch_apply<T, NM, D, RG, LENS>;
         const dim3 grid = unit_grid((const void *)kern, 64 * W, hd.units, num_cus);
         return L.run(kApply, [&] { return launched([&] { hipLaunchKernelGGL(kern, grid, block, 0, L.stream, p, hd); }); });
     }
-    auto kern = ma::l_half_step<T, NM, D, RG>;
+    auto kern = ma::l_half_step<T, NM, D, RG, LENS>;
     const dim3 grid = unit_grid((const void *)kern, 64 * W, hd.units, num_cus);
     return L.run(kL, [&] { return launched([&] { hipLaunchKernelGGL(kern, grid, block, 0, L.stream, p, hd); }); });
 }
@@ -103,9 +103,10 @@ int dispatch_r(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int 
     if constexpr (std::is_same<T, float>::value && NB * D > 8192) {
         return fail(MA_EUNSUPPORTED, "fp32 tile too large");
     } else {
-        // masked softmax over i when the tile is padded, the last block is short
-        // or the heads have their own lengths
-        const bool ragged = hd.lens || hd.b != NB || hd.n != hd.m * hd.b;
+        // masked softmax over i when the tile is padded or the last block is
+        // short; per-sequence lengths have instantiations of their own
+        if (hd.lens) return launch_r<T, NB, D, true, true>(L, B, hd, BH, nc, first, final_);
+        const bool ragged = hd.b != NB || hd.n != hd.m * hd.b;
         return ragged ? launch_r<T, NB, D, true>(L, B, hd, BH, nc, first, final_)
                       : launch_r<T, NB, D, false>(L, B, hd, BH, nc, first, final_);
     }
@@ -117,8 +118,9 @@ int dispatch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int 
     if constexpr (std::is_same<T, float>::value && NM * D > 8192) {
         return fail(MA_EUNSUPPORTED, "fp32 tile too large");
     } else {
-        return (hd.lens || hd.m != NM) ? launch_l<T, NM, D, true>(L, B, hd, BH, nc, apply)
-                                       : launch_l<T, NM, D, false>(L, B, hd, BH, nc, apply);
+        if (hd.lens) return launch_l<T, NM, D, true, true>(L, B, hd, BH, nc, apply);
+        return hd.m != NM ? launch_l<T, NM, D, true>(L, B, hd, BH, nc, apply)
+                          : launch_l<T, NM, D, false>(L, B, hd, BH, nc, apply);
     }
 }
 
@@ -166,9 +168,10 @@ int run_half_steps(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDi
 }
 
 // ---- one workgroup per head ----
-template <typename T, bool RGB, bool RGM> int launch_fused(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
+template <typename T, bool RGB, bool RGM, bool LENS = false>
+int launch_fused(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
 {
-    using U = ma::FusedHead<T, RGB, RGM>;
+    using U = ma::FusedHead<T, RGB, RGM, LENS>;
     // one workgroup per compute unit (its LDS holds one), each looping over heads
     const int64_t grid = c.BH < c.num_cus ? c.BH : c.num_cus;
     hd.units = c.BH;
@@ -177,7 +180,7 @@ template <typename T, bool RGB, bool RGM> int launch_fused(Launcher &L, const Ca
     const int T_ = c.T;
     return L.run(kFused, [&] {
         return launched([&] {
-            hipLaunchKernelGGL((ma::monarch_fused_head<T, RGB, RGM>), dim3((unsigned)grid), dim3(64 * U::NW), 0,
+            hipLaunchKernelGGL((ma::monarch_fused_head<T, RGB, RGM, LENS>), dim3((unsigned)grid), dim3(64 * U::NW), 0,
                                L.stream, p, hd, BH, T_);
         });
     });
@@ -188,7 +191,8 @@ template <typename T> int run_fused(Launcher &L, const CallBufs &B, ma::HeadDims
     if constexpr (sizeof(T) != 2) {
         return fail(MA_EUNSUPPORTED, "the fused kernel needs 16-bit elements");
     } else {
-        const bool rgb = hd.lens || hd.b != 16 || hd.n != hd.m * hd.b, rgm = hd.lens || hd.m != 16;
+        if (hd.lens) return launch_fused<T, true, true, true>(L, B, hd, c);
+        const bool rgb = hd.b != 16 || hd.n != hd.m * hd.b, rgm = hd.m != 16;
         if (rgb && rgm) return launch_fused<T, true, true>(L, B, hd, c);
         if (rgb) return launch_fused<T, true, false>(L, B, hd, c);
         if (rgm) return launch_fused<T, false, true>(L, B, hd, c);
@@ -224,7 +228,7 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
     const int32_t dtype = std::is_same<T, float>::value ? MA_F32 : std::is_same<T, __bf16>::value ? MA_BF16 : MA_F16;
     ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};
     hd.lens = B.lens;
-    hd.H = c.H;
+    hd.H = (int)c.H;
     if (path == kFusedHead && !fused_applies(dtype, c.d, c.m, c.b))
         return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d <= 64 and m, b <= 16");
     int rc;

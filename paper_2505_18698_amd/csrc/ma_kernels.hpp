@@ -192,6 +192,16 @@ template <typename T, int NR, int D, int NTH> struct TileChunks {
             *reinterpret_cast<u32x4 *>(sRow + r * LDR + col) = c[h];
         }
     }
+
+    // stage(), with rows >= valid written as zero whatever was fetched
+    template <int LDR> __device__ inline void stage(T *sRow, int tid, int valid) const
+    {
+#pragma unroll
+        for (int h = 0; h < CH; ++h) {
+            const int idx = tid + h * NTH, r = idx / CPR, col = (idx % CPR) * V;
+            *reinterpret_cast<u32x4 *>(sRow + r * LDR + col) = r < valid ? c[h] : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
 };
 
 // Lane 16g + c receives X[x0 + 4g + q][c0 + c], q = 0..3, from the row-major
@@ -225,6 +235,13 @@ template <typename T, int D> struct RowFrags {
                 f[c] = typename M::frag{};
             }
         }
+    }
+
+    // Zero the row when `drop` (a register select: no wait on anything else).
+    __device__ inline void clear_if(bool drop)
+    {
+#pragma unroll
+        for (int c = 0; c < D / M::KC; ++c) f[c] = drop ? typename M::frag{} : f[c];
     }
 };
 
@@ -510,14 +527,16 @@ struct HeadDims {
     // Per-sequence lengths (batch padding): head bh has lens[bh / H] real
     // rows (clamped to 0..n), or n when lens is null.
     const int *lens = nullptr;
-    int64_t H = 1;
+    int H = 1;
 };
 
-// Real rows of head bh.
+// Real rows of head bh.  The kernels read it in fetch() but use it only from
+// stage() on: their tile loads take the static bound n, so that they never
+// wait for this load, and the rows beyond it are zeroed on their way to LDS.
 __device__ inline int live_rows(const HeadDims &hd, int64_t bh)
 {
     if (!hd.lens) return hd.n;
-    const int len = hd.lens[bh / hd.H];
+    const int len = hd.lens[(int)bh / hd.H];  // bh < 2^31: the grids are checked on the host
     return len < 0 ? 0 : len > hd.n ? hd.n : len;
 }
 
@@ -578,7 +597,8 @@ __device__ inline float row_lse(float mx, float sum) { return kLn2 * (mx + __bui
 // NB = b rounded up to 16.  FIRST: alpha_R = the rows of Q (L^(0) = I) and
 // c_R = 1.  FINAL: also Y.
 // ---------------------------------------------------------------------------------------
-template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct RHalf {
+template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool LENS = false> struct RHalf {
+    static_assert(!LENS || RAGGED, "per-sequence lengths need the masked softmax");
     static constexpr int NT = NB / 16, RT = Split<NT>::RT, W = Split<NT>::W, NTH = 64 * W;
     static constexpr bool NF = NormFirst<NT, D>::value;
     static constexpr int LDK = Ld<T, D>::row;
@@ -589,11 +609,16 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
         TileChunks<T, NB, D, NTH> kt, vt;  // Kbar[k]; Vbar[k] (FINAL)
         RowFrags<T, D> bf[RT];             // rows j of alpha_R[k] (of Q when FIRST)
         float cr[RT];                      // c_R[k][j] (not FIRST)
+        int nl, row0;                      // real rows of the head, first key row k*b (LENS)
     };
 
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, int tid, Regs &gr)
     {
-        const int m = hd.m, b = hd.b, kv = block_keys(b, RAGGED ? live_rows(hd, bh) : hd.n, k);
+        if constexpr (LENS) {
+            gr.nl = live_rows(hd, bh);
+            gr.row0 = k * hd.b;
+        }
+        const int m = hd.m, b = hd.b, kv = block_keys(b, hd.n, k);  // rows in memory
         const int dd = hd.d;
         const int64_t N = (int64_t)m * b, hoff = bh * N * D, toff = bh * (int64_t)hd.n * dd;
         const int lane = tid & 63, wave = tid >> 6;
@@ -620,11 +645,17 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
         }
     }
 
-    __device__ static void stage(const Regs &gr, char *lds, int tid)
+    __device__ static void stage(const HeadDims &, const Regs &gr, char *lds, int tid)
     {
         T *Ks = reinterpret_cast<T *>(lds);
-        gr.kt.template stage<LDK>(Ks, tid);
-        if constexpr (FINAL) gr.vt.template stage<LDK>(Ks + NB * LDK, tid);
+        if constexpr (LENS) {  // keys >= nl: zero (they are masked, zero keeps them finite)
+            const int kv = gr.nl - gr.row0;
+            gr.kt.template stage<LDK>(Ks, tid, kv);
+            if constexpr (FINAL) gr.vt.template stage<LDK>(Ks + NB * LDK, tid, kv);
+        } else {
+            gr.kt.template stage<LDK>(Ks, tid);
+            if constexpr (FINAL) gr.vt.template stage<LDK>(Ks + NB * LDK, tid);
+        }
     }
 
     // After stage() and a barrier.
@@ -634,7 +665,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
         T *Ks = reinterpret_cast<T *>(lds);
         T *Vs = Ks + NB * LDK;
         // keys >= kv: padding, masked (omega); kv <= 0: padding only, R = 0
-        const int m = hd.m, b = hd.b, kv = block_keys(b, RAGGED ? live_rows(hd, bh) : hd.n, k);
+        const int m = hd.m, b = hd.b, kv = block_keys(b, LENS ? gr.nl : hd.n, k);
         const int64_t N = (int64_t)m * b;
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
@@ -647,11 +678,20 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
             rscale[r] = (FIRST || jr[r] >= b) ? hd.s_log2e : hd.s_log2e * fast_rcp(fmaxf(gr.cr[r], kTiny));
         }
 
+        RowFrags<T, D> bfq[RT];  // at t = 1 with per-sequence lengths: Q rows beyond the length zeroed
+        if constexpr (FIRST && LENS) {
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+                bfq[r] = gr.bf[r];
+                bfq[r].clear_if(jr[r] >= kv);
+            }
+        }
+        const RowFrags<T, D> *bf = (FIRST && LENS) ? bfq : gr.bf;
         f32x4 sc[RT][NT];  // lane holds S'[i = 16t + 4g + qq][j] of row tile r
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             f32x4 acc[RT];
-            gemm_scores_rt<T, D, RT>(Ks + (16 * t + c16) * LDK, gr.bf, acc, g);
+            gemm_scores_rt<T, D, RT>(Ks + (16 * t + c16) * LDK, bf, acc, g);
 #pragma unroll
             for (int r = 0; r < RT; ++r) sc[r][t] = acc[r];
         }
@@ -677,7 +717,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
             }
             sum = lanegroup_sum(sum);
             t2 = lanegroup_sum(t2);
-            const bool live = !RAGGED || kv > 0;
+            const bool live = !LENS || kv > 0;
             inv[r] = live ? fast_rcp(sum) : 0.f;
             // c_L = sum_i R log R = sum_i R (Z - max) - log(sum)   (natural-log units)
             if (g == 0 && jr[r] < b)
@@ -723,7 +763,8 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED> struct
 // softmax over k), then, after the probabilities have gone through LDS, RT
 // tiles of 16 key-block columns k (c_R and alpha_R).
 // ---------------------------------------------------------------------------------------
-template <typename T, int NM, int D, bool RAGGED> struct LHalf {
+template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHalf {
+    static_assert(!LENS || RAGGED, "per-sequence lengths need the masked softmax");
     static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W, NTH = 64 * W;
     static constexpr int LDQ = Ld<T, D>::row, LDP = Ld<T, NM>::row;
     static constexpr int A_ELEMS = NM * LDQ, P_ELEMS = NM * LDP;
@@ -733,6 +774,7 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
     struct Regs {
         TileChunks<T, NM, D, NTH> qt, at;  // Qbar[j] (rows l), alpha_L[j] (rows k)
         float cl;                          // c_L[k = tid][j]
+        int nl, j;                         // real rows of the head, the class (LENS)
     };
 
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, int tid, Regs &gr)
@@ -742,25 +784,31 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
         const int dd = hd.d;
         const T *qh = p.q + bh * (int64_t)hd.n * dd;
         const T *al = p.aL + hoff + (int64_t)j * m * D;
-        const int nl = RAGGED ? live_rows(hd, bh) : hd.n;
-        const int ml = (nl - j + b - 1) / b;  // real rows l of class j: l*b + j < nl
+        if constexpr (LENS) {
+            gr.nl = live_rows(hd, bh);
+            gr.j = j;
+        }
+        const int ml = (hd.n - j + b - 1) / b;  // rows l of class j in memory: l*b + j < n
         gr.qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * dd; }, ml, tid, dd);
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
     }
 
-    __device__ static void stage(const Regs &gr, char *lds, int tid)
+    __device__ static void stage(const HeadDims &hd, const Regs &gr, char *lds, int tid)
     {
         T *Qs = reinterpret_cast<T *>(lds);
         T *APs = Qs + NM * LDQ;
-        gr.qt.template stage<LDQ>(Qs, tid);
+        if constexpr (LENS)  // real rows l of class j: l*b + j < nl
+            gr.qt.template stage<LDQ>(Qs, tid, (gr.nl - gr.j + hd.b - 1) / hd.b);
+        else
+            gr.qt.template stage<LDQ>(Qs, tid);
         gr.at.template stage<LDQ>(APs, tid);
         if (tid < NM) reinterpret_cast<float *>(APs + AP_ELEMS)[tid] = gr.cl * kLog2e;
     }
 
     // After stage() and a barrier.
-    __device__ static void compute(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, const Regs &, char *lds,
-                                   int tid)
+    __device__ static void compute(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, const Regs &gr,
+                                   char *lds, int tid)
     {
         T *Qs = reinterpret_cast<T *>(lds);
         T *APs = Qs + NM * LDQ;  // alpha_L, then P
@@ -770,7 +818,7 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
-        const int mk = RAGGED ? live_blocks(m, b, live_rows(hd, bh)) : m;  // blocks k >= mk: no real key
+        const int mk = LENS ? live_blocks(m, b, gr.nl) : m;  // blocks k >= mk: no real key
 
         // scores and softmax over k for the query rows of this wave
         int lr[RT];
@@ -812,7 +860,7 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
             }
             sum = lanegroup_sum(sum);
             // tile rows l >= m carry no weight, nor does a head without a real key
-            const bool live = lr[r] < m && (!RAGGED || mk > 0);
+            const bool live = lr[r] < m && (!LENS || mk > 0);
             inv[r] = live ? fast_rcp(sum) : 0.f;
             lse[r] = live ? row_lse(mx, sum) : 0.f;
         }
@@ -869,7 +917,8 @@ template <typename T, int NM, int D, bool RAGGED> struct LHalf {
 // Last L half-step fused with the second Monarch product and the store of O
 // for (head bh, class j); each wave owns RT tiles of 16 query rows l.
 // ---------------------------------------------------------------------------------------
-template <typename T, int NM, int D, bool RAGGED> struct Apply {
+template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Apply {
+    static_assert(!LENS || RAGGED, "per-sequence lengths need the masked softmax");
     static constexpr int NT = NM / 16, RT = Split<NT>::RT, W = Split<NT>::W, NTH = 64 * W;
     static constexpr bool NF = NormFirst<NT, D>::value;
     static constexpr int LDK = Ld<T, D>::row;
@@ -879,6 +928,7 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         TileChunks<T, NM, D, NTH> at, yt;  // alpha_L[j], Y[j] (rows k)
         float cl;                          // c_L[k = tid][j]
         RowFrags<T, D> bf[RT];             // Qbar[j] rows l
+        int nl;                            // real rows of the head (LENS)
     };
 
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, int tid, Regs &gr)
@@ -891,17 +941,17 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
         gr.yt.fetch([=](int kk) { return yj + (int64_t)kk * D; }, m, tid);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
-        const int nl = RAGGED ? live_rows(hd, bh) : hd.n;
+        if constexpr (LENS) gr.nl = live_rows(hd, bh);
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int l = (wave * RT + r) * 16 + (lane & 15);
-            gr.bf[r].load((int64_t)l * b + j < nl ? p.q + bh * (int64_t)hd.n * hd.d + ((int64_t)l * b + j) * hd.d
-                                                  : nullptr,
+            gr.bf[r].load((int64_t)l * b + j < hd.n ? p.q + bh * (int64_t)hd.n * hd.d + ((int64_t)l * b + j) * hd.d
+                                                    : nullptr,
                           lane >> 4, hd.d);  // Qbar[j][l]; zero for padded rows
         }
     }
 
-    __device__ static void stage(const Regs &gr, char *lds, int tid)
+    __device__ static void stage(const HeadDims &, const Regs &gr, char *lds, int tid)
     {
         T *As = reinterpret_cast<T *>(lds);
         T *Ys = As + NM * LDK;
@@ -922,17 +972,26 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
-        const int nl = RAGGED ? live_rows(hd, bh) : hd.n;
-        const int mk = RAGGED ? live_blocks(m, b, nl) : m;  // blocks k >= mk: no real key
+        const int nl = LENS ? gr.nl : hd.n;
+        const int mk = LENS ? live_blocks(m, b, nl) : m;  // blocks k >= mk: no real key
         int lr[RT];
 #pragma unroll
         for (int r = 0; r < RT; ++r) lr[r] = (wave * RT + r) * 16 + c16;
+        RowFrags<T, D> bfq[RT];  // with per-sequence lengths: query rows beyond the length zeroed
+        if constexpr (LENS) {
+#pragma unroll
+            for (int r = 0; r < RT; ++r) {
+                bfq[r] = gr.bf[r];
+                bfq[r].clear_if((int64_t)lr[r] * b + j >= nl);
+            }
+        }
+        const RowFrags<T, D> *bf = LENS ? bfq : gr.bf;
 
         f32x4 sc[RT][NT];  // lane holds Z[k = 16t + 4g + qq][l] (log2 units) of row tile r
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             f32x4 acc[RT];
-            gemm_scores_rt<T, D, RT>(As + (16 * t + c16) * LDK, gr.bf, acc, g);
+            gemm_scores_rt<T, D, RT>(As + (16 * t + c16) * LDK, bf, acc, g);
             const f32x4 bias = *reinterpret_cast<const f32x4 *>(cLs + 16 * t + 4 * g);
 #pragma unroll
             for (int r = 0; r < RT; ++r) {
@@ -957,7 +1016,7 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
                 }
             }
             sum = lanegroup_sum(sum);
-            const bool any = !RAGGED || mk > 0;  // a head without a real key has L = 0
+            const bool any = !LENS || mk > 0;  // a head without a real key has L = 0
             inv[r] = any ? fast_rcp(sum) : 0.f;
             lse[r] = (lr[r] < m && any) ? row_lse(mx, sum) : 0.f;
             if constexpr (NF) {
@@ -993,7 +1052,7 @@ template <typename T, int NM, int D, bool RAGGED> struct Apply {
         for (int r = 0; r < RT; ++r) {  // rows nl..n-1 (batch padding) are written as zero
             const int64_t row = (int64_t)lr[r] * b + j;
             store_row<T, D>(row < hd.n ? p.out + bh * (int64_t)hd.n * hd.d + row * hd.d : nullptr, o[r],
-                            row < nl ? inv[r] : 0.f, lane, hd.d);
+                            (!LENS || row < nl) ? inv[r] : 0.f, lane, hd.d);
         }
     }
 };
@@ -1012,7 +1071,7 @@ template <typename U, typename T> __device__ inline void run_units(const Bufs<T>
     typename U::Regs cur, nxt;
     U::fetch(p, hd, u / per, (int)(u % per), tid, cur);
     while (true) {
-        U::stage(cur, lds, tid);
+        U::stage(hd, cur, lds, tid);
         __syncthreads();
         const int64_t un = u + gridDim.x;
         if (un < hd.units) U::fetch(p, hd, un / per, (int)(un % per), tid, nxt);
@@ -1024,26 +1083,26 @@ template <typename U, typename T> __device__ inline void run_units(const Bufs<T>
     }
 }
 
-template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED>
+template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool LENS>
 __global__ __launch_bounds__(64 * Split<NB / 16>::W) void r_half_step(Bufs<T> p, HeadDims hd)
 {
-    using U = RHalf<T, NB, D, FIRST, FINAL, RAGGED>;
+    using U = RHalf<T, NB, D, FIRST, FINAL, RAGGED, LENS>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
     run_units<U>(p, hd, hd.m, lds);
 }
 
-template <typename T, int NM, int D, bool RAGGED>
+template <typename T, int NM, int D, bool RAGGED, bool LENS>
 __global__ __launch_bounds__(64 * Split<NM / 16>::W) void l_half_step(Bufs<T> p, HeadDims hd)
 {
-    using U = LHalf<T, NM, D, RAGGED>;
+    using U = LHalf<T, NM, D, RAGGED, LENS>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
     run_units<U>(p, hd, hd.b, lds);
 }
 
-template <typename T, int NM, int D, bool RAGGED>
+template <typename T, int NM, int D, bool RAGGED, bool LENS>
 __global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> p, HeadDims hd)
 {
-    using U = Apply<T, NM, D, RAGGED>;
+    using U = Apply<T, NM, D, RAGGED, LENS>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
     run_units<U>(p, hd, hd.b, lds);
 }
@@ -1068,7 +1127,8 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> 
 // effect in program order, so a unit may overwrite a block it has read.  The
 // arithmetic of a unit is that of RHalf / LHalf / Apply at 16 rows.
 // ---------------------------------------------------------------------------------------
-template <typename T, bool RGB, bool RGM> struct FusedHead {
+template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
+    static_assert(!LENS || (RGB && RGM), "per-sequence lengths need the masked softmaxes");
     static_assert(sizeof(T) == 2, "16-bit elements only");
     static constexpr int D = 64, NW = 16, LD = D + 8;  // 64 * NW threads (the launch bound below); rows + 16 bytes
     // Blocks are BS elements apart: 16 rows plus 16 bytes, so that the 16
@@ -1082,7 +1142,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         T *Qs, *Ks, *As, *Rs;
         float *cRs, *cLs;  // c_R[k][j] at k*CS + j, c_L[j][k] at j*CS + k
         int m, b, n, d, lane, g, c16;  // n: rows of a head in q, k, v, out; d <= D
-        int nl, mk;        // real rows of the head being computed (rows >= nl are zero padding), live key blocks
+        int nl, mk;        // with per-sequence lengths: real rows of the head being computed, live key blocks
         float s_log2e;
         int64_t bh;        // the head being computed
         int steps;         // T, the step count
@@ -1101,7 +1161,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             if (jv) rs = c.s_log2e * fast_rcp(fmaxf(c.cRs[k * CS + j], kTiny));
         }
         T *Kk = c.Ks + k * BS;
-        const int kv = block_keys(c.b, c.nl, k);  // keys >= kv: padding, masked (omega); none: R = 0
+        const int kv = block_keys(c.b, LENS ? c.nl : c.n, k);  // keys >= kv: padding, masked (omega); none: R = 0
         f32x4 sc;  // lane holds S'[i = 4g + qq][j]
         gemm_scores_rt<T, D, 1>(Kk + c.c16 * LD, &bf, &sc, c.g);
         const float nb = -tiles_max<1, RGB>(&sc, kv, c.g) * rs;
@@ -1117,7 +1177,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         }
         sum = lanegroup_sum(sum);
         t2 = lanegroup_sum(t2);
-        const bool live = !RGB || kv > 0;
+        const bool live = !LENS || kv > 0;
         const float inv = live ? fast_rcp(sum) : 0.f;
         if (c.g == 0 && jv) c.cLs[j * CS + k] = live ? kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum)) : 0.f;
         static_assert(NormFirst<1, D>::value, "probabilities normalised before the products, as in RHalf");
@@ -1155,17 +1215,18 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             const float bias = (!RGM || kk < c.m) ? c.cLs[j * CS + kk] * kLog2e : 0.f;
             sc[qq] = __builtin_fmaf(acc[qq], c.s_log2e, -bias);
         }
-        const float mx = tiles_max<1, RGM>(&sc, c.mk, c.g);  // blocks k >= mk: no real key
+        const int mk = LENS ? c.mk : c.m;  // blocks k >= mk: no real key
+        const float mx = tiles_max<1, RGM>(&sc, mk, c.g);
         float sum = 0.f;
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
             float e = __builtin_amdgcn_exp2f(sc[qq] - mx);
-            if (RGM && 4 * c.g + qq >= c.mk) e = 0.f;
+            if (RGM && 4 * c.g + qq >= mk) e = 0.f;
             sum += e;
             sc[qq] = e;
         }
         sum = lanegroup_sum(sum);
-        const bool any = !RGM || c.mk > 0;  // a head without a real key has L = 0
+        const bool any = !LENS || mk > 0;  // a head without a real key has L = 0
         inv = any ? fast_rcp(sum) : 0.f;
         lse = (c.c16 < c.m && any) ? row_lse(mx, sum) : 0.f;
         return sc;
@@ -1211,17 +1272,17 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
 #pragma unroll
         for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, 1>(c.Ks + j * LD, BS, 16 * vt, pf, c.lane);
         const int row = l * c.b + j;  // rows nl..n-1 (batch padding) are written as zero
-        store_row<T, D>(row < c.n ? out_h + (int64_t)row * c.d : nullptr, o, row < c.nl ? 1.0f : 0.f, c.lane, c.d);
+        store_row<T, D>(row < c.n ? out_h + (int64_t)row * c.d : nullptr, o, (!LENS || row < c.nl) ? 1.0f : 0.f,
+                        c.lane, c.d);
     }
 
     static constexpr int PER = 2 * 256 * 8 / (64 * NW);  // 16-byte chunks of Qs and Ks per thread
 
     // Issue the loads of head bh: Qbar and Kbar chunks (zero where there is no
     // row) for the LDS regions, and Vbar[w] for wave w's last R half-step.
-    // Rows >= nl (padding) and columns >= d are zero and never read; a head
-    // has n rows in memory.
-    __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int nl, int d, int64_t bh, int tid,
-                                     u32x4 *raw, u32x4 *vb)
+    // Rows >= n (padding) and columns >= d are zero and never read.
+    __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int d, int64_t bh, int tid, u32x4 *raw,
+                                     u32x4 *vb)
     {
         const int64_t hoff = bh * (int64_t)n * d;
         const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
@@ -1230,9 +1291,9 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
             const int idx = tid + h * 64 * NW;
             const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
             raw[h] = u32x4{0u, 0u, 0u, 0u};
-            if (reg == 0 && blk < b && r < m && r * b + blk < nl && col < d)
+            if (reg == 0 && blk < b && r < m && r * b + blk < n && col < d)
                 raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * d + col);  // Qbar[blk][r]
-            if (reg == 1 && blk < m && r < b && blk * b + r < nl && col < d)
+            if (reg == 1 && blk < m && r < b && blk * b + r < n && col < d)
                 raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * d + col);  // Kbar[blk][r]
         }
         const int w = tid >> 6, lane = tid & 63;
@@ -1240,7 +1301,7 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
         for (int h = 0; h < 2; ++h) {
             const int r = (lane >> 3) + 8 * h, col = (lane & 7) * 8;
             vb[h] = u32x4{0u, 0u, 0u, 0u};
-            if (w < m && r < b && w * b + r < nl && col < d)
+            if (w < m && r < b && w * b + r < n && col < d)
                 vb[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * d + col);
         }
     }
@@ -1281,17 +1342,30 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
 
         u32x4 raw[PER], vcur[2], vnext[2];
         int64_t bh = blockIdx.x;
-        load_head(p, m, b, c.n, live_rows(hd, bh), c.d, bh, tid, raw, vcur);
+        load_head(p, m, b, c.n, c.d, bh, tid, raw, vcur);
         for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) *chunk(c.As, idx) = u32x4{0u, 0u, 0u, 0u};
         for (; bh < BH; bh += gridDim.x) {
             c.bh = bh;
-            c.nl = live_rows(hd, bh);
-            c.mk = live_blocks(m, b, c.nl);
+            if constexpr (LENS) {
+                // the loads of this head were issued with the static bound n:
+                // rows >= nl are zeroed here, on their way to LDS
+                c.nl = live_rows(hd, bh);
+                c.mk = live_blocks(m, b, c.nl);
 #pragma unroll
-            for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
+                for (int h = 0; h < PER; ++h) {
+                    const int idx = tid + h * 64 * NW, blk = (idx >> 7) & 15, r = (idx >> 3) & 15;
+                    const int row = (idx >> 11) == 0 ? r * b + blk : blk * b + r;  // Qbar[blk][r] or Kbar[blk][r]
+                    *chunk(c.Qs, idx) = row < c.nl ? raw[h] : u32x4{0u, 0u, 0u, 0u};
+                }
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    if (w * b + (c.lane >> 3) + 8 * h >= c.nl) vcur[h] = u32x4{0u, 0u, 0u, 0u};  // Vbar[w]
+            } else {
+#pragma unroll
+                for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
+            }
             __syncthreads();
-            if (bh + gridDim.x < BH)
-                load_head(p, m, b, c.n, live_rows(hd, bh + gridDim.x), c.d, bh + gridDim.x, tid, raw, vnext);
+            if (bh + gridDim.x < BH) load_head(p, m, b, c.n, c.d, bh + gridDim.x, tid, raw, vnext);
 
             for (int t = 1; t <= T_; ++t) {
                 const bool first = t == 1, last = t == T_;
@@ -1318,10 +1392,10 @@ template <typename T, bool RGB, bool RGM> struct FusedHead {
     }
 };
 
-template <typename T, bool RGB, bool RGM>
+template <typename T, bool RGB, bool RGM, bool LENS>
 __global__ __launch_bounds__(1024) void monarch_fused_head(Bufs<T> p, HeadDims hd, int64_t BH, int T_)
 {
-    using U = FusedHead<T, RGB, RGM>;
+    using U = FusedHead<T, RGB, RGM, LENS>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
     U::run(p, hd, BH, T_, lds);
 }
