@@ -106,9 +106,10 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out,
  *        checked on the host: they are clamped to 0..N.  Owned by the caller.
  * Batch element beta is computed as the single sequence of its first
  * lens[beta] rows, post-padded with zero rows to m * b at the batch's m and
- * b: rows >= lens[beta] of q, k, v are not read, keys at positions >=
- * lens[beta] are masked out of every R softmax, and the padded query rows
- * take part in the iteration as zero rows.  Here whole key blocks can be
+ * b: rows >= lens[beta] of q, k, v count as zero whatever they hold (the
+ * kernels may load them, up to row N - 1, and replace them by zero), keys at
+ * positions >= lens[beta] are masked out of every R softmax, and the padded
+ * query rows take part in the iteration as zero rows.  Here whole key blocks can be
  * padding, which the paper leaves undefined: such a block gets R = 0 and no
  * weight in the L softmax (Z_L = -inf), so that M keeps unit row sums and
  * zero columns at every padded key; a sequence of length 0 has M = 0.

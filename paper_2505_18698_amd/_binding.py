@@ -148,7 +148,8 @@ def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
 def monarch_attn_fwd_varlen(q, k, v, out, lens, m: int, b: int, T: int, stream=None):
     """monarch_attn_fwd over a batch of post-padded sequences: lens (int32 device
     tensor [B]) holds the real rows of each batch element; rows >= lens[beta]
-    of q, k, v are not read and those of out are written as zero.  Returns `out`."""
+    of q, k, v count as zero whatever they hold, and those of out are written
+    as zero.  Returns `out`."""
     import torch
 
     _check_tensors(q, k, v, out)

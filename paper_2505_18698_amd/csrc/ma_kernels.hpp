@@ -553,10 +553,11 @@ __device__ inline int live_blocks(int m, int b, int nl) { return min(m, (nl + b 
 // rows >= n of q, k, v are never read (zero is loaded instead), keys >= n are
 // masked out of every R softmax, rows >= n of out are never written, and the
 // states cover all N rows.  With per-sequence lengths (HeadDims::lens) the
-// same holds for the real rows nl <= n of each head, and whole key blocks
-// can be padding: such a block gets R = 0 (zero alpha_L, c_L, Y) and no
-// weight in the L softmax (Z_L = -inf), rows nl..n-1 of out are written as
-// zero.  Layouts (per head):
+// real rows nl <= n of each head play the part of n: rows nl..n-1 of q, k, v
+// may be loaded but are replaced by zero, whole key blocks can be padding
+// (such a block gets R = 0, i.e. zero alpha_L, c_L, Y, and no weight in the
+// L softmax, Z_L = -inf), and rows nl..n-1 of out are written as zero.
+// Layouts (per head):
 //   q, k, v, out [B*H][n][d], d <= D (columns d..D-1 of every tile are zero);
 //   alpha_R [m][b][D] (row k*b + j), alpha_L and Y [b][m][D] (row j*m + k),
 //   c_L [m][b] (written by the R half-step of block k for all j),

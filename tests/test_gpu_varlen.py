@@ -128,7 +128,7 @@ def test_full_lengths_equal_the_plain_call(ma, path, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_padding_rows_are_not_read(ma, path, dtype):
+def test_padding_row_contents_do_not_matter(ma, path, dtype):
     """NaN in every padded row of q, k and v changes nothing."""
     m, b, d, T = 10, 16, 64, 2
     lens = [160, 77, 16, 3]
