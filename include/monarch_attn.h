@@ -196,6 +196,22 @@ int monarch_attn_bwd(const void *q, const void *k, const void *v, const void *do
                      int64_t B, int64_t H, int64_t N, int64_t d,
                      int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
 
+/*
+ * monarch_attn_bwd_varlen -- the gradient of monarch_attn_fwd_varlen (a batch
+ * of sequences padded to N rows, lens[B] real rows per batch element, device
+ * int32, clamped to 0..N; see there).  Key blocks of padding only have R = 0
+ * and no L weight, so they pass no gradient.  Rows lens[beta]..N-1 of q, k,
+ * v count as zero in the forward pass, so rows lens[beta]..N-1 of dq, dk and
+ * dv are written as zero, and those rows of dout and of the inputs are
+ * ignored whatever they hold.  lens must not overlap dq, dk or dv.  The
+ * other arguments, the limits, the workspace and the errors are those of
+ * monarch_attn_bwd.
+ */
+int monarch_attn_bwd_varlen(const void *q, const void *k, const void *v, const void *dout,
+                            void *dq, void *dk, void *dv, const int32_t *lens,
+                            int64_t B, int64_t H, int64_t N, int64_t d,
+                            int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
+
 /* MA_OK if monarch_attn_bwd supports (N, d, m, b, T, dtype), else MA_EINVAL or
  * MA_EUNSUPPORTED (with last_error set).  Makes no HIP call. */
 int monarch_attn_bwd_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype);

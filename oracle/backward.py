@@ -34,6 +34,12 @@ Derivation (per head, Qbar = s * Q in the layout of eq. beta_r):
   identity L^(0)) gives dQbar directly; for t > 1 the L update of step t-1
   gets dL = d alpha_R . Qbar + d c_R and dQbar += L d alpha_R, and the sweep
   continues.  Finally dQ = s * dQbar (rows l*b + j).
+
+Batch padding (``batch_padding=True``): a sequence of n rows at the batch's m
+and b may have whole key blocks of padding.  As in the forward oracle, such
+a block has R = 0 and no L weight (Z_L = -inf), so it passes no gradient;
+rows past n are inputs that the forward replaces by zero, so their
+gradients are zero.
 """
 from __future__ import annotations
 
@@ -43,10 +49,14 @@ import torch
 
 # -- the forward pass in torch (for autograd) ---------------------------------------------
 
-def torch_forward(q, k, v, m: int, b: int, T: int):
-    """O for one head; q, k, v float64 torch tensors [N, d], N <= m*b (post-padding)."""
+def torch_forward(q, k, v, m: int, b: int, T: int, batch_padding: bool = False):
+    """O for one head; q, k, v float64 torch tensors [N, d], N <= m*b (post-padding;
+    with batch_padding any 1 <= N <= m*b, whole blocks of padding allowed)."""
     n, d = q.shape
-    assert (m - 1) * b < n <= m * b and T >= 1
+    if batch_padding:
+        assert 1 <= n <= m * b and T >= 1
+    else:
+        assert (m - 1) * b < n <= m * b and T >= 1
     pad = m * b - n
     if pad:
         z = q.new_zeros(pad, d)
@@ -59,12 +69,18 @@ def torch_forward(q, k, v, m: int, b: int, T: int):
     if pad:
         pos = torch.arange(m * b).reshape(m, 1, b)
         keymask = keymask.masked_fill(pos >= n, float("-inf"))
+    live = -(-n // b)                                    # key blocks with a real key
+    empty = (torch.arange(m) >= live)[:, None, None]     # blocks of padding only: R = 0
+    keymask = keymask.masked_fill(empty, 0.0)            # (their softmax input is kept finite)
+    lmask = torch.zeros(m, dtype=q.dtype).masked_fill(torch.arange(m) >= live, float("-inf"))
     L = torch.eye(m, dtype=q.dtype).expand(b, m, m)      # L^(0)[j, k, l] = delta_kl
     for _ in range(T):
         alpha_r = torch.einsum("jkl,jld->kjd", L, Qb)    # eq. beta_r
         c_r = L.sum(dim=2).transpose(0, 1)               # [k, j]
+        c_r = torch.where(empty[:, :, 0], torch.ones_like(c_r), c_r)   # zero (unused) on empty blocks
         beta_r = torch.einsum("kjd,kid->kji", alpha_r, Kb)
         R = torch.softmax(beta_r / c_r[..., None] + keymask, dim=2)      # eq. R_update
+        R = torch.where(empty, torch.zeros_like(R), R)
         alpha_l = torch.einsum("kji,kid->jkd", R, Kb)    # eq. beta_l
         # sum_i R log R over the real keys (masked entries are exactly 0 and
         # contribute 0; the inner where keeps log away from them, also in the gradient)
@@ -72,16 +88,19 @@ def torch_forward(q, k, v, m: int, b: int, T: int):
         c_l = torch.where(live, R * torch.log(torch.where(live, R, torch.ones_like(R))), torch.zeros_like(R))
         c_l = c_l.sum(dim=2).transpose(0, 1)                               # [j, k]
         beta_l = torch.einsum("jld,jkd->jlk", Qb, alpha_l)
-        L = torch.softmax(beta_l - c_l[:, None, :], dim=2).permute(0, 2, 1)  # eq. L_update, [j, k, l]
+        L = torch.softmax(beta_l - c_l[:, None, :] + lmask, dim=2).permute(0, 2, 1)  # eq. L_update, [j, k, l]
     Y = torch.einsum("kji,kid->jkd", R, Vb)              # eq. monarch_multiply
     Oj = torch.einsum("jkl,jkd->jld", L, Y)              # O[l*b + j] = Oj[j, l]
     return Oj.permute(1, 0, 2).reshape(m * b, d)[:n]
 
 
-def autograd_grads(q, k, v, dout, m: int, b: int, T: int):
-    """(dQ, dK, dV) of <O, dout> for one head, numpy float64 arrays in and out."""
+def autograd_grads(q, k, v, dout, m: int, b: int, T: int, batch_padding: bool = False):
+    """(dQ, dK, dV) of <O, dout> for one head, numpy float64 arrays in and out
+    (with batch_padding, n = 0 rows gives empty gradients)."""
+    if q.shape[0] == 0:
+        return (np.zeros((0, q.shape[1])),) * 3
     tq, tk, tv = (torch.tensor(np.asarray(x, dtype=np.float64), requires_grad=True) for x in (q, k, v))
-    o = torch_forward(tq, tk, tv, m, b, T)
+    o = torch_forward(tq, tk, tv, m, b, T, batch_padding)
     gq, gk, gv = torch.autograd.grad(o, (tq, tk, tv), torch.tensor(np.asarray(dout, dtype=np.float64)))
     return gq.numpy(), gk.numpy(), gv.numpy()
 
@@ -110,11 +129,14 @@ def _softmax_back(p, dp):
     return p * (dp - np.dot(dp, p))
 
 
-def state_form_backward(q, k, v, dout, m: int, b: int, T: int):
+def state_form_backward(q, k, v, dout, m: int, b: int, T: int, batch_padding: bool = False):
     """(dQ, dK, dV) for one head by the reverse sweep of the module docstring."""
     q, k, v, dout = (np.asarray(x, dtype=np.float64) for x in (q, k, v, dout))
     n, d = q.shape
-    assert (m - 1) * b < n <= m * b
+    if batch_padding:
+        assert 0 <= n <= m * b
+    else:
+        assert (m - 1) * b < n <= m * b
     Np = m * b
     qp, kp, vp, dop = (np.zeros((Np, d)) for _ in range(4))
     qp[:n], kp[:n], vp[:n], dop[:n] = q, k, v, dout
@@ -122,7 +144,8 @@ def state_form_backward(q, k, v, dout, m: int, b: int, T: int):
     Qb = np.stack([np.stack([s * qp[l * b + j] for l in range(m)]) for j in range(b)])  # [j, l, d]
     Kb = kp.reshape(m, b, d)
     Vb = vp.reshape(m, b, d)
-    nkeys = [min(b, n - kk * b) for kk in range(m)]
+    nkeys = [max(min(b, n - kk * b), 0) for kk in range(m)]   # 0: a block of padding only
+    live = -(-n // b)                                          # blocks with a real key
 
     # forward, keeping the states of every step
     aR = [np.stack([np.stack([Qb[j, kk] for j in range(b)]) for kk in range(m)])]   # alpha_R^(1)[k, j]
@@ -130,7 +153,7 @@ def state_form_backward(q, k, v, dout, m: int, b: int, T: int):
     aL, cL, Rs, Ls = [], [], [], []
     for t in range(T):
         R = np.zeros((m, b, b))
-        for kk in range(m):
+        for kk in range(live):
             for j in range(b):
                 z = Kb[kk, : nkeys[kk]] @ aR[t][kk, j] / cR[t][kk, j]
                 R[kk, j, : nkeys[kk]] = _softmax(z)
@@ -143,7 +166,8 @@ def state_form_backward(q, k, v, dout, m: int, b: int, T: int):
         L = np.zeros((b, m, m))
         for j in range(b):
             for l in range(m):
-                L[j, :, l] = _softmax(al[j] @ Qb[j, l] - cl[j])
+                if live:
+                    L[j, :live, l] = _softmax((al[j] @ Qb[j, l] - cl[j])[:live])
         Rs.append(R), aL.append(al), cL.append(cl), Ls.append(L)
         if t + 1 < T:
             aR.append(np.einsum("jkl,jld->kjd", L, Qb))
@@ -170,14 +194,14 @@ def state_form_backward(q, k, v, dout, m: int, b: int, T: int):
         dcl = np.zeros_like(cl)
         for j in range(b):
             for l in range(m):
-                dz = _softmax_back(L[j, :, l], dL[j, :, l])
+                dz = _softmax_back(L[j, :, l], dL[j, :, l])   # zero on the blocks left out
                 dQb[j, l] += dz @ al[j]
                 dal[j] += np.outer(dz, Qb[j, l])
                 dcl[j] -= dz
         # R update of step t
         daR = np.zeros((m, b, d))
         dcR = np.zeros((m, b))
-        for kk in range(m):
+        for kk in range(live):      # blocks of padding only have R = 0 and pass nothing back
             nk = nkeys[kk]
             for j in range(b):
                 r = R[kk, j, :nk]

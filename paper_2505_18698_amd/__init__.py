@@ -29,6 +29,7 @@ try:
         monarch_attention,
         monarch_attention_autograd,
         monarch_attn_bwd,
+        monarch_attn_bwd_varlen,
         monarch_attn_bwd_check,
         monarch_attn_bwd_workspace_bytes,
         monarch_attn_check,

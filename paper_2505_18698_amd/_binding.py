@@ -25,6 +25,7 @@ EXPORTS = (
     "monarch_attn_fwd_objective",
     "monarch_attn_exact_fwd",
     "monarch_attn_bwd",
+    "monarch_attn_bwd_varlen",
     "monarch_attn_bwd_check",
     "monarch_attn_bwd_workspace_bytes",
     "monarch_attn_last_error",
@@ -60,6 +61,8 @@ def _load() -> ctypes.CDLL:
     lib.monarch_attn_exact_fwd.restype = ctypes.c_int
     lib.monarch_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
     lib.monarch_attn_bwd.restype = ctypes.c_int
+    lib.monarch_attn_bwd_varlen.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
+    lib.monarch_attn_bwd_varlen.restype = ctypes.c_int
     lib.monarch_attn_bwd_check.argtypes = [i64, i64, i64, i64, i32, i32]
     lib.monarch_attn_bwd_check.restype = ctypes.c_int
     lib.monarch_attn_bwd_workspace_bytes.argtypes = [i64, i64, i64, i64, i64, i64, i32, i32]
@@ -145,6 +148,14 @@ def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
     return out
 
 
+def _check_lens(q, lens):
+    import torch
+
+    if not isinstance(lens, torch.Tensor) or lens.device != q.device or lens.dtype != torch.int32 \
+            or not lens.is_contiguous() or tuple(lens.shape) != (q.shape[0],):
+        raise ValueError("lens must be a contiguous int32 tensor [B] on the device of q")
+
+
 def monarch_attn_fwd_varlen(q, k, v, out, lens, m: int, b: int, T: int, stream=None):
     """monarch_attn_fwd over a batch of post-padded sequences: lens (int32 device
     tensor [B]) holds the real rows of each batch element; rows >= lens[beta]
@@ -153,9 +164,7 @@ def monarch_attn_fwd_varlen(q, k, v, out, lens, m: int, b: int, T: int, stream=N
     import torch
 
     _check_tensors(q, k, v, out)
-    if not isinstance(lens, torch.Tensor) or lens.device != q.device or lens.dtype != torch.int32 \
-            or not lens.is_contiguous() or tuple(lens.shape) != (q.shape[0],):
-        raise ValueError("lens must be a contiguous int32 tensor [B] on the device of q")
+    _check_lens(q, lens)
     B, H, N, d = q.shape
     stream = _stream(q, stream)
     with torch.cuda.device(q.device):
@@ -215,6 +224,23 @@ def monarch_attn_bwd(q, k, v, dout, dq, dk, dv, m: int, b: int, T: int, stream=N
     return dq, dk, dv
 
 
+def monarch_attn_bwd_varlen(q, k, v, dout, dq, dk, dv, lens, m: int, b: int, T: int, stream=None):
+    """The gradient of monarch_attn_fwd_varlen (lens: int32 device tensor [B]);
+    rows >= lens[beta] of dq, dk, dv are written as zero.  Returns (dq, dk, dv)."""
+    import torch
+
+    _check_tensors(q, k, v, dout)
+    _check_tensors(q, dq, dk, dv)
+    _check_lens(q, lens)
+    B, H, N, d = q.shape
+    stream = _stream(q, stream)
+    with torch.cuda.device(q.device):
+        _check(LIB.monarch_attn_bwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), dq.data_ptr(),
+                                           dk.data_ptr(), dv.data_ptr(), lens.data_ptr(), B, H, N, d, m, b, T,
+                                           dtype_code(q.dtype), stream))
+    return dq, dk, dv
+
+
 def monarch_attn_bwd_check(N: int, d: int, m: int, b: int, T: int, dtype: int) -> int:
     return LIB.monarch_attn_bwd_check(N, d, m, b, T, dtype)
 
@@ -235,37 +261,46 @@ _AUTOGRAD_FN = None
 
 
 def _autograd_function():
-    """torch.autograd.Function whose forward is monarch_attn_fwd and whose
-    backward is monarch_attn_bwd (both on torch's current stream)."""
+    """torch.autograd.Function whose forward is monarch_attn_fwd (or _varlen)
+    and whose backward is monarch_attn_bwd (or _varlen), both on torch's
+    current stream."""
     global _AUTOGRAD_FN
     if _AUTOGRAD_FN is None:
         import torch
 
         class MonarchAttentionFn(torch.autograd.Function):
             @staticmethod
-            def forward(ctx, q, k, v, m, b, T):
+            def forward(ctx, q, k, v, m, b, T, lens):
                 q, k, v = q.contiguous(), k.contiguous(), v.contiguous()
-                ctx.save_for_backward(q, k, v)
+                ctx.save_for_backward(q, k, v, lens) if lens is not None else ctx.save_for_backward(q, k, v)
                 ctx.shape = (m, b, T)
                 out = torch.empty_like(q)
-                return monarch_attn_fwd(q, k, v, out, m, b, T)
+                if lens is None:
+                    return monarch_attn_fwd(q, k, v, out, m, b, T)
+                return monarch_attn_fwd_varlen(q, k, v, out, lens, m, b, T)
 
             @staticmethod
             def backward(ctx, dout):
-                q, k, v = ctx.saved_tensors
+                saved = ctx.saved_tensors
+                q, k, v = saved[:3]
                 m, b, T = ctx.shape
                 dq, dk, dv = (torch.empty_like(q) for _ in range(3))
-                monarch_attn_bwd(q, k, v, dout.contiguous(), dq, dk, dv, m, b, T)
-                return dq, dk, dv, None, None, None
+                if len(saved) == 3:
+                    monarch_attn_bwd(q, k, v, dout.contiguous(), dq, dk, dv, m, b, T)
+                else:
+                    monarch_attn_bwd_varlen(q, k, v, dout.contiguous(), dq, dk, dv, saved[3], m, b, T)
+                return dq, dk, dv, None, None, None, None
 
         _AUTOGRAD_FN = MonarchAttentionFn
     return _AUTOGRAD_FN
 
 
-def monarch_attention_autograd(q, k, v, m: int, b: int, T: int):
+def monarch_attention_autograd(q, k, v, m: int, b: int, T: int, lens=None):
     """MonarchAttention as a differentiable torch op: the forward pass and, on
-    backward, the gradient (monarch_attn_bwd) with respect to q, k and v."""
-    return _autograd_function().apply(q, k, v, m, b, T)
+    backward, the gradient with respect to q, k and v.  With lens (int32
+    device tensor [B]) the batch is padded per sequence, as in
+    monarch_attn_fwd_varlen."""
+    return _autograd_function().apply(q, k, v, m, b, T, lens)
 
 
 def monarch_attn_check(N: int, d: int, m: int, b: int, T: int, dtype: int) -> int:

@@ -57,9 +57,22 @@ template <typename T> struct BwdBufs {
 struct BwdDims {
     int m, b, n, d;  // as in the forward (the states are D = 64, 96 or 128 wide, d <= D)
     float s;         // 1/sqrt(d)
+    // Per-sequence lengths (batch padding): head bh has lens[bh / H] real
+    // rows, clamped to 0..n, or n when lens is null.  Rows past them count as
+    // zero in the forward, so their gradients are zero.
+    const int *lens = nullptr;
+    int H = 1;
 };
 
 namespace bwd {
+
+// Real rows of head bh (bh < 2^31: the grids are checked on the host).
+__device__ inline int live_rows(const BwdDims &dm, int64_t bh)
+{
+    if (!dm.lens) return dm.n;
+    const int len = dm.lens[(int)bh / dm.H];
+    return len < 0 ? 0 : len > dm.n ? dm.n : len;
+}
 
 // Row strides (floats) of the LDS tiles: 16-byte rows, 68 floats for tiles
 // of up to 64 columns, 100 and 148 for 96 and 128.  The 64-column stride is
@@ -272,7 +285,9 @@ template <typename T, int S, int D, bool LAST> struct LBwd {
         const int m = dm.m, b = dm.b, n = dm.n, d = dm.d;
         const int64_t bh = blockIdx.x / b;
         const int j = blockIdx.x % b;
-        const int ml = (n - j + b - 1) / b;  // rows l with l*b + j < n
+        const int nl = live_rows(dm, bh);
+        const int ml = (nl - j + b - 1) / b;  // real rows l: l*b + j < nl
+        const int mk = min(m, (nl + b - 1) / b);  // key blocks k < mk hold a real key
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
         // whole-unit tiles (rows k): alpha_L[j][k]; Y[j][k] (LAST) or d alpha_R'[k][j]
         float *aL = lds, *X = aL + S * LD;
@@ -313,20 +328,20 @@ template <typename T, int S, int D, bool LAST> struct LBwd {
             // SPAN lanes and CPL columns k per lane for each
             for (int base = wave * RPW; base < C; base += W * RPW) {
                 const int l = base + lane / SPAN, col = lane % SPAN;
-                const bool live = l0 + l < m;
+                const bool live = l0 + l < m && mk > 0;  // no real key at all: L = 0
                 float *row = Lm + l * LS;
                 float z[CPL], mx = -INFINITY;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
                     const int k = col + 64 * u;
-                    z[u] = live && k < m ? dm.s * row[k] - cL[k] : -INFINITY;
+                    z[u] = live && k < mk ? dm.s * row[k] - cL[k] : -INFINITY;
                     mx = fmaxf(mx, z[u]);
                 }
                 mx = group_max<SPAN>(mx);
                 float sum = 0.f;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
-                    z[u] = live && col + 64 * u < m ? __expf(z[u] - mx) : 0.f;
+                    z[u] = live && col + 64 * u < mk ? __expf(z[u] - mx) : 0.f;
                     sum += z[u];
                 }
                 sum = group_sum<SPAN>(sum);
@@ -418,7 +433,8 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
         const int m = dm.m, b = dm.b, n = dm.n, d = dm.d;
         const int64_t bh = blockIdx.x / m;
         const int k = blockIdx.x % m;
-        const int kv = min(b, n - k * b);  // real keys (and query rows) of block k
+        const int kn = min(b, n - k * b);                   // rows of block k in memory
+        const int kv = min(b, live_rows(dm, bh) - k * b);  // real keys (and query rows); <= 0: padding only
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
         const int64_t row0 = (int64_t)k * b;  // first row of block k
         // whole-unit tiles (rows i): Kbar, Vbar (LAST)
@@ -437,6 +453,7 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
         for (int ch = 0; ch < G_::NCH; ++ch) {
             const int j0 = ch * C;
             const int jb = min(max(b - j0, 0), C), jq = min(max(kv - j0, 0), C);  // live rows; rows of Q (t = 1)
+            const int jn = min(max(kn - j0, 0), C);                                // rows of dq in memory (t = 1)
             if constexpr (FIRST) {
                 load_tile<T, NTH, C, D, LD>(aR, jq, d, [&](int jj) { return p.q + toff + (row0 + j0 + jj) * d; }, tid);
             } else {
@@ -466,9 +483,9 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
             // lane for each): R, then dZ scaled by s / c_R[j] in place of dR
             for (int base = wave * RPW; base < C; base += W * RPW) {
                 const int jj = base + lane / SPAN, col = lane % SPAN;
-                const bool live = jj < jb;
+                const bool live = jj < jb && kv > 0;  // a block of padding only has R = 0
                 float *rr = Rm + jj * LS, *dr = dR + jj * LS;
-                const float sc = dm.s / cR[jj];  // c_R = 1 past the live rows
+                const float sc = live ? dm.s / cR[jj] : 0.f;
                 float z[CPL], mx = -INFINITY;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
@@ -509,7 +526,7 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
                     }
                 }
                 dzlog = group_sum<SPAN>(dzlog);
-                if (!FIRST && live && col == 0) p.dcR[coff + row0 + j0 + jj] = -dzlog / cR[jj];
+                if (!FIRST && jj < jb && col == 0) p.dcR[coff + row0 + j0 + jj] = live ? -dzlog / cR[jj] : 0.f;
             }
             __syncthreads();
 
@@ -519,8 +536,9 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
                 T *dq = p.dq + toff + (row0 + j0) * d;
                 gemm<W, C, D, S>(
                     wave, lane,
-                    [&](int jj, int e, float v) {
-                        if (jj < jq && e < d) dq[(int64_t)jj * d + e] = static_cast<T>(dQ[(int64_t)jj * d + e] + v);
+                    [&](int jj, int e, float v) {  // rows past the length: zero
+                        if (jj < jn && e < d)
+                            dq[(int64_t)jj * d + e] = static_cast<T>(jj < jq ? dQ[(int64_t)jj * d + e] + v : 0.f);
                     },
                     pair<false, false, LS, LD>(dR, Kb));
             } else {
@@ -542,9 +560,9 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
             float *dKg = p.dK + toff + row0 * d;
             T *dk = p.dk + toff + row0 * d;
             dK.store(wave, lane, [&](int i, int e, float v) {
-                if (i < kv && e < d) {
+                if (i < (FIRST ? kn : kv) && e < d) {  // at t = 1 rows past the length get zero
                     const int64_t o = (int64_t)i * d + e;
-                    const float acc = LAST ? v : v + dKg[o];
+                    const float acc = i >= kv ? 0.f : LAST ? v : v + dKg[o];
                     if constexpr (FIRST) {
                         dk[o] = static_cast<T>(acc);
                     } else {
@@ -556,7 +574,7 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
         if constexpr (LAST) {
             T *dv = p.dv + toff + row0 * d;
             dV.store(wave, lane, [&](int i, int e, float v) {
-                if (i < kv && e < d) dv[(int64_t)i * d + e] = static_cast<T>(v);
+                if (i < kn && e < d) dv[(int64_t)i * d + e] = static_cast<T>(i < kv ? v : 0.f);
             });
         }
     }

@@ -31,7 +31,9 @@ int launch_r_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, in
 // The reverse sweep, t = T .. 1: the L update of step t, then its R update.
 template <typename T, int S, int D> int bwd_sweep(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {
-    const ma::BwdDims dm{c.m, c.b, c.n, c.d, (float)(1.0 / std::sqrt((double)c.d))};
+    ma::BwdDims dm{c.m, c.b, c.n, c.d, (float)(1.0 / std::sqrt((double)c.d))};
+    dm.lens = B.lens;
+    dm.H = (int)c.H;
     ma::BwdBufs<T> p{(const T *)B.q, (const T *)B.k, (const T *)B.v, (const T *)B.dout, nullptr, nullptr,
                      (const T *)B.Y, nullptr, nullptr, B.dQ, B.dK, (T *)B.dq, (T *)B.dk, (T *)B.dv, B.daL, B.dcL,
                      B.dY, B.daR, B.dcR};
@@ -62,6 +64,8 @@ template <typename T, int D> int run_bwd_d(Launcher &L, const BwdCallBufs &B, co
 {
     ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};
     hd.T = c.T;
+    hd.lens = B.lens;  // the recompute takes the same per-sequence lengths
+    hd.H = (int)c.H;
     int rc;
     for (int t = 1; t <= c.T; ++t) {
         hd.t = t;

@@ -108,6 +108,7 @@ struct BwdCallBufs {
     float *cR, *cL;
     size_t st, cst;
     float *dQ, *dK, *daL, *dcL, *dY, *daR, *dcR;
+    const int *lens = nullptr;  // [B] real rows per batch element (device), or null
 };
 
 // Enqueue the gradient (forward recompute, then the reverse sweep) for one element type.

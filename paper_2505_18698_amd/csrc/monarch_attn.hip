@@ -265,8 +265,9 @@ BwdLayout bwd_layout(int64_t BH, int64_t N, int64_t d, int64_t m, int64_t b, int
                      T};
 }
 
-int backward(const void *q, const void *k, const void *v, const void *dout, void *dq, void *dk, void *dv, int64_t B,
-             int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
+int backward(const void *q, const void *k, const void *v, const void *dout, void *dq, void *dk, void *dv,
+             const int32_t *lens, bool need_lens, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b,
+             int32_t T, int32_t dtype, void *stream)
 {
     g_err[0] = '\0';
     if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
@@ -277,6 +278,8 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)dout | (uintptr_t)dq | (uintptr_t)dk |
          (uintptr_t)dv) & 15u)
         return fail(MA_EINVAL, "all tensors must be 16-byte aligned");
+    if (need_lens && !lens) return fail(MA_EINVAL, "null lens pointer");
+    if (need_lens && ((uintptr_t)lens & 3u)) return fail(MA_EINVAL, "lens must be 4-byte aligned");
     const int64_t BH = B * H;
     if (BH * (int64_t)(m > b ? m : b) > (int64_t)0x7fffffff) return fail(MA_EUNSUPPORTED, "too many heads for one grid");
     const size_t tb = (size_t)BH * N * d * elem_bytes(dtype);
@@ -287,6 +290,8 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
             if (overlaps(outs[o], tb, ins[i], tb)) return fail(MA_EINVAL, "dq, dk, dv must not overlap q, k, v or dout");
         for (int o2 = o + 1; o2 < 3; ++o2)
             if (overlaps(outs[o], tb, outs[o2], tb)) return fail(MA_EINVAL, "dq, dk and dv must not overlap");
+        if (lens && overlaps(outs[o], tb, lens, (size_t)B * sizeof(int32_t)))
+            return fail(MA_EINVAL, "lens must not overlap dq, dk or dv");
     }
     int dev = 0, num_cus = 0;
     if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
@@ -296,6 +301,7 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
     if ((rc = acquire_workspace(dev, (hipStream_t)stream, lay.total(), &base, ws_hold)) != MA_OK) return rc;
     BwdCallBufs bufs{};
     bufs.q = q, bufs.k = k, bufs.v = v, bufs.dout = dout, bufs.dq = dq, bufs.dk = dk, bufs.dv = dv;
+    bufs.lens = lens;
     char *p = base;
     bufs.st = lay.st;
     bufs.cst = lay.cs / sizeof(float);
@@ -494,7 +500,14 @@ int monarch_attn_bwd(const void *q, const void *k, const void *v, const void *do
                      int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
                      void *stream)
 {
-    return backward(q, k, v, dout, dq, dk, dv, B, H, N, d, m, b, T, dtype, stream);
+    return backward(q, k, v, dout, dq, dk, dv, nullptr, false, B, H, N, d, m, b, T, dtype, stream);
+}
+
+int monarch_attn_bwd_varlen(const void *q, const void *k, const void *v, const void *dout, void *dq, void *dk,
+                            void *dv, const int32_t *lens, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m,
+                            int64_t b, int32_t T, int32_t dtype, void *stream)
+{
+    return backward(q, k, v, dout, dq, dk, dv, lens, true, B, H, N, d, m, b, T, dtype, stream);
 }
 
 int monarch_attn_bwd_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype)

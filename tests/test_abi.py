@@ -170,6 +170,21 @@ def test_varlen_rejects_null_or_misaligned_lens():
     assert f(None, None, None, None, None, 0, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_OK
 
 
+def test_bwd_varlen_rejects_null_or_misaligned_lens():
+    import paper_2505_18698_amd as ma
+
+    f = ma.LIB.monarch_attn_bwd_varlen
+    t = [FAKE * (i + 1) for i in range(7)]  # q, k, v, dout, dq, dk, dv: 1 MiB apart, no overlap
+    assert f(*t, None, 2, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_EINVAL
+    assert "lens" in ma.monarch_attn_last_error()
+    assert f(*t, 9 * FAKE + 2, 2, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_EINVAL
+    assert "aligned" in ma.monarch_attn_last_error()
+    assert f(*t, 5 * FAKE + 64, 2, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_EINVAL  # inside dq
+    assert "overlap" in ma.monarch_attn_last_error()
+    assert f(None, None, None, None, None, None, None, None, 0, 1, 256, 64, 16, 16, 1, 1, None) == ma.MA_OK
+    assert f(*t, 9 * FAKE, 2, 1, 256, 64, 16, 16, 33, 1, None) == ma.MA_EUNSUPPORTED  # T > 32, as the plain call
+
+
 # ---- the gradient entry point ----
 
 @pytest.mark.parametrize(

@@ -164,3 +164,136 @@ def test_single_key_blocks_are_exact_attention(ma):
             ref = nv.dense_softmax_attention(q[bi, h, :n], k[bi, h, :n], v[bi, h, :n])
             assert oracle.rel_frobenius(o[bi, h, :n], ref) <= 1e-5
         assert np.all(o[bi, :, n:] == 0.0)
+
+
+# ---- the gradient of a padded batch (monarch_attn_bwd_varlen) ----
+
+GTOL = {"f32": 2e-5, "bf16": 3e-2, "f16": 3e-2}  # as the plain gradient's parity tests
+
+
+def run_bwd_varlen(ma, q, k, v, dout, lens, m, b, T, dtype):
+    import torch
+
+    td = _td(dtype)
+    tq, tk, tv, tg = (torch.from_numpy(x).to(td).cuda() for x in (q, k, v, dout))
+    outs = [torch.full_like(tq, float("nan")) for _ in range(3)]
+    ma.monarch_attn_bwd_varlen(tq, tk, tv, tg, *outs, torch.tensor(lens, dtype=torch.int32, device="cuda"), m, b, T)
+    torch.cuda.synchronize()
+    return [o.double().cpu().numpy() for o in outs]
+
+
+def check_bwd_varlen(got, q, k, v, dout, lens, m, b, T, dtype, label):
+    import oracle.backward as ob
+
+    lens = [int(x) for x in lens]
+    want = [[], [], []]
+    have = [[], [], []]
+    for bi, n in enumerate(lens):
+        for g in got:
+            assert np.isfinite(g).all(), (label, "non-finite or unwritten elements")
+            assert np.all(g[bi, :, n:] == 0.0), (label, "padding rows of the gradient not zero", bi)
+        for h in range(q.shape[1]):
+            ref = ob.autograd_grads(q[bi, h, :n], k[bi, h, :n], v[bi, h, :n], dout[bi, h, :n], m, b, T,
+                                    batch_padding=True)
+            for c in range(3):
+                want[c].append(ref[c].ravel())
+                have[c].append(got[c][bi, h, :n].ravel())
+    errs = [oracle.rel_frobenius(np.concatenate(x), np.concatenate(w)) for x, w in zip(have, want)]
+    print(f"{label} lens={lens} rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
+    for name, e in zip(("dq", "dk", "dv"), errs):
+        assert e <= GTOL[dtype], (label, name, e)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize(
+    "m,b,d,lens",
+    [
+        (8, 8, 32, [64, 20, 0, 5]),
+        (10, 10, 64, [100, 37, 9, 1]),
+        (8, 48, 64, [384, 100, 47, 0]),
+        (13, 29, 72, [377, 29, 30]),
+        (24, 16, 128, [384, 5, 200]),
+    ],
+)
+@pytest.mark.parametrize("T", [1, 2])
+def test_varlen_gradient_matches_oracle(ma, dtype, m, b, d, lens, T):
+    if dtype == "f32" and max(-(-m // 16) * 16, -(-b // 16) * 16) * (64 if d <= 64 else 96 if d <= 96 else 128) > 8192:
+        pytest.skip("fp32 tiles of this size are not supported")
+    N = m * b
+    q, k, v = si.random_qkv(len(lens), 2, N, d, dtype, seed=11 * m + b + T, scale=1.5)
+    g = si.random_cotangent((len(lens), 2, N, d), dtype, seed=m + T)
+    got = run_bwd_varlen(ma, q, k, v, g, lens, m, b, T, dtype)
+    check_bwd_varlen(got, q, k, v, g, lens, m, b, T, dtype, f"bwd varlen {dtype} m={m} b={b} d={d} T={T}")
+
+
+def test_varlen_gradient_three_steps_f16(ma):
+    m, b, d, T = 9, 12, 64, 3
+    lens = [103, 60, 12, 11]
+    q, k, v = si.random_qkv(len(lens), 2, 103, d, "f16", seed=91, scale=1.5)
+    g = si.random_cotangent((len(lens), 2, 103, d), "f16", seed=91)
+    got = run_bwd_varlen(ma, q, k, v, g, lens, m, b, T, "f16")
+    check_bwd_varlen(got, q, k, v, g, lens, m, b, T, "f16", "bwd varlen f16 ragged N T=3")
+
+
+def test_varlen_gradient_long_sequences(ma):
+    """N = 4096 = 64 x 64, most of two sequences padding."""
+    m = b = 64
+    lens = [4096, 1000, 65]
+    q, k, v = si.random_qkv(len(lens), 1, m * b, 64, "bf16", seed=93, scale=1.5)
+    g = si.random_cotangent((len(lens), 1, m * b, 64), "bf16", seed=93)
+    got = run_bwd_varlen(ma, q, k, v, g, lens, m, b, 2, "bf16")
+    check_bwd_varlen(got, q, k, v, g, lens, m, b, 2, "bf16", "bwd varlen long")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_varlen_gradient_ignores_padding_contents(ma, dtype):
+    """NaN in every padded row of q, k, v and dout changes nothing."""
+    m, b, d, T = 10, 16, 64, 2
+    lens = [160, 77, 16, 3]
+    q, k, v = si.random_qkv(len(lens), 2, m * b, d, dtype, seed=95)
+    g = si.random_cotangent((len(lens), 2, m * b, d), dtype, seed=95)
+    g1 = run_bwd_varlen(ma, q, k, v, g, lens, m, b, T, dtype)
+    q2, k2, v2, gg = q.copy(), k.copy(), v.copy(), g.copy()
+    for bi, n in enumerate(lens):
+        for x in (q2, k2, v2, gg):
+            x[bi, :, n:] = np.nan
+    g2 = run_bwd_varlen(ma, q2, k2, v2, gg, lens, m, b, T, dtype)
+    for a, c in zip(g1, g2):
+        np.testing.assert_array_equal(a, c)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_varlen_gradient_full_lengths_equal_the_plain_call(ma, dtype):
+    import torch
+
+    m, b, d, T = 12, 12, 64, 2
+    q, k, v = si.random_qkv(3, 2, m * b, d, dtype, seed=97)
+    g = si.random_cotangent((3, 2, m * b, d), dtype, seed=97)
+    got = run_bwd_varlen(ma, q, k, v, g, [m * b] * 3, m, b, T, dtype)
+    td = _td(dtype)
+    tq, tk, tv, tg = (torch.from_numpy(x).to(td).cuda() for x in (q, k, v, g))
+    outs = [torch.empty_like(tq) for _ in range(3)]
+    ma.monarch_attn_bwd(tq, tk, tv, tg, *outs, m, b, T)
+    torch.cuda.synchronize()
+    for a, o in zip(got, outs):
+        np.testing.assert_array_equal(a, o.double().cpu().numpy())
+
+
+def test_autograd_with_lengths(ma):
+    """monarch_attention_autograd(..., lens=...) runs the varlen forward and gradient."""
+    import torch
+
+    m, b, d, T = 8, 8, 64, 2
+    lens = [64, 30, 0]
+    q, k, v = si.random_qkv(3, 2, m * b, d, "bf16", seed=99)
+    g = si.random_cotangent((3, 2, m * b, d), "bf16", seed=99)
+    tq, tk, tv = (torch.from_numpy(x).to(torch.bfloat16).cuda().requires_grad_() for x in (q, k, v))
+    tl = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    o = ma.monarch_attention_autograd(tq, tk, tv, m, b, T, lens=tl)
+    o.backward(torch.from_numpy(g).to(torch.bfloat16).cuda())
+    torch.cuda.synchronize()
+    want = run_bwd_varlen(ma, q, k, v, g, lens, m, b, T, "bf16")
+    for t, w in zip((tq, tk, tv), want):
+        np.testing.assert_array_equal(t.grad.double().cpu().numpy(), w)
+    fwd = run_varlen(ma, q, k, v, lens, m, b, T, "bf16")
+    np.testing.assert_array_equal(o.detach().double().cpu().numpy(), fwd)

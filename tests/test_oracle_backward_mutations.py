@@ -60,7 +60,8 @@ def _softmax_back_variant(kind):
 
 def _torch_forward_variant(kind):
     """A copy of the torch forward with one mistake."""
-    def torch_forward(q, k, v, m, b, T):
+    def torch_forward(q, k, v, m, b, T, batch_padding=False):
+        assert not batch_padding  # the battery runs single sequences
         n, d = q.shape
         pad = m * b - n
         if pad:

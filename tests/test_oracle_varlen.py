@@ -120,3 +120,79 @@ def test_varlen_rejects_lengths_out_of_range(oracle_lib):
     for lens in ([9, 1], [-1, 3]):
         with pytest.raises(ValueError):
             oracle.monarch_attention_varlen(q, k, v, np.array(lens), 2, 4, 1)
+
+
+# ---- the gradient under batch padding (oracle/backward.py) ----
+
+def _one(n, d, seed):
+    q, k, v = si.random_qkv(1, 1, n, d, "f32", seed=seed, scale=1.5)
+    do = si.random_cotangent((n, d), "f32", seed=seed)
+    return (x[0, 0].astype(np.float64) for x in (q, k, v)), do.astype(np.float64)
+
+
+@pytest.mark.parametrize("n,m,b,T", [(5, 4, 3, 1), (5, 4, 3, 2), (2, 3, 4, 2), (7, 4, 3, 3)])
+def test_padded_torch_forward_matches_oracle(n, m, b, T):
+    import torch
+
+    import oracle.backward as bw
+
+    (q, k, v), _ = _one(n, 6, seed=100 + n + T)
+    o = bw.torch_forward(*(torch.tensor(x) for x in (q, k, v)), m, b, T, batch_padding=True).numpy()
+    ref = nv.monarch_attention_varlen(q[None, None], k[None, None], v[None, None], [n], m, b, T)[0, 0, :n]
+    np.testing.assert_allclose(o, ref, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("n,m,b,T", [(4, 3, 3, 1), (4, 3, 3, 2), (2, 3, 2, 2)])
+def test_padded_autograd_matches_finite_differences(n, m, b, T):
+    import torch
+
+    import oracle.backward as bw
+
+    (q, k, v), _ = _one(n, 3, seed=110 + n + T)
+    args = [torch.tensor(x, requires_grad=True) for x in (q, k, v)]
+    assert torch.autograd.gradcheck(lambda a, c, e: bw.torch_forward(a, c, e, m, b, T, batch_padding=True), args,
+                                    eps=1e-6, atol=1e-7)
+
+
+@pytest.mark.parametrize("T", [1, 2, 3])
+def test_padded_single_key_blocks_give_the_attention_gradient(T):
+    """b = 1: exact attention over the real keys, so the textbook gradient."""
+    import oracle.backward as bw
+
+    (q, k, v), do = _one(7, 4, seed=120 + T)
+    got = bw.autograd_grads(q, k, v, do, 12, 1, T, batch_padding=True)
+    for g, w in zip(got, bw.attention_grads(q, k, v, do)):
+        np.testing.assert_allclose(g, w, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("n,m,b", [(5, 4, 3), (9, 5, 4), (3, 6, 4)])
+def test_padded_one_step_gradient_matches_fewer_blocks(n, m, b):
+    """At T = 1 the real rows are those of the problem without the empty blocks,
+    as functions of the real inputs, so the gradients agree too."""
+    import oracle.backward as bw
+
+    (q, k, v), do = _one(n, 5, seed=130 + n)
+    got = bw.autograd_grads(q, k, v, do, m, b, 1, batch_padding=True)
+    want = bw.autograd_grads(q, k, v, do, -(-n // b), b, 1)
+    for g, w in zip(got, want):
+        np.testing.assert_allclose(g, w, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("n,m,b,T", [(5, 4, 3, 2), (1, 4, 3, 2), (9, 5, 4, 3), (13, 4, 4, 2)])
+def test_padded_state_form_backward_matches_autograd(n, m, b, T):
+    import oracle.backward as bw
+
+    (q, k, v), do = _one(n, 6, seed=140 + n + T)
+    got = bw.state_form_backward(q, k, v, do, m, b, T, batch_padding=True)
+    want = bw.autograd_grads(q, k, v, do, m, b, T, batch_padding=True)
+    for g, w in zip(got, want):
+        np.testing.assert_allclose(g, w, rtol=0, atol=1e-11)
+
+
+def test_padded_gradient_of_an_empty_sequence_is_empty():
+    import oracle.backward as bw
+
+    z = np.zeros((0, 4))
+    for g in bw.autograd_grads(z, z, z, z, 3, 3, 2, batch_padding=True) + \
+            bw.state_form_backward(z, z, z, z, 3, 3, 2, batch_padding=True):
+        assert g.shape == (0, 4)
