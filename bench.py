@@ -39,9 +39,9 @@ point and ViT-B/16 with its class token, with its per-kernel durations and
 the roofline of its dominant gradient kernel.  Reported beside the headline,
 not in it.
 
-varlen: monarch_attn_fwd_varlen on a padded batch (RoBERTa-base shape at
-N = 384, b = 48, T = 1; lengths iid uniform on 64..384), beside the plain
-call on the same tensors.
+varlen: monarch_attn_fwd_varlen and monarch_attn_bwd_varlen on a padded
+batch (RoBERTa-base shape at N = 384, b = 48, T = 1; lengths iid uniform on
+64..384), each beside the plain call on the same tensors.
 
 quality: the error of O against exact softmax attention and the gap of the
 variational objective to its exact-softmax maximum, for T = 1, 2, 3, on the
@@ -479,18 +479,34 @@ def measure_varlen(ma, torch, w, steps, warmup, low=64):
     ms = time_calls(torch, step_varlen, steps, warmup)
     ms_plain = time_calls(torch, step_plain, steps, warmup)
     kern, kern_plain = kernel_times(ma, step_varlen, steps), kernel_times(ma, step_plain, steps)
-    del sets
+
+    # the gradient of the same padded batch, beside the plain gradient
+    dout = torch.from_numpy(si.random_cotangent((w.B, w.H, w.N, w.d), w.dtype, seed=0)).to(td).cuda()
+    grads = [torch.empty_like(sets[0][0]) for _ in range(3)]
+
+    def bwd_varlen(i):
+        qq, kk, vv, _ = sets[i % nsets]
+        ma.monarch_attn_bwd_varlen(qq, kk, vv, dout, *grads, lens, w.m, w.b, w.T)
+
+    def bwd_plain(i):
+        qq, kk, vv, _ = sets[i % nsets]
+        ma.monarch_attn_bwd(qq, kk, vv, dout, *grads, w.m, w.b, w.T)
+
+    ms_bwd = time_calls(torch, bwd_varlen, steps, warmup)
+    ms_bwd_plain = time_calls(torch, bwd_plain, steps, warmup)
+    del sets, dout, grads
     torch.cuda.empty_cache()
     real = int(lens_np.sum())
     cfg = w.describe()
     cfg.update({"lengths": f"iid uniform on {min(low, w.N)}..{w.N}, seed 0", "real_rows": real,
                 "padded_rows": w.B * w.N, "rotating_input_sets": nsets})
     log(f"[bench] varlen {w.name}: {ms * 1e3:.1f} us per call (plain call {ms_plain * 1e3:.1f} us), "
-        f"{real} of {w.B * w.N} rows real")
+        f"gradient {ms_bwd * 1e3:.1f} us (plain {ms_bwd_plain * 1e3:.1f} us), {real} of {w.B * w.N} rows real")
     return {"config": cfg, "value": round(w.B * w.H * w.N / (ms * 1e-3), 1), "unit": UNIT,
             "ms_per_call": round(ms, 6), "plain_ms_per_call": round(ms_plain, 6),
             "real_heads_tokens_per_s": round(w.H * real / (ms * 1e-3), 1),
-            "kernels_us": kern, "plain_kernels_us": kern_plain}
+            "kernels_us": kern, "plain_kernels_us": kern_plain,
+            "gradient_ms_per_call": round(ms_bwd, 6), "plain_gradient_ms_per_call": round(ms_bwd_plain, 6)}
 
 
 def quality(ma, torch, w, steps_list=(1, 2, 3)):

@@ -273,7 +273,7 @@ __device__ inline void load_tile(float *dst, int nr, int nc, Src src, int tid)
 // The L update of class j of step t undone (LAST: t = T, the update that also
 // produced O).  S >= m; query rows l in chunks of C.
 // ---------------------------------------------------------------------------------------
-template <typename T, int S, int D, bool LAST> struct LBwd {
+template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
     using G_ = Geo<S, D>;
     static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
     static constexpr int SPAN = G_::SPAN, RPW = G_::RPW;
@@ -285,9 +285,9 @@ template <typename T, int S, int D, bool LAST> struct LBwd {
         const int m = dm.m, b = dm.b, n = dm.n, d = dm.d;
         const int64_t bh = blockIdx.x / b;
         const int j = blockIdx.x % b;
-        const int nl = live_rows(dm, bh);
-        const int ml = (nl - j + b - 1) / b;  // real rows l: l*b + j < nl
-        const int mk = min(m, (nl + b - 1) / b);  // key blocks k < mk hold a real key
+        const int nl = LENS ? live_rows(dm, bh) : n;
+        const int ml = (nl - j + b - 1) / b;                 // real rows l: l*b + j < nl
+        const int mk = LENS ? min(m, (nl + b - 1) / b) : m;  // key blocks k < mk hold a real key
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
         // whole-unit tiles (rows k): alpha_L[j][k]; Y[j][k] (LAST) or d alpha_R'[k][j]
         float *aL = lds, *X = aL + S * LD;
@@ -328,7 +328,7 @@ template <typename T, int S, int D, bool LAST> struct LBwd {
             // SPAN lanes and CPL columns k per lane for each
             for (int base = wave * RPW; base < C; base += W * RPW) {
                 const int l = base + lane / SPAN, col = lane % SPAN;
-                const bool live = l0 + l < m && mk > 0;  // no real key at all: L = 0
+                const bool live = l0 + l < m && (!LENS || mk > 0);  // no real key at all: L = 0
                 float *row = Lm + l * LS;
                 float z[CPL], mx = -INFINITY;
 #pragma unroll
@@ -421,7 +421,7 @@ template <typename T, int S, int D, bool LAST> struct LBwd {
 // The R update of block k of step t undone (FIRST: t = 1, LAST: t = T).
 // S >= b; rows j in chunks of C.
 // ---------------------------------------------------------------------------------------
-template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
+template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> struct RBwd {
     using G_ = Geo<S, D>;
     static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
     static constexpr int SPAN = G_::SPAN, RPW = G_::RPW;
@@ -433,8 +433,8 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
         const int m = dm.m, b = dm.b, n = dm.n, d = dm.d;
         const int64_t bh = blockIdx.x / m;
         const int k = blockIdx.x % m;
-        const int kn = min(b, n - k * b);                   // rows of block k in memory
-        const int kv = min(b, live_rows(dm, bh) - k * b);  // real keys (and query rows); <= 0: padding only
+        const int kn = min(b, n - k * b);                                // rows of block k in memory
+        const int kv = LENS ? min(b, live_rows(dm, bh) - k * b) : kn;  // real keys (and query rows); <= 0: none
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
         const int64_t row0 = (int64_t)k * b;  // first row of block k
         // whole-unit tiles (rows i): Kbar, Vbar (LAST)
@@ -483,9 +483,9 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
             // lane for each): R, then dZ scaled by s / c_R[j] in place of dR
             for (int base = wave * RPW; base < C; base += W * RPW) {
                 const int jj = base + lane / SPAN, col = lane % SPAN;
-                const bool live = jj < jb && kv > 0;  // a block of padding only has R = 0
+                const bool live = jj < jb && (!LENS || kv > 0);  // a block of padding only has R = 0
                 float *rr = Rm + jj * LS, *dr = dR + jj * LS;
-                const float sc = live ? dm.s / cR[jj] : 0.f;
+                const float sc = (!LENS || live) ? dm.s / cR[jj] : 0.f;  // c_R = 1 past the rows j < b
                 float z[CPL], mx = -INFINITY;
 #pragma unroll
                 for (int u = 0; u < CPL; ++u) {
@@ -526,7 +526,8 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
                     }
                 }
                 dzlog = group_sum<SPAN>(dzlog);
-                if (!FIRST && jj < jb && col == 0) p.dcR[coff + row0 + j0 + jj] = live ? -dzlog / cR[jj] : 0.f;
+                if (!FIRST && jj < jb && col == 0)  // zero for a block of padding only (read by l_bwd)
+                    p.dcR[coff + row0 + j0 + jj] = (!LENS || live) ? -dzlog / cR[jj] : 0.f;
             }
             __syncthreads();
 
@@ -537,8 +538,9 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
                 gemm<W, C, D, S>(
                     wave, lane,
                     [&](int jj, int e, float v) {  // rows past the length: zero
-                        if (jj < jn && e < d)
-                            dq[(int64_t)jj * d + e] = static_cast<T>(jj < jq ? dQ[(int64_t)jj * d + e] + v : 0.f);
+                        if (jj < (LENS ? jn : jq) && e < d)
+                            dq[(int64_t)jj * d + e] =
+                                static_cast<T>((!LENS || jj < jq) ? dQ[(int64_t)jj * d + e] + v : 0.f);
                     },
                     pair<false, false, LS, LD>(dR, Kb));
             } else {
@@ -560,9 +562,9 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
             float *dKg = p.dK + toff + row0 * d;
             T *dk = p.dk + toff + row0 * d;
             dK.store(wave, lane, [&](int i, int e, float v) {
-                if (i < (FIRST ? kn : kv) && e < d) {  // at t = 1 rows past the length get zero
+                if (i < (LENS && FIRST ? kn : kv) && e < d) {  // at t = 1 rows past the length get zero
                     const int64_t o = (int64_t)i * d + e;
-                    const float acc = i >= kv ? 0.f : LAST ? v : v + dKg[o];
+                    const float acc = (LENS && i >= kv) ? 0.f : LAST ? v : v + dKg[o];
                     if constexpr (FIRST) {
                         dk[o] = static_cast<T>(acc);
                     } else {
@@ -574,24 +576,24 @@ template <typename T, int S, int D, bool FIRST, bool LAST> struct RBwd {
         if constexpr (LAST) {
             T *dv = p.dv + toff + row0 * d;
             dV.store(wave, lane, [&](int i, int e, float v) {
-                if (i < kn && e < d) dv[(int64_t)i * d + e] = static_cast<T>(i < kv ? v : 0.f);
+                if (i < (LENS ? kn : kv) && e < d) dv[(int64_t)i * d + e] = static_cast<T>((!LENS || i < kv) ? v : 0.f);
             });
         }
     }
 };
 
-template <typename T, int S, int D, bool LAST>
+template <typename T, int S, int D, bool LAST, bool LENS>
 __global__ __launch_bounds__(64 * unit_waves(S)) void l_bwd(BwdBufs<T> p, BwdDims dm)
 {
-    __shared__ __attribute__((aligned(16))) float lds[LBwd<T, S, D, LAST>::LDS_FLOATS];
-    LBwd<T, S, D, LAST>::run(p, dm, lds);
+    __shared__ __attribute__((aligned(16))) float lds[LBwd<T, S, D, LAST, LENS>::LDS_FLOATS];
+    LBwd<T, S, D, LAST, LENS>::run(p, dm, lds);
 }
 
-template <typename T, int S, int D, bool FIRST, bool LAST>
+template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS>
 __global__ __launch_bounds__(64 * unit_waves(S)) void r_bwd(BwdBufs<T> p, BwdDims dm)
 {
-    __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, D, FIRST, LAST>::LDS_FLOATS];
-    RBwd<T, S, D, FIRST, LAST>::run(p, dm, lds);
+    __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, D, FIRST, LAST, LENS>::LDS_FLOATS];
+    RBwd<T, S, D, FIRST, LAST, LENS>::run(p, dm, lds);
 }
 
 }  // namespace bwd

@@ -9,27 +9,29 @@
 namespace ma_host {
 
 // ---- gradient ----
-template <typename T, int S, int D, bool LAST>
+template <typename T, int S, int D, bool LAST, bool LENS>
 int launch_l_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
     const dim3 grid((unsigned)(BH * dm.b)), block(ma::bwd::Geo<S, D>::NTH);
     return L.run(kBwdL, [&] {
-        return launched([&] { hipLaunchKernelGGL((ma::bwd::l_bwd<T, S, D, LAST>), grid, block, 0, L.stream, p, dm); });
+        return launched(
+            [&] { hipLaunchKernelGGL((ma::bwd::l_bwd<T, S, D, LAST, LENS>), grid, block, 0, L.stream, p, dm); });
     });
 }
 
-template <typename T, int S, int D, bool FIRST, bool LAST>
+template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS>
 int launch_r_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
     const dim3 grid((unsigned)(BH * dm.m)), block(ma::bwd::Geo<S, D>::NTH);
     return L.run(kBwdR, [&] {
         return launched(
-            [&] { hipLaunchKernelGGL((ma::bwd::r_bwd<T, S, D, FIRST, LAST>), grid, block, 0, L.stream, p, dm); });
+            [&] { hipLaunchKernelGGL((ma::bwd::r_bwd<T, S, D, FIRST, LAST, LENS>), grid, block, 0, L.stream, p, dm); });
     });
 }
 
 // The reverse sweep, t = T .. 1: the L update of step t, then its R update.
-template <typename T, int S, int D> int bwd_sweep(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+// LENS: per-sequence lengths (instantiations of their own).
+template <typename T, int S, int D, bool LENS> int bwd_sweep_impl(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {
     ma::BwdDims dm{c.m, c.b, c.n, c.d, (float)(1.0 / std::sqrt((double)c.d))};
     dm.lens = B.lens;
@@ -44,17 +46,23 @@ template <typename T, int S, int D> int bwd_sweep(Launcher &L, const BwdCallBufs
         p.cL = B.cL + (size_t)(t - 1) * B.cst;
         p.aR = first ? nullptr : (const T *)(B.aR + (size_t)(t - 2) * B.st);
         p.cR = first ? nullptr : B.cR + (size_t)(t - 2) * B.cst;
-        rc = last ? launch_l_bwd<T, S, D, true>(L, p, dm, c.BH) : launch_l_bwd<T, S, D, false>(L, p, dm, c.BH);
+        rc = last ? launch_l_bwd<T, S, D, true, LENS>(L, p, dm, c.BH) : launch_l_bwd<T, S, D, false, LENS>(L, p, dm, c.BH);
         if (rc != MA_OK) return rc;
         if (first) {
-            rc = last ? launch_r_bwd<T, S, D, true, true>(L, p, dm, c.BH) : launch_r_bwd<T, S, D, true, false>(L, p, dm, c.BH);
+            rc = last ? launch_r_bwd<T, S, D, true, true, LENS>(L, p, dm, c.BH)
+                      : launch_r_bwd<T, S, D, true, false, LENS>(L, p, dm, c.BH);
         } else {
-            rc = last ? launch_r_bwd<T, S, D, false, true>(L, p, dm, c.BH)
-                      : launch_r_bwd<T, S, D, false, false>(L, p, dm, c.BH);
+            rc = last ? launch_r_bwd<T, S, D, false, true, LENS>(L, p, dm, c.BH)
+                      : launch_r_bwd<T, S, D, false, false, LENS>(L, p, dm, c.BH);
         }
         if (rc != MA_OK) return rc;
     }
     return MA_OK;
+}
+
+template <typename T, int S, int D> int bwd_sweep(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+{
+    return B.lens ? bwd_sweep_impl<T, S, D, true>(L, B, c) : bwd_sweep_impl<T, S, D, false>(L, B, c);
 }
 
 // The forward half-steps again, each step's states to buffers of their own,
