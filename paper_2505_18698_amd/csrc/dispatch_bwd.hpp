@@ -29,9 +29,55 @@ int launch_r_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, in
     });
 }
 
+// One launch of the L-update gradient of a step, on tiles of S >= m rows (and
+// of the R-update gradient, S >= b): each kernel takes the tile of its own
+// dimension.  128-row tiles exist for state widths D <= 96 only.
+template <typename T, int D, bool LENS>
+int l_bwd_step(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH, bool last)
+{
+    switch (tile_rows(dm.m)) {
+    case 16: return last ? launch_l_bwd<T, 16, D, true, LENS>(L, p, dm, BH) : launch_l_bwd<T, 16, D, false, LENS>(L, p, dm, BH);
+    case 32: return last ? launch_l_bwd<T, 32, D, true, LENS>(L, p, dm, BH) : launch_l_bwd<T, 32, D, false, LENS>(L, p, dm, BH);
+    case 64: return last ? launch_l_bwd<T, 64, D, true, LENS>(L, p, dm, BH) : launch_l_bwd<T, 64, D, false, LENS>(L, p, dm, BH);
+    default:
+        if constexpr (D == 128) {
+            return fail(MA_EUNSUPPORTED, "the gradient does not take 128-row blocks with d > 96");
+        } else {
+            return last ? launch_l_bwd<T, 128, D, true, LENS>(L, p, dm, BH)
+                        : launch_l_bwd<T, 128, D, false, LENS>(L, p, dm, BH);
+        }
+    }
+}
+
+template <typename T, int S, int D, bool LENS>
+int r_bwd_tile(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH, bool first, bool last)
+{
+    if (first)
+        return last ? launch_r_bwd<T, S, D, true, true, LENS>(L, p, dm, BH)
+                    : launch_r_bwd<T, S, D, true, false, LENS>(L, p, dm, BH);
+    return last ? launch_r_bwd<T, S, D, false, true, LENS>(L, p, dm, BH)
+                : launch_r_bwd<T, S, D, false, false, LENS>(L, p, dm, BH);
+}
+
+template <typename T, int D, bool LENS>
+int r_bwd_step(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH, bool first, bool last)
+{
+    switch (tile_rows(dm.b)) {
+    case 16: return r_bwd_tile<T, 16, D, LENS>(L, p, dm, BH, first, last);
+    case 32: return r_bwd_tile<T, 32, D, LENS>(L, p, dm, BH, first, last);
+    case 64: return r_bwd_tile<T, 64, D, LENS>(L, p, dm, BH, first, last);
+    default:
+        if constexpr (D == 128) {
+            return fail(MA_EUNSUPPORTED, "the gradient does not take 128-row blocks with d > 96");
+        } else {
+            return r_bwd_tile<T, 128, D, LENS>(L, p, dm, BH, first, last);
+        }
+    }
+}
+
 // The reverse sweep, t = T .. 1: the L update of step t, then its R update.
 // LENS: per-sequence lengths (instantiations of their own).
-template <typename T, int S, int D, bool LENS> int bwd_sweep_impl(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+template <typename T, int D, bool LENS> int bwd_sweep_impl(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {
     ma::BwdDims dm{c.m, c.b, c.n, c.d, (float)(1.0 / std::sqrt((double)c.d))};
     dm.lens = B.lens;
@@ -46,23 +92,15 @@ template <typename T, int S, int D, bool LENS> int bwd_sweep_impl(Launcher &L, c
         p.cL = B.cL + (size_t)(t - 1) * B.cst;
         p.aR = first ? nullptr : (const T *)(B.aR + (size_t)(t - 2) * B.st);
         p.cR = first ? nullptr : B.cR + (size_t)(t - 2) * B.cst;
-        rc = last ? launch_l_bwd<T, S, D, true, LENS>(L, p, dm, c.BH) : launch_l_bwd<T, S, D, false, LENS>(L, p, dm, c.BH);
-        if (rc != MA_OK) return rc;
-        if (first) {
-            rc = last ? launch_r_bwd<T, S, D, true, true, LENS>(L, p, dm, c.BH)
-                      : launch_r_bwd<T, S, D, true, false, LENS>(L, p, dm, c.BH);
-        } else {
-            rc = last ? launch_r_bwd<T, S, D, false, true, LENS>(L, p, dm, c.BH)
-                      : launch_r_bwd<T, S, D, false, false, LENS>(L, p, dm, c.BH);
-        }
-        if (rc != MA_OK) return rc;
+        if ((rc = l_bwd_step<T, D, LENS>(L, p, dm, c.BH, last)) != MA_OK) return rc;
+        if ((rc = r_bwd_step<T, D, LENS>(L, p, dm, c.BH, first, last)) != MA_OK) return rc;
     }
     return MA_OK;
 }
 
-template <typename T, int S, int D> int bwd_sweep(Launcher &L, const BwdCallBufs &B, const CallDims &c)
+template <typename T, int D> int bwd_sweep(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {
-    return B.lens ? bwd_sweep_impl<T, S, D, true>(L, B, c) : bwd_sweep_impl<T, S, D, false>(L, B, c);
+    return B.lens ? bwd_sweep_impl<T, D, true>(L, B, c) : bwd_sweep_impl<T, D, false>(L, B, c);
 }
 
 // The forward half-steps again, each step's states to buffers of their own,
@@ -88,17 +126,7 @@ template <typename T, int D> int run_bwd_d(Launcher &L, const BwdCallBufs &B, co
                          B.cR + (size_t)(t - 1) * B.cst, B.cL + (size_t)(t - 1) * B.cst, nullptr, nullptr};
         if ((rc = l_step<T, D>(L, l, hd, c.BH, c.num_cus, false)) != MA_OK) return rc;
     }
-    switch (tile_rows(c.m > c.b ? c.m : c.b)) {
-    case 16: return bwd_sweep<T, 16, D>(L, B, c);
-    case 32: return bwd_sweep<T, 32, D>(L, B, c);
-    case 64: return bwd_sweep<T, 64, D>(L, B, c);
-    default:
-        if constexpr (D == 128) {
-            return fail(MA_EUNSUPPORTED, "the gradient does not take 128-row blocks with d > 96");
-        } else {
-            return bwd_sweep<T, 128, D>(L, B, c);
-        }
-    }
+    return bwd_sweep<T, D>(L, B, c);
 }
 
 template <typename T> int run_bwd_impl(Launcher &L, const BwdCallBufs &B, const CallDims &c)
