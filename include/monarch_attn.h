@@ -180,7 +180,7 @@ int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *ou
  *                 16-byte aligned, overlapping neither each other nor the
  *                 inputs.  Fully overwritten.  All owned by the caller.
  * B, H, N, d, m, b, T, dtype, stream : as monarch_attn_fwd, and in addition
- *                 T <= 32, and m, b <= 64 when d > 96 (else MA_EUNSUPPORTED).
+ *                 T <= 32 (else MA_EUNSUPPORTED).
  *
  * Runs the forward half-steps again, keeping the states of every step, then
  * one launch per half-step in reverse order; all of it on `stream`,

@@ -83,12 +83,21 @@ constexpr int row_stride(int cols) { return cols <= 64 ? 68 : cols <= 96 ? 100 :
 
 constexpr int unit_waves(int S) { return S >= 64 ? 16 : S / 4; }
 
+// Tiles of 128 rows at D = 128 (16-bit elements only: the forward takes fp32
+// at D = 128 for blocks of up to 64 rows) hold their whole-unit tiles that
+// are exact in the element type (alpha_L in l_bwd, K and V in r_bwd) as
+// 16-bit LDS tiles of row stride LD16, converted on every read: two fp32
+// 128 x 128 tiles alone would fill the LDS.
 template <int S, int D> struct Geo {
+    static constexpr bool HALF = S == 128 && D == 128;
+    static constexpr int LD16 = D + 8;  // row stride (elements) of a 16-bit tile: 16-byte rows
     static constexpr int W = unit_waves(S);
     static constexpr int NTH = 64 * W;
     static constexpr int LD = row_stride(D);
     static constexpr int LS = row_stride(S);
-    static constexpr int lds_floats(int c) { return 2 * S * LD + 3 * c * LD + 2 * c * LS + 2 * S; }
+    // floats of the whole-unit tiles (the larger need, l_bwd's, when HALF)
+    static constexpr int UNIT = HALF ? S * LD16 / 2 + S * LD : 2 * S * LD;
+    static constexpr int lds_floats(int c) { return UNIT + 3 * c * LD + 2 * c * LS + 2 * S; }
     static constexpr int C = lds_floats(S) <= 40960 ? S : lds_floats(32) <= 40960 ? 32 : 16;
     static constexpr int NCH = S / C;
     // row passes: a row of S scores spans SPAN lanes (CPL columns each), a wave
@@ -137,32 +146,49 @@ template <int G> __device__ inline float group_max(float x)
 // scalar reads otherwise.  The contraction length is a compile-time constant:
 // the loop unrolls, every read is the lane's base address plus an immediate
 // offset, and all reads can be issued ahead of the MFMAs.
-template <bool TA, bool TB, int LA, int LB> struct Pair {
-    const float *A, *B;
+// Four consecutive elements of an LDS tile as floats: one 16-byte read of
+// fp32, or one 8-byte read of 16-bit elements converted exactly.
+template <typename E> __device__ inline void read4(const E *p, float *v)
+{
+    if constexpr (std::is_same<E, float>::value) {
+        const f32x4 x = *reinterpret_cast<const f32x4 *>(p);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) v[s] = x[s];
+    } else {
+        E e[4];
+        *reinterpret_cast<u32x2 *>(e) = *reinterpret_cast<const u32x2 *>(p);
+#pragma unroll
+        for (int s = 0; s < 4; ++s) v[s] = static_cast<float>(e[s]);
+    }
+}
+
+// Operands of a product, as LDS tiles (element types EA, EB: fp32, or the
+// 16-bit element type for the whole-unit tiles of 128 x 128 units) with row
+// strides LA, LB:
+//   A(r, k) = TA ? A[k][r] : A[r][k],   B(k, n) = TB ? B[n][k] : B[k][n].
+template <bool TA, bool TB, int LA, int LB, typename EA = float, typename EB = float> struct Pair {
+    const EA *A;
+    const EB *B;
 
     // acc += sum_{k < K} A(r, k) B(k, n)
     template <int K> __device__ void accumulate(f32x4 &acc, int r, int n, int g) const
     {
-        const float *pa = TA ? A + 4 * g * LA + r : A + r * LA + 4 * g;
-        const float *pb = TB ? B + n * LB + 4 * g : B + 4 * g * LB + n;
+        const EA *pa = TA ? A + 4 * g * LA + r : A + r * LA + 4 * g;
+        const EB *pb = TB ? B + n * LB + 4 * g : B + 4 * g * LB + n;
 #pragma unroll
         for (int k0 = 0; k0 < K; k0 += 16) {
             float a[4], b[4];
             if constexpr (TA) {
 #pragma unroll
-                for (int s = 0; s < 4; ++s) a[s] = pa[(k0 + s) * LA];
+                for (int s = 0; s < 4; ++s) a[s] = static_cast<float>(pa[(k0 + s) * LA]);
             } else {
-                const f32x4 v = *reinterpret_cast<const f32x4 *>(pa + k0);
-#pragma unroll
-                for (int s = 0; s < 4; ++s) a[s] = v[s];
+                read4(pa + k0, a);
             }
             if constexpr (TB) {
-                const f32x4 v = *reinterpret_cast<const f32x4 *>(pb + k0);
-#pragma unroll
-                for (int s = 0; s < 4; ++s) b[s] = v[s];
+                read4(pb + k0, b);
             } else {
 #pragma unroll
-                for (int s = 0; s < 4; ++s) b[s] = pb[(k0 + s) * LB];
+                for (int s = 0; s < 4; ++s) b[s] = static_cast<float>(pb[(k0 + s) * LB]);
             }
 #pragma unroll
             for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
@@ -170,10 +196,10 @@ template <bool TA, bool TB, int LA, int LB> struct Pair {
     }
 };
 
-template <bool TA, bool TB, int LA, int LB>
-__device__ inline Pair<TA, TB, LA, LB> pair(const float *A, const float *B)
+template <bool TA, bool TB, int LA, int LB, typename EA, typename EB>
+__device__ inline Pair<TA, TB, LA, LB, EA, EB> pair(const EA *A, const EB *B)
 {
-    return Pair<TA, TB, LA, LB>{A, B};
+    return Pair<TA, TB, LA, LB, EA, EB>{A, B};
 }
 
 // out(r, c) = sum over the pairs of A(r, :) B(:, c) for r < M, c < N, with
@@ -269,6 +295,31 @@ __device__ inline void load_tile(float *dst, int nr, int nc, Src src, int tid)
     }
 }
 
+// load_tile into a tile of the element type itself (no conversion): rows of
+// C elements at row stride LDT, zero past nr rows and nc columns.
+template <typename E, int NTH, int R, int C, int LDT, typename Src>
+__device__ inline void load_tile_raw(E *dst, int nr, int nc, Src src, int tid)
+{
+    constexpr int V = 16 / (int)sizeof(E), CPR = C / V;
+    static_assert(LDT % V == 0, "16-byte rows");
+    for (int idx = tid; idx < R * CPR; idx += NTH) {
+        const int r = idx / CPR, c = (idx % CPR) * V;
+        uint4 x = {0u, 0u, 0u, 0u};
+        if (r < nr && c < nc) x = *reinterpret_cast<const uint4 *>(src(r) + c);
+        *reinterpret_cast<uint4 *>(dst + r * LDT + c) = x;
+    }
+}
+
+// A whole-unit tile in the element type when HALF, else in fp32.
+template <typename T, int NTH, int R, int C, int LDT, bool HALF, typename U, typename Src>
+__device__ inline void load_unit(U *dst, int nr, int nc, Src src, int tid)
+{
+    if constexpr (HALF)
+        load_tile_raw<T, NTH, R, C, LDT>(dst, nr, nc, src, tid);
+    else
+        load_tile<T, NTH, R, C, LDT>(dst, nr, nc, src, tid);
+}
+
 // ---------------------------------------------------------------------------------------
 // The L update of class j of step t undone (LAST: t = T, the update that also
 // produced O).  S >= m; query rows l in chunks of C.
@@ -277,7 +328,12 @@ template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
     using G_ = Geo<S, D>;
     static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
     static constexpr int SPAN = G_::SPAN, RPW = G_::RPW;
-    static constexpr int LDS_FLOATS = 2 * S * LD + 2 * C * LD + 2 * C * LS + 2 * S;
+    static constexpr bool HALF = G_::HALF;
+    static_assert(!HALF || sizeof(T) == 2, "16-bit unit tiles need 16-bit elements");
+    using UT = typename std::conditional<HALF, T, float>::type;  // alpha_L tile
+    static constexpr int LDU = HALF ? G_::LD16 : LD;
+    static constexpr int UF = S * LDU * (int)sizeof(UT) / 4;  // its floats
+    static constexpr int LDS_FLOATS = UF + S * LD + 2 * C * LD + 2 * C * LS + 2 * S;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
     {
@@ -290,12 +346,14 @@ template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
         const int mk = LENS ? min(m, (nl + b - 1) / b) : m;  // key blocks k < mk hold a real key
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
         // whole-unit tiles (rows k): alpha_L[j][k]; Y[j][k] (LAST) or d alpha_R'[k][j]
-        float *aL = lds, *X = aL + S * LD;
+        UT *aL = reinterpret_cast<UT *>(lds);
+        float *X = lds + UF;
         // chunk tiles (rows l of the chunk): Qbar, dO (LAST) or L d alpha_R', L, dL then dW
         float *Qb = X + S * LD, *G = Qb + C * LD, *Lm = G + C * LD, *dL = Lm + C * LS;
         float *cL = dL + C * LS, *dcR = cL + S;
 
-        load_tile<T, NTH, S, D, LD>(aL, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * D; }, tid);
+        load_unit<T, NTH, S, D, LDU, HALF>(aL, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * D; },
+                                           tid);
         if constexpr (LAST) {
             load_tile<T, NTH, S, D, LD>(X, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * D; }, tid);
         } else {
@@ -322,7 +380,7 @@ template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
             __syncthreads();
 
             // unnormalised scores <Qbar[l], alpha_L[k]>
-            gemm<W, C, S, D>(wave, lane, to_lds<LS>(Lm), pair<false, true, LD, LD>(Qb, aL));
+            gemm<W, C, S, D>(wave, lane, to_lds<LS>(Lm), pair<false, true, LD, LDU>(Qb, aL));
             __syncthreads();
             // L[l][k] = softmax_k (s score - c_L[k]): RPW rows l per wave instruction,
             // SPAN lanes and CPL columns k per lane for each
@@ -394,7 +452,7 @@ template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
                         }
                     }
                 },
-                pair<false, false, LS, LD>(dL, aL));
+                pair<false, false, LS, LDU>(dL, aL));
             // d alpha_L[k] += dW^T Qbar;  d c_L[k] += sum_l dW[l][k]
             daL.template add<C>(wave, lane, pair<true, false, LS, LD>(dL, Qb));
             if (tid < S) {
@@ -425,7 +483,12 @@ template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> st
     using G_ = Geo<S, D>;
     static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
     static constexpr int SPAN = G_::SPAN, RPW = G_::RPW;
-    static constexpr int LDS_FLOATS = (LAST ? 2 : 1) * S * LD + (LAST ? 3 : 2) * C * LD + 2 * C * LS + 2 * C;
+    static constexpr bool HALF = G_::HALF;
+    static_assert(!HALF || sizeof(T) == 2, "16-bit unit tiles need 16-bit elements");
+    using UT = typename std::conditional<HALF, T, float>::type;  // K and V tiles
+    static constexpr int LDU = HALF ? G_::LD16 : LD;
+    static constexpr int UF = S * LDU * (int)sizeof(UT) / 4;  // floats of one
+    static constexpr int LDS_FLOATS = (LAST ? 2 : 1) * UF + (LAST ? 3 : 2) * C * LD + 2 * C * LS + 2 * C;
 
     __device__ static void run(const BwdBufs<T> &p, const BwdDims &dm, float *lds)
     {
@@ -438,14 +501,15 @@ template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> st
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
         const int64_t row0 = (int64_t)k * b;  // first row of block k
         // whole-unit tiles (rows i): Kbar, Vbar (LAST)
-        float *Kb = lds, *Vb = Kb + S * LD;
+        UT *Kb = reinterpret_cast<UT *>(lds), *Vb = Kb + S * LDU;
         // chunk tiles (rows j of the chunk): alpha_R, d alpha_L, dY (LAST), R, dR then dZ s / c_R
-        float *aR = Kb + (LAST ? 2 : 1) * S * LD, *dA = aR + C * LD, *dYt = dA + C * LD;
+        float *aR = lds + (LAST ? 2 : 1) * UF, *dA = aR + C * LD, *dYt = dA + C * LD;
         float *Rm = dA + (LAST ? 2 : 1) * C * LD, *dR = Rm + C * LS;
         float *cR = dR + C * LS, *dcL = cR + C;
 
-        load_tile<T, NTH, S, D, LD>(Kb, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
-        if constexpr (LAST) load_tile<T, NTH, S, D, LD>(Vb, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
+        load_unit<T, NTH, S, D, LDU, HALF>(Kb, kv, d, [&](int i) { return p.k + toff + (row0 + i) * d; }, tid);
+        if constexpr (LAST)
+            load_unit<T, NTH, S, D, LDU, HALF>(Vb, kv, d, [&](int i) { return p.v + toff + (row0 + i) * d; }, tid);
         Acc<W, S, D> dK, dV;  // sums over all rows j
         dK.zero();
         if constexpr (LAST) dV.zero();
@@ -472,11 +536,12 @@ template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> st
             __syncthreads();
 
             // unnormalised scores <alpha_R[j], Kbar[i]>;  dR = d alpha_L Kbar^T (+ dY Vbar^T)
-            gemm<W, C, S, D>(wave, lane, to_lds<LS>(Rm), pair<false, true, LD, LD>(aR, Kb));
+            gemm<W, C, S, D>(wave, lane, to_lds<LS>(Rm), pair<false, true, LD, LDU>(aR, Kb));
             if constexpr (LAST) {
-                gemm<W, C, S, D>(wave, lane, to_lds<LS>(dR), pair<false, true, LD, LD>(dA, Kb), pair<false, true, LD, LD>(dYt, Vb));
+                gemm<W, C, S, D>(wave, lane, to_lds<LS>(dR), pair<false, true, LD, LDU>(dA, Kb),
+                                 pair<false, true, LD, LDU>(dYt, Vb));
             } else {
-                gemm<W, C, S, D>(wave, lane, to_lds<LS>(dR), pair<false, true, LD, LD>(dA, Kb));
+                gemm<W, C, S, D>(wave, lane, to_lds<LS>(dR), pair<false, true, LD, LDU>(dA, Kb));
             }
             __syncthreads();
             // per row j (RPW rows per wave instruction, SPAN lanes and CPL keys i per
@@ -542,7 +607,7 @@ template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> st
                             dq[(int64_t)jj * d + e] =
                                 static_cast<T>((!LENS || jj < jq) ? dQ[(int64_t)jj * d + e] + v : 0.f);
                     },
-                    pair<false, false, LS, LD>(dR, Kb));
+                    pair<false, false, LS, LDU>(dR, Kb));
             } else {
                 float *daR = p.daR + soff + (row0 + j0) * D;
                 gemm<W, C, D, S>(
@@ -550,7 +615,7 @@ template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> st
                     [&](int jj, int e, float v) {
                         if (jj < jb && e < d) daR[(int64_t)jj * D + e] = v;
                     },
-                    pair<false, false, LS, LD>(dR, Kb));
+                    pair<false, false, LS, LDU>(dR, Kb));
             }
             // dKbar[i] += sum_j R[j][i] d alpha_L[j] + dZs[j][i] alpha_R[j];  dVbar[i] += sum_j R[j][i] dY[j]
             dK.template add<C>(wave, lane, pair<true, false, LS, LD>(Rm, dA), pair<true, false, LS, LD>(dR, aR));

@@ -31,7 +31,8 @@ int launch_r_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, in
 
 // One launch of the L-update gradient of a step, on tiles of S >= m rows (and
 // of the R-update gradient, S >= b): each kernel takes the tile of its own
-// dimension.  128-row tiles exist for state widths D <= 96 only.
+// dimension.  128-row tiles at D = 128 hold 16-bit unit tiles (16-bit
+// elements only, the only ones the forward takes at that size).
 template <typename T, int D, bool LENS>
 int l_bwd_step(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH, bool last)
 {
@@ -40,8 +41,8 @@ int l_bwd_step(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int6
     case 32: return last ? launch_l_bwd<T, 32, D, true, LENS>(L, p, dm, BH) : launch_l_bwd<T, 32, D, false, LENS>(L, p, dm, BH);
     case 64: return last ? launch_l_bwd<T, 64, D, true, LENS>(L, p, dm, BH) : launch_l_bwd<T, 64, D, false, LENS>(L, p, dm, BH);
     default:
-        if constexpr (D == 128) {
-            return fail(MA_EUNSUPPORTED, "the gradient does not take 128-row blocks with d > 96");
+        if constexpr (D == 128 && std::is_same<T, float>::value) {  // the forward takes no such fp32 shape
+            return fail(MA_EUNSUPPORTED, "fp32 128-row blocks need d <= 96");
         } else {
             return last ? launch_l_bwd<T, 128, D, true, LENS>(L, p, dm, BH)
                         : launch_l_bwd<T, 128, D, false, LENS>(L, p, dm, BH);
@@ -67,8 +68,8 @@ int r_bwd_step(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int6
     case 32: return r_bwd_tile<T, 32, D, LENS>(L, p, dm, BH, first, last);
     case 64: return r_bwd_tile<T, 64, D, LENS>(L, p, dm, BH, first, last);
     default:
-        if constexpr (D == 128) {
-            return fail(MA_EUNSUPPORTED, "the gradient does not take 128-row blocks with d > 96");
+        if constexpr (D == 128 && std::is_same<T, float>::value) {  // the forward takes no such fp32 shape
+            return fail(MA_EUNSUPPORTED, "fp32 128-row blocks need d <= 96");
         } else {
             return r_bwd_tile<T, 128, D, LENS>(L, p, dm, BH, first, last);
         }
@@ -105,7 +106,7 @@ template <typename T, int D> int bwd_sweep(Launcher &L, const BwdCallBufs &B, co
 
 // The forward half-steps again, each step's states to buffers of their own,
 // then the reverse sweep.  States of width D = tile_d(d); every (m, b, d) the
-// forward takes except 128-row tiles with D = 128 (checked by the caller).
+// forward takes.
 template <typename T, int D> int run_bwd_d(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {
     ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};

@@ -231,16 +231,13 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
 
 // ---- gradient ----
 
-// The gradient kernels hold one unit's matrices in fp32 LDS tiles: blocks of
-// up to 128 rows (as the forward) at state widths D = 64 or 96, of up to 64
-// rows at D = 128.
+// The gradient takes every shape the forward takes (its 128-row units at
+// D = 128 hold the tiles that are exact in the 16-bit element type as such),
+// for T <= 32.
 int check_bwd_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype)
 {
     const int rc = check_shape(N, d, m, b, T, dtype);
     if (rc != MA_OK) return rc;
-    if ((m > 64 || b > 64) && tile_d(d) == 128)
-        return fail(MA_EUNSUPPORTED, "the gradient needs m, b <= 64 when d > 96 (got m=%lld, b=%lld, d=%lld)",
-                    (long long)m, (long long)b, (long long)d);
     if (T > 32) return fail(MA_EUNSUPPORTED, "the gradient supports T <= 32 (got %d)", T);
     return MA_OK;
 }

@@ -201,7 +201,7 @@ def test_bwd_varlen_rejects_null_or_misaligned_lens():
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 257, 64, 16, 16, 1, 1), 1),    # N > m b
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 16512, 64, 129, 128, 1, 1), 2),  # m > 128
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 16512, 64, 128, 129, 1, 1), 2),  # b > 128
-        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 8192, 128, 128, 64, 1, 1), 2),  # m > 64 with d > 96
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 8192, 128, 128, 64, 1, 0), 2),  # fp32 m > 64, d > 96
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 33, 1), 2),   # T > 32
     ],
 )
@@ -228,8 +228,10 @@ def test_bwd_invalid_arguments_rejected_before_any_hip_call(args, code):
         ((384, 64, 3, 128, 1, 1), True),
         ((7600, 48, 60, 128, 2, 1), True),
         ((16384, 64, 128, 128, 2, 0), True),
-        ((16384, 128, 128, 128, 2, 1), False),   # 128-row tiles with d > 96
-        ((8192, 128, 64, 128, 2, 1), False),
+        ((16384, 128, 128, 128, 2, 1), True),    # 128-row tiles at d = 128 (16-bit unit tiles)
+        ((8192, 128, 64, 128, 2, 1), True),
+        ((8192, 128, 128, 64, 2, 2), True),
+        ((8192, 128, 128, 64, 2, 0), False),     # fp32: the forward takes no 128-row block at d = 128
         ((256, 72, 16, 16, 3, 1), True),          # DiT
         ((256, 96, 16, 16, 2, 1), True),
         ((4096, 128, 64, 64, 2, 1), True),
@@ -256,7 +258,8 @@ def test_bwd_workspace_bytes_formula():
     # fp32 states are twice as wide; unsupported shapes give 0
     st32 = _align(BH * Np * 64 * 4)
     assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_F32) == want + 2 * T * (st32 - st)
-    assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 16384, 128, 128, 128, 2, ma.MA_BF16) == 0
+    assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 16384, 128, 128, 128, 2, ma.MA_F32) == 0
+    assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 256, 64, 16, 16, 33, ma.MA_BF16) == 0
     # d = 72: states and state gradients 96 wide
     B, H, N, d, m, b, T = 1, 2, 256, 72, 16, 16, 3
     Np, BH = m * b, B * H

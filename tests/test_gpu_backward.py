@@ -155,6 +155,26 @@ def test_wide_heads(ma, dtype, H, n, m, b, d, T):
     run_case(ma, 1, H, n, m, b, d, T, dtype, seed=n + d)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize(
+    "H,n,m,b,d,T",
+    [
+        (2, 1280, 80, 16, 128, 2),    # l_bwd on 128-row tiles at d = 128: 16-bit alpha_L tile
+        (2, 1280, 16, 80, 128, 2),    # r_bwd on 128-row tiles at d = 128: 16-bit K and V tiles
+        (1, 10000, 100, 100, 128, 1),  # both, padded tiles
+        (1, 1400, 70, 20, 104, 3),    # d = 104 on 128-wide tiles
+        (1, 2000, 20, 100, 120, 2),
+    ],
+)
+def test_128_row_blocks_at_d128(ma, dtype, H, n, m, b, d, T):
+    run_case(ma, 1, H, n, m, b, d, T, dtype, seed=n + m + d)
+
+
+def test_long_sequence_d128_gradient(ma):
+    """The N = 16384 = 128 x 128, d = 128 sweep shape (bf16, T = 2), oracle on one head."""
+    run_case(ma, 1, 2, 16384, 128, 128, 128, 2, "bf16", seed=5, heads=[(0, 1)])
+
+
 def test_dit_workload_sampled_heads(ma):
     """DiT-XL/2 at 256 x 256 (32 images x 16 heads, N = 256, d = 72, T = 3), oracle on 3 heads."""
     w = si.WORKLOADS["dit_xl_n256"]

@@ -297,3 +297,12 @@ def test_autograd_with_lengths(ma):
         np.testing.assert_array_equal(t.grad.double().cpu().numpy(), w)
     fwd = run_varlen(ma, q, k, v, lens, m, b, T, "bf16")
     np.testing.assert_array_equal(o.detach().double().cpu().numpy(), fwd)
+
+
+def test_varlen_gradient_128_row_blocks_at_d128(ma):
+    """Per-sequence lengths with 16-bit whole-unit tiles (m = 72 and b = 80 at d = 128)."""
+    for m, b, lens in ((72, 16, [1152, 500, 17]), (16, 80, [1280, 81, 700])):
+        q, k, v = si.random_qkv(len(lens), 1, m * b, 128, "bf16", seed=m + b, scale=1.5)
+        g = si.random_cotangent((len(lens), 1, m * b, 128), "bf16", seed=m + b)
+        got = run_bwd_varlen(ma, q, k, v, g, lens, m, b, 2, "bf16")
+        check_bwd_varlen(got, q, k, v, g, lens, m, b, 2, "bf16", f"bwd varlen m={m} b={b} d=128")
