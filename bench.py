@@ -668,7 +668,7 @@ def main():
     ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
     ap.add_argument("--also", default="speed_n4096,speed_n4096_t3,vit_b16_n196,vit_b16_n197",
                     help="comma-separated extra workloads ('' for none)")
-    ap.add_argument("--backward", default="speed_n16384,speed_n4096,vit_b16_n197",
+    ap.add_argument("--backward", default="speed_n16384,speed_n4096,vit_b16_n197,sweep_n16384_d128",
                     help="comma-separated workloads for the gradient timing ('' for none)")
     ap.add_argument("--sweep", default=",".join(f"sweep_n{n}_d{d}" for n in (256, 1024, 4096, 16384)
                                                    for d in (64, 128)),
