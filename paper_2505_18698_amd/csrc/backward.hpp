@@ -83,13 +83,22 @@ constexpr int row_stride(int cols) { return cols <= 64 ? 68 : cols <= 96 ? 100 :
 
 constexpr int unit_waves(int S) { return S >= 64 ? 16 : S / 4; }
 
-// Tiles of 128 rows at D = 128 (16-bit elements only: the forward takes fp32
-// at D = 128 for blocks of up to 64 rows) hold their whole-unit tiles that
-// are exact in the element type (alpha_L in l_bwd, K and V in r_bwd) as
-// 16-bit LDS tiles of row stride LD16, converted on every read: two fp32
-// 128 x 128 tiles alone would fill the LDS.
-template <int S, int D> struct Geo {
-    static constexpr bool HALF = S == 128 && D == 128;
+// Whether two workgroups of a unit kernel share a CU: 64-row units at D = 64
+// with 16-bit elements, whose LDS (16-bit unit tiles) leaves room for two.
+// Their kernels carry a waves-per-SIMD bound that keeps the registers of two.
+constexpr bool two_per_cu(int S, int D, int elem_bytes) { return S == 64 && D == 64 && elem_bytes == 2; }
+
+// With 16-bit elements (H16) the whole-unit tiles that are exact in the
+// element type (alpha_L in l_bwd, K and V in r_bwd) can be held as 16-bit
+// LDS tiles of row stride LD16, converted on every read (HALF):
+// - at 128 rows and D = 128, where two fp32 128 x 128 tiles alone would fill
+//   the LDS (the forward takes fp32 at D = 128 for blocks of up to 64 rows);
+// - at 64 rows and D = 64, where with rows in chunks of 32 it brings a unit under half
+//   the LDS, so that two workgroups share a CU and one's loads overlap the
+//   other's compute.
+template <int S, int D, bool H16 = false> struct Geo {
+    static constexpr bool HALF = H16 && (S == 128 ? D == 128 : S == 64 && D == 64);
+    static constexpr int BUDGET = (HALF && S == 64) ? 20480 : 40960;  // floats of LDS per workgroup
     static constexpr int LD16 = D + 8;  // row stride (elements) of a 16-bit tile: 16-byte rows
     static constexpr int W = unit_waves(S);
     static constexpr int NTH = 64 * W;
@@ -98,7 +107,7 @@ template <int S, int D> struct Geo {
     // floats of the whole-unit tiles (the larger need, l_bwd's, when HALF)
     static constexpr int UNIT = HALF ? S * LD16 / 2 + S * LD : 2 * S * LD;
     static constexpr int lds_floats(int c) { return UNIT + 3 * c * LD + 2 * c * LS + 2 * S; }
-    static constexpr int C = lds_floats(S) <= 40960 ? S : lds_floats(32) <= 40960 ? 32 : 16;
+    static constexpr int C = lds_floats(S) <= BUDGET ? S : lds_floats(32) <= BUDGET ? 32 : 16;
     static constexpr int NCH = S / C;
     // row passes: a row of S scores spans SPAN lanes (CPL columns each), a wave
     // instruction covers RPW rows
@@ -325,7 +334,7 @@ __device__ inline void load_unit(U *dst, int nr, int nc, Src src, int tid)
 // produced O).  S >= m; query rows l in chunks of C.
 // ---------------------------------------------------------------------------------------
 template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
-    using G_ = Geo<S, D>;
+    using G_ = Geo<S, D, sizeof(T) == 2>;
     static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
     static constexpr int SPAN = G_::SPAN, RPW = G_::RPW;
     static constexpr bool HALF = G_::HALF;
@@ -480,7 +489,7 @@ template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
 // S >= b; rows j in chunks of C.
 // ---------------------------------------------------------------------------------------
 template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> struct RBwd {
-    using G_ = Geo<S, D>;
+    using G_ = Geo<S, D, sizeof(T) == 2>;
     static constexpr int W = G_::W, NTH = G_::NTH, C = G_::C, LS = G_::LS, CPL = G_::CPL, LD = G_::LD;
     static constexpr int SPAN = G_::SPAN, RPW = G_::RPW;
     static constexpr bool HALF = G_::HALF;
@@ -656,6 +665,23 @@ __global__ __launch_bounds__(64 * unit_waves(S)) void l_bwd(BwdBufs<T> p, BwdDim
 
 template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS>
 __global__ __launch_bounds__(64 * unit_waves(S)) void r_bwd(BwdBufs<T> p, BwdDims dm)
+{
+    __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, D, FIRST, LAST, LENS>::LDS_FLOATS];
+    RBwd<T, S, D, FIRST, LAST, LENS>::run(p, dm, lds);
+}
+
+// The same kernels with registers bounded for two workgroups per CU.
+template <typename T, int S, int D, bool LAST, bool LENS>
+__global__ __launch_bounds__(64 * unit_waves(S)) __attribute__((amdgpu_waves_per_eu(2 * unit_waves(S) / 4))) void l_bwd2(
+    BwdBufs<T> p, BwdDims dm)
+{
+    __shared__ __attribute__((aligned(16))) float lds[LBwd<T, S, D, LAST, LENS>::LDS_FLOATS];
+    LBwd<T, S, D, LAST, LENS>::run(p, dm, lds);
+}
+
+template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS>
+__global__ __launch_bounds__(64 * unit_waves(S)) __attribute__((amdgpu_waves_per_eu(2 * unit_waves(S) / 4))) void r_bwd2(
+    BwdBufs<T> p, BwdDims dm)
 {
     __shared__ __attribute__((aligned(16))) float lds[RBwd<T, S, D, FIRST, LAST, LENS>::LDS_FLOATS];
     RBwd<T, S, D, FIRST, LAST, LENS>::run(p, dm, lds);

@@ -12,20 +12,28 @@ namespace ma_host {
 template <typename T, int S, int D, bool LAST, bool LENS>
 int launch_l_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
-    const dim3 grid((unsigned)(BH * dm.b)), block(ma::bwd::Geo<S, D>::NTH);
+    const dim3 grid((unsigned)(BH * dm.b)), block(ma::bwd::Geo<S, D, sizeof(T) == 2>::NTH);
     return L.run(kBwdL, [&] {
-        return launched(
-            [&] { hipLaunchKernelGGL((ma::bwd::l_bwd<T, S, D, LAST, LENS>), grid, block, 0, L.stream, p, dm); });
+        return launched([&] {
+            if constexpr (ma::bwd::two_per_cu(S, D, sizeof(T)))
+                hipLaunchKernelGGL((ma::bwd::l_bwd2<T, S, D, LAST, LENS>), grid, block, 0, L.stream, p, dm);
+            else
+                hipLaunchKernelGGL((ma::bwd::l_bwd<T, S, D, LAST, LENS>), grid, block, 0, L.stream, p, dm);
+        });
     });
 }
 
 template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS>
 int launch_r_bwd(Launcher &L, const ma::BwdBufs<T> &p, const ma::BwdDims &dm, int64_t BH)
 {
-    const dim3 grid((unsigned)(BH * dm.m)), block(ma::bwd::Geo<S, D>::NTH);
+    const dim3 grid((unsigned)(BH * dm.m)), block(ma::bwd::Geo<S, D, sizeof(T) == 2>::NTH);
     return L.run(kBwdR, [&] {
-        return launched(
-            [&] { hipLaunchKernelGGL((ma::bwd::r_bwd<T, S, D, FIRST, LAST, LENS>), grid, block, 0, L.stream, p, dm); });
+        return launched([&] {
+            if constexpr (ma::bwd::two_per_cu(S, D, sizeof(T)))
+                hipLaunchKernelGGL((ma::bwd::r_bwd2<T, S, D, FIRST, LAST, LENS>), grid, block, 0, L.stream, p, dm);
+            else
+                hipLaunchKernelGGL((ma::bwd::r_bwd<T, S, D, FIRST, LAST, LENS>), grid, block, 0, L.stream, p, dm);
+        });
     });
 }
 
