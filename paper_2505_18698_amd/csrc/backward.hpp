@@ -28,11 +28,12 @@
 //       of dZ sum to zero, so log R stands in for the logits);  at t = 1
 //       d alpha_R is added to dQ (alpha_R = the rows of Q) and c_R is constant.
 //
-// Every unit keeps its matrices in fp32 LDS tiles and runs every product on
-// v_mfma_f32_16x16x4f32.  Up to 64 rows per side a unit holds all of them at
-// once; at 128 (m or b up to 128) it walks its own rows (j in r_bwd, l in
-// l_bwd) in chunks of 32, the sums over those rows (dK, dV, dY, d alpha_L,
-// d c_L) accumulating in registers.  The gradients of the states and the dQ, dK
+// Every unit keeps its matrices in LDS tiles, fp32 except the whole-unit tiles
+// that are exact in a 16-bit element type at 64 and 128 rows (see Geo), and
+// runs every product on v_mfma_f32_16x16x4f32.  A unit sizes its tiles by its
+// own dimension (m for l_bwd, b for r_bwd).  When its tiles do not fit at
+// once, it walks its own rows (j in r_bwd, l in l_bwd) in chunks, the sums
+// over those rows (dK, dV, dY, d alpha_L, d c_L) accumulating in registers.  The gradients of the states and the dQ, dK
 // accumulators are fp32 in the workspace.  Within a launch the units write
 // disjoint rows, and launches that touch the same rows are ordered on the
 // stream, so read-modify-writes need no atomics and the result is
