@@ -124,11 +124,38 @@ def _check_tensors(q, k, v, out):
 
 
 def _stream(q, stream):
+    """The hipStream_t to launch on: `stream`, or torch's current stream of
+    q's device (read through torch's raw-stream hook where it exists: a
+    fraction of the cost of torch.cuda.current_stream)."""
     import torch
 
     if stream is None:
+        raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+        if raw is not None:
+            return raw(q.device.index)
         return torch.cuda.current_stream(q.device).cuda_stream
     return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+class _OnDevice:
+    """Make q's device current for the call (a no-op when it already is)."""
+
+    __slots__ = ("dev", "guard")
+
+    def __init__(self, q):
+        import torch
+
+        self.dev = q.device.index
+        self.guard = None if self.dev == torch.cuda.current_device() else torch.cuda.device(self.dev)
+
+    def __enter__(self):
+        if self.guard is not None:
+            self.guard.__enter__()
+
+    def __exit__(self, *exc):
+        if self.guard is not None:
+            return self.guard.__exit__(*exc)
+        return False
 
 
 def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
@@ -142,7 +169,7 @@ def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
     _check_tensors(q, k, v, out)
     B, H, N, d = q.shape
     stream = _stream(q, stream)
-    with torch.cuda.device(q.device):
+    with _OnDevice(q):
         _check(monarch_attn_fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                     B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
     return out
@@ -167,7 +194,7 @@ def monarch_attn_fwd_varlen(q, k, v, out, lens, m: int, b: int, T: int, stream=N
     _check_lens(q, lens)
     B, H, N, d = q.shape
     stream = _stream(q, stream)
-    with torch.cuda.device(q.device):
+    with _OnDevice(q):
         _check(LIB.monarch_attn_fwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                            lens.data_ptr(), B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
     return out
@@ -184,7 +211,7 @@ def monarch_attn_fwd_objective(q, k, v, out, obj, m: int, b: int, T: int, stream
         raise ValueError("obj must be a contiguous float32 device tensor [B, H, T]")
     B, H, N, d = q.shape
     stream = _stream(q, stream)
-    with torch.cuda.device(q.device):
+    with _OnDevice(q):
         _check(LIB.monarch_attn_fwd_objective(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                               obj.data_ptr(), B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
     return out, obj
@@ -201,7 +228,7 @@ def monarch_attn_exact_fwd(q, k, v, out, lse=None, stream=None):
                             or not lse.is_contiguous() or tuple(lse.shape) != (B, H, N)):
         raise ValueError("lse must be a contiguous float32 device tensor [B, H, N]")
     stream = _stream(q, stream)
-    with torch.cuda.device(q.device):
+    with _OnDevice(q):
         _check(LIB.monarch_attn_exact_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                           None if lse is None else lse.data_ptr(), B, H, N, d,
                                           dtype_code(q.dtype), stream))
@@ -218,7 +245,7 @@ def monarch_attn_bwd(q, k, v, dout, dq, dk, dv, m: int, b: int, T: int, stream=N
     _check_tensors(q, dq, dk, dv)
     B, H, N, d = q.shape
     stream = _stream(q, stream)
-    with torch.cuda.device(q.device):
+    with _OnDevice(q):
         _check(LIB.monarch_attn_bwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), dq.data_ptr(),
                                     dk.data_ptr(), dv.data_ptr(), B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
     return dq, dk, dv
@@ -234,7 +261,7 @@ def monarch_attn_bwd_varlen(q, k, v, dout, dq, dk, dv, lens, m: int, b: int, T: 
     _check_lens(q, lens)
     B, H, N, d = q.shape
     stream = _stream(q, stream)
-    with torch.cuda.device(q.device):
+    with _OnDevice(q):
         _check(LIB.monarch_attn_bwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), dout.data_ptr(), dq.data_ptr(),
                                            dk.data_ptr(), dv.data_ptr(), lens.data_ptr(), B, H, N, d, m, b, T,
                                            dtype_code(q.dtype), stream))
