@@ -56,7 +56,8 @@ typedef enum {
  *           aligned, not overlapping q, k or v.  Fully overwritten.
  *           All four buffers are owned by the caller; the library neither
  *           frees nor retains them.
- * B, H    : batch and head counts (>= 0).
+ * B, H    : batch and head counts (>= 0); B * H * max(m, b) < 2^31 (one
+ *           workgroup per block or class of every head), else MA_EUNSUPPORTED.
  * N, m, b : sequence length, number of blocks and block size:
  *           m = ceil(N / b), i.e. (m - 1) * b < N <= m * b (m = 0 for an
  *           empty sequence, N = 0; b >= 1).  When N < m * b
@@ -154,7 +155,8 @@ int monarch_attn_fwd_objective(const void *q, const void *k, const void *v, void
  * maximises it, eq. softmax_variational_attention).
  *
  * q, k, v, out : DEVICE pointers to [B, H, N, d] tensors as in
- *                monarch_attn_fwd (any N >= 1; d as there).
+ *                monarch_attn_fwd (any N >= 1 below 2^31; d as there;
+ *                B * H * ceil(N / 64) < 2^31, else MA_EUNSUPPORTED).
  * lse          : NULL, or a DEVICE pointer to B*H*N floats (4-byte aligned,
  *                not overlapping the tensors), lse[(b*H + h)*N + row].
  * Asynchronous on `stream`; arguments are checked before any HIP call

@@ -105,6 +105,16 @@ bool overlaps(const void *a, size_t na, const void *b, size_t nb)
     return x < y + nb && y < x + na;
 }
 
+// B * H heads of `per` workgroups each must fit one grid (fewer than 2^31
+// workgroups), checked without forming a product that could overflow.
+int check_heads(int64_t B, int64_t H, int64_t per)
+{
+    if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
+    const int64_t lim = (int64_t)0x7fffffff / (per > 0 ? per : 1);
+    if (B > lim || H > lim || (H > 0 && B > lim / H)) return fail(MA_EUNSUPPORTED, "too many heads for one grid");
+    return MA_OK;
+}
+
 // The current device and its compute-unit count (queried once per device).
 int current_device(int &dev, int &num_cus)
 {
@@ -163,6 +173,7 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
     int rc = check_shape(N, d, m, b, T, dtype);
     if (rc != MA_OK) return rc;
+    if ((rc = check_heads(B, H, m > b ? m : b)) != MA_OK) return rc;
     if (B == 0 || H == 0 || N == 0) return MA_OK;  // nothing to compute: no launch, no pointer read
     if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
     if (need_obj && !obj) return fail(MA_EINVAL, "null objective pointer");
@@ -172,7 +183,6 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)out) & 15u)
         return fail(MA_EINVAL, "q, k, v and out must be 16-byte aligned");
     const int64_t BH = B * H;
-    if (BH * (int64_t)(m > b ? m : b) > (int64_t)0x7fffffff) return fail(MA_EUNSUPPORTED, "too many heads for one grid");
     const size_t tensor_bytes = (size_t)BH * N * d * elem_bytes(dtype);
     if (overlaps(out, tensor_bytes, q, tensor_bytes) || overlaps(out, tensor_bytes, k, tensor_bytes) ||
         overlaps(out, tensor_bytes, v, tensor_bytes))
@@ -270,6 +280,7 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
     if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
     int rc = check_bwd_shape(N, d, m, b, T, dtype);
     if (rc != MA_OK) return rc;
+    if ((rc = check_heads(B, H, m > b ? m : b)) != MA_OK) return rc;
     if (B == 0 || H == 0 || N == 0) return MA_OK;  // nothing to compute: no launch, no pointer read
     if (!q || !k || !v || !dout || !dq || !dk || !dv) return fail(MA_EINVAL, "null tensor pointer");
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)dout | (uintptr_t)dq | (uintptr_t)dk |
@@ -278,7 +289,6 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
     if (need_lens && !lens) return fail(MA_EINVAL, "null lens pointer");
     if (need_lens && ((uintptr_t)lens & 3u)) return fail(MA_EINVAL, "lens must be 4-byte aligned");
     const int64_t BH = B * H;
-    if (BH * (int64_t)(m > b ? m : b) > (int64_t)0x7fffffff) return fail(MA_EUNSUPPORTED, "too many heads for one grid");
     const size_t tb = (size_t)BH * N * d * elem_bytes(dtype);
     const void *ins[4] = {q, k, v, dout};
     void *outs[3] = {dq, dk, dv};
@@ -453,6 +463,8 @@ int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *ou
     if (B == 0 || H == 0 || N == 0) return MA_OK;  // nothing to compute: no launch, no pointer read
     if (!q || !k || !v || !out) return fail(MA_EINVAL, "null tensor pointer");
     if (N > 0x7fffffff) return fail(MA_EUNSUPPORTED, "N too large");
+    int rc = check_heads(B, H, (N + 63) / 64);  // one workgroup per 64 query rows
+    if (rc != MA_OK) return rc;
     if (((uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)out) & 15u)
         return fail(MA_EINVAL, "q, k, v and out must be 16-byte aligned");
     if ((uintptr_t)lse & 3u) return fail(MA_EINVAL, "lse must be 4-byte aligned");
@@ -470,7 +482,6 @@ int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *ou
     Launcher L{(hipStream_t)stream, g_timing.enabled};
     if (!L.timed) tlock.unlock();
     (void)hipGetLastError();
-    int rc;
     switch (dtype) {
     case MA_F32: rc = run_exact<float>(L, bufs, lse, BH, (int)N, (int)d); break;
     case MA_BF16: rc = run_exact<__bf16>(L, bufs, lse, BH, (int)N, (int)d); break;

@@ -56,6 +56,8 @@ FAKE = 1 << 20  # an aligned non-null address that is never dereferenced: every 
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 512, 64, 2, 256, 1, 1), 2),        # b > 128
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, 65, 1), 2),       # T > 64
         ((FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 16384, 128, 128, 128, 1, 0), 2),   # fp32 tile too big
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1 << 24, 1 << 24, 256, 64, 16, 16, 1, 1), 2),  # B H * 16 >= 2^31
+        ((FAKE, FAKE, FAKE, 2 * FAKE, 1 << 40, 1 << 40, 256, 64, 16, 16, 1, 1), 2),  # B H overflows int64
     ],
 )
 def test_invalid_arguments_rejected_before_any_hip_call(args, code):
@@ -203,6 +205,7 @@ def test_bwd_varlen_rejects_null_or_misaligned_lens():
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 16512, 64, 128, 129, 1, 1), 2),  # b > 128
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 8192, 128, 128, 64, 1, 0), 2),  # fp32 m > 64, d > 96
         ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1, 1, 256, 64, 16, 16, 33, 1), 2),   # T > 32
+        ((FAKE, FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, 4 * FAKE, 1 << 40, 1 << 40, 256, 64, 16, 16, 1, 1), 2),  # B H overflows
     ],
 )
 def test_bwd_invalid_arguments_rejected_before_any_hip_call(args, code):
@@ -282,3 +285,15 @@ def test_empty_calls_succeed_without_touching_pointers(B, H, N, m):
     # the other arguments are still checked
     assert ma.monarch_attn_fwd_raw(0, 0, 0, 0, B, H, N, 64, m, 16, 2, 9, None) == ma.MA_EINVAL
     assert ma.monarch_attn_fwd_raw(0, 0, 0, 0, B, H, N, 100, m, 16, 2, 1, None) == ma.MA_EUNSUPPORTED
+
+
+def test_head_counts_that_overflow_a_grid_are_rejected():
+    """B * H is checked without forming a product that could overflow."""
+    import paper_2505_18698_amd as ma
+
+    big = 1 << 40
+    assert ma.LIB.monarch_attn_exact_fwd(FAKE, FAKE, FAKE, 2 * FAKE, None, big, big, 256, 64, 1, None) == \
+        ma.MA_EUNSUPPORTED
+    assert ma.LIB.monarch_attn_fwd_objective(FAKE, FAKE, FAKE, 2 * FAKE, 3 * FAKE, big, 3, 256, 64, 16, 16, 2, 1,
+                                             None) == ma.MA_EUNSUPPORTED
+    assert "too many heads" in ma.monarch_attn_last_error()
