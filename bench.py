@@ -10,6 +10,8 @@ T=2, the one-workgroup-per-head kernel; and N=197 with the class token,
 post-padded to 15 x 14) are reported alongside in "also".
 
 Timed regions (HIP events on the stream the library launches on):
+  0. (untimed) W warm-up steps, repeated in rounds of W until 0.25 s of
+     calls have run, so that the GPU has left its idle clocks.
   1. K steps back to back -> ms_per_step and value = B*H*N / time.
   2. K more steps with the library's per-launch events enabled -> the average
      duration of each kernel; the one with the largest share of the step is
@@ -18,7 +20,9 @@ Inputs rotate over several copies (>= 512 MB in total) so that the 256 MB
 last-level cache cannot serve them from one step to the next.
 
 Each workload also reports the p10 / median / p90 of single calls (each
-between its own events) and a "hot" time on one input set.  measured_peaks
+between its own events), a "hot" time on one input set, and the time per call
+when the rotating calls are captured into a HIP graph and replayed (no host
+launch cost; graph_ms_per_call).  measured_peaks
 holds a 1 GiB device copy and 8192^3 GEMMs (bf16, fp32) timed on this GPU;
 every roofline record adds its fraction of that measured peak beside the
 fraction of the published one.
@@ -118,6 +122,27 @@ def plan_for(w, kinds):
     return plan
 
 
+WARM_S = 0.25  # seconds of untimed calls before a timed region (at least W calls)
+
+
+def warm_up(torch, step, warmup):
+    """W untimed calls, repeated in rounds of W until they have kept the GPU
+    busy for WARM_S seconds: after an idle spell (input generation, the
+    previous workload's host work) the GPU takes several milliseconds of work
+    to reach its steady clocks, and the timed region should see those.
+    W = 0 runs nothing."""
+    if warmup <= 0:
+        return
+    t0, i = time.perf_counter(), 0
+    while True:
+        for _ in range(warmup):
+            step(i)
+            i += 1
+        torch.cuda.synchronize()
+        if time.perf_counter() - t0 >= WARM_S:
+            return
+
+
 def call_work(w):
     """Compulsory bytes (Q, K, V in, O out: N rows) and flops of the method
     (on the Np = m * b rows it runs over) of one call."""
@@ -146,9 +171,7 @@ def measure(ma, torch, w, steps, warmup):
         qq, kk, vv, oo = sets[i % nsets]
         ma.monarch_attn_fwd(qq, kk, vv, oo, w.m, w.b, w.T)
 
-    for i in range(warmup):
-        step(i)
-    torch.cuda.synchronize()
+    warm_up(torch, step, warmup)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     for i in range(steps):
@@ -157,7 +180,8 @@ def measure(ma, torch, w, steps, warmup):
     end.synchronize()
     ms = start.elapsed_time(end) / steps
     log(f"[bench] {w.name}: {ms * 1e3:.1f} us per step over {steps} steps ({nsets} rotating input sets)")
-    extra = {"per_call_us": per_call_distribution(torch, step, steps), "hot_ms_per_step": hot_time(torch, step, steps)}
+    extra = {"per_call_us": per_call_distribution(torch, step, steps), "hot_ms_per_step": hot_time(torch, step, steps),
+             "graph_ms_per_call": graph_time(torch, step, steps, nsets)}
 
     # per-launch kernel durations
     plan, sums = None, None
@@ -219,6 +243,35 @@ def hot_time(torch, step, steps):
     b.record()
     b.synchronize()
     return round(a.elapsed_time(b) / steps, 6)
+
+
+def graph_time(torch, step, steps, nsets):
+    """ms per call when one call per input set is captured into a HIP graph
+    and the graph is replayed: the calls' GPU time without the host's launch
+    and binding cost.  The capture stream's workspace is sized by an eager
+    call on it first (a call under capture does not allocate)."""
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for i in range(nsets):
+            step(i)
+    s.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for i in range(nsets):
+            step(i)
+    reps = max(1, -(-steps // nsets))
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    b.synchronize()
+    ms = a.elapsed_time(b) / (reps * nsets)
+    del g
+    return round(ms, 6)
 
 
 def measured_peaks(torch):
@@ -286,9 +339,7 @@ def sdpa_context(ma, torch, w, steps, warmup, monarch_ms):
     for backend in (SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION):
         try:
             with sdpa_kernel(backend):
-                for i in range(warmup):
-                    F.scaled_dot_product_attention(*sets[i % nsets])
-                torch.cuda.synchronize()
+                warm_up(torch, lambda i: F.scaled_dot_product_attention(*sets[i % nsets]), warmup)
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a.record()
                 for i in range(steps):
@@ -359,9 +410,7 @@ def measure_backward(ma, torch, w, steps, warmup):
     def step(i):
         ma.monarch_attn_bwd(*sets[i % nsets], w.m, w.b, w.T)
 
-    for i in range(warmup):
-        step(i)
-    torch.cuda.synchronize()
+    warm_up(torch, step, warmup)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     for i in range(steps):
@@ -421,10 +470,8 @@ QUALITY_WORKLOADS = ("vit_b16_n196", "roberta_n1024", "lm_n16384")
 
 
 def time_calls(torch, step, steps, warmup):
-    """ms per call of `step(i)` over `steps` calls back to back, after `warmup`."""
-    for i in range(warmup):
-        step(i)
-    torch.cuda.synchronize()
+    """ms per call of `step(i)` over `steps` calls back to back, after the warm-up."""
+    warm_up(torch, step, warmup)
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
     for i in range(steps):
@@ -643,9 +690,7 @@ def copy_sweep(torch, sizes_mb, steps, warmup):
         n = int(mb * (1 << 20)) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
-        for _ in range(warmup):
-            dst.copy_(src)
-        torch.cuda.synchronize()
+        warm_up(torch, lambda i: dst.copy_(src), warmup)
         start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         start.record()
         for _ in range(steps):

@@ -88,6 +88,17 @@ typedef enum {
  * host thread) are enqueued one whole call at a time.  A stream's workspace
  * is grown with hipMalloc by the first call that needs more, after waiting
  * for that stream.  After the launches hipGetLastError is checked (MA_EHIP).
+ *
+ * HIP graph capture: a call on a stream being captured is recorded as its
+ * kernel launches, with the stream's workspace address baked in.  It makes
+ * no allocation, wait or event call, so the stream's workspace must already
+ * be large enough (an earlier call of that size on the same stream);
+ * otherwise the call fails with MA_EUNSUPPORTED and records nothing.  A
+ * buffer that a captured call used is never freed when a later call grows
+ * that workspace, only by monarch_attn_release_workspace, so captured graphs
+ * stay valid until then.  Capture with per-launch timing enabled fails with
+ * MA_EUNSUPPORTED.  The same holds for every entry point that takes a
+ * stream.
  * The message of the last failure on the calling thread is returned by
  * monarch_attn_last_error().
  */
@@ -240,9 +251,11 @@ int monarch_attn_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, in
 size_t monarch_attn_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,
                                     int64_t m, int64_t b, int32_t T, int32_t dtype);
 
-/* Free the workspaces of the current device (all streams).  Waits for calls
- * being enqueued and for the device to go idle first, so it may be called
- * while other threads use the library; their next call allocates again. */
+/* Free the workspaces of the current device (all streams), including every
+ * buffer kept alive for captured graphs (see monarch_attn_fwd): a graph that
+ * captured a call must not be replayed after this.  Waits for calls being
+ * enqueued and for the device to go idle first, so it may be called while
+ * other threads use the library; their next call allocates again. */
 int monarch_attn_release_workspace(void);
 
 /*

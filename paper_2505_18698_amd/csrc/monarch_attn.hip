@@ -11,6 +11,7 @@
 #include <memory>
 #include <mutex>
 #include <unordered_map>
+#include <vector>
 
 #include "host_common.hpp"
 
@@ -84,6 +85,12 @@ struct Workspace {
     std::mutex mu;
     void *ptr = nullptr;
     size_t bytes = 0;
+    // A call captured into a HIP graph bakes `ptr` into the graph, so a
+    // buffer that was ever used under capture is not freed when the
+    // workspace grows: it is kept in `retired` until
+    // monarch_attn_release_workspace.
+    bool captured = false;
+    std::vector<void *> retired;
 };
 
 struct Device {
@@ -131,10 +138,25 @@ int current_device(int &dev, int &num_cus)
     return MA_OK;
 }
 
+// Whether `stream` is being captured into a HIP graph.
+int stream_capturing(hipStream_t stream, bool &capturing)
+{
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &st) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(MA_EHIP, "hipStreamIsCapturing failed");
+    }
+    capturing = st != hipStreamCaptureStatusNone;
+    return MA_OK;
+}
+
 // The workspace of (dev, stream), locked into `hold` for the caller and grown
 // with hipMalloc to at least `need` bytes.  Growing first waits for the
-// stream, whose earlier calls may still use the old buffer.
-int acquire_workspace(int dev, hipStream_t stream, size_t need, char **base, std::unique_lock<std::mutex> &hold)
+// stream, whose earlier calls may still use the old buffer.  A stream under
+// graph capture cannot allocate or wait: its workspace must already be
+// large enough.
+int acquire_workspace(int dev, hipStream_t stream, bool capturing, size_t need, char **base,
+                      std::unique_lock<std::mutex> &hold)
 {
     Workspace *w;
     {
@@ -145,11 +167,21 @@ int acquire_workspace(int dev, hipStream_t stream, size_t need, char **base, std
     }
     hold = std::unique_lock<std::mutex>(w->mu);
     if (w->bytes < need) {
+        if (capturing)
+            return fail(MA_EUNSUPPORTED,
+                        "the stream is being captured and its workspace holds %zu of the %zu bytes this call needs: "
+                        "make a call of this size on the stream before capturing",
+                        w->bytes, need);
         if (w->ptr) {
-            if (hipStreamSynchronize(stream) != hipSuccess) return fail(MA_EHIP, "hipStreamSynchronize failed");
-            (void)hipFree(w->ptr);
+            if (w->captured) {
+                w->retired.push_back(w->ptr);  // a captured graph may still use it
+            } else {
+                if (hipStreamSynchronize(stream) != hipSuccess) return fail(MA_EHIP, "hipStreamSynchronize failed");
+                (void)hipFree(w->ptr);
+            }
             w->ptr = nullptr;
             w->bytes = 0;
+            w->captured = false;
         }
         void *p = nullptr;
         if (hipMalloc(&p, need) != hipSuccess) {
@@ -159,7 +191,17 @@ int acquire_workspace(int dev, hipStream_t stream, size_t need, char **base, std
         w->ptr = p;
         w->bytes = need;
     }
+    if (capturing) w->captured = true;
     *base = (char *)w->ptr;
+    return MA_OK;
+}
+
+// Per-launch timing records events, which a graph capture would take in.
+int check_capture(hipStream_t stream, bool &capturing)
+{
+    int rc = stream_capturing(stream, capturing);
+    if (rc != MA_OK) return rc;
+    if (capturing && g_timing.enabled) return fail(MA_EUNSUPPORTED, "per-launch timing is on: it cannot be captured");
     return MA_OK;
 }
 
@@ -200,13 +242,16 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, obj, lens};
     int dev = 0, num_cus = 0;
     if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
+    bool capturing = false;
+    if ((rc = check_capture((hipStream_t)stream, capturing)) != MA_OK) return rc;
     std::unique_lock<std::mutex> ws_hold;  // the stream's workspace, held until the launches are enqueued
     const bool states = !uses_fused(path, dtype, d, m, b);  // the fused kernel keeps its states in LDS
     const size_t obj_part_bytes = obj ? align_up((size_t)BH * T * b * sizeof(float)) : 0;
     if (states || obj) {
         const size_t state_ws = states ? workspace_bytes(BH, m * b, d, dtype) : 0;
         char *base = nullptr;
-        if ((rc = acquire_workspace(dev, (hipStream_t)stream, state_ws + obj_part_bytes, &base, ws_hold)) != MA_OK)
+        if ((rc = acquire_workspace(dev, (hipStream_t)stream, capturing, state_ws + obj_part_bytes, &base,
+                                    ws_hold)) != MA_OK)
             return rc;
         if (states) {
             bufs.aR = base;
@@ -302,10 +347,13 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
     }
     int dev = 0, num_cus = 0;
     if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
+    bool capturing = false;
+    if ((rc = check_capture((hipStream_t)stream, capturing)) != MA_OK) return rc;
     const BwdLayout lay = bwd_layout(BH, N, d, m, b, T, dtype);
     char *base = nullptr;
     std::unique_lock<std::mutex> ws_hold;  // the stream's workspace, held until the launches are enqueued
-    if ((rc = acquire_workspace(dev, (hipStream_t)stream, lay.total(), &base, ws_hold)) != MA_OK) return rc;
+    if ((rc = acquire_workspace(dev, (hipStream_t)stream, capturing, lay.total(), &base, ws_hold)) != MA_OK)
+        return rc;
     BwdCallBufs bufs{};
     bufs.q = q, bufs.k = k, bufs.v = v, bufs.dout = dout, bufs.dq = dq, bufs.dk = dk, bufs.dv = dv;
     bufs.lens = lens;
@@ -376,14 +424,19 @@ int monarch_attn_release_workspace(void)
     for (auto &entry : D.ws) {
         Workspace &w = *entry.second;
         std::lock_guard<std::mutex> wl(w.mu);
-        if (!w.ptr) continue;
+        if (!w.ptr && w.retired.empty()) continue;
         if (!synced) {
             if (hipDeviceSynchronize() != hipSuccess) return fail(MA_EHIP, "hipDeviceSynchronize failed");
             synced = true;
         }
-        if (hipFree(w.ptr) != hipSuccess) return fail(MA_EHIP, "freeing the workspace failed");
+        while (!w.retired.empty()) {
+            if (hipFree(w.retired.back()) != hipSuccess) return fail(MA_EHIP, "freeing the workspace failed");
+            w.retired.pop_back();
+        }
+        if (w.ptr && hipFree(w.ptr) != hipSuccess) return fail(MA_EHIP, "freeing the workspace failed");
         w.ptr = nullptr;
         w.bytes = 0;
+        w.captured = false;
     }
     return MA_OK;
 }
@@ -478,6 +531,8 @@ int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *ou
                 overlaps(lse, lse_bytes, v, tensor_bytes) || overlaps(lse, lse_bytes, out, tensor_bytes)))
         return fail(MA_EINVAL, "lse must not overlap q, k, v or out");
     CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
+    bool capturing = false;
+    if ((rc = check_capture((hipStream_t)stream, capturing)) != MA_OK) return rc;
     std::unique_lock<std::mutex> tlock(g_timing_mutex);
     Launcher L{(hipStream_t)stream, g_timing.enabled};
     if (!L.timed) tlock.unlock();
