@@ -16,6 +16,10 @@ Timed regions (HIP events on the stream the library launches on):
   2. K more steps with the library's per-launch events enabled -> the average
      duration of each kernel; the one with the largest share of the step is
      the "dominant kernel" whose algorithmic bytes and flops give `roofline`.
+     A pair of events adds a roughly fixed time to every launch it brackets
+     (about 2.5 us here), so each duration has the per-launch excess of the
+     event-read step over the step of region 1 taken off (launch_overhead_us;
+     the raw reading is kept as event_us).
 Inputs rotate over several copies (>= 512 MB in total) so that the 256 MB
 last-level cache cannot serve them from one step to the next.
 
@@ -143,6 +147,17 @@ def warm_up(torch, step, warmup):
             return
 
 
+def launch_overhead_ms(event_ms, step_ms):
+    """Per-launch cost of the per-launch events: each launch's pair of events
+    adds a roughly fixed time (dispatch after the first event, completion
+    before the second) to the duration it reads.  Estimated as the excess of
+    the event-read durations of one step over the un-instrumented step time,
+    shared equally over the step's launches (0 if there is none); subtracting
+    it leaves each kernel the time it took in the timed region, gaps between
+    launches included."""
+    return max(0.0, (sum(event_ms) - step_ms) / len(event_ms)) if event_ms else 0.0
+
+
 def call_work(w):
     """Compulsory bytes (Q, K, V in, O out: N rows) and flops of the method
     (on the Np = m * b rows it runs over) of one call."""
@@ -199,11 +214,14 @@ def measure(ma, torch, w, steps, warmup):
     finally:
         ma.monarch_attn_timing_enable(False)
     kernels = []
+    over = launch_overhead_ms([t / steps for t in sums], ms)
+    extra["launch_overhead_us"] = round(over * 1e3, 3)
     for (name, nbytes, nflops), tot in zip(plan, sums):
-        avg_ms = tot / steps
+        avg_ms = tot / steps - over
         kernels.append({
             "kernel": name,
             "avg_us": round(avg_ms * 1e3, 3),
+            "event_us": round(tot / steps * 1e3, 3),
             "alg_bytes": nbytes,
             "alg_flops": nflops,
             "GB_s": round(nbytes / (avg_ms * 1e-3) / 1e9, 1),
@@ -444,15 +462,17 @@ def measure_backward(ma, torch, w, steps, warmup):
     nrec = len(fwd_plan)
     assert kinds[:nrec] == [p[0] for p in fwd_plan], (kinds, fwd_plan)
     kernels = []
+    over = launch_overhead_ms([t / steps for t in sums], ms)
     for j, kind in enumerate(kinds):
-        avg_ms = sums[j] / steps
+        avg_ms = sums[j] / steps - over
         if j < nrec:
             nbytes, nflops = fwd_plan[j][1], fwd_plan[j][2]
             step_t = None
         else:
             step_t = w.T - (j - nrec) // 2
             nbytes, nflops = bwd_kernel_work(w, kind, step_t)
-        kernels.append({"kernel": kind, "step": step_t, "avg_us": round(avg_ms * 1e3, 3), "alg_bytes": nbytes,
+        kernels.append({"kernel": kind, "step": step_t, "avg_us": round(avg_ms * 1e3, 3),
+                        "event_us": round(sums[j] / steps * 1e3, 3), "alg_bytes": nbytes,
                         "alg_flops": nflops, "GB_s": round(nbytes / (avg_ms * 1e-3) / 1e9, 1),
                         "TFLOP_s": round(nflops / (avg_ms * 1e-3) / 1e12, 2)})
     sweep = kernels[nrec:]
@@ -463,7 +483,7 @@ def measure_backward(ma, torch, w, steps, warmup):
     return {"config": w.describe(), "value": round(w.B * w.H * w.N / (ms * 1e-3), 1), "unit": UNIT,
             "ms_per_call": round(ms, 6), "recompute_us": round(sum(x["avg_us"] for x in kernels[:nrec]), 3),
             "sweep_us": round(sum(x["avg_us"] for x in sweep), 3), "roofline": roof, "kernels": kernels,
-            "rotating_input_sets": nsets}
+            "launch_overhead_us": round(over * 1e3, 3), "rotating_input_sets": nsets}
 
 
 QUALITY_WORKLOADS = ("vit_b16_n196", "roberta_n1024", "lm_n16384")
