@@ -119,8 +119,8 @@ def _check_tensors(q, k, v, out):
             raise TypeError(f"{name} must be a device tensor")
         if t.dim() != 4 or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous [B, H, N, d] tensor")
-        if t.shape != q.shape or t.dtype != q.dtype:
-            raise ValueError(f"{name} must match q in shape and dtype")
+        if t.shape != q.shape or t.dtype != q.dtype or t.device != q.device:
+            raise ValueError(f"{name} must match q in shape, dtype and device")
 
 
 def _stream(q, stream):
@@ -206,9 +206,9 @@ def monarch_attn_fwd_objective(q, k, v, out, obj, m: int, b: int, T: int, stream
     import torch
 
     _check_tensors(q, k, v, out)
-    if not isinstance(obj, torch.Tensor) or not obj.is_cuda or obj.dtype != torch.float32 \
+    if not isinstance(obj, torch.Tensor) or obj.device != q.device or obj.dtype != torch.float32 \
             or not obj.is_contiguous() or tuple(obj.shape) != (q.shape[0], q.shape[1], T):
-        raise ValueError("obj must be a contiguous float32 device tensor [B, H, T]")
+        raise ValueError("obj must be a contiguous float32 tensor [B, H, T] on the device of q")
     B, H, N, d = q.shape
     stream = _stream(q, stream)
     with _OnDevice(q):
@@ -224,9 +224,10 @@ def monarch_attn_exact_fwd(q, k, v, out, lse=None, stream=None):
 
     _check_tensors(q, k, v, out)
     B, H, N, d = q.shape
-    if lse is not None and (not isinstance(lse, torch.Tensor) or not lse.is_cuda or lse.dtype != torch.float32
-                            or not lse.is_contiguous() or tuple(lse.shape) != (B, H, N)):
-        raise ValueError("lse must be a contiguous float32 device tensor [B, H, N]")
+    if lse is not None and (not isinstance(lse, torch.Tensor) or lse.device != q.device
+                            or lse.dtype != torch.float32 or not lse.is_contiguous()
+                            or tuple(lse.shape) != (B, H, N)):
+        raise ValueError("lse must be a contiguous float32 tensor [B, H, N] on the device of q")
     stream = _stream(q, stream)
     with _OnDevice(q):
         _check(LIB.monarch_attn_exact_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
