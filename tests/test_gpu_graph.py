@@ -193,3 +193,39 @@ def test_timing_cannot_be_captured(ma):
         ma.monarch_attn_timing_enable(False)
     torch.cuda.synchronize()
     assert np.isfinite(out.float().cpu().numpy()).all()
+
+
+@pytest.mark.parametrize("entry", ["varlen", "objective", "exact"])
+def test_other_entry_points_replay_match_eager(ma, entry):
+    """The padded-batch, objective and exact-attention calls under capture."""
+    import torch
+
+    B, H, N, d, m, b, T = 3, 2, 640, 64, 20, 32, 2
+    sets = _inputs(B, H, N, d, seed=1000, n_sets=2)
+    q, k, v = (t.clone() for t in sets[0])
+    lens = torch.tensor([640, 333, 17], dtype=torch.int32, device="cuda")
+    out = torch.empty_like(q)
+    aux = torch.empty(B, H, T if entry == "objective" else N, dtype=torch.float32, device="cuda")
+
+    def call(o, a):
+        if entry == "varlen":
+            ma.monarch_attn_fwd_varlen(q, k, v, o, lens, m, b, T)
+        elif entry == "objective":
+            ma.monarch_attn_fwd_objective(q, k, v, o, a, m, b, T)
+        else:
+            ma.monarch_attn_exact_fwd(q, k, v, o, a)
+
+    g = _warm_and_capture(lambda: call(out, aux), torch.cuda.Stream())
+    for r, (qs, ks, vs) in enumerate(sets + sets[:1]):
+        q.copy_(qs), k.copy_(ks), v.copy_(vs)
+        out.fill_(float("nan")), aux.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        eo, ea = torch.full_like(out, float("nan")), torch.full_like(aux, float("nan"))
+        call(eo, ea)
+        torch.cuda.synchronize()
+        print(f"{entry} replay {r}: bitwise equal to eager", flush=True)
+        assert torch.equal(out, eo), (entry, r)
+        if entry != "varlen":  # the padded-batch call has no second output
+            assert torch.equal(aux, ea), (entry, r)
+    del g
