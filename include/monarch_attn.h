@@ -71,7 +71,9 @@ typedef enum {
  *           fp16) or 4 (fp32), so that every row is a whole number of 16-byte
  *           chunks.  The kernels work on tiles of width D = 64, 96 or 128
  *           (the smallest that holds d) with the extra columns zero.  fp32
- *           also needs 16*ceil(m/16)*D <= 8192 and 16*ceil(b/16)*D <= 8192.
+ *           also needs tile(m)*D <= 8192 and tile(b)*D <= 8192, where
+ *           tile(x) is the kernels' tile height for x rows: the smallest of
+ *           16, 32, 64 and 128 that holds x.
  * T       : number of (R, L) update pairs, 1 <= T <= 64.
  * dtype   : an ma_dtype value.
  * stream  : the hipStream_t to launch on (NULL = the null stream).

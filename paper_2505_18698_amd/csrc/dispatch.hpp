@@ -124,13 +124,6 @@ int dispatch_l(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int 
     }
 }
 
-// Tile size (16, 32, 64 or 128 rows) used for a block of n <= 128 rows.
-inline int tile_rows(int n)
-{
-    const int p = pad16(n);
-    return p <= 16 ? 16 : p <= 32 ? 32 : p <= 64 ? 64 : 128;
-}
-
 template <typename T, int D>
 int r_step(Launcher &L, const CallBufs &B, ma::HeadDims hd, int64_t BH, int nc, bool first, bool final_)
 {

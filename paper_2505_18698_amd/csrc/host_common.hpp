@@ -15,6 +15,13 @@ int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 
 inline int pad16(int64_t x) { return (int)((x + 15) / 16 * 16); }
 
+// Tile size (16, 32, 64 or 128 rows) the kernels use for a block of n <= 128 rows.
+inline int tile_rows(int64_t n)
+{
+    const int p = pad16(n);
+    return p <= 16 ? 16 : p <= 32 ? 32 : p <= 64 ? 64 : 128;
+}
+
 // Kernel kinds reported by the timing interface.
 enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4, kObjSum = 5, kExact = 6, kBwdL = 7, kBwdR = 8 };
 

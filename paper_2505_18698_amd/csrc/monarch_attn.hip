@@ -52,10 +52,11 @@ int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t d
     if (d > 128 || d % (16 / (int64_t)elem_bytes(dtype)) != 0)
         return fail(MA_EUNSUPPORTED, "d must be a multiple of %d up to 128 (got %lld)", (int)(16 / elem_bytes(dtype)),
                     (long long)d);
+    // fp32 tiles of the half-steps: tile rows (16, 32, 64 or 128) times D at most 8192 elements
     const int64_t D = tile_d(d);
-    if (dtype == MA_F32 && ((int64_t)pad16(m) * D > 8192 || (int64_t)pad16(b) * D > 8192))
-        return fail(MA_EUNSUPPORTED, "fp32 needs 16*ceil(m/16)*D <= 8192 and 16*ceil(b/16)*D <= 8192, D = %lld",
-                    (long long)D);
+    if (dtype == MA_F32 && ((int64_t)tile_rows(m) * D > 8192 || (int64_t)tile_rows(b) * D > 8192))
+        return fail(MA_EUNSUPPORTED, "fp32 needs tile(m)*D <= 8192 and tile(b)*D <= 8192 (tile: 16, 32, 64 or 128 "
+                    "rows, D = %lld)", (long long)D);
     return MA_OK;
 }
 

@@ -92,6 +92,10 @@ def test_invalid_arguments_rejected_before_any_hip_call(args, code):
         ((256, 36, 16, 16, 2, 0), True),      # fp32: multiples of 4
         ((256, 100, 16, 16, 2, 1), False),
         ((16384, 96, 128, 128, 2, 0), False), # fp32 tile too big at D = 96
+        ((274, 88, 4, 75, 2, 0), False),      # fp32: b = 75 takes a 128-row tile, 128 x 96 > 8192
+        ((2923, 84, 37, 80, 1, 0), False),    # fp32: the same at b = 80
+        ((4096, 128, 64, 64, 2, 0), True),    # fp32: 64-row tiles at D = 128
+        ((2560, 96, 40, 64, 2, 0), True),     # fp32: 64 x 96
     ],
 )
 def test_supported_shapes(shape, ok):

@@ -1,0 +1,148 @@
+"""Seeded random shapes against the oracle: the forward pass on both paths,
+padded batches, and the gradient.
+
+Each case draws its own element type, m and b (1..128), N in ((m - 1) b, m b],
+d (every multiple of 16 bytes up to 128), T, batch and head counts and the
+input scale from its seed, and keeps only shapes the library reports as
+supported (monarch_attn_check, no GPU call).  Bars as in the other parity
+tests: rel-Frobenius <= 1e-5 / 2e-5 (fp32 forward / gradient) and <= 2e-2 /
+3e-2 (bf16, fp16), outputs starting as NaN so that an unwritten element
+fails, rows past a sequence's length exactly zero.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import oracle.backward as ob
+import synth_inputs as si
+
+pytestmark = pytest.mark.gpu
+
+FWD_TOL = {"f32": 1e-5, "bf16": 2e-2, "f16": 2e-2}
+BWD_TOL = {"f32": 2e-5, "bf16": 3e-2, "f16": 3e-2}
+
+
+@pytest.fixture(scope="module")
+def ma():
+    import torch
+
+    assert torch.cuda.is_available(), "no GPU visible"
+    import paper_2505_18698_amd as lib
+
+    return lib
+
+
+def _td(dtype):
+    import torch
+
+    return {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+
+
+def _code(ma, dtype):
+    return {"f32": ma.MA_F32, "bf16": ma.MA_BF16, "f16": ma.MA_F16}[dtype]
+
+
+def draw(ma, seed, max_np, max_t, check):
+    """(dtype, B, H, m, b, n, d, T, scale) for case `seed`: the first supported draw."""
+    rs = np.random.RandomState(seed)
+    while True:
+        dtype = str(rs.choice(["f32", "bf16", "f16"]))
+        m, b = int(rs.randint(1, 129)), int(rs.randint(1, 129))
+        if m * b > max_np:
+            continue
+        n = int(rs.randint((m - 1) * b + 1, m * b + 1))
+        unit = 4 if dtype == "f32" else 8
+        d = unit * int(rs.randint(1, 128 // unit + 1))
+        T = int(rs.randint(1, max_t + 1))
+        if check(n, d, m, b, T, _code(ma, dtype)) != 0:
+            continue
+        B, H = int(rs.randint(1, 3)), int(rs.randint(1, 3))
+        scale = float(rs.choice([0.5, 1.0, 1.5]))
+        return dtype, B, H, m, b, n, d, T, scale
+
+
+def _to_dev(arrays, dtype):
+    import torch
+
+    return [torch.from_numpy(x).to(_td(dtype)).cuda() for x in arrays]
+
+
+@pytest.mark.parametrize("path", ["auto", "half_steps"])
+@pytest.mark.parametrize("case", range(40))
+def test_random_forward(ma, case, path):
+    import torch
+
+    dtype, B, H, m, b, n, d, T, scale = draw(ma, 7000 + case, 4096, 4, ma.monarch_attn_check)
+    label = f"fwd {path} {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T} scale{scale}"
+    print(label, flush=True)
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=7000 + case, scale=scale)
+    ref = oracle.monarch_attention(q, k, v, m, b, T)
+    prev = ma.monarch_attn_set_path(ma.PATH_AUTO if path == "auto" else ma.PATH_HALF_STEPS)
+    try:
+        tq, tk, tv = _to_dev((q, k, v), dtype)
+        out = torch.full_like(tq, float("nan"))
+        ma.monarch_attn_fwd(tq, tk, tv, out, m, b, T)
+        torch.cuda.synchronize()
+    finally:
+        ma.monarch_attn_set_path(prev)
+    o = out.double().cpu().numpy()
+    assert np.isfinite(o).all(), label
+    err = oracle.rel_frobenius(o, ref)
+    print(f"  rel_frob={err:.3e}", flush=True)
+    assert err <= FWD_TOL[dtype], (label, err)
+
+
+@pytest.mark.parametrize("case", range(16))
+def test_random_padded_batch(ma, case):
+    import torch
+
+    dtype, _, H, m, b, n, d, T, scale = draw(ma, 8000 + case, 4096, 3, ma.monarch_attn_check)
+    rs = np.random.RandomState(8500 + case)
+    B = int(rs.randint(2, 5))
+    edges = [0, 1, n, max(0, n - 1), min(n, b), min(n, b + 1)]
+    lens = [int(rs.choice(edges)) if rs.rand() < 0.4 else int(rs.randint(0, n + 1)) for _ in range(B)]
+    label = f"varlen {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T} lens={lens}"
+    print(label, flush=True)
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=8000 + case, scale=scale)
+    ref = oracle.monarch_attention_varlen(q, k, v, np.array(lens), m, b, T)
+    tq, tk, tv = _to_dev((q, k, v), dtype)
+    out = torch.full_like(tq, float("nan"))
+    ma.monarch_attn_fwd_varlen(tq, tk, tv, out, torch.tensor(lens, dtype=torch.int32, device="cuda"), m, b, T)
+    torch.cuda.synchronize()
+    o = out.double().cpu().numpy()
+    assert np.isfinite(o).all(), label
+    for bi, ln in enumerate(lens):
+        assert np.all(o[bi, :, ln:] == 0.0), (label, bi)
+    real = np.concatenate([o[bi, :, :ln].ravel() for bi, ln in enumerate(lens)])
+    want = np.concatenate([ref[bi, :, :ln].ravel() for bi, ln in enumerate(lens)])
+    err = float(np.linalg.norm(real - want) / np.linalg.norm(want)) if np.linalg.norm(want) > 0 else 0.0
+    print(f"  rel_frob={err:.3e}", flush=True)
+    assert err <= FWD_TOL[dtype], (label, err)
+
+
+@pytest.mark.parametrize("case", range(16))
+def test_random_gradient(ma, case):
+    import torch
+
+    dtype, B, H, m, b, n, d, T, scale = draw(ma, 9000 + case, 512, 3, ma.LIB.monarch_attn_bwd_check)
+    label = f"bwd {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T} scale{scale}"
+    print(label, flush=True)
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=9000 + case, scale=scale)
+    g = si.random_cotangent((B, H, n, d), dtype, seed=9000 + case)
+    tq, tk, tv, tg = _to_dev((q, k, v, g), dtype)
+    outs = [torch.full_like(tq, float("nan")) for _ in range(3)]
+    ma.monarch_attn_bwd(tq, tk, tv, tg, *outs, m, b, T)
+    torch.cuda.synchronize()
+    got = [x.double().cpu().numpy() for x in outs]
+    want = [np.zeros(q.shape) for _ in range(3)]
+    for i in range(B):
+        for h in range(H):
+            for w, r in zip(want, ob.autograd_grads(q[i, h], k[i, h], v[i, h], g[i, h], m, b, T)):
+                w[i, h] = r
+    errs = []
+    for name, x, w in zip(("dq", "dk", "dv"), got, want):
+        assert np.isfinite(x).all(), (label, name)
+        errs.append(oracle.rel_frobenius(x, w))
+    print(f"  rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
+    for name, e in zip(("dq", "dk", "dv"), errs):
+        assert e <= BWD_TOL[dtype], (label, name, e)
