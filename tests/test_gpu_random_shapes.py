@@ -42,17 +42,17 @@ def _code(ma, dtype):
     return {"f32": ma.MA_F32, "bf16": ma.MA_BF16, "f16": ma.MA_F16}[dtype]
 
 
-def draw(ma, seed, max_np, max_t, check):
+def draw(ma, seed, max_np, max_t, check, max_mb=128, max_d=128, dtypes=("f32", "bf16", "f16")):
     """(dtype, B, H, m, b, n, d, T, scale) for case `seed`: the first supported draw."""
     rs = np.random.RandomState(seed)
     while True:
-        dtype = str(rs.choice(["f32", "bf16", "f16"]))
-        m, b = int(rs.randint(1, 129)), int(rs.randint(1, 129))
+        dtype = str(rs.choice(list(dtypes)))
+        m, b = int(rs.randint(1, max_mb + 1)), int(rs.randint(1, max_mb + 1))
         if m * b > max_np:
             continue
         n = int(rs.randint((m - 1) * b + 1, m * b + 1))
         unit = 4 if dtype == "f32" else 8
-        d = unit * int(rs.randint(1, 128 // unit + 1))
+        d = unit * int(rs.randint(1, max_d // unit + 1))
         T = int(rs.randint(1, max_t + 1))
         if check(n, d, m, b, T, _code(ma, dtype)) != 0:
             continue
@@ -68,11 +68,11 @@ def _to_dev(arrays, dtype):
 
 
 @pytest.mark.parametrize("path", ["auto", "half_steps"])
-@pytest.mark.parametrize("case", range(40))
+@pytest.mark.parametrize("case", range(100))
 def test_random_forward(ma, case, path):
     import torch
 
-    dtype, B, H, m, b, n, d, T, scale = draw(ma, 7000 + case, 4096, 4, ma.monarch_attn_check)
+    dtype, B, H, m, b, n, d, T, scale = draw(ma, 7000 + case, 4096, 6, ma.monarch_attn_check)
     label = f"fwd {path} {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T} scale{scale}"
     print(label, flush=True)
     q, k, v = si.random_qkv(B, H, n, d, dtype, seed=7000 + case, scale=scale)
@@ -92,7 +92,37 @@ def test_random_forward(ma, case, path):
     assert err <= FWD_TOL[dtype], (label, err)
 
 
-@pytest.mark.parametrize("case", range(16))
+@pytest.mark.parametrize("case", range(40))
+def test_random_small_heads(ma, case):
+    """m, b <= 16 and d <= 64 in 16-bit types: the one-workgroup-per-head
+    kernel on the automatic path, and the half-step kernels."""
+    import torch
+
+    dtype, B, H, m, b, n, d, T, scale = draw(ma, 7500 + case, 256, 5, ma.monarch_attn_check, max_mb=16, max_d=64,
+                                              dtypes=("bf16", "f16"))
+    B, H = 2 * B, 3 * H  # several workgroups
+    label = f"small {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T}"
+    print(label, flush=True)
+    assert ma.fused_applies(d, m, b, _code(ma, dtype))
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=7500 + case, scale=scale)
+    ref = oracle.monarch_attention(q, k, v, m, b, T)
+    for path in (ma.PATH_FUSED, ma.PATH_HALF_STEPS):
+        prev = ma.monarch_attn_set_path(path)
+        try:
+            tq, tk, tv = _to_dev((q, k, v), dtype)
+            out = torch.full_like(tq, float("nan"))
+            ma.monarch_attn_fwd(tq, tk, tv, out, m, b, T)
+            torch.cuda.synchronize()
+        finally:
+            ma.monarch_attn_set_path(prev)
+        o = out.double().cpu().numpy()
+        assert np.isfinite(o).all(), (label, path)
+        err = oracle.rel_frobenius(o, ref)
+        print(f"  path {path} rel_frob={err:.3e}", flush=True)
+        assert err <= FWD_TOL[dtype], (label, path, err)
+
+
+@pytest.mark.parametrize("case", range(40))
 def test_random_padded_batch(ma, case):
     import torch
 
@@ -120,11 +150,11 @@ def test_random_padded_batch(ma, case):
     assert err <= FWD_TOL[dtype], (label, err)
 
 
-@pytest.mark.parametrize("case", range(16))
+@pytest.mark.parametrize("case", range(48))
 def test_random_gradient(ma, case):
     import torch
 
-    dtype, B, H, m, b, n, d, T, scale = draw(ma, 9000 + case, 512, 3, ma.LIB.monarch_attn_bwd_check)
+    dtype, B, H, m, b, n, d, T, scale = draw(ma, 9000 + case, 1024, 3, ma.LIB.monarch_attn_bwd_check)
     label = f"bwd {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T} scale{scale}"
     print(label, flush=True)
     q, k, v = si.random_qkv(B, H, n, d, dtype, seed=9000 + case, scale=scale)
