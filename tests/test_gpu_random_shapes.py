@@ -176,3 +176,30 @@ def test_random_gradient(ma, case):
     print(f"  rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
     for name, e in zip(("dq", "dk", "dv"), errs):
         assert e <= BWD_TOL[dtype], (label, name, e)
+
+
+# relative to max |f|; the derivation is beside the objective parity test
+OBJ_TOL = {"f32": 1e-5, "bf16": 1e-3, "f16": 1e-3}
+
+
+@pytest.mark.parametrize("case", range(30))
+def test_random_objective(ma, case):
+    import torch
+
+    dtype, B, H, m, b, n, d, T, scale = draw(ma, 9500 + case, 4096, 4, ma.monarch_attn_check)
+    label = f"objective {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T} scale{scale}"
+    print(label, flush=True)
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=9500 + case, scale=scale)
+    ref_o, ref_f = oracle.monarch_attention_objective(q, k, v, m, b, T)
+    tq, tk, tv = _to_dev((q, k, v), dtype)
+    out = torch.full_like(tq, float("nan"))
+    obj = torch.full((B, H, T), float("nan"), dtype=torch.float32, device="cuda")
+    ma.monarch_attn_fwd_objective(tq, tk, tv, out, obj, m, b, T)
+    torch.cuda.synchronize()
+    o, f = out.double().cpu().numpy(), obj.double().cpu().numpy()
+    assert np.isfinite(o).all() and np.isfinite(f).all(), label
+    err = oracle.rel_frobenius(o, ref_o)
+    rel = float(np.abs(f - ref_f).max() / max(np.abs(ref_f).max(), 1e-30))
+    print(f"  rel_frob={err:.3e} objective max rel err={rel:.3e}", flush=True)
+    assert err <= FWD_TOL[dtype], (label, err)
+    assert rel <= OBJ_TOL[dtype], (label, rel)
