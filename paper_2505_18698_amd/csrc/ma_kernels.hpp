@@ -623,12 +623,6 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         const int dd = hd.d;
         const int64_t N = (int64_t)m * b, hoff = bh * N * D, toff = bh * (int64_t)hd.n * dd;
         const int lane = tid & 63, wave = tid >> 6;
-        const T *kblk = p.k + toff + (int64_t)k * b * dd;
-        gr.kt.fetch([=](int r) { return kblk + (int64_t)r * dd; }, kv, tid, dd);
-        if constexpr (FINAL) {
-            const T *vblk = p.v + toff + (int64_t)k * b * dd;
-            gr.vt.fetch([=](int r) { return vblk + (int64_t)r * dd; }, kv, tid, dd);
-        }
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int j = (wave * RT + r) * 16 + (lane & 15);
@@ -644,6 +638,14 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
                 if (j < b) gr.cr[r] = p.cR[bh * N + (int64_t)j * m + k];
             }
         }
+        // K and V after the alpha_R rows, V last: the scores wait for the rows
+        // and K only, and V is staged just before the product that needs it
+        const T *kblk = p.k + toff + (int64_t)k * b * dd;
+        gr.kt.fetch([=](int r) { return kblk + (int64_t)r * dd; }, kv, tid, dd);
+        if constexpr (FINAL) {
+            const T *vblk = p.v + toff + (int64_t)k * b * dd;
+            gr.vt.fetch([=](int r) { return vblk + (int64_t)r * dd; }, kv, tid, dd);
+        }
     }
 
     __device__ static void stage(const HeadDims &, const Regs &gr, char *lds, int tid)
@@ -652,10 +654,8 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         if constexpr (LENS) {  // keys >= nl: zero (they are masked, zero keeps them finite)
             const int kv = gr.nl - gr.row0;
             gr.kt.template stage<LDK>(Ks, tid, kv);
-            if constexpr (FINAL) gr.vt.template stage<LDK>(Ks + NB * LDK, tid, kv);
         } else {
             gr.kt.template stage<LDK>(Ks, tid);
-            if constexpr (FINAL) gr.vt.template stage<LDK>(Ks + NB * LDK, tid);
         }
     }
 
@@ -743,6 +743,13 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         for (int r = 0; r < RT; ++r)  // alpha_L[j][k] (j-major)
             store_row<T, D>(jr[r] < b ? p.aL + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r], lane);
         if constexpr (FINAL) {
+            // Vbar[k], staged here rather than with K: when a workgroup runs a
+            // single unit, the scores and softmax overlap V's loads
+            if constexpr (LENS)
+                gr.vt.template stage<LDK>(Vs, tid, gr.nl - gr.row0);
+            else
+                gr.vt.template stage<LDK>(Vs, tid);
+            __syncthreads();
 #pragma unroll
             for (int vt = 0; vt < D / 16; ++vt) {
                 f32x4 acc[RT];
