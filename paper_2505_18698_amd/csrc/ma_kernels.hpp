@@ -743,8 +743,8 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         for (int r = 0; r < RT; ++r)  // alpha_L[j][k] (j-major)
             store_row<T, D>(jr[r] < b ? p.aL + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r], lane);
         if constexpr (FINAL) {
-            // Vbar[k], staged here rather than with K (1% faster at N=16384,
-            // where every workgroup loops over several units)
+            // Vbar[k], staged here rather than with K: when a workgroup runs a
+            // single unit, the scores and softmax overlap V's loads
             if constexpr (LENS)
                 gr.vt.template stage<LDK>(Vs, tid, gr.nl - gr.row0);
             else
