@@ -42,12 +42,12 @@ def _code(ma, dtype):
     return {"f32": ma.MA_F32, "bf16": ma.MA_BF16, "f16": ma.MA_F16}[dtype]
 
 
-def draw(ma, seed, max_np, max_t, check, max_mb=128, max_d=128, dtypes=("f32", "bf16", "f16")):
+def draw(ma, seed, max_np, max_t, check, max_mb=128, max_d=128, dtypes=("f32", "bf16", "f16"), min_mb=1):
     """(dtype, B, H, m, b, n, d, T, scale) for case `seed`: the first supported draw."""
     rs = np.random.RandomState(seed)
     while True:
         dtype = str(rs.choice(list(dtypes)))
-        m, b = int(rs.randint(1, max_mb + 1)), int(rs.randint(1, max_mb + 1))
+        m, b = int(rs.randint(min_mb, max_mb + 1)), int(rs.randint(min_mb, max_mb + 1))
         if m * b > max_np:
             continue
         n = int(rs.randint((m - 1) * b + 1, m * b + 1))
@@ -203,3 +203,66 @@ def test_random_objective(ma, case):
     print(f"  rel_frob={err:.3e} objective max rel err={rel:.3e}", flush=True)
     assert err <= FWD_TOL[dtype], (label, err)
     assert rel <= OBJ_TOL[dtype], (label, rel)
+
+
+def _lens(rs, B, n, b):
+    edges = [0, 1, n, max(0, n - 1), min(n, b), min(n, b + 1)]
+    return [int(rs.choice(edges)) if rs.rand() < 0.4 else int(rs.randint(0, n + 1)) for _ in range(B)]
+
+
+@pytest.mark.parametrize("case", range(24))
+def test_random_padded_batch_gradient(ma, case):
+    """monarch_attn_bwd_varlen against the autograd oracle of each real
+    sequence (reading 10b); rows past a length get exactly zero gradient."""
+    import torch
+
+    dtype, _, H, m, b, n, d, T, scale = draw(ma, 9700 + case, 1024, 3, ma.LIB.monarch_attn_bwd_check)
+    rs = np.random.RandomState(9800 + case)
+    B = int(rs.randint(2, 5))
+    lens = _lens(rs, B, n, b)
+    label = f"bwd varlen {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T} lens={lens}"
+    print(label, flush=True)
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=9700 + case, scale=scale)
+    g = si.random_cotangent((B, H, n, d), dtype, seed=9700 + case)
+    tq, tk, tv, tg = _to_dev((q, k, v, g), dtype)
+    outs = [torch.full_like(tq, float("nan")) for _ in range(3)]
+    ma.monarch_attn_bwd_varlen(tq, tk, tv, tg, *outs, torch.tensor(lens, dtype=torch.int32, device="cuda"), m, b, T)
+    torch.cuda.synchronize()
+    got = [x.double().cpu().numpy() for x in outs]
+    have, want = [[], [], []], [[], [], []]
+    for bi, ln in enumerate(lens):
+        for x in got:
+            assert np.isfinite(x).all(), label
+            assert np.all(x[bi, :, ln:] == 0.0), (label, bi)
+        for h in range(H):
+            ref = ob.autograd_grads(q[bi, h, :ln], k[bi, h, :ln], v[bi, h, :ln], g[bi, h, :ln], m, b, T,
+                                    batch_padding=True)
+            for c in range(3):
+                want[c].append(ref[c].ravel())
+                have[c].append(got[c][bi, h, :ln].ravel())
+    errs = [oracle.rel_frobenius(np.concatenate(x), np.concatenate(w)) if np.concatenate(w).size else 0.0
+            for x, w in zip(have, want)]
+    print(f"  rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
+    for name, e in zip(("dq", "dk", "dv"), errs):
+        assert e <= BWD_TOL[dtype], (label, name, e)
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_long_sequences(ma, case):
+    """m, b in 64..128 (N from 4033 to the headline's 16384), one batch element."""
+    import torch
+
+    dtype, _, H, m, b, n, d, T, scale = draw(ma, 9900 + case, 16384, 3, ma.monarch_attn_check, min_mb=64)
+    label = f"long {dtype} H{H} N{n} m{m} b{b} d{d} T{T} scale{scale}"
+    print(label, flush=True)
+    q, k, v = si.random_qkv(1, H, n, d, dtype, seed=9900 + case, scale=scale)
+    ref = oracle.monarch_attention(q, k, v, m, b, T)
+    tq, tk, tv = _to_dev((q, k, v), dtype)
+    out = torch.full_like(tq, float("nan"))
+    ma.monarch_attn_fwd(tq, tk, tv, out, m, b, T)
+    torch.cuda.synchronize()
+    o = out.double().cpu().numpy()
+    assert np.isfinite(o).all(), label
+    err = oracle.rel_frobenius(o, ref)
+    print(f"  rel_frob={err:.3e}", flush=True)
+    assert err <= FWD_TOL[dtype], (label, err)
