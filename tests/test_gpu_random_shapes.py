@@ -266,3 +266,101 @@ def test_random_long_sequences(ma, case):
     err = oracle.rel_frobenius(o, ref)
     print(f"  rel_frob={err:.3e}", flush=True)
     assert err <= FWD_TOL[dtype], (label, err)
+
+
+# Unit roundoff of the 16-bit element types (round to nearest).
+UNIT_ROUNDOFF = {"bf16": 2.0 ** -8, "f16": 2.0 ** -11}
+
+
+def sensitivity(fn, inputs, dtype, draws=4):
+    """How far the exact (fp64) result fn(*inputs) moves, relative-Frobenius,
+    when every input element is scaled by 1 + e, e uniform on [-u, u] with u
+    the element type's unit roundoff: the change one rounding of the inputs
+    causes, the largest over `draws` seeded draws (single draws scatter by 5x
+    at T = 32).  The path rounds its states to the element type at every
+    step, so where the T-step map amplifies such changes its error is of this
+    size whatever the arithmetic; for small T it is far below the 16-bit bars."""
+    u = UNIT_ROUNDOFF[dtype]
+    base = [np.asarray(x, dtype=np.float64) for x in inputs]
+    a = fn(*base)
+    worst = 0.0
+    for seed in range(draws):
+        rs = np.random.RandomState(seed)
+        c = fn(*[x * (1.0 + rs.uniform(-u, u, x.shape)) for x in base])
+        if isinstance(a, tuple):
+            worst = max(worst, max(oracle.rel_frobenius(ci, ai) for ci, ai in zip(c, a)))
+        else:
+            worst = max(worst, oracle.rel_frobenius(c, a))
+    return worst
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("path", ["auto", "half_steps"])
+@pytest.mark.parametrize("m,b,d", [(16, 16, 64), (24, 40, 48)])
+def test_maximum_step_count_forward(ma, dtype, path, m, b, d):
+    """T = 64, the largest the forward takes: 128 half-step launches (or one
+    fused launch), and the objective after every step."""
+    import torch
+
+    T = 64
+    n = m * b - 3
+    q, k, v = si.random_qkv(2, 2, n, d, dtype, seed=64 + m, scale=1.5)
+    ref_o, ref_f = oracle.monarch_attention_objective(q, k, v, m, b, T)
+    prev = ma.monarch_attn_set_path(ma.PATH_AUTO if path == "auto" else ma.PATH_HALF_STEPS)
+    try:
+        tq, tk, tv = _to_dev((q, k, v), dtype)
+        out = torch.full_like(tq, float("nan"))
+        ma.monarch_attn_fwd(tq, tk, tv, out, m, b, T)
+        out2 = torch.full_like(tq, float("nan"))
+        obj = torch.full((2, 2, T), float("nan"), dtype=torch.float32, device="cuda")
+        ma.monarch_attn_fwd_objective(tq, tk, tv, out2, obj, m, b, T)
+        torch.cuda.synchronize()
+    finally:
+        ma.monarch_attn_set_path(prev)
+    o, o2, f = (x.double().cpu().numpy() for x in (out, out2, obj))
+    assert torch.equal(out, out2)
+    err = oracle.rel_frobenius(o, ref_o)
+    rel = float(np.abs(f - ref_f).max() / np.abs(ref_f).max())
+    # at T = 64 the map is ill-conditioned: the 16-bit bar is the exact
+    # method's own movement under one rounding of its inputs, if larger
+    tol = FWD_TOL[dtype]
+    if dtype != "f32":
+        tol = max(tol, sensitivity(lambda a, c, e: oracle.monarch_attention(a, c, e, m, b, T), (q, k, v), dtype))
+    print(f"T=64 {path} {dtype} m{m} b{b} d{d}: rel_frob={err:.3e} (bar {tol:.3e}) objective={rel:.3e}", flush=True)
+    assert np.isfinite(o).all() and np.isfinite(f).all()
+    assert err <= tol and rel <= OBJ_TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_maximum_step_count_gradient(ma, dtype):
+    """T = 32, the largest the gradient takes (64 recompute and 64 sweep launches)."""
+    import torch
+
+    m, b, d, T = 8, 8, 32, 32
+    n = m * b - 5
+    q, k, v = si.random_qkv(1, 2, n, d, dtype, seed=32, scale=1.5)
+    g = si.random_cotangent((1, 2, n, d), dtype, seed=32)
+    tq, tk, tv, tg = _to_dev((q, k, v, g), dtype)
+    outs = [torch.full_like(tq, float("nan")) for _ in range(3)]
+    ma.monarch_attn_bwd(tq, tk, tv, tg, *outs, m, b, T)
+    torch.cuda.synchronize()
+    got = [x.double().cpu().numpy() for x in outs]
+    want = [np.zeros(q.shape) for _ in range(3)]
+    for h in range(2):
+        for w, r in zip(want, ob.autograd_grads(q[0, h], k[0, h], v[0, h], g[0, h], m, b, T)):
+            w[0, h] = r
+    errs = [oracle.rel_frobenius(x, w) for x, w in zip(got, want)]
+    tol = BWD_TOL[dtype]
+    if dtype != "f32":  # as in the forward test: the exact gradient's movement under one input rounding
+
+        def grads(a, c, e):
+            parts = [ob.autograd_grads(a[0, h], c[0, h], e[0, h], g[0, h], m, b, T) for h in range(2)]
+            return tuple(np.stack([p[i] for p in parts]) for i in range(3))
+
+        tol = max(tol, sensitivity(grads, (q, k, v), dtype))
+    print(f"T=32 gradient {dtype}: rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e} (bar {tol:.3e})",
+          flush=True)
+    for x in got:
+        assert np.isfinite(x).all()
+    for e in errs:
+        assert e <= tol
