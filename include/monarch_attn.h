@@ -31,7 +31,11 @@ extern "C" {
 
 /* Element types of q, k, v and out.  bf16/fp16 run the matrix products on
  * MFMA with fp32 accumulation; all softmax statistics and the normalisers
- * c_R, c_L are fp32.  fp32 runs fp32 MFMA throughout. */
+ * c_R, c_L are fp32.  fp32 runs fp32 MFMA throughout.  With 16-bit types
+ * the states are rounded to the element type at every step; over tens of
+ * steps the iteration can amplify that rounding as much as it amplifies one
+ * rounding of its inputs (to a few 1e-2 relative at T = 16-64 on random
+ * inputs), while for T of 1 to 4 the error stays near 5e-3. */
 typedef enum { MA_F32 = 0, MA_BF16 = 1, MA_F16 = 2 } ma_dtype;
 
 typedef enum {
