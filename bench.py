@@ -14,14 +14,26 @@ Timed regions (HIP events on the stream the library launches on):
      calls have run, so that the GPU has left its idle clocks.
   1. K steps back to back -> ms_per_step and value = B*H*N / time.
   2. K more steps with the library's per-launch events enabled -> the average
-     duration of each kernel; the one with the largest share of the step is
-     the "dominant kernel" whose algorithmic bytes and flops give `roofline`.
-     A pair of events adds a roughly fixed time to every launch it brackets
-     (about 2.5 us here), so each duration has the per-launch excess of the
-     event-read step over the step of region 1 taken off (launch_overhead_us;
-     the raw reading is kept as event_us).
+     duration of each kernel.  A pair of events adds a roughly fixed time to
+     every launch it brackets (about 2.5 us here), so each duration has the
+     per-launch excess of the event-read step over the step of region 1 taken
+     off (launch_overhead_us; the raw reading is kept as event_us).
 Inputs rotate over several copies (>= 512 MB in total) so that the 256 MB
 last-level cache cannot serve them from one step to the next.
+
+`roofline` is that of the whole call: the compulsory bytes 4 N d s per head
+(Q, K, V read once, O written once) over the call time against 8 TB/s, or
+the method's flops against the MFMA peak when those bound it.  `traffic` is
+the HBM bytes one call moves by the committed rocprofv3 counters (null once
+a kernel's sources changed since they were taken).  The dominant kernel
+(largest share of the step) is named beside it with its fraction on the
+bytes of the paper's state organisation (design IO), a secondary figure.
+
+The last line of stdout is one compact JSON record (< 4 KB): the headline,
+its roofline, the CPU baseline and a short line per extra workload.  The full
+record (per-kernel times, per-call distributions, hot and graph-replayed
+times, the sweep, the gradient, padded batches and quality) goes to the file
+named by --details.
 
 Each workload also reports the p10 / median / p90 of single calls (each
 between its own events), a "hot" time on one input set, and the time per call
@@ -33,19 +45,18 @@ fraction of the published one.
 
 sweep: the long-sequence points N = 256, 1024, 4096, 16384 (sqrt(N) x
 sqrt(N), d = 64 and 128, T = 2, 16 heads), with the call roofline and the
-dominant kernel of each; at d = 64 and the paper's quoted N it also times
-torch's fused scaled_dot_product_attention (flash or memory-efficient
-backend) on the same shape, as context beside the paper's own speed-ups over
-FlashAttention-2 on its hardware.
+dominant kernel of each.  With --sdpa, at d = 64 and the paper's quoted N it
+also times torch's fused scaled_dot_product_attention on the same shape, as
+context beside the paper's own speed-ups over FlashAttention-2 on its
+hardware (off by default: a comparison system, not part of the method).
 
 cpu_baseline: the fp64 C oracle, as it stands, on this host's cores, on the
-same workload (repeated whole forward passes, about 10-30 s in total).
+same workload (repeated whole forward passes, about 10-15 s in total).
 
 backward: monarch_attn_bwd (the gradient: forward recompute keeping every
 step's states, then the reverse sweep) timed the same way on the 4K speed
 point and ViT-B/16 with its class token, with its per-kernel durations and
-the roofline of its dominant gradient kernel.  Reported beside the headline,
-not in it.
+the roofline of its dominant gradient kernel.  In the details file only.
 
 varlen: monarch_attn_fwd_varlen and monarch_attn_bwd_varlen on a padded
 batch (RoBERTa-base shape at N = 384, b = 48, T = 1; lengths iid uniform on
@@ -723,6 +734,51 @@ def copy_sweep(torch, sizes_mb, steps, warmup):
         del src, dst
 
 
+def call_traffic(w, kernels):
+    """Measured HBM bytes of one call: the sum over its launches of the
+    committed rocprofv3 byte counters, or None unless every launch has a
+    record taken with its current sources."""
+    tot = 0
+    for k in kernels:
+        t = measured_traffic(k["kernel"], w.name)
+        if t is None:
+            return None
+        tot += t
+    return tot
+
+
+def headline_roofline(w, ms, kernels, peaks):
+    """The roofline of the call: the compulsory bytes 4 N d s per head (Q, K,
+    V in, O out) or the method's flops, whichever bounds it, over the call
+    time.  The dominant kernel's figure on the bytes of the paper's state
+    organisation (design IO) is kept beside it as a secondary field."""
+    compulsory, flops = call_work(w)
+    t = ms * 1e-3
+    t_hbm = compulsory / (HBM_PEAK_GBS * 1e9)
+    t_mfma = flops / (MFMA_PEAK_TFLOPS[w.dtype] * 1e12)
+    if t_hbm >= t_mfma:
+        achieved = compulsory / t / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        achieved = flops / t / 1e12
+        peak = MFMA_PEAK_TFLOPS[w.dtype]
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4)}
+    roof["traffic"] = call_traffic(w, kernels)
+    roof["scope"] = "call"
+    roof["alg_bytes"] = compulsory
+    roof["alg_flops"] = flops
+    if peaks:
+        key = "copy_GB_s" if roof["unit"] == "GB/s" else "gemm_bf16_TFLOP_s"
+        roof["frac_of_measured"] = round(roof["achieved"] / peaks[key], 4)
+    dom = max(kernels, key=lambda x: x["avg_us"])
+    dk = roofline_of(dom, w.dtype, w.name)
+    roof["dominant_kernel"] = {"kernel": dom["kernel"], "avg_us": dom["avg_us"], "launches": len(kernels),
+                               "design_io_frac": dk["frac"], "design_io_bound": dk["bound"]}
+    return roof
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -731,7 +787,7 @@ def main():
     ap.add_argument("--workload", default="speed_n16384")
     ap.add_argument("--d", type=int, default=None, help="override the head dimension")
     ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
-    ap.add_argument("--also", default="speed_n4096,speed_n4096_t3,vit_b16_n196,vit_b16_n197",
+    ap.add_argument("--also", default="speed_n4096,vit_b16_n196,speed_n4096_t3,vit_b16_n197",
                     help="comma-separated extra workloads ('' for none)")
     ap.add_argument("--backward", default="speed_n16384,speed_n4096,vit_b16_n197,sweep_n16384_d128",
                     help="comma-separated workloads for the gradient timing ('' for none)")
@@ -740,11 +796,15 @@ def main():
                     help="comma-separated workloads of the N / d sweep ('' for none)")
     ap.add_argument("--varlen", default="roberta_n384_b48",
                     help="comma-separated workloads timed as padded batches with per-sequence lengths ('' for none)")
-    ap.add_argument("--no-sdpa", action="store_true", help="skip the torch fused-attention context timing")
+    ap.add_argument("--sdpa", action="store_true",
+                    help="also time torch's fused attention on the sweep shapes (context only)")
     ap.add_argument("--no-measured-peaks", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-quality", action="store_true",
                     help="skip the approximation-quality figures (error against exact attention, objective gap)")
+    ap.add_argument("--details", default="bench_details.json",
+                    help="file for the full record (per-kernel times, sweep, gradient, padded batches, quality); "
+                         "'' for none")
     ap.add_argument("--copy-mb", type=str, default=None,
                     help="instead of the benchmark: time torch's device copy at these sizes (MB, comma "
                          "separated); the reference kernel for scaling HBM byte counters")
@@ -781,11 +841,42 @@ def main():
 
     peaks = measured_peaks(torch) if not args.no_measured_peaks else None
     ms, kernels, meta, nsets, extra = measure(ma, torch, w, args.steps, args.warmup)
-    share = [k["avg_us"] for k in kernels]
-    dom = kernels[share.index(max(share))]
     value = w.B * w.H * w.N / (ms * 1e-3)
-    cfg = w.describe()
-    cfg.update({"alpha": meta.get("alpha"), "rotating_input_sets": nsets})
+    cfg = {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "m": w.m, "b": w.b, "d": w.d, "T": w.T,
+           "inputs": w.recipe, "alpha": meta.get("alpha"), "rotating_input_sets": nsets}
+    roof = headline_roofline(w, ms, kernels, peaks)
+    details = {"headline": {"config": w.describe(), "ms_per_step": ms, "kernels": kernels, **extra,
+                            "roofline": roof, "call_roofline": call_roofline(w, ms)},
+               "measured_peaks": peaks}
+    also, also_short = [], []
+    for name in [x for x in args.also.split(",") if x]:
+        w2 = si.WORKLOADS[name]
+        ms2, kern2, meta2, nsets2, extra2 = measure(ma, torch, w2, args.steps, args.warmup)
+        r2 = headline_roofline(w2, ms2, kern2, peaks)
+        cfg2 = w2.describe()
+        cfg2.update({"alpha": meta2.get("alpha"), "rotating_input_sets": nsets2})
+        also.append({"config": cfg2, "value": round(w2.B * w2.H * w2.N / (ms2 * 1e-3), 1), "unit": UNIT,
+                     "ms_per_step": round(ms2, 6), "roofline": r2, "kernels": kern2, **extra2})
+        also_short.append({"workload": name, "value": round(w2.B * w2.H * w2.N / (ms2 * 1e-3), 1),
+                           "ms_per_step": round(ms2, 6), "roofline_frac": r2["frac"], "bound": r2["bound"]})
+    details["also"] = also
+    sweep = []
+    for name in [x for x in args.sweep.split(",") if x]:
+        w3 = si.WORKLOADS[name]
+        ms3, kern3, meta3, _, extra3 = measure(ma, torch, w3, args.steps, args.warmup)
+        rec = {"workload": name, "N": w3.N, "d": w3.d, "T": w3.T, "alpha": meta3.get("alpha"),
+               "value": round(w3.B * w3.H * w3.N / (ms3 * 1e-3), 1), "ms_per_step": round(ms3, 6),
+               "roofline": headline_roofline(w3, ms3, kern3, peaks), "kernels": kern3, **extra3}
+        if args.sdpa and w3.d == 64 and w3.N in PAPER_SPEEDUP_VS_FA2:
+            rec["context_vs_torch_sdpa"] = sdpa_context(ma, torch, w3, args.steps, args.warmup, ms3)
+        sweep.append(rec)
+    details["sweep"] = sweep
+    details["backward"] = [measure_backward(ma, torch, si.WORKLOADS[name], args.steps, args.warmup)
+                           for name in [x for x in args.backward.split(",") if x]]
+    details["varlen"] = [measure_varlen(ma, torch, si.WORKLOADS[name], args.steps, args.warmup)
+                         for name in [x for x in args.varlen.split(",") if x]]
+    if not args.no_quality:
+        details["quality"] = [quality(ma, torch, si.WORKLOADS[name]) for name in QUALITY_WORKLOADS]
     result = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -800,47 +891,19 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic",
         "config": cfg,
-        "roofline": with_measured(roofline_of(dom, w.dtype, w.name), peaks),
-        "call_roofline": call_roofline(w, ms),
-        "kernels": kernels,
-        **extra,
-        "measured_peaks": peaks,
+        "roofline": roof,
+        "also": also_short,
     }
-    also = []
-    for name in [x for x in args.also.split(",") if x]:
-        w2 = si.WORKLOADS[name]
-        ms2, kern2, meta2, nsets2, extra2 = measure(ma, torch, w2, args.steps, args.warmup)
-        sh2 = [k["avg_us"] for k in kern2]
-        dom2 = kern2[sh2.index(max(sh2))]
-        cfg2 = w2.describe()
-        cfg2.update({"alpha": meta2.get("alpha"), "rotating_input_sets": nsets2})
-        also.append({"config": cfg2, "value": round(w2.B * w2.H * w2.N / (ms2 * 1e-3), 1), "unit": UNIT,
-                     "ms_per_step": round(ms2, 6),
-                     "roofline": with_measured(roofline_of(dom2, w2.dtype, w2.name), peaks),
-                     "call_roofline": call_roofline(w2, ms2), "kernels": kern2, **extra2})
-    result["also"] = also
-    sweep = []
-    for name in [x for x in args.sweep.split(",") if x]:
-        w3 = si.WORKLOADS[name]
-        ms3, kern3, meta3, _, extra3 = measure(ma, torch, w3, args.steps, args.warmup)
-        dom3 = max(kern3, key=lambda x: x["avg_us"])
-        rec = {"workload": name, "N": w3.N, "d": w3.d, "T": w3.T, "alpha": meta3.get("alpha"),
-               "value": round(w3.B * w3.H * w3.N / (ms3 * 1e-3), 1), "ms_per_step": round(ms3, 6),
-               "call_roofline": call_roofline(w3, ms3), "dominant": dom3["kernel"],
-               "roofline": with_measured(roofline_of(dom3, w3.dtype, name), peaks), **extra3}
-        if not args.no_sdpa and w3.d == 64 and w3.N in PAPER_SPEEDUP_VS_FA2:
-            rec["context_vs_torch_sdpa"] = sdpa_context(ma, torch, w3, args.steps, args.warmup, ms3)
-        sweep.append(rec)
-    result["sweep"] = sweep
-    result["backward"] = [measure_backward(ma, torch, si.WORKLOADS[name], args.steps, args.warmup)
-                          for name in [x for x in args.backward.split(",") if x]]
-    result["varlen"] = [measure_varlen(ma, torch, si.WORKLOADS[name], args.steps, args.warmup)
-                        for name in [x for x in args.varlen.split(",") if x]]
-    if not args.no_quality:
-        result["quality"] = [quality(ma, torch, si.WORKLOADS[name]) for name in QUALITY_WORKLOADS]
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w)
-    print(json.dumps(result), flush=True)
+    if args.details:
+        details["result"] = result
+        with open(args.details, "w") as f:
+            json.dump(details, f, indent=1)
+        result["details"] = args.details
+    line = json.dumps(result, separators=(",", ":"))
+    assert len(line) < 4096, len(line)
+    print(line, flush=True)
 
 
 if __name__ == "__main__":

@@ -32,11 +32,18 @@ extern "C" {
 /* Element types of q, k, v and out.  bf16/fp16 run the matrix products on
  * MFMA with fp32 accumulation; all softmax statistics and the normalisers
  * c_R, c_L are fp32.  fp32 runs fp32 MFMA throughout.  With 16-bit types
- * the states are rounded to the element type at every step; over tens of
- * steps the iteration can amplify that rounding as much as it amplifies one
- * rounding of its inputs (to a few 1e-2 relative at T = 16-64 on random
- * inputs), while for T of 1 to 4 the error stays near 5e-3. */
+ * the states are rounded to the element type at every step, and over many
+ * steps the iteration amplifies that rounding as much as it amplifies one
+ * rounding of its inputs (a few 1e-2 relative at T = 16-64 on random
+ * inputs, near 5e-3 for T of 1 to 4).  16-bit calls therefore take at most
+ * MONARCH_ATTN_MAX_T_16BIT steps in the forward pass and
+ * MONARCH_ATTN_MAX_T_16BIT_BWD in the gradient, the counts up to which
+ * their 2e-2 (forward) and 3e-2 (gradient) relative accuracy has been
+ * validated; fp32 takes up to 64 (32 for the gradient). */
 typedef enum { MA_F32 = 0, MA_BF16 = 1, MA_F16 = 2 } ma_dtype;
+
+#define MONARCH_ATTN_MAX_T_16BIT 4
+#define MONARCH_ATTN_MAX_T_16BIT_BWD 4
 
 typedef enum {
     MA_OK = 0,
@@ -78,7 +85,9 @@ typedef enum {
  *           also needs tile(m)*D <= 8192 and tile(b)*D <= 8192, where
  *           tile(x) is the kernels' tile height for x rows: the smallest of
  *           16, 32, 64 and 128 that holds x.
- * T       : number of (R, L) update pairs, 1 <= T <= 64.
+ * T       : number of (R, L) update pairs, 1 <= T <= 64 for fp32 and
+ *           1 <= T <= MONARCH_ATTN_MAX_T_16BIT for bf16 and fp16 (larger T:
+ *           MA_EUNSUPPORTED).
  * dtype   : an ma_dtype value.
  * stream  : the hipStream_t to launch on (NULL = the null stream).
  *
@@ -199,7 +208,8 @@ int monarch_attn_exact_fwd(const void *q, const void *k, const void *v, void *ou
  *                 16-byte aligned, overlapping neither each other nor the
  *                 inputs.  Fully overwritten.  All owned by the caller.
  * B, H, N, d, m, b, T, dtype, stream : as monarch_attn_fwd, and in addition
- *                 T <= 32 (else MA_EUNSUPPORTED).
+ *                 T <= 32 for fp32 and T <= MONARCH_ATTN_MAX_T_16BIT_BWD
+ *                 for bf16 and fp16 (else MA_EUNSUPPORTED).
  *
  * Runs the forward half-steps again, keeping the states of every step, then
  * one launch per half-step in reverse order; all of it on `stream`,
@@ -247,6 +257,13 @@ size_t monarch_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t
 /* Text of the last failure on this thread ("" if none).  Valid until the next
  * call into the library from this thread. */
 const char *monarch_attn_last_error(void);
+
+/* Identifier of the sources the library was built from: the first 16 hex
+ * digits of a SHA-256 over the kernel, dispatch and C ABI sources and this
+ * header (paper_2505_18698_amd/build.py computes it).  A static string; makes
+ * no HIP call.  The Python binding refuses a library whose identifier does
+ * not match the sources beside it. */
+const char *monarch_attn_build_id(void);
 
 /* MA_OK if (N, d, m, b, T, dtype) is a supported shape, else MA_EINVAL or
  * MA_EUNSUPPORTED (with last_error set).  Makes no HIP call. */

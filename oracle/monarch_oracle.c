@@ -66,6 +66,16 @@
 #include <omp.h>
 #endif
 
+/* Index of the calling thread within the current parallel region (0 without OpenMP). */
+static int thread_index(void)
+{
+#ifdef _OPENMP
+    return omp_get_thread_num();
+#else
+    return 0;
+#endif
+}
+
 #define MO_OK 0
 #define MO_EINVAL 1
 #define MO_ENOMEM 4
@@ -238,9 +248,18 @@ static int forward(const double *q, const double *k, const double *v, double *ou
 #ifdef _OPENMP
     const int nt = threads > 0 ? threads : omp_get_max_threads(); /* this call only */
 #else
+    const int nt = 1;
     (void)threads;
 #endif
     const int64_t zlen = (m > b ? m : b);
+    /* per-thread scratch rows, allocated (and checked) before the parallel regions */
+    double *zbuf = malloc(sizeof(double) * (size_t)(nt * zlen));
+    double *hbuf = malloc(sizeof(double) * (size_t)(nt * m));
+    if (!zbuf || !hbuf) {
+        free(zbuf); free(hbuf);
+        free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
+        return MO_ENOMEM;
+    }
 
 #pragma omp parallel for schedule(static) num_threads(nt)
     for (int64_t h = 0; h < BH; ++h)
@@ -259,8 +278,8 @@ static int forward(const double *q, const double *k, const double *v, double *ou
         const int last = (t == T);
 #pragma omp parallel num_threads(nt)
         {
-            double *z = malloc(sizeof(double) * (size_t)zlen);
-            double *hl = malloc(sizeof(double) * (size_t)m);
+            double *z = zbuf + (size_t)thread_index() * (size_t)zlen;
+            double *hl = hbuf + (size_t)thread_index() * (size_t)m;
 #pragma omp for collapse(2) schedule(static)
             for (int64_t h = 0; h < BH; ++h)
                 for (int64_t kk = 0; kk < m; ++kk) {
@@ -275,8 +294,6 @@ static int forward(const double *q, const double *k, const double *v, double *ou
                     l_half_step(Qs + h * nd, aL + h * nd, cL + h * Np, Y + h * nd, aR + h * nd,
                                 cR + h * Np, last ? Op + h * nd : NULL, m, b, d, j,
                                 lens ? (lens[h / H] + b - 1) / b : m, z, obj ? fpart + h * b + j : NULL, hl);
-            free(z);
-            free(hl);
         }
         if (obj) {
             for (int64_t h = 0; h < BH; ++h) {
@@ -294,6 +311,7 @@ static int forward(const double *q, const double *k, const double *v, double *ou
         memset(out + h * N * d + n * d, 0, sizeof(double) * (size_t)((N - n) * d));
     }
     free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
+    free(zbuf); free(hbuf);
     return MO_OK;
 }
 
@@ -332,12 +350,15 @@ int ma_oracle_dense_attn_f64(const double *q, const double *k, const double *v, 
 #ifdef _OPENMP
     const int nt = threads > 0 ? threads : omp_get_max_threads(); /* this call only */
 #else
+    const int nt = 1;
     (void)threads;
 #endif
     const double s = 1.0 / sqrt((double)d);
+    double *zbuf = malloc(sizeof(double) * (size_t)nt * (size_t)N); /* one score row per thread */
+    if (!zbuf) return MO_ENOMEM;
 #pragma omp parallel num_threads(nt)
     {
-        double *z = malloc(sizeof(double) * (size_t)N);
+        double *z = zbuf + (size_t)thread_index() * (size_t)N;
 #pragma omp for collapse(2) schedule(static)
         for (int64_t h = 0; h < BH; ++h)
             for (int64_t r = 0; r < rows; ++r) {
@@ -362,8 +383,8 @@ int ma_oracle_dense_attn_f64(const double *q, const double *k, const double *v, 
                     for (int64_t e = 0; e < d; ++e) o[e] += w * vh[c * d + e];
                 }
             }
-        free(z);
     }
+    free(zbuf);
     return MO_OK;
 }
 

@@ -12,6 +12,8 @@ try:
         KIND_NAMES,
         LIB,
         LIB_PATH,
+        MAX_T_16BIT,
+        MAX_T_16BIT_BWD,
         MA_BF16,
         MA_EHIP,
         MA_EINVAL,
@@ -32,6 +34,7 @@ try:
         monarch_attn_bwd_varlen,
         monarch_attn_bwd_check,
         monarch_attn_bwd_workspace_bytes,
+        monarch_attn_build_id,
         monarch_attn_check,
         monarch_attn_fwd,
         monarch_attn_fwd_objective,

@@ -35,6 +35,7 @@ EXPORTS = (
     "monarch_attn_set_path",
     "monarch_attn_timing_enable",
     "monarch_attn_timing_read",
+    "monarch_attn_build_id",
 )
 
 
@@ -81,10 +82,39 @@ def _load() -> ctypes.CDLL:
     lib.monarch_attn_timing_enable.restype = ctypes.c_int
     lib.monarch_attn_timing_read.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32), i32]
     lib.monarch_attn_timing_read.restype = ctypes.c_int32
+    lib.monarch_attn_build_id.argtypes = []
+    lib.monarch_attn_build_id.restype = ctypes.c_char_p
+    _check_provenance(lib)
     return lib
 
 
+def _source_hash() -> str:
+    import importlib.util
+
+    spec = importlib.util.spec_from_file_location("_ma_build_hash", os.path.join(_PKG, "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod.source_hash()
+
+
+def _check_provenance(lib) -> None:
+    """Refuse a library built from other sources than the ones beside it."""
+    built = lib.monarch_attn_build_id().decode()
+    here = _source_hash()
+    if built != here:
+        raise ImportError(
+            f"{LIB_PATH} was built from sources {built}, but the sources here hash to {here}: "
+            "rebuild it (`python -m paper_2505_18698_amd.build`)")
+
+
+def monarch_attn_build_id() -> str:
+    """The source hash compiled into the library."""
+    return LIB.monarch_attn_build_id().decode()
+
+
 LIB = _load()
+MAX_T_16BIT = 4      # MONARCH_ATTN_MAX_T_16BIT
+MAX_T_16BIT_BWD = 4  # MONARCH_ATTN_MAX_T_16BIT_BWD
 
 
 def monarch_attn_last_error() -> str:

@@ -37,6 +37,27 @@ def sources() -> list[str]:
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+HEADER = os.path.join(ROOT, "include", "monarch_attn.h")
+
+
+def source_hash() -> str:
+    """First 16 hex digits of a SHA-256 over every file the library is built
+    from (csrc/*.hip, csrc/*.hpp and the C header), names and contents, in
+    name order.  Compiled into the library as monarch_attn_build_id(); the
+    binding compares the two at import."""
+    import hashlib
+
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.hpp"))) + [HEADER]
+    for path in files:
+        h.update(os.path.relpath(path, ROOT).encode())
+        h.update(b"\0")
+        with open(path, "rb") as f:
+            h.update(f.read())
+        h.update(b"\0")
+    return h.hexdigest()[:16]
+
+
 def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
     return res.returncode, res.stdout + res.stderr
@@ -44,12 +65,13 @@ def _run(cmd):
 
 def build(verbose: bool = False, extra_flags=()) -> str:
     cc = hipcc()
+    build_id = f'-DMA_BUILD_ID="{source_hash()}"'
     with tempfile.TemporaryDirectory(prefix="ma_build_") as tmp:
         objs, jobs = [], []
         for src in sources():
             obj = os.path.join(tmp, os.path.basename(src) + ".o")
             objs.append(obj)
-            jobs.append([cc, *FLAGS, *extra_flags, "-I", os.path.join(ROOT, "include"), "-c", src, "-o", obj])
+            jobs.append([cc, *FLAGS, build_id, *extra_flags, "-I", os.path.join(ROOT, "include"), "-c", src, "-o", obj])
         workers = min(len(jobs), max(1, min(8, os.cpu_count() or 1)))
         with concurrent.futures.ThreadPoolExecutor(workers) as ex:
             results = list(ex.map(_run, jobs))

@@ -222,6 +222,7 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
     ma::HeadDims hd{c.m, c.b, c.n, c.d, c.s_log2e, 0};
     hd.lens = B.lens;
     hd.H = (int)c.H;
+    hd.colnorm = 1;
     if (path == kFusedHead && !fused_applies(dtype, c.d, c.m, c.b))
         return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d <= 64 and m, b <= 16");
     int rc;

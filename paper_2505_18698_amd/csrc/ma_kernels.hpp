@@ -528,6 +528,10 @@ struct HeadDims {
     // rows (clamped to 0..n), or n when lens is null.
     const int *lens = nullptr;
     int H = 1;
+    // fp32 L half-step: store alpha_R and c_R of every (k, j) divided by the
+    // largest weight L[j][k][l] over l (see LHalf).  Off in the gradient's
+    // recompute, whose reverse sweep takes the unscaled states.
+    int colnorm = 0;
 };
 
 // Real rows of head bh.  The kernels read it in fetch() but use it only from
@@ -856,8 +860,17 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
                 for (int qq = 0; qq < 4; ++qq) sc[r][t][qq] = __builtin_fmaf(acc[r][qq], hd.s_log2e, -bias[qq]);
             }
         }
+        // fp32 with colnorm: the logits are kept, and P holds log2 L (below)
+        constexpr bool F32 = std::is_same<T, float>::value;
+        const bool logp = F32 && hd.colnorm;
+        f32x4 zk[F32 ? RT : 1][F32 ? NT : 1];
+        float lz[RT];
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
+            if constexpr (F32) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t) zk[r][t] = sc[r][t];
+            }
             const float mx = tiles_max<NT, RAGGED>(sc[r], mk, g);
             float sum = 0.f;
 #pragma unroll
@@ -875,6 +888,8 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
             const bool live = lr[r] < m && (!LENS || mk > 0);
             inv[r] = live ? fast_rcp(sum) : 0.f;
             lse[r] = live ? row_lse(mx, sum) : 0.f;
+            lz[r] = 0.f;  // log2 of the row normaliser (fp32)
+            if constexpr (F32) lz[r] = live ? mx + __builtin_amdgcn_logf(sum) : 0.f;
         }
         float *objs = cLs + NM;  // one objective share per wave
         if (p.obj_part) {
@@ -891,13 +906,28 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
             p.obj_part[(bh * hd.T + hd.t - 1) * b + j] = f;
         }
 
-        // P[l][k] (row-major, k contiguous) into the alpha_L space
+        // P[l][k] (row-major, k contiguous) into the alpha_L space: L[j][k][l],
+        // or with logp its log2 (kMasked where L is zero)
         using PT = typename std::conditional<std::is_same<T, float>::value, float, T>::type;
         PT *Ps = reinterpret_cast<PT *>(APs);
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
 #pragma unroll
-            for (int t = 0; t < NT; ++t) store4<PT>(Ps + lr[r] * LDP + 16 * t + 4 * g, sc[r][t] * inv[r]);
+            for (int t = 0; t < NT; ++t) {
+                if constexpr (F32) {
+                    if (logp) {
+                        f32x4 y;
+#pragma unroll
+                        for (int qq = 0; qq < 4; ++qq) {
+                            const bool on = inv[r] != 0.f && (!RAGGED || 16 * t + 4 * g + qq < mk);
+                            y[qq] = on ? zk[r][t][qq] - lz[r] : kMasked;
+                        }
+                        store4<PT>(Ps + lr[r] * LDP + 16 * t + 4 * g, y);
+                        continue;
+                    }
+                }
+                store4<PT>(Ps + lr[r] * LDP + 16 * t + 4 * g, sc[r][t] * inv[r]);
+            }
         }
         __syncthreads();
 
@@ -908,7 +938,29 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
         for (int r = 0; r < RT; ++r) {
             kr[r] = (wave * RT + r) * 16 + c16;
             pf[r].gather(Ps, LDP, (wave * RT + r) * 16, lane);
-            const f32x4 cs = gemm_colsum<T, NT>(pf[r]);  // c_R[k][j] = sum_l L[j][k][l]
+            if constexpr (F32) {
+                // Column k of L divided by its largest entry: w[l] = 2^(log2 L[j][k][l] - max_l log2 L),
+                // so c_R and alpha_R are the eq. beta_r sums times one positive factor per (k, j),
+                // which eq. R_update (beta_R / c_R) does not see.  The largest weight is 1, so a
+                // column whose weights all lie far below 1 keeps them instead of underflowing.
+                if (logp) {
+                    float mxc = kMasked;
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                        for (int qq = 0; qq < 4; ++qq) mxc = fmaxf(mxc, pf[r].p[t][qq]);
+                    }
+                    mxc = wave_xor_max<32>(wave_xor_max<16>(mxc));
+                    const bool any = mxc > 0.5f * kMasked;
+#pragma unroll
+                    for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                        for (int qq = 0; qq < 4; ++qq)
+                            pf[r].p[t][qq] = any ? __builtin_amdgcn_exp2f(pf[r].p[t][qq] - mxc) : 0.f;
+                    }
+                }
+            }
+            const f32x4 cs = gemm_colsum<T, NT>(pf[r]);  // c_R[k][j] = sum_l L[j][k][l] (times the factor)
             if (g == 0 && kr[r] < m) p.cR[bh * N + (int64_t)j * m + kr[r]] = cs[0];
         }
         f32x4 out[RT][D / 16];

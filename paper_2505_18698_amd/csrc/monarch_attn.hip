@@ -47,6 +47,10 @@ int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t d
                     (long long)b);
     if (T < 1) return fail(MA_EINVAL, "T must be >= 1 (got %d)", T);
     if (T > 64) return fail(MA_EUNSUPPORTED, "T > 64 is not supported (got %d)", T);
+    if (dtype != MA_F32 && T > MONARCH_ATTN_MAX_T_16BIT)
+        return fail(MA_EUNSUPPORTED,
+                    "bf16 and fp16 take T <= %d, the step count up to which their accuracy is validated (got %d)",
+                    MONARCH_ATTN_MAX_T_16BIT, T);
     if (m > 128 || b > 128) return fail(MA_EUNSUPPORTED, "m and b must be <= 128 (got m=%lld, b=%lld)", (long long)m, (long long)b);
     // rows of 16-byte multiples (so every row of q, k, v, out is 16-byte aligned), at most 128 wide
     if (d > 128 || d % (16 / (int64_t)elem_bytes(dtype)) != 0)
@@ -295,6 +299,11 @@ int check_bwd_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32
     const int rc = check_shape(N, d, m, b, T, dtype);
     if (rc != MA_OK) return rc;
     if (T > 32) return fail(MA_EUNSUPPORTED, "the gradient supports T <= 32 (got %d)", T);
+    if (dtype != MA_F32 && T > MONARCH_ATTN_MAX_T_16BIT_BWD)
+        return fail(MA_EUNSUPPORTED,
+                    "the gradient in bf16 and fp16 takes T <= %d, the step count up to which its accuracy is "
+                    "validated (got %d)",
+                    MONARCH_ATTN_MAX_T_16BIT_BWD, T);
     return MA_OK;
 }
 
@@ -397,9 +406,15 @@ int backward(const void *q, const void *k, const void *v, const void *dout, void
 
 }  // namespace
 
+#ifndef MA_BUILD_ID
+#error "MA_BUILD_ID (the source hash) is defined by paper_2505_18698_amd/build.py"
+#endif
+
 extern "C" {
 
 const char *monarch_attn_last_error(void) { return g_err; }
+
+const char *monarch_attn_build_id(void) { return MA_BUILD_ID; }
 
 int monarch_attn_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype)
 {

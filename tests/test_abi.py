@@ -104,6 +104,48 @@ def test_supported_shapes(shape, ok):
     assert (ma.monarch_attn_check(*shape) == 0) == ok
 
 
+@pytest.mark.parametrize("dtype", [1, 2])
+def test_step_count_cap_of_16bit_types(dtype):
+    """bf16 and fp16 take T up to the validated count (forward and gradient
+    apart); fp32 up to 64 (32 for the gradient)."""
+    import paper_2505_18698_amd as ma
+
+    t16, t16b = ma.MAX_T_16BIT, ma.MAX_T_16BIT_BWD
+    assert ma.monarch_attn_check(256, 64, 16, 16, t16, dtype) == 0
+    assert ma.monarch_attn_check(256, 64, 16, 16, t16 + 1, dtype) == ma.MA_EUNSUPPORTED
+    assert "validated" in ma.monarch_attn_last_error()
+    assert ma.monarch_attn_bwd_check(256, 64, 16, 16, t16b, dtype) == 0
+    assert ma.monarch_attn_bwd_check(256, 64, 16, 16, t16b + 1, dtype) == ma.MA_EUNSUPPORTED
+    assert ma.monarch_attn_check(256, 64, 16, 16, 64, 0) == 0
+    assert ma.monarch_attn_check(256, 64, 16, 16, 65, 0) == ma.MA_EUNSUPPORTED
+    assert ma.monarch_attn_bwd_check(256, 64, 16, 16, 32, 0) == 0
+    assert ma.monarch_attn_bwd_check(256, 64, 16, 16, 33, 0) == ma.MA_EUNSUPPORTED
+    rc = ma.monarch_attn_fwd_raw(FAKE, FAKE, FAKE, 2 * FAKE, 1, 1, 256, 64, 16, 16, t16 + 1, dtype, None)
+    assert rc == ma.MA_EUNSUPPORTED
+
+
+def test_step_count_caps_match_the_header():
+    import paper_2505_18698_amd as ma
+
+    text = open(HEADER).read()
+    assert re.search(r"#define MONARCH_ATTN_MAX_T_16BIT (\d+)", text).group(1) == str(ma.MAX_T_16BIT)
+    assert re.search(r"#define MONARCH_ATTN_MAX_T_16BIT_BWD (\d+)", text).group(1) == str(ma.MAX_T_16BIT_BWD)
+
+
+def test_build_id_matches_the_sources():
+    """The library carries the hash of the sources it was built from, and it
+    is that of the sources in the tree (the binding refuses it otherwise)."""
+    import importlib.util
+
+    import paper_2505_18698_amd as ma
+
+    spec = importlib.util.spec_from_file_location("_b", os.path.join(ROOT, "paper_2505_18698_amd", "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    assert ma.monarch_attn_build_id() == mod.source_hash()
+    assert re.fullmatch(r"[0-9a-f]{16}", ma.monarch_attn_build_id())
+
+
 def test_workspace_bytes_formula():
     import paper_2505_18698_amd as ma
 
@@ -112,7 +154,7 @@ def test_workspace_bytes_formula():
     state = B * H * N * d * 2   # alpha_R, alpha_L, Y
     cvec = B * H * N * 4        # c_R, c_L
     assert got == 3 * state + 2 * cvec
-    assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 20, 1) == got  # independent of T
+    assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 128, 4, 1) == got  # independent of T
     assert ma.monarch_attn_workspace_bytes(B, H, N, d, 128, 127, 2, 1) == 0
     # a padded sequence: the states cover m * b rows
     padded = ma.monarch_attn_workspace_bytes(1, 1, 197, 64, 15, 14, 2, 1)
@@ -228,8 +270,10 @@ def test_bwd_invalid_arguments_rejected_before_any_hip_call(args, code):
         ((197, 64, 15, 14, 2, 2), True),
         ((4096, 64, 64, 64, 2, 0), True),
         ((7, 8, 7, 1, 1, 1), True),
-        ((1024, 64, 32, 32, 32, 1), True),
-        ((1024, 64, 32, 32, 33, 1), False),
+        ((1024, 64, 32, 32, 32, 0), True),
+        ((1024, 64, 32, 32, 33, 0), False),
+        ((1024, 64, 32, 32, 4, 1), True),
+        ((1024, 64, 32, 32, 5, 1), False),       # bf16 gradient: T above its validated count
         ((16384, 64, 128, 128, 2, 1), True),
         ((8192, 64, 128, 64, 2, 1), True),
         ((384, 64, 3, 128, 1, 1), True),

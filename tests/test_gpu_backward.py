@@ -15,6 +15,7 @@ import pytest
 
 import oracle
 import oracle.backward as ob
+import parity
 import synth_inputs as si
 
 pytestmark = pytest.mark.gpu
@@ -361,7 +362,11 @@ def test_peaky_attention(ma, scale):
     torch.cuda.synchronize()
     o = out.double().cpu().numpy()
     assert np.isfinite(o).all()
-    assert oracle.rel_frobenius(o, oracle.monarch_attention(q, k, v, m, b, T)) <= 1e-4
+    ref_o = oracle.monarch_attention(q, k, v, m, b, T)
+    assert oracle.rel_frobenius(o, ref_o) <= 1e-5
+    # one class: the fp64 oracle moves a class by up to 7e-6 under one fp32
+    # ulp of these inputs at scale 4, against 1.5e-6 for the whole tensor
+    assert parity.worst_class(o, ref_o, b)[0] <= 5e-5
     got = gpu_grads(ma, q, k, v, dout, m, b, T, "f32")
     ref = oracle_grads(q, k, v, dout, m, b, T, [(0, 0), (0, 1)])
     errs = []
