@@ -122,6 +122,29 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out,
                      int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
 
 /*
+ * monarch_attn_fwd_noalloc -- monarch_attn_fwd for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same operation, arguments, kernels and
+ * results (bit for bit) as monarch_attn_fwd, but the states of the half-step
+ * path live in a scratch array that the library holds for the whole process
+ * on every device it runs on (MONARCH_ATTN_NOALLOC_SCRATCH_BYTES per device,
+ * set up by the first such call on that device), instead of the per-stream
+ * workspace.  The call makes no hipMalloc, hipFree or other allocating call.
+ *
+ * A call whose states need more than MONARCH_ATTN_NOALLOC_SCRATCH_BYTES
+ * (monarch_attn_workspace_bytes) returns MA_EUNSUPPORTED, launching nothing.
+ * All calls on one device share its one scratch array, and the array keeps
+ * the last call's contents: calls that can overlap on one device (different
+ * streams, or replays of captured graphs on different streams) race and must
+ * be ordered by the caller.  Nothing in the array needs to start at zero.
+ */
+int monarch_attn_fwd_noalloc(const void *q, const void *k, const void *v, void *out,
+                             int64_t B, int64_t H, int64_t N, int64_t d,
+                             int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
+
+#define MONARCH_ATTN_NOALLOC_SCRATCH_BYTES (64ull << 20)
+
+/*
  * monarch_attn_fwd_varlen -- monarch_attn_fwd over a batch of sequences of
  * different lengths, each post-padded to N rows (Appendix "Padding and
  * Masking", which names batched sequences padded to a maximum length as the

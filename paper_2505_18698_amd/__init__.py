@@ -14,6 +14,7 @@ try:
         LIB_PATH,
         MAX_T_16BIT,
         MAX_T_16BIT_BWD,
+        NOALLOC_SCRATCH_BYTES,
         MA_BF16,
         MA_EHIP,
         MA_EINVAL,
@@ -37,6 +38,7 @@ try:
         monarch_attn_build_id,
         monarch_attn_check,
         monarch_attn_fwd,
+        monarch_attn_fwd_noalloc,
         monarch_attn_fwd_objective,
         monarch_attn_fwd_varlen,
         monarch_attn_exact_fwd,

@@ -36,6 +36,7 @@ EXPORTS = (
     "monarch_attn_timing_enable",
     "monarch_attn_timing_read",
     "monarch_attn_build_id",
+    "monarch_attn_fwd_noalloc",
 )
 
 
@@ -82,6 +83,8 @@ def _load() -> ctypes.CDLL:
     lib.monarch_attn_timing_enable.restype = ctypes.c_int
     lib.monarch_attn_timing_read.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32), i32]
     lib.monarch_attn_timing_read.restype = ctypes.c_int32
+    lib.monarch_attn_fwd_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
+    lib.monarch_attn_fwd_noalloc.restype = ctypes.c_int
     lib.monarch_attn_build_id.argtypes = []
     lib.monarch_attn_build_id.restype = ctypes.c_char_p
     _check_provenance(lib)
@@ -202,6 +205,23 @@ def monarch_attn_fwd(q, k, v, out, m: int, b: int, T: int, stream=None):
     with _OnDevice(q):
         _check(monarch_attn_fwd_raw(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                     B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # MONARCH_ATTN_NOALLOC_SCRATCH_BYTES
+
+
+def monarch_attn_fwd_noalloc(q, k, v, out, m: int, b: int, T: int, stream=None):
+    """monarch_attn_fwd without any device allocation: the states go to the
+    library's per-device scratch array (NOALLOC_SCRATCH_BYTES; larger calls
+    raise MA_EUNSUPPORTED).  Calls that can overlap on one device race on that
+    array.  Returns `out`."""
+    _check_tensors(q, k, v, out)
+    B, H, N, d = q.shape
+    stream = _stream(q, stream)
+    with _OnDevice(q):
+        _check(LIB.monarch_attn_fwd_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                            B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
     return out
 
 

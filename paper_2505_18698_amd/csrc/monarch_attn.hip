@@ -98,7 +98,14 @@ struct Workspace {
     std::vector<void *> retired;
 };
 
+// The scratch of monarch_attn_fwd_noalloc: the states of the half-step path,
+// one array per device for the life of the process.  In host code `scratch`
+// names a host-side stand-in: its device address comes from
+// hipGetSymbolAddress (Device::scratch), once per device.
+static __device__ __align__(256) unsigned char scratch[MONARCH_ATTN_NOALLOC_SCRATCH_BYTES];
+
 struct Device {
+    void *scratch = nullptr;  // device address of `scratch` on this device (null: not looked up yet)
     int num_cus = 0;  // 0: not queried yet
     // Entries are never erased (a caller may be waiting on an entry's mutex);
     // release only frees their memory.
@@ -140,6 +147,25 @@ int current_device(int &dev, int &num_cus)
         D.num_cus = n;
     }
     num_cus = D.num_cus;
+    return MA_OK;
+}
+
+// The device address of the no-allocation scratch on device `dev` (the
+// current device), looked up on its first use there.
+int noalloc_scratch(int dev, char **base)
+{
+    std::lock_guard<std::mutex> lock(g_dev_mutex);
+    Device &D = g_dev[dev];
+    if (!D.scratch) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return fail(MA_EHIP, "hipGetSymbolAddress of the scratch array failed: %s", hipGetErrorString(e));
+        }
+        D.scratch = p;
+    }
+    *base = (char *)D.scratch;
     return MA_OK;
 }
 
@@ -212,9 +238,11 @@ int check_capture(hipStream_t stream, bool &capturing)
 
 // The forward pass; with obj != nullptr also the objective per (head, step);
 // with need_lens, per-sequence lengths lens[B] (device).
+// noalloc: the states go to the scratch array instead of the stream's
+// workspace (no objective, no lengths).
 int forward(const void *q, const void *k, const void *v, void *out, float *obj, bool need_obj, const int32_t *lens,
             bool need_lens, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
-            void *stream)
+            void *stream, bool noalloc = false)
 {
     g_err[0] = '\0';
     if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
@@ -255,9 +283,17 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     if (states || obj) {
         const size_t state_ws = states ? workspace_bytes(BH, m * b, d, dtype) : 0;
         char *base = nullptr;
-        if ((rc = acquire_workspace(dev, (hipStream_t)stream, capturing, state_ws + obj_part_bytes, &base,
-                                    ws_hold)) != MA_OK)
+        if (noalloc) {
+            if (state_ws + obj_part_bytes > MONARCH_ATTN_NOALLOC_SCRATCH_BYTES)
+                return fail(MA_EUNSUPPORTED,
+                            "the states of this call take %zu bytes, more than the %llu bytes of the no-allocation "
+                            "scratch",
+                            state_ws + obj_part_bytes, (unsigned long long)MONARCH_ATTN_NOALLOC_SCRATCH_BYTES);
+            if ((rc = noalloc_scratch(dev, &base)) != MA_OK) return rc;
+        } else if ((rc = acquire_workspace(dev, (hipStream_t)stream, capturing, state_ws + obj_part_bytes, &base,
+                                           ws_hold)) != MA_OK) {
             return rc;
+        }
         if (states) {
             bufs.aR = base;
             bufs.aL = base + st;
@@ -511,6 +547,12 @@ int monarch_attn_fwd(const void *q, const void *k, const void *v, void *out, int
                      int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
 {
     return forward(q, k, v, out, nullptr, false, nullptr, false, B, H, N, d, m, b, T, dtype, stream);
+}
+
+int monarch_attn_fwd_noalloc(const void *q, const void *k, const void *v, void *out, int64_t B, int64_t H, int64_t N,
+                             int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
+{
+    return forward(q, k, v, out, nullptr, false, nullptr, false, B, H, N, d, m, b, T, dtype, stream, true);
 }
 
 int monarch_attn_fwd_varlen(const void *q, const void *k, const void *v, void *out, const int32_t *lens, int64_t B,

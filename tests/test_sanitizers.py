@@ -4,7 +4,7 @@
   shapes (rectangular, post-padded, batch-padded with lengths 0, 1 and whole
   blocks of padding, the objective, exact attention) and its argument
   checks, OpenMP on, leak checking on.
-* The C ABI's host code (monarch_attn.hip compiled for the host only) with
+* The C ABI's host code (monarch_attn.hip, sanitizers on its host pass) with
   tests/sanitize/abi_main.cpp, which stands in for the dispatch units: the
   argument checks of every entry point, the shape queries and workspace
   sizes, head counts at and beyond the grid limit, and the empty calls.  No
@@ -41,13 +41,14 @@ def test_oracle_under_asan_ubsan(tmp_path):
 
 @pytest.mark.skipif(not os.path.exists(HIPCC), reason="hipcc not found")
 def test_abi_host_code_under_asan_ubsan(tmp_path):
-    # host-only compilation: every sanitizer flag applies to the host pass only
-    common = [HIPCC, "--offload-arch=gfx950", "--cuda-host-only", "-O1", "-g", "-std=c++17",
+    # every sanitizer flag applies to the host pass only (the device pass holds
+    # only the scratch array of the no-allocation entry point)
+    common = [HIPCC, "--offload-arch=gfx950", "-O1", "-g", "-std=c++17",
               "-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host", "-fno-sanitize-recover=all",
               "-fno-omit-frame-pointer", '-DMA_BUILD_ID="0123456789abcdef"', "-I", os.path.join(ROOT, "include")]
     abi_o, main_o, exe = (str(tmp_path / x) for x in ("abi.o", "main.o", "abi_san"))
     _run(common + ["-c", os.path.join(ROOT, "paper_2505_18698_amd", "csrc", "monarch_attn.hip"), "-o", abi_o])
-    _run(common + ["-x", "hip", "-c", os.path.join(SAN, "abi_main.cpp"), "-o", main_o])
+    _run(common + ["--cuda-host-only", "-x", "hip", "-c", os.path.join(SAN, "abi_main.cpp"), "-o", main_o])
     _run([HIPCC, "--offload-arch=gfx950", "-Xarch_host", "-fsanitize=address,undefined", abi_o, main_o, "-o", exe])
     # the HIP runtime keeps allocations of its own to the end of the process: no leak check here
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=0:abort_on_error=1")
