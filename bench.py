@@ -127,11 +127,11 @@ def launch_plan(w):
 
 def plan_for(w, kinds):
     """Launch plan matching the kernels one call actually ran."""
-    if kinds == ["monarch_fused_head"]:
+    if kinds in (["monarch_fused_head"], ["monarch_fused_group"]):
         # one launch for the whole pass: its algorithmic traffic is the compulsory
         # Q, K, V in and O out (the states stay in LDS)
         compulsory, flops = call_work(w)
-        return [("monarch_fused_head", compulsory, flops)]
+        return [(kinds[0], compulsory, flops)]
     plan = launch_plan(w)
     assert kinds == [p[0] for p in plan], (kinds, plan)
     return plan

@@ -111,7 +111,11 @@ typedef enum {
  * otherwise the call fails with MA_EUNSUPPORTED and records nothing.  A
  * buffer that a captured call used is never freed when a later call grows
  * that workspace, only by monarch_attn_release_workspace, so captured graphs
- * stay valid until then.  Capture with per-launch timing enabled fails with
+ * stay valid until then.  The first call on that stream not under capture
+ * after a capture moves the stream to a fresh buffer, so eager calls never
+ * share one with a graph.  All graphs captured on one stream between two
+ * eager calls share one buffer: such graphs must not be replayed at the
+ * same time (on different streams) as each other.  Capture with per-launch timing enabled fails with
  * MA_EUNSUPPORTED.  The same holds for every entry point that takes a
  * stream.
  * The message of the last failure on the calling thread is returned by
@@ -307,7 +311,7 @@ int monarch_attn_release_workspace(void);
 /*
  * Execution path of monarch_attn_fwd (process-wide; returns the previous
  * value, or -1 on an unknown value):
- *   0  automatic (default): path 2 where it applies, else path 1;
+ *   0  automatic (default), see below;
  *   1  one launch per half-step (the state form of the paper's
  *      Implementation paragraph, the states crossing launches through the
  *      workspace);
@@ -316,7 +320,16 @@ int monarch_attn_release_workspace(void);
  *      sequences, Sec. 4, paragraph "Benchmarking"): bf16 or fp16, d <= 64,
  *      m <= 16 and b <= 16; any other shape returns MA_EUNSUPPORTED.  Uses
  *      no workspace.
- * Both paths compute the same operation with the same per-unit arithmetic.
+ *   3  one workgroup per (batch, head, group of residue classes j) running
+ *      every step in one launch with the states of its classes in LDS (the
+ *      classes of a head are independent given K and V): bf16 or fp16,
+ *      d <= 64, m <= 64 and b <= 64, in monarch_attn_fwd and
+ *      monarch_attn_fwd_noalloc only (not with per-sequence lengths or the
+ *      objective); any other call returns MA_EUNSUPPORTED.  Uses no
+ *      workspace.
+ * Automatic selection takes path 2 where it applies, else path 1 (path 3
+ * only when asked for).  All paths compute the same operation with the same
+ * per-unit arithmetic, and give the same bits.
  */
 int monarch_attn_set_path(int32_t path);
 
@@ -331,8 +344,8 @@ int monarch_attn_set_path(int32_t path);
  * 3 last L half-step with the Monarch product and the store of O,
  * 4 the one-workgroup-per-head kernel, 5 the sum of the objective shares,
  * 6 exact attention, 7 an L half-step of the gradient, 8 an R half-step of
- * the gradient); it returns the number of launches of that call, or -1 on
- * error.
+ * the gradient, 9 the one-workgroup-per-group-of-classes kernel); it returns
+ * the number of launches of that call, or -1 on error.
  */
 int monarch_attn_timing_enable(int32_t flag);
 int32_t monarch_attn_timing_read(float *ms, int32_t *kind, int32_t cap);

@@ -26,9 +26,11 @@ try:
         PATH_AUTO,
         PATH_HALF_STEPS,
         PATH_FUSED,
+        PATH_GROUPED,
         MonarchAttnError,
         dtype_code,
         fused_applies,
+        grouped_applies,
         monarch_attention,
         monarch_attention_autograd,
         monarch_attn_bwd,

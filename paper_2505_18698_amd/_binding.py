@@ -15,8 +15,9 @@ MA_F32, MA_BF16, MA_F16 = 0, 1, 2
 MA_OK, MA_EINVAL, MA_EUNSUPPORTED, MA_EHIP, MA_ENOMEM = 0, 1, 2, 3, 4
 STATUS_NAMES = {0: "MA_OK", 1: "MA_EINVAL", 2: "MA_EUNSUPPORTED", 3: "MA_EHIP", 4: "MA_ENOMEM"}
 KIND_NAMES = {0: "r_half_step", 1: "l_half_step", 2: "r_half_step_final", 3: "monarch_apply",
-              4: "monarch_fused_head", 5: "objective_sum", 6: "exact_attention", 7: "l_bwd", 8: "r_bwd"}
-PATH_AUTO, PATH_HALF_STEPS, PATH_FUSED = 0, 1, 2
+              4: "monarch_fused_head", 5: "objective_sum", 6: "exact_attention", 7: "l_bwd", 8: "r_bwd",
+              9: "monarch_fused_group"}
+PATH_AUTO, PATH_HALF_STEPS, PATH_FUSED, PATH_GROUPED = 0, 1, 2, 3
 
 # Every symbol declared in include/monarch_attn.h.
 EXPORTS = (
@@ -386,8 +387,14 @@ def monarch_attn_check(N: int, d: int, m: int, b: int, T: int, dtype: int) -> in
 
 
 def fused_applies(d: int, m: int, b: int, dtype: int) -> bool:
-    """Whether the one-workgroup-per-head kernel covers this shape (PATH_AUTO takes it then)."""
+    """Whether the one-workgroup-per-head kernel covers this shape."""
     return dtype in (MA_BF16, MA_F16) and d <= 64 and m <= 16 and b <= 16
+
+
+def grouped_applies(d: int, m: int, b: int, dtype: int) -> bool:
+    """Whether the one-workgroup-per-(head, group of classes) kernel (PATH_GROUPED)
+    covers this shape (without per-sequence lengths or the objective)."""
+    return dtype in (MA_BF16, MA_F16) and d <= 64 and m <= 64 and b <= 64
 
 
 def monarch_attn_workspace_bytes(B, H, N, d, m, b, T, dtype) -> int:

@@ -16,6 +16,7 @@
 #include <type_traits>
 #include <unordered_map>
 
+#include "grouped.hpp"
 #include "host_common.hpp"
 #include "ma_kernels.hpp"
 
@@ -193,6 +194,109 @@ template <typename T> int run_fused(Launcher &L, const CallBufs &B, ma::HeadDims
     }
 }
 
+// ---- one workgroup per (head, group of residue classes) ----
+
+// Workgroups of `kern` resident per CU at `lds` bytes of dynamic LDS, with
+// the kernel allowed that much LDS (set once per kernel).
+inline int resident_per_cu_lds(const void *kern, int threads, int lds)
+{
+    static std::mutex mu;
+    static std::unordered_map<const void *, int> attr;                // LDS bytes allowed so far
+    static std::unordered_map<uint64_t, int> cache;                    // (kernel, lds) -> workgroups
+    std::lock_guard<std::mutex> lock(mu);
+    int &allowed = attr[kern];
+    if (allowed < lds) {
+        if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) {
+            (void)hipGetLastError();
+            return 0;
+        }
+        allowed = lds;
+    }
+    const uint64_t key = (uint64_t)(uintptr_t)kern * 1000003u + (uint64_t)lds;
+    auto it = cache.find(key);
+    if (it != cache.end()) return it->second;
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kern, threads, lds) != hipSuccess) {
+        (void)hipGetLastError();
+        n = 0;
+    }
+    cache.emplace(key, n);
+    return n;
+}
+
+constexpr int kMaxLds = 160 * 1024;
+
+// Classes per workgroup: the largest G (at most 16 and at most b) whose LDS
+// fits and that still gives every compute unit a workgroup; else the
+// smallest that fits.
+template <typename U> int group_size(int64_t BH, int b, int num_cus)
+{
+    const int cand[5] = {16, 8, 4, 2, 1};
+    int best = 0;
+    for (int i = 0; i < 5; ++i) {
+        const int G = cand[i] < b ? cand[i] : b;
+        if (U::lds_bytes(G) > kMaxLds) continue;
+        best = G;
+        if (BH * ((b + G - 1) / G) >= num_cus) return G;
+    }
+    return best;
+}
+
+template <typename T, int NB, int NM, bool RG>
+int launch_group(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
+{
+    using U = ma::FusedGroup<T, NB, NM, 64, RG>;
+    auto kern = ma::monarch_fused_group<T, NB, NM, 64, RG>;
+    const int G = group_size<U>(c.BH, c.b, c.num_cus);
+    if (G < 1) return fail(MA_EUNSUPPORTED, "the grouped kernel's LDS does not fit");
+    const int lds = U::lds_bytes(G);
+    const int per_cu = resident_per_cu_lds((const void *)kern, U::NTH, lds);
+    if (per_cu < 1) return fail(MA_EUNSUPPORTED, "the grouped kernel cannot be resident with %d bytes of LDS", lds);
+    const int groups = (c.b + G - 1) / G;
+    const int64_t units = c.BH * groups;
+    if (units > 0x7fffffff) return fail(MA_EUNSUPPORTED, "too many units for one grid");
+    const int64_t cap = (int64_t)per_cu * c.num_cus;
+    const int64_t grid = units < cap ? units : cap;
+    const int xcd_perm = units % 8 == 0 ? 1 : 0;
+    hd.units = units;
+    const ma::Bufs<T> p = typed<T>(B);
+    const int T_ = c.T;
+    return L.run(kGroup, [&] {
+        return launched([&] {
+            hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(U::NTH), (unsigned)lds, L.stream, p, hd, G, groups,
+                               units, xcd_perm, T_);
+        });
+    });
+}
+
+template <typename T, int NB, int NM> int dispatch_group_rg(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
+{
+    const bool rg = c.b != NB || c.m != NM || c.n != c.m * c.b;
+    return rg ? launch_group<T, NB, NM, true>(L, B, hd, c) : launch_group<T, NB, NM, false>(L, B, hd, c);
+}
+
+template <typename T, int NB> int dispatch_group_m(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
+{
+    switch (tile_rows(c.m)) {
+    case 16: return dispatch_group_rg<T, NB, 16>(L, B, hd, c);
+    case 32: return dispatch_group_rg<T, NB, 32>(L, B, hd, c);
+    default: return dispatch_group_rg<T, NB, 64>(L, B, hd, c);
+    }
+}
+
+template <typename T> int run_group(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
+{
+    if constexpr (sizeof(T) != 2) {
+        return fail(MA_EUNSUPPORTED, "the grouped kernel needs 16-bit elements");
+    } else {
+        switch (tile_rows(c.b)) {
+        case 16: return dispatch_group_m<T, 16>(L, B, hd, c);
+        case 32: return dispatch_group_m<T, 32>(L, B, hd, c);
+        default: return dispatch_group_m<T, 64>(L, B, hd, c);
+        }
+    }
+}
+
 template <typename T, int D> int launch_exact(Launcher &L, const CallBufs &B, float *lse, int64_t BH, int n, int d)
 {
     const ma::Bufs<T> p = typed<T>(B);
@@ -223,11 +327,17 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
     hd.lens = B.lens;
     hd.H = (int)c.H;
     hd.colnorm = 1;
-    if (path == kFusedHead && !fused_applies(dtype, c.d, c.m, c.b))
-        return fail(MA_EUNSUPPORTED, "the fused kernel needs bf16/fp16, d <= 64 and m, b <= 16");
+    const int fam = family_of(path, dtype, c.d, c.m, c.b, B.lens != nullptr, B.obj != nullptr);
+    if (fam == kFamNone)
+        return fail(MA_EUNSUPPORTED, path == kFusedHead
+                                         ? "the one-workgroup-per-head kernel needs bf16/fp16, d <= 64 and m, b <= 16"
+                                         : "the grouped kernel needs bf16/fp16, d <= 64, m, b <= 64, no lengths and "
+                                           "no objective");
     int rc;
-    if (uses_fused(path, dtype, c.d, c.m, c.b)) {
+    if (fam == kFamFused) {
         rc = run_fused<T>(L, B, hd, c);
+    } else if (fam == kFamGroup) {
+        rc = run_group<T>(L, B, hd, c);
     } else {
         switch (tile_d(c.d)) {
         case 64: rc = run_half_steps<T, 64>(L, B, hd, c); break;

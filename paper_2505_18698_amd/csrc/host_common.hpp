@@ -23,7 +23,8 @@ inline int tile_rows(int64_t n)
 }
 
 // Kernel kinds reported by the timing interface.
-enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4, kObjSum = 5, kExact = 6, kBwdL = 7, kBwdR = 8 };
+enum Kind { kR = 0, kL = 1, kRFinal = 2, kApply = 3, kFused = 4, kObjSum = 5, kExact = 6, kBwdL = 7, kBwdR = 8,
+            kGroup = 9 };
 
 // Per-launch HIP events around every kernel when timing is enabled.
 constexpr int kMaxLaunches = 2 * 64 + 2;
@@ -79,10 +80,13 @@ struct CallDims {
     int num_cus;  // compute units of the device
 };
 
-// Path selection (monarch_attn_set_path): 0 = the fused kernel for small
-// heads when it applies, else one launch per half-step; 1 = one launch per
-// half-step; 2 = the fused kernel or MA_EUNSUPPORTED.
-enum Path { kAuto = 0, kHalfSteps = 1, kFusedHead = 2 };
+// Path selection (monarch_attn_set_path): 0 = automatic; 1 = one launch per
+// half-step; 2 = one workgroup per head (or MA_EUNSUPPORTED); 3 = one
+// workgroup per (head, group of residue classes) (or MA_EUNSUPPORTED).
+enum Path { kAuto = 0, kHalfSteps = 1, kFusedHead = 2, kGrouped = 3 };
+
+// The kernel family that runs a forward call.
+enum Family { kFamHalf = 0, kFamFused = 1, kFamGroup = 2, kFamNone = -1 };
 
 // Tile width of the kernels for head dimension d (columns d..D-1 are zero).
 inline int tile_d(int64_t d) { return d <= 64 ? 64 : d <= 96 ? 96 : 128; }
@@ -94,10 +98,26 @@ inline bool fused_applies(int32_t dtype, int64_t d, int64_t m, int64_t b)
     return (dtype == MA_BF16 || dtype == MA_F16) && d <= 64 && m <= 16 && b <= 16;
 }
 
-// Whether a call with these arguments runs the fused kernel under `path`.
-inline bool uses_fused(int path, int32_t dtype, int64_t d, int64_t m, int64_t b)
+// The one-workgroup-per-(head, group of classes) kernel keeps the states of
+// its classes in LDS: 16-bit elements, d <= 64, m and b at most 64, and
+// neither per-sequence lengths nor the objective.
+inline bool grouped_applies(int32_t dtype, int64_t d, int64_t m, int64_t b, bool lens, bool obj)
 {
-    return path != kHalfSteps && fused_applies(dtype, d, m, b);
+    return (dtype == MA_BF16 || dtype == MA_F16) && d <= 64 && m <= 64 && b <= 64 && !lens && !obj;
+}
+
+// The family that runs a call under `path` (kFamNone: the forced path does
+// not take the shape).  Automatic: the one-workgroup-per-head kernel where it
+// applies, else the half-steps (the grouped kernel is slower than both on
+// every measured shape, so it runs only when asked for).
+inline int family_of(int path, int32_t dtype, int64_t d, int64_t m, int64_t b, bool lens, bool obj)
+{
+    switch (path) {
+    case kHalfSteps: return kFamHalf;
+    case kFusedHead: return fused_applies(dtype, d, m, b) ? kFamFused : kFamNone;
+    case kGrouped: return grouped_applies(dtype, d, m, b, lens, obj) ? kFamGroup : kFamNone;
+    default: return fused_applies(dtype, d, m, b) ? kFamFused : kFamHalf;
+    }
 }
 
 // Enqueue the whole forward pass for one element type (defined per dtype).

@@ -185,7 +185,9 @@ int stream_capturing(hipStream_t stream, bool &capturing)
 // with hipMalloc to at least `need` bytes.  Growing first waits for the
 // stream, whose earlier calls may still use the old buffer.  A stream under
 // graph capture cannot allocate or wait: its workspace must already be
-// large enough.
+// large enough.  The first call not under capture after a capture moves to a
+// fresh buffer: a graph replays on whatever stream its caller picks, so it
+// must not share its buffer with the eager calls on the capture stream.
 int acquire_workspace(int dev, hipStream_t stream, bool capturing, size_t need, char **base,
                       std::unique_lock<std::mutex> &hold)
 {
@@ -197,12 +199,13 @@ int acquire_workspace(int dev, hipStream_t stream, bool capturing, size_t need, 
         w = slot.get();
     }
     hold = std::unique_lock<std::mutex>(w->mu);
-    if (w->bytes < need) {
+    if (w->bytes < need || (w->captured && !capturing)) {
         if (capturing)
             return fail(MA_EUNSUPPORTED,
                         "the stream is being captured and its workspace holds %zu of the %zu bytes this call needs: "
                         "make a call of this size on the stream before capturing",
                         w->bytes, need);
+        if (w->bytes > need) need = w->bytes;  // a move off a captured buffer keeps its size
         if (w->ptr) {
             if (w->captured) {
                 w->retired.push_back(w->ptr);  // a captured graph may still use it
@@ -278,7 +281,8 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     bool capturing = false;
     if ((rc = check_capture((hipStream_t)stream, capturing)) != MA_OK) return rc;
     std::unique_lock<std::mutex> ws_hold;  // the stream's workspace, held until the launches are enqueued
-    const bool states = !uses_fused(path, dtype, d, m, b);  // the fused kernel keeps its states in LDS
+    const int fam = family_of(path, dtype, d, m, b, need_lens, need_obj);
+    const bool states = fam == kFamHalf;  // the other families keep their states in LDS
     const size_t obj_part_bytes = obj ? align_up((size_t)BH * T * b * sizeof(float)) : 0;
     if (states || obj) {
         const size_t state_ws = states ? workspace_bytes(BH, m * b, d, dtype) : 0;
@@ -496,7 +500,7 @@ int monarch_attn_release_workspace(void)
 int monarch_attn_set_path(int32_t path)
 {
     g_err[0] = '\0';
-    if (path != kAuto && path != kHalfSteps && path != kFusedHead) {
+    if (path != kAuto && path != kHalfSteps && path != kFusedHead && path != kGrouped) {
         fail(MA_EINVAL, "unknown path %d", path);
         return -1;
     }

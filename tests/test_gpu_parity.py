@@ -35,15 +35,26 @@ def _tile(n):
     return 16 if p <= 16 else 32 if p <= 32 else 64 if p <= 64 else 128
 
 
-# Every parity test runs on both execution paths: one launch per half-step,
-# and one workgroup per head with the states in LDS (small heads only).
-@pytest.fixture(params=["half_steps", "fused"])
+# Every parity test runs on the three execution paths: one launch per
+# half-step, one workgroup per head with the states in LDS (small heads
+# only), and one workgroup per group of residue classes of a head (16-bit,
+# d <= 64, m, b <= 64).
+PATHS = {"half_steps": "PATH_HALF_STEPS", "fused": "PATH_FUSED", "grouped": "PATH_GROUPED"}
+
+
+@pytest.fixture(params=list(PATHS))
 def ma(lib, request):
-    path = lib.PATH_HALF_STEPS if request.param == "half_steps" else lib.PATH_FUSED
-    prev = lib.monarch_attn_set_path(path)
+    prev = lib.monarch_attn_set_path(getattr(lib, PATHS[request.param]))
     lib.path_name = request.param
     yield lib
     lib.monarch_attn_set_path(prev)
+
+
+def skip_unless_path_applies(ma, d, m, b, td, objective=False):
+    if ma.path_name == "fused" and not ma.fused_applies(d, m, b, ma.dtype_code(td)):
+        pytest.skip("the fused kernel covers 16-bit elements, d = 64, m and b <= 16")
+    if ma.path_name == "grouped" and (objective or not ma.grouped_applies(d, m, b, ma.dtype_code(td))):
+        pytest.skip("the grouped kernel covers 16-bit elements, d <= 64, m and b <= 64, no objective")
 
 
 def _torch_dtype(dtype):
@@ -56,8 +67,7 @@ def gpu_run(ma, q, k, v, m, b, T, dtype):
     import torch
 
     td = _torch_dtype(dtype)
-    if ma.path_name == "fused" and not ma.fused_applies(q.shape[-1], m, b, ma.dtype_code(td)):
-        pytest.skip("the fused kernel covers 16-bit elements, d = 64, m and b <= 16")
+    skip_unless_path_applies(ma, q.shape[-1], m, b, td)
     dq = torch.from_numpy(q).to(td).cuda()
     dk = torch.from_numpy(k).to(td).cuda()
     dv = torch.from_numpy(v).to(td).cuda()
@@ -302,6 +312,72 @@ def test_fused_and_half_steps_agree_bitwise(lib, dtype, B, H, m, b, T):
     assert torch.equal(got, ref), float((got.float() - ref.float()).abs().max())
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize(
+    "B,H,n,m,b,d,T",
+    [
+        (1, 16, 4096, 64, 64, 64, 1),     # the 4K speed point, T = 1 .. 3
+        (1, 16, 4096, 64, 64, 64, 3),
+        (2, 6, 1024, 32, 32, 64, 2),      # RoBERTa blocks
+        (3, 5, 196, 14, 14, 64, 2),       # ViT
+        (3, 5, 197, 15, 14, 64, 2),       # ViT with its class token (padded)
+        (1, 16, 256, 16, 16, 64, 2),      # one class per workgroup
+        (2, 3, 1000, 40, 25, 48, 3),      # padded tiles in both, d = 48
+        (1, 4, 2048, 32, 64, 32, 2),      # m != b
+        (2, 2, 700, 64, 11, 64, 1),       # b = 11 over 16-row tiles, m = 64
+        (1, 3, 63, 63, 1, 64, 2),         # b = 1
+        (1, 3, 40, 1, 40, 16, 2),         # m = 1
+    ],
+)
+def test_grouped_and_half_steps_agree_bitwise(lib, dtype, B, H, n, m, b, d, T):
+    """The grouped kernel runs the unit arithmetic of the half-step kernels on
+    the same element-type states, only held in LDS, so both paths give the
+    same bits."""
+    import torch
+
+    td = _torch_dtype(dtype)
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=300 + m * 17 + b, scale=1.5)
+    t = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
+
+    def run(path):
+        lib.monarch_attn_set_path(path)
+        out = torch.full_like(t[0], float("nan"))
+        lib.monarch_attn_fwd(t[0], t[1], t[2], out, m, b, T)
+        torch.cuda.synchronize()
+        return out.cpu()
+
+    prev = lib.monarch_attn_set_path(lib.PATH_HALF_STEPS)
+    try:
+        ref, got = run(lib.PATH_HALF_STEPS), run(lib.PATH_GROUPED)
+    finally:
+        lib.monarch_attn_set_path(prev)
+    assert bool(torch.isfinite(got).all())
+    assert torch.equal(got, ref), float((got.float() - ref.float()).abs().max())
+
+
+def test_grouped_path_unsupported_call_is_rejected(lib):
+    """The forced grouped path refuses what it does not cover (b > 64, fp32,
+    the objective), launching nothing."""
+    import torch
+
+    prev = lib.monarch_attn_set_path(lib.PATH_GROUPED)
+    try:
+        for m, b, td in ((8, 80, torch.bfloat16), (16, 16, torch.float32)):
+            q = torch.zeros(1, 1, m * b, 64, device="cuda", dtype=td)
+            out = torch.full_like(q, 3.0)
+            with pytest.raises(lib.MonarchAttnError) as exc:
+                lib.monarch_attn_fwd(q, q.clone(), q.clone(), out, m, b, 2)
+            assert exc.value.status == lib.MA_EUNSUPPORTED
+            torch.cuda.synchronize()
+            assert bool((out == 3.0).all())
+        q = torch.zeros(1, 1, 256, 64, device="cuda", dtype=torch.bfloat16)
+        obj = torch.empty((1, 1, 2), device="cuda", dtype=torch.float32)
+        with pytest.raises(lib.MonarchAttnError):
+            lib.monarch_attn_fwd_objective(q, q, q, torch.empty_like(q), obj, 16, 16, 2)
+    finally:
+        lib.monarch_attn_set_path(prev)
+
+
 # -- sequence lengths that are not a multiple of b (post-padding with the key mask) -------
 
 GUARD = 4096  # NaN elements after every tensor: a read past row N shows up as NaN in O
@@ -318,8 +394,7 @@ def gpu_run_padded(ma, q, k, v, m, b, T, dtype):
     import torch
 
     td = _torch_dtype(dtype)
-    if ma.path_name == "fused" and not ma.fused_applies(q.shape[-1], m, b, ma.dtype_code(td)):
-        pytest.skip("the fused kernel covers 16-bit elements, d = 64, m and b <= 16")
+    skip_unless_path_applies(ma, q.shape[-1], m, b, td)
     bufs = [_guarded(torch, x, td) for x in (q, k, v)]
     oflat, out = _guarded(torch, np.full(q.shape, np.nan, dtype=np.float32), td)
     ma.monarch_attn_fwd(bufs[0][1], bufs[1][1], bufs[2][1], out, m, b, T)
@@ -431,8 +506,7 @@ def gpu_objective(ma, q, k, v, m, b, T, dtype):
     import torch
 
     td = _torch_dtype(dtype)
-    if ma.path_name == "fused" and not ma.fused_applies(q.shape[-1], m, b, ma.dtype_code(td)):
-        pytest.skip("the fused kernel covers 16-bit elements, d <= 64, m and b <= 16")
+    skip_unless_path_applies(ma, q.shape[-1], m, b, td, objective=True)
     t = [torch.from_numpy(x).to(td).cuda() for x in (q, k, v)]
     out = torch.empty_like(t[0])
     obj = torch.full((q.shape[0], q.shape[1], T), float("nan"), dtype=torch.float32, device="cuda")

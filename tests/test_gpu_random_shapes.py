@@ -104,7 +104,7 @@ def test_random_forward(ma, case, path):
 @pytest.mark.parametrize("case", range(40))
 def test_random_small_heads(ma, case):
     """m, b <= 16 and d <= 64 in 16-bit types: the one-workgroup-per-head
-    kernel on the automatic path, and the half-step kernels."""
+    kernel (the automatic path), the grouped kernel and the half-step kernels."""
     import torch
 
     dtype, B, H, m, b, n, d, T, scale = draw(ma, 7500 + case, 256, 5, ma.monarch_attn_check, max_mb=16, max_d=64,
@@ -115,7 +115,7 @@ def test_random_small_heads(ma, case):
     assert ma.fused_applies(d, m, b, _code(ma, dtype))
     q, k, v = si.random_qkv(B, H, n, d, dtype, seed=7500 + case, scale=scale)
     ref = oracle.monarch_attention(q, k, v, m, b, T)
-    for path in (ma.PATH_FUSED, ma.PATH_HALF_STEPS):
+    for path in (ma.PATH_FUSED, ma.PATH_GROUPED, ma.PATH_HALF_STEPS):
         prev = ma.monarch_attn_set_path(path)
         try:
             tq, tk, tv = _to_dev((q, k, v), dtype)
