@@ -177,6 +177,34 @@ int monarch_attn_fwd_varlen(const void *q, const void *k, const void *v, void *o
                             int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
 
 /*
+ * monarch_attn_fwd_prepad -- monarch_attn_fwd over pre-padded sequences:
+ * the padding rows come before the real ones (the last sentence of Appendix
+ * "Padding and Masking": the key mask then removes the positions below
+ * m b - n of the padded sequence, n its real rows, instead of those from n
+ * on).
+ *
+ * lens : NULL, or a DEVICE pointer to B int32 values as in
+ *        monarch_attn_fwd_varlen (4-byte aligned, clamped to 0..N).
+ *        NULL: all N rows of every head are real, and the sequence is
+ *        pre-padded with m b - N zero rows.  Otherwise batch element beta
+ *        holds its lens[beta] real rows as the LAST lens[beta] of its N rows
+ *        (a left-padded batch), pre-padded with zero rows to m b; rows
+ *        0 .. N - lens[beta] - 1 of q, k, v count as zero whatever they hold
+ *        and are written as zero in out.  Whole key blocks can then be
+ *        padding, with the convention of monarch_attn_fwd_varlen (R = 0, no
+ *        weight in the L softmax).
+ * The result is that of the post-padded problem on the row-reversed tensors,
+ * row-reversed: reversing the m b positions sends block l to m - 1 - l and
+ * row j to b - 1 - j, which keeps L^(0) = I and both softmaxes.  The kernels
+ * run exactly that, reading and writing rows in reverse order.  The other
+ * arguments, the errors, the workspace and the asynchrony are those of
+ * monarch_attn_fwd (paths 1 and 2 only; path 3 returns MA_EUNSUPPORTED).
+ */
+int monarch_attn_fwd_prepad(const void *q, const void *k, const void *v, void *out, const int32_t *lens,
+                            int64_t B, int64_t H, int64_t N, int64_t d,
+                            int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream);
+
+/*
  * monarch_attn_fwd_objective -- monarch_attn_fwd, plus the value of the
  * variational objective f(M; Q, K) = <M, s Q K^T> + H(M) (Sec. 3, eq.
  * softmax_variational_attention, in its separable form for Monarch M) after

@@ -55,6 +55,9 @@ def _load():
         lib.ma_oracle_fwd_varlen_f64.argtypes = [dp, dp, dp, dp, ctypes.POINTER(ctypes.c_int64),
                                                  i64, i64, i64, i64, i64, i64, i32, i32]
         lib.ma_oracle_fwd_varlen_f64.restype = ctypes.c_int
+        lib.ma_oracle_fwd_prepad_f64.argtypes = [dp, dp, dp, dp, ctypes.POINTER(ctypes.c_int64),
+                                                 i64, i64, i64, i64, i64, i64, i32, i32]
+        lib.ma_oracle_fwd_prepad_f64.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -108,6 +111,30 @@ def monarch_attention_varlen(q, k, v, lens, m: int, b: int, T: int, threads: int
     out = np.empty_like(q)
     rc = _load().ma_oracle_fwd_varlen_f64(_dptr(q), _dptr(k), _dptr(v), _dptr(out),
                                           lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)),
+                                          B, H, N, d, m, b, T, threads)
+    if rc != 0:
+        raise ValueError(f"oracle rejected the arguments (code {rc})")
+    return out
+
+
+def monarch_attention_prepad(q, k, v, m: int, b: int, T: int, lens=None, threads: int = 0) -> np.ndarray:
+    """O for pre-padded sequences (Appendix "Padding and Masking", its last
+    sentence: the padding rows come first).  q, k, v float64 [B, H, N, d].
+    lens None: all N rows are real, pre-padded to m*b.  lens[B]: batch
+    element beta's real rows are its LAST lens[beta] rows (a left-padded
+    batch), pre-padded to m*b; its other rows of O are zero."""
+    q = np.ascontiguousarray(q, dtype=np.float64)
+    k = np.ascontiguousarray(k, dtype=np.float64)
+    v = np.ascontiguousarray(v, dtype=np.float64)
+    B, H, N, d = q.shape
+    lp = None
+    if lens is not None:
+        lens = np.ascontiguousarray(lens, dtype=np.int64)
+        if lens.shape != (B,):
+            raise ValueError("lens must hold one length per batch element")
+        lp = lens.ctypes.data_as(ctypes.POINTER(ctypes.c_int64))
+    out = np.empty_like(q)
+    rc = _load().ma_oracle_fwd_prepad_f64(_dptr(q), _dptr(k), _dptr(v), _dptr(out), lp,
                                           B, H, N, d, m, b, T, threads)
     if rc != 0:
         raise ValueError(f"oracle rejected the arguments (code {rc})")

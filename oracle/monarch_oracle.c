@@ -82,15 +82,18 @@ static int thread_index(void)
 
 /* One R half-step for unit (head, k), eq. R_update, beta_r, beta_l.
  * aR[k][j][:] and cR[k][j] are the inputs; writes aL[j][k][:], cL[j][k] and,
- * when y != NULL, Y[j][k][:].  Keys i >= nkeys of block k are padding: the
- * mask omega = -inf is added to their Z_R (Appendix "Padding and Masking"). */
+ * when y != NULL, Y[j][k][:].  kreal[k*b + i] is 0 where key position
+ * k*b + i is padding: the mask omega = -inf is added to its Z_R (Appendix
+ * "Padding and Masking"). */
 static void r_half_step(const double *Kh, const double *Vh, const double *aR, const double *cR,
                         double *aL, double *cL, double *Y, int64_t m, int64_t b, int64_t d,
-                        int64_t k, int64_t nkeys, double *z)
+                        int64_t k, const unsigned char *kreal, double *z)
 {
     const double *Kk = Kh + k * b * d; /* Kbar[k][i] = K[k*b + i] */
     const double *Vk = Vh ? Vh + k * b * d : NULL;
-    if (nkeys <= 0) { /* a block of padding only: R[k] = 0 */
+    int64_t nkeys = 0; /* real keys of block k */
+    for (int64_t i = 0; i < b; ++i) nkeys += kreal[k * b + i] != 0;
+    if (nkeys == 0) { /* a block of padding only: R[k] = 0 */
         for (int64_t j = 0; j < b; ++j) {
             cL[j * m + k] = 0.0;
             memset(aL + (j * m + k) * d, 0, (size_t)d * sizeof(double));
@@ -105,7 +108,7 @@ static void r_half_step(const double *Kh, const double *Vh, const double *aR, co
         for (int64_t i = 0; i < b; ++i) {
             double beta = 0.0;
             for (int64_t v = 0; v < d; ++v) beta += a[v] * Kk[i * d + v];
-            z[i] = i < nkeys ? beta / c : -INFINITY; /* + omega[k][j][i] */
+            z[i] = kreal[k * b + i] ? beta / c : -INFINITY; /* + omega[k][j][i] */
             if (z[i] > zmax) zmax = z[i];
         }
         double sum = 0.0;
@@ -144,13 +147,15 @@ static void r_half_step(const double *Kh, const double *Vh, const double *aR, co
  * in the separable form of Sec. 3 ("Softmax Objective"):
  *   sum_k <alpha_R[k][j], alpha_L[j][k]> + (1^T R_kj) H(L_jk) + (1^T L_jk) H(R_kj),
  * with 1^T R_kj = 1, 1^T L_jk = c_R[k][j], H(R_kj) = -c_L[j][k] and
- * H(L_jk) = -sum_l L log L (hl: m doubles of scratch).  Key blocks k >= live
- * hold no real key (batch padding): Z_L = -inf for them, and L = 0 when live
- * is 0. */
+ * H(L_jk) = -sum_l L log L (hl: m doubles of scratch).  Key blocks k with
+ * blive[k] == 0 hold no real key (batch padding): Z_L = -inf for them, and
+ * L = 0 when no block holds one. */
 static void l_half_step(const double *Qs, const double *aL, const double *cL, const double *Y,
                         double *aR, double *cR, double *O, int64_t m, int64_t b, int64_t d,
-                        int64_t j, int64_t live, double *z, double *fj, double *hl)
+                        int64_t j, const unsigned char *blive, double *z, double *fj, double *hl)
 {
+    int64_t live = 0; /* key blocks holding a real key */
+    for (int64_t k = 0; k < m; ++k) live += blive[k] != 0;
     if (fj) {
         for (int64_t k = 0; k < m; ++k) hl[k] = 0.0;
     }
@@ -167,7 +172,7 @@ static void l_half_step(const double *Qs, const double *aL, const double *cL, co
             const double *al = aL + (j * m + k) * d;
             double beta = 0.0;
             for (int64_t v = 0; v < d; ++v) beta += al[v] * qb[v];
-            z[k] = k < live ? beta - cL[j * m + k] : -INFINITY;
+            z[k] = blive[k] ? beta - cL[j * m + k] : -INFINITY;
             if (z[k] > zmax) zmax = z[k];
         }
         if (live > 0) {
@@ -215,10 +220,20 @@ static void l_half_step(const double *Qs, const double *aL, const double *cL, co
 /* The forward pass; obj (NULL, or B*H*T doubles) receives f(M^(t); Q, K)
  * after every step t (the objective of Sec. 3 with the factors of step t, on
  * all m*b rows of the padded problem): obj[(h * T) + t - 1].  lens (NULL, or
- * B lengths <= N) gives the real rows of each batch element. */
+ * B lengths <= N) gives the real rows of each batch element.
+ *
+ * Placement of the n real rows of a head (n = lens[e] or N) in the padded
+ * sequence of Np = m*b positions (Appendix "Padding and Masking"):
+ *   post-padding (pre = 0): the first n rows of the tensor at positions
+ *                           0 .. n-1; positions n .. Np-1 are padding;
+ *   pre-padding  (pre = 1): the last n rows of the tensor (rows N-n .. N-1)
+ *                           at positions Np-n .. Np-1; positions below
+ *                           Np-n are padding.
+ * Padded positions hold zero rows and their keys are masked (omega = -inf
+ * on Z_R); O is written at the real rows and is zero on the others. */
 static int forward(const double *q, const double *k, const double *v, double *out, double *obj,
-                   const int64_t *lens, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b,
-                   int32_t T, int32_t threads)
+                   const int64_t *lens, int pre, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m,
+                   int64_t b, int32_t T, int32_t threads)
 {
     if (!q || !k || !v || !out) return MO_EINVAL;
     if (B < 1 || H < 1 || d < 1 || m < 1 || b < 1 || T < 1 || N < 1) return MO_EINVAL;
@@ -241,8 +256,11 @@ static int forward(const double *q, const double *k, const double *v, double *ou
     double *cR = malloc(sizeof(double) * (size_t)(BH * Np));
     double *cL = malloc(sizeof(double) * (size_t)(BH * Np));
     double *fpart = malloc(sizeof(double) * (size_t)(BH * b)); /* objective share of (head, j) */
-    if (!Qs || !Kp || !Vp || !Op || !aR || !aL || !Y || !cR || !cL || !fpart) {
+    unsigned char *kreal = calloc((size_t)(BH * Np), 1);         /* real key positions of each head */
+    unsigned char *blive = calloc((size_t)(BH * m), 1);          /* key blocks holding a real key */
+    if (!Qs || !Kp || !Vp || !Op || !aR || !aL || !Y || !cR || !cL || !fpart || !kreal || !blive) {
         free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
+        free(kreal); free(blive);
         return MO_ENOMEM;
     }
 #ifdef _OPENMP
@@ -258,16 +276,24 @@ static int forward(const double *q, const double *k, const double *v, double *ou
     if (!zbuf || !hbuf) {
         free(zbuf); free(hbuf);
         free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
+        free(kreal); free(blive);
         return MO_ENOMEM;
     }
 
 #pragma omp parallel for schedule(static) num_threads(nt)
-    for (int64_t h = 0; h < BH; ++h)
-        for (int64_t e = 0; e < (lens ? lens[h / H] : N) * d; ++e) { /* rows >= the length stay zero */
-            Qs[h * nd + e] = s * q[h * N * d + e]; /* scale absorbed into Q */
-            Kp[h * nd + e] = k[h * N * d + e];
-            Vp[h * nd + e] = v[h * N * d + e];
+    for (int64_t h = 0; h < BH; ++h) {
+        const int64_t n = lens ? lens[h / H] : N;
+        const int64_t row0 = pre ? N - n : 0, pos0 = pre ? Np - n : 0; /* first real row, its position */
+        for (int64_t r = 0; r < n; ++r) {
+            for (int64_t e = 0; e < d; ++e) {
+                Qs[h * nd + (pos0 + r) * d + e] = s * q[(h * N + row0 + r) * d + e]; /* scale absorbed into Q */
+                Kp[h * nd + (pos0 + r) * d + e] = k[(h * N + row0 + r) * d + e];
+                Vp[h * nd + (pos0 + r) * d + e] = v[(h * N + row0 + r) * d + e];
+            }
+            kreal[h * Np + pos0 + r] = 1;
+            blive[h * m + (pos0 + r) / b] = 1;
         }
+    }
     /* t = 1 state from L^(0) = I: alpha_R[k][j] = s*Q[k*b+j], c_R = 1. */
 #pragma omp parallel for schedule(static) num_threads(nt)
     for (int64_t e = 0; e < BH * nd; ++e) aR[e] = Qs[e];
@@ -282,18 +308,15 @@ static int forward(const double *q, const double *k, const double *v, double *ou
             double *hl = hbuf + (size_t)thread_index() * (size_t)m;
 #pragma omp for collapse(2) schedule(static)
             for (int64_t h = 0; h < BH; ++h)
-                for (int64_t kk = 0; kk < m; ++kk) {
-                    const int64_t n = lens ? lens[h / H] : N;
-                    const int64_t nkeys = n - kk * b < b ? n - kk * b : b; /* <= 0: padding only */
+                for (int64_t kk = 0; kk < m; ++kk)
                     r_half_step(Kp + h * nd, last ? Vp + h * nd : NULL, aR + h * nd, cR + h * Np,
-                                aL + h * nd, cL + h * Np, last ? Y + h * nd : NULL, m, b, d, kk, nkeys, z);
-                }
+                                aL + h * nd, cL + h * Np, last ? Y + h * nd : NULL, m, b, d, kk, kreal + h * Np, z);
 #pragma omp for collapse(2) schedule(static)
             for (int64_t h = 0; h < BH; ++h)
                 for (int64_t j = 0; j < b; ++j)
                     l_half_step(Qs + h * nd, aL + h * nd, cL + h * Np, Y + h * nd, aR + h * nd,
-                                cR + h * Np, last ? Op + h * nd : NULL, m, b, d, j,
-                                lens ? (lens[h / H] + b - 1) / b : m, z, obj ? fpart + h * b + j : NULL, hl);
+                                cR + h * Np, last ? Op + h * nd : NULL, m, b, d, j, blive + h * m, z,
+                                obj ? fpart + h * b + j : NULL, hl);
         }
         if (obj) {
             for (int64_t h = 0; h < BH; ++h) {
@@ -303,14 +326,16 @@ static int forward(const double *q, const double *k, const double *v, double *ou
             }
         }
     }
-    /* the first N rows of every head; with lens, zero beyond the length */
+    /* O at the real rows of every head, zero on the others */
 #pragma omp parallel for schedule(static) num_threads(nt)
     for (int64_t h = 0; h < BH; ++h) {
         const int64_t n = lens ? lens[h / H] : N;
-        memcpy(out + h * N * d, Op + h * nd, sizeof(double) * (size_t)(n * d));
-        memset(out + h * N * d + n * d, 0, sizeof(double) * (size_t)((N - n) * d));
+        const int64_t row0 = pre ? N - n : 0, pos0 = pre ? Np - n : 0;
+        memset(out + h * N * d, 0, sizeof(double) * (size_t)(N * d));
+        memcpy(out + (h * N + row0) * d, Op + h * nd + pos0 * d, sizeof(double) * (size_t)(n * d));
     }
     free(Qs); free(Kp); free(Vp); free(Op); free(aR); free(aL); free(Y); free(cR); free(cL); free(fpart);
+    free(kreal); free(blive);
     free(zbuf); free(hbuf);
     return MO_OK;
 }
@@ -319,7 +344,7 @@ int ma_oracle_fwd_obj_f64(const double *q, const double *k, const double *v, dou
                           int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
                           int32_t threads)
 {
-    return forward(q, k, v, out, obj, NULL, B, H, N, d, m, b, T, threads);
+    return forward(q, k, v, out, obj, NULL, 0, B, H, N, d, m, b, T, threads);
 }
 
 /* Batch padding: lens[B] real rows per batch element (0 <= lens <= N). */
@@ -328,7 +353,20 @@ int ma_oracle_fwd_varlen_f64(const double *q, const double *k, const double *v, 
                              int64_t b, int32_t T, int32_t threads)
 {
     if (!lens) return MO_EINVAL;
-    return forward(q, k, v, out, NULL, lens, B, H, N, d, m, b, T, threads);
+    return forward(q, k, v, out, NULL, lens, 0, B, H, N, d, m, b, T, threads);
+}
+
+/* Pre-padded sequences (the last sentence of Appendix "Padding and
+ * Masking"): the padding rows come before the real ones.  lens == NULL: all
+ * N rows are real and the sequence is pre-padded to m*b; otherwise batch
+ * element e holds lens[e] real rows as the LAST lens[e] rows of its N
+ * (a left-padded batch), pre-padded to m*b, and its other rows of out are
+ * zero. */
+int ma_oracle_fwd_prepad_f64(const double *q, const double *k, const double *v, double *out, const int64_t *lens,
+                             int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T,
+                             int32_t threads)
+{
+    return forward(q, k, v, out, NULL, lens, 1, B, H, N, d, m, b, T, threads);
 }
 
 int ma_oracle_fwd_f64(const double *q, const double *k, const double *v, double *out, int64_t B,

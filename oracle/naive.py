@@ -74,14 +74,27 @@ def pad_rows(x: np.ndarray, m: int, b: int) -> np.ndarray:
     return out
 
 
-def key_mask(n: int, m: int, b: int) -> np.ndarray:
-    """omega[k, i] = 0 if key position k*b + i < n else -inf (Appendix "Padding and Masking")."""
+def key_mask(n: int, m: int, b: int, pre: bool = False) -> np.ndarray:
+    """omega[k, i] = 0 at real key positions and -inf at padded ones (Appendix
+    "Padding and Masking").  Post-padding: position k*b + i is real when it is
+    below n.  Pre-padding: the m*b - n padded rows come first, so a position
+    is real when it is at least m*b - n (the appendix's condition with
+    0-based positions)."""
     omega = np.zeros((m, b))
     for k in range(m):
         for i in range(b):
-            if k * b + i >= n:
+            pos = k * b + i
+            real = pos >= m * b - n if pre else pos < n
+            if not real:
                 omega[k, i] = -np.inf
     return omega
+
+
+def front_pad_rows(x: np.ndarray, m: int, b: int) -> np.ndarray:
+    """Pre-pad the rows of x with zero rows to m*b rows (real rows last)."""
+    out = np.zeros((m * b,) + x.shape[1:])
+    out[m * b - x.shape[0]:] = x
+    return out
 
 
 def live_blocks(n: int, b: int) -> int:
@@ -121,19 +134,22 @@ def r_update(L: np.ndarray, Qb: np.ndarray, Kb: np.ndarray, omega=None) -> np.nd
 
 def l_update(R: np.ndarray, Qb: np.ndarray, Kb: np.ndarray, live=None) -> np.ndarray:
     """L = softmax_k(beta_L - c_L) with beta_L, c_L from R (eqs. L_update, beta_l).
-    live: key blocks k < live hold a real key; the others (batch padding) get
+    live: the key blocks that hold a real key, as a count (blocks k < live,
+    post-padding) or a boolean array over k; the others (batch padding) get
     Z_L = -inf, and L = 0 when no block does."""
     m, b, _ = R.shape
-    live = m if live is None else live
+    if live is None:
+        live = m
+    mask = np.arange(m) < live if np.isscalar(live) else np.asarray(live, dtype=bool)
     L = np.zeros((b, m, m))
-    if live == 0:
+    if not mask.any():
         return L
     for j in range(b):
         alpha_l = np.stack([R[k, j] @ Kb[k] for k in range(m)])       # [k, v]
         c_l = np.array([_xlogx_sum(R[k, j]) for k in range(m)])        # sum_i R log R
         for l in range(m):
             beta_l = alpha_l @ Qb[j, l]                                 # over k
-            L[j, :live, l] = _softmax((beta_l - c_l)[:live])
+            L[j, mask, l] = _softmax((beta_l - c_l)[mask])
     return L
 
 
@@ -141,14 +157,14 @@ def _f64(*xs):
     return [np.asarray(x, dtype=np.float64) for x in xs]
 
 
-def monarch_apply(L: np.ndarray, R: np.ndarray, v: np.ndarray) -> np.ndarray:
+def monarch_apply(L: np.ndarray, R: np.ndarray, v: np.ndarray, pre_pad: bool = False) -> np.ndarray:
     """O = M V by the two-step product of eq. monarch_multiply; v with N <= m*b rows
-    (zero-padded), O with the same N rows."""
+    (zero-padded after them, or before them with pre_pad), O with the same N rows."""
     (v,) = _f64(v)
     b, m, _ = L.shape
     n = v.shape[0]
     if n < m * b:
-        v = pad_rows(v, m, b)
+        v = front_pad_rows(v, m, b) if pre_pad else pad_rows(v, m, b)
     Vb = kbar(v, m, b)
     Y = np.empty((b, m, v.shape[1]))
     for j in range(b):
@@ -158,19 +174,20 @@ def monarch_apply(L: np.ndarray, R: np.ndarray, v: np.ndarray) -> np.ndarray:
     for l in range(m):
         for j in range(b):
             O[l * b + j] = L[j, :, l] @ Y[j]     # sum_k L[j,k,l] Y[j,k,:]
-    return O[:n]
+    return O[m * b - n:] if pre_pad else O[:n]
 
 
-def factors(q, k, m, b, T, *, history=False, n=None, batch_padding=False):
+def factors(q, k, m, b, T, *, history=False, n=None, batch_padding=False, pre_pad=False):
     """Run T (R, L) update pairs from L^(0) = I (Sec. 3).  q, k: one head [N, d].
 
-    N < m*b rows are zero-padded to m*b.  Arrays that already have m*b rows
-    with n < m*b are taken as padded by the caller (rows >= n are padding,
-    whatever they hold).  With batch_padding, n may be any length 0..m*b
-    (whole blocks of padding allowed, see the module docstring); otherwise
-    m = ceil(n / b).  Returns (L, R) after T steps; with history=True also
-    the list of (L, R) pairs after every half-step, starting with
-    (L^(0), None).
+    N < m*b rows are zero-padded to m*b, after the real rows or, with
+    pre_pad, before them.  Arrays that already have m*b rows with n < m*b
+    are taken as padded by the caller (post-padding only: rows >= n are
+    padding, whatever they hold).  With batch_padding, n may be any length
+    0..m*b (whole blocks of padding allowed, see the module docstring);
+    otherwise m = ceil(n / b).  Returns (L, R) after T steps; with
+    history=True also the list of (L, R) pairs after every half-step,
+    starting with (L^(0), None).
     """
     q, k = _f64(q, k)
     rows, d = q.shape
@@ -181,10 +198,12 @@ def factors(q, k, m, b, T, *, history=False, n=None, batch_padding=False):
         assert (m - 1) * b < n <= m * b and T >= 1    # m = ceil(N / b)
     if rows < m * b:
         assert rows == n
-        q, k = pad_rows(q, m, b), pad_rows(k, m, b)
-    assert q.shape[0] == m * b
-    omega = key_mask(n, m, b) if n < m * b else None
-    live = live_blocks(n, b)
+        pad = front_pad_rows if pre_pad else pad_rows
+        q, k = pad(q, m, b), pad(k, m, b)
+    assert q.shape[0] == m * b and (not pre_pad or rows == n)
+    omega = key_mask(n, m, b, pre=pre_pad) if n < m * b else None
+    # key blocks holding a real key: the first ceil(n / b), or with pre-padding the last ones
+    live = live_blocks(n, b) if omega is None or not pre_pad else ~np.all(np.isneginf(omega), axis=1)
     s = 1.0 / np.sqrt(d)
     Qb = qbar(s * q, m, b)
     Kb = kbar(k, m, b)
@@ -199,35 +218,41 @@ def factors(q, k, m, b, T, *, history=False, n=None, batch_padding=False):
     return (L, R, hist) if history else (L, R)
 
 
-def monarch_attention_head(q, k, v, m, b, T):
-    """One head: O = M^(T) V.  q, k, v: [N, d] (widened to float64)."""
-    L, R = factors(q, k, m, b, T)
-    return monarch_apply(L, R, v)
+def monarch_attention_head(q, k, v, m, b, T, pre_pad=False):
+    """One head: O = M^(T) V.  q, k, v: [N, d] (widened to float64); with
+    pre_pad the N rows are pre-padded to m*b instead of post-padded."""
+    L, R = factors(q, k, m, b, T, pre_pad=pre_pad)
+    return monarch_apply(L, R, v, pre_pad=pre_pad)
 
 
-def monarch_attention(q, k, v, m, b, T):
+def monarch_attention(q, k, v, m, b, T, pre_pad=False):
     """All heads: q, k, v [B, H, N, d] (widened to float64)."""
     q, k, v = _f64(q, k, v)
     out = np.empty_like(v)
     for bi in range(q.shape[0]):
         for h in range(q.shape[1]):
-            out[bi, h] = monarch_attention_head(q[bi, h], k[bi, h], v[bi, h], m, b, T)
+            out[bi, h] = monarch_attention_head(q[bi, h], k[bi, h], v[bi, h], m, b, T, pre_pad=pre_pad)
     return out
 
 
-def monarch_attention_varlen(q, k, v, lens, m, b, T):
-    """A batch of post-padded sequences: q, k, v [B, H, N, d], lens[B] <= N real
-    rows per batch element.  Each head is the single-sequence problem of its
-    first lens[beta] rows at the batch's m and b (with ``batch_padding``);
-    rows >= lens[beta] of O are zero."""
+def monarch_attention_varlen(q, k, v, lens, m, b, T, pre_pad=False):
+    """A batch of padded sequences: q, k, v [B, H, N, d], lens[B] <= N real rows
+    per batch element.  Post-padding: the real rows are the first lens[beta]
+    rows, each head is the single-sequence problem of those rows post-padded
+    to m*b at the batch's m and b (with ``batch_padding``), and rows
+    >= lens[beta] of O are zero.  pre_pad: the real rows are the last
+    lens[beta] rows, the sequence is pre-padded to m*b, and rows
+    < N - lens[beta] of O are zero."""
     q, k, v = _f64(q, k, v)
     out = np.zeros_like(v)
+    N = q.shape[2]
     for bi in range(q.shape[0]):
         n = int(lens[bi])
-        assert 0 <= n <= q.shape[2] <= m * b
+        assert 0 <= n <= N <= m * b
+        rows = slice(N - n, N) if pre_pad else slice(0, n)
         for h in range(q.shape[1]):
-            L, R = factors(q[bi, h, :n], k[bi, h, :n], m, b, T, n=n, batch_padding=True)
-            out[bi, h, :n] = monarch_apply(L, R, v[bi, h, :n])
+            L, R = factors(q[bi, h, rows], k[bi, h, rows], m, b, T, n=n, batch_padding=True, pre_pad=pre_pad)
+            out[bi, h, rows] = monarch_apply(L, R, v[bi, h, rows], pre_pad=pre_pad)
     return out
 
 

@@ -42,6 +42,7 @@ try:
         monarch_attn_fwd,
         monarch_attn_fwd_noalloc,
         monarch_attn_fwd_objective,
+        monarch_attn_fwd_prepad,
         monarch_attn_fwd_varlen,
         monarch_attn_exact_fwd,
         monarch_attn_fwd_raw,

@@ -38,6 +38,7 @@ EXPORTS = (
     "monarch_attn_timing_read",
     "monarch_attn_build_id",
     "monarch_attn_fwd_noalloc",
+    "monarch_attn_fwd_prepad",
 )
 
 
@@ -84,6 +85,8 @@ def _load() -> ctypes.CDLL:
     lib.monarch_attn_timing_enable.restype = ctypes.c_int
     lib.monarch_attn_timing_read.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_int32), i32]
     lib.monarch_attn_timing_read.restype = ctypes.c_int32
+    lib.monarch_attn_fwd_prepad.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
+    lib.monarch_attn_fwd_prepad.restype = ctypes.c_int
     lib.monarch_attn_fwd_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, i64, i64, i32, i32, vp]
     lib.monarch_attn_fwd_noalloc.restype = ctypes.c_int
     lib.monarch_attn_build_id.argtypes = []
@@ -248,6 +251,24 @@ def monarch_attn_fwd_varlen(q, k, v, out, lens, m: int, b: int, T: int, stream=N
     with _OnDevice(q):
         _check(LIB.monarch_attn_fwd_varlen(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                                            lens.data_ptr(), B, H, N, d, m, b, T, dtype_code(q.dtype), stream))
+    return out
+
+
+def monarch_attn_fwd_prepad(q, k, v, out, m: int, b: int, T: int, lens=None, stream=None):
+    """monarch_attn_fwd over pre-padded sequences (the padding rows first).
+    lens None: all N rows real, pre-padded to m*b.  lens (int32 device tensor
+    [B]): batch element beta's real rows are its LAST lens[beta] rows; its
+    other rows of q, k, v count as zero and are written as zero in `out`.
+    Returns `out`."""
+    _check_tensors(q, k, v, out)
+    if lens is not None:
+        _check_lens(q, lens)
+    B, H, N, d = q.shape
+    stream = _stream(q, stream)
+    with _OnDevice(q):
+        _check(LIB.monarch_attn_fwd_prepad(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                           None if lens is None else lens.data_ptr(), B, H, N, d, m, b, T,
+                                           dtype_code(q.dtype), stream))
     return out
 
 

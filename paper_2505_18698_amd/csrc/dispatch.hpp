@@ -327,12 +327,14 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
     hd.lens = B.lens;
     hd.H = (int)c.H;
     hd.colnorm = 1;
-    const int fam = family_of(path, dtype, c.d, c.m, c.b, B.lens != nullptr, B.obj != nullptr);
+    hd.rev = B.rev;
+    // the grouped kernel takes neither lengths nor the objective nor pre-padding
+    const int fam = family_of(path, dtype, c.d, c.m, c.b, B.lens != nullptr || B.rev, B.obj != nullptr);
     if (fam == kFamNone)
         return fail(MA_EUNSUPPORTED, path == kFusedHead
                                          ? "the one-workgroup-per-head kernel needs bf16/fp16, d <= 64 and m, b <= 16"
-                                         : "the grouped kernel needs bf16/fp16, d <= 64, m, b <= 64, no lengths and "
-                                           "no objective");
+                                         : "the grouped kernel needs bf16/fp16, d <= 64, m, b <= 64, no lengths, "
+                                           "no pre-padding and no objective");
     int rc;
     if (fam == kFamFused) {
         rc = run_fused<T>(L, B, hd, c);

@@ -70,6 +70,7 @@ struct CallBufs {
     float *obj_part;  // [B*H][T][b] shares (workspace)
     float *obj;       // [B*H][T] result (caller's)
     const int *lens = nullptr;  // [B] real rows per batch element (device), or null
+    int rev = 0;                // pre-padded sequences (HeadDims::rev)
 };
 
 struct CallDims {

@@ -532,7 +532,18 @@ struct HeadDims {
     // largest weight L[j][k][l] over l (see LHalf).  Off in the gradient's
     // recompute, whose reverse sweep takes the unscaled states.
     int colnorm = 0;
+    // Pre-padded sequences: the kernels run the post-padded problem of the
+    // row-reversed tensors, i.e. their row x is row n - 1 - x in memory (for
+    // q, k, v and out alike).  The relabelling x -> m b - 1 - x of the padded
+    // positions sends block l to m - 1 - l and row j to b - 1 - j: it keeps
+    // L^(0) = I and the R and L softmaxes (a permutation of the keys within a
+    // block, and of the blocks), and turns padding at the front into padding
+    // at the end (Appendix "Padding and Masking").
+    int rev = 0;
 };
+
+// Row of q, k, v, out in memory for row x (< n) of the kernels' problem.
+__device__ inline int64_t mrow(const HeadDims &hd, int64_t x) { return hd.rev ? (int64_t)hd.n - 1 - x : x; }
 
 // Real rows of head bh.  The kernels read it in fetch() but use it only from
 // stage() on: their tile loads take the static bound n, so that they never
@@ -632,7 +643,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
             const int j = (wave * RT + r) * 16 + (lane & 15);
             const T *row = nullptr;  // alpha_R[k][j]; at t = 1 Q row k*b + j (zero if padding)
             if constexpr (FIRST) {
-                if (j < kv) row = p.q + toff + ((int64_t)k * b + j) * dd;
+                if (j < kv) row = p.q + toff + mrow(hd, (int64_t)k * b + j) * dd;
             } else {
                 if (j < b) row = p.aR + hoff + ((int64_t)k * b + j) * D;
             }
@@ -644,11 +655,12 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         }
         // K and V after the alpha_R rows, V last: the scores wait for the rows
         // and K only, and V is staged just before the product that needs it
-        const T *kblk = p.k + toff + (int64_t)k * b * dd;
-        gr.kt.fetch([=](int r) { return kblk + (int64_t)r * dd; }, kv, tid, dd);
+        const T *kh = p.k + toff;
+        const int64_t r0 = (int64_t)k * b;
+        gr.kt.fetch([=](int r) { return kh + mrow(hd, r0 + r) * dd; }, kv, tid, dd);
         if constexpr (FINAL) {
-            const T *vblk = p.v + toff + (int64_t)k * b * dd;
-            gr.vt.fetch([=](int r) { return vblk + (int64_t)r * dd; }, kv, tid, dd);
+            const T *vh = p.v + toff;
+            gr.vt.fetch([=](int r) { return vh + mrow(hd, r0 + r) * dd; }, kv, tid, dd);
         }
     }
 
@@ -805,7 +817,7 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
             gr.j = j;
         }
         const int ml = (hd.n - j + b - 1) / b;  // rows l of class j in memory: l*b + j < n
-        gr.qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * dd; }, ml, tid, dd);
+        gr.qt.fetch([=](int l) { return qh + mrow(hd, (int64_t)l * b + j) * dd; }, ml, tid, dd);
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
     }
@@ -1009,8 +1021,9 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int l = (wave * RT + r) * 16 + (lane & 15);
-            gr.bf[r].load((int64_t)l * b + j < hd.n ? p.q + bh * (int64_t)hd.n * hd.d + ((int64_t)l * b + j) * hd.d
-                                                    : nullptr,
+            gr.bf[r].load((int64_t)l * b + j < hd.n
+                              ? p.q + bh * (int64_t)hd.n * hd.d + mrow(hd, (int64_t)l * b + j) * hd.d
+                              : nullptr,
                           lane >> 4, hd.d);  // Qbar[j][l]; zero for padded rows
         }
     }
@@ -1115,7 +1128,7 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
 #pragma unroll
         for (int r = 0; r < RT; ++r) {  // rows nl..n-1 (batch padding) are written as zero
             const int64_t row = (int64_t)lr[r] * b + j;
-            store_row<T, D>(row < hd.n ? p.out + bh * (int64_t)hd.n * hd.d + row * hd.d : nullptr, o[r],
+            store_row<T, D>(row < hd.n ? p.out + bh * (int64_t)hd.n * hd.d + mrow(hd, row) * hd.d : nullptr, o[r],
                             (!LENS || row < nl) ? inv[r] : 0.f, lane, hd.d);
         }
     }
@@ -1206,6 +1219,7 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
         T *Qs, *Ks, *As, *Rs;
         float *cRs, *cLs;  // c_R[k][j] at k*CS + j, c_L[j][k] at j*CS + k
         int m, b, n, d, lane, g, c16;  // n: rows of a head in q, k, v, out; d <= D
+        int rev;                       // pre-padded: row x in memory at n - 1 - x (HeadDims::rev)
         int nl, mk;        // with per-sequence lengths: real rows of the head being computed, live key blocks
         float s_log2e;
         int64_t bh;        // the head being computed
@@ -1336,7 +1350,8 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
 #pragma unroll
         for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, 1>(c.Ks + j * LD, BS, 16 * vt, pf, c.lane);
         const int row = l * c.b + j;  // rows nl..n-1 (batch padding) are written as zero
-        store_row<T, D>(row < c.n ? out_h + (int64_t)row * c.d : nullptr, o, (!LENS || row < c.nl) ? 1.0f : 0.f,
+        const int64_t mr = c.rev ? (int64_t)c.n - 1 - row : row;
+        store_row<T, D>(row < c.n ? out_h + mr * c.d : nullptr, o, (!LENS || row < c.nl) ? 1.0f : 0.f,
                         c.lane, c.d);
     }
 
@@ -1345,9 +1360,9 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
     // Issue the loads of head bh: Qbar and Kbar chunks (zero where there is no
     // row) for the LDS regions, and Vbar[w] for wave w's last R half-step.
     // Rows >= n (padding) and columns >= d are zero and never read.
-    __device__ static void load_head(const Bufs<T> &p, int m, int b, int n, int d, int64_t bh, int tid, u32x4 *raw,
-                                     u32x4 *vb)
+    __device__ static void load_head(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int tid, u32x4 *raw, u32x4 *vb)
     {
+        const int m = hd.m, b = hd.b, n = hd.n, d = hd.d;
         const int64_t hoff = bh * (int64_t)n * d;
         const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
 #pragma unroll
@@ -1356,9 +1371,9 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
             const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
             raw[h] = u32x4{0u, 0u, 0u, 0u};
             if (reg == 0 && blk < b && r < m && r * b + blk < n && col < d)
-                raw[h] = *reinterpret_cast<const u32x4 *>(qh + ((int64_t)r * b + blk) * d + col);  // Qbar[blk][r]
+                raw[h] = *reinterpret_cast<const u32x4 *>(qh + mrow(hd, (int64_t)r * b + blk) * d + col);  // Qbar[blk][r]
             if (reg == 1 && blk < m && r < b && blk * b + r < n && col < d)
-                raw[h] = *reinterpret_cast<const u32x4 *>(kh + ((int64_t)blk * b + r) * d + col);  // Kbar[blk][r]
+                raw[h] = *reinterpret_cast<const u32x4 *>(kh + mrow(hd, (int64_t)blk * b + r) * d + col);  // Kbar[blk][r]
         }
         const int w = tid >> 6, lane = tid & 63;
 #pragma unroll
@@ -1366,7 +1381,7 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
             const int r = (lane >> 3) + 8 * h, col = (lane & 7) * 8;
             vb[h] = u32x4{0u, 0u, 0u, 0u};
             if (w < m && r < b && w * b + r < n && col < d)
-                vb[h] = *reinterpret_cast<const u32x4 *>(vh + ((int64_t)w * b + r) * d + col);
+                vb[h] = *reinterpret_cast<const u32x4 *>(vh + mrow(hd, (int64_t)w * b + r) * d + col);
         }
     }
 
@@ -1395,6 +1410,7 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
         c.b = hd.b;
         c.n = hd.n;
         c.d = hd.d;
+        c.rev = hd.rev;
         c.s_log2e = hd.s_log2e;
         c.steps = T_;
         c.obj_part = p.obj_part;
@@ -1406,7 +1422,7 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
 
         u32x4 raw[PER], vcur[2], vnext[2];
         int64_t bh = blockIdx.x;
-        load_head(p, m, b, c.n, c.d, bh, tid, raw, vcur);
+        load_head(p, hd, bh, tid, raw, vcur);
         for (int idx = tid; idx < 2 * 256 * 8; idx += 64 * NW) *chunk(c.As, idx) = u32x4{0u, 0u, 0u, 0u};
         for (; bh < BH; bh += gridDim.x) {
             c.bh = bh;
@@ -1429,7 +1445,7 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
                 for (int h = 0; h < PER; ++h) *chunk(c.Qs, tid + h * 64 * NW) = raw[h];
             }
             __syncthreads();
-            if (bh + gridDim.x < BH) load_head(p, m, b, c.n, c.d, bh + gridDim.x, tid, raw, vnext);
+            if (bh + gridDim.x < BH) load_head(p, hd, bh + gridDim.x, tid, raw, vnext);
 
             for (int t = 1; t <= T_; ++t) {
                 const bool first = t == 1, last = t == T_;

@@ -242,10 +242,10 @@ int check_capture(hipStream_t stream, bool &capturing)
 // The forward pass; with obj != nullptr also the objective per (head, step);
 // with need_lens, per-sequence lengths lens[B] (device).
 // noalloc: the states go to the scratch array instead of the stream's
-// workspace (no objective, no lengths).
+// workspace (no objective, no lengths).  prepad: pre-padded sequences.
 int forward(const void *q, const void *k, const void *v, void *out, float *obj, bool need_obj, const int32_t *lens,
             bool need_lens, int64_t B, int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
-            void *stream, bool noalloc = false)
+            void *stream, bool noalloc = false, bool prepad = false)
 {
     g_err[0] = '\0';
     if (B < 0 || H < 0) return fail(MA_EINVAL, "B and H must be >= 0");
@@ -275,13 +275,13 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     const int path = g_path.load();
     const size_t st = state_bytes(BH, m * b, d, dtype);
     const size_t cs = align_up((size_t)BH * m * b * sizeof(float));
-    CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, obj, lens};
+    CallBufs bufs{q, k, v, out, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, obj, lens, prepad ? 1 : 0};
     int dev = 0, num_cus = 0;
     if ((rc = current_device(dev, num_cus)) != MA_OK) return rc;
     bool capturing = false;
     if ((rc = check_capture((hipStream_t)stream, capturing)) != MA_OK) return rc;
     std::unique_lock<std::mutex> ws_hold;  // the stream's workspace, held until the launches are enqueued
-    const int fam = family_of(path, dtype, d, m, b, need_lens, need_obj);
+    const int fam = family_of(path, dtype, d, m, b, need_lens || prepad, need_obj);
     const bool states = fam == kFamHalf;  // the other families keep their states in LDS
     const size_t obj_part_bytes = obj ? align_up((size_t)BH * T * b * sizeof(float)) : 0;
     if (states || obj) {
@@ -557,6 +557,13 @@ int monarch_attn_fwd_noalloc(const void *q, const void *k, const void *v, void *
                              int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype, void *stream)
 {
     return forward(q, k, v, out, nullptr, false, nullptr, false, B, H, N, d, m, b, T, dtype, stream, true);
+}
+
+int monarch_attn_fwd_prepad(const void *q, const void *k, const void *v, void *out, const int32_t *lens, int64_t B,
+                            int64_t H, int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype,
+                            void *stream)
+{
+    return forward(q, k, v, out, nullptr, false, lens, lens != nullptr, B, H, N, d, m, b, T, dtype, stream, false, true);
 }
 
 int monarch_attn_fwd_varlen(const void *q, const void *k, const void *v, void *out, const int32_t *lens, int64_t B,

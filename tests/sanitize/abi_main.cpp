@@ -72,6 +72,11 @@ int main()
            "varlen null lens");
     expect(monarch_attn_fwd_objective(F, F, F, O, nullptr, 1, 1, 256, 64, 16, 16, 1, 1, nullptr) == MA_EINVAL,
            "objective null obj");
+    expect(monarch_attn_fwd_prepad(F, F, F, O, reinterpret_cast<const int32_t *>(F + 2), 1, 1, 250, 64, 16, 16, 1,
+                                   1, nullptr) == MA_EINVAL,
+           "prepad misaligned lens");
+    expect(monarch_attn_fwd_prepad(F, F, F, O, nullptr, 1, 1, 240, 64, 16, 16, 1, 1, nullptr) == MA_EINVAL,
+           "prepad m != ceil(N / b)");
     expect(monarch_attn_exact_fwd(F, F, F, O, reinterpret_cast<float *>(F + 2), 1, 1, 256, 64, 1, nullptr) ==
                MA_EINVAL,
            "exact misaligned lse");

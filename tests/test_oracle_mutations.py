@@ -214,8 +214,8 @@ def _l_update_variant(kind):
     return l_update
 
 
-def _apply_transposed(L, R, v):
-    return nv.__dict__["_orig_apply"](np.transpose(L, (0, 2, 1)).copy(), R, v)
+def _apply_transposed(L, R, v, pre_pad=False):
+    return nv.__dict__["_orig_apply"](np.transpose(L, (0, 2, 1)).copy(), R, v, pre_pad=pre_pad)
 
 
 def _qbar_wrong(q, m, b):
@@ -223,7 +223,7 @@ def _qbar_wrong(q, m, b):
     return q.reshape(b, m, d).copy()      # rows j*m + l instead of l*b + j
 
 
-def _factors_uniform_init(q, k, m, b, T, *, history=False, n=None, batch_padding=False):
+def _factors_uniform_init(q, k, m, b, T, *, history=False, n=None, batch_padding=False, pre_pad=False):
     rows, d = q.shape
     n = rows if n is None else n
     if rows < m * b:
