@@ -97,7 +97,7 @@ typedef enum {
  * reading no pointer (they may be NULL); this holds for every entry point.
  * Arguments are checked before any HIP call; on MA_EINVAL or
  * MA_EUNSUPPORTED nothing is launched and `out` is untouched.  Path 1 (see
- * monarch_attn_set_path) uses a device workspace (3 m b D elements plus 2 m b
+ * monarch_attn_set_path) uses a device workspace (3 m b d elements plus 2 m b
  * floats per head) owned by the library, one per (device, stream): calls on
  * different streams may run concurrently, and calls on one stream (from any
  * host thread) are enqueued one whole call at a time.  A stream's workspace
@@ -301,9 +301,9 @@ int monarch_attn_bwd_varlen(const void *q, const void *k, const void *v, const v
 int monarch_attn_bwd_check(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t dtype);
 
 /* Bytes of device workspace monarch_attn_bwd needs (0 on bad arguments):
- * 2T state tensors of m b D elements (D = 64, 96 or 128, the smallest that
- * holds d) and 2T - 1 arrays of m b floats per head for the recomputed forward
- * pass, 2 N d floats (dQ, dK accumulators), 3 m b D floats and 2 m b floats
+ * 2T state tensors of m b d elements and 2T - 1 arrays of m b floats per
+ * head for the recomputed forward pass, 2 N d floats (dQ, dK accumulators),
+ * 3 m b D floats (D = 64, 96 or 128, the smallest that holds d) and 2 m b floats
  * (state gradients) per head, each array rounded up to 256 bytes.  Makes no
  * HIP call. */
 size_t monarch_attn_bwd_workspace_bytes(int64_t B, int64_t H, int64_t N, int64_t d,

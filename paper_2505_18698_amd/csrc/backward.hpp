@@ -56,7 +56,7 @@ template <typename T> struct BwdBufs {
 };
 
 struct BwdDims {
-    int m, b, n, d;  // as in the forward (the states are D = 64, 96 or 128 wide, d <= D)
+    int m, b, n, d;  // as in the forward (the states have rows of d elements, the fp32 state gradients of D)
     float s;         // 1/sqrt(d)
     // Per-sequence lengths (batch padding): head bh has lens[bh / H] real
     // rows, clamped to 0..n, or n when lens is null.  Rows past them count as
@@ -355,6 +355,7 @@ template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
         const int ml = (nl - j + b - 1) / b;                 // real rows l: l*b + j < nl
         const int mk = LENS ? min(m, (nl + b - 1) / b) : m;  // key blocks k < mk hold a real key
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
+        const int64_t xoff = bh * Np * d;  // the forward's states: rows of d elements
         // whole-unit tiles (rows k): alpha_L[j][k]; Y[j][k] (LAST) or d alpha_R'[k][j]
         UT *aL = reinterpret_cast<UT *>(lds);
         float *X = lds + UF;
@@ -362,10 +363,10 @@ template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
         float *Qb = X + S * LD, *G = Qb + C * LD, *Lm = G + C * LD, *dL = Lm + C * LS;
         float *cL = dL + C * LS, *dcR = cL + S;
 
-        load_unit<T, NTH, S, D, LDU, HALF>(aL, m, d, [&](int k) { return p.aL + soff + ((int64_t)j * m + k) * D; },
+        load_unit<T, NTH, S, D, LDU, HALF>(aL, m, d, [&](int k) { return p.aL + xoff + ((int64_t)j * m + k) * d; },
                                            tid);
         if constexpr (LAST) {
-            load_tile<T, NTH, S, D, LD>(X, m, d, [&](int k) { return p.Y + soff + ((int64_t)j * m + k) * D; }, tid);
+            load_tile<T, NTH, S, D, LD>(X, m, d, [&](int k) { return p.Y + xoff + ((int64_t)j * m + k) * d; }, tid);
         } else {
             load_tile<float, NTH, S, D, LD>(X, m, d, [&](int k) { return p.daR + soff + ((int64_t)k * b + j) * D; },
                                          tid);
@@ -509,6 +510,7 @@ template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> st
         const int kn = min(b, n - k * b);                                // rows of block k in memory
         const int kv = LENS ? min(b, live_rows(dm, bh) - k * b) : kn;  // real keys (and query rows); <= 0: none
         const int64_t Np = (int64_t)m * b, toff = bh * n * d, soff = bh * Np * D, coff = bh * Np;
+        const int64_t xoff = bh * Np * d;     // the forward's states: rows of d elements
         const int64_t row0 = (int64_t)k * b;  // first row of block k
         // whole-unit tiles (rows i): Kbar, Vbar (LAST)
         UT *Kb = reinterpret_cast<UT *>(lds), *Vb = Kb + S * LDU;
@@ -531,7 +533,7 @@ template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> st
             if constexpr (FIRST) {
                 load_tile<T, NTH, C, D, LD>(aR, jq, d, [&](int jj) { return p.q + toff + (row0 + j0 + jj) * d; }, tid);
             } else {
-                load_tile<T, NTH, C, D, LD>(aR, jb, d, [&](int jj) { return p.aR + soff + (row0 + j0 + jj) * D; },
+                load_tile<T, NTH, C, D, LD>(aR, jb, d, [&](int jj) { return p.aR + xoff + (row0 + j0 + jj) * d; },
                                          tid);
             }
             load_tile<float, NTH, C, D, LD>(

@@ -113,7 +113,7 @@ template <typename T, int D> int bwd_sweep(Launcher &L, const BwdCallBufs &B, co
 }
 
 // The forward half-steps again, each step's states to buffers of their own,
-// then the reverse sweep.  States of width D = tile_d(d); every (m, b, d) the
+// then the reverse sweep.  States with rows of d elements; every (m, b, d) the
 // forward takes.
 template <typename T, int D> int run_bwd_d(Launcher &L, const BwdCallBufs &B, const CallDims &c)
 {

@@ -520,7 +520,7 @@ template <typename T, int D> __device__ inline void store_row_lds(T *row, const 
 struct HeadDims {
     int m, b;          // blocks and block size
     int n;             // rows of q, k, v, out per head, (m - 1) * b < n <= m * b
-    int d;             // head dimension of q, k, v, out (<= the tile width D; the states use D)
+    int d;             // head dimension of q, k, v, out and of the state rows (<= the tile width D)
     float s_log2e;     // log2(e) / sqrt(d)
     int64_t units;     // work units of a half-step launch (grid size)
     int t = 0, T = 0;  // step of this L half-step (1..T) and the step count, for the objective
@@ -574,7 +574,7 @@ __device__ inline int live_blocks(int m, int b, int nl) { return min(m, (nl + b 
 // L softmax, Z_L = -inf), and rows nl..n-1 of out are written as zero.
 // Layouts (per head):
 //   q, k, v, out [B*H][n][d], d <= D (columns d..D-1 of every tile are zero);
-//   alpha_R [m][b][D] (row k*b + j), alpha_L and Y [b][m][D] (row j*m + k),
+//   alpha_R [m][b][d] (row k*b + j), alpha_L and Y [b][m][d] (row j*m + k),
 //   c_L [m][b] (written by the R half-step of block k for all j),
 //   c_R [b][m] (written by the L half-step of class j for all k).
 template <typename T> struct Bufs {
@@ -636,7 +636,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         }
         const int m = hd.m, b = hd.b, kv = block_keys(b, hd.n, k);  // rows in memory
         const int dd = hd.d;
-        const int64_t N = (int64_t)m * b, hoff = bh * N * D, toff = bh * (int64_t)hd.n * dd;
+        const int64_t N = (int64_t)m * b, hoff = bh * N * dd, toff = bh * (int64_t)hd.n * dd;  // states: rows of d
         const int lane = tid & 63, wave = tid >> 6;
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
@@ -645,9 +645,9 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
             if constexpr (FIRST) {
                 if (j < kv) row = p.q + toff + mrow(hd, (int64_t)k * b + j) * dd;
             } else {
-                if (j < b) row = p.aR + hoff + ((int64_t)k * b + j) * D;
+                if (j < b) row = p.aR + hoff + ((int64_t)k * b + j) * dd;
             }
-            gr.bf[r].load(row, lane >> 4, FIRST ? dd : D);
+            gr.bf[r].load(row, lane >> 4, dd);
             gr.cr[r] = 1.0f;
             if constexpr (!FIRST) {
                 if (j < b) gr.cr[r] = p.cR[bh * N + (int64_t)j * m + k];
@@ -684,7 +684,8 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         // keys >= kv: padding, masked (omega); kv <= 0: padding only, R = 0
         const int m = hd.m, b = hd.b, kv = block_keys(b, LENS ? gr.nl : hd.n, k);
         const int64_t N = (int64_t)m * b;
-        const int64_t hoff = bh * N * D;
+        const int dd = hd.d;
+        const int64_t hoff = bh * N * dd;  // states: rows of d elements
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
         int jr[RT];
@@ -757,7 +758,8 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         }
 #pragma unroll
         for (int r = 0; r < RT; ++r)  // alpha_L[j][k] (j-major)
-            store_row<T, D>(jr[r] < b ? p.aL + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r], lane);
+            store_row<T, D>(jr[r] < b ? p.aL + hoff + ((int64_t)jr[r] * m + k) * dd : nullptr, out[r], inv[r], lane,
+                            dd);
         if constexpr (FINAL) {
             // Vbar[k], staged here rather than with K: when a workgroup runs a
             // single unit, the scores and softmax overlap V's loads
@@ -775,8 +777,8 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
             }
 #pragma unroll
             for (int r = 0; r < RT; ++r)
-                store_row<T, D>(jr[r] < b ? p.Y + hoff + ((int64_t)jr[r] * m + k) * D : nullptr, out[r], inv[r],
-                                lane);
+                store_row<T, D>(jr[r] < b ? p.Y + hoff + ((int64_t)jr[r] * m + k) * dd : nullptr, out[r], inv[r],
+                                lane, dd);
         }
     }
 };
@@ -808,17 +810,17 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, int tid, Regs &gr)
     {
         const int m = hd.m, b = hd.b;
-        const int64_t N = (int64_t)m * b, hoff = bh * N * D;
         const int dd = hd.d;
+        const int64_t N = (int64_t)m * b, hoff = bh * N * dd;  // states: rows of d elements
         const T *qh = p.q + bh * (int64_t)hd.n * dd;
-        const T *al = p.aL + hoff + (int64_t)j * m * D;
+        const T *al = p.aL + hoff + (int64_t)j * m * dd;
         if constexpr (LENS) {
             gr.nl = live_rows(hd, bh);
             gr.j = j;
         }
         const int ml = (hd.n - j + b - 1) / b;  // rows l of class j in memory: l*b + j < n
         gr.qt.fetch([=](int l) { return qh + mrow(hd, (int64_t)l * b + j) * dd; }, ml, tid, dd);
-        gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
+        gr.at.fetch([=](int kk) { return al + (int64_t)kk * dd; }, m, tid, dd);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
     }
 
@@ -843,7 +845,7 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
         float *cLs = reinterpret_cast<float *>(APs + AP_ELEMS);
         const int m = hd.m, b = hd.b;
         const int64_t N = (int64_t)m * b;
-        const int64_t hoff = bh * N * D;
+        const int64_t hoff = bh * N * hd.d;  // states: rows of d elements
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
         const int mk = LENS ? live_blocks(m, b, gr.nl) : m;  // blocks k >= mk: no real key
@@ -985,7 +987,8 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
         }
 #pragma unroll
         for (int r = 0; r < RT; ++r)  // alpha_R[k][j] (k-major)
-            store_row<T, D>(kr[r] < m ? p.aR + hoff + ((int64_t)kr[r] * b + j) * D : nullptr, out[r], 1.0f, lane);
+            store_row<T, D>(kr[r] < m ? p.aR + hoff + ((int64_t)kr[r] * b + j) * hd.d : nullptr, out[r], 1.0f, lane,
+                            hd.d);
     }
 };
 
@@ -1010,12 +1013,13 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, int tid, Regs &gr)
     {
         const int m = hd.m, b = hd.b;
-        const int64_t N = (int64_t)m * b, hoff = bh * N * D;
+        const int dd = hd.d;
+        const int64_t N = (int64_t)m * b, hoff = bh * N * dd;  // states: rows of d elements
         const int lane = tid & 63, wave = tid >> 6;
-        const T *al = p.aL + hoff + (int64_t)j * m * D;
-        const T *yj = p.Y + hoff + (int64_t)j * m * D;
-        gr.at.fetch([=](int kk) { return al + (int64_t)kk * D; }, m, tid);
-        gr.yt.fetch([=](int kk) { return yj + (int64_t)kk * D; }, m, tid);
+        const T *al = p.aL + hoff + (int64_t)j * m * dd;
+        const T *yj = p.Y + hoff + (int64_t)j * m * dd;
+        gr.at.fetch([=](int kk) { return al + (int64_t)kk * dd; }, m, tid, dd);
+        gr.yt.fetch([=](int kk) { return yj + (int64_t)kk * dd; }, m, tid, dd);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
         if constexpr (LENS) gr.nl = live_rows(hd, bh);
 #pragma unroll
@@ -1045,8 +1049,6 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
         T *Ys = As + NM * LDK;
         float *cLs = reinterpret_cast<float *>(Ys + NM * LDK);
         const int m = hd.m, b = hd.b;
-        const int64_t N = (int64_t)m * b;
-        const int64_t hoff = bh * N * D;
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
         const int nl = LENS ? gr.nl : hd.n;

@@ -67,11 +67,10 @@ int check_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32_t d
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Np = m * b: the states cover the padded sequence, with rows of the tile
-// width D = tile_d(d).
+// Np = m * b: the states cover the padded sequence, with rows of d elements.
 size_t state_bytes(int64_t BH, int64_t Np, int64_t d, int32_t dtype)
 {
-    return align_up((size_t)BH * Np * tile_d(d) * elem_bytes(dtype));
+    return align_up((size_t)BH * Np * d * elem_bytes(dtype));
 }
 
 size_t workspace_bytes(int64_t BH, int64_t Np, int64_t d, int32_t dtype)
@@ -348,7 +347,7 @@ int check_bwd_shape(int64_t N, int64_t d, int64_t m, int64_t b, int32_t T, int32
 }
 
 // Workspace of one gradient call, in this order: alpha_R of steps 2..T, alpha_L
-// of steps 1..T and Y (element type, tile width D = tile_d(d)); c_R of steps
+// of steps 1..T and Y (element type, rows of d elements); c_R of steps
 // 2..T and c_L of steps 1..T (fp32); the fp32 accumulators of dQ and dK
 // ([B*H][N][d]); the fp32 gradients d alpha_L, dY, d alpha_R (width D) and
 // d c_L, d c_R.

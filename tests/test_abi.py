@@ -159,8 +159,9 @@ def test_workspace_bytes_formula():
     # a padded sequence: the states cover m * b rows
     padded = ma.monarch_attn_workspace_bytes(1, 1, 197, 64, 15, 14, 2, 1)
     assert padded == 3 * _align(210 * 64 * 2) + 2 * _align(210 * 4)
-    # d = 72: states in tiles of width 96
-    assert ma.monarch_attn_workspace_bytes(1, 2, 256, 72, 16, 16, 2, 1) == 3 * _align(2 * 256 * 96 * 2) + 2 * _align(2 * 256 * 4)
+    # d = 72: state rows of 72 elements (the kernels' tiles are 96 wide; the padding never reaches memory)
+    assert ma.monarch_attn_workspace_bytes(1, 2, 256, 72, 16, 16, 2, 1) == 3 * _align(2 * 256 * 72 * 2) + 2 * _align(2 * 256 * 4)
+    assert ma.monarch_attn_workspace_bytes(1, 2, 7600, 48, 60, 128, 2, 1) == 3 * _align(2 * 7680 * 48 * 2) + 2 * _align(2 * 7680 * 4)
 
 
 def _align(x):
@@ -311,10 +312,10 @@ def test_bwd_workspace_bytes_formula():
     assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_F32) == want + 2 * T * (st32 - st)
     assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 16384, 128, 128, 128, 2, ma.MA_F32) == 0
     assert ma.monarch_attn_bwd_workspace_bytes(1, 1, 256, 64, 16, 16, 33, ma.MA_BF16) == 0
-    # d = 72: states and state gradients 96 wide
+    # d = 72: states with rows of 72 elements, state gradients 96 wide
     B, H, N, d, m, b, T = 1, 2, 256, 72, 16, 16, 3
     Np, BH = m * b, B * H
-    st, cs = _align(BH * Np * 96 * 2), _align(BH * Np * 4)
+    st, cs = _align(BH * Np * 72 * 2), _align(BH * Np * 4)
     acc, sg = _align(BH * N * d * 4), _align(BH * Np * 96 * 4)
     assert ma.monarch_attn_bwd_workspace_bytes(B, H, N, d, m, b, T, ma.MA_BF16) == \
         2 * T * st + (2 * T - 1) * cs + 2 * acc + 3 * sg + 2 * cs
