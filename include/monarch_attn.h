@@ -351,12 +351,12 @@ int monarch_attn_release_workspace(void);
  *   3  one workgroup per (batch, head, group of residue classes j) running
  *      every step in one launch with the states of its classes in LDS (the
  *      classes of a head are independent given K and V): bf16 or fp16,
- *      d <= 64, m <= 64 and b <= 64, in monarch_attn_fwd and
+ *      d <= 64, m <= 64 and b <= 32, in monarch_attn_fwd and
  *      monarch_attn_fwd_noalloc only (not with per-sequence lengths or the
  *      objective); any other call returns MA_EUNSUPPORTED.  Uses no
  *      workspace.
- * Automatic selection takes path 2 where it applies, else path 1 (path 3
- * only when asked for).  All paths compute the same operation with the same
+ * Automatic selection takes path 2 where it applies; else path 3 where it
+ * applies with m <= 32 and T >= 2; else path 1.  All paths compute the same operation with the same
  * per-unit arithmetic, and give the same bits.
  */
 int monarch_attn_set_path(int32_t path);

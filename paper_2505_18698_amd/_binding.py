@@ -415,7 +415,7 @@ def fused_applies(d: int, m: int, b: int, dtype: int) -> bool:
 def grouped_applies(d: int, m: int, b: int, dtype: int) -> bool:
     """Whether the one-workgroup-per-(head, group of classes) kernel (PATH_GROUPED)
     covers this shape (without per-sequence lengths or the objective)."""
-    return dtype in (MA_BF16, MA_F16) and d <= 64 and m <= 64 and b <= 64
+    return dtype in (MA_BF16, MA_F16) and d <= 64 and m <= 64 and b <= 32
 
 
 def monarch_attn_workspace_bytes(B, H, N, d, m, b, T, dtype) -> int:

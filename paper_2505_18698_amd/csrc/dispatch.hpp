@@ -289,11 +289,8 @@ template <typename T> int run_group(Launcher &L, const CallBufs &B, ma::HeadDims
     if constexpr (sizeof(T) != 2) {
         return fail(MA_EUNSUPPORTED, "the grouped kernel needs 16-bit elements");
     } else {
-        switch (tile_rows(c.b)) {
-        case 16: return dispatch_group_m<T, 16>(L, B, hd, c);
-        case 32: return dispatch_group_m<T, 32>(L, B, hd, c);
-        default: return dispatch_group_m<T, 64>(L, B, hd, c);
-        }
+        // (b <= 32: grouped_applies)
+        return tile_rows(c.b) == 16 ? dispatch_group_m<T, 16>(L, B, hd, c) : dispatch_group_m<T, 32>(L, B, hd, c);
     }
 }
 
@@ -329,11 +326,11 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
     hd.colnorm = 1;
     hd.rev = B.rev;
     // the grouped kernel takes neither lengths nor the objective nor pre-padding
-    const int fam = family_of(path, dtype, c.d, c.m, c.b, B.lens != nullptr || B.rev, B.obj != nullptr);
+    const int fam = family_of(path, dtype, c.d, c.m, c.b, c.T, B.lens != nullptr || B.rev, B.obj != nullptr);
     if (fam == kFamNone)
         return fail(MA_EUNSUPPORTED, path == kFusedHead
                                          ? "the one-workgroup-per-head kernel needs bf16/fp16, d <= 64 and m, b <= 16"
-                                         : "the grouped kernel needs bf16/fp16, d <= 64, m, b <= 64, no lengths, "
+                                         : "the grouped kernel needs bf16/fp16, d <= 64, m <= 64, b <= 32, no lengths, "
                                            "no pre-padding and no objective");
     int rc;
     if (fam == kFamFused) {

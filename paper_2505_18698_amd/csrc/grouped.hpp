@@ -32,20 +32,26 @@ namespace ma {
 
 template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
     static_assert(sizeof(T) == 2, "16-bit elements only");
-    static constexpr int W = 4, NTH = 64 * W;
+    static constexpr int W = 8, NTH = 64 * W;
     static constexpr int NTB = NB / 16, NTM = NM / 16;
     static constexpr int LDA = D + 8;                 // state rows: 16 bytes of padding
     static constexpr int LDK = Ld<T, D>::row;         // K, V and Qbar staging rows
     static constexpr int LDP = NM + 8;                // probability tile of the L half-step
-    // per-wave staging: Kbar[k] and Vbar[k], or Qbar[j] and P
-    static constexpr int SW_R = 2 * NB * LDK, SW_L = NM * LDK + NM * LDP;
-    static constexpr int SW = SW_R > SW_L ? SW_R : SW_L;
+    // staging: in an R half-step every wave holds Kbar[k], later Vbar[k] in
+    // its place; in an L half-step each of the (at most G) busy waves holds
+    // Qbar[j] and P.  The two phases are separated by barriers and share one
+    // area.
+    static constexpr int SW_R = NB * LDK, SW_L = NM * LDK + NM * LDP;
+    __host__ __device__ static constexpr int stage_elems(int G)
+    {
+        return W * SW_R > (G < W ? G : W) * SW_L ? W * SW_R : (G < W ? G : W) * SW_L;
+    }
     static constexpr bool NFR = NormFirst<NTB, D>::value, NFL = NormFirst<NTM, D>::value;
 
     // LDS bytes for G classes per workgroup
     __host__ __device__ static constexpr int lds_bytes(int G)
     {
-        return (2 * G * NM * LDA + W * SW) * (int)sizeof(T) + 2 * G * NM * 4;
+        return (2 * G * NM * LDA + stage_elems(G)) * (int)sizeof(T) + 2 * G * NM * 4;
     }
 
     struct Ctx {
@@ -63,12 +69,16 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
 
     // R half-step of block k for the group (one wave).  FIRST: alpha_R[k][j] =
     // Q[k*b + j] and c_R = 1 (L^(0) = I).  FINAL: also Y.
+    // kt (and vt) hold block k on entry; as soon as each is in LDS the same
+    // registers take the loads of block kn (if kn < m), which land while this
+    // block is computed.
     template <bool FIRST, bool FINAL>
-    __device__ static void r_block(const Ctx &c, int k, const TileChunks<T, NB, D, 64> &kt,
-                                   const TileChunks<T, NB, D, 64> &vt)
+    __device__ static void r_block(const Ctx &c, int k, int kn, TileChunks<T, NB, D, 64> &kt,
+                                   TileChunks<T, NB, D, 64> &vt)
     {
-        T *Ks = c.S, *Vs = c.S + NB * LDK;
+        T *Ks = c.S + c.wave * SW_R, *Vs = Ks;  // Vbar[k] takes Kbar[k]'s place once alpha_L is formed
         kt.template stage<LDK>(Ks, c.lane);
+        if (kn < c.m) fetch_rows(c, c.kh, kn, kt);
         const int jj = c.c16, j = c.j0 + jj;
         const bool jv = jj < c.gv;
         RowFrags<T, D> bf;  // row j of alpha_R[k]
@@ -115,84 +125,76 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
         }
         ProbFrags<T, NTB> pf;
         pf.pack(sc);
+        // keep the compiler from hoisting the operand reads of the products
+        // above this point (their registers would add to the scores' and the
+        // prefetched blocks')
+        asm volatile("" ::: "memory");
         f32x4 out[D / 16];
 #pragma unroll
         for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, NTB>(Ks, LDK, 16 * vt, pf, c.lane) * inv;
         store_row_lds<T, D>(jv ? slot(c.A, jj, k) : nullptr, out, c.lane);  // alpha_L[j][k] over alpha_R[k][j]
         if constexpr (FINAL) {
             vt.template stage<LDK>(Vs, c.lane);
+            if (kn < c.m) fetch_rows(c, c.vh, kn, vt);
+            asm volatile("" ::: "memory");
 #pragma unroll
             for (int q = 0; q < D / 16; ++q) out[q] = gemm_aggregate<T, NTB>(Vs, LDK, 16 * q, pf, c.lane) * inv;
             store_row_lds<T, D>(jv ? slot(c.Yg, jj, k) : nullptr, out, c.lane);  // Y[j][k]
         }
     }
 
-    // Kbar[k] (and Vbar[k]) into registers: rows k*b + i < n, zero beyond.
-    template <bool FINAL>
-    __device__ static void fetch_block(const Ctx &c, int k, TileChunks<T, NB, D, 64> &kt, TileChunks<T, NB, D, 64> &vt)
+    // Rows k*b + i < n of block k of K or V (base kh or vh) into registers, zero beyond.
+    __device__ static void fetch_rows(const Ctx &c, const T *base, int k, TileChunks<T, NB, D, 64> &t)
     {
         const int kv = block_keys(c.b, c.n, k);
-        const T *kb = c.kh + (int64_t)k * c.b * c.d;
-        kt.fetch([=](int r) { return kb + (int64_t)r * c.d; }, kv, c.lane, c.d);
-        if constexpr (FINAL) {
-            const T *vb = c.vh + (int64_t)k * c.b * c.d;
-            vt.fetch([=](int r) { return vb + (int64_t)r * c.d; }, kv, c.lane, c.d);
-        }
+        const T *blk = base + (int64_t)k * c.b * c.d;
+        const int d = c.d;
+        t.fetch([=](int r) { return blk + (int64_t)r * d; }, kv, c.lane, d);
     }
 
     template <bool FIRST, bool FINAL> __device__ static void r_phase(const Ctx &c)
     {
-        TileChunks<T, NB, D, 64> kt, vt, kn, vn;
+        TileChunks<T, NB, D, 64> kt, vt;
         int k = c.wave;
-        if (k < c.m) fetch_block<FINAL>(c, k, kt, vt);
-        for (; k < c.m; k += W) {
-            if (k + W < c.m) fetch_block<FINAL>(c, k + W, kn, vn);  // lands while this block is computed
-            r_block<FIRST, FINAL>(c, k, kt, vt);
-            kt = kn;
-            if constexpr (FINAL) vt = vn;
+        if (k < c.m) {
+            fetch_rows(c, c.kh, k, kt);
+            if constexpr (FINAL) fetch_rows(c, c.vh, k, vt);
         }
+        for (; k < c.m; k += W) r_block<FIRST, FINAL>(c, k, k + W, kt, vt);
     }
 
-    // Scores and softmax over k of class j0 + jj, all NM query rows l: lane
-    // holds Z[k = 16t + 4g + q][l = 16r + c16] (log2 units) in sc[r][t]; on
-    // return sc holds exp2(Z - max) and inv[r] = 1 / row sum (0 for rows
-    // l >= m).
-    __device__ static void l_scores(const Ctx &c, int jj, const RowFrags<T, D> *bf, f32x4 (*sc)[NTM], float *inv)
+    // Scores and softmax over k of class j0 + jj for the query rows
+    // l = 16r + c16 of row tile r (B fragments bf): lane holds
+    // Z[k = 16t + 4g + q][l] (log2 units) in sc[t]; on return sc holds
+    // exp2(Z - max), and the result is 1 / row sum (0 for rows l >= m).
+    __device__ static float l_row_scores(const Ctx &c, int jj, int r, const RowFrags<T, D> &bf, f32x4 *sc)
     {
         const T *Aj = slot(c.A, jj, 0);
 #pragma unroll
         for (int t = 0; t < NTM; ++t) {
-            f32x4 acc[NTM];
-            gemm_scores_rt<T, D, NTM>(Aj + (16 * t + c.c16) * LDA, bf, acc, c.g);
-            f32x4 bias;
+            f32x4 acc;
+            gemm_scores_rt<T, D, 1>(Aj + (16 * t + c.c16) * LDA, &bf, &acc, c.g);
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int kk = 16 * t + 4 * c.g + q;
-                bias[q] = (!RG || kk < c.m) ? c.cL[jj * NM + kk] * kLog2e : 0.f;
-            }
-#pragma unroll
-            for (int r = 0; r < NTM; ++r) {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) sc[r][t][q] = __builtin_fmaf(acc[r][q], c.s_log2e, -bias[q]);
+                const float bias = (!RG || kk < c.m) ? c.cL[jj * NM + kk] * kLog2e : 0.f;
+                sc[t][q] = __builtin_fmaf(acc[q], c.s_log2e, -bias);
             }
         }
+        const float mx = tiles_max<NTM, RG>(sc, c.m, c.g);
+        float sum = 0.f;
 #pragma unroll
-        for (int r = 0; r < NTM; ++r) {
-            const float mx = tiles_max<NTM, RG>(sc[r], c.m, c.g);
-            float sum = 0.f;
+        for (int t = 0; t < NTM; ++t) {
 #pragma unroll
-            for (int t = 0; t < NTM; ++t) {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    float e = __builtin_amdgcn_exp2f(sc[r][t][q] - mx);
-                    if (RG && 16 * t + 4 * c.g + q >= c.m) e = 0.f;
-                    sum += e;
-                    sc[r][t][q] = e;
-                }
+            for (int q = 0; q < 4; ++q) {
+                float e = __builtin_amdgcn_exp2f(sc[t][q] - mx);
+                if (RG && 16 * t + 4 * c.g + q >= c.m) e = 0.f;
+                sum += e;
+                sc[t][q] = e;
             }
-            sum = lanegroup_sum(sum);
-            inv[r] = 16 * r + c.c16 < c.m ? fast_rcp(sum) : 0.f;  // padded query rows carry no weight
         }
+        sum = lanegroup_sum(sum);
+        return 16 * r + c.c16 < c.m ? fast_rcp(sum) : 0.f;  // padded query rows carry no weight
     }
 
     // Qbar[j] rows l into registers: rows l*b + j < n, zero beyond.
@@ -205,30 +207,28 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
     }
 
     // L half-step of class j0 + jj (one wave): alpha_R[:][j] and c_R[:][j]
-    // over the slots (jj, *).
-    __device__ static void l_class(const Ctx &c, int jj, const TileChunks<T, NM, D, 64> &qt)
+    // over the slots (jj, *).  qt holds Qbar[j] on entry; once it is in LDS
+    // the same registers take the loads of class jn (if jn < gv).
+    __device__ static void l_class(const Ctx &c, int jj, int jn, TileChunks<T, NM, D, 64> &qt)
     {
-        T *Qs = c.S, *Ps = c.S + NM * LDK;
+        T *Qs = c.S + c.wave * SW_L, *Ps = Qs + NM * LDK;
         qt.template stage<LDK>(Qs, c.lane);
-        RowFrags<T, D> bf[NTM];  // Qbar[j][l] for l = 16r + c16
-#pragma unroll
+        if (jn < c.gv) fetch_qbar(c, c.j0 + jn, qt);
+        // P[l][k] = L[j][k][l], row-major (k contiguous), one row tile at a time
+#pragma unroll 1
         for (int r = 0; r < NTM; ++r) {
+            RowFrags<T, D> bf;  // Qbar[j][l] for l = 16r + c16
 #pragma unroll
             for (int cc = 0; cc < D / Mma<T>::KC; ++cc)
-                bf[r].f[cc] = *reinterpret_cast<const typename Mma<T>::frag *>(Qs + (16 * r + c.c16) * LDK +
-                                                                               cc * Mma<T>::KC + c.g * Mma<T>::KPL);
-        }
-        f32x4 sc[NTM][NTM];
-        float inv[NTM];
-        l_scores(c, jj, bf, sc, inv);
-        // P[l][k] = L[j][k][l], row-major (k contiguous)
+                bf.f[cc] = *reinterpret_cast<const typename Mma<T>::frag *>(Qs + (16 * r + c.c16) * LDK +
+                                                                            cc * Mma<T>::KC + c.g * Mma<T>::KPL);
+            f32x4 sc[NTM];
+            const float inv = l_row_scores(c, jj, r, bf, sc);
 #pragma unroll
-        for (int r = 0; r < NTM; ++r) {
-#pragma unroll
-            for (int t = 0; t < NTM; ++t) store4<T>(Ps + (16 * r + c.c16) * LDP + 16 * t + 4 * c.g, sc[r][t] * inv[r]);
+            for (int t = 0; t < NTM; ++t) store4<T>(Ps + (16 * r + c.c16) * LDP + 16 * t + 4 * c.g, sc[t] * inv);
         }
         // columns k: c_R[k][j] = sum_l L[j][k][l], alpha_R[k][j] = sum_l L[j][k][l] Qbar[j][l]
-#pragma unroll
+#pragma unroll 1
         for (int kt = 0; kt < NTM; ++kt) {
             const int k = 16 * kt + c.c16;
             ProbFrags<T, NTM> pf;
@@ -244,44 +244,42 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
 
     __device__ static void l_phase(const Ctx &c)
     {
-        TileChunks<T, NM, D, 64> qt, qn;
+        TileChunks<T, NM, D, 64> qt;
         int jj = c.wave;
         if (jj < c.gv) fetch_qbar(c, c.j0 + jj, qt);
-        for (; jj < c.gv; jj += W) {
-            if (jj + W < c.gv) fetch_qbar(c, c.j0 + jj + W, qn);
-            l_class(c, jj, qt);
-            qt = qn;
-        }
+        for (; jj < c.gv; jj += W) l_class(c, jj, jj + W, qt);
     }
 
     // Last L half-step of class j0 + jj with O[l*b + j] = sum_k L[j][k][l] Y[j][k].
     __device__ static void apply_class(const Ctx &c, int jj)
     {
         const int j = c.j0 + jj;
-        RowFrags<T, D> bf[NTM];
-#pragma unroll
-        for (int r = 0; r < NTM; ++r) {
-            const int64_t row = (int64_t)(16 * r + c.c16) * c.b + j;
-            bf[r].load(row < c.n ? c.qh + row * c.d : nullptr, c.g, c.d);
-        }
-        f32x4 sc[NTM][NTM];
-        float inv[NTM];
-        l_scores(c, jj, bf, sc, inv);
         const T *Yj = slot(c.Yg, jj, 0);
-#pragma unroll
+        RowFrags<T, D> bf;
+        {
+            const int64_t row = (int64_t)c.c16 * c.b + j;
+            bf.load(row < c.n ? c.qh + row * c.d : nullptr, c.g, c.d);
+        }
+#pragma unroll 1
         for (int r = 0; r < NTM; ++r) {
+            f32x4 sc[NTM];
+            float inv = l_row_scores(c, jj, r, bf, sc);
+            if (r + 1 < NTM) {  // the next row tile's query rows, while this one is finished
+                const int64_t row = (int64_t)(16 * (r + 1) + c.c16) * c.b + j;
+                bf.load(row < c.n ? c.qh + row * c.d : nullptr, c.g, c.d);
+            }
             if constexpr (NFL) {
 #pragma unroll
-                for (int t = 0; t < NTM; ++t) sc[r][t] *= inv[r];
-                inv[r] = 1.0f;
+                for (int t = 0; t < NTM; ++t) sc[t] *= inv;
+                inv = 1.0f;
             }
             ProbFrags<T, NTM> pf;
-            pf.pack(sc[r]);
+            pf.pack(sc);
             f32x4 o[D / 16];
 #pragma unroll
             for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, NTM>(Yj, LDA, 16 * vt, pf, c.lane);
             const int64_t row = (int64_t)(16 * r + c.c16) * c.b + j;
-            store_row<T, D>(row < c.n ? c.oh + row * c.d : nullptr, o, inv[r], c.lane, c.d);
+            store_row<T, D>(row < c.n ? c.oh + row * c.d : nullptr, o, inv, c.lane, c.d);
         }
     }
 
@@ -304,8 +302,8 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
         c.c16 = c.lane & 15;
         c.A = reinterpret_cast<T *>(lds);
         c.Yg = c.A + G * NM * LDA;
-        c.S = c.Yg + G * NM * LDA + c.wave * SW;
-        c.cR = reinterpret_cast<float *>(c.Yg + G * NM * LDA + W * SW);
+        c.S = c.Yg + G * NM * LDA;
+        c.cR = reinterpret_cast<float *>(c.S + stage_elems(G));
         c.cL = c.cR + G * NM;
         // rows k >= m of the state regions are never written: zero them once
         // (they meet zero probabilities in the products, and 0 * NaN is NaN)
@@ -354,7 +352,7 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
 };
 
 template <typename T, int NB, int NM, int D, bool RG>
-__global__ __launch_bounds__(256) void monarch_fused_group(Bufs<T> p, HeadDims hd, int G, int groups, int64_t units,
+__global__ __launch_bounds__(512) void monarch_fused_group(Bufs<T> p, HeadDims hd, int G, int groups, int64_t units,
                                                            int xcd_perm, int T_)
 {
     extern __shared__ __attribute__((aligned(16))) char lds_dyn[];

@@ -100,24 +100,29 @@ inline bool fused_applies(int32_t dtype, int64_t d, int64_t m, int64_t b)
 }
 
 // The one-workgroup-per-(head, group of classes) kernel keeps the states of
-// its classes in LDS: 16-bit elements, d <= 64, m and b at most 64, and
-// neither per-sequence lengths nor the objective.
+// its classes in LDS: 16-bit elements, d <= 64, m at most 64, b at most 32,
+// and neither per-sequence lengths nor the objective.
 inline bool grouped_applies(int32_t dtype, int64_t d, int64_t m, int64_t b, bool lens, bool obj)
 {
-    return (dtype == MA_BF16 || dtype == MA_F16) && d <= 64 && m <= 64 && b <= 64 && !lens && !obj;
+    return (dtype == MA_BF16 || dtype == MA_F16) && d <= 64 && m <= 64 && b <= 32 && !lens && !obj;
 }
 
 // The family that runs a call under `path` (kFamNone: the forced path does
 // not take the shape).  Automatic: the one-workgroup-per-head kernel where it
-// applies, else the half-steps (the grouped kernel is slower than both on
-// every measured shape, so it runs only when asked for).
-inline int family_of(int path, int32_t dtype, int64_t d, int64_t m, int64_t b, bool lens, bool obj)
+// applies; else the grouped kernel where it applies with m <= 32 and T >= 2
+// (measured faster than the half-steps there; with more blocks every group
+// streams more of K and V, and at T = 1 the half-steps are two launches);
+// else the half-steps.  All families give the same bits.
+inline int family_of(int path, int32_t dtype, int64_t d, int64_t m, int64_t b, int T, bool lens, bool obj)
 {
     switch (path) {
     case kHalfSteps: return kFamHalf;
     case kFusedHead: return fused_applies(dtype, d, m, b) ? kFamFused : kFamNone;
     case kGrouped: return grouped_applies(dtype, d, m, b, lens, obj) ? kFamGroup : kFamNone;
-    default: return fused_applies(dtype, d, m, b) ? kFamFused : kFamHalf;
+    default:
+        if (fused_applies(dtype, d, m, b)) return kFamFused;
+        if (grouped_applies(dtype, d, m, b, lens, obj) && m <= 32 && T >= 2) return kFamGroup;
+        return kFamHalf;
     }
 }
 

@@ -38,7 +38,7 @@ def _tile(n):
 # Every parity test runs on the three execution paths: one launch per
 # half-step, one workgroup per head with the states in LDS (small heads
 # only), and one workgroup per group of residue classes of a head (16-bit,
-# d <= 64, m, b <= 64).
+# d <= 64, m <= 64, b <= 32).
 PATHS = {"half_steps": "PATH_HALF_STEPS", "fused": "PATH_FUSED", "grouped": "PATH_GROUPED"}
 
 
@@ -54,7 +54,7 @@ def skip_unless_path_applies(ma, d, m, b, td, objective=False):
     if ma.path_name == "fused" and not ma.fused_applies(d, m, b, ma.dtype_code(td)):
         pytest.skip("the fused kernel covers 16-bit elements, d = 64, m and b <= 16")
     if ma.path_name == "grouped" and (objective or not ma.grouped_applies(d, m, b, ma.dtype_code(td))):
-        pytest.skip("the grouped kernel covers 16-bit elements, d <= 64, m and b <= 64, no objective")
+        pytest.skip("the grouped kernel covers 16-bit elements, d <= 64, m <= 64, b <= 32, no objective")
 
 
 def _torch_dtype(dtype):
@@ -316,17 +316,17 @@ def test_fused_and_half_steps_agree_bitwise(lib, dtype, B, H, m, b, T):
 @pytest.mark.parametrize(
     "B,H,n,m,b,d,T",
     [
-        (1, 16, 4096, 64, 64, 64, 1),     # the 4K speed point, T = 1 .. 3
-        (1, 16, 4096, 64, 64, 64, 3),
+        (1, 16, 2048, 64, 32, 64, 1),     # 64 blocks of 32, T = 1 .. 3
+        (1, 16, 2048, 64, 32, 64, 3),
         (2, 6, 1024, 32, 32, 64, 2),      # RoBERTa blocks
         (3, 5, 196, 14, 14, 64, 2),       # ViT
         (3, 5, 197, 15, 14, 64, 2),       # ViT with its class token (padded)
         (1, 16, 256, 16, 16, 64, 2),      # one class per workgroup
         (2, 3, 1000, 40, 25, 48, 3),      # padded tiles in both, d = 48
-        (1, 4, 2048, 32, 64, 32, 2),      # m != b
+        (1, 4, 2048, 64, 32, 32, 2),      # m != b
         (2, 2, 700, 64, 11, 64, 1),       # b = 11 over 16-row tiles, m = 64
         (1, 3, 63, 63, 1, 64, 2),         # b = 1
-        (1, 3, 40, 1, 40, 16, 2),         # m = 1
+        (1, 3, 30, 1, 30, 16, 2),         # m = 1
     ],
 )
 def test_grouped_and_half_steps_agree_bitwise(lib, dtype, B, H, n, m, b, d, T):
@@ -356,13 +356,13 @@ def test_grouped_and_half_steps_agree_bitwise(lib, dtype, B, H, n, m, b, d, T):
 
 
 def test_grouped_path_unsupported_call_is_rejected(lib):
-    """The forced grouped path refuses what it does not cover (b > 64, fp32,
+    """The forced grouped path refuses what it does not cover (b > 32, fp32,
     the objective), launching nothing."""
     import torch
 
     prev = lib.monarch_attn_set_path(lib.PATH_GROUPED)
     try:
-        for m, b, td in ((8, 80, torch.bfloat16), (16, 16, torch.float32)):
+        for m, b, td in ((8, 33, torch.bfloat16), (8, 80, torch.bfloat16), (16, 16, torch.float32)):
             q = torch.zeros(1, 1, m * b, 64, device="cuda", dtype=td)
             out = torch.full_like(q, 3.0)
             with pytest.raises(lib.MonarchAttnError) as exc:
