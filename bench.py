@@ -7,7 +7,8 @@ synthetic Q, K, V already resident in HBM.  The headline workload is the
 long-sequence speed point (B=1, H=16, N=16384 = 128 x 128, d=64, bf16, T=2);
 the medium point (N=4096 = 64 x 64, T=1 and T=3) and ViT-B/16 (384 heads, N=196 = 14 x 14,
 T=2, the one-workgroup-per-head kernel; and N=197 with the class token,
-post-padded to 15 x 14) are reported alongside in "also".
+post-padded to 15 x 14) and RoBERTa-base-shaped attention (192 heads, N=1024
+= 32 x 32, T=2, the grouped kernel) are reported alongside in "also".
 
 Timed regions (HIP events on the stream the library launches on):
   0. (untimed) W warm-up steps, repeated in rounds of W until 0.25 s of
@@ -629,8 +630,8 @@ def quality(ma, torch, w, steps_list=(1, 2, 3)):
 # definitions and their launch configuration (the gradient's launches live
 # apart, so that changing them leaves the forward records valid).
 CSRC = os.path.join(ROOT, "paper_2505_18698_amd", "csrc")
-FWD_SOURCES = ("ma_kernels.hpp", "dispatch.hpp")
-BWD_SOURCES = ("backward.hpp", "dispatch_bwd.hpp", "ma_kernels.hpp", "dispatch.hpp")
+FWD_SOURCES = ("ma_kernels.hpp", "grouped.hpp", "dispatch.hpp")
+BWD_SOURCES = ("backward.hpp", "dispatch_bwd.hpp", "ma_kernels.hpp", "grouped.hpp", "dispatch.hpp")
 
 
 def kernel_sources_sha(kernel):
@@ -787,7 +788,7 @@ def main():
     ap.add_argument("--workload", default="speed_n16384")
     ap.add_argument("--d", type=int, default=None, help="override the head dimension")
     ap.add_argument("--T", type=int, default=None, help="override the number of steps T")
-    ap.add_argument("--also", default="speed_n4096,vit_b16_n196,speed_n4096_t3,vit_b16_n197",
+    ap.add_argument("--also", default="speed_n4096,vit_b16_n196,speed_n4096_t3,vit_b16_n197,roberta_n1024",
                     help="comma-separated extra workloads ('' for none)")
     ap.add_argument("--backward", default="speed_n16384,speed_n4096,vit_b16_n197,sweep_n16384_d128",
                     help="comma-separated workloads for the gradient timing ('' for none)")

@@ -356,7 +356,7 @@ int monarch_attn_release_workspace(void);
  *      objective); any other call returns MA_EUNSUPPORTED.  Uses no
  *      workspace.
  * Automatic selection takes path 2 where it applies; else path 3 where it
- * applies with m <= 32 and T >= 2; else path 1.  All paths compute the same operation with the same
+ * applies with m <= 32; else path 1.  All paths compute the same operation with the same
  * per-unit arithmetic, and give the same bits.
  */
 int monarch_attn_set_path(int32_t path);

@@ -227,19 +227,28 @@ inline int resident_per_cu_lds(const void *kern, int threads, int lds)
 constexpr int kMaxLds = 160 * 1024;
 
 // Classes per workgroup: the largest G (at most 16 and at most b) whose LDS
-// fits and that still gives every compute unit a workgroup; else the
-// smallest that fits.
-template <typename U> int group_size(int64_t BH, int b, int num_cus)
+// fits and that still gives every compute unit a workgroup, unless that G
+// needs more rounds of resident workgroups than the next larger one (then
+// that one); if no G fills the device, the smallest that fits.  A unit's R
+// half-steps stream all of the head's K and V whatever G is, so a second
+// round costs about a whole unit, and fewer, larger groups move fewer bytes.
+template <typename U> int group_size(const void *kern, int64_t BH, int b, int num_cus)
 {
     const int cand[5] = {16, 8, 4, 2, 1};
-    int best = 0;
+    int prev = 0;
+    int64_t prev_rounds = 0;
     for (int i = 0; i < 5; ++i) {
         const int G = cand[i] < b ? cand[i] : b;
-        if (U::lds_bytes(G) > kMaxLds) continue;
-        best = G;
-        if (BH * ((b + G - 1) / G) >= num_cus) return G;
+        if (G == prev || U::lds_bytes(G) > kMaxLds) continue;
+        const int per_cu = resident_per_cu_lds(kern, U::NTH, U::lds_bytes(G));
+        if (per_cu < 1) continue;
+        const int64_t units = BH * ((b + G - 1) / G), slots = (int64_t)per_cu * num_cus;
+        const int64_t rounds = (units + slots - 1) / slots;
+        if (units >= num_cus) return prev && prev_rounds < rounds ? prev : G;
+        prev = G;
+        prev_rounds = rounds;
     }
-    return best;
+    return prev;
 }
 
 template <typename T, int NB, int NM, bool RG>
@@ -247,7 +256,7 @@ int launch_group(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims
 {
     using U = ma::FusedGroup<T, NB, NM, 64, RG>;
     auto kern = ma::monarch_fused_group<T, NB, NM, 64, RG>;
-    const int G = group_size<U>(c.BH, c.b, c.num_cus);
+    const int G = group_size<U>((const void *)kern, c.BH, c.b, c.num_cus);
     if (G < 1) return fail(MA_EUNSUPPORTED, "the grouped kernel's LDS does not fit");
     const int lds = U::lds_bytes(G);
     const int per_cu = resident_per_cu_lds((const void *)kern, U::NTH, lds);
@@ -326,7 +335,7 @@ template <typename T> int run_call_impl(Launcher &L, const CallBufs &B, const Ca
     hd.colnorm = 1;
     hd.rev = B.rev;
     // the grouped kernel takes neither lengths nor the objective nor pre-padding
-    const int fam = family_of(path, dtype, c.d, c.m, c.b, c.T, B.lens != nullptr || B.rev, B.obj != nullptr);
+    const int fam = family_of(path, dtype, c.d, c.m, c.b, B.lens != nullptr || B.rev, B.obj != nullptr);
     if (fam == kFamNone)
         return fail(MA_EUNSUPPORTED, path == kFusedHead
                                          ? "the one-workgroup-per-head kernel needs bf16/fp16, d <= 64 and m, b <= 16"

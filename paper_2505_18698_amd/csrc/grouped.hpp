@@ -37,6 +37,12 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
     static constexpr int LDA = D + 8;                 // state rows: 16 bytes of padding
     static constexpr int LDK = Ld<T, D>::row;         // K, V and Qbar staging rows
     static constexpr int LDP = NM + 8;                // probability tile of the L half-step
+    // Classes are CLS elements apart in A and Y, NM rows plus 16 bytes: the 16
+    // lanes that read or write row k of 16 classes then start 16 bytes apart
+    // modulo the 256 bytes of a bank row (NM * LDA elements alone are a
+    // multiple of 256 bytes, which put all 16 on the same banks).  c_R and c_L
+    // rows are CSF floats apart for the same reason.
+    static constexpr int CLS = NM * LDA + 8, CSF = NM + 1;
     // staging: in an R half-step every wave holds Kbar[k], later Vbar[k] in
     // its place; in an L half-step each of the (at most G) busy waves holds
     // Qbar[j] and P.  The two phases are separated by barriers and share one
@@ -51,12 +57,12 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
     // LDS bytes for G classes per workgroup
     __host__ __device__ static constexpr int lds_bytes(int G)
     {
-        return (2 * G * NM * LDA + stage_elems(G)) * (int)sizeof(T) + 2 * G * NM * 4;
+        return (2 * G * CLS + stage_elems(G)) * (int)sizeof(T) + 2 * G * CSF * 4;
     }
 
     struct Ctx {
         T *A, *Yg, *S;        // states, Y, this wave's staging
-        float *cR, *cL;       // [G][NM]
+        float *cR, *cL;       // [G][CSF]
         int m, b, n, d, G, gv, j0;
         int lane, g, c16, wave;
         float s_log2e;
@@ -65,7 +71,7 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
     };
 
     // Slot (jj, k) of a state region.
-    __device__ static T *slot(T *base, int jj, int k) { return base + ((int64_t)jj * NM + k) * LDA; }
+    __device__ static T *slot(T *base, int jj, int k) { return base + jj * CLS + k * LDA; }
 
     // R half-step of block k for the group (one wave).  FIRST: alpha_R[k][j] =
     // Q[k*b + j] and c_R = 1 (L^(0) = I).  FINAL: also Y.
@@ -94,7 +100,7 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
         }
         float rs = c.s_log2e;
         if constexpr (!FIRST) {
-            if (jv) rs = c.s_log2e * fast_rcp(fmaxf(c.cR[jj * NM + k], kTiny));
+            if (jv) rs = c.s_log2e * fast_rcp(fmaxf(c.cR[jj * CSF + k], kTiny));
         }
         const int kv = block_keys(c.b, c.n, k);  // keys >= kv: padding, masked (omega)
         f32x4 sc[NTB];                            // lane holds S'[i = 16t + 4g + q][j]
@@ -117,7 +123,7 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
         sum = lanegroup_sum(sum);
         t2 = lanegroup_sum(t2);
         float inv = fast_rcp(sum);
-        if (c.g == 0 && jv) c.cL[jj * NM + k] = kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum));
+        if (c.g == 0 && jv) c.cL[jj * CSF + k] = kLn2 * (t2 * inv - __builtin_amdgcn_logf(sum));
         if constexpr (NFR) {
 #pragma unroll
             for (int t = 0; t < NTB; ++t) sc[t] *= inv;
@@ -177,7 +183,7 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int kk = 16 * t + 4 * c.g + q;
-                const float bias = (!RG || kk < c.m) ? c.cL[jj * NM + kk] * kLog2e : 0.f;
+                const float bias = (!RG || kk < c.m) ? c.cL[jj * CSF + kk] * kLog2e : 0.f;
                 sc[t][q] = __builtin_fmaf(acc[q], c.s_log2e, -bias);
             }
         }
@@ -234,7 +240,7 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
             ProbFrags<T, NTM> pf;
             pf.gather(Ps, LDP, 16 * kt, c.lane);
             const f32x4 cs = gemm_colsum<T, NTM>(pf);
-            if (c.g == 0 && k < c.m) c.cR[jj * NM + k] = cs[0];
+            if (c.g == 0 && k < c.m) c.cR[jj * CSF + k] = cs[0];
             f32x4 out[D / 16];
 #pragma unroll
             for (int vt = 0; vt < D / 16; ++vt) out[vt] = gemm_aggregate<T, NTM>(Qs, LDK, 16 * vt, pf, c.lane);
@@ -301,10 +307,10 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
         c.g = c.lane >> 4;
         c.c16 = c.lane & 15;
         c.A = reinterpret_cast<T *>(lds);
-        c.Yg = c.A + G * NM * LDA;
-        c.S = c.Yg + G * NM * LDA;
+        c.Yg = c.A + G * CLS;
+        c.S = c.Yg + G * CLS;
         c.cR = reinterpret_cast<float *>(c.S + stage_elems(G));
-        c.cL = c.cR + G * NM;
+        c.cL = c.cR + G * CSF;
         // rows k >= m of the state regions are never written: zero them once
         // (they meet zero probabilities in the products, and 0 * NaN is NaN)
         if (NM > c.m) {

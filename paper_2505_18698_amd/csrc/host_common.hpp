@@ -109,11 +109,12 @@ inline bool grouped_applies(int32_t dtype, int64_t d, int64_t m, int64_t b, bool
 
 // The family that runs a call under `path` (kFamNone: the forced path does
 // not take the shape).  Automatic: the one-workgroup-per-head kernel where it
-// applies; else the grouped kernel where it applies with m <= 32 and T >= 2
-// (measured faster than the half-steps there; with more blocks every group
-// streams more of K and V, and at T = 1 the half-steps are two launches);
-// else the half-steps.  All families give the same bits.
-inline int family_of(int path, int32_t dtype, int64_t d, int64_t m, int64_t b, int T, bool lens, bool obj)
+// applies; else the grouped kernel where it applies with m <= 32 (measured
+// faster than the half-steps there at 16 and 192 heads and T = 1, 2, apart
+// from 24-row blocks at T = 1 with many heads, up to 15% slower; with more
+// blocks every group streams more of K and V); else the half-steps.  All
+// families give the same bits.
+inline int family_of(int path, int32_t dtype, int64_t d, int64_t m, int64_t b, bool lens, bool obj)
 {
     switch (path) {
     case kHalfSteps: return kFamHalf;
@@ -121,7 +122,7 @@ inline int family_of(int path, int32_t dtype, int64_t d, int64_t m, int64_t b, i
     case kGrouped: return grouped_applies(dtype, d, m, b, lens, obj) ? kFamGroup : kFamNone;
     default:
         if (fused_applies(dtype, d, m, b)) return kFamFused;
-        if (grouped_applies(dtype, d, m, b, lens, obj) && m <= 32 && T >= 2) return kFamGroup;
+        if (grouped_applies(dtype, d, m, b, lens, obj) && m <= 32) return kFamGroup;
         return kFamHalf;
     }
 }

@@ -280,7 +280,7 @@ int forward(const void *q, const void *k, const void *v, void *out, float *obj, 
     bool capturing = false;
     if ((rc = check_capture((hipStream_t)stream, capturing)) != MA_OK) return rc;
     std::unique_lock<std::mutex> ws_hold;  // the stream's workspace, held until the launches are enqueued
-    const int fam = family_of(path, dtype, d, m, b, T, need_lens || prepad, need_obj);
+    const int fam = family_of(path, dtype, d, m, b, need_lens || prepad, need_obj);
     const bool states = fam == kFamHalf;  // the other families keep their states in LDS
     const size_t obj_part_bytes = obj ? align_up((size_t)BH * T * b * sizeof(float)) : 0;
     if (states || obj) {
