@@ -545,6 +545,33 @@ struct HeadDims {
 // Row of q, k, v, out in memory for row x (< n) of the kernels' problem.
 __device__ inline int64_t mrow(const HeadDims &hd, int64_t x) { return hd.rev ? (int64_t)hd.n - 1 - x : x; }
 
+// Memory rows of the kernels' rows x0 + i*step (i = 0, 1, ...) are
+// mrow_u<RV>(x0) + i * rstep<RV>(step): the reversal folds into the first row
+// and the sign of the step, so a row address stays one multiply-add.  The
+// half-step kernels compile their unit loop with RV = false for calls without
+// pre-padding (no reversal at all) and RV = true for the rest.
+template <bool RV> __device__ inline int64_t mrow_u(const HeadDims &hd, int64_t x)
+{
+    return RV ? mrow(hd, x) : x;
+}
+template <bool RV> __device__ inline int64_t rstep(const HeadDims &hd, int64_t step)
+{
+    return RV && hd.rev ? -step : step;
+}
+
+// The head dimension as the unit code sees it: the compile-time constant DK
+// when DK != 0 (the kernels run their unit loop with DK = D when d == D, the
+// usual case), else the run-time d.  The row strides of q, k, v, out and of
+// the states, and the column bound of their loads and stores, then fold into
+// constants where the tile is full.
+template <int DK> __device__ inline auto head_dim(int d)
+{
+    if constexpr (DK != 0)
+        return std::integral_constant<int, DK>{};
+    else
+        return d;
+}
+
 // Real rows of head bh.  The kernels read it in fetch() but use it only from
 // stage() on: their tile loads take the static bound n, so that they never
 // wait for this load, and the rows beyond it are zeroed on their way to LDS.
@@ -628,6 +655,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         int nl, row0;                      // real rows of the head, first key row k*b (LENS)
     };
 
+    template <int DK, bool RV>
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, int tid, Regs &gr)
     {
         if constexpr (LENS) {
@@ -635,17 +663,18 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
             gr.row0 = k * hd.b;
         }
         const int m = hd.m, b = hd.b, kv = block_keys(b, hd.n, k);  // rows in memory
-        const int dd = hd.d;
+        const auto dd = head_dim<DK>(hd.d);
         const int64_t N = (int64_t)m * b, hoff = bh * N * dd, toff = bh * (int64_t)hd.n * dd;  // states: rows of d
         const int lane = tid & 63, wave = tid >> 6;
+        const int64_t r0 = (int64_t)k * b, first = mrow_u<RV>(hd, r0), step = rstep<RV>(hd, 1);
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int j = (wave * RT + r) * 16 + (lane & 15);
             const T *row = nullptr;  // alpha_R[k][j]; at t = 1 Q row k*b + j (zero if padding)
             if constexpr (FIRST) {
-                if (j < kv) row = p.q + toff + mrow(hd, (int64_t)k * b + j) * dd;
+                if (j < kv) row = p.q + toff + (first + j * step) * dd;
             } else {
-                if (j < b) row = p.aR + hoff + ((int64_t)k * b + j) * dd;
+                if (j < b) row = p.aR + hoff + (r0 + j) * dd;
             }
             gr.bf[r].load(row, lane >> 4, dd);
             gr.cr[r] = 1.0f;
@@ -655,12 +684,12 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         }
         // K and V after the alpha_R rows, V last: the scores wait for the rows
         // and K only, and V is staged just before the product that needs it
-        const T *kh = p.k + toff;
-        const int64_t r0 = (int64_t)k * b;
-        gr.kt.fetch([=](int r) { return kh + mrow(hd, r0 + r) * dd; }, kv, tid, dd);
+        const int64_t sd = step * dd;
+        const T *kb = p.k + toff + first * dd;
+        gr.kt.fetch([=](int r) { return kb + r * sd; }, kv, tid, dd);
         if constexpr (FINAL) {
-            const T *vh = p.v + toff;
-            gr.vt.fetch([=](int r) { return vh + mrow(hd, r0 + r) * dd; }, kv, tid, dd);
+            const T *vb = p.v + toff + first * dd;
+            gr.vt.fetch([=](int r) { return vb + r * sd; }, kv, tid, dd);
         }
     }
 
@@ -676,6 +705,7 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
     }
 
     // After stage() and a barrier.
+    template <int DK, bool RV>
     __device__ static void compute(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int k, const Regs &gr,
                                    char *lds, int tid)
     {
@@ -684,8 +714,6 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
         // keys >= kv: padding, masked (omega); kv <= 0: padding only, R = 0
         const int m = hd.m, b = hd.b, kv = block_keys(b, LENS ? gr.nl : hd.n, k);
         const int64_t N = (int64_t)m * b;
-        const int dd = hd.d;
-        const int64_t hoff = bh * N * dd;  // states: rows of d elements
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
         int jr[RT];
@@ -756,10 +784,11 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
 #pragma unroll
             for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
         }
+        const auto dd = head_dim<DK>(hd.d);  // states: rows of d elements
 #pragma unroll
         for (int r = 0; r < RT; ++r)  // alpha_L[j][k] (j-major)
-            store_row<T, D>(jr[r] < b ? p.aL + hoff + ((int64_t)jr[r] * m + k) * dd : nullptr, out[r], inv[r], lane,
-                            dd);
+            store_row<T, D>(jr[r] < b ? p.aL + bh * N * dd + ((int64_t)jr[r] * m + k) * dd : nullptr, out[r],
+                            inv[r], lane, dd);
         if constexpr (FINAL) {
             // Vbar[k], staged here rather than with K: when a workgroup runs a
             // single unit, the scores and softmax overlap V's loads
@@ -777,8 +806,8 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
             }
 #pragma unroll
             for (int r = 0; r < RT; ++r)
-                store_row<T, D>(jr[r] < b ? p.Y + hoff + ((int64_t)jr[r] * m + k) * dd : nullptr, out[r], inv[r],
-                                lane, dd);
+                store_row<T, D>(jr[r] < b ? p.Y + bh * N * dd + ((int64_t)jr[r] * m + k) * dd : nullptr, out[r],
+                                inv[r], lane, dd);
         }
     }
 };
@@ -807,19 +836,22 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
         int nl, j;                         // real rows of the head, the class (LENS)
     };
 
+    template <int DK, bool RV>
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, int tid, Regs &gr)
     {
         const int m = hd.m, b = hd.b;
-        const int dd = hd.d;
-        const int64_t N = (int64_t)m * b, hoff = bh * N * dd;  // states: rows of d elements
-        const T *qh = p.q + bh * (int64_t)hd.n * dd;
-        const T *al = p.aL + hoff + (int64_t)j * m * dd;
+        const int64_t N = (int64_t)m * b;
         if constexpr (LENS) {
             gr.nl = live_rows(hd, bh);
             gr.j = j;
         }
         const int ml = (hd.n - j + b - 1) / b;  // rows l of class j in memory: l*b + j < n
-        gr.qt.fetch([=](int l) { return qh + mrow(hd, (int64_t)l * b + j) * dd; }, ml, tid, dd);
+        const auto dd = head_dim<DK>(hd.d);
+        const int64_t hoff = bh * N * dd;  // states: rows of d elements
+        const T *qb = p.q + bh * (int64_t)hd.n * dd + mrow_u<RV>(hd, j) * dd;  // Qbar[j][0]
+        const int64_t sq = rstep<RV>(hd, b) * dd;                           // Qbar[j][l] -> Qbar[j][l + 1]
+        const T *al = p.aL + hoff + (int64_t)j * m * dd;
+        gr.qt.fetch([=](int l) { return qb + l * sq; }, ml, tid, dd);
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * dd; }, m, tid, dd);
         gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
     }
@@ -837,6 +869,7 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
     }
 
     // After stage() and a barrier.
+    template <int DK, bool RV>
     __device__ static void compute(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, const Regs &gr,
                                    char *lds, int tid)
     {
@@ -845,7 +878,6 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
         float *cLs = reinterpret_cast<float *>(APs + AP_ELEMS);
         const int m = hd.m, b = hd.b;
         const int64_t N = (int64_t)m * b;
-        const int64_t hoff = bh * N * hd.d;  // states: rows of d elements
         const int lane = tid & 63, wave = tid >> 6;
         const int g = lane >> 4, c16 = lane & 15;
         const int mk = LENS ? live_blocks(m, b, gr.nl) : m;  // blocks k >= mk: no real key
@@ -985,10 +1017,11 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
 #pragma unroll
             for (int r = 0; r < RT; ++r) out[r][vt] = acc[r];
         }
+        const auto dd = head_dim<DK>(hd.d);  // states: rows of d elements
 #pragma unroll
         for (int r = 0; r < RT; ++r)  // alpha_R[k][j] (k-major)
-            store_row<T, D>(kr[r] < m ? p.aR + hoff + ((int64_t)kr[r] * b + j) * hd.d : nullptr, out[r], 1.0f, lane,
-                            hd.d);
+            store_row<T, D>(kr[r] < m ? p.aR + bh * N * dd + ((int64_t)kr[r] * b + j) * dd : nullptr, out[r],
+                            1.0f, lane, dd);
     }
 };
 
@@ -1010,26 +1043,27 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
         int nl;                            // real rows of the head (LENS)
     };
 
+    template <int DK, bool RV>
     __device__ static void fetch(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, int tid, Regs &gr)
     {
         const int m = hd.m, b = hd.b;
-        const int dd = hd.d;
-        const int64_t N = (int64_t)m * b, hoff = bh * N * dd;  // states: rows of d elements
+        const int64_t N = (int64_t)m * b;
         const int lane = tid & 63, wave = tid >> 6;
+        const auto dd = head_dim<DK>(hd.d);
+        const int64_t hoff = bh * N * dd;  // states: rows of d elements
         const T *al = p.aL + hoff + (int64_t)j * m * dd;
         const T *yj = p.Y + hoff + (int64_t)j * m * dd;
         gr.at.fetch([=](int kk) { return al + (int64_t)kk * dd; }, m, tid, dd);
         gr.yt.fetch([=](int kk) { return yj + (int64_t)kk * dd; }, m, tid, dd);
-        gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
-        if constexpr (LENS) gr.nl = live_rows(hd, bh);
+        const T *qb = p.q + bh * (int64_t)hd.n * dd + mrow_u<RV>(hd, j) * dd;  // Qbar[j][0]
+        const int64_t sq = rstep<RV>(hd, b) * dd;
 #pragma unroll
         for (int r = 0; r < RT; ++r) {
             const int l = (wave * RT + r) * 16 + (lane & 15);
-            gr.bf[r].load((int64_t)l * b + j < hd.n
-                              ? p.q + bh * (int64_t)hd.n * hd.d + mrow(hd, (int64_t)l * b + j) * hd.d
-                              : nullptr,
-                          lane >> 4, hd.d);  // Qbar[j][l]; zero for padded rows
+            gr.bf[r].load((int64_t)l * b + j < hd.n ? qb + l * sq : nullptr, lane >> 4, dd);  // Qbar[j][l]; zero if padded
         }
+        gr.cl = tid < m ? p.cL[bh * N + (int64_t)tid * b + j] : 0.f;
+        if constexpr (LENS) gr.nl = live_rows(hd, bh);
     }
 
     __device__ static void stage(const HeadDims &, const Regs &gr, char *lds, int tid)
@@ -1042,6 +1076,7 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
     }
 
     // After stage() and a barrier.
+    template <int DK, bool RV>
     __device__ static void compute(const Bufs<T> &p, const HeadDims &hd, int64_t bh, int j, const Regs &gr,
                                    char *lds, int tid)
     {
@@ -1127,11 +1162,14 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
 #pragma unroll
             for (int r = 0; r < RT; ++r) o[r][vt] = acc[r];
         }
+        const auto dd = head_dim<DK>(hd.d);
+        T *ob = p.out + bh * (int64_t)hd.n * dd + mrow_u<RV>(hd, j) * dd;  // O[j], row 0 of class j
+        const int64_t so = rstep<RV>(hd, b) * dd;
 #pragma unroll
         for (int r = 0; r < RT; ++r) {  // rows nl..n-1 (batch padding) are written as zero
             const int64_t row = (int64_t)lr[r] * b + j;
-            store_row<T, D>(row < hd.n ? p.out + bh * (int64_t)hd.n * hd.d + mrow(hd, row) * hd.d : nullptr, o[r],
-                            (!LENS || row < nl) ? inv[r] : 0.f, lane, hd.d);
+            store_row<T, D>(row < hd.n ? ob + lr[r] * so : nullptr, o[r], (!LENS || row < nl) ? inv[r] : 0.f, lane,
+                            dd);
         }
     }
 };
@@ -1143,18 +1181,19 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
 // LDS, so that they land while it computes.  `per` is the number of units
 // per head (m for R, b for L).
 // ---------------------------------------------------------------------------------------
-template <typename U, typename T> __device__ inline void run_units(const Bufs<T> &p, const HeadDims &hd, int per, char *lds)
+template <typename U, int DK, bool RV, typename T>
+__device__ inline void run_units_d(const Bufs<T> &p, const HeadDims &hd, int per, char *lds)
 {
     const int tid = threadIdx.x;
     int64_t u = blockIdx.x;
     typename U::Regs cur, nxt;
-    U::fetch(p, hd, u / per, (int)(u % per), tid, cur);
+    U::template fetch<DK, RV>(p, hd, u / per, (int)(u % per), tid, cur);
     while (true) {
         U::stage(hd, cur, lds, tid);
         __syncthreads();
         const int64_t un = u + gridDim.x;
-        if (un < hd.units) U::fetch(p, hd, un / per, (int)(un % per), tid, nxt);
-        U::compute(p, hd, u / per, (int)(u % per), cur, lds, tid);
+        if (un < hd.units) U::template fetch<DK, RV>(p, hd, un / per, (int)(un % per), tid, nxt);
+        U::template compute<DK, RV>(p, hd, u / per, (int)(u % per), cur, lds, tid);
         if (un >= hd.units) break;
         __syncthreads();  // LDS is restaged next
         cur = nxt;
@@ -1162,12 +1201,23 @@ template <typename U, typename T> __device__ inline void run_units(const Bufs<T>
     }
 }
 
+// The unit loop of the usual call (d fills the tile, no pre-padding), with
+// the head dimension a constant and no row reversal, or of any other call
+// (one uniform branch per workgroup; both loops are compiled into the kernel).
+template <typename U, int D, typename T> __device__ inline void run_units(const Bufs<T> &p, const HeadDims &hd, int per, char *lds)
+{
+    if (hd.d == D && !hd.rev)
+        run_units_d<U, D, false>(p, hd, per, lds);
+    else
+        run_units_d<U, 0, true>(p, hd, per, lds);
+}
+
 template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool LENS>
 __global__ __launch_bounds__(64 * Split<NB / 16>::W) void r_half_step(Bufs<T> p, HeadDims hd)
 {
     using U = RHalf<T, NB, D, FIRST, FINAL, RAGGED, LENS>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
-    run_units<U>(p, hd, hd.m, lds);
+    run_units<U, D>(p, hd, hd.m, lds);
 }
 
 template <typename T, int NM, int D, bool RAGGED, bool LENS>
@@ -1175,7 +1225,7 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) void l_half_step(Bufs<T> p,
 {
     using U = LHalf<T, NM, D, RAGGED, LENS>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
-    run_units<U>(p, hd, hd.b, lds);
+    run_units<U, D>(p, hd, hd.b, lds);
 }
 
 template <typename T, int NM, int D, bool RAGGED, bool LENS>
@@ -1183,7 +1233,7 @@ __global__ __launch_bounds__(64 * Split<NM / 16>::W) void monarch_apply(Bufs<T> 
 {
     using U = Apply<T, NM, D, RAGGED, LENS>;
     __shared__ __attribute__((aligned(16))) char lds[U::LDS_BYTES];
-    run_units<U>(p, hd, hd.b, lds);
+    run_units<U, D>(p, hd, hd.b, lds);
 }
 
 // ---------------------------------------------------------------------------------------
