@@ -101,6 +101,26 @@ int main()
     expect(monarch_attn_set_path(7) == -1, "unknown path");
     expect(monarch_attn_set_path(1) == 0 && monarch_attn_set_path(0) == 1, "path round trip");
     expect(std::strlen(monarch_attn_build_id()) == 16, "build id");
+    // the schedule a forward call runs (ma_host::family_of): automatic,
+    // then forced; 16-bit types are 1 (bf16) and 2 (fp16), fp32 is 0
+    using namespace ma_host;
+    expect(family_of(kAuto, MA_BF16, 64, 14, 14, false, false) == kFamFused, "auto: ViT heads in one workgroup");
+    expect(family_of(kAuto, MA_F16, 64, 16, 16, false, false) == kFamFused, "auto: 16 x 16 in one workgroup");
+    expect(family_of(kAuto, MA_BF16, 64, 32, 32, false, false) == kFamGroup, "auto: 32 x 32 grouped");
+    expect(family_of(kAuto, MA_BF16, 48, 17, 8, false, false) == kFamGroup, "auto: m = 17 grouped");
+    expect(family_of(kAuto, MA_BF16, 64, 33, 32, false, false) == kFamHalf, "auto: m = 33 half-steps");
+    expect(family_of(kAuto, MA_BF16, 64, 16, 33, false, false) == kFamHalf, "auto: b = 33 half-steps");
+    expect(family_of(kAuto, MA_BF16, 72, 16, 16, false, false) == kFamHalf, "auto: d = 72 half-steps");
+    expect(family_of(kAuto, MA_F32, 64, 16, 16, false, false) == kFamHalf, "auto: fp32 half-steps");
+    expect(family_of(kAuto, MA_BF16, 64, 32, 32, true, false) == kFamHalf, "auto: lengths half-steps");
+    expect(family_of(kAuto, MA_BF16, 64, 14, 14, true, false) == kFamFused, "auto: lengths, small heads fused");
+    expect(family_of(kAuto, MA_BF16, 64, 32, 32, false, true) == kFamHalf, "auto: objective half-steps");
+    expect(family_of(kAuto, MA_BF16, 64, 128, 128, false, false) == kFamHalf, "auto: 16K half-steps");
+    expect(family_of(kHalfSteps, MA_BF16, 64, 14, 14, false, false) == kFamHalf, "forced half-steps");
+    expect(family_of(kFusedHead, MA_BF16, 64, 17, 16, false, false) == kFamNone, "forced fused, m = 17");
+    expect(family_of(kGrouped, MA_BF16, 64, 64, 32, false, false) == kFamGroup, "forced grouped, m = 64");
+    expect(family_of(kGrouped, MA_BF16, 64, 8, 33, false, false) == kFamNone, "forced grouped, b = 33");
+    expect(family_of(kGrouped, MA_F32, 64, 16, 16, false, false) == kFamNone, "forced grouped, fp32");
     if (fails) return 1;
     std::printf("ABI sanitizer run: ok\n");
     return 0;

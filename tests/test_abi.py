@@ -179,6 +179,20 @@ def test_fused_path_applicability():
     assert not ma.fused_applies(64, 16, 16, ma.MA_F32)
 
 
+def test_grouped_path_applicability():
+    """The binding's mirror of the grouped kernel's scope (the C side is
+    checked in the host-code sanitizer run)."""
+    import paper_2505_18698_amd as ma
+
+    assert ma.grouped_applies(64, 32, 32, ma.MA_BF16)
+    assert ma.grouped_applies(64, 64, 32, ma.MA_F16)
+    assert ma.grouped_applies(48, 1, 1, ma.MA_BF16)
+    assert not ma.grouped_applies(64, 16, 33, ma.MA_BF16)
+    assert not ma.grouped_applies(64, 65, 32, ma.MA_BF16)
+    assert not ma.grouped_applies(72, 16, 16, ma.MA_BF16)
+    assert not ma.grouped_applies(64, 16, 16, ma.MA_F32)
+
+
 def test_timing_read_without_a_timed_call_fails_cleanly():
     import paper_2505_18698_amd as ma
 
