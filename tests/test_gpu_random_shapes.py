@@ -102,6 +102,45 @@ def test_random_forward(ma, case, path):
 
 
 @pytest.mark.parametrize("case", range(40))
+def test_random_grouped(ma, case):
+    """The grouped kernel's scope (16-bit, d <= 64, m <= 64, b <= 32) with
+    head counts from 1 to 96, so that the group size and the number of
+    resident rounds vary: parity with the oracle, and the bits of the
+    half-step kernels."""
+    import torch
+
+    def check(n, d, m, b, T, code):
+        return ma.monarch_attn_check(n, d, m, b, T, code) if b <= 32 else 1
+
+    dtype, B, H, m, b, n, d, T, scale = draw(ma, 7800 + case, 2048, 4, check, max_mb=64, max_d=64,
+                                              dtypes=("bf16", "f16"))
+    H = int(np.random.RandomState(7800 + case).choice([1, 3, 16, 48]))
+    label = f"grouped {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T}"
+    print(label, flush=True)
+    assert ma.grouped_applies(d, m, b, _code(ma, dtype))
+    q, k, v = si.random_qkv(B, H, n, d, dtype, seed=7800 + case, scale=scale)
+    ref = oracle.monarch_attention(q, k, v, m, b, T)
+    outs = {}
+    for path in (ma.PATH_GROUPED, ma.PATH_HALF_STEPS):
+        prev = ma.monarch_attn_set_path(path)
+        try:
+            tq, tk, tv = _to_dev((q, k, v), dtype)
+            out = torch.full_like(tq, float("nan"))
+            ma.monarch_attn_fwd(tq, tk, tv, out, m, b, T)
+            torch.cuda.synchronize()
+        finally:
+            ma.monarch_attn_set_path(prev)
+        outs[path] = out.cpu()
+    assert torch.equal(outs[ma.PATH_GROUPED], outs[ma.PATH_HALF_STEPS]), label
+    o = outs[ma.PATH_GROUPED].double().numpy()
+    assert np.isfinite(o).all(), label
+    err = oracle.rel_frobenius(o, ref)
+    print(f"  rel_frob={err:.3e}", flush=True)
+    assert err <= FWD_TOL[dtype], (label, err)
+    assert_classes(o, ref, b, dtype, label, T)
+
+
+@pytest.mark.parametrize("case", range(40))
 def test_random_small_heads(ma, case):
     """m, b <= 16 and d <= 64 in 16-bit types: the one-workgroup-per-head
     kernel (the automatic path), the grouped kernel and the half-step kernels."""
