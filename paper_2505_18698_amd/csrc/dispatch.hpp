@@ -251,12 +251,11 @@ template <typename U> int group_size(const void *kern, int64_t BH, int b, int nu
     return prev;
 }
 
-template <typename T, int NB, int NM, bool RG>
-int launch_group(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
+template <typename T, int NB, int NM, bool RG, bool YG>
+int launch_group(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c, int G)
 {
-    using U = ma::FusedGroup<T, NB, NM, 64, RG>;
-    auto kern = ma::monarch_fused_group<T, NB, NM, 64, RG>;
-    const int G = group_size<U>((const void *)kern, c.BH, c.b, c.num_cus);
+    using U = ma::FusedGroup<T, NB, NM, 64, RG, YG>;
+    auto kern = ma::monarch_fused_group<T, NB, NM, 64, RG, YG>;
     if (G < 1) return fail(MA_EUNSUPPORTED, "the grouped kernel's LDS does not fit");
     const int lds = U::lds_bytes(G);
     const int per_cu = resident_per_cu_lds((const void *)kern, U::NTH, lds);
@@ -278,10 +277,21 @@ int launch_group(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims
     });
 }
 
+template <typename T, int NB, int NM, bool RG, bool YG> int group_size_of(const CallDims &c)
+{
+    using U = ma::FusedGroup<T, NB, NM, 64, RG, YG>;
+    return group_size<U>((const void *)ma::monarch_fused_group<T, NB, NM, 64, RG, YG>, c.BH, c.b, c.num_cus);
+}
+
+// Full tiles: Y through O where that allows larger groups than Y in LDS
+// (fewer groups stream K and V), else Y in LDS (no round trip of Y).
 template <typename T, int NB, int NM> int dispatch_group_rg(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)
 {
     const bool rg = c.b != NB || c.m != NM || c.n != c.m * c.b;
-    return rg ? launch_group<T, NB, NM, true>(L, B, hd, c) : launch_group<T, NB, NM, false>(L, B, hd, c);
+    if (rg) return launch_group<T, NB, NM, true, false>(L, B, hd, c, group_size_of<T, NB, NM, true, false>(c));
+    const int g_lds = group_size_of<T, NB, NM, false, false>(c), g_out = group_size_of<T, NB, NM, false, true>(c);
+    return g_out > g_lds ? launch_group<T, NB, NM, false, true>(L, B, hd, c, g_out)
+                         : launch_group<T, NB, NM, false, false>(L, B, hd, c, g_lds);
 }
 
 template <typename T, int NB> int dispatch_group_m(Launcher &L, const CallBufs &B, ma::HeadDims hd, const CallDims &c)

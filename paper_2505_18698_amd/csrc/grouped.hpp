@@ -12,8 +12,17 @@
 //             after it (the R half-step of block k reads slot (jj, k) and
 //             writes it back; the L half-step of class j0+jj reads and writes
 //             the slots (jj, *), so both update in place)
-//   Y[jj][k]  Y[j0+jj][k] (last step)
+//   Y[jj][k]  Y[j0+jj][k] (last step; only where the tiles are ragged)
 //   cR[jj][k], cL[jj][k] in fp32.
+//
+// With YG (full tiles only: n = m b, m and b the tile sizes), Y goes
+// through the output tensor instead: Y[j][k] is stored at row k*b + j of O,
+// a row of class j, and the last L half-step of class j stages its Y rows
+// into the wave's staging area before it overwrites the same rows with O.
+// That halves the LDS of a class, so up to twice as many classes share a
+// workgroup, and K and V are streamed once per group and step.  It costs a
+// round trip of Y through memory, so the host takes it only where it
+// allows larger groups.
 //
 // Only Q, K, V and O touch global memory: K (and V) are streamed block by
 // block in every R half-step, from the L2 that the other groups of the same
@@ -30,8 +39,9 @@
 
 namespace ma {
 
-template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
+template <typename T, int NB, int NM, int D, bool RG, bool YG> struct FusedGroup {
     static_assert(sizeof(T) == 2, "16-bit elements only");
+    static_assert(!(RG && YG), "Y through O needs full tiles");
     static constexpr int W = 8, NTH = 64 * W;
     static constexpr int NTB = NB / 16, NTM = NM / 16;
     static constexpr int LDA = D + 8;                 // state rows: 16 bytes of padding
@@ -53,11 +63,12 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
         return W * SW_R > (G < W ? G : W) * SW_L ? W * SW_R : (G < W ? G : W) * SW_L;
     }
     static constexpr bool NFR = NormFirst<NTB, D>::value, NFL = NormFirst<NTM, D>::value;
+    static constexpr int NREG = YG ? 1 : 2;  // state regions: A, and Y unless it goes through O
 
     // LDS bytes for G classes per workgroup
     __host__ __device__ static constexpr int lds_bytes(int G)
     {
-        return (2 * G * CLS + stage_elems(G)) * (int)sizeof(T) + 2 * G * CSF * 4;
+        return (NREG * G * CLS + stage_elems(G)) * (int)sizeof(T) + 2 * G * CSF * 4;
     }
 
     struct Ctx {
@@ -145,7 +156,10 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
             asm volatile("" ::: "memory");
 #pragma unroll
             for (int q = 0; q < D / 16; ++q) out[q] = gemm_aggregate<T, NTB>(Vs, LDK, 16 * q, pf, c.lane) * inv;
-            store_row_lds<T, D>(jv ? slot(c.Yg, jj, k) : nullptr, out, c.lane);  // Y[j][k]
+            if constexpr (YG)  // Y[j][k] at row k*b + j of O
+                store_row<T, D>(jv ? c.oh + ((int64_t)k * c.b + j) * c.d : nullptr, out, 1.0f, c.lane, c.d);
+            else
+                store_row_lds<T, D>(jv ? slot(c.Yg, jj, k) : nullptr, out, c.lane);  // Y[j][k]
         }
     }
 
@@ -203,14 +217,15 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
         return 16 * r + c.c16 < c.m ? fast_rcp(sum) : 0.f;  // padded query rows carry no weight
     }
 
-    // Qbar[j] rows l into registers: rows l*b + j < n, zero beyond.
-    __device__ static void fetch_qbar(const Ctx &c, int j, TileChunks<T, NM, D, 64> &qt)
+    // The rows l*b + j < n of class j of a [n][d] tensor (Qbar[j] of q; with
+    // Y through O, Y[j] of out) into registers, zero beyond.
+    __device__ static void fetch_class(const Ctx &c, const T *base, int j, TileChunks<T, NM, D, 64> &qt)
     {
         const int ml = (c.n - j + c.b - 1) / c.b;
-        const T *qh = c.qh;
         const int b = c.b, d = c.d;
-        qt.fetch([=](int l) { return qh + ((int64_t)l * b + j) * d; }, ml, c.lane, d);
+        qt.fetch([=](int l) { return base + ((int64_t)l * b + j) * d; }, ml, c.lane, d);
     }
+    __device__ static void fetch_qbar(const Ctx &c, int j, TileChunks<T, NM, D, 64> &qt) { fetch_class(c, c.qh, j, qt); }
 
     // L half-step of class j0 + jj (one wave): alpha_R[:][j] and c_R[:][j]
     // over the slots (jj, *).  qt holds Qbar[j] on entry; once it is in LDS
@@ -260,7 +275,19 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
     __device__ static void apply_class(const Ctx &c, int jj)
     {
         const int j = c.j0 + jj;
-        const T *Yj = slot(c.Yg, jj, 0);
+        const T *Yj;
+        int ldy;
+        if constexpr (YG) {  // Y[j] from the rows of O that this class is about to overwrite
+            T *Ys = c.S + c.wave * SW_L;
+            TileChunks<T, NM, D, 64> yt;
+            fetch_class(c, c.oh, j, yt);
+            yt.template stage<LDK>(Ys, c.lane);  // (a wave's LDS accesses take effect in order)
+            Yj = Ys;
+            ldy = LDK;
+        } else {
+            Yj = slot(c.Yg, jj, 0);
+            ldy = LDA;
+        }
         RowFrags<T, D> bf;
         {
             const int64_t row = (int64_t)c.c16 * c.b + j;
@@ -283,7 +310,7 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
             pf.pack(sc);
             f32x4 o[D / 16];
 #pragma unroll
-            for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, NTM>(Yj, LDA, 16 * vt, pf, c.lane);
+            for (int vt = 0; vt < D / 16; ++vt) o[vt] = gemm_aggregate<T, NTM>(Yj, ldy, 16 * vt, pf, c.lane);
             const int64_t row = (int64_t)(16 * r + c.c16) * c.b + j;
             store_row<T, D>(row < c.n ? c.oh + row * c.d : nullptr, o, inv, c.lane, c.d);
         }
@@ -307,16 +334,16 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
         c.g = c.lane >> 4;
         c.c16 = c.lane & 15;
         c.A = reinterpret_cast<T *>(lds);
-        c.Yg = c.A + G * CLS;
-        c.S = c.Yg + G * CLS;
+        c.Yg = YG ? nullptr : c.A + G * CLS;
+        c.S = c.A + NREG * G * CLS;
         c.cR = reinterpret_cast<float *>(c.S + stage_elems(G));
         c.cL = c.cR + G * CSF;
         // rows k >= m of the state regions are never written: zero them once
         // (they meet zero probabilities in the products, and 0 * NaN is NaN)
         if (NM > c.m) {
-            for (int idx = tid; idx < 2 * G * (NM - c.m) * (D / 8); idx += NTH) {
+            for (int idx = tid; idx < NREG * G * (NM - c.m) * (D / 8); idx += NTH) {
                 const int col = (idx % (D / 8)) * 8, rest = idx / (D / 8);
-                const int k = c.m + rest % (NM - c.m), jr = rest / (NM - c.m);  // jr < 2 G: region jr / G
+                const int k = c.m + rest % (NM - c.m), jr = rest / (NM - c.m);  // jr < NREG G: region jr / G
                 T *base = jr < G ? c.A : c.Yg;
                 *reinterpret_cast<u32x4 *>(slot(base, jr % G, k) + col) = u32x4{0u, 0u, 0u, 0u};
             }
@@ -357,12 +384,12 @@ template <typename T, int NB, int NM, int D, bool RG> struct FusedGroup {
     }
 };
 
-template <typename T, int NB, int NM, int D, bool RG>
+template <typename T, int NB, int NM, int D, bool RG, bool YG>
 __global__ __launch_bounds__(512) void monarch_fused_group(Bufs<T> p, HeadDims hd, int G, int groups, int64_t units,
                                                            int xcd_perm, int T_)
 {
     extern __shared__ __attribute__((aligned(16))) char lds_dyn[];
-    FusedGroup<T, NB, NM, D, RG>::run(p, hd, G, groups, units, xcd_perm, T_, lds_dyn);
+    FusedGroup<T, NB, NM, D, RG, YG>::run(p, hd, G, groups, units, xcd_perm, T_, lds_dyn);
 }
 
 }  // namespace ma

@@ -319,6 +319,8 @@ def test_fused_and_half_steps_agree_bitwise(lib, dtype, B, H, m, b, T):
         (1, 16, 2048, 64, 32, 64, 1),     # 64 blocks of 32, T = 1 .. 3
         (1, 16, 2048, 64, 32, 64, 3),
         (2, 6, 1024, 32, 32, 64, 2),      # RoBERTa blocks
+        (16, 12, 1024, 32, 32, 64, 2),    # RoBERTa-base, 192 heads: Y through O, 16 classes a group
+        (8, 12, 512, 32, 16, 64, 1),      # 96 heads of 32 x 16: Y through O
         (3, 5, 196, 14, 14, 64, 2),       # ViT
         (3, 5, 197, 15, 14, 64, 2),       # ViT with its class token (padded)
         (1, 16, 256, 16, 16, 64, 2),      # one class per workgroup
