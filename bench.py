@@ -814,7 +814,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}, WORLD_SIZE {world}); "
-              "the forward pass is not sharded across GPUs in this build.", file=sys.stderr)
+              "the forward pass is not sharded across GPUs (heads would split across them with no communication).", file=sys.stderr)
         sys.exit(2)
 
     import torch
