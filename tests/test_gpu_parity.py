@@ -77,9 +77,9 @@ def gpu_run(ma, q, k, v, m, b, T, dtype):
     return out.double().cpu().numpy()
 
 
-def check(o, ref, dtype, label="", b=None, T=1):
+def check(o, ref, dtype, label="", b=None):
     """Whole-tensor bar, and with b (the block size of a Monarch output) the
-    bar on every residue class (parity.class_bar, which depends on T)."""
+    bar on every residue class (parity.class_bar: twice the whole-tensor bar)."""
     err = oracle.rel_frobenius(o, ref)
     per_head = [oracle.rel_frobenius(o[i, h], ref[i, h]) for i in range(o.shape[0]) for h in range(o.shape[1])]
     msg = f"{label} rel_frob={err:.3e} max_head={max(per_head):.3e}"
@@ -91,7 +91,7 @@ def check(o, ref, dtype, label="", b=None, T=1):
     assert np.isfinite(o).all()
     assert err <= TOL[dtype], (label, err)
     if cls is not None:
-        assert cls <= parity.class_bar(dtype, TOL[dtype], T), (label, cls, where)
+        assert cls <= parity.class_bar(TOL[dtype]), (label, cls, where)
     return err
 
 
@@ -117,14 +117,14 @@ def test_random_shapes(ma, dtype, B, H, m, b, d, T):
     q, k, v = si.random_qkv(B, H, m * b, d, dtype, seed=m * 1000 + b, scale=1.5)
     ref = oracle.monarch_attention(q, k, v, m, b, T)
     o = gpu_run(ma, q, k, v, m, b, T, dtype)
-    check(o, ref, dtype, f"{dtype} B{B} H{H} m{m} b{b} d{d} T{T}", b=b, T=T)
+    check(o, ref, dtype, f"{dtype} B{B} H{H} m{m} b{b} d{d} T{T}", b=b)
 
 
 def test_tiny_f32_workload(ma):
     w = si.WORKLOADS["tiny_f32_n256"]
     q, k, v, _ = si.make_qkv(w)
     ref = oracle.monarch_attention(q, k, v, w.m, w.b, w.T)
-    check(gpu_run(ma, q, k, v, w.m, w.b, w.T, w.dtype), ref, w.dtype, w.name, b=w.b, T=w.T)
+    check(gpu_run(ma, q, k, v, w.m, w.b, w.T, w.dtype), ref, w.dtype, w.name, b=w.b)
 
 
 @pytest.mark.parametrize("name", ["vit_b16_n196", "roberta_n1024"])
@@ -132,7 +132,7 @@ def test_full_workloads(ma, name):
     w = si.WORKLOADS[name]
     q, k, v, _ = si.make_qkv(w)
     ref = oracle.monarch_attention(q, k, v, w.m, w.b, w.T)
-    check(gpu_run(ma, q, k, v, w.m, w.b, w.T, w.dtype), ref, w.dtype, w.name, b=w.b, T=w.T)
+    check(gpu_run(ma, q, k, v, w.m, w.b, w.T, w.dtype), ref, w.dtype, w.name, b=w.b)
 
 
 @pytest.mark.parametrize("T", [1, 2, 3])
@@ -140,7 +140,7 @@ def test_speed_n4096(ma, T):
     w = si.WORKLOADS["speed_n4096"].with_(T=T)
     q, k, v, _ = si.make_qkv(w)
     ref = oracle.monarch_attention(q, k, v, w.m, w.b, w.T)
-    check(gpu_run(ma, q, k, v, w.m, w.b, w.T, w.dtype), ref, w.dtype, f"{w.name} T{T}", b=w.b, T=T)
+    check(gpu_run(ma, q, k, v, w.m, w.b, w.T, w.dtype), ref, w.dtype, f"{w.name} T{T}", b=w.b)
 
 
 @pytest.mark.parametrize("d", [64, 128])
@@ -153,7 +153,7 @@ def test_speed_n16384_sampled_heads(ma, d):
     assert np.isfinite(o).all()
     heads = [0, 11]
     ref = oracle.monarch_attention(q[:, heads], k[:, heads], v[:, heads], w.m, w.b, w.T)
-    check(o[:, heads], ref, w.dtype, f"{w.name} d{d} heads{heads}", b=w.b, T=w.T)
+    check(o[:, heads], ref, w.dtype, f"{w.name} d{d} heads{heads}", b=w.b)
 
 
 # -- special cases with a textbook answer ---------------------------------------------
@@ -164,7 +164,7 @@ def test_single_block_equals_softmax_attention(ma, dtype, m, b):
     q, k, v = si.random_qkv(1, 2, m * b, 64, dtype, seed=7, scale=1.5)
     o = gpu_run(ma, q, k, v, m, b, 2, dtype)
     ref = np.stack([[nv.dense_softmax_attention(q[0, h], k[0, h], v[0, h]) for h in range(2)]])
-    check(o, ref, dtype, f"exact m{m} b{b}", b=b, T=2)
+    check(o, ref, dtype, f"exact m{m} b{b}", b=b)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -174,7 +174,7 @@ def test_identical_queries_equal_softmax_attention(ma, dtype):
     q[:] = q[:, :, :1]
     o = gpu_run(ma, q, k, v, m, b, 2, dtype)
     ref = nv.dense_softmax_attention(q[0, 0], k[0, 0], v[0, 0])[None, None]
-    check(o, ref, dtype, "identical queries", b=b, T=2)
+    check(o, ref, dtype, "identical queries", b=b)
 
 
 def test_zero_keys_give_mean_of_values(ma):
@@ -271,7 +271,7 @@ def test_fused_path_unsupported_shape_is_rejected(lib):
     finally:
         lib.monarch_attn_set_path(prev)
     ref = oracle.monarch_attention(q, k, v, m, b, 2)
-    check(out.double().cpu().numpy(), ref, "bf16", "auto fallback m8 b40", b=b, T=2)
+    check(out.double().cpu().numpy(), ref, "bf16", "auto fallback m8 b40", b=b)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
@@ -422,7 +422,7 @@ def test_padded_lengths(ma, B, H, n, m, b, T, dtype):
     q, k, v = si.random_qkv(B, H, n, 64, dtype, seed=n + 31 * b, scale=1.5)
     ref = oracle.monarch_attention(q, k, v, m, b, T)
     o = gpu_run_padded(ma, q, k, v, m, b, T, dtype)
-    check(o, ref, dtype, f"padded {dtype} B{B} H{H} N{n} m{m} b{b} T{T}", b=b, T=T)
+    check(o, ref, dtype, f"padded {dtype} B{B} H{H} N{n} m{m} b{b} T{T}", b=b)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -432,7 +432,7 @@ def test_padded_single_block_is_exact_attention(ma, dtype):
     q, k, v = si.random_qkv(1, 2, n, 64, dtype, seed=12, scale=1.5)
     o = gpu_run_padded(ma, q, k, v, 1, b, 2, dtype)
     ref = np.stack([[nv.dense_softmax_attention(q[0, h], k[0, h], v[0, h]) for h in range(2)]])
-    check(o, ref, dtype, "padded exact m1 b16 N5", b=b, T=2)
+    check(o, ref, dtype, "padded exact m1 b16 N5", b=b)
 
 
 @pytest.mark.parametrize("n,m,b", [(197, 15, 14), (250, 16, 16), (37, 3, 13)])
@@ -477,7 +477,7 @@ def test_other_head_dims(ma, B, H, n, m, b, d, T, dtype):
     q, k, v = si.random_qkv(B, H, n, d, dtype, seed=d * 13 + n, scale=1.5)
     ref = oracle.monarch_attention(q, k, v, m, b, T)
     o = gpu_run_padded(ma, q, k, v, m, b, T, dtype)
-    check(o, ref, dtype, f"{dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T}", b=b, T=T)
+    check(o, ref, dtype, f"{dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T}", b=b)
 
 
 @pytest.mark.parametrize(
@@ -492,7 +492,7 @@ def test_rectangular_blocks(ma, n, m, b, T):
     heads = [0, 2]
     o = gpu_run_padded(ma, q, k, v, m, b, T, "bf16")
     ref = oracle.monarch_attention(q[:, heads], k[:, heads], v[:, heads], m, b, T)
-    check(o[:, heads], ref, "bf16", f"rect N{n} m{m} b{b} T{T}", b=b, T=T)
+    check(o[:, heads], ref, "bf16", f"rect N{n} m{m} b{b} T{T}", b=b)
 
 
 # -- the objective per step (convergence diagnostic) ---------------------------------------
@@ -531,7 +531,7 @@ def test_objective_matches_oracle(ma, B, H, n, m, b, T, dtype):
     q, k, v = si.random_qkv(B, H, n, 64, dtype, seed=n + T, scale=1.5)
     o, f = gpu_objective(ma, q, k, v, m, b, T, dtype)
     ref_o, ref_f = oracle.monarch_attention_objective(q, k, v, m, b, T)
-    check(o, ref_o, dtype, f"objective call O {dtype} N{n} m{m} b{b} T{T}", b=b, T=T)
+    check(o, ref_o, dtype, f"objective call O {dtype} N{n} m{m} b{b} T{T}", b=b)
     rel = np.abs(f - ref_f).max() / np.abs(ref_f).max()
     print(f"objective {dtype} N{n} m{m} b{b} T{T}: max rel err {rel:.3e}; f = {f[0, 0]}", flush=True)
     assert np.isfinite(f).all()
@@ -659,7 +659,7 @@ def test_concurrent_streams_get_separate_workspaces(lib):
         assert not errors, errors
         torch.cuda.synchronize()
         for o, ref, shape in zip(outs, refs, shapes):
-            check(o.double().cpu().numpy(), ref, "bf16", "concurrent streams", b=shape[3], T=shape[5])
+            check(o.double().cpu().numpy(), ref, "bf16", "concurrent streams", b=shape[3])
     finally:
         lib.monarch_attn_set_path(prev)
 

@@ -97,7 +97,7 @@ def test_prepad_matches_oracle(ma, B, H, n, m, b, d, T, dtype):
     print(f"prepad {ma.path_name} {dtype} B{B} H{H} N{n} m{m} b{b} d{d} T{T}: rel_frob={err:.3e} "
           f"max_class={cls:.3e} at {where}", flush=True)
     assert err <= TOL[dtype]
-    assert cls <= parity.class_bar(dtype, TOL[dtype], T)
+    assert cls <= parity.class_bar(TOL[dtype])
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])

@@ -63,10 +63,10 @@ def draw(ma, seed, max_np, max_t, check, max_mb=128, max_d=128, dtypes=("f32", "
         return dtype, B, H, m, b, n, d, T, scale
 
 
-def assert_classes(o, ref, b, dtype, label, T):
+def assert_classes(o, ref, b, dtype, label):
     cls, where = parity.worst_class(o, ref, b)
     print(f"  max_class={cls:.3e} at (batch, head, j)={where}", flush=True)
-    assert cls <= parity.class_bar(dtype, FWD_TOL[dtype], T), (label, cls, where)
+    assert cls <= parity.class_bar(FWD_TOL[dtype]), (label, cls, where)
 
 
 def _to_dev(arrays, dtype):
@@ -98,7 +98,7 @@ def test_random_forward(ma, case, path):
     err = oracle.rel_frobenius(o, ref)
     print(f"  rel_frob={err:.3e}", flush=True)
     assert err <= FWD_TOL[dtype], (label, err)
-    assert_classes(o, ref, b, dtype, label, T)
+    assert_classes(o, ref, b, dtype, label)
 
 
 @pytest.mark.parametrize("case", range(40))
@@ -137,7 +137,7 @@ def test_random_grouped(ma, case):
     err = oracle.rel_frobenius(o, ref)
     print(f"  rel_frob={err:.3e}", flush=True)
     assert err <= FWD_TOL[dtype], (label, err)
-    assert_classes(o, ref, b, dtype, label, T)
+    assert_classes(o, ref, b, dtype, label)
 
 
 @pytest.mark.parametrize("case", range(40))
@@ -168,7 +168,7 @@ def test_random_small_heads(ma, case):
         err = oracle.rel_frobenius(o, ref)
         print(f"  path {path} rel_frob={err:.3e}", flush=True)
         assert err <= FWD_TOL[dtype], (label, path, err)
-        assert_classes(o, ref, b, dtype, (label, path), T)
+        assert_classes(o, ref, b, dtype, (label, path))
 
 
 @pytest.mark.parametrize("case", range(40))
@@ -252,7 +252,7 @@ def test_random_objective(ma, case):
     print(f"  rel_frob={err:.3e} objective max rel err={rel:.3e}", flush=True)
     assert err <= FWD_TOL[dtype], (label, err)
     assert rel <= OBJ_TOL[dtype], (label, rel)
-    assert_classes(o, ref_o, b, dtype, label, T)
+    assert_classes(o, ref_o, b, dtype, label)
 
 
 def _lens(rs, B, n, b):
@@ -316,7 +316,7 @@ def test_random_long_sequences(ma, case):
     err = oracle.rel_frobenius(o, ref)
     print(f"  rel_frob={err:.3e}", flush=True)
     assert err <= FWD_TOL[dtype], (label, err)
-    assert_classes(o, ref, b, dtype, label, T)
+    assert_classes(o, ref, b, dtype, label)
 
 
 def _max_t(ma, dtype, fp32_max, bwd=False):
@@ -356,7 +356,33 @@ def test_maximum_step_count_forward(ma, dtype, path, m, b, d):
     print(f"{label}: rel_frob={err:.3e} objective={rel:.3e}", flush=True)
     assert np.isfinite(o).all() and np.isfinite(f).all()
     assert err <= FWD_TOL[dtype] and rel <= OBJ_TOL[dtype], (label, err, rel)
-    assert_classes(o, ref_o, b, dtype, label, T)
+    assert_classes(o, ref_o, b, dtype, label)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("T", [3, 4])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_ill_conditioned_class(ma, dtype, T, seed):
+    """The random shape whose worst residue class is the most sensitive found
+    (m = 59, b = 38, d = 112: the fp64 method moves that class by up to
+    9.4e-2 at T = 4 under half an ulp of its bf16 inputs), at the largest
+    16-bit step counts: every class within twice the whole-tensor bar."""
+    import torch
+
+    m, b, d = 59, 38, 112
+    n = m * b - 7 * seed
+    q, k, v = si.random_qkv(1, 2, n, d, dtype, seed=1000 + seed, scale=1.5)
+    ref = oracle.monarch_attention(q, k, v, m, b, T)
+    tq, tk, tv = _to_dev((q, k, v), dtype)
+    out = torch.full_like(tq, float("nan"))
+    ma.monarch_attn_fwd(tq, tk, tv, out, m, b, T)
+    torch.cuda.synchronize()
+    o = out.double().cpu().numpy()
+    err = oracle.rel_frobenius(o, ref)
+    label = f"ill-conditioned {dtype} T{T} seed{seed} N{n}"
+    print(f"{label}: rel_frob={err:.3e}", flush=True)
+    assert np.isfinite(o).all() and err <= FWD_TOL[dtype], (label, err)
+    assert_classes(o, ref, b, dtype, label)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
