@@ -30,6 +30,39 @@ def class_errors(o, ref, b):
     return rel
 
 
+def block_errors(o, ref, b):
+    """Relative Frobenius error of every (batch, head, key block k) of
+    [B, H, N, d] arrays: the rows k*b .. k*b + b - 1 < N, which the R update
+    of block k (eq. R_update) reads together.  Zero references count as in
+    class_errors."""
+    o = np.asarray(o, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    B, H, N, d = ref.shape
+    m = -(-N // b)
+    pad = m * b - N
+    diff = o - ref
+    if pad:
+        z = np.zeros((B, H, pad, d))
+        diff = np.concatenate([diff, z], axis=2)
+        ref = np.concatenate([ref, z], axis=2)
+    num = np.sqrt((diff.reshape(B, H, m, b, d) ** 2).sum(axis=(3, 4)))
+    den = np.sqrt((ref.reshape(B, H, m, b, d) ** 2).sum(axis=(3, 4)))
+    with np.errstate(divide="ignore", invalid="ignore"):
+        return np.where(den > 0, num / np.where(den > 0, den, 1.0), np.where(num > 0, np.inf, 0.0))
+
+
+def worst_grad_unit(dq, dk, dv, ref_dq, ref_dk, ref_dv, b):
+    """The largest error of one residue class of dQ (rows l*b + j, as for O)
+    and of one key block of dK and dV, with its (name, (batch, head, unit))."""
+    out = []
+    for name, x, r, f in (("dq", dq, ref_dq, class_errors), ("dk", dk, ref_dk, block_errors),
+                          ("dv", dv, ref_dv, block_errors)):
+        rel = f(x, r, b)
+        idx = np.unravel_index(int(np.argmax(rel)), rel.shape)
+        out.append((float(rel[idx]), name, tuple(int(i) for i in idx)))
+    return max(out)
+
+
 def worst_class(o, ref, b):
     """The largest class error (see class_errors) and its (batch, head, j)."""
     rel = class_errors(o, ref, b)

@@ -60,16 +60,26 @@ def oracle_grads(q, k, v, dout, m, b, T, heads):
     return res
 
 
-def check(got, ref, heads, dtype, label):
-    errs = []
+def check(got, ref, heads, dtype, label, b=None):
+    """Whole-tensor bar on each gradient over the checked heads and, with b,
+    twice that bar on every residue class of dQ and key block of dK, dV."""
+    errs, sel = [], []
     for name, x, r in zip(("dq", "dk", "dv"), got, ref):
         xs = np.stack([x[i, h] for i, h in heads])
         rs = np.stack([r[i, h] for i, h in heads])
         assert np.isfinite(x).all(), (label, name, "non-finite or unwritten elements")
         errs.append(oracle.rel_frobenius(xs, rs))
-    print(f"{label} rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
+        sel.append((xs[None], rs[None]))
+    msg = f"{label} rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}"
+    unit = None
+    if b is not None:
+        unit = parity.worst_grad_unit(sel[0][0], sel[1][0], sel[2][0], sel[0][1], sel[1][1], sel[2][1], b)
+        msg += f" max_unit={unit[0]:.3e} ({unit[1]} at {unit[2]})"
+    print(msg, flush=True)
     for name, e in zip(("dq", "dk", "dv"), errs):
         assert e <= TOL[dtype], (label, name, e)
+    if unit is not None:
+        assert unit[0] <= parity.class_bar(TOL[dtype]), (label, unit)
     return errs
 
 
@@ -79,7 +89,7 @@ def run_case(ma, B, H, n, m, b, d, T, dtype, seed=0, heads=None, scale=1.5):
     heads = heads or [(i, h) for i in range(B) for h in range(H)]
     got = gpu_grads(ma, q, k, v, dout, m, b, T, dtype)
     ref = oracle_grads(q, k, v, dout, m, b, T, heads)
-    return check(got, ref, heads, dtype, f"{dtype} B{B} H{H} n{n} m{m} b{b} d{d} T{T}")
+    return check(got, ref, heads, dtype, f"{dtype} B{B} H{H} n{n} m{m} b{b} d{d} T{T}", b)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
@@ -184,7 +194,7 @@ def test_dit_workload_sampled_heads(ma):
     heads = [(0, 0), (13, 7), (31, 15)]
     got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
     ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
-    check(got, ref, heads, w.dtype, w.name)
+    check(got, ref, heads, w.dtype, w.name, w.b)
 
 
 @pytest.mark.parametrize("T", [1, 3])
@@ -200,7 +210,7 @@ def test_single_block_is_softmax_attention(ma, n, T):
     for h in range(2):
         for r, g in zip(ref, ob.attention_grads(q[0, h], k[0, h], v[0, h], dout[0, h])):
             r[0, h] = g
-    check(got, ref, [(0, 0), (0, 1)], "f32", f"softmax n{n} T{T}")
+    check(got, ref, [(0, 0), (0, 1)], "f32", f"softmax n{n} T{T}", n)
 
 
 def test_deterministic(ma):
@@ -250,7 +260,7 @@ def test_speed_n4096_sampled_heads(ma, T):
     heads = [(0, 0), (0, 7), (0, 15)]
     got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
     ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
-    check(got, ref, heads, w.dtype, f"{w.name} T{T}")
+    check(got, ref, heads, w.dtype, f"{w.name} T{T}", w.b)
 
 
 def test_vit_workload_sampled_heads(ma):
@@ -261,7 +271,7 @@ def test_vit_workload_sampled_heads(ma):
     heads = [(0, 0), (5, 3), (17, 11), (31, 6)]
     got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
     ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
-    check(got, ref, heads, w.dtype, w.name)
+    check(got, ref, heads, w.dtype, w.name, w.b)
 
 
 def test_forward_and_gradient_calls_share_the_workspace(ma):
@@ -285,7 +295,7 @@ def test_forward_and_gradient_calls_share_the_workspace(ma):
                 assert err <= 2e-2, ("forward", rnd, n, err)
                 got = gpu_grads(ma, q, k, v, dout, m, b, T, "bf16")
                 ref = oracle_grads(q, k, v, dout, m, b, T, [(0, 0)])
-                check(got, ref, [(0, 0)], "bf16", f"interleaved round {rnd} n{n} m{m} b{b} d{d} T{T}")
+                check(got, ref, [(0, 0)], "bf16", f"interleaved round {rnd} n{n} m{m} b{b} d{d} T{T}", b)
             if rnd == 0:
                 ma.monarch_attn_release_workspace()
     finally:
@@ -301,7 +311,7 @@ def test_long_sequence_sampled_heads(ma, name, heads):
     dout = si.random_cotangent((w.B, w.H, w.N, w.d), w.dtype, seed=3)
     got = gpu_grads(ma, q, k, v, dout, w.m, w.b, w.T, w.dtype)
     ref = oracle_grads(q, k, v, dout, w.m, w.b, w.T, heads)
-    check(got, ref, heads, w.dtype, name)
+    check(got, ref, heads, w.dtype, name, w.b)
 
 
 def test_timing_reports_every_gradient_launch(ma):
@@ -341,7 +351,7 @@ def test_autograd_function_matches_oracle(ma):
     torch.cuda.synchronize()
     got = [x.grad.double().cpu().numpy() for x in (tq, tk, tv)]
     ref = oracle_grads(q, k, v, g, m, b, T, [(0, 0), (0, 1)])
-    check(got, ref, [(0, 0), (0, 1)], "bf16", "autograd function")
+    check(got, ref, [(0, 0), (0, 1)], "bf16", "autograd function", b)
     fwd = oracle.monarch_attention(q, k, v, m, b, T)
     assert oracle.rel_frobenius(out.detach().double().cpu().numpy(), fwd) <= 2e-2
 

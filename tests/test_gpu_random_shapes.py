@@ -222,9 +222,12 @@ def test_random_gradient(ma, case):
     for name, x, w in zip(("dq", "dk", "dv"), got, want):
         assert np.isfinite(x).all(), (label, name)
         errs.append(oracle.rel_frobenius(x, w))
-    print(f"  rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
+    unit = parity.worst_grad_unit(*got, *want, b)
+    print(f"  rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e} max_unit={unit[0]:.3e} ({unit[1]} at {unit[2]})",
+          flush=True)
     for name, e in zip(("dq", "dk", "dv"), errs):
         assert e <= BWD_TOL[dtype], (label, name, e)
+    assert unit[0] <= parity.class_bar(BWD_TOL[dtype]), (label, unit)
 
 
 # relative to max |f|; the derivation is beside the objective parity test
@@ -280,6 +283,7 @@ def test_random_padded_batch_gradient(ma, case):
     torch.cuda.synchronize()
     got = [x.double().cpu().numpy() for x in outs]
     have, want = [[], [], []], [[], [], []]
+    full = [np.zeros(q.shape) for _ in range(3)]  # the references, zero past each length
     for bi, ln in enumerate(lens):
         for x in got:
             assert np.isfinite(x).all(), label
@@ -290,11 +294,15 @@ def test_random_padded_batch_gradient(ma, case):
             for c in range(3):
                 want[c].append(ref[c].ravel())
                 have[c].append(got[c][bi, h, :ln].ravel())
+                full[c][bi, h, :ln] = ref[c]
     errs = [oracle.rel_frobenius(np.concatenate(x), np.concatenate(w)) if np.concatenate(w).size else 0.0
             for x, w in zip(have, want)]
-    print(f"  rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
+    unit = parity.worst_grad_unit(*got, *full, b)
+    print(f"  rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e} max_unit={unit[0]:.3e} ({unit[1]} at {unit[2]})",
+          flush=True)
     for name, e in zip(("dq", "dk", "dv"), errs):
         assert e <= BWD_TOL[dtype], (label, name, e)
+    assert unit[0] <= parity.class_bar(BWD_TOL[dtype]), (label, unit)
 
 
 @pytest.mark.parametrize("case", range(12))
@@ -406,8 +414,11 @@ def test_maximum_step_count_gradient(ma, dtype):
         for w, r in zip(want, ob.autograd_grads(q[0, h], k[0, h], v[0, h], g[0, h], m, b, T)):
             w[0, h] = r
     errs = [oracle.rel_frobenius(x, w) for x, w in zip(got, want)]
-    print(f"T={T} gradient {dtype}: rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e}", flush=True)
+    unit = parity.worst_grad_unit(*got, *want, b)
+    print(f"T={T} gradient {dtype}: rel_frob dq={errs[0]:.3e} dk={errs[1]:.3e} dv={errs[2]:.3e} "
+          f"max_unit={unit[0]:.3e} ({unit[1]} at {unit[2]})", flush=True)
     for x in got:
         assert np.isfinite(x).all()
     for e in errs:
         assert e <= BWD_TOL[dtype], (dtype, T, errs)
+    assert unit[0] <= parity.class_bar(BWD_TOL[dtype]), (dtype, T, unit)
