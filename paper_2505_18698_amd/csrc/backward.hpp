@@ -139,10 +139,10 @@ template <int G> __device__ inline float group_sum(float x)
 
 template <int G> __device__ inline float group_max(float x)
 {
-    x = fmaxf(x, dpp<kQuadXor1>(x));
-    x = fmaxf(x, dpp<kQuadXor2>(x));
-    x = fmaxf(x, dpp<kRowHalfMirror>(x));
-    x = fmaxf(x, dpp<kRowMirror>(x));
+    x = max_nan(x, dpp<kQuadXor1>(x));
+    x = max_nan(x, dpp<kQuadXor2>(x));
+    x = max_nan(x, dpp<kRowHalfMirror>(x));
+    x = max_nan(x, dpp<kRowMirror>(x));
     if constexpr (G >= 32) x = wave_xor_max<16>(x);
     if constexpr (G >= 64) x = wave_xor_max<32>(x);
     return x;
@@ -404,7 +404,7 @@ template <typename T, int S, int D, bool LAST, bool LENS = false> struct LBwd {
                 for (int u = 0; u < CPL; ++u) {
                     const int k = col + 64 * u;
                     z[u] = live && k < mk ? dm.s * row[k] - cL[k] : -INFINITY;
-                    mx = fmaxf(mx, z[u]);
+                    mx = max_nan(mx, z[u]);
                 }
                 mx = group_max<SPAN>(mx);
                 float sum = 0.f;
@@ -568,7 +568,7 @@ template <typename T, int S, int D, bool FIRST, bool LAST, bool LENS = false> st
                 for (int u = 0; u < CPL; ++u) {
                     const int i = col + 64 * u;
                     z[u] = live && i < kv ? sc * rr[i] : -INFINITY;
-                    mx = fmaxf(mx, z[u]);
+                    mx = max_nan(mx, z[u]);
                 }
                 mx = group_max<SPAN>(mx);
                 if (!live) mx = 0.f;  // rows past b: every term below is zero

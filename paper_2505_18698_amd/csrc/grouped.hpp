@@ -126,8 +126,9 @@ template <typename T, int NB, int NM, int D, bool RG, bool YG> struct FusedGroup
                 const float u = __builtin_fmaf(sc[t][q], rs, nb);
                 float e = __builtin_amdgcn_exp2f(u);
                 if (RG && 16 * t + 4 * c.g + q >= kv) e = 0.f;
-                sum += e;
-                t2 = __builtin_fmaf(e, u, t2);
+                const bool first = t == 0 && q == 0;  // the sums start at their first term
+                sum = first ? e : sum + e;
+                t2 = first ? e * u : __builtin_fmaf(e, u, t2);
                 sc[t][q] = e;
             }
         }
@@ -209,7 +210,7 @@ template <typename T, int NB, int NM, int D, bool RG, bool YG> struct FusedGroup
             for (int q = 0; q < 4; ++q) {
                 float e = __builtin_amdgcn_exp2f(sc[t][q] - mx);
                 if (RG && 16 * t + 4 * c.g + q >= c.m) e = 0.f;
-                sum += e;
+                sum = (t == 0 && q == 0) ? e : sum + e;
                 sc[t][q] = e;
             }
         }

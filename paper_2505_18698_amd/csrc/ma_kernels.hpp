@@ -126,11 +126,17 @@ template <int MASK> __device__ inline void xor_pair(uint32_t x, uint32_t &a, uin
     }
 }
 
+// max(a, b) that propagates NaN (IEEE 754-2019 maximum): one v_maximum3_f32
+// on gfx950, where fmaxf first canonicalises each operand with a v_max_f32
+// of its own.  The scores are finite or NaN from arithmetic, so the two agree
+// wherever neither is NaN, and a NaN reaches the row's maximum either way.
+__device__ inline float max_nan(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 template <int MASK> __device__ inline float wave_xor_max(float x)
 {
     uint32_t a, b;
     xor_pair<MASK>(__float_as_uint(x), a, b);
-    return fmaxf(__uint_as_float(a), __uint_as_float(b));
+    return max_nan(__uint_as_float(a), __uint_as_float(b));
 }
 
 template <int MASK> __device__ inline float wave_xor_sum(float x)
@@ -447,7 +453,7 @@ __device__ inline float tiles_max(const f32x4 *z, int n, int g)
     for (int t = 0; t < NT; ++t) {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            if (!RAGGED || 16 * t + 4 * g + q < n) mx = fmaxf(mx, z[t][q]);
+            if (!RAGGED || 16 * t + 4 * g + q < n) mx = max_nan(mx, z[t][q]);
     }
     mx = wave_xor_max<16>(mx);
     return wave_xor_max<32>(mx);
@@ -756,8 +762,9 @@ template <typename T, int NB, int D, bool FIRST, bool FINAL, bool RAGGED, bool L
                     const float u = __builtin_fmaf(sc[r][t][qq], rs, nb);
                     float e = __builtin_amdgcn_exp2f(u);
                     if (RAGGED && 16 * t + 4 * g + qq >= kv) e = 0.f;
-                    sum += e;
-                    t2 = __builtin_fmaf(e, u, t2);
+                    const bool first = t == 0 && qq == 0;  // the sums start at their first term
+                    sum = first ? e : sum + e;
+                    t2 = first ? e * u : __builtin_fmaf(e, u, t2);
                     sc[r][t][qq] = e;
                 }
             }
@@ -925,7 +932,7 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
                 for (int qq = 0; qq < 4; ++qq) {
                     float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
                     if (RAGGED && 16 * t + 4 * g + qq >= mk) e = 0.f;
-                    sum += e;
+                    sum = (t == 0 && qq == 0) ? e : sum + e;
                     sc[r][t][qq] = e;
                 }
             }
@@ -994,7 +1001,7 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct LHal
 #pragma unroll
                     for (int t = 0; t < NT; ++t) {
 #pragma unroll
-                        for (int qq = 0; qq < 4; ++qq) mxc = fmaxf(mxc, pf[r].p[t][qq]);
+                        for (int qq = 0; qq < 4; ++qq) mxc = max_nan(mxc, pf[r].p[t][qq]);
                     }
                     mxc = wave_xor_max<32>(wave_xor_max<16>(mxc));
                     const bool any = mxc > 0.5f * kMasked;
@@ -1125,7 +1132,7 @@ template <typename T, int NM, int D, bool RAGGED, bool LENS = false> struct Appl
                 for (int qq = 0; qq < 4; ++qq) {
                     float e = __builtin_amdgcn_exp2f(sc[r][t][qq] - mx);
                     if (RAGGED && 16 * t + 4 * g + qq >= mk) e = 0.f;
-                    sum += e;
+                    sum = (t == 0 && qq == 0) ? e : sum + e;
                     sc[r][t][qq] = e;
                 }
             }
@@ -1301,8 +1308,8 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
             const float u = __builtin_fmaf(sc[qq], rs, nb);
             float e = __builtin_amdgcn_exp2f(u);
             if (RGB && 4 * c.g + qq >= kv) e = 0.f;
-            sum += e;
-            t2 = __builtin_fmaf(e, u, t2);
+            sum = qq == 0 ? e : sum + e;
+            t2 = qq == 0 ? e * u : __builtin_fmaf(e, u, t2);
             sc[qq] = e;
         }
         sum = lanegroup_sum(sum);
@@ -1341,8 +1348,9 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
         f32x4 sc;
 #pragma unroll
         for (int qq = 0; qq < 4; ++qq) {
-            const int kk = 4 * c.g + qq;
-            const float bias = (!RGM || kk < c.m) ? c.cLs[j * CS + kk] * kLog2e : 0.f;
+            // entries k >= m hold no c_L (their LDS words are never written);
+            // the selects below leave them out of the maximum and the sum
+            const float bias = c.cLs[j * CS + 4 * c.g + qq] * kLog2e;
             sc[qq] = __builtin_fmaf(acc[qq], c.s_log2e, -bias);
         }
         const int mk = LENS ? c.mk : c.m;  // blocks k >= mk: no real key
@@ -1352,7 +1360,7 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
         for (int qq = 0; qq < 4; ++qq) {
             float e = __builtin_amdgcn_exp2f(sc[qq] - mx);
             if (RGM && 4 * c.g + qq >= mk) e = 0.f;
-            sum += e;
+            sum = qq == 0 ? e : sum + e;
             sc[qq] = e;
         }
         sum = lanegroup_sum(sum);
@@ -1605,7 +1613,7 @@ template <typename T, int D> struct ExactAttn {
                 sc[t] = acc * s_log2e;
             }
             const float tmax = tiles_max<NT, true>(sc, kv, g);
-            const float mnew = fmaxf(mx, tmax);
+            const float mnew = max_nan(mx, tmax);
             const float corr = __builtin_amdgcn_exp2f(mx - mnew);
             float tsum = 0.f;
 #pragma unroll
