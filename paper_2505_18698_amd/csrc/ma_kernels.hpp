@@ -1425,15 +1425,18 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
         const int m = hd.m, b = hd.b, n = hd.n, d = hd.d;
         const int64_t hoff = bh * (int64_t)n * d;
         const T *qh = p.q + hoff, *kh = p.k + hoff, *vh = p.v + hoff;
+        // Row x of the problem is memory row x0 + sx * x (mrow); offsets within
+        // a head (at most 256 rows of 64 elements) are formed in 32 bits.
+        const int x0 = hd.rev ? n - 1 : 0, sx = hd.rev ? -1 : 1;
 #pragma unroll
         for (int h = 0; h < PER; ++h) {
             const int idx = tid + h * 64 * NW;
             const int reg = idx >> 11, blk = (idx >> 7) & 15, r = (idx >> 3) & 15, col = (idx & 7) * 8;
             raw[h] = u32x4{0u, 0u, 0u, 0u};
             if (reg == 0 && blk < b && r < m && r * b + blk < n && col < d)
-                raw[h] = *reinterpret_cast<const u32x4 *>(qh + mrow(hd, (int64_t)r * b + blk) * d + col);  // Qbar[blk][r]
+                raw[h] = *reinterpret_cast<const u32x4 *>(qh + (x0 + sx * (r * b + blk)) * d + col);  // Qbar[blk][r]
             if (reg == 1 && blk < m && r < b && blk * b + r < n && col < d)
-                raw[h] = *reinterpret_cast<const u32x4 *>(kh + mrow(hd, (int64_t)blk * b + r) * d + col);  // Kbar[blk][r]
+                raw[h] = *reinterpret_cast<const u32x4 *>(kh + (x0 + sx * (blk * b + r)) * d + col);  // Kbar[blk][r]
         }
         const int w = tid >> 6, lane = tid & 63;
 #pragma unroll
@@ -1441,7 +1444,7 @@ template <typename T, bool RGB, bool RGM, bool LENS = false> struct FusedHead {
             const int r = (lane >> 3) + 8 * h, col = (lane & 7) * 8;
             vb[h] = u32x4{0u, 0u, 0u, 0u};
             if (w < m && r < b && w * b + r < n && col < d)
-                vb[h] = *reinterpret_cast<const u32x4 *>(vh + mrow(hd, (int64_t)w * b + r) * d + col);
+                vb[h] = *reinterpret_cast<const u32x4 *>(vh + (x0 + sx * (w * b + r)) * d + col);
         }
     }
 
