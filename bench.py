@@ -780,6 +780,35 @@ def headline_roofline(w, ms, kernels, peaks):
     return roof
 
 
+def compact_record(w, value, ms, steps, warmup, cfg, roof, also_short):
+    """The headline record (the last stdout line, with cpu_baseline and the
+    details file name added by main)."""
+    return {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": UNIT,
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": cfg,
+        "roofline": roof,
+        "also": also_short,
+    }
+
+
+def record_line(result):
+    """One compact JSON line, under the 4 KB a log tail keeps whole."""
+    line = json.dumps(result, separators=(",", ":"))
+    assert len(line) < 4096, len(line)
+    return line
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -878,23 +907,7 @@ def main():
                          for name in [x for x in args.varlen.split(",") if x]]
     if not args.no_quality:
         details["quality"] = [quality(ma, torch, si.WORKLOADS[name]) for name in QUALITY_WORKLOADS]
-    result = {
-        "metric": METRIC,
-        "value": round(value, 1),
-        "unit": UNIT,
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms, 6),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": w.dtype,
-        "data": "synthetic",
-        "config": cfg,
-        "roofline": roof,
-        "also": also_short,
-    }
+    result = compact_record(w, value, ms, args.steps, args.warmup, cfg, roof, also_short)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w)
     if args.details:
@@ -902,9 +915,7 @@ def main():
         with open(args.details, "w") as f:
             json.dump(details, f, indent=1)
         result["details"] = args.details
-    line = json.dumps(result, separators=(",", ":"))
-    assert len(line) < 4096, len(line)
-    print(line, flush=True)
+    print(record_line(result), flush=True)
 
 
 if __name__ == "__main__":
